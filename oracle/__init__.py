@@ -1,0 +1,30 @@
+"""fp64 CPU oracle of the Monte Carlo mutation-selection method (MCA).
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports, calls or
+links this package: only the test-suite, the smoke check and the CPU-baseline
+leg of the benchmark use it.  It shares no code with the HIP library: not a
+kernel, header, helper, table or constant generator.  The seeded input
+generators (package ``workloads``) are the only code both sides consume, and
+they hold none of the method's arithmetic.
+
+Contents (each function cites the passage of the paper it follows):
+
+* ``philox``     Philox4x64-10 counter-based generator, written from its
+                 published definition (Salmon et al., SC'11), and the decoding
+                 of one draw into a single-parameter mutation (Eq. 1, Eq. 12).
+* ``mlp``        fp64 forward pass and average cross-entropy (Eq. 2) of a
+                 bias-free MLP, by full recomputation (the definition), and an
+                 fp64 incremental evaluator (Sec. 2.4: only the changed local
+                 fields are recomputed) pinned against the full recompute.
+* ``transformer`` fp64 forward pass and loss of the pre-LN causal decoder.
+* ``mca``        the greedy selection loop (Eq. 1, Eq. 5, Eq. 6) over K
+                 candidates per step in stream order.
+
+Every function computes in float64 from fp32 state; the mutated parameter
+itself is formed in fp32 exactly as a single-precision implementation would
+(Sec. 2: computations in single precision).
+
+Pin status: every function here is pinned by a test under ``tests/`` against
+something other than itself (library routines, closed forms, brute force);
+none is "parity unpinned".
+"""
