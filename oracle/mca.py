@@ -34,16 +34,11 @@ class StepRecord:
     L_after: float
 
 
-def step(model, t: int, K: int, seed: int, tag: int, delta: float,
-         mode: str = "weight", accept_ties: bool = False,
-         scan_all: bool = True, force: Optional[int] = None) -> StepRecord:
-    """One step of K candidates.
-
-    scan_all=False stops at the first improving candidate (the sequential
-    method); scan_all=True evaluates all K (the batched step, used for parity).
-    `force` (None, -1 or k) overrides the decision; used only by parity tests
-    where the decision lies inside the floating-point tie band.
-    """
+def evaluate(model, t: int, K: int, seed: int, tag: int, delta: float,
+             mode: str = "weight", accept_ties: bool = False, scan_all: bool = True):
+    """Score candidates (t, 0..K-1) against the committed state without
+    committing.  Returns (L_t, candidates, losses, index of the first that
+    passes the test or -1).  scan_all=False stops at that first candidate."""
     L_t = model.loss()
     cands, losses = [], []
     chosen = -1
@@ -56,6 +51,21 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
             chosen = k
             if not scan_all:
                 break
+    return L_t, cands, losses, chosen
+
+
+def step(model, t: int, K: int, seed: int, tag: int, delta: float,
+         mode: str = "weight", accept_ties: bool = False,
+         scan_all: bool = True, force: Optional[int] = None) -> StepRecord:
+    """One step of K candidates: evaluate, then commit the first that passes.
+
+    scan_all=False stops at the first improving candidate (the sequential
+    method); scan_all=True evaluates all K (the batched step, used for parity).
+    `force` (None, -1 or k) overrides the decision; used only by parity tests
+    where the decision lies inside the floating-point tie band.
+    """
+    L_t, cands, losses, chosen = evaluate(model, t, K, seed, tag, delta, mode,
+                                          accept_ties, scan_all)
     if force is not None:
         chosen = force
     if chosen >= 0:

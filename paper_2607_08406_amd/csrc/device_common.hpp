@@ -1,0 +1,191 @@
+// Device-side building blocks shared by every MCA kernel: the network
+// description passed by value to each launch, the per-candidate prepared
+// values, the device state word block, the transfer functions, the per-sample
+// cross-entropy, and the Philox4x64-10 candidate stream.
+//
+// All floating point here is IEEE fp32 with contraction disabled at build
+// time; the only fused multiply-adds are the explicit fmaf() calls, so the
+// same expression evaluates to the same bits in every kernel that uses it
+// (evaluation, commit and the full forward pass agree bit for bit on an
+// unchanged sample).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mca.h"
+
+namespace mca {
+
+constexpr int kTile = 256;          // samples per block in the column kernels
+constexpr int kMaxK = 1024;         // candidates per step (one select thread each)
+constexpr int kCMax = MCA_MAX_CLASSES;
+
+// Everything a kernel needs to know about the net and where it lives in HBM.
+// Unit-major caches: Z[l] is [n_{l+1}][Ns] (the samples of one unit are
+// contiguous), XT is [n_0][Ns]; weights stay [n_{l+1}][n_l] row-major.
+struct NetDev {
+  int32_t L;        // weight matrices
+  int32_t C;        // logits per sample (= widths[L])
+  int32_t act;      // MCA_ACT_*
+  float gamma;
+  int32_t ternary;  // weights are code * scale
+  int32_t pick;     // MCA_PICK_*
+  float delta;
+  float bound;      // > 0: reject |w'| >= bound
+  int32_t ties;     // accept dL <= 0
+  int32_t pad0;
+  uint64_t seed, tag;
+  int64_t N, Ns;    // samples, row stride of the unit-major caches
+  int64_t P;        // parameters
+  int32_t widths[MCA_MAX_LAYERS + 1];
+  int64_t offs[MCA_MAX_LAYERS + 1];   // flat offset of each layer, offs[L] = P
+  float scales[MCA_MAX_LAYERS];
+  float* W[MCA_MAX_LAYERS];
+  int8_t* codes[MCA_MAX_LAYERS];
+  float* Z[MCA_MAX_LAYERS];           // Z[l] = output local fields of layer l
+  const float* XT;
+  float* ell;                         // per-sample loss cache
+  const int32_t* y;
+};
+
+// A candidate's new value, prepared once per step against the committed state.
+struct Aux {
+  float w_old;
+  float w_new;
+  float de;       // fl32(w_new - w_old): the increment the caches apply
+  int32_t valid;  // 0: |w_new| >= bound, rejected without evaluation
+};
+
+// Committed scalars and counters, one 256-byte block in the workspace.
+struct DevState {
+  double L;              // committed loss
+  uint64_t t;            // next step index
+  int32_t chosen;        // decision of the last selected step (-1: none)
+  int32_t K;
+  uint64_t steps, evaluated, accepted, wasted, tie;
+  uint64_t trace_base;   // step index stored at trace slot 0
+  uint64_t pad[6];
+};
+static_assert(sizeof(DevState) <= 256, "state block");
+
+// ---------------------------------------------------------------------------
+// transfer function and loss
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float act_fn(float z, int act, float gamma) {
+  if (act == MCA_ACT_TANH) return tanhf(z);
+  float t = gamma * z;
+  t = t * z;
+  return expf(-t);
+}
+
+// Cross-entropy of one sample from its C logits: logsumexp(z) - z[y], with the
+// maximum subtracted first.  Summation order c = 0..C-1.
+__device__ __forceinline__ float ce_loss(const float (&z)[kCMax], int C, int y) {
+  float m = z[0];
+#pragma unroll
+  for (int c = 1; c < kCMax; ++c)
+    if (c < C) m = fmaxf(m, z[c]);
+  float s = 0.f, zy = 0.f;
+#pragma unroll
+  for (int c = 0; c < kCMax; ++c) {
+    if (c < C) s += expf(z[c] - m);
+    zy = (c == y) ? z[c] : zy;
+  }
+  return (logf(s) + m) - zy;
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)
+// ---------------------------------------------------------------------------
+
+struct Words { uint64_t w0, w1, w2, w3; };
+
+__device__ __forceinline__ Words philox4x64_10(uint64_t x0, uint64_t x1, uint64_t x2,
+                                               uint64_t x3, uint64_t k0, uint64_t k1) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += W0; k1 += W1; }
+    const uint64_t lo0 = M0 * x0, hi0 = __umul64hi(M0, x0);
+    const uint64_t lo1 = M1 * x2, hi1 = __umul64hi(M1, x2);
+    const uint64_t n0 = hi1 ^ x1 ^ k0, n2 = hi0 ^ x3 ^ k1;
+    x0 = n0; x1 = lo1; x2 = n2; x3 = lo0;
+  }
+  return Words{x0, x1, x2, x3};
+}
+
+// Decode draw (t, k) into a candidate (Eq. 1; Eq. 12 for ternary codes).
+__device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t t, uint64_t k) {
+  const Words w = philox4x64_10(t, k, 0, 0, net.seed, net.tag);
+  int layer;
+  int64_t off;
+  if (net.pick == MCA_PICK_LAYER) {
+    layer = (int)__umul64hi(w.w1, (uint64_t)net.L);
+    const int64_t size = net.offs[layer + 1] - net.offs[layer];
+    off = (int64_t)__umul64hi(w.w0, (uint64_t)size);
+  } else {
+    const int64_t flat = (int64_t)__umul64hi(w.w0, (uint64_t)net.P);
+    layer = 0;
+    for (int l = 1; l < net.L; ++l)
+      if (flat >= net.offs[l]) layer = l;
+    off = flat - net.offs[layer];
+  }
+  const int64_t nin = net.widths[layer];
+  mca_cand c;
+  c.flat = net.offs[layer] + off;
+  c.layer = layer;
+  c.j = (int32_t)(off / nin);
+  c.i = (int32_t)(off - (int64_t)c.j * nin);
+  c.reserved = 0;
+  if (net.ternary) {
+    const int cur = net.codes[layer][off];
+    const int b = (int)(w.w3 >> 63);
+    // the b-th of the two other codes, ascending
+    const int nc = (cur == -1) ? (b ? 1 : 0) : (cur == 0 ? (b ? 1 : -1) : (b ? 0 : -1));
+    const float s = net.scales[layer];
+    const float a = (float)nc * s;
+    const float o = (float)cur * s;
+    c.d = a - o;
+    c.code = nc;
+  } else {
+    const float m = (float)(uint32_t)(w.w2 >> 40);
+    const float r = m * 0x1p-23f - 1.0f;
+    c.d = net.delta * r;
+    c.code = 0;
+  }
+  return c;
+}
+
+// New value of a candidate against the committed weights.
+__device__ __forceinline__ Aux prepare_candidate(const NetDev& net, const mca_cand& c) {
+  Aux a;
+  const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+  a.w_old = net.W[c.layer][idx];
+  a.w_new = net.ternary ? (float)c.code * net.scales[c.layer] : a.w_old + c.d;
+  a.de = a.w_new - a.w_old;
+  a.valid = !(net.bound > 0.f && fabsf(a.w_new) >= net.bound);
+  return a;
+}
+
+__device__ __forceinline__ bool accepts(double dL, int ties) {
+  // NaN compares false either way, +inf never passes
+  return ties ? (dL <= 0.0) : (dL < 0.0);
+}
+
+// Sum of v over a block of kTile threads (4 waves of 64), fixed order.
+// The result is valid in thread 0.
+__device__ __forceinline__ float block_sum_256(float v, float* smem4) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) smem4[wave] = v;
+  __syncthreads();
+  float r = 0.f;
+  if (threadIdx.x == 0) r = ((smem4[0] + smem4[1]) + smem4[2]) + smem4[3];
+  return r;
+}
+
+}  // namespace mca

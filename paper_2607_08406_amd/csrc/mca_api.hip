@@ -1,0 +1,601 @@
+// C ABI of the MCA library: validation, workspace layout, uploads, and the
+// host side of the step loop.  The device work lives in the kernel files; this
+// file only enqueues it on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mca.h"
+#include "device_common.hpp"
+#include "mlp_kernels.hpp"
+
+using mca::Aux;
+using mca::DevState;
+using mca::NetDev;
+
+namespace {
+
+constexpr int64_t kTraceCap = 4096;  // steps per trace chunk kept on the device
+constexpr size_t kAlign = 256;
+
+thread_local std::string g_thread_error;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Byte offsets of every buffer inside the caller's workspace.
+struct Layout {
+  int64_t Ns = 0;
+  int ntiles = 0;
+  size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
+  size_t tr_chosen = 0, tr_dl = 0;
+  size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
+  size_t total = 0;
+};
+
+std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max, int* code) {
+  *code = MCA_EINVAL;
+  if (net == nullptr) return "net description is NULL";
+  if (net->kind == MCA_NET_TRANSFORMER) {
+    *code = MCA_EUNSUPPORTED;
+    return "Transformer nets are not implemented by this build";
+  }
+  if (net->kind != MCA_NET_MLP) return "unknown net kind";
+  const int L = net->n_layers;
+  if (L < 1 || L > MCA_MAX_LAYERS) return "n_layers out of range [1, 32]";
+  for (int l = 0; l <= L; ++l)
+    if (net->widths[l] < 1) return "widths must be positive";
+  if (net->widths[L] > MCA_MAX_CLASSES) return "output width exceeds MCA_MAX_CLASSES (16)";
+  for (int l = 0; l < L; ++l)
+    if ((int64_t)net->widths[l] * net->widths[l + 1] >= (int64_t)1 << 31)
+      return "a weight matrix has 2^31 or more entries";
+  if (net->act != MCA_ACT_TANH && net->act != MCA_ACT_GAUSS) return "unknown transfer function";
+  if (net->act == MCA_ACT_GAUSS && !(std::isfinite(net->gamma) && net->gamma > 0.f))
+    return "gamma must be finite and positive";
+  if (net->weight_mode != MCA_WEIGHTS_FP32 && net->weight_mode != MCA_WEIGHTS_TERNARY)
+    return "unknown weight mode";
+  if (net->weight_mode == MCA_WEIGHTS_TERNARY)
+    for (int l = 0; l < L; ++l)
+      if (!(std::isfinite(net->scales[l]) && net->scales[l] > 0.f))
+        return "ternary scales must be finite and positive";
+  if (net->pick != MCA_PICK_WEIGHT && net->pick != MCA_PICK_LAYER) return "unknown pick mode";
+  if (!std::isfinite(net->delta) || net->delta < 0.f) return "delta must be finite and >= 0";
+  if (!std::isfinite(net->bound)) return "bound must be finite (<= 0 disables it)";
+  if (n_samples < 1 || n_samples > ((int64_t)1 << 31)) return "n_samples out of range";
+  if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
+  if (L >= 3) {
+    *code = MCA_EUNSUPPORTED;
+    return "MLPs with three or more weight matrices are not implemented by this build";
+  }
+  *code = MCA_OK;
+  return "";
+}
+
+Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
+  Layout lo;
+  lo.Ns = (N + 63) / 64 * 64;
+  lo.ntiles = (int)((N + mca::kTile - 1) / mca::kTile);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const int L = net->n_layers;
+  lo.xt = take((size_t)net->widths[0] * lo.Ns * sizeof(float));
+  for (int l = 0; l < L; ++l) lo.w[l] = take((size_t)net->widths[l + 1] * net->widths[l] * sizeof(float));
+  if (net->weight_mode == MCA_WEIGHTS_TERNARY)
+    for (int l = 0; l < L; ++l) lo.codes[l] = take((size_t)net->widths[l + 1] * net->widths[l]);
+  for (int l = 0; l < L; ++l) lo.z[l] = take((size_t)net->widths[l + 1] * lo.Ns * sizeof(float));
+  lo.ell = take(lo.Ns * sizeof(float));
+  lo.y = take(lo.Ns * sizeof(int32_t));
+  lo.cands = take((size_t)k_max * sizeof(mca_cand));
+  lo.aux = take((size_t)k_max * sizeof(Aux));
+  lo.partial = take((size_t)k_max * lo.ntiles * sizeof(float));
+  lo.dl = take((size_t)k_max * sizeof(double));
+  lo.bsum = take((size_t)lo.ntiles * sizeof(double));
+  lo.state = take(sizeof(DevState));
+  lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
+  lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
+  lo.total = off;
+  return lo;
+}
+
+__global__ void k_set_trace_base(DevState* st, uint64_t v) { st->trace_base = v; }
+__global__ void k_set_next_step(DevState* st, uint64_t v) { st->t = v; }
+
+}  // namespace
+
+struct mca_ctx {
+  mca_net_desc desc{};
+  NetDev net{};
+  Layout lo;
+  hipStream_t stream = nullptr;
+  int32_t k_max = 0;
+  char* ws = nullptr;
+  mca_cand* cands = nullptr;
+  Aux* aux = nullptr;
+  float* partial = nullptr;
+  double* dl = nullptr;
+  double* bsum = nullptr;
+  DevState* st = nullptr;
+  int32_t* tr_chosen = nullptr;
+  double* tr_dl = nullptr;
+  bool pending = false;
+  int32_t pending_K = 0;
+  bool poisoned = false;
+  std::string err;
+  // phase timing
+  bool timing = false;
+  struct Rec { int phase; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  mca_timing acc{};
+};
+
+namespace {
+
+int fail(mca_ctx* ctx, int code, const std::string& msg) {
+  if (ctx) ctx->err = msg; else g_thread_error = msg;
+  return code;
+}
+
+int device_fail(mca_ctx* ctx, hipError_t e, const char* what) {
+  std::string msg = std::string(what) + ": " + hipGetErrorString(e);
+  if (ctx) { ctx->poisoned = true; ctx->err = msg; } else g_thread_error = msg;
+  return MCA_EDEVICE;
+}
+
+#define MCA_HIP(ctx, expr)                                   \
+  do {                                                       \
+    hipError_t e_ = (expr);                                  \
+    if (e_ != hipSuccess) return device_fail(ctx, e_, #expr); \
+  } while (0)
+
+#define MCA_LIVE(ctx)                                                  \
+  do {                                                                 \
+    if ((ctx) == nullptr) return fail(nullptr, MCA_EINVAL, "ctx is NULL"); \
+    if ((ctx)->poisoned) return fail(ctx, MCA_EPOISONED, "context poisoned by an earlier device error: " + (ctx)->err); \
+  } while (0)
+
+hipEvent_t get_event(mca_ctx* ctx) {
+  if (!ctx->pool.empty()) {
+    hipEvent_t e = ctx->pool.back();
+    ctx->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Wraps one launch in a pair of events when timing is on.
+template <class F>
+hipError_t timed(mca_ctx* ctx, int phase, F&& launch) {
+  if (!ctx->timing) return launch();
+  hipEvent_t a = get_event(ctx), b = get_event(ctx);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, ctx->stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, ctx->stream);
+  if (e != hipSuccess) return e;
+  ctx->recs.push_back({phase, a, b});
+  return hipSuccess;
+}
+
+int flush_timing(mca_ctx* ctx) {
+  if (ctx->recs.empty()) return MCA_OK;
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  for (auto& r : ctx->recs) {
+    float ms = 0.f;
+    MCA_HIP(ctx, hipEventElapsedTime(&ms, r.a, r.b));
+    ctx->acc.ms[r.phase] += ms;
+    ctx->acc.launches[r.phase] += 1;
+    ctx->pool.push_back(r.a);
+    ctx->pool.push_back(r.b);
+  }
+  ctx->recs.clear();
+  return MCA_OK;
+}
+
+int run_forward(mca_ctx* ctx) {
+  MCA_HIP(ctx, timed(ctx, 5, [&] { return mca::launch_forward(ctx->net, ctx->bsum, ctx->st, ctx->stream); }));
+  return MCA_OK;
+}
+
+int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const* codes) {
+  const mca_net_desc& d = ctx->desc;
+  const int L = d.n_layers;
+  if (params == nullptr) return fail(ctx, MCA_EINVAL, "params is NULL");
+  const bool tern = d.weight_mode == MCA_WEIGHTS_TERNARY;
+  if (tern && codes == nullptr) return fail(ctx, MCA_EINVAL, "ternary weights need codes");
+  for (int l = 0; l < L; ++l) {
+    if (params[l] == nullptr) return fail(ctx, MCA_EINVAL, "a parameter pointer is NULL");
+    const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
+    if (tern) {
+      if (codes[l] == nullptr) return fail(ctx, MCA_EINVAL, "a code pointer is NULL");
+      for (size_t e = 0; e < n; ++e) {
+        const int c = codes[l][e];
+        if (c < -1 || c > 1) return fail(ctx, MCA_EINVAL, "ternary code outside {-1, 0, 1}");
+        const float v = (float)c * d.scales[l];
+        if (std::memcmp(&v, &params[l][e], sizeof(float)) != 0 && !(v == 0.f && params[l][e] == 0.f))
+          return fail(ctx, MCA_EINVAL, "ternary parameter differs from code * scale");
+      }
+    } else {
+      for (size_t e = 0; e < n; ++e)
+        if (!std::isfinite(params[l][e])) return fail(ctx, MCA_EINVAL, "non-finite parameter");
+    }
+  }
+  for (int l = 0; l < L; ++l) {
+    const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
+    MCA_HIP(ctx, hipMemcpyAsync(ctx->net.W[l], params[l], n * sizeof(float), hipMemcpyHostToDevice, ctx->stream));
+    if (tern) MCA_HIP(ctx, hipMemcpyAsync(ctx->net.codes[l], codes[l], n, hipMemcpyHostToDevice, ctx->stream));
+  }
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int write_state(mca_ctx* ctx, uint64_t t, bool keep_counters) {
+  DevState s{};
+  if (keep_counters) {
+    MCA_HIP(ctx, hipMemcpyAsync(&s, ctx->st, sizeof s, hipMemcpyDeviceToHost, ctx->stream));
+    MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  }
+  s.t = t;
+  s.chosen = -1;
+  MCA_HIP(ctx, hipMemcpyAsync(ctx->st, &s, sizeof s, hipMemcpyHostToDevice, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int read_state(mca_ctx* ctx, DevState* s) {
+  MCA_HIP(ctx, hipMemcpyAsync(s, ctx->st, sizeof *s, hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
+  const mca_net_desc& d = ctx->desc;
+  for (int k = 0; k < K; ++k) {
+    const int l = c[k].layer;
+    if (l < 0 || l >= d.n_layers) return fail(ctx, MCA_EINVAL, "candidate layer out of range");
+    if (c[k].j < 0 || c[k].j >= d.widths[l + 1] || c[k].i < 0 || c[k].i >= d.widths[l])
+      return fail(ctx, MCA_EINVAL, "candidate index out of range");
+    if (d.weight_mode == MCA_WEIGHTS_TERNARY) {
+      if (c[k].code < -1 || c[k].code > 1) return fail(ctx, MCA_EINVAL, "candidate code outside {-1, 0, 1}");
+    } else if (!std::isfinite(c[k].d)) {
+      return fail(ctx, MCA_EINVAL, "candidate increment is not finite");
+    }
+  }
+  return MCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mca_abi_version(void) { return MCA_ABI_VERSION; }
+
+size_t mca_struct_size(int32_t which) {
+  switch (which) {
+    case 0: return sizeof(mca_net_desc);
+    case 1: return sizeof(mca_cand);
+    case 2: return sizeof(mca_data);
+    case 3: return sizeof(mca_stats);
+    case 4: return sizeof(mca_trace);
+    case 5: return sizeof(mca_timing);
+    default: return 0;
+  }
+}
+
+int mca_plan(const mca_net_desc* net, int64_t n_samples, int32_t k_max, size_t* workspace_bytes) {
+  int code;
+  std::string msg = check_desc(net, n_samples, k_max, &code);
+  if (code != MCA_OK) return fail(nullptr, code, msg);
+  if (workspace_bytes == nullptr) return fail(nullptr, MCA_EINVAL, "workspace_bytes is NULL");
+  *workspace_bytes = make_layout(net, n_samples, k_max).total;
+  return MCA_OK;
+}
+
+int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, int32_t n_params,
+             const int8_t* const* codes, const mca_data* data, int32_t k_max, void* workspace,
+             size_t workspace_bytes, void* hip_stream) {
+  if (out == nullptr) return fail(nullptr, MCA_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (data == nullptr) return fail(nullptr, MCA_EINVAL, "data is NULL");
+  int code;
+  std::string msg = check_desc(net, data->n_samples, k_max, &code);
+  if (code != MCA_OK) return fail(nullptr, code, msg);
+  if (n_params != net->n_layers) return fail(nullptr, MCA_EINVAL, "n_params must equal n_layers");
+  if (data->x == nullptr || data->y == nullptr) return fail(nullptr, MCA_EINVAL, "data.x or data.y is NULL");
+  if (workspace == nullptr) return fail(nullptr, MCA_EINVAL, "workspace is NULL");
+  if (((uintptr_t)workspace) % kAlign != 0) return fail(nullptr, MCA_EINVAL, "workspace is not 256-byte aligned");
+  const int64_t N = data->n_samples;
+  const Layout lo = make_layout(net, N, k_max);
+  if (workspace_bytes < lo.total) return fail(nullptr, MCA_ENOSPACE, "workspace smaller than mca_plan()");
+  const int L = net->n_layers, C = net->widths[L], n0 = net->widths[0];
+  for (int64_t n = 0; n < N; ++n)
+    if (data->y[n] < 0 || data->y[n] >= C) return fail(nullptr, MCA_EINVAL, "label out of range");
+  for (int64_t e = 0; e < N * n0; ++e)
+    if (!std::isfinite(data->x[e])) return fail(nullptr, MCA_EINVAL, "non-finite input");
+
+  mca_ctx* ctx = new (std::nothrow) mca_ctx();
+  if (ctx == nullptr) return fail(nullptr, MCA_EINVAL, "out of host memory");
+  ctx->desc = *net;
+  ctx->lo = lo;
+  ctx->k_max = k_max;
+  ctx->stream = (hipStream_t)hip_stream;
+  ctx->ws = (char*)workspace;
+  char* ws = ctx->ws;
+  NetDev& nd = ctx->net;
+  nd.L = L;
+  nd.C = C;
+  nd.act = net->act;
+  nd.gamma = net->gamma;
+  nd.ternary = net->weight_mode == MCA_WEIGHTS_TERNARY;
+  nd.pick = net->pick;
+  nd.delta = net->delta;
+  nd.bound = net->bound;
+  nd.ties = net->accept_ties ? 1 : 0;
+  nd.seed = net->seed;
+  nd.tag = net->stream_tag;
+  nd.N = N;
+  nd.Ns = lo.Ns;
+  int64_t off = 0;
+  for (int l = 0; l <= L; ++l) nd.widths[l] = net->widths[l];
+  for (int l = 0; l < L; ++l) {
+    nd.offs[l] = off;
+    off += (int64_t)net->widths[l + 1] * net->widths[l];
+    nd.scales[l] = net->scales[l];
+    nd.W[l] = (float*)(ws + lo.w[l]);
+    nd.codes[l] = nd.ternary ? (int8_t*)(ws + lo.codes[l]) : nullptr;
+    nd.Z[l] = (float*)(ws + lo.z[l]);
+  }
+  nd.offs[L] = off;
+  nd.P = off;
+  nd.XT = (const float*)(ws + lo.xt);
+  nd.ell = (float*)(ws + lo.ell);
+  nd.y = (const int32_t*)(ws + lo.y);
+  ctx->cands = (mca_cand*)(ws + lo.cands);
+  ctx->aux = (Aux*)(ws + lo.aux);
+  ctx->partial = (float*)(ws + lo.partial);
+  ctx->dl = (double*)(ws + lo.dl);
+  ctx->bsum = (double*)(ws + lo.bsum);
+  ctx->st = (DevState*)(ws + lo.state);
+  ctx->tr_chosen = (int32_t*)(ws + lo.tr_chosen);
+  ctx->tr_dl = (double*)(ws + lo.tr_dl);
+
+  // inputs, transposed to the unit-major layout (zero padding to Ns)
+  {
+    std::vector<float> xt((size_t)n0 * lo.Ns, 0.f);
+    for (int64_t n = 0; n < N; ++n)
+      for (int i = 0; i < n0; ++i) xt[(size_t)i * lo.Ns + n] = data->x[(size_t)n * n0 + i];
+    std::vector<int32_t> y((size_t)lo.Ns, 0);
+    std::memcpy(y.data(), data->y, (size_t)N * sizeof(int32_t));
+    hipError_t e = hipMemcpyAsync((void*)nd.XT, xt.data(), xt.size() * sizeof(float), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync((void*)nd.y, y.data(), y.size() * sizeof(int32_t), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) {
+      device_fail(nullptr, e, "upload of the data set");
+      delete ctx;
+      return MCA_EDEVICE;
+    }
+  }
+  int rc = upload_params(ctx, params, codes);
+  if (rc == MCA_OK) rc = write_state(ctx, 0, false);
+  if (rc == MCA_OK) rc = run_forward(ctx);
+  if (rc == MCA_OK) {
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) rc = device_fail(ctx, e, "forward pass");
+  }
+  if (rc != MCA_OK) {
+    g_thread_error = ctx->err;
+    delete ctx;
+    return rc;
+  }
+  *out = ctx;
+  return MCA_OK;
+}
+
+int mca_propose(mca_ctx* ctx, uint64_t step, int32_t K, mca_cand* out_host) {
+  MCA_LIVE(ctx);
+  if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
+  if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
+  // the proposal reuses the candidate buffers of a pending batch
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(ctx->net, step, false, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
+  MCA_HIP(ctx, hipMemcpyAsync(out_host, ctx->cands, (size_t)K * sizeof(mca_cand), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double* loss_out,
+                    double* dloss_out) {
+  MCA_LIVE(ctx);
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is already pending");
+  if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
+  if (cands_host == nullptr) return fail(ctx, MCA_EINVAL, "cands_host is NULL");
+  int rc = check_cands(ctx, cands_host, K);
+  if (rc != MCA_OK) return rc;
+  MCA_HIP(ctx, hipMemcpyAsync(ctx->cands, cands_host, (size_t)K * sizeof(mca_cand), hipMemcpyHostToDevice, ctx->stream));
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 1, [&] { return mca::launch_eval(ctx->net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(ctx->net, ctx->partial, ctx->lo.ntiles, ctx->aux, K, ctx->dl, ctx->st, false, nullptr, nullptr, 0, ctx->stream); }));
+  std::vector<double> dl(K);
+  DevState s{};
+  MCA_HIP(ctx, hipMemcpyAsync(dl.data(), ctx->dl, (size_t)K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipMemcpyAsync(&s, ctx->st, sizeof s, hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  for (int k = 0; k < K; ++k) {
+    if (loss_out) loss_out[k] = s.L + dl[k];
+    if (dloss_out) dloss_out[k] = dl[k];
+  }
+  ctx->pending = true;
+  ctx->pending_K = K;
+  return MCA_OK;
+}
+
+int mca_commit(mca_ctx* ctx, int32_t k) {
+  MCA_LIVE(ctx);
+  if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
+  if (k < 0 || k >= ctx->pending_K) return fail(ctx, MCA_EINVAL, "k outside the pending batch");
+  MCA_HIP(ctx, timed(ctx, 3, [&] { return mca::launch_commit(ctx->net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream); }));
+  ctx->pending = false;
+  ctx->pending_K = 0;
+  return MCA_OK;
+}
+
+int mca_rollback(mca_ctx* ctx) {
+  MCA_LIVE(ctx);
+  if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
+  ctx->pending = false;
+  ctx->pending_K = 0;
+  return MCA_OK;
+}
+
+int mca_set_step(mca_ctx* ctx, uint64_t next_step) {
+  MCA_LIVE(ctx);
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  hipLaunchKernelGGL(k_set_next_step, dim3(1), dim3(1), 0, ctx->stream, ctx->st, next_step);
+  MCA_HIP(ctx, hipGetLastError());
+  return MCA_OK;
+}
+
+int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, mca_stats* stats) {
+  MCA_LIVE(ctx);
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
+  if (trace != nullptr && trace->chosen == nullptr) return fail(ctx, MCA_EINVAL, "trace.chosen is NULL");
+  DevState before{};
+  int rc = read_state(ctx, &before);
+  if (rc != MCA_OK) return rc;
+  const NetDev& net = ctx->net;
+  uint64_t done = 0;
+  while (done < n_steps) {
+    const uint64_t chunk = std::min<uint64_t>(n_steps - done, (uint64_t)kTraceCap);
+    int32_t* trc = nullptr;
+    double* trd = nullptr;
+    if (trace != nullptr) {
+      hipLaunchKernelGGL(k_set_trace_base, dim3(1), dim3(1), 0, ctx->stream, ctx->st, before.t + done);
+      MCA_HIP(ctx, hipGetLastError());
+      trc = ctx->tr_chosen;
+      trd = trace->dloss ? ctx->tr_dl : nullptr;
+    }
+    for (uint64_t s = 0; s < chunk; ++s) {
+      MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(net, 0, true, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 1, [&] { return mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->aux, K, ctx->dl, ctx->st, true, trc, trd, kTraceCap, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 3, [&] { return mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, -1, ctx->lo.ntiles, ctx->stream); }));
+    }
+    if (trace != nullptr) {
+      MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));
+      if (trace->dloss)
+        MCA_HIP(ctx, hipMemcpyAsync(trace->dloss + done * K, ctx->tr_dl, chunk * K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+      MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    }
+    done += chunk;
+  }
+  DevState after{};
+  rc = read_state(ctx, &after);
+  if (rc != MCA_OK) return rc;
+  if (stats != nullptr) {
+    stats->steps = after.steps - before.steps;
+    stats->evaluated = after.evaluated - before.evaluated;
+    stats->accepted = after.accepted - before.accepted;
+    stats->wasted = after.wasted - before.wasted;
+    stats->tie_band = after.tie - before.tie;
+    stats->loss = after.L;
+    stats->next_step = after.t;
+  }
+  return MCA_OK;
+}
+
+int mca_get_params(mca_ctx* ctx, float* const* params_out, int8_t* const* codes_out) {
+  MCA_LIVE(ctx);
+  if (params_out == nullptr) return fail(ctx, MCA_EINVAL, "params_out is NULL");
+  const mca_net_desc& d = ctx->desc;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
+    if (params_out[l] == nullptr) return fail(ctx, MCA_EINVAL, "a params_out pointer is NULL");
+    MCA_HIP(ctx, hipMemcpyAsync(params_out[l], ctx->net.W[l], n * sizeof(float), hipMemcpyDeviceToHost, ctx->stream));
+    if (codes_out != nullptr && ctx->net.ternary && codes_out[l] != nullptr)
+      MCA_HIP(ctx, hipMemcpyAsync(codes_out[l], ctx->net.codes[l], n, hipMemcpyDeviceToHost, ctx->stream));
+  }
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int mca_get_loss(mca_ctx* ctx, double* loss, uint64_t* next_step) {
+  MCA_LIVE(ctx);
+  DevState s{};
+  int rc = read_state(ctx, &s);
+  if (rc != MCA_OK) return rc;
+  if (loss) *loss = s.L;
+  if (next_step) *next_step = s.t;
+  return MCA_OK;
+}
+
+int mca_set_state(mca_ctx* ctx, const float* const* params, const int8_t* const* codes,
+                  uint64_t next_step) {
+  MCA_LIVE(ctx);
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  int rc = upload_params(ctx, params, codes);
+  if (rc == MCA_OK) rc = write_state(ctx, next_step, true);
+  if (rc == MCA_OK) rc = run_forward(ctx);
+  if (rc == MCA_OK) MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return rc;
+}
+
+int mca_refresh(mca_ctx* ctx) {
+  MCA_LIVE(ctx);
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  int rc = run_forward(ctx);
+  if (rc == MCA_OK) MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return rc;
+}
+
+int mca_get_sample_losses(mca_ctx* ctx, float* out_host) {
+  MCA_LIVE(ctx);
+  if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
+  MCA_HIP(ctx, hipMemcpyAsync(out_host, ctx->net.ell, (size_t)ctx->net.N * sizeof(float), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int mca_set_timing(mca_ctx* ctx, int32_t enable) {
+  MCA_LIVE(ctx);
+  ctx->timing = enable != 0;
+  return MCA_OK;
+}
+
+int mca_get_timing(mca_ctx* ctx, mca_timing* out, int32_t reset) {
+  MCA_LIVE(ctx);
+  int rc = flush_timing(ctx);
+  if (rc != MCA_OK) return rc;
+  if (out) *out = ctx->acc;
+  if (reset) ctx->acc = mca_timing{};
+  return MCA_OK;
+}
+
+void mca_destroy(mca_ctx* ctx) {
+  if (ctx == nullptr) return;
+  if (!ctx->poisoned) (void)hipStreamSynchronize(ctx->stream);
+  for (auto& r : ctx->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : ctx->pool) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+const char* mca_last_error(const mca_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_thread_error.c_str();
+}
+
+}  // extern "C"

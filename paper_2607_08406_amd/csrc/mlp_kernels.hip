@@ -1,0 +1,332 @@
+// HIP kernels (gfx950) for the MLP hot path of MCA: candidate stream,
+// incremental evaluation, selection, commit, and the full forward pass that
+// fills the caches.
+//
+// Incremental evaluation (Sec. 2.4): a change of W_l[j, i] moves only row j of
+// the unit-major cache Z_l, by de * a_{l-1}[i, n] for every sample n; if layer
+// l is the output layer that is a logit row, otherwise the changed activation
+// da[n] = phi(z'[n]) - phi(z[n]) moves the next layer's local fields by the
+// rank-1 term da[n] * W_{l+1}[:, j].  Samples whose input a_{l-1}[i, n] is zero
+// (about 81 % of an image column) are skipped: nothing changes for them.  The
+// loss change is dL = (1/N) sum_n (l'_n - l_n) over the changed samples only,
+// against the cached per-sample losses, which keeps fp32 cancellation out of
+// dL (a difference of two ~2.3 totals would drown changes of 1e-6).
+#include "device_common.hpp"
+#include "mlp_kernels.hpp"
+
+namespace mca {
+
+// ---------------------------------------------------------------------------
+// candidate stream
+// ---------------------------------------------------------------------------
+
+__global__ void k_propose(NetDev net, uint64_t t_host, int use_dev_t, const DevState* st,
+                          int K, mca_cand* cands, Aux* aux) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= K) return;
+  const uint64_t t = use_dev_t ? st->t : t_host;
+  const mca_cand c = decode_candidate(net, t, (uint64_t)k);
+  cands[k] = c;
+  aux[k] = prepare_candidate(net, c);
+}
+
+__global__ void k_prepare(NetDev net, const mca_cand* cands, int K, Aux* aux) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= K) return;
+  aux[k] = prepare_candidate(net, cands[k]);
+}
+
+// ---------------------------------------------------------------------------
+// per-sample incremental update for a mutation in one of the last two layers
+// ---------------------------------------------------------------------------
+
+// Loss change of sample n under candidate (l, j, i, de); with STORE the new
+// local fields and loss are written to the caches (the commit), computed by
+// exactly the same expressions as the evaluation.
+template <bool STORE>
+__device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, int i,
+                                               float de, int64_t n) {
+  const int L = net.L, C = net.C;
+  const int64_t Ns = net.Ns;
+  const float ain = (l == 0) ? net.XT[(int64_t)i * Ns + n]
+                             : act_fn(net.Z[l - 1][(int64_t)i * Ns + n], net.act, net.gamma);
+  if (ain == 0.f) return 0.f;  // z' == z for this sample
+  float* zrow = net.Z[l] + (int64_t)j * Ns;
+  const float zl = zrow[n];
+  const float zn = zl + de * ain;
+  const float* ZL = net.Z[L - 1];
+  float z[kCMax];
+  if (l == L - 1) {
+    // the mutated weight feeds logit j directly
+#pragma unroll
+    for (int c = 0; c < kCMax; ++c)
+      z[c] = (c < C) ? ((c == j) ? zn : ZL[(int64_t)c * Ns + n]) : 0.f;
+  } else {
+    // last hidden layer: rank-1 update of the logits through W_L[:, j]
+    const float da = act_fn(zn, net.act, net.gamma) - act_fn(zl, net.act, net.gamma);
+    if (da == 0.f) {
+      if (STORE) zrow[n] = zn;
+      return 0.f;
+    }
+    const float* WL = net.W[L - 1];
+    const int nh = net.widths[L - 1];
+#pragma unroll
+    for (int c = 0; c < kCMax; ++c)
+      z[c] = (c < C) ? fmaf(da, WL[(int64_t)c * nh + j], ZL[(int64_t)c * Ns + n]) : 0.f;
+  }
+  const float ln = ce_loss(z, C, net.y[n]);
+  const float dl = ln - net.ell[n];
+  if (STORE) {
+    zrow[n] = zn;
+    if (l != L - 1) {
+      float* ZLw = net.Z[L - 1];
+#pragma unroll
+      for (int c = 0; c < kCMax; ++c)
+        if (c < C) ZLw[(int64_t)c * Ns + n] = z[c];
+    }
+    net.ell[n] = ln;
+  }
+  return dl;
+}
+
+// grid (tiles, K): block (tile, k) sums the loss change of candidate k over
+// the tile's kTile samples; partial[k * ntiles + tile].
+__global__ __launch_bounds__(kTile) void k_eval_column(NetDev net, const mca_cand* cands,
+                                                       const Aux* aux, float* partial,
+                                                       int ntiles) {
+  __shared__ float red[4];
+  const int k = blockIdx.y, tile = blockIdx.x;
+  const mca_cand c = cands[k];
+  const Aux a = aux[k];
+  const int64_t n = (int64_t)tile * kTile + threadIdx.x;
+  float dl = 0.f;
+  if (a.valid && n < net.N) dl = column_sample<false>(net, c.layer, c.j, c.i, a.de, n);
+  const float s = block_sum_256(dl, red);
+  if (threadIdx.x == 0) partial[(int64_t)k * ntiles + tile] = s;
+}
+
+// ---------------------------------------------------------------------------
+// selection (Eq. 6): one block, thread k owns candidate k
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kMaxK) void k_select(NetDev net, const float* partial, int ntiles,
+                                                  const Aux* aux, int K, double* dL,
+                                                  DevState* st, int do_select,
+                                                  int32_t* tr_chosen, double* tr_dl,
+                                                  int64_t tr_cap) {
+  __shared__ int first;
+  __shared__ int ntie;
+  const int k = threadIdx.x;
+  if (k == 0) { first = K; ntie = 0; }
+  __syncthreads();
+  double v = 0.0;
+  if (k < K) {
+    double s = 0.0;
+    const float* p = partial + (int64_t)k * ntiles;
+    for (int t = 0; t < ntiles; ++t) s += (double)p[t];
+    v = aux[k].valid ? s / (double)net.N : __builtin_huge_val();
+    dL[k] = v;
+    if (do_select && accepts(v, net.ties)) atomicMin(&first, k);
+  }
+  if (!do_select) return;
+  __syncthreads();
+  const int kc = first;
+  if (k < K && k <= kc && fabs(v) < 1e-6) atomicAdd(&ntie, 1);
+  __syncthreads();
+  if (tr_chosen != nullptr) {
+    const int64_t slot = (int64_t)(st->t - st->trace_base);
+    if (slot >= 0 && slot < tr_cap) {
+      if (k == 0) tr_chosen[slot] = (kc < K) ? kc : -1;
+      if (tr_dl != nullptr && k < K) tr_dl[slot * K + k] = v;
+    }
+  }
+  __syncthreads();
+  if (k == 0) {
+    st->chosen = (kc < K) ? kc : -1;
+    st->t += 1;
+    st->steps += 1;
+    st->evaluated += (uint64_t)K;
+    st->tie += (uint64_t)ntie;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// commit (Eq. 6 accept branch): k_host >= 0 commits that candidate, otherwise
+// the device decision st->chosen (no-op when -1)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kTile) void k_commit_column(NetDev net, const mca_cand* cands,
+                                                         const Aux* aux, const double* dL,
+                                                         DevState* st, int k_host) {
+  const int k = (k_host >= 0) ? k_host : st->chosen;
+  if (k < 0) return;
+  const mca_cand c = cands[k];
+  const Aux a = aux[k];
+  const int64_t n = (int64_t)blockIdx.x * kTile + threadIdx.x;
+  if (n < net.N) (void)column_sample<true>(net, c.layer, c.j, c.i, a.de, n);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    net.W[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = a.w_new;
+    if (net.ternary) net.codes[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = (int8_t)c.code;
+    st->L += dL[k];
+    st->accepted += 1;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// full forward pass (cache fill): Z_l = W_l phi(Z_{l-1}) with phi applied while
+// the B tile is staged in LDS, then the per-sample losses and their mean
+// ---------------------------------------------------------------------------
+
+// C[M][ldc] = A[M][Kd] * f(B[Kd][ldb]), 64x64 tile per block, 4x4 per thread.
+template <int ACT>  // -1: identity, else MCA_ACT_*
+__global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, int M, int Kd,
+                                                  const float* __restrict__ B, int64_t ldb,
+                                                  int64_t ncols, float* __restrict__ Cm,
+                                                  int64_t ldc, float gamma) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[r][c] = 0.f;
+  for (int k0 = 0; k0 < Kd; k0 += 16) {
+    for (int e = threadIdx.x; e < 1024; e += 256) {
+      const int r = e >> 4, kk = e & 15;
+      const int64_t gm = m0 + r;
+      const int gk = k0 + kk;
+      As[kk][r] = (gm < M && gk < Kd) ? A[gm * Kd + gk] : 0.f;
+    }
+    for (int e = threadIdx.x; e < 1024; e += 256) {
+      const int kk = e >> 6, cc = e & 63;
+      const int gk = k0 + kk;
+      const int64_t gn = n0 + cc;
+      float v = 0.f;
+      if (gk < Kd && gn < ncols) {
+        v = B[(int64_t)gk * ldb + gn];
+        if (ACT >= 0) v = act_fn(v, ACT, gamma);
+      }
+      Bs[kk][cc] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) av[r] = As[kk][ty * 4 + r];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) bv[c] = Bs[kk][tx * 4 + c];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(av[r], bv[c], acc[r][c]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t gm = m0 + ty * 4 + r;
+    if (gm >= M) continue;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t gn = n0 + tx * 4 + c;
+      if (gn < ncols) Cm[gm * ldc + gn] = acc[r][c];
+    }
+  }
+}
+
+// l_n for every sample from the cached logits; fp64 block sums of l_n.
+__global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net, double* bsum) {
+  __shared__ double red[kTile];
+  const int64_t n = (int64_t)blockIdx.x * kTile + threadIdx.x;
+  double v = 0.0;
+  if (n < net.N) {
+    float z[kCMax];
+#pragma unroll
+    for (int c = 0; c < kCMax; ++c) z[c] = (c < net.C) ? net.Z[net.L - 1][(int64_t)c * net.Ns + n] : 0.f;
+    const float l = ce_loss(z, net.C, net.y[n]);
+    net.ell[n] = l;
+    v = (double)l;
+  }
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int s = kTile / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) bsum[blockIdx.x] = red[0];
+}
+
+__global__ void k_loss_total(NetDev net, const double* bsum, int nb, DevState* st) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  double s = 0.0;
+  for (int b = 0; b < nb; ++b) s += bsum[b];
+  st->L = s / (double)net.N;
+}
+
+// ---------------------------------------------------------------------------
+// host-side launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch_propose(const NetDev& net, uint64_t t, bool use_dev_t, const DevState* st,
+                          int K, mca_cand* cands, Aux* aux, hipStream_t s) {
+  hipLaunchKernelGGL(k_propose, dim3((K + 63) / 64), dim3(64), 0, s, net, t, use_dev_t ? 1 : 0,
+                     st, K, cands, aux);
+  return hipGetLastError();
+}
+
+hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* aux,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(k_prepare, dim3((K + 63) / 64), dim3(64), 0, s, net, cands, K, aux);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
+                       float* partial, int ntiles, hipStream_t s) {
+  hipLaunchKernelGGL(k_eval_column, dim3(ntiles, K), dim3(kTile), 0, s, net, cands, aux,
+                     partial, ntiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const NetDev& net, const float* partial, int ntiles, const Aux* aux,
+                         int K, double* dL, DevState* st, bool do_select, int32_t* tr_chosen,
+                         double* tr_dl, int64_t tr_cap, hipStream_t s) {
+  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, partial, ntiles, aux, K, dL, st,
+                     do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* aux,
+                         const double* dL, DevState* st, int k_host, int ntiles, hipStream_t s) {
+  hipLaunchKernelGGL(k_commit_column, dim3(ntiles), dim3(kTile), 0, s, net, cands, aux, dL, st,
+                     k_host);
+  return hipGetLastError();
+}
+
+hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s) {
+  const int64_t N = net.N;
+  for (int l = 0; l < net.L; ++l) {
+    const int M = net.widths[l + 1], Kd = net.widths[l];
+    const float* B = (l == 0) ? net.XT : net.Z[l - 1];
+    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+    if (l == 0)
+      hipLaunchKernelGGL(k_gemm_fwd<-1>, grid, dim3(256), 0, s, net.W[0], M, Kd, B, net.Ns, N,
+                         net.Z[0], net.Ns, net.gamma);
+    else if (net.act == MCA_ACT_TANH)
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
+    else
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int nb = (int)((N + kTile - 1) / kTile);
+  hipLaunchKernelGGL(k_ce_forward, dim3(nb), dim3(kTile), 0, s, net, bsum);
+  hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(64), 0, s, net, bsum, nb, st);
+  return hipGetLastError();
+}
+
+}  // namespace mca

@@ -1,0 +1,23 @@
+// Host-side launchers of the MLP kernels (implemented in mlp_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "device_common.hpp"
+
+namespace mca {
+
+hipError_t launch_propose(const NetDev& net, uint64_t t, bool use_dev_t, const DevState* st,
+                          int K, mca_cand* cands, Aux* aux, hipStream_t s);
+hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* aux,
+                          hipStream_t s);
+hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
+                       float* partial, int ntiles, hipStream_t s);
+hipError_t launch_select(const NetDev& net, const float* partial, int ntiles, const Aux* aux,
+                         int K, double* dL, DevState* st, bool do_select, int32_t* tr_chosen,
+                         double* tr_dl, int64_t tr_cap, hipStream_t s);
+hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* aux,
+                         const double* dL, DevState* st, int k_host, int ntiles, hipStream_t s);
+hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s);
+
+}  // namespace mca

@@ -1,0 +1,94 @@
+"""The C-ABI library loads, exports every symbol include/mca.h declares, and
+its struct layouts match the binding's mirrors.  Validation paths of the pure
+planning call run without a GPU; nothing here launches device code."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def binding():
+    from paper_2607_08406_amd import mca
+    if not os.path.exists(mca.LIB_PATH):
+        pytest.fail("libmca.so is not built: run __graft_entry__.build() first")
+    mca.load_library()
+    return mca
+
+
+def declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(mca_\w+)\s*\(", text))
+    return sorted(names)
+
+
+def test_exports_every_declared_symbol(binding):
+    lib = ctypes.CDLL(binding.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) <= set(binding._SIGNATURES), set(names) - set(binding._SIGNATURES)
+
+
+def test_struct_mirrors(binding):
+    lib = binding.load_library()
+    for n, st in enumerate(binding.STRUCTS):
+        assert lib.mca_struct_size(n) == ctypes.sizeof(st)
+    assert ctypes.sizeof(binding.mca_cand) == 32 == binding.CAND_DTYPE.itemsize
+    assert lib.mca_struct_size(99) == 0
+    assert binding.mca_abi_version() == 1
+
+
+def test_plan_sizes(binding):
+    d = binding.mlp_desc((784, 16384, 10), "tanh", delta=0.05)
+    b = binding.mca_plan(d, 10000, 64)
+    # X^T + W1 + W2 + Z1 + Z2 dominate: 4 * (784*10048 + 784*16384 + 163840 + 16384*10048 + 10*10048)
+    core = 4 * (784 * 10048 + 784 * 16384 + 16384 * 10 + 16384 * 10048 + 10 * 10048)
+    assert core < b < core + 8 * 2 ** 20
+    assert binding.mca_plan(d, 10000, 1) < b
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (dict(n_layers=0), "MCA_EINVAL"),
+    (dict(act=7), "MCA_EINVAL"),
+    (dict(pick=3), "MCA_EINVAL"),
+    (dict(kind=1), "MCA_EUNSUPPORTED"),
+    (dict(kind=5), "MCA_EINVAL"),
+    (dict(delta=float("nan")), "MCA_EINVAL"),
+])
+def test_plan_rejects_bad_descriptions(binding, mutate, code):
+    d = binding.mlp_desc((64, 32, 10), "tanh", delta=0.1)
+    for k, v in mutate.items():
+        setattr(d, k, v)
+    with pytest.raises(binding.MCAError) as e:
+        binding.mca_plan(d, 1024, 1)
+    assert code in str(e.value)
+
+
+def test_plan_rejects_bad_sizes(binding):
+    d = binding.mlp_desc((64, 32, 10), "tanh", delta=0.1)
+    for N, K in [(0, 1), (1024, 0), (1024, 1025)]:
+        with pytest.raises(binding.MCAError):
+            binding.mca_plan(d, N, K)
+    d = binding.mlp_desc((64, 32, 17), "tanh", delta=0.1)
+    with pytest.raises(binding.MCAError):
+        binding.mca_plan(d, 100, 1)
+    d = binding.mlp_desc((4, 3, 2), "gauss", ternary_scales=[0.0, 1.0])
+    with pytest.raises(binding.MCAError):
+        binding.mca_plan(d, 100, 1)
+
+
+def test_last_error_message(binding):
+    d = binding.mlp_desc((64, 32, 10), "tanh", delta=0.1)
+    with pytest.raises(binding.MCAError):
+        binding.mca_plan(d, 1024, 5000)
+    assert "k_max" in binding.mca_last_error(None)

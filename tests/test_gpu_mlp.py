@@ -1,0 +1,236 @@
+"""GPU parity of the MLP hot path against the fp64 oracle (through the C ABI).
+
+Workloads: the 64-32-10 tanh net (1,024 samples, K=1, the whole 20,000-step
+window), a reduced wide net 784-512-10 (1,000 samples: three full 256-sample
+tiles and a ragged tail of 232) and the full 784-16384-10 net on 10,000
+samples at K=64, in the launch configuration the benchmark times.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mca as omca
+from oracle.mlp import FullMLP, IncrementalMLP, MLPState
+from parity_util import (REL_TOL, TIE, assert_cands_equal, assert_state_equal, check_losses,
+                         explicit_steps, make_pair, replay_trace)
+from workloads import CONFIGS, mlp_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def banner(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def mca():
+    from paper_2607_08406_amd import mca as m
+    m.load_library()
+    assert torch.cuda.is_available()
+    return m
+
+
+def small_wide():
+    return CONFIGS["wide"].scaled(name="wide_small", widths=(784, 512, 10), n_samples=1000)
+
+
+def test_tiny_init_and_explicit_steps(mca):
+    cfg = CONFIGS["tiny"]
+    banner("tiny explicit steps")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=4)
+    L, t = ctx.loss()
+    assert t == 0 and abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    full = FullMLP(MLPState(w["weights"]), w["X"], w["y"], cfg.act)
+    assert abs(L - full.loss()) <= REL_TOL * full.loss()
+    ties, acc = explicit_steps(ctx, ref, cfg, 0, 300, 4)
+    assert acc > 50
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
+def test_tiny_device_loop_full_window(mca):
+    """All 20,000 steps of the tiny workload (K=1) in the device loop, replayed
+    on the oracle: every decision equal outside the tie band, weights bit-equal."""
+    cfg = CONFIGS["tiny"]
+    banner("tiny 20000-step device loop")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=1)
+    st, chosen, dloss = ctx.run_steps(cfg.steps, 1, trace=True, trace_dloss=True)
+    assert st.steps == cfg.steps and st.evaluated == cfg.steps and st.next_step == cfg.steps
+    ties, acc = replay_trace(ref, cfg, 0, chosen, dloss, 1)
+    assert acc == st.accepted
+    assert ties <= 20
+    assert_state_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ctx.refresh()
+    L2, _ = ctx.loss()
+    assert abs(L2 - L) <= 1e-6 * L  # drift of the incremental caches
+    ctx.close()
+
+
+def test_small_wide_explicit_and_loop(mca):
+    cfg = small_wide()
+    banner("wide 784-512-10 N=1000 explicit + loop")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=64)
+    ties, acc = explicit_steps(ctx, ref, cfg, 0, 40, 64)
+    assert acc > 10
+    assert_state_equal(ctx, ref)
+    assert ctx.loss()[1] == 0  # the explicit path leaves the step counter alone
+    ctx.set_step(40)
+    st, chosen, dloss = ctx.run_steps(60, 64, trace=True, trace_dloss=True)
+    assert st.next_step == 100
+    replay_trace(ref, cfg, 40, chosen, dloss, 64)
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
+def test_full_wide_workload(mca):
+    """784-16384-10 on 10,000 samples, K=64: init loss, 20 device steps with
+    every candidate's dL, replayed on the incremental oracle; two sampled
+    candidates against full recomputation."""
+    cfg = CONFIGS["wide"]
+    banner("wide 784-16384-10 N=10000 K=64")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=64)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    cands = ctx.propose(0, 64)
+    L_t, rc, rl, chosen = omca.evaluate(ref, 0, 64, cfg.seed_stream, cfg.stream_tag, cfg.delta)
+    assert_cands_equal(cands, rc)
+    losses, dl = ctx.eval_losses(cands)
+    check_losses(losses, L_t, rl)
+    full = FullMLP(MLPState(w["weights"]), w["X"], w["y"], cfg.act)
+    for k in (0, 1):
+        assert abs(losses[k] - full.eval(rc[k])) <= REL_TOL * losses[k]
+    ctx.rollback()
+    st, ch, dloss = ctx.run_steps(20, 64, trace=True, trace_dloss=True)
+    assert st.steps == 20
+    replay_trace(ref, cfg, 0, ch, dloss, 64)
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
+def test_zero_increment_and_bound(mca):
+    cfg = small_wide()
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=8)
+    cands = ctx.propose(3, 8)
+    cands["d"] = 0.0
+    losses, dl = ctx.eval_losses(cands)
+    assert np.all(dl == 0.0)
+    L, _ = ctx.loss()
+    assert np.all(losses == L)
+    ctx.rollback()
+    ctx.close()
+    desc = mca.mlp_desc(cfg.widths, cfg.act, delta=cfg.delta, bound=1e-3, seed=cfg.seed_stream,
+                        stream_tag=cfg.stream_tag)
+    ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=8)
+    losses, dl = ctx.eval_losses(ctx.propose(0, 8))
+    assert np.all(np.isinf(dl))  # every init weight is far above the bound
+    ctx.rollback()
+    st, _, _ = ctx.run_steps(5, 8)
+    assert st.accepted == 0
+    ctx.close()
+
+
+def test_rollback_is_byte_identical(mca):
+    cfg = small_wide()
+    w = mlp_workload(cfg)
+    ctx, _ = make_pair(cfg, w, k_max=16)
+    p0, _ = ctx.params()
+    l0 = ctx.sample_losses()
+    L0 = ctx.loss()
+    ctx.eval_losses(ctx.propose(0, 16))
+    ctx.rollback()
+    p1, _ = ctx.params()
+    for a, b in zip(p0, p1):
+        assert a.tobytes() == b.tobytes()
+    assert ctx.sample_losses().tobytes() == l0.tobytes()
+    assert ctx.loss() == L0
+    ctx.close()
+
+
+def test_error_paths(mca):
+    cfg = CONFIGS["tiny"]
+    w = mlp_workload(cfg)
+    ctx, _ = make_pair(cfg, w, k_max=4)
+    with pytest.raises(mca.MCAError, match="ESTATE"):
+        ctx.commit(0)
+    with pytest.raises(mca.MCAError, match="ESTATE"):
+        ctx.rollback()
+    with pytest.raises(mca.MCAError, match="EINVAL"):
+        ctx.propose(0, 5)
+    cands = ctx.propose(0, 4)
+    bad = cands.copy()
+    bad[1]["j"] = 32
+    with pytest.raises(mca.MCAError, match="EINVAL"):
+        ctx.eval_losses(bad)
+    ctx.eval_losses(cands)
+    with pytest.raises(mca.MCAError, match="ESTATE"):
+        ctx.eval_losses(cands)
+    with pytest.raises(mca.MCAError, match="ESTATE"):
+        ctx.run_steps(1, 4)
+    with pytest.raises(mca.MCAError, match="EINVAL"):
+        ctx.commit(4)
+    ctx.commit(3)
+    with pytest.raises(mca.MCAError, match="ESTATE"):
+        ctx.commit(3)
+    ctx.close()
+    bad_y = w["y"].copy()
+    bad_y[0] = 10
+    desc = mca.mlp_desc(cfg.widths, cfg.act, delta=cfg.delta)
+    with pytest.raises(mca.MCAError, match="EINVAL"):
+        mca.Context(desc, w["weights"], w["X"], bad_y, k_max=1)
+
+
+def test_resume_is_exact(mca):
+    cfg = small_wide()
+    w = mlp_workload(cfg)
+    a, _ = make_pair(cfg, w, k_max=16)
+    a.run_steps(60, 16)
+    pa, _ = a.params()
+    b, _ = make_pair(cfg, w, k_max=16)
+    b.run_steps(30, 16)
+    pb, _ = b.params()
+    _, t = b.loss()
+    c, _ = make_pair(cfg, w, k_max=16)
+    c.set_state(pb, None, t)
+    c.run_steps(30, 16)
+    pc, _ = c.params()
+    for x, y in zip(pa, pc):
+        assert x.tobytes() == y.tobytes()
+    for ctx in (a, b, c):
+        ctx.close()
+
+
+@pytest.mark.parametrize("N", [1, 63, 257])
+def test_degenerate_sample_counts(mca, N):
+    cfg = CONFIGS["tiny"].scaled(n_samples=N)
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=8)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    explicit_steps(ctx, ref, cfg, 0, 20, 8)
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
+def test_gauss_and_ternary_two_layer(mca):
+    """Gaussian transfer and ternary codes (Eq. 12) on a two-layer net."""
+    base = CONFIGS["ternary"]
+    cfg = base.scaled(name="ternary2", widths=(784, 256, 10), n_samples=777, K=32)
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=32)
+    ties, acc = explicit_steps(ctx, ref, cfg, 0, 30, 32)
+    assert acc > 5
+    assert_state_equal(ctx, ref)
+    ctx.set_step(30)
+    st, ch, dl = ctx.run_steps(30, 32, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 30, ch, dl, 32)
+    assert_state_equal(ctx, ref)
+    ctx.close()
