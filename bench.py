@@ -1,0 +1,177 @@
+"""Throughput of the MCA hot path on one MI355X.
+
+A step is one pass of the whole hot path over the data set: K candidates
+proposed from the counter-based stream, each scored incrementally against
+the committed state (column update, rank-1 update of the logits, fused
+softmax cross-entropy, loss-change reduction), the first improving one
+committed.  The default workload is the single-hidden-layer wide net
+784-16384-10 (tanh) on 10,000 synthetic 28x28 template images, K = 64.
+
+Prints one JSON line: candidate evaluations per second (value), accepted
+mutations per second, the roofline of the dominant kernel from HIP events
+recorded on the library's stream during the timed region, and the fp64 CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def algorithmic_bytes_per_step(cfg) -> float:
+    """Bytes one evaluation launch must move at least (one step of K candidates).
+
+    Shared by all candidates of the step: the logits (4 N C), the cached
+    per-sample losses (4 N) and the labels (N, one byte each).  Per candidate
+    in the last hidden layer: the input column and the mutated unit's row of
+    local fields (8 N); per candidate in the output layer: the input unit's row
+    of local fields (4 N).  Candidates fall in each layer in proportion to its
+    size (uniform draw over all weights).
+    """
+    N, C, K = cfg.n_samples, cfg.n_classes, cfg.K
+    sizes = cfg.layer_sizes()
+    P = float(sum(sizes))
+    shared = 4.0 * N * C + 4.0 * N + N
+    per_cand = 0.0
+    L = cfg.n_layers
+    for l, s in enumerate(sizes):
+        per_cand += (s / P) * (8.0 * N if l == L - 2 else 4.0 * N)
+    return shared + K * per_cand
+
+
+def cpu_baseline(cfg, w, seconds: float):
+    """The fp64 oracle (incremental mode, all K candidates scored per step, as
+    the device does) on the host cores, for about `seconds` of work."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import mca as omca
+    from oracle.mlp import IncrementalMLP, MLPState
+    t0 = time.perf_counter()
+    ref = IncrementalMLP(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"],
+                         cfg.act, cfg.gamma)
+    t_init = time.perf_counter() - t0
+    n_steps = 0
+    evals = 0
+    acc = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        rec = omca.step(ref, n_steps, cfg.K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
+                        cfg.layer_pick, cfg.accept_ties, scan_all=True)
+        n_steps += 1
+        evals += len(rec.losses)
+        acc += rec.chosen >= 0
+    el = time.perf_counter() - t0
+    blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
+    return {"value": evals / el, "unit": "candidate evals/s", "cores": 1,
+            "kind": "oracle",
+            "sample": (f"fp64 incremental oracle, first {n_steps} steps x K={cfg.K} of the "
+                       f"same workload from the same seeded init ({el:.1f} s; numpy "
+                       f"element-wise work on one thread, BLAS threads {blas} used only "
+                       f"by its {t_init:.1f} s forward pass, not timed)"),
+            "accepted_per_s": acc / el}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workload", default="wide")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tile", type=int, default=0, help="samples per workgroup (16..64)")
+    ap.add_argument("--per-phase", action="store_true",
+                    help="one launch per phase per step instead of the persistent loop")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the MCA path here is single-GPU; sharding is a design note only)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_08406_amd import mca
+    from workloads import CONFIGS, mlp_workload
+
+    cfg = CONFIGS[args.workload]
+    w = mlp_workload(cfg)
+    desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
+                        ternary_scales=w["scales"], pick=cfg.layer_pick,
+                        accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                        stream_tag=cfg.stream_tag)
+    ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=cfg.K, codes=w["codes"])
+    if args.tile:
+        ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
+    if args.per_phase:
+        ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, 0)
+    print(f"[bench] {cfg.name}: context ready, warmup {args.warmup} steps", file=sys.stderr,
+          flush=True)
+    ctx.run_steps(args.warmup, cfg.K)
+    mca.mca_get_timing(ctx.ctx, reset=True)
+    # the dominant kernel: the persistent step loop (one launch runs every
+    # timed step), or the evaluation kernel when each phase is its own launch
+    mca.mca_set_timing(ctx.ctx, (1 << mca.PHASES.index("eval")) | (1 << mca.PHASES.index("step_loop")))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    st, _, _ = ctx.run_steps(args.steps, cfg.K)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms, launches = mca.mca_get_timing(ctx.ctx, reset=True)
+    mca.mca_set_timing(ctx.ctx, 0)
+    print(f"[bench] timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
+
+    loop = launches[mca.PHASES.index("step_loop")] > 0
+    dominant = mca.PHASES.index("step_loop" if loop else "eval")
+    kernel = "k_step_loop" if loop else "k_eval_column"
+    n_launch = max(int(launches[dominant]), 1)
+    avg_s = ms[dominant] / 1e3 / n_launch
+    # one loop launch covers all timed steps; one eval launch covers one step
+    bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
+    achieved = bytes_launch / avg_s / 1e9
+    result = {
+        "metric": "candidate loss evals/sec + accepted mutations/sec at 1 GPU; % HBM/MFMA roofline",
+        "value": st.evaluated / wall,
+        "unit": "candidate evals/s",
+        "accepted_per_s": st.accepted / wall,
+        "accept_rate_per_step": st.accepted / max(st.steps, 1),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": (f"{cfg.name} MLP {'-'.join(map(str, cfg.widths))} {cfg.act}, "
+                                f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}"),
+                   "K": cfg.K, "n_samples": cfg.n_samples, "widths": list(cfg.widths),
+                   "n_params": cfg.n_params},
+        "roofline": {"bound": "hbm", "kernel": kernel,
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
+                     "launches": int(launches[dominant]),
+                     "bytes_per_step": algorithmic_bytes_per_step(cfg)},
+        "final_loss": st.loss,
+    }
+    ctx.close()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -190,6 +190,19 @@ int mca_commit(mca_ctx* ctx, int32_t k);
  * byte-identical to before the evaluation.  MCA_ESTATE without a pending batch. */
 int mca_rollback(mca_ctx* ctx);
 
+/* Tuning options of mca_run_steps (mca_set_option):
+ *   MCA_OPT_PERSISTENT_LOOP  1 (default): run eligible nets (mutations reach
+ *                            at most the last two layers, K <= 64) in one
+ *                            cooperative launch per call; 0: one launch per
+ *                            phase per step.  Both give the same results up
+ *                            to the order of the loss-change sums.
+ *   MCA_OPT_LOOP_TILE        samples per workgroup of the persistent loop,
+ *                            16..64 (default 64). */
+#define MCA_OPT_PERSISTENT_LOOP 1
+#define MCA_OPT_LOOP_TILE 2
+/* Set a tuning option; MCA_EINVAL for an unknown option or value. */
+int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value);
+
 /* Set the device's next step index (the step mca_run_steps starts from).  The
  * explicit path (mca_propose with an explicit step, mca_eval_losses,
  * mca_commit / mca_rollback) never changes it.  MCA_ESTATE while a batch is
@@ -222,11 +235,12 @@ int mca_refresh(mca_ctx* ctx);
 /* Copy the cached per-sample losses l_n (fp32, n_samples values).  Synchronises. */
 int mca_get_sample_losses(mca_ctx* ctx, float* out_host);
 
-/* Phase timers: enable (1) / disable (0) recording a pair of HIP events on the
- * context's stream around every kernel launch (no synchronisation per launch),
- * and read (and optionally reset) the accumulated device time per phase;
- * mca_get_timing synchronises.  The events add a little launch overhead. */
-int mca_set_timing(mca_ctx* ctx, int32_t enable);
+/* Phase timers: phase_mask bit p enables recording a pair of HIP events on the
+ * context's stream around every launch of phase p (phases as in mca_timing;
+ * 0 disables all); no synchronisation per launch.  mca_get_timing reads (and
+ * optionally resets) the accumulated device time per phase and synchronises.
+ * The events add a little launch overhead. */
+int mca_set_timing(mca_ctx* ctx, int32_t phase_mask);
 int mca_get_timing(mca_ctx* ctx, mca_timing* out, int32_t reset);
 
 /* Release the context (not the caller's workspace).  NULL is ignored. */

@@ -13,7 +13,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/mca.h"
+#include "mca.h"
 
 namespace mca {
 
@@ -49,6 +49,17 @@ struct NetDev {
   const int32_t* y;
 };
 
+// Kernels index the pointer and size arrays of NetDev with runtime values (the
+// candidate's layer).  Indexing the by-value kernel argument that way makes
+// the compiler fetch each pointer from the kernel-argument segment with a
+// dependent vector load; one thread therefore copies the descriptor to LDS
+// with static offsets (scalar loads) and every lane indexes the LDS copy.
+// Every thread of the block must call this (it synchronises the block).
+__device__ __forceinline__ void stage_net(NetDev& dst, const NetDev& src) {
+  if (threadIdx.x == 0) dst = src;
+  __syncthreads();
+}
+
 // A candidate's new value, prepared once per step against the committed state.
 struct Aux {
   float w_old;
@@ -73,27 +84,46 @@ static_assert(sizeof(DevState) <= 256, "state block");
 // transfer function and loss
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ float act_fn(float z, int act, float gamma) {
-  if (act == MCA_ACT_TANH) return tanhf(z);
-  float t = gamma * z;
-  t = t * z;
-  return expf(-t);
+// The transcendentals of the hot path use the hardware exp2/log2/rcp units:
+// e^x = 2^(x log2 e), ln x = log2(x) ln 2, tanh z = 1 - 2 / (e^{2z} + 1).
+// Their error (a few ulp, absolute error of tanh near 1e-7) is far below the
+// fp32 rounding of the caches; every kernel (forward, evaluation, commit)
+// calls these same functions, so an unchanged sample evaluates to the same
+// bits everywhere.
+__device__ __forceinline__ float fast_exp(float x) {
+  return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
+}
+__device__ __forceinline__ float fast_log(float x) {
+  return __builtin_amdgcn_logf(x) * 0.6931471805599453f;
+}
+__device__ __forceinline__ float fast_tanh(float z) {
+  const float e = fast_exp(z + z);
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
 }
 
-// Cross-entropy of one sample from its C logits: logsumexp(z) - z[y], with the
-// maximum subtracted first.  Summation order c = 0..C-1.
-__device__ __forceinline__ float ce_loss(const float (&z)[kCMax], int C, int y) {
+__device__ __forceinline__ float act_fn(float z, int act, float gamma) {
+  if (act == MCA_ACT_TANH) return fast_tanh(z);
+  float t = gamma * z;
+  t = t * z;
+  return fast_exp(-t);
+}
+
+// Cross-entropy of one sample from its C <= CM logits: logsumexp(z) - z[y],
+// with the maximum subtracted first.  Summation order c = 0..C-1, so every
+// CM >= C gives the same bits.
+template <int CM>
+__device__ __forceinline__ float ce_loss(const float (&z)[CM], int C, int y) {
   float m = z[0];
 #pragma unroll
-  for (int c = 1; c < kCMax; ++c)
+  for (int c = 1; c < CM; ++c)
     if (c < C) m = fmaxf(m, z[c]);
   float s = 0.f, zy = 0.f;
 #pragma unroll
-  for (int c = 0; c < kCMax; ++c) {
-    if (c < C) s += expf(z[c] - m);
+  for (int c = 0; c < CM; ++c) {
+    if (c < C) s += fast_exp(z[c] - m);
     zy = (c == y) ? z[c] : zy;
   }
-  return (logf(s) + m) - zy;
+  return (fast_log(s) + m) - zy;
 }
 
 // ---------------------------------------------------------------------------
@@ -117,8 +147,12 @@ __device__ __forceinline__ Words philox4x64_10(uint64_t x0, uint64_t x1, uint64_
   return Words{x0, x1, x2, x3};
 }
 
-// Decode draw (t, k) into a candidate (Eq. 1; Eq. 12 for ternary codes).
-__device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t t, uint64_t k) {
+// Decode draw (t, k) into a candidate (Eq. 1; Eq. 12 for ternary codes) in
+// two parts.  decode_index() needs no state: parameter, row, column and, for
+// continuous weights, the increment; for ternary weights it leaves the
+// selecting bit (w3 >> 63) in c.code.  finish_ternary() then picks the new
+// code from the committed one.
+__device__ __forceinline__ mca_cand decode_index(const NetDev& net, uint64_t t, uint64_t k) {
   const Words w = philox4x64_10(t, k, 0, 0, net.seed, net.tag);
   int layer;
   int64_t off;
@@ -133,29 +167,42 @@ __device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t
       if (flat >= net.offs[l]) layer = l;
     off = flat - net.offs[layer];
   }
-  const int64_t nin = net.widths[layer];
+  // every layer has fewer than 2^31 entries: 32-bit division suffices
+  const uint32_t nin = (uint32_t)net.widths[layer];
   mca_cand c;
   c.flat = net.offs[layer] + off;
   c.layer = layer;
-  c.j = (int32_t)(off / nin);
-  c.i = (int32_t)(off - (int64_t)c.j * nin);
+  c.j = (int32_t)((uint32_t)off / nin);
+  c.i = (int32_t)((uint32_t)off - (uint32_t)c.j * nin);
   c.reserved = 0;
   if (net.ternary) {
-    const int cur = net.codes[layer][off];
-    const int b = (int)(w.w3 >> 63);
-    // the b-th of the two other codes, ascending
-    const int nc = (cur == -1) ? (b ? 1 : 0) : (cur == 0 ? (b ? 1 : -1) : (b ? 0 : -1));
-    const float s = net.scales[layer];
-    const float a = (float)nc * s;
-    const float o = (float)cur * s;
-    c.d = a - o;
-    c.code = nc;
+    c.d = 0.f;
+    c.code = (int)(w.w3 >> 63);
   } else {
     const float m = (float)(uint32_t)(w.w2 >> 40);
     const float r = m * 0x1p-23f - 1.0f;
     c.d = net.delta * r;
     c.code = 0;
   }
+  return c;
+}
+
+// c.code holds the selecting bit on entry and the new code on return.
+__device__ __forceinline__ void finish_ternary(const NetDev& net, mca_cand& c, int cur) {
+  const int b = c.code;
+  // the b-th of the two other codes, ascending
+  const int nc = (cur == -1) ? (b ? 1 : 0) : (cur == 0 ? (b ? 1 : -1) : (b ? 0 : -1));
+  const float s = net.scales[c.layer];
+  const float a = (float)nc * s;
+  const float o = (float)cur * s;
+  c.d = a - o;
+  c.code = nc;
+}
+
+__device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t t, uint64_t k) {
+  mca_cand c = decode_index(net, t, k);
+  if (net.ternary)
+    finish_ternary(net, c, net.codes[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i]);
   return c;
 }
 

@@ -1,0 +1,487 @@
+// Persistent step loop for MLPs whose mutations touch only the last two
+// layers (one hidden layer, or a logit-layer weight): one cooperative launch
+// runs many steps of propose -> evaluate -> select -> commit.
+//
+// Work split: tile workgroup g < G owns T <= 64 consecutive samples for the
+// whole launch.  Its share of the logits, cached per-sample losses and labels
+// stays in LDS; the hidden local fields Z_l stay in HBM but each tile of a row
+// is only ever read and written by its owner.  Every tile workgroup decodes
+// the step's K candidates itself (the stream is counter-based), scores all of
+// them on its tile and publishes one partial loss change per candidate
+// (+inf for a candidate rejected by the weight bound).  The reduction is
+// sharded by candidate: wave w of reducer workgroup r owns candidate 4r + w,
+// adds its G partial sums in a fixed order (fp64) and publishes the loss
+// change dL_k.  Every tile workgroup reads all K loss changes and takes the
+// same decision itself: the first candidate in stream order that passes the
+// test (Eq. 6).  It then applies the commit to its own tile with the same
+// expressions the evaluation used.  Tile 0 also keeps the committed loss and
+// the counters.  While a tile workgroup waits, its idle waves draw the next
+// step's candidates (the draw needs no state).
+//
+// Sparse inputs: a sample whose input to the mutated weight is zero does not
+// change (about 81 % of an image column), so a workgroup first compacts the
+// (candidate, sample) pairs with a non-zero input into an LDS work list and
+// spreads that list over all its lanes.  Each pair writes its loss change to
+// its own (candidate, sample) slot and the slots are summed in sample order,
+// so the order in which the list was built does not change any result.
+//
+// Weights are read with ordinary cached loads.  Every tile workgroup writes
+// every committed weight itself, so each CU's L1 and each XCD's L2 that may
+// hold the old value is updated by a local store; during the one step in
+// which that store may still be in flight the value comes from LDS.
+//
+// Cross-workgroup words carry their own step tag, so no separate flag, fence
+// or L2 writeback is needed: a partial sum is one 64-bit word (fp32 value |
+// 32-bit step tag), each tile's K words padded to whole 128-byte lines so no
+// two tiles write the same line; a loss change is one fp64 word whose 16 low
+// mantissa bits are replaced by the step tag (2^-36 relative truncation, the
+// same bits for every reader).  They are written and read with relaxed
+// agent-scope atomics, which the compiler emits as coherent (sc1) accesses.
+// A reader polls until the tag is the one it expects.  Tags are cleared
+// before each launch.
+//
+// Every wait is bounded: a spin that exceeds its limit raises an abort flag
+// that all other waits observe, so the grid always drains.
+#include "device_common.hpp"
+#include "loop_kernel.hpp"
+
+namespace mca {
+
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kLoopThreads = 64 * kWaves;
+constexpr int kMaxTilesPerLane = 16;  // G <= 64 * 16 tiles in the persistent loop
+
+template <class T>
+__device__ __forceinline__ T ld_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <class T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait until every memory operation this wave issued has completed
+__device__ __forceinline__ void wait_own_memory() { __builtin_amdgcn_s_waitcnt(0); }
+
+__device__ __forceinline__ uint64_t pack(float v, uint32_t tag) {
+  return ((uint64_t)__float_as_uint(v) << 32) | tag;
+}
+// 16-bit step tag of a loss-change word: 1..65535, never the cleared value 0,
+// and different for consecutive steps.
+__device__ __forceinline__ uint32_t tag16(uint64_t s) { return (uint32_t)(s % 65535u) + 1u; }
+__device__ __forceinline__ uint64_t pack_dl(double v, uint32_t tag) {
+  return ((uint64_t)__double_as_longlong(v) & ~0xFFFFull) | tag;
+}
+__device__ __forceinline__ double unpack_dl(uint64_t w) {
+  return __longlong_as_double((long long)(w & ~0xFFFFull));
+}
+
+// Bounded spin helper: returns true when the grid must abort.
+__device__ __forceinline__ bool spin_step(uint32_t& spins, const LoopArgs& a) {
+  ++spins;
+  if ((spins & 255u) == 0u && ld_agent(&a.sync->abort) != 0u) return true;
+  if (spins > a.spin_limit) {
+    st_agent(&a.sync->abort, 1u);
+    return true;
+  }
+  __builtin_amdgcn_s_sleep(1);
+  return false;
+}
+
+// The last committed mutation, kept in LDS for one step.
+struct LastCommit {
+  int layer, j, i, code;
+  float w_new;
+  int valid;
+};
+
+// One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
+// the activation feeding it); zh: the cached local field of the mutated unit
+// when it is a hidden unit; zL: the sample's logits in LDS (stride 64).  The
+// new local field, logits and loss come back for a commit.  The same
+// expressions as column_sample() of the multi-kernel path, written without
+// branches on the candidate's layer (pairs of different candidates share a
+// wave).
+template <int CM>
+__device__ __forceinline__ float pair_eval(const NetDev& net, int layer, int j, float de,
+                                           const float* wcol, float ain, float zh,
+                                           const float* zL, float ell, int y, float& zn,
+                                           float (&z)[CM], float& ln) {
+  const int L = net.L, C = net.C;
+  const bool logit = layer == L - 1;
+  const float zb = logit ? zL[j * 64] : zh;
+  zn = zb + de * ain;
+  const float da = act_fn(zn, net.act, net.gamma) - act_fn(zb, net.act, net.gamma);
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) {
+    const float zc = (cc < C) ? zL[cc * 64] : 0.f;
+    const float hid = (cc < C) ? fmaf(da, wcol[cc], zc) : 0.f;
+    z[cc] = logit ? ((cc == j) ? zn : zc) : hid;
+  }
+  ln = ce_loss<CM>(z, C, y);
+  const bool changed = logit || da != 0.f;
+  return changed ? ln - ell : 0.f;
+}
+
+__device__ __forceinline__ float input_of(const NetDev& net, int layer, float a_raw) {
+  return (layer == 0) ? a_raw : act_fn(a_raw, net.act, net.gamma);
+}
+
+}  // namespace
+
+// KW = candidates per wave (K <= 4 KW), a compile-time bound so the operands
+// of a wave's candidates stay in registers; CM = bound on the class count.
+template <int KW, int CM>
+__global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
+  __shared__ NetDev net;
+  stage_net(net, a.net);
+  __shared__ float zl_lds[CM * 64];
+  __shared__ float ell_lds[64];
+  __shared__ int y_lds[64];
+  __shared__ mca_cand cand_lds[2][kLoopMaxK];
+  __shared__ Aux aux_lds[kLoopMaxK];
+  __shared__ float wcol_lds[kLoopMaxK][CM];
+  __shared__ float ain_lds[kLoopMaxK][64];
+  __shared__ float zh_lds[kLoopMaxK][64];
+  __shared__ float dlp_lds[kLoopMaxK][64];
+  __shared__ uint16_t list_lds[kLoopMaxK * 64];
+  __shared__ int list_n;
+  __shared__ LastCommit last;
+  __shared__ int dec_k;
+  __shared__ int aborted;
+
+  const int K = a.K, T = a.T, G = a.G;
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int C = net.C, L = net.L;
+  const int kpad = a.kpad;  // partial words per tile, a multiple of 16
+  if (tid == 0) aborted = 0;
+
+  if (g >= G) {
+    // ---------------------------------------------------- candidate reducers
+    const int k = (g - G) * kWaves + wave;
+    if (k >= K) return;
+    for (uint64_t s = 0; s < a.n_steps; ++s) {
+      const uint32_t tag = (uint32_t)(s + 1);
+      uint64_t w[kMaxTilesPerLane];
+#pragma unroll
+      for (int b = 0; b < kMaxTilesPerLane; ++b) w[b] = 0;
+      uint32_t spins = 0;
+      bool fresh = false, ab = false;
+      while (!fresh && !ab) {
+        fresh = true;
+#pragma unroll
+        for (int b = 0; b < kMaxTilesPerLane; ++b) {
+          const int gg = lane + 64 * b;
+          if (gg < G && (uint32_t)w[b] != tag) w[b] = ld_agent(&a.partials[(size_t)gg * kpad + k]);
+        }
+#pragma unroll
+        for (int b = 0; b < kMaxTilesPerLane; ++b) {
+          const int gg = lane + 64 * b;
+          fresh = fresh && (gg >= G || (uint32_t)w[b] == tag);
+        }
+        fresh = __all(fresh);
+        if (!fresh) ab = __any(spin_step(spins, a));
+      }
+      if (ab) return;
+      // fixed order: tiles lane, lane+64, ... in each lane, then a fixed
+      // butterfly over the lanes
+      double acc = 0.0;
+#pragma unroll
+      for (int b = 0; b < kMaxTilesPerLane; ++b)
+        if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) acc += __shfl_xor(acc, o, 64);
+      if (lane == 0) st_agent(&a.dls[k], pack_dl(acc / (double)net.N, tag16(s)));  // +inf: rejected
+    }
+    return;
+  }
+
+  // ------------------------------------------------------------ tile workgroup
+  const int64_t n = (int64_t)g * T + lane;
+  const bool live = lane < T && n < net.N;
+  const int nh = net.widths[L - 1];
+  const int64_t Ns = net.Ns;
+  // the tile's logits, losses and labels move to LDS for the whole launch
+  if (wave == 0) {
+    for (int c = 0; c < CM; ++c)
+      zl_lds[c * 64 + lane] = (live && c < C) ? net.Z[L - 1][(int64_t)c * Ns + n] : 0.f;
+    ell_lds[lane] = live ? net.ell[n] : 0.f;
+    y_lds[lane] = live ? net.y[n] : 0;
+  }
+  if (tid == 0) last.valid = 0;
+  for (int k = tid; k < K; k += kLoopThreads) cand_lds[0][k] = decode_index(net, a.t0, (uint64_t)k);
+  // committed scalars, carried in registers by tile 0, lane 0
+  double L_acc = 0.0;
+  uint64_t n_acc = 0, n_tie = 0;
+  int last_k = -1;
+  if (g == 0 && tid == 0) {
+    L_acc = a.st->L;
+    n_acc = a.st->accepted;
+    n_tie = a.st->tie;
+  }
+  __syncthreads();
+
+  for (uint64_t s = 0; s < a.n_steps; ++s) {
+    const uint32_t tag = (uint32_t)(s + 1);
+    const int buf = (int)(s & 1);
+    mca_cand* cands = cand_lds[buf];
+    // 1. every load of the step at once: the tile operands of this wave's
+    // candidates; per candidate its committed weight, code and logit column
+    float ar[KW], zr[KW];
+#pragma unroll
+    for (int q = 0; q < KW; ++q) {
+      const int k = wave + kWaves * q;
+      ar[q] = 0.f;
+      zr[q] = 0.f;
+      if (k < K && live) {
+        // indices only: a ternary candidate's code is being finished below
+        const int l = cands[k].layer, ci = cands[k].i, cj = cands[k].j;
+        const float* src = (l == 0) ? net.XT : net.Z[l - 1];
+        ar[q] = src[(int64_t)ci * Ns + n];
+        zr[q] = net.Z[l][(int64_t)cj * Ns + n];
+      }
+    }
+    if (tid < K) {
+      const int k = tid;
+      mca_cand c = cands[k];
+      const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+      float w = net.W[c.layer][idx];
+      int cur = net.ternary ? (int)net.codes[c.layer][idx] : 0;
+      const bool hid = c.layer == L - 2;
+      const int jj = hid ? c.j : 0;
+      float col[CM];
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc) col[cc] = net.W[L - 1][(int64_t)(cc < C ? cc : 0) * nh + jj];
+      const LastCommit lc = last;
+      if (lc.valid) {  // committed last step: its store may still be in flight
+        if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
+          w = lc.w_new;
+          cur = lc.code;
+        }
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc)
+          if (lc.layer == L - 1 && lc.j == cc && lc.i == jj) col[cc] = lc.w_new;
+      }
+      if (net.ternary) {
+        finish_ternary(net, c, cur);
+        cands[k].d = c.d;
+        cands[k].code = c.code;
+      }
+      Aux au;
+      au.w_old = w;
+      au.w_new = net.ternary ? (float)c.code * net.scales[c.layer] : w + c.d;
+      au.de = au.w_new - au.w_old;
+      au.valid = !(net.bound > 0.f && fabsf(au.w_new) >= net.bound);
+      aux_lds[k] = au;
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc) wcol_lds[k][cc] = (hid && cc < C) ? col[cc] : 0.f;
+    }
+    if (tid == 0) list_n = 0;
+    wait_own_memory();  // also retires this wave's stores of the previous step
+    __syncthreads();
+    // 2a. compact the pairs whose input is non-zero into the work list
+#pragma unroll
+    for (int q = 0; q < KW; ++q) {
+      const int k = wave + kWaves * q;
+      if (k < K) {
+        const int l = cands[k].layer;
+        const float ain = input_of(net, l, ar[q]);
+        ain_lds[k][lane] = ain;
+        zh_lds[k][lane] = zr[q];
+        dlp_lds[k][lane] = 0.f;
+        const bool act = live && ain != 0.f;
+        const uint64_t m = __ballot(act);
+        int base = 0;
+        if (lane == 0 && m) base = atomicAdd(&list_n, (int)__popcll(m));
+        base = __shfl(base, 0, 64);
+        if (act) {
+          const int pos = base + (int)__popcll(m & ((1ull << lane) - 1ull));
+          list_lds[pos] = (uint16_t)((k << 6) | lane);
+        }
+      }
+    }
+    __syncthreads();
+    // 2b. every lane of the workgroup scores list entries
+    const int n_list = list_n;
+    for (int e = tid; e < n_list; e += kLoopThreads) {
+      const int code = list_lds[e];
+      const int k = code >> 6, sl = code & 63;
+      const mca_cand& c = cands[k];
+      float zn, z[CM], ln;
+      dlp_lds[k][sl] = pair_eval<CM>(net, c.layer, c.j, aux_lds[k].de, wcol_lds[k], ain_lds[k][sl],
+                                     zh_lds[k][sl], &zl_lds[sl], ell_lds[sl], y_lds[sl], zn, z, ln);
+    }
+    __syncthreads();
+    // 2c. per candidate: sum its 64 slots in sample order (4 threads x 16),
+    // publish the tile's partial sum
+    uint64_t* part = a.partials + (size_t)g * kpad;
+    {
+      const int k = tid >> 2, r = tid & 3;
+      float v = 0.f;
+      if (k < K) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v += dlp_lds[k][r * 16 + i];
+      }
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      if (k < K && r == 0) st_agent(&part[k], pack(aux_lds[k].valid ? v : __builtin_huge_valf(), tag));
+    }
+    // 3. wave 0 gathers the K loss changes and decides (every tile takes the
+    // same decision from the same words); waves 1-3 draw the next candidates
+    if (wave == 0) {
+      const uint32_t t16 = tag16(s);
+      uint64_t d = 0;
+      uint32_t spins = 0;
+      bool ab = false;
+      while (true) {
+        if (lane < K && (uint32_t)(d & 0xFFFFu) != t16) d = ld_agent(&a.dls[lane]);
+        if (__all(lane >= K || (uint32_t)(d & 0xFFFFu) == t16)) break;
+        if ((ab = __any(spin_step(spins, a)))) break;
+      }
+      const double v = unpack_dl(d);
+      const uint64_t acc_mask = __ballot(!ab && lane < K && accepts(v, net.ties));
+      const int kc = acc_mask ? (int)__ffsll((unsigned long long)acc_mask) - 1 : -1;
+      if (lane == 0) {
+        aborted = ab ? 1 : 0;
+        dec_k = ab ? -1 : kc;
+      }
+      if (g == 0 && !ab) {
+        const uint64_t tie_mask = __ballot(lane < K && fabs(v) < 1e-6);
+        const double vk = __shfl(v, kc < 0 ? 0 : kc, 64);
+        if (lane == 0) {
+          const uint64_t upto = (kc >= 0) ? ((kc == 63) ? ~0ull : ((2ull << kc) - 1ull)) : ~0ull;
+          n_tie += (uint64_t)__popcll(tie_mask & upto);
+          if (kc >= 0) {
+            L_acc += vk;
+            ++n_acc;
+          }
+          last_k = kc;
+        }
+        const uint64_t t = a.t0 + s;
+        if (a.tr_chosen != nullptr) {
+          const int64_t slot = (int64_t)(t - a.trace_base);
+          if (slot >= 0 && slot < a.tr_cap) {
+            if (lane == 0) a.tr_chosen[slot] = kc;
+            if (a.tr_dl != nullptr && lane < K) a.tr_dl[slot * K + lane] = v;
+          }
+        }
+      }
+    } else if (s + 1 < a.n_steps) {
+      for (int k = tid - 64; k < K; k += kLoopThreads - 64)
+        cand_lds[buf ^ 1][k] = decode_index(net, a.t0 + s + 1, (uint64_t)k);
+    }
+    __syncthreads();
+    if (aborted) break;
+    // 4. commit on this tile by the wave that loaded the winner's operands;
+    // every workgroup writes the new weight
+    const int kc = dec_k;
+    if (kc >= 0 && wave == (kc % kWaves)) {
+      const int qc = kc / kWaves;
+      float a_raw = 0.f, z_raw = 0.f;
+#pragma unroll
+      for (int q = 0; q < KW; ++q)
+        if (q == qc) { a_raw = ar[q]; z_raw = zr[q]; }
+      const mca_cand c = cands[kc];
+      const Aux au = aux_lds[kc];
+      const float ain = input_of(net, c.layer, a_raw);
+      float zn, z[CM], ln;
+      (void)pair_eval<CM>(net, c.layer, c.j, au.de, wcol_lds[kc], ain, z_raw, &zl_lds[lane],
+                          ell_lds[lane], y_lds[lane], zn, z, ln);
+      if (live && ain != 0.f) {
+        if (c.layer != L - 1) net.Z[c.layer][(int64_t)c.j * Ns + n] = zn;
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc)
+          if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
+        ell_lds[lane] = ln;
+      }
+      if (lane == 0) {
+        const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+        net.W[c.layer][idx] = au.w_new;
+        if (net.ternary) net.codes[c.layer][idx] = (int8_t)c.code;
+        last.layer = c.layer;
+        last.j = c.j;
+        last.i = c.i;
+        last.code = c.code;
+        last.w_new = au.w_new;
+        last.valid = 1;
+      }
+      wait_own_memory();  // the tile's new local fields are in place for the next step
+    }
+    if (kc < 0 && tid == 0) last.valid = 0;
+    __syncthreads();
+  }
+  // the tile's logits and losses go back to HBM; tile 0 writes the state
+  if (wave == 0 && live) {
+    for (int c = 0; c < C; ++c) net.Z[L - 1][(int64_t)c * Ns + n] = zl_lds[c * 64 + lane];
+    net.ell[n] = ell_lds[lane];
+  }
+  if (g == 0 && tid == 0 && !aborted) {
+    DevState* st = a.st;
+    st->L = L_acc;
+    st->t = a.t0 + a.n_steps;
+    st->steps += a.n_steps;
+    st->evaluated += a.n_steps * (uint64_t)K;
+    st->accepted = n_acc;
+    st->tie = n_tie;
+    st->chosen = last_k;
+  }
+}
+
+// Clears the tags before a launch (a fill kernel, so the sequence can be
+// captured in a graph).
+__global__ void k_reset_loop(LoopSync* s, uint64_t* partials, int64_t n_words, uint64_t* dls,
+                             int K) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_words) partials[i] = 0;
+  if (i < K) dls[i] = 0;
+  if (i == 0) s->abort = 0;
+}
+
+namespace {
+template <int KW>
+const void* loop_fn(int C) {
+  return C == 10 ? (const void*)k_step_loop<KW, 10> : (const void*)k_step_loop<KW, kCMax>;
+}
+
+const void* pick_loop(int K, int C) {
+  const int kw = (K + kWaves - 1) / kWaves;
+  if (kw <= 1) return loop_fn<1>(C);
+  if (kw <= 2) return loop_fn<2>(C);
+  if (kw <= 4) return loop_fn<4>(C);
+  if (kw <= 8) return loop_fn<8>(C);
+  return loop_fn<16>(C);
+}
+}  // namespace
+
+int step_loop_reducers(int K) { return (K + kWaves - 1) / kWaves; }
+
+hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s) {
+  const int64_t words = (int64_t)a.G * a.kpad;
+  const int64_t n = words > a.K ? words : a.K;
+  hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sync,
+                     a.partials, words, a.dls, a.K);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  void* args[] = {(void*)&a};
+  // G tile workgroups and the candidate reducers
+  return hipLaunchCooperativeKernel(pick_loop(a.K, a.net.C),
+                                    dim3(a.G + step_loop_reducers(a.K)), dim3(kLoopThreads), args,
+                                    0, s);
+}
+
+hipError_t step_loop_max_blocks(int K, int C, int* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  int per_cu = 0, cus = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, pick_loop(K, C), kLoopThreads, 0);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  *out = per_cu * cus;
+  return hipSuccess;
+}
+
+}  // namespace mca

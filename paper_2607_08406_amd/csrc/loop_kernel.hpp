@@ -1,0 +1,44 @@
+// Persistent cooperative step loop (loop_kernel.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "device_common.hpp"
+
+namespace mca {
+
+constexpr int kLoopMaxK = 64;  // candidates per step in the persistent loop
+
+// Abort word of the step loop, on its own 256-byte line.
+struct LoopSync {
+  uint32_t abort;      // set when a bounded wait ran out
+  uint32_t pad[63];
+};
+
+struct LoopArgs {
+  NetDev net;
+  int K;                // candidates per step (<= kLoopMaxK)
+  int T;                // samples per workgroup tile (<= 64)
+  int G;                // tile workgroups (<= 64 * 16)
+  int kpad;             // partial words per tile: K rounded up to 16 (128 bytes)
+  uint64_t t0;          // first step index
+  uint64_t n_steps;     // steps in this launch (< 2^32)
+  uint64_t* partials;   // [G][kpad] tagged per-tile loss-change sums
+  uint64_t* dls;        // [K] tagged loss changes
+  LoopSync* sync;
+  DevState* st;
+  int32_t* tr_chosen;   // trace (nullable)
+  double* tr_dl;        // trace of every dL (nullable)
+  int64_t tr_cap;
+  uint64_t trace_base;  // step index of trace slot 0
+  uint32_t spin_limit;  // polls before a wait gives up and aborts the grid
+};
+
+constexpr int kLoopMaxTiles = 64 * 16;
+
+// Workgroups of the candidate reducers for K candidates (one wave each).
+int step_loop_reducers(int K);
+hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s);
+hipError_t step_loop_max_blocks(int K, int C, int* out);
+
+}  // namespace mca

@@ -6,12 +6,14 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
 
-#include "../../include/mca.h"
+#include "mca.h"
 #include "device_common.hpp"
+#include "loop_kernel.hpp"
 #include "mlp_kernels.hpp"
 
 using mca::Aux;
@@ -22,6 +24,7 @@ namespace {
 
 constexpr int64_t kTraceCap = 4096;  // steps per trace chunk kept on the device
 constexpr size_t kAlign = 256;
+constexpr int kMinLoopTile = 16;
 
 thread_local std::string g_thread_error;
 
@@ -32,7 +35,8 @@ struct Layout {
   int64_t Ns = 0;
   int ntiles = 0;
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
-  size_t tr_chosen = 0, tr_dl = 0;
+  size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
+  int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
   size_t total = 0;
 };
@@ -101,6 +105,15 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.state = take(sizeof(DevState));
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
+  // persistent loop: tiles of T samples (16..64), one workgroup each; the
+  // partial sums are sized for the smallest tile
+  lo.loop_T = 64;
+  lo.loop_G = (int)((N + lo.loop_T - 1) / lo.loop_T);
+  const int64_t g_max = (N + kMinLoopTile - 1) / kMinLoopTile;
+  const int64_t kpad = (std::min<int32_t>(k_max, mca::kLoopMaxK) + 15) / 16 * 16;
+  lo.loop_partials = take((size_t)g_max * kpad * sizeof(uint64_t));
+  lo.loop_dls = take((size_t)mca::kLoopMaxK * sizeof(uint64_t));
+  lo.loop_sync = take(sizeof(mca::LoopSync));
   lo.total = off;
   return lo;
 }
@@ -125,12 +138,16 @@ struct mca_ctx {
   DevState* st = nullptr;
   int32_t* tr_chosen = nullptr;
   double* tr_dl = nullptr;
+  uint64_t* loop_partials = nullptr;
+  uint64_t* loop_dls = nullptr;
+  mca::LoopSync* loop_sync = nullptr;
+  bool use_loop = true;
   bool pending = false;
   int32_t pending_K = 0;
   bool poisoned = false;
   std::string err;
   // phase timing
-  bool timing = false;
+  int32_t timing = 0;  // bit mask of timed phases
   struct Rec { int phase; hipEvent_t a, b; };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
@@ -176,7 +193,7 @@ hipEvent_t get_event(mca_ctx* ctx) {
 // Wraps one launch in a pair of events when timing is on.
 template <class F>
 hipError_t timed(mca_ctx* ctx, int phase, F&& launch) {
-  if (!ctx->timing) return launch();
+  if (!(ctx->timing & (1 << phase))) return launch();
   hipEvent_t a = get_event(ctx), b = get_event(ctx);
   if (!a || !b) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(a, ctx->stream);
@@ -370,6 +387,9 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   ctx->st = (DevState*)(ws + lo.state);
   ctx->tr_chosen = (int32_t*)(ws + lo.tr_chosen);
   ctx->tr_dl = (double*)(ws + lo.tr_dl);
+  ctx->loop_partials = (uint64_t*)(ws + lo.loop_partials);
+  ctx->loop_dls = (uint64_t*)(ws + lo.loop_dls);
+  ctx->loop_sync = (mca::LoopSync*)(ws + lo.loop_sync);
 
   // inputs, transposed to the unit-major layout (zero padding to Ns)
   {
@@ -459,6 +479,22 @@ int mca_rollback(mca_ctx* ctx) {
   return MCA_OK;
 }
 
+int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value) {
+  MCA_LIVE(ctx);
+  if (option == MCA_OPT_PERSISTENT_LOOP) {
+    if (value != 0 && value != 1) return fail(ctx, MCA_EINVAL, "MCA_OPT_PERSISTENT_LOOP takes 0 or 1");
+    ctx->use_loop = value != 0;
+    return MCA_OK;
+  }
+  if (option == MCA_OPT_LOOP_TILE) {
+    if (value < kMinLoopTile || value > 64) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_TILE takes 16..64");
+    ctx->lo.loop_T = (int)value;
+    ctx->lo.loop_G = (int)((ctx->net.N + value - 1) / value);
+    return MCA_OK;
+  }
+  return fail(ctx, MCA_EINVAL, "unknown option");
+}
+
 int mca_set_step(mca_ctx* ctx, uint64_t next_step) {
   MCA_LIVE(ctx);
   if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
@@ -477,6 +513,48 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   if (rc != MCA_OK) return rc;
   const NetDev& net = ctx->net;
   uint64_t done = 0;
+  int max_blocks = 0;
+  if (ctx->use_loop && net.L <= 2 && K <= mca::kLoopMaxK)
+    MCA_HIP(ctx, mca::step_loop_max_blocks(K, net.C, &max_blocks));
+  // G tile workgroups plus the candidate reducers must all be resident at once
+  const bool loop_ok = ctx->use_loop && net.L <= 2 && K <= mca::kLoopMaxK &&
+                       ctx->lo.loop_G <= mca::kLoopMaxTiles &&
+                       ctx->lo.loop_G + mca::step_loop_reducers(K) <= max_blocks;
+  while (loop_ok && done < n_steps) {
+    const uint64_t cap = trace ? (uint64_t)kTraceCap : ((uint64_t)1 << 22);
+    const uint64_t chunk = std::min<uint64_t>(n_steps - done, cap);
+    mca::LoopArgs a{};
+    a.net = net;
+    a.K = K;
+    a.T = ctx->lo.loop_T;
+    a.t0 = before.t + done;
+    a.n_steps = chunk;
+    a.G = ctx->lo.loop_G;
+    a.kpad = (K + 15) / 16 * 16;
+    a.partials = ctx->loop_partials;
+    a.dls = ctx->loop_dls;
+    a.sync = ctx->loop_sync;
+    a.st = ctx->st;
+    a.tr_chosen = trace ? ctx->tr_chosen : nullptr;
+    a.tr_dl = (trace && trace->dloss) ? ctx->tr_dl : nullptr;
+    a.tr_cap = kTraceCap;
+    a.trace_base = a.t0;
+    a.spin_limit = 1u << 22;
+    MCA_HIP(ctx, timed(ctx, 4, [&] { return mca::launch_step_loop(a, ctx->stream); }));
+    mca::LoopSync sync{};
+    MCA_HIP(ctx, hipMemcpyAsync(&sync, ctx->loop_sync, sizeof sync, hipMemcpyDeviceToHost, ctx->stream));
+    if (trace != nullptr) {
+      MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));
+      if (trace->dloss)
+        MCA_HIP(ctx, hipMemcpyAsync(trace->dloss + done * K, ctx->tr_dl, chunk * K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+    }
+    MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    if (sync.abort != 0) {
+      ctx->poisoned = true;
+      return fail(ctx, MCA_EDEVICE, "step loop aborted: a bounded wait between workgroups ran out");
+    }
+    done += chunk;
+  }
   while (done < n_steps) {
     const uint64_t chunk = std::min<uint64_t>(n_steps - done, (uint64_t)kTraceCap);
     int32_t* trc = nullptr;
@@ -568,9 +646,9 @@ int mca_get_sample_losses(mca_ctx* ctx, float* out_host) {
   return MCA_OK;
 }
 
-int mca_set_timing(mca_ctx* ctx, int32_t enable) {
+int mca_set_timing(mca_ctx* ctx, int32_t phase_mask) {
   MCA_LIVE(ctx);
-  ctx->timing = enable != 0;
+  ctx->timing = phase_mask;
   return MCA_OK;
 }
 

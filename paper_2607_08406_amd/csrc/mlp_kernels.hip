@@ -20,8 +20,10 @@ namespace mca {
 // candidate stream
 // ---------------------------------------------------------------------------
 
-__global__ void k_propose(NetDev net, uint64_t t_host, int use_dev_t, const DevState* st,
+__global__ void k_propose(NetDev net_arg, uint64_t t_host, int use_dev_t, const DevState* st,
                           int K, mca_cand* cands, Aux* aux) {
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= K) return;
   const uint64_t t = use_dev_t ? st->t : t_host;
@@ -30,7 +32,9 @@ __global__ void k_propose(NetDev net, uint64_t t_host, int use_dev_t, const DevS
   aux[k] = prepare_candidate(net, c);
 }
 
-__global__ void k_prepare(NetDev net, const mca_cand* cands, int K, Aux* aux) {
+__global__ void k_prepare(NetDev net_arg, const mca_cand* cands, int K, Aux* aux) {
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= K) return;
   aux[k] = prepare_candidate(net, cands[k]);
@@ -91,10 +95,12 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
 
 // grid (tiles, K): block (tile, k) sums the loss change of candidate k over
 // the tile's kTile samples; partial[k * ntiles + tile].
-__global__ __launch_bounds__(kTile) void k_eval_column(NetDev net, const mca_cand* cands,
+__global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca_cand* cands,
                                                        const Aux* aux, float* partial,
                                                        int ntiles) {
   __shared__ float red[4];
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
   const int k = blockIdx.y, tile = blockIdx.x;
   const mca_cand c = cands[k];
   const Aux a = aux[k];
@@ -109,7 +115,7 @@ __global__ __launch_bounds__(kTile) void k_eval_column(NetDev net, const mca_can
 // selection (Eq. 6): one block, thread k owns candidate k
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kMaxK) void k_select(NetDev net, const float* partial, int ntiles,
+__global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float* partial, int ntiles,
                                                   const Aux* aux, int K, double* dL,
                                                   DevState* st, int do_select,
                                                   int32_t* tr_chosen, double* tr_dl,
@@ -155,9 +161,11 @@ __global__ __launch_bounds__(kMaxK) void k_select(NetDev net, const float* parti
 // the device decision st->chosen (no-op when -1)
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kTile) void k_commit_column(NetDev net, const mca_cand* cands,
+__global__ __launch_bounds__(kTile) void k_commit_column(NetDev net_arg, const mca_cand* cands,
                                                          const Aux* aux, const double* dL,
                                                          DevState* st, int k_host) {
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
   const int k = (k_host >= 0) ? k_host : st->chosen;
   if (k < 0) return;
   const mca_cand c = cands[k];
@@ -238,8 +246,10 @@ __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, i
 }
 
 // l_n for every sample from the cached logits; fp64 block sums of l_n.
-__global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net, double* bsum) {
+__global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net_arg, double* bsum) {
   __shared__ double red[kTile];
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
   const int64_t n = (int64_t)blockIdx.x * kTile + threadIdx.x;
   double v = 0.0;
   if (n < net.N) {

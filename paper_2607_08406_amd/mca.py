@@ -27,6 +27,7 @@ MCA_NET_MLP, MCA_NET_TRANSFORMER = 0, 1
 MCA_ACT_TANH, MCA_ACT_GAUSS = 0, 1
 MCA_WEIGHTS_FP32, MCA_WEIGHTS_TERNARY = 0, 1
 MCA_PICK_WEIGHT, MCA_PICK_LAYER = 0, 1
+MCA_OPT_PERSISTENT_LOOP, MCA_OPT_LOOP_TILE = 1, 2
 
 STATUS_NAMES = {0: "MCA_OK", -1: "MCA_EINVAL", -2: "MCA_ESTATE", -3: "MCA_ENOSPACE",
                 -4: "MCA_EDEVICE", -5: "MCA_EPOISONED", -6: "MCA_EUNSUPPORTED"}
@@ -95,6 +96,7 @@ _SIGNATURES = {
     "mca_eval_losses": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
     "mca_commit": (ctypes.c_int, [_P, ctypes.c_int32]),
     "mca_rollback": (ctypes.c_int, [_P]),
+    "mca_set_option": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int64]),
     "mca_set_step": (ctypes.c_int, [_P, ctypes.c_uint64]),
     "mca_run_steps": (ctypes.c_int, [_P, ctypes.c_uint64, ctypes.c_int32,
                                      ctypes.POINTER(mca_trace), ctypes.POINTER(mca_stats)]),
@@ -229,6 +231,10 @@ def mca_rollback(ctx):
     _check(load_library().mca_rollback(ctx), ctx)
 
 
+def mca_set_option(ctx, option: int, value: int):
+    _check(load_library().mca_set_option(ctx, option, value), ctx)
+
+
 def mca_set_step(ctx, next_step: int):
     _check(load_library().mca_set_step(ctx, next_step), ctx)
 
@@ -284,8 +290,11 @@ def mca_get_sample_losses(ctx, n: int) -> np.ndarray:
     return out
 
 
-def mca_set_timing(ctx, enable: bool):
-    _check(load_library().mca_set_timing(ctx, int(enable)), ctx)
+PHASES = ["propose", "eval", "select", "commit", "step_loop", "forward"]
+
+
+def mca_set_timing(ctx, phase_mask: int):
+    _check(load_library().mca_set_timing(ctx, int(phase_mask)), ctx)
 
 
 def mca_get_timing(ctx, reset: bool = False):
@@ -336,6 +345,9 @@ class Context:
 
     def rollback(self):
         mca_rollback(self.ctx)
+
+    def set_option(self, option, value):
+        mca_set_option(self.ctx, option, value)
 
     def set_step(self, next_step):
         mca_set_step(self.ctx, next_step)

@@ -51,13 +51,16 @@ def test_tiny_init_and_explicit_steps(mca):
     ctx.close()
 
 
-def test_tiny_device_loop_full_window(mca):
+@pytest.mark.parametrize("persistent", [1, 0])
+def test_tiny_device_loop_full_window(mca, persistent):
     """All 20,000 steps of the tiny workload (K=1) in the device loop, replayed
-    on the oracle: every decision equal outside the tie band, weights bit-equal."""
+    on the oracle: every decision equal outside the tie band, weights bit-equal.
+    Both the persistent cooperative loop and the one-launch-per-phase loop."""
     cfg = CONFIGS["tiny"]
-    banner("tiny 20000-step device loop")
+    banner(f"tiny 20000-step device loop persistent={persistent}")
     w = mlp_workload(cfg)
     ctx, ref = make_pair(cfg, w, k_max=1)
+    ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, persistent)
     st, chosen, dloss = ctx.run_steps(cfg.steps, 1, trace=True, trace_dloss=True)
     assert st.steps == cfg.steps and st.evaluated == cfg.steps and st.next_step == cfg.steps
     ties, acc = replay_trace(ref, cfg, 0, chosen, dloss, 1)
@@ -72,11 +75,14 @@ def test_tiny_device_loop_full_window(mca):
     ctx.close()
 
 
-def test_small_wide_explicit_and_loop(mca):
+@pytest.mark.parametrize("persistent,tile", [(1, 64), (1, 40), (1, 16), (0, 64)])
+def test_small_wide_explicit_and_loop(mca, persistent, tile):
     cfg = small_wide()
-    banner("wide 784-512-10 N=1000 explicit + loop")
+    banner(f"wide 784-512-10 N=1000 explicit + loop persistent={persistent} tile={tile}")
     w = mlp_workload(cfg)
     ctx, ref = make_pair(cfg, w, k_max=64)
+    ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, persistent)
+    ctx.set_option(mca.MCA_OPT_LOOP_TILE, tile)
     ties, acc = explicit_steps(ctx, ref, cfg, 0, 40, 64)
     assert acc > 10
     assert_state_equal(ctx, ref)
@@ -180,6 +186,10 @@ def test_error_paths(mca):
     ctx.commit(3)
     with pytest.raises(mca.MCAError, match="ESTATE"):
         ctx.commit(3)
+    for opt, val in [(mca.MCA_OPT_LOOP_TILE, 15), (mca.MCA_OPT_LOOP_TILE, 65),
+                     (mca.MCA_OPT_PERSISTENT_LOOP, 2), (99, 1)]:
+        with pytest.raises(mca.MCAError, match="EINVAL"):
+            ctx.set_option(opt, val)
     ctx.close()
     bad_y = w["y"].copy()
     bad_y[0] = 10
