@@ -47,6 +47,23 @@ def algorithmic_bytes_per_step(cfg) -> float:
     return shared + K * per_cand
 
 
+def measured_traffic(kernel: str, workload: str, steps: int):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary (calibrated against a plain copy), or None when the kernel source
+    has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in ["loop_kernel.hip", "loop_kernel.hpp", "device_common.hpp"]:
+        h.update(open(os.path.join(ROOT, "paper_2607_08406_amd", "csrc", f), "rb").read())
+    if rec.get("source_sha256") != h.hexdigest():
+        return None
+    return rec["hbm_bytes_per_step"] * steps
+
+
 def cpu_baseline(cfg, w, seconds: float):
     """The fp64 oracle (incremental mode, all K candidates scored per step, as
     the device does) on the host cores, for about `seconds` of work."""
@@ -80,6 +97,17 @@ def cpu_baseline(cfg, w, seconds: float):
             "accepted_per_s": acc / el}
 
 
+def copy_calibration(nbytes: int):
+    """A plain device-to-device copy of nbytes (torch's copy kernel), 5 launches."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "launches": 5}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -91,7 +119,13 @@ def main():
     ap.add_argument("--tile", type=int, default=0, help="samples per workgroup (16..64)")
     ap.add_argument("--per-phase", action="store_true",
                     help="one launch per phase per step instead of the persistent loop")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run a plain device copy of this many bytes (5 times): the "
+                         "reference kernel that calibrates FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the MCA path here is single-GPU; sharding is a design note only)",
@@ -160,7 +194,9 @@ def main():
                    "n_params": cfg.n_params},
         "roofline": {"bound": "hbm", "kernel": kernel,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": (measured_traffic(kernel, "wide_784-16384-10_K64", args.steps)
+                                 if loop and cfg.name == "wide" else None),
                      "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
                      "launches": int(launches[dominant]),
                      "bytes_per_step": algorithmic_bytes_per_step(cfg)},
