@@ -9,14 +9,17 @@
 // the step's K candidates itself (the stream is counter-based), scores all of
 // them on its tile and publishes one partial loss change per candidate
 // (+inf for a candidate rejected by the weight bound).  The reduction is
-// sharded by candidate: wave w of reducer workgroup r owns candidate 4r + w,
+// sharded by candidate: wave w < 4 of reducer workgroup r owns candidate 4r + w,
 // adds its G partial sums in a fixed order (fp64) and publishes the loss
 // change dL_k.  Every tile workgroup reads all K loss changes and takes the
 // same decision itself: the first candidate in stream order that passes the
 // test (Eq. 6).  It then applies the commit to its own tile with the same
 // expressions the evaluation used.  Tile 0 also keeps the committed loss and
-// the counters.  While a tile workgroup waits, its idle waves draw the next
-// step's candidates (the draw needs no state).
+// the counters.  While wave 0 of a tile workgroup waits for the loss changes,
+// waves 1-15 draw the next step's candidates (the draw needs no state) and
+// stage their operands and weights in a second LDS buffer; what the pending
+// commit changes (one hidden row of the tile, one weight, code or
+// logit-layer column entry) is patched in LDS before use.
 //
 // Sparse inputs: a sample whose input to the mutated weight is zero does not
 // change (about 81 % of an image column), so a workgroup first compacts the
@@ -27,13 +30,14 @@
 //
 // Weights are read with ordinary cached loads.  Every tile workgroup writes
 // every committed weight itself, so each CU's L1 and each XCD's L2 that may
-// hold the old value is updated by a local store; during the one step in
-// which that store may still be in flight the value comes from LDS.
+// hold the old value is updated by a local store; the committing wave waits
+// for its stores during the next step, before any wave reads them again, and
+// until then the value comes from LDS.
 //
 // Cross-workgroup words carry their own step tag, so no separate flag, fence
 // or L2 writeback is needed: a partial sum is one 64-bit word (fp32 value |
-// 32-bit step tag), each tile's K words padded to whole 128-byte lines so no
-// two tiles write the same line; a loss change is one fp64 word whose 16 low
+// 32-bit step tag), stored candidate-major so a reducer polls one candidate's
+// G contiguous words; a loss change is one fp64 word whose 16 low
 // mantissa bits are replaced by the step tag (2^-36 relative truncation, the
 // same bits for every reader).  They are written and read with relaxed
 // agent-scope atomics, which the compiler emits as coherent (sc1) accesses.
@@ -47,11 +51,37 @@
 
 namespace mca {
 
+// Phase timestamps for profiling builds (compiled with -DMCA_PHASE_PROBES);
+// they expand to nothing otherwise.  Slot layout: tile g (0: first tile, 1:
+// last tile) phase p of step s < 256 at (g * 256 + s) * 8 + p; every tile's
+// publish time at 6144 + s * 512 + g; candidate 0's reducer and tile 0's
+// wave 0 at 137216 + s * 4 + {0 fresh, 1 published, 2 poll start, 3 seen};
+// every candidate's publish time at 138240 + s * 64 + k; tile 0's poll
+// iterations at 154624 + s.
+#ifdef MCA_PHASE_PROBES
+__device__ int64_t* g_phase_probes;
+#define MCA_PROBE(slot)                                                        \
+  do {                                                                         \
+    if (probes) probes[slot] = (int64_t)__builtin_amdgcn_s_memrealtime();      \
+  } while (0)
+extern "C" hipError_t mca_set_phase_probes(void* p) {
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_phase_probes), &p, sizeof p);
+}
+#else
+#define MCA_PROBE(slot) \
+  do {                  \
+  } while (0)
+#endif
+constexpr int64_t kProbePost = 6144, kProbeRed = 6144 + 256 * 512;
+constexpr int64_t kProbeRedAll = kProbeRed + 256 * 4;  // + s * 64 + k: candidate k published
+
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 16;  // 1024 threads: four waves per SIMD hide the list's latencies
 constexpr int kLoopThreads = 64 * kWaves;
-constexpr int kMaxTilesPerLane = 16;  // G <= 64 * 16 tiles in the persistent loop
+constexpr int kReducerWaves = 4;      // candidates per reducer workgroup
+constexpr int kMaxTilesPerLane = 8;   // G <= 64 * 8 tiles in the persistent loop
+constexpr int kReplicas = 8;          // copies of each published loss change
 
 template <class T>
 __device__ __forceinline__ T ld_agent(const T* p) {
@@ -136,18 +166,26 @@ template <int KW, int CM>
 __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ NetDev net;
   stage_net(net, a.net);
+#ifdef MCA_PHASE_PROBES
+  int64_t* const probes = g_phase_probes;
+#endif
   __shared__ float zl_lds[CM * 64];
   __shared__ float ell_lds[64];
   __shared__ int y_lds[64];
   __shared__ mca_cand cand_lds[2][kLoopMaxK];
   __shared__ Aux aux_lds[kLoopMaxK];
   __shared__ float wcol_lds[kLoopMaxK][CM];
-  __shared__ float ain_lds[kLoopMaxK][64];
-  __shared__ float zh_lds[kLoopMaxK][64];
+  __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
+  __shared__ float zh_lds[2][kLoopMaxK][64];
+  __shared__ float pw_lds[2][kLoopMaxK];
+  __shared__ int pcode_lds[2][kLoopMaxK];
+  __shared__ float pcol_lds[2][kLoopMaxK][CM];
   __shared__ float dlp_lds[kLoopMaxK][64];
   __shared__ uint16_t list_lds[kLoopMaxK * 64];
   __shared__ int list_n;
   __shared__ LastCommit last;
+  __shared__ float zrow_lds[64];  // the committed hidden row of this tile
+  __shared__ double red_lds[kReducerWaves][64];  // reducer lane sums
   __shared__ int dec_k;
   __shared__ int aborted;
 
@@ -155,15 +193,21 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = net.C, L = net.L;
-  const int kpad = a.kpad;  // partial words per tile, a multiple of 16
   if (tid == 0) aborted = 0;
 
   if (g >= G) {
     // ---------------------------------------------------- candidate reducers
-    const int k = (g - G) * kWaves + wave;
+    // Waves 0-3 of each reducer workgroup own one candidate each (one wave
+    // per SIMD: a single polling wave per SIMD is not starved by the issue
+    // priority of older waves); the other waves have nothing to do.
+    if (wave >= kReducerWaves) return;  // no block barrier follows in the reducers
+    const int k = (g - G) * kReducerWaves + wave;
     if (k >= K) return;
+    const uint64_t* mine = a.partials + (size_t)k * a.gpad;  // candidate-major: G words
+    double* sums = red_lds[wave];
     for (uint64_t s = 0; s < a.n_steps; ++s) {
       const uint32_t tag = (uint32_t)(s + 1);
+      // lane l adds tiles l, l+64, ... in that order
       uint64_t w[kMaxTilesPerLane];
 #pragma unroll
       for (int b = 0; b < kMaxTilesPerLane; ++b) w[b] = 0;
@@ -174,7 +218,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
         for (int b = 0; b < kMaxTilesPerLane; ++b) {
           const int gg = lane + 64 * b;
-          if (gg < G && (uint32_t)w[b] != tag) w[b] = ld_agent(&a.partials[(size_t)gg * kpad + k]);
+          if (gg < G && (uint32_t)w[b] != tag) w[b] = ld_agent(&mine[gg]);
         }
 #pragma unroll
         for (int b = 0; b < kMaxTilesPerLane; ++b) {
@@ -185,15 +229,27 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         if (!fresh) ab = __any(spin_step(spins, a));
       }
       if (ab) return;
-      // fixed order: tiles lane, lane+64, ... in each lane, then a fixed
-      // butterfly over the lanes
+      if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4);
       double acc = 0.0;
 #pragma unroll
       for (int b = 0; b < kMaxTilesPerLane; ++b)
         if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) acc += __shfl_xor(acc, o, 64);
-      if (lane == 0) st_agent(&a.dls[k], pack_dl(acc / (double)net.N, tag16(s)));  // +inf: rejected
+      // lane 0 adds the 64 lane sums in lane order (LDS, this wave only)
+      sums[lane] = acc;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      double tot = 0.0;
+      if (lane == 0) {
+#pragma unroll 8
+        for (int r = 0; r < 64; ++r) tot += sums[r];
+      }
+      tot = __shfl(tot, 0, 64);
+      const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
+      if (lane < kReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
+      if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 1);
+      if (lane == 0 && s < 256) MCA_PROBE(kProbeRedAll + (int64_t)s * 64 + k);
+      __builtin_amdgcn_wave_barrier();  // lane 0 read every slot before they are rewritten
     }
     return;
   }
@@ -211,7 +267,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     y_lds[lane] = live ? net.y[n] : 0;
   }
   if (tid == 0) last.valid = 0;
-  for (int k = tid; k < K; k += kLoopThreads) cand_lds[0][k] = decode_index(net, a.t0, (uint64_t)k);
   // committed scalars, carried in registers by tile 0, lane 0
   double L_acc = 0.0;
   uint64_t n_acc = 0, n_tie = 0;
@@ -221,41 +276,94 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     n_acc = a.st->accepted;
     n_tie = a.st->tie;
   }
+  bool committed = false;  // this wave committed last step: its stores are in flight
+  // Waves 1-15 stage step t: wave w draws and loads candidates k = w-1,
+  // w+14, ... (Philox on one lane per candidate), writes the candidate
+  // records, the inputs of the mutated weights (activation applied), the
+  // mutated units' cached local fields, and each candidate's weight, code and
+  // logit-layer column to LDS buffer b.
+  auto stage = [&](uint64_t t, int b) {
+    constexpr int kStagers = kWaves - 1;
+    constexpr int kPer = (kLoopMaxK + kStagers - 1) / kStagers;  // candidates per staging wave
+    const int w = wave - 1;
+    if (lane < kPer) {
+      const int k = w + kStagers * lane;
+      if (k < K) cand_lds[b][k] = decode_index(net, t, (uint64_t)k);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    // every load first ...
+    float a_raw[kPer], z_raw[kPer], wv[kPer];
+    int code[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int k = w + kStagers * q;
+      a_raw[q] = 0.f;
+      z_raw[q] = 0.f;
+      wv[q] = 0.f;
+      code[q] = 0;
+      if (k < K) {
+        const int l = cand_lds[b][k].layer, ci = cand_lds[b][k].i, cj = cand_lds[b][k].j;
+        if (live) {
+          const float* src = (l == 0) ? net.XT : net.Z[l - 1];
+          a_raw[q] = src[(int64_t)ci * Ns + n];
+          z_raw[q] = net.Z[l][(int64_t)cj * Ns + n];
+        }
+        const int64_t idx = (int64_t)cj * net.widths[l] + ci;
+        const int jj = (l == L - 2) ? cj : 0;
+        if (lane < CM) wv[q] = net.W[L - 1][(int64_t)(lane < C ? lane : 0) * nh + jj];
+        if (lane == CM) wv[q] = net.W[l][idx];
+        if (lane == CM + 1 && net.ternary) code[q] = (int)net.codes[l][idx];
+      }
+    }
+    // ... then the stores to LDS
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int k = w + kStagers * q;
+      if (k < K) {
+        const int l = cand_lds[b][k].layer;
+        ain_lds[b][k][lane] = live ? input_of(net, l, a_raw[q]) : 0.f;
+        zh_lds[b][k][lane] = z_raw[q];
+        if (lane < CM) pcol_lds[b][k][lane] = wv[q];
+        if (lane == CM) pw_lds[b][k] = wv[q];
+        if (lane == CM + 1) pcode_lds[b][k] = code[q];
+      }
+    }
+  };
+  if (wave > 0) stage(a.t0, 0);
   __syncthreads();
 
+  const int psel = (g == 0) ? 0 : ((g == G - 1) ? 1 : -1);
+#define MCA_TILE_PROBE(p) \
+  if (psel >= 0 && tid == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (p))
   for (uint64_t s = 0; s < a.n_steps; ++s) {
     const uint32_t tag = (uint32_t)(s + 1);
     const int buf = (int)(s & 1);
     mca_cand* cands = cand_lds[buf];
-    // 1. every load of the step at once: the tile operands of this wave's
-    // candidates; per candidate its committed weight, code and logit column
-    float ar[KW], zr[KW];
-#pragma unroll
-    for (int q = 0; q < KW; ++q) {
-      const int k = wave + kWaves * q;
-      ar[q] = 0.f;
-      zr[q] = 0.f;
-      if (k < K && live) {
-        // indices only: a ternary candidate's code is being finished below
-        const int l = cands[k].layer, ci = cands[k].i, cj = cands[k].j;
-        const float* src = (l == 0) ? net.XT : net.Z[l - 1];
-        ar[q] = src[(int64_t)ci * Ns + n];
-        zr[q] = net.Z[l][(int64_t)cj * Ns + n];
+    MCA_TILE_PROBE(0);
+    // 1. patch what last step's commit changed, then each candidate's new value
+    const LastCommit lc = last;
+    if (lc.valid && lc.layer == L - 2) {
+      for (int k = wave; k < K; k += kWaves) {
+        const int l = cands[k].layer;
+        if (l == L - 2 && cands[k].j == lc.j) zh_lds[buf][k][lane] = zrow_lds[lane];
+        if (l == L - 1 && cands[k].i == lc.j) {
+          const float zr = zrow_lds[lane];
+          ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
+        }
       }
     }
     if (tid < K) {
       const int k = tid;
       mca_cand c = cands[k];
-      const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
-      float w = net.W[c.layer][idx];
-      int cur = net.ternary ? (int)net.codes[c.layer][idx] : 0;
       const bool hid = c.layer == L - 2;
       const int jj = hid ? c.j : 0;
+      float w = pw_lds[buf][k];
+      int cur = pcode_lds[buf][k];
       float col[CM];
 #pragma unroll
-      for (int cc = 0; cc < CM; ++cc) col[cc] = net.W[L - 1][(int64_t)(cc < C ? cc : 0) * nh + jj];
-      const LastCommit lc = last;
-      if (lc.valid) {  // committed last step: its store may still be in flight
+      for (int cc = 0; cc < CM; ++cc) col[cc] = pcol_lds[buf][k][cc];
+      if (lc.valid) {
         if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
           w = lc.w_new;
           cur = lc.code;
@@ -278,18 +386,17 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
       for (int cc = 0; cc < CM; ++cc) wcol_lds[k][cc] = (hid && cc < C) ? col[cc] : 0.f;
     }
+    if (committed) wait_own_memory();  // last step's commit stores land before the next staging
+    committed = false;
     if (tid == 0) list_n = 0;
-    wait_own_memory();  // also retires this wave's stores of the previous step
     __syncthreads();
+    MCA_TILE_PROBE(1);
     // 2a. compact the pairs whose input is non-zero into the work list
 #pragma unroll
     for (int q = 0; q < KW; ++q) {
       const int k = wave + kWaves * q;
       if (k < K) {
-        const int l = cands[k].layer;
-        const float ain = input_of(net, l, ar[q]);
-        ain_lds[k][lane] = ain;
-        zh_lds[k][lane] = zr[q];
+        const float ain = ain_lds[buf][k][lane];
         dlp_lds[k][lane] = 0.f;
         const bool act = live && ain != 0.f;
         const uint64_t m = __ballot(act);
@@ -310,36 +417,48 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
       float zn, z[CM], ln;
-      dlp_lds[k][sl] = pair_eval<CM>(net, c.layer, c.j, aux_lds[k].de, wcol_lds[k], ain_lds[k][sl],
-                                     zh_lds[k][sl], &zl_lds[sl], ell_lds[sl], y_lds[sl], zn, z, ln);
+      dlp_lds[k][sl] = pair_eval<CM>(net, c.layer, c.j, aux_lds[k].de, wcol_lds[k],
+                                     ain_lds[buf][k][sl], zh_lds[buf][k][sl], &zl_lds[sl],
+                                     ell_lds[sl], y_lds[sl], zn, z, ln);
     }
     __syncthreads();
     // 2c. per candidate: sum its 64 slots in sample order (4 threads x 16),
     // publish the tile's partial sum
-    uint64_t* part = a.partials + (size_t)g * kpad;
+    uint64_t* part = a.partials + g;  // candidate k's word: part[k * gpad]
     {
-      const int k = tid >> 2, r = tid & 3;
+      // 16 threads per candidate, 4 samples each in order, then a fixed butterfly
+      const int k = tid >> 4, r = tid & 15;
       float v = 0.f;
       if (k < K) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) v += dlp_lds[k][r * 16 + i];
+        for (int i = 0; i < 4; ++i) v += dlp_lds[k][r * 4 + i];
       }
-      v += __shfl_xor(v, 1, 64);
-      v += __shfl_xor(v, 2, 64);
-      if (k < K && r == 0) st_agent(&part[k], pack(aux_lds[k].valid ? v : __builtin_huge_valf(), tag));
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
+      if (k < K && r == 0)
+        st_agent(&part[(size_t)k * a.gpad], pack(aux_lds[k].valid ? v : __builtin_huge_valf(), tag));
     }
     // 3. wave 0 gathers the K loss changes and decides (every tile takes the
     // same decision from the same words); waves 1-3 draw the next candidates
+    MCA_TILE_PROBE(2);
+    if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
+    if (wave > 0 && s + 1 < a.n_steps) stage(a.t0 + s + 1, buf ^ 1);
     if (wave == 0) {
       const uint32_t t16 = tag16(s);
+      const uint64_t* dls = a.dls + (g % kReplicas) * kLoopMaxK;
       uint64_t d = 0;
       uint32_t spins = 0;
       bool ab = false;
+      if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 2);
       while (true) {
-        if (lane < K && (uint32_t)(d & 0xFFFFu) != t16) d = ld_agent(&a.dls[lane]);
+        if (lane < K && (uint32_t)(d & 0xFFFFu) != t16) d = ld_agent(&dls[lane]);
         if (__all(lane >= K || (uint32_t)(d & 0xFFFFu) == t16)) break;
         if ((ab = __any(spin_step(spins, a)))) break;
       }
+      if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 3);
+#ifdef MCA_PHASE_PROBES
+      if (g == 0 && lane == 0 && s < 256 && probes) probes[kProbeRedAll + 256 * 64 + (int64_t)s] = spins;
+#endif
       const double v = unpack_dl(d);
       const uint64_t acc_mask = __ballot(!ab && lane < K && accepts(v, net.ties));
       const int kc = acc_mask ? (int)__ffsll((unsigned long long)acc_mask) - 1 : -1;
@@ -368,34 +487,30 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
           }
         }
       }
-    } else if (s + 1 < a.n_steps) {
-      for (int k = tid - 64; k < K; k += kLoopThreads - 64)
-        cand_lds[buf ^ 1][k] = decode_index(net, a.t0 + s + 1, (uint64_t)k);
     }
     __syncthreads();
+    MCA_TILE_PROBE(3);
     if (aborted) break;
-    // 4. commit on this tile by the wave that loaded the winner's operands;
-    // every workgroup writes the new weight
+    // 4. commit on this tile (wave 1; the winner's operands are staged in
+    // LDS); every workgroup writes the new weight
     const int kc = dec_k;
-    if (kc >= 0 && wave == (kc % kWaves)) {
-      const int qc = kc / kWaves;
-      float a_raw = 0.f, z_raw = 0.f;
-#pragma unroll
-      for (int q = 0; q < KW; ++q)
-        if (q == qc) { a_raw = ar[q]; z_raw = zr[q]; }
+    if (kc >= 0 && wave == 1) {
       const mca_cand c = cands[kc];
       const Aux au = aux_lds[kc];
-      const float ain = input_of(net, c.layer, a_raw);
+      const float ain = ain_lds[buf][kc][lane];
+      const float z_raw = zh_lds[buf][kc][lane];
       float zn, z[CM], ln;
       (void)pair_eval<CM>(net, c.layer, c.j, au.de, wcol_lds[kc], ain, z_raw, &zl_lds[lane],
                           ell_lds[lane], y_lds[lane], zn, z, ln);
-      if (live && ain != 0.f) {
+      const bool ch = live && ain != 0.f;
+      if (ch) {
         if (c.layer != L - 1) net.Z[c.layer][(int64_t)c.j * Ns + n] = zn;
 #pragma unroll
         for (int cc = 0; cc < CM; ++cc)
           if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
         ell_lds[lane] = ln;
       }
+      zrow_lds[lane] = ch ? zn : z_raw;
       if (lane == 0) {
         const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
         net.W[c.layer][idx] = au.w_new;
@@ -407,11 +522,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         last.w_new = au.w_new;
         last.valid = 1;
       }
-      wait_own_memory();  // the tile's new local fields are in place for the next step
+      committed = true;
     }
     if (kc < 0 && tid == 0) last.valid = 0;
     __syncthreads();
+    MCA_TILE_PROBE(4);
   }
+#undef MCA_TILE_PROBE
   // the tile's logits and losses go back to HBM; tile 0 writes the state
   if (wave == 0 && live) {
     for (int c = 0; c < C; ++c) net.Z[L - 1][(int64_t)c * Ns + n] = zl_lds[c * 64 + lane];
@@ -435,7 +552,7 @@ __global__ void k_reset_loop(LoopSync* s, uint64_t* partials, int64_t n_words, u
                              int K) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_words) partials[i] = 0;
-  if (i < K) dls[i] = 0;
+  if (i < (int64_t)kReplicas * kLoopMaxK) dls[i] = 0;
   if (i == 0) s->abort = 0;
 }
 
@@ -449,17 +566,15 @@ const void* pick_loop(int K, int C) {
   const int kw = (K + kWaves - 1) / kWaves;
   if (kw <= 1) return loop_fn<1>(C);
   if (kw <= 2) return loop_fn<2>(C);
-  if (kw <= 4) return loop_fn<4>(C);
-  if (kw <= 8) return loop_fn<8>(C);
-  return loop_fn<16>(C);
+  return loop_fn<4>(C);
 }
 }  // namespace
 
-int step_loop_reducers(int K) { return (K + kWaves - 1) / kWaves; }
+int step_loop_reducers(int K) { return (K + kReducerWaves - 1) / kReducerWaves; }
 
 hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s) {
-  const int64_t words = (int64_t)a.G * a.kpad;
-  const int64_t n = words > a.K ? words : a.K;
+  const int64_t words = (int64_t)a.K * a.gpad;
+  const int64_t n = words > (int64_t)kReplicas * kLoopMaxK ? words : (int64_t)kReplicas * kLoopMaxK;
   hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sync,
                      a.partials, words, a.dls, a.K);
   hipError_t e = hipGetLastError();

@@ -19,12 +19,12 @@ struct LoopArgs {
   NetDev net;
   int K;                // candidates per step (<= kLoopMaxK)
   int T;                // samples per workgroup tile (<= 64)
-  int G;                // tile workgroups (<= 64 * 16)
-  int kpad;             // partial words per tile: K rounded up to 16 (128 bytes)
+  int G;                // tile workgroups (<= kLoopMaxTiles)
+  int gpad;             // words per candidate row of partials: G rounded up to 16
   uint64_t t0;          // first step index
   uint64_t n_steps;     // steps in this launch (< 2^32)
-  uint64_t* partials;   // [G][kpad] tagged per-tile loss-change sums
-  uint64_t* dls;        // [K] tagged loss changes
+  uint64_t* partials;   // [K][gpad] tagged per-tile loss-change sums
+  uint64_t* dls;        // [8][kLoopMaxK] tagged loss changes, 8 replicas
   LoopSync* sync;
   DevState* st;
   int32_t* tr_chosen;   // trace (nullable)
@@ -34,9 +34,9 @@ struct LoopArgs {
   uint32_t spin_limit;  // polls before a wait gives up and aborts the grid
 };
 
-constexpr int kLoopMaxTiles = 64 * 16;
+constexpr int kLoopMaxTiles = 64 * 8;
 
-// Workgroups of the candidate reducers for K candidates (one wave each).
+// Workgroups of the candidate reducers for K candidates (four candidates each).
 int step_loop_reducers(int K);
 hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s);
 hipError_t step_loop_max_blocks(int K, int C, int* out);

@@ -110,9 +110,9 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.loop_T = 64;
   lo.loop_G = (int)((N + lo.loop_T - 1) / lo.loop_T);
   const int64_t g_max = (N + kMinLoopTile - 1) / kMinLoopTile;
-  const int64_t kpad = (std::min<int32_t>(k_max, mca::kLoopMaxK) + 15) / 16 * 16;
-  lo.loop_partials = take((size_t)g_max * kpad * sizeof(uint64_t));
-  lo.loop_dls = take((size_t)mca::kLoopMaxK * sizeof(uint64_t));
+  const int64_t gpad = (g_max + 15) / 16 * 16;
+  lo.loop_partials = take((size_t)std::min<int32_t>(k_max, mca::kLoopMaxK) * gpad * sizeof(uint64_t));
+  lo.loop_dls = take((size_t)8 * mca::kLoopMaxK * sizeof(uint64_t));  // 8 replicas
   lo.loop_sync = take(sizeof(mca::LoopSync));
   lo.total = off;
   return lo;
@@ -530,7 +530,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     a.t0 = before.t + done;
     a.n_steps = chunk;
     a.G = ctx->lo.loop_G;
-    a.kpad = (K + 15) / 16 * 16;
+    a.gpad = (ctx->lo.loop_G + 15) / 16 * 16;
     a.partials = ctx->loop_partials;
     a.dls = ctx->loop_dls;
     a.sync = ctx->loop_sync;
