@@ -60,6 +60,20 @@ __device__ __forceinline__ void stage_net(NetDev& dst, const NetDev& src) {
   __syncthreads();
 }
 
+// Accesses through NetDev's pointers.  A pointer read from the LDS copy of the
+// descriptor has no known address space, so a plain dereference becomes a
+// flat access; a flat access counts on the LDS counter too, so every later LDS
+// wait would also wait for it.  These helpers state that the pointee is in
+// global memory.
+template <class T>
+__device__ __forceinline__ T gload(const T* p) {
+  return *(const __attribute__((address_space(1))) T*)p;
+}
+template <class T>
+__device__ __forceinline__ void gstore(T* p, T v) {
+  *(__attribute__((address_space(1))) T*)p = v;
+}
+
 // A candidate's new value, prepared once per step against the committed state.
 struct Aux {
   float w_old;

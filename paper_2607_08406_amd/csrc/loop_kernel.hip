@@ -134,20 +134,27 @@ struct LastCommit {
 // branches on the candidate's layer (pairs of different candidates share a
 // wave).
 template <int CM>
-__device__ __forceinline__ float pair_eval(const NetDev& net, int layer, int j, float de,
-                                           const float* wcol, float ain, float zh,
+__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
+                                           float de, const float* wcol, float ain, float zh,
                                            const float* zL, float ell, int y, float& zn,
                                            float (&z)[CM], float& ln) {
-  const int L = net.L, C = net.C;
   const bool logit = layer == L - 1;
-  const float zb = logit ? zL[j * 64] : zh;
-  zn = zb + de * ain;
-  const float da = act_fn(zn, net.act, net.gamma) - act_fn(zb, net.act, net.gamma);
+  // every operand is loaded unconditionally (the LDS rows hold CM entries,
+  // zero beyond C) so the loads issue together
+  float zc[CM], wc[CM];
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) {
-    const float zc = (cc < C) ? zL[cc * 64] : 0.f;
-    const float hid = (cc < C) ? fmaf(da, wcol[cc], zc) : 0.f;
-    z[cc] = logit ? ((cc == j) ? zn : zc) : hid;
+    zc[cc] = zL[cc * 64];
+    wc[cc] = wcol[cc];
+  }
+  const float zj = zL[(logit ? j : 0) * 64];
+  const float zb = logit ? zj : zh;
+  zn = zb + de * ain;
+  const float da = act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) {
+    const float hid = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
+    z[cc] = logit ? ((cc == j) ? zn : zc[cc]) : hid;
   }
   ln = ce_loss<CM>(z, C, y);
   const bool changed = logit || da != 0.f;
@@ -192,7 +199,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   const int K = a.K, T = a.T, G = a.G;
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int C = net.C, L = net.L;
+  // the CM < kCMax variants run only for C == CM: a compile-time class count
+  const int C = (CM < kCMax) ? CM : net.C, L = net.L;
+  const int act = net.act;
+  const float gamma = net.gamma;
   if (tid == 0) aborted = 0;
 
   if (g >= G) {
@@ -234,22 +244,29 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
       for (int b = 0; b < kMaxTilesPerLane; ++b)
         if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
-      // lane 0 adds the 64 lane sums in lane order (LDS, this wave only)
+      // the 64 lane sums go through LDS (this wave only)
       sums[lane] = acc;
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      double tot = 0.0;
-      if (lane == 0) {
-#pragma unroll 8
-        for (int r = 0; r < 64; ++r) tot += sums[r];
+      // lanes 0-7 add eight lane sums each in order, then every lane adds
+      // those eight in order
+      double s8 = 0.0;
+      if (lane < 8) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) s8 += sums[lane * 8 + r];
       }
-      tot = __shfl(tot, 0, 64);
+      double p8[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) p8[r] = __shfl(s8, r, 64);
+      double tot = p8[0];
+#pragma unroll
+      for (int r = 1; r < 8; ++r) tot += p8[r];
       const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
       if (lane < kReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
       if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 1);
       if (lane == 0 && s < 256) MCA_PROBE(kProbeRedAll + (int64_t)s * 64 + k);
-      __builtin_amdgcn_wave_barrier();  // lane 0 read every slot before they are rewritten
+      __builtin_amdgcn_wave_barrier();  // lanes 0-7 read every slot before they are rewritten
     }
     return;
   }
@@ -262,9 +279,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // the tile's logits, losses and labels move to LDS for the whole launch
   if (wave == 0) {
     for (int c = 0; c < CM; ++c)
-      zl_lds[c * 64 + lane] = (live && c < C) ? net.Z[L - 1][(int64_t)c * Ns + n] : 0.f;
-    ell_lds[lane] = live ? net.ell[n] : 0.f;
-    y_lds[lane] = live ? net.y[n] : 0;
+      zl_lds[c * 64 + lane] = (live && c < C) ? gload(&net.Z[L - 1][(int64_t)c * Ns + n]) : 0.f;
+    ell_lds[lane] = live ? gload(&net.ell[n]) : 0.f;
+    y_lds[lane] = live ? gload(&net.y[n]) : 0;
   }
   if (tid == 0) last.valid = 0;
   // committed scalars, carried in registers by tile 0, lane 0
@@ -306,14 +323,14 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const int l = cand_lds[b][k].layer, ci = cand_lds[b][k].i, cj = cand_lds[b][k].j;
         if (live) {
           const float* src = (l == 0) ? net.XT : net.Z[l - 1];
-          a_raw[q] = src[(int64_t)ci * Ns + n];
-          z_raw[q] = net.Z[l][(int64_t)cj * Ns + n];
+          a_raw[q] = gload(&src[(int64_t)ci * Ns + n]);
+          z_raw[q] = gload(&net.Z[l][(int64_t)cj * Ns + n]);
         }
         const int64_t idx = (int64_t)cj * net.widths[l] + ci;
         const int jj = (l == L - 2) ? cj : 0;
-        if (lane < CM) wv[q] = net.W[L - 1][(int64_t)(lane < C ? lane : 0) * nh + jj];
-        if (lane == CM) wv[q] = net.W[l][idx];
-        if (lane == CM + 1 && net.ternary) code[q] = (int)net.codes[l][idx];
+        if (lane < CM) wv[q] = gload(&net.W[L - 1][(int64_t)(lane < C ? lane : 0) * nh + jj]);
+        if (lane == CM) wv[q] = gload(&net.W[l][idx]);
+        if (lane == CM + 1 && net.ternary) code[q] = (int)gload(&net.codes[l][idx]);
       }
     }
     // ... then the stores to LDS
@@ -386,8 +403,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
       for (int cc = 0; cc < CM; ++cc) wcol_lds[k][cc] = (hid && cc < C) ? col[cc] : 0.f;
     }
-    if (committed) wait_own_memory();  // last step's commit stores land before the next staging
-    committed = false;
     if (tid == 0) list_n = 0;
     __syncthreads();
     MCA_TILE_PROBE(1);
@@ -417,10 +432,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
       float zn, z[CM], ln;
-      dlp_lds[k][sl] = pair_eval<CM>(net, c.layer, c.j, aux_lds[k].de, wcol_lds[k],
+      dlp_lds[k][sl] = pair_eval<CM>(L, C, act, gamma, c.layer, c.j, aux_lds[k].de, wcol_lds[k],
                                      ain_lds[buf][k][sl], zh_lds[buf][k][sl], &zl_lds[sl],
                                      ell_lds[sl], y_lds[sl], zn, z, ln);
     }
+    // last step's commit stores land before this step's staging reads HBM
+    if (committed) wait_own_memory();
+    committed = false;
     __syncthreads();
     // 2c. per candidate: sum its 64 slots in sample order (4 threads x 16),
     // publish the tile's partial sum
@@ -500,11 +518,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const float ain = ain_lds[buf][kc][lane];
       const float z_raw = zh_lds[buf][kc][lane];
       float zn, z[CM], ln;
-      (void)pair_eval<CM>(net, c.layer, c.j, au.de, wcol_lds[kc], ain, z_raw, &zl_lds[lane],
+      (void)pair_eval<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[kc], ain, z_raw,
+                          &zl_lds[lane],
                           ell_lds[lane], y_lds[lane], zn, z, ln);
       const bool ch = live && ain != 0.f;
       if (ch) {
-        if (c.layer != L - 1) net.Z[c.layer][(int64_t)c.j * Ns + n] = zn;
+        if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
 #pragma unroll
         for (int cc = 0; cc < CM; ++cc)
           if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
@@ -513,8 +532,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       zrow_lds[lane] = ch ? zn : z_raw;
       if (lane == 0) {
         const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
-        net.W[c.layer][idx] = au.w_new;
-        if (net.ternary) net.codes[c.layer][idx] = (int8_t)c.code;
+        gstore(&net.W[c.layer][idx], au.w_new);
+        if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
         last.layer = c.layer;
         last.j = c.j;
         last.i = c.i;
@@ -531,8 +550,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #undef MCA_TILE_PROBE
   // the tile's logits and losses go back to HBM; tile 0 writes the state
   if (wave == 0 && live) {
-    for (int c = 0; c < C; ++c) net.Z[L - 1][(int64_t)c * Ns + n] = zl_lds[c * 64 + lane];
-    net.ell[n] = ell_lds[lane];
+    for (int c = 0; c < C; ++c) gstore(&net.Z[L - 1][(int64_t)c * Ns + n], zl_lds[c * 64 + lane]);
+    gstore(&net.ell[n], ell_lds[lane]);
   }
   if (g == 0 && tid == 0 && !aborted) {
     DevState* st = a.st;
