@@ -16,10 +16,11 @@
 // test (Eq. 6).  It then applies the commit to its own tile with the same
 // expressions the evaluation used.  Tile 0 also keeps the committed loss and
 // the counters.  While wave 0 of a tile workgroup waits for the loss changes,
-// waves 1-15 draw the next step's candidates (the draw needs no state) and
-// stage their operands and weights in a second LDS buffer; what the pending
-// commit changes (one hidden row of the tile, one weight, code or
-// logit-layer column entry) is patched in LDS before use.
+// the other waves work ahead (the draw needs no state): wave 1 draws the
+// candidates of step s+3, the staging waves write the operands and weights of
+// step s+1 to a second LDS buffer and start the loads of step s+2; what the
+// commits made since those loads (one hidden row of the tile, one weight,
+// code or logit-layer column entry each) is patched in LDS before use.
 //
 // Sparse inputs: a sample whose input to the mutated weight is zero does not
 // change (about 81 % of an image column), so a workgroup first compacts the
@@ -119,7 +120,7 @@ __device__ __forceinline__ bool spin_step(uint32_t& spins, const LoopArgs& a) {
   return false;
 }
 
-// The last committed mutation, kept in LDS for one step.
+// A committed mutation, kept in LDS for two steps.
 struct LastCommit {
   int layer, j, i, code;
   float w_new;
@@ -179,7 +180,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float zl_lds[CM * 64];
   __shared__ float ell_lds[64];
   __shared__ int y_lds[64];
-  __shared__ mca_cand cand_lds[2][kLoopMaxK];
+  __shared__ mca_cand cand_lds[4][kLoopMaxK];  // draws of steps s .. s+3, by step mod 4
   __shared__ Aux aux_lds[kLoopMaxK];
   __shared__ float wcol_lds[kLoopMaxK][CM];
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
@@ -187,11 +188,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float pw_lds[2][kLoopMaxK];
   __shared__ int pcode_lds[2][kLoopMaxK];
   __shared__ float pcol_lds[2][kLoopMaxK][CM];
-  __shared__ float dlp_lds[kLoopMaxK][64];
+  __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
   __shared__ uint16_t list_lds[kLoopMaxK * 64];
   __shared__ int list_n;
-  __shared__ LastCommit last;
-  __shared__ float zrow_lds[64];  // the committed hidden row of this tile
+  __shared__ LastCommit last[2];     // commits of the last two steps, by step parity
+  __shared__ float zrow_lds[2][64];  // their committed hidden rows of this tile
   __shared__ double red_lds[kReducerWaves][64];  // reducer lane sums
   __shared__ int dec_k;
   __shared__ int aborted;
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     ell_lds[lane] = live ? gload(&net.ell[n]) : 0.f;
     y_lds[lane] = live ? gload(&net.y[n]) : 0;
   }
-  if (tid == 0) last.valid = 0;
+  if (tid < 2) last[tid].valid = 0;
   // committed scalars, carried in registers by tile 0, lane 0
   double L_acc = 0.0;
   uint64_t n_acc = 0, n_tie = 0;
@@ -294,24 +295,26 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     n_tie = a.st->tie;
   }
   bool committed = false;  // this wave committed last step: its stores are in flight
-  // Waves 1-15 stage step t: wave w draws and loads candidates k = w-1,
-  // w+14, ... (Philox on one lane per candidate), writes the candidate
-  // records, the inputs of the mutated weights (activation applied), the
-  // mutated units' cached local fields, and each candidate's weight, code and
-  // logit-layer column to LDS buffer b.
-  auto stage = [&](uint64_t t, int b) {
-    constexpr int kStagers = kWaves - 1;
-    constexpr int kPer = (kLoopMaxK + kStagers - 1) / kStagers;  // candidates per staging wave
-    const int w = wave - 1;
-    if (lane < kPer) {
-      const int k = w + kStagers * lane;
-      if (k < K) cand_lds[b][k] = decode_index(net, t, (uint64_t)k);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    // every load first ...
-    float a_raw[kPer], z_raw[kPer], wv[kPer];
-    int code[kPer];
+  // The stream is drawn three steps ahead: wave 1, lane k decodes candidate
+  // k of step t into cand_lds[t mod 4] (one Philox block per lane, so the
+  // 64-bit multiplies of a draw cost one wave's issue time).  Waves 2-15
+  // stage the candidates k = w-2, w+12, ... of wave w in two parts.
+  // issue(cb): start the loads of each candidate's input (of the mutated
+  // weight), cached local field, weight, code and logit-layer column into
+  // registers.  land(cb, b): write those registers (activation applied to the
+  // input) to LDS buffer b.  The loads of step s+2 are issued during step s
+  // and land during step s+1, so their latency hides behind a whole step;
+  // what the commits of steps s and s+1 change is patched in LDS at the start
+  // of step s+2.
+  constexpr int kStagers = kWaves - 2;
+  constexpr int kPer = (kLoopMaxK + kStagers - 1) / kStagers;  // candidates per staging wave
+  float a_raw[kPer], z_raw[kPer], wv[kPer];
+  int code[kPer];
+  auto draw = [&](uint64_t t, int cb) {
+    if (lane < K) cand_lds[cb][lane] = decode_index(net, t, (uint64_t)lane);
+  };
+  auto issue = [&](int cb) {
+    const int w = wave - 2;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
@@ -320,7 +323,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       wv[q] = 0.f;
       code[q] = 0;
       if (k < K) {
-        const int l = cand_lds[b][k].layer, ci = cand_lds[b][k].i, cj = cand_lds[b][k].j;
+        const int l = cand_lds[cb][k].layer, ci = cand_lds[cb][k].i, cj = cand_lds[cb][k].j;
         if (live) {
           const float* src = (l == 0) ? net.XT : net.Z[l - 1];
           a_raw[q] = gload(&src[(int64_t)ci * Ns + n]);
@@ -333,12 +336,14 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         if (lane == CM + 1 && net.ternary) code[q] = (int)gload(&net.codes[l][idx]);
       }
     }
-    // ... then the stores to LDS
+  };
+  auto land = [&](int cb, int b) {
+    const int w = wave - 2;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
       if (k < K) {
-        const int l = cand_lds[b][k].layer;
+        const int l = cand_lds[cb][k].layer;
         ain_lds[b][k][lane] = live ? input_of(net, l, a_raw[q]) : 0.f;
         zh_lds[b][k][lane] = z_raw[q];
         if (lane < CM) pcol_lds[b][k][lane] = wv[q];
@@ -347,7 +352,14 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
     }
   };
-  if (wave > 0) stage(a.t0, 0);
+  if (wave == 1)
+    for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(a.t0 + d, (int)d);
+  __syncthreads();
+  if (wave >= 2) {
+    issue(0);
+    land(0, 0);
+    if (a.n_steps > 1) issue(1);
+  }
   __syncthreads();
 
   const int psel = (g == 0) ? 0 : ((g == G - 1) ? 1 : -1);
@@ -356,17 +368,22 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   for (uint64_t s = 0; s < a.n_steps; ++s) {
     const uint32_t tag = (uint32_t)(s + 1);
     const int buf = (int)(s & 1);
-    mca_cand* cands = cand_lds[buf];
+    const int cb = (int)(s & 3);
+    mca_cand* cands = cand_lds[cb];
     MCA_TILE_PROBE(0);
-    // 1. patch what last step's commit changed, then each candidate's new value
-    const LastCommit lc = last;
-    if (lc.valid && lc.layer == L - 2) {
-      for (int k = wave; k < K; k += kWaves) {
-        const int l = cands[k].layer;
-        if (l == L - 2 && cands[k].j == lc.j) zh_lds[buf][k][lane] = zrow_lds[lane];
-        if (l == L - 1 && cands[k].i == lc.j) {
-          const float zr = zrow_lds[lane];
-          ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
+    // 1. patch what the commits of the last two steps changed (the staged
+    // values were loaded before them), oldest first, then each candidate's
+    // new value
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int slot = (int)((s + p) & 1);  // p = 0: step s-2, p = 1: step s-1
+      const LastCommit lc = last[slot];
+      if (lc.valid && lc.layer == L - 2) {
+        const float zr = zrow_lds[slot][lane];
+        for (int k = wave; k < K; k += kWaves) {
+          const int l = cands[k].layer;
+          if (l == L - 2 && cands[k].j == lc.j) zh_lds[buf][k][lane] = zr;
+          if (l == L - 1 && cands[k].i == lc.j) ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
         }
       }
     }
@@ -380,14 +397,18 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       float col[CM];
 #pragma unroll
       for (int cc = 0; cc < CM; ++cc) col[cc] = pcol_lds[buf][k][cc];
-      if (lc.valid) {
-        if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
-          w = lc.w_new;
-          cur = lc.code;
-        }
 #pragma unroll
-        for (int cc = 0; cc < CM; ++cc)
-          if (lc.layer == L - 1 && lc.j == cc && lc.i == jj) col[cc] = lc.w_new;
+      for (int p = 0; p < 2; ++p) {
+        const LastCommit lc = last[(s + p) & 1];
+        if (lc.valid) {
+          if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
+            w = lc.w_new;
+            cur = lc.code;
+          }
+#pragma unroll
+          for (int cc = 0; cc < CM; ++cc)
+            if (lc.layer == L - 1 && lc.j == cc && lc.i == jj) col[cc] = lc.w_new;
+        }
       }
       if (net.ternary) {
         finish_ternary(net, c, cur);
@@ -404,6 +425,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       for (int cc = 0; cc < CM; ++cc) wcol_lds[k][cc] = (hid && cc < C) ? col[cc] : 0.f;
     }
     if (tid == 0) list_n = 0;
+    MCA_TILE_PROBE(5);
     __syncthreads();
     MCA_TILE_PROBE(1);
     // 2a. compact the pairs whose input is non-zero into the work list
@@ -440,27 +462,35 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     if (committed) wait_own_memory();
     committed = false;
     __syncthreads();
-    // 2c. per candidate: sum its 64 slots in sample order (4 threads x 16),
-    // publish the tile's partial sum
+    // 2c. wave 0, lane k: sum candidate k's 64 slots (four runs of 16
+    // consecutive samples, then the runs pairwise) and publish the tile's
+    // partial sum.  Only wave 0 stores here: a store still in flight would
+    // make the staging waves' waits for their own loads wait for it too.
     uint64_t* part = a.partials + g;  // candidate k's word: part[k * gpad]
-    {
-      // 16 threads per candidate, 4 samples each in order, then a fixed butterfly
-      const int k = tid >> 4, r = tid & 15;
-      float v = 0.f;
-      if (k < K) {
+    if (wave == 0 && lane < K) {
+      float r0 = 0.f, r1 = 0.f, r2 = 0.f, r3 = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v += dlp_lds[k][r * 4 + i];
+      for (int i = 0; i < 16; ++i) {
+        r0 += dlp_lds[lane][i];
+        r1 += dlp_lds[lane][16 + i];
+        r2 += dlp_lds[lane][32 + i];
+        r3 += dlp_lds[lane][48 + i];
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-      if (k < K && r == 0)
-        st_agent(&part[(size_t)k * a.gpad], pack(aux_lds[k].valid ? v : __builtin_huge_valf(), tag));
+      const float v = (r0 + r1) + (r2 + r3);
+      st_agent(&part[(size_t)lane * a.gpad], pack(aux_lds[lane].valid ? v : __builtin_huge_valf(), tag));
     }
     // 3. wave 0 gathers the K loss changes and decides (every tile takes the
-    // same decision from the same words); waves 1-3 draw the next candidates
+    // same decision from the same words); wave 1 draws step s+3, waves 2-15 land
+    // step s+1 and issue step s+2
     MCA_TILE_PROBE(2);
     if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
-    if (wave > 0 && s + 1 < a.n_steps) stage(a.t0 + s + 1, buf ^ 1);
+    if (wave == 1 && s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
+    if (wave >= 2) {
+      if (s + 1 < a.n_steps) land((int)((s + 1) & 3), buf ^ 1);
+      if (s + 2 < a.n_steps) issue((int)((s + 2) & 3));
+    }
+    if (psel >= 0 && (tid == 64 || tid == 64 * 15) && s < 256)
+      MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (tid == 64 ? 6 : 7));
     if (wave == 0) {
       const uint32_t t16 = tag16(s);
       const uint64_t* dls = a.dls + (g % kReplicas) * kLoopMaxK;
@@ -529,21 +559,22 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
           if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
         ell_lds[lane] = ln;
       }
-      zrow_lds[lane] = ch ? zn : z_raw;
+      zrow_lds[buf][lane] = ch ? zn : z_raw;
       if (lane == 0) {
         const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
         gstore(&net.W[c.layer][idx], au.w_new);
         if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
-        last.layer = c.layer;
-        last.j = c.j;
-        last.i = c.i;
-        last.code = c.code;
-        last.w_new = au.w_new;
-        last.valid = 1;
+        LastCommit& lc = last[buf];
+        lc.layer = c.layer;
+        lc.j = c.j;
+        lc.i = c.i;
+        lc.code = c.code;
+        lc.w_new = au.w_new;
+        lc.valid = 1;
       }
       committed = true;
     }
-    if (kc < 0 && tid == 0) last.valid = 0;
+    if (kc < 0 && tid == 0) last[buf].valid = 0;
     __syncthreads();
     MCA_TILE_PROBE(4);
   }
