@@ -127,6 +127,34 @@ struct LastCommit {
   int valid;
 };
 
+// A candidate's new value against the committed weights, with its new code.
+struct Prep {
+  float w_old, w_new;
+  float de;    // fl32(w_new - w_old): the increment the caches apply
+  int valid;   // 0: |w_new| >= bound, rejected without evaluation
+  int code;    // new ternary code
+  int pad[3];
+};
+
+// c.code holds the selecting bit of a ternary draw (decode_index); w and cur
+// are the committed weight and code.
+__device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, float w, int cur) {
+  Prep x;
+  x.w_old = w;
+  if (net.ternary) {
+    mca_cand t = c;
+    finish_ternary(net, t, cur);
+    x.code = t.code;
+    x.w_new = (float)t.code * net.scales[c.layer];
+  } else {
+    x.code = 0;
+    x.w_new = w + c.d;
+  }
+  x.de = x.w_new - x.w_old;
+  x.valid = !(net.bound > 0.f && fabsf(x.w_new) >= net.bound);
+  return x;
+}
+
 // One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
 // the activation feeding it); zh: the cached local field of the mutated unit
 // when it is a hidden unit; zL: the sample's logits in LDS (stride 64).  The
@@ -181,13 +209,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float ell_lds[64];
   __shared__ int y_lds[64];
   __shared__ mca_cand cand_lds[4][kLoopMaxK];  // draws of steps s .. s+3, by step mod 4
-  __shared__ Aux aux_lds[kLoopMaxK];
-  __shared__ float wcol_lds[kLoopMaxK][CM];
+  __shared__ Prep prep_lds[2][kLoopMaxK];       // staged per step parity
+  __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column of a hidden unit
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
   __shared__ float zh_lds[2][kLoopMaxK][64];
-  __shared__ float pw_lds[2][kLoopMaxK];
-  __shared__ int pcode_lds[2][kLoopMaxK];
-  __shared__ float pcol_lds[2][kLoopMaxK][CM];
   __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
   __shared__ uint16_t list_lds[kLoopMaxK * 64];
   __shared__ int list_n;
@@ -297,68 +322,122 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   bool committed = false;  // this wave committed last step: its stores are in flight
   // The stream is drawn three steps ahead: wave 1, lane k decodes candidate
   // k of step t into cand_lds[t mod 4] (one Philox block per lane, so the
-  // 64-bit multiplies of a draw cost one wave's issue time).  Waves 2-15
-  // stage the candidates k = w-2, w+12, ... of wave w in two parts.
-  // issue(cb): start the loads of each candidate's input (of the mutated
-  // weight), cached local field, weight, code and logit-layer column into
-  // registers.  land(cb, b): write those registers (activation applied to the
-  // input) to LDS buffer b.  The loads of step s+2 are issued during step s
-  // and land during step s+1, so their latency hides behind a whole step;
-  // what the commits of steps s and s+1 change is patched in LDS at the start
-  // of step s+2.
+  // 64-bit multiplies of a draw cost one wave's issue time).  The operands of
+  // a step are staged in two parts: the loads of step s+2 are issued during
+  // step s into registers and land in LDS buffer (s+2) mod 2 during step s+1,
+  // so their latency hides behind a whole step.  Landing applies the commit
+  // made after the loads were issued; the commit of the step just before is
+  // applied at the start of the step itself.
+  //  - per candidate (wave 1, lane k): the weight, its code and, for a hidden
+  //    unit, its logit-layer column; landing computes the new value (Prep);
+  //  - per sample (waves 2-15, candidates k = w-2, w+12, ... of wave w, the
+  //    candidate's fields in scalar registers): the input of the mutated weight
+  //    and the cached local field of a mutated hidden unit.
+  // The persistent loop runs L <= 2, so the layer pointers are taken from the
+  // kernel argument with constant indices (scalar registers).
+  const int Lk = a.net.L;
+  const bool two = Lk == 2;
+  const float* const in_hid = a.net.XT;                       // input of layer 0 (L = 2)
+  const float* const in_log = two ? a.net.Z[0] : a.net.XT;    // input of the logit layer
+  const float* const z_hid = a.net.Z[0];                      // hidden local fields (L = 2)
+  const float* const w_log = two ? a.net.W[1] : a.net.W[0];
+  const int8_t* const c_log = two ? a.net.codes[1] : a.net.codes[0];
+  const int nin_log = two ? a.net.widths[1] : a.net.widths[0];
+  const int nin_hid = a.net.widths[0];
+  const bool ternary = a.net.ternary != 0;
   constexpr int kStagers = kWaves - 2;
   constexpr int kPer = (kLoopMaxK + kStagers - 1) / kStagers;  // candidates per staging wave
-  float a_raw[kPer], z_raw[kPer], wv[kPer];
-  int code[kPer];
+  float a_raw[kPer], z_raw[kPer];  // per-sample loads in flight
+  float w_reg = 0.f, col_reg[CM];  // per-candidate loads in flight (wave 1)
+  int code_reg = 0;
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) col_reg[cc] = 0.f;
   auto draw = [&](uint64_t t, int cb) {
     if (lane < K) cand_lds[cb][lane] = decode_index(net, t, (uint64_t)lane);
   };
-  auto issue = [&](int cb) {
-    const int w = wave - 2;
+  auto issue_cand = [&](int cb) {
+    if (lane < K) {
+      const mca_cand c = cand_lds[cb][lane];
+      const bool hid = c.layer == Lk - 2;
+      const int64_t idx = (int64_t)c.j * (hid ? nin_hid : nin_log) + c.i;
+      w_reg = gload(hid ? &a.net.W[0][idx] : &w_log[idx]);
+      code_reg = ternary ? (int)gload(hid ? &a.net.codes[0][idx] : &c_log[idx]) : 0;
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc)
+        col_reg[cc] = (hid && cc < C) ? gload(&w_log[(int64_t)cc * nh + c.j]) : 0.f;
+    }
+  };
+  // slot: the commit applied while landing
+  auto land_cand = [&](int cb, int b, int slot) {
+    if (lane < K) {
+      const mca_cand c = cand_lds[cb][lane];
+      const LastCommit lc = last[slot];
+      float w = w_reg;
+      int cur = code_reg;
+      if (lc.valid && lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
+        w = lc.w_new;
+        cur = lc.code;
+      }
+      const bool colhit = lc.valid && lc.layer == Lk - 1 && c.layer == Lk - 2 && lc.i == c.j;
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc) wcol_lds[b][lane][cc] = (colhit && cc == lc.j) ? lc.w_new : col_reg[cc];
+      prep_lds[b][lane] = make_prep(net, c, w, cur);
+    }
+  };
+  auto issue_samples = [&](int cb) {
+    const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
       a_raw[q] = 0.f;
       z_raw[q] = 0.f;
-      wv[q] = 0.f;
-      code[q] = 0;
       if (k < K) {
-        const int l = cand_lds[cb][k].layer, ci = cand_lds[cb][k].i, cj = cand_lds[cb][k].j;
+        const int l = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].layer);
+        const int ci = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].i);
+        const int cj = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].j);
+        const bool hid = l == Lk - 2;
         if (live) {
-          const float* src = (l == 0) ? net.XT : net.Z[l - 1];
-          a_raw[q] = gload(&src[(int64_t)ci * Ns + n]);
-          z_raw[q] = gload(&net.Z[l][(int64_t)cj * Ns + n]);
+          a_raw[q] = gload(&(hid ? in_hid : in_log)[(int64_t)ci * Ns + n]);
+          if (hid) z_raw[q] = gload(&z_hid[(int64_t)cj * Ns + n]);
         }
-        const int64_t idx = (int64_t)cj * net.widths[l] + ci;
-        const int jj = (l == L - 2) ? cj : 0;
-        if (lane < CM) wv[q] = gload(&net.W[L - 1][(int64_t)(lane < C ? lane : 0) * nh + jj]);
-        if (lane == CM) wv[q] = gload(&net.W[l][idx]);
-        if (lane == CM + 1 && net.ternary) code[q] = (int)gload(&net.codes[l][idx]);
       }
     }
   };
-  auto land = [&](int cb, int b) {
-    const int w = wave - 2;
+  auto land_samples = [&](int cb, int b, int slot) {
+    const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
+    const int lvalid = __builtin_amdgcn_readfirstlane(last[slot].valid);
+    const int llayer = __builtin_amdgcn_readfirstlane(last[slot].layer);
+    const int lj = __builtin_amdgcn_readfirstlane(last[slot].j);
+    const bool row = lvalid && llayer == Lk - 2;  // a hidden row of this tile changed
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
       if (k < K) {
-        const int l = cand_lds[cb][k].layer;
-        ain_lds[b][k][lane] = live ? input_of(net, l, a_raw[q]) : 0.f;
-        zh_lds[b][k][lane] = z_raw[q];
-        if (lane < CM) pcol_lds[b][k][lane] = wv[q];
-        if (lane == CM) pw_lds[b][k] = wv[q];
-        if (lane == CM + 1) pcode_lds[b][k] = code[q];
+        const int l = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].layer);
+        const int ci = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].i);
+        const int cj = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].j);
+        const bool hid = l == Lk - 2;
+        float ar = a_raw[q], zz = z_raw[q];
+        if (row && hid && cj == lj) zz = zrow_lds[slot][lane];
+        if (row && !hid && ci == lj) ar = zrow_lds[slot][lane];
+        // the logit layer's input is an activation when a hidden layer feeds it
+        const float in = (!hid && two) ? act_fn(ar, act, gamma) : ar;
+        ain_lds[b][k][lane] = live ? in : 0.f;
+        zh_lds[b][k][lane] = zz;
       }
     }
   };
   if (wave == 1)
     for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(a.t0 + d, (int)d);
   __syncthreads();
-  if (wave >= 2) {
-    issue(0);
-    land(0, 0);
-    if (a.n_steps > 1) issue(1);
+  if (wave == 1) {
+    issue_cand(0);
+    land_cand(0, 0, 1);
+    if (a.n_steps > 1) issue_cand(1);
+  } else if (wave >= 2) {
+    issue_samples(0);
+    land_samples(0, 0, 1);
+    if (a.n_steps > 1) issue_samples(1);
   }
   __syncthreads();
 
@@ -371,58 +450,35 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     const int cb = (int)(s & 3);
     mca_cand* cands = cand_lds[cb];
     MCA_TILE_PROBE(0);
-    // 1. patch what the commits of the last two steps changed (the staged
-    // values were loaded before them), oldest first, then each candidate's
-    // new value
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int slot = (int)((s + p) & 1);  // p = 0: step s-2, p = 1: step s-1
+    // 1. the staged values include every commit up to step s-2; apply the
+    // commit of step s-1 where it touches a candidate (its weight, its
+    // unit's row of this tile, or its logit-layer column), which is rare
+    {
+      const int slot = buf ^ 1;
       const LastCommit lc = last[slot];
-      if (lc.valid && lc.layer == L - 2) {
-        const float zr = zrow_lds[slot][lane];
-        for (int k = wave; k < K; k += kWaves) {
-          const int l = cands[k].layer;
-          if (l == L - 2 && cands[k].j == lc.j) zh_lds[buf][k][lane] = zr;
-          if (l == L - 1 && cands[k].i == lc.j) ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
+      if (lc.valid && wave == 0) {
+        bool row = false;
+        mca_cand c;
+        if (lane < K) {
+          c = cands[lane];
+          const bool hid = c.layer == L - 2;
+          if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i)
+            prep_lds[buf][lane] = make_prep(net, c, lc.w_new, lc.code);
+          if (lc.layer == L - 1 && hid && lc.i == c.j) wcol_lds[buf][lane][lc.j] = lc.w_new;
+          row = lc.layer == L - 2 && ((hid && c.j == lc.j) || (c.layer == L - 1 && c.i == lc.j));
         }
-      }
-    }
-    if (tid < K) {
-      const int k = tid;
-      mca_cand c = cands[k];
-      const bool hid = c.layer == L - 2;
-      const int jj = hid ? c.j : 0;
-      float w = pw_lds[buf][k];
-      int cur = pcode_lds[buf][k];
-      float col[CM];
-#pragma unroll
-      for (int cc = 0; cc < CM; ++cc) col[cc] = pcol_lds[buf][k][cc];
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const LastCommit lc = last[(s + p) & 1];
-        if (lc.valid) {
-          if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i) {
-            w = lc.w_new;
-            cur = lc.code;
+        uint64_t rows = __ballot(row);
+        if (rows) {
+          const float zr = zrow_lds[slot][lane];
+          while (rows) {
+            const int k = (int)__ffsll((unsigned long long)rows) - 1;
+            rows &= rows - 1;
+            const int l = __shfl(c.layer, k, 64);
+            if (l == L - 2) zh_lds[buf][k][lane] = zr;
+            else ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
           }
-#pragma unroll
-          for (int cc = 0; cc < CM; ++cc)
-            if (lc.layer == L - 1 && lc.j == cc && lc.i == jj) col[cc] = lc.w_new;
         }
       }
-      if (net.ternary) {
-        finish_ternary(net, c, cur);
-        cands[k].d = c.d;
-        cands[k].code = c.code;
-      }
-      Aux au;
-      au.w_old = w;
-      au.w_new = net.ternary ? (float)c.code * net.scales[c.layer] : w + c.d;
-      au.de = au.w_new - au.w_old;
-      au.valid = !(net.bound > 0.f && fabsf(au.w_new) >= net.bound);
-      aux_lds[k] = au;
-#pragma unroll
-      for (int cc = 0; cc < CM; ++cc) wcol_lds[k][cc] = (hid && cc < C) ? col[cc] : 0.f;
     }
     if (tid == 0) list_n = 0;
     MCA_TILE_PROBE(5);
@@ -454,7 +510,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
       float zn, z[CM], ln;
-      dlp_lds[k][sl] = pair_eval<CM>(L, C, act, gamma, c.layer, c.j, aux_lds[k].de, wcol_lds[k],
+      dlp_lds[k][sl] = pair_eval<CM>(L, C, act, gamma, c.layer, c.j, prep_lds[buf][k].de,
+                                     wcol_lds[buf][k],
                                      ain_lds[buf][k][sl], zh_lds[buf][k][sl], &zl_lds[sl],
                                      ell_lds[sl], y_lds[sl], zn, z, ln);
     }
@@ -477,17 +534,20 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         r3 += dlp_lds[lane][48 + i];
       }
       const float v = (r0 + r1) + (r2 + r3);
-      st_agent(&part[(size_t)lane * a.gpad], pack(aux_lds[lane].valid ? v : __builtin_huge_valf(), tag));
+      st_agent(&part[(size_t)lane * a.gpad], pack(prep_lds[buf][lane].valid ? v : __builtin_huge_valf(), tag));
     }
     // 3. wave 0 gathers the K loss changes and decides (every tile takes the
     // same decision from the same words); wave 1 draws step s+3, waves 2-15 land
     // step s+1 and issue step s+2
     MCA_TILE_PROBE(2);
     if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
-    if (wave == 1 && s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
-    if (wave >= 2) {
-      if (s + 1 < a.n_steps) land((int)((s + 1) & 3), buf ^ 1);
-      if (s + 2 < a.n_steps) issue((int)((s + 2) & 3));
+    if (wave == 1) {
+      if (s + 1 < a.n_steps) land_cand((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      if (s + 2 < a.n_steps) issue_cand((int)((s + 2) & 3));
+      if (s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
+    } else if (wave >= 2) {
+      if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
     }
     if (psel >= 0 && (tid == 64 || tid == 64 * 15) && s < 256)
       MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (tid == 64 ? 6 : 7));
@@ -544,11 +604,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     const int kc = dec_k;
     if (kc >= 0 && wave == 1) {
       const mca_cand c = cands[kc];
-      const Aux au = aux_lds[kc];
+      const Prep au = prep_lds[buf][kc];
       const float ain = ain_lds[buf][kc][lane];
       const float z_raw = zh_lds[buf][kc][lane];
       float zn, z[CM], ln;
-      (void)pair_eval<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[kc], ain, z_raw,
+      (void)pair_eval<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
                           &zl_lds[lane],
                           ell_lds[lane], y_lds[lane], zn, z, ln);
       const bool ch = live && ain != 0.f;
@@ -563,12 +623,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       if (lane == 0) {
         const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
         gstore(&net.W[c.layer][idx], au.w_new);
-        if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
+        if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)au.code);
         LastCommit& lc = last[buf];
         lc.layer = c.layer;
         lc.j = c.j;
         lc.i = c.i;
-        lc.code = c.code;
+        lc.code = au.code;
         lc.w_new = au.w_new;
         lc.valid = 1;
       }
