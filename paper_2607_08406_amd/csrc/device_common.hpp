@@ -47,16 +47,21 @@ struct NetDev {
   const float* XT;
   float* ell;                         // per-sample loss cache
   const int32_t* y;
+  float* WT;                          // three-layer nets: W_1 transposed ([n_1][n_2]), else null
 };
 
 // Kernels index the pointer and size arrays of NetDev with runtime values (the
 // candidate's layer).  Indexing the by-value kernel argument that way makes
 // the compiler fetch each pointer from the kernel-argument segment with a
-// dependent vector load; one thread therefore copies the descriptor to LDS
-// with static offsets (scalar loads) and every lane indexes the LDS copy.
-// Every thread of the block must call this (it synchronises the block).
+// dependent vector load; the block therefore copies the descriptor to LDS
+// once (one word per thread) and every lane indexes the LDS copy.  Every
+// thread of the block must call this (it synchronises the block).
 __device__ __forceinline__ void stage_net(NetDev& dst, const NetDev& src) {
-  if (threadIdx.x == 0) dst = src;
+  static_assert(sizeof(NetDev) % 4 == 0, "descriptor copied in words");
+  constexpr int kWords = (int)(sizeof(NetDev) / 4);
+  const uint32_t* s = reinterpret_cast<const uint32_t*>(&src);
+  uint32_t* d = reinterpret_cast<uint32_t*>(&dst);
+  for (int w = (int)threadIdx.x; w < kWords; w += (int)blockDim.x) d[w] = s[w];
   __syncthreads();
 }
 

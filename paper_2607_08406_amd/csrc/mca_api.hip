@@ -15,6 +15,7 @@
 #include "device_common.hpp"
 #include "loop_kernel.hpp"
 #include "mlp_kernels.hpp"
+#include "slab_kernels.hpp"
 
 using mca::Aux;
 using mca::DevState;
@@ -36,6 +37,8 @@ struct Layout {
   int ntiles = 0;
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
+  size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
+  int nslab = 0;
   int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
   size_t total = 0;
@@ -71,9 +74,13 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   if (!std::isfinite(net->bound)) return "bound must be finite (<= 0 disables it)";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31)) return "n_samples out of range";
   if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
-  if (L >= 3) {
+  if (L >= 4) {
     *code = MCA_EUNSUPPORTED;
-    return "MLPs with three or more weight matrices are not implemented by this build";
+    return "MLPs with four or more weight matrices are not implemented by this build";
+  }
+  if (L == 3 && net->widths[2] > mca::kSlabMaxUnits) {
+    *code = MCA_EUNSUPPORTED;
+    return "three-layer MLPs need a second hidden layer of at most 1024 units";
   }
   *code = MCA_OK;
   return "";
@@ -105,6 +112,12 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.state = take(sizeof(DevState));
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
+  if (L == 3) {
+    lo.wt = take((size_t)net->widths[1] * net->widths[2] * sizeof(float));
+    const int T = mca::slab_tile(net->widths[L]);
+    lo.nslab = (int)((N + T - 1) / T);
+    lo.pslab = take((size_t)k_max * lo.nslab * sizeof(float));
+  }
   // persistent loop: tiles of T samples (16..64), one workgroup each; the
   // partial sums are sized for the smallest tile
   lo.loop_T = 64;
@@ -133,6 +146,7 @@ struct mca_ctx {
   mca_cand* cands = nullptr;
   Aux* aux = nullptr;
   float* partial = nullptr;
+  float* pslab = nullptr;
   double* dl = nullptr;
   double* bsum = nullptr;
   DevState* st = nullptr;
@@ -254,6 +268,8 @@ int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const*
     MCA_HIP(ctx, hipMemcpyAsync(ctx->net.W[l], params[l], n * sizeof(float), hipMemcpyHostToDevice, ctx->stream));
     if (tern) MCA_HIP(ctx, hipMemcpyAsync(ctx->net.codes[l], codes[l], n, hipMemcpyHostToDevice, ctx->stream));
   }
+  if (ctx->net.WT != nullptr)  // W_1 [n_2][n_1] -> W_T [n_1][n_2]
+    MCA_HIP(ctx, mca::launch_transpose(ctx->net.W[1], d.widths[2], d.widths[1], ctx->net.WT, ctx->stream));
   MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
   return MCA_OK;
 }
@@ -291,6 +307,26 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
     }
   }
   return MCA_OK;
+}
+
+// Scores the K staged candidates: the column kernel for the last two layers,
+// the tile kernel for the first layer of a three-layer net.
+hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
+  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream);
+  if (e == hipSuccess && net.WT != nullptr)
+    e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->pslab, ctx->lo.nslab, -2, ctx->st,
+                         ctx->dl, ctx->stream);
+  return e;
+}
+
+// Commits candidate k (k < 0: the device decision); each kernel applies only
+// the candidates of the layers it scores.
+hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
+  hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
+  if (e == hipSuccess && net.WT != nullptr)
+    e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->pslab, ctx->lo.nslab, k, ctx->st,
+                         ctx->dl, ctx->stream);
+  return e;
 }
 
 }  // namespace
@@ -379,6 +415,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.XT = (const float*)(ws + lo.xt);
   nd.ell = (float*)(ws + lo.ell);
   nd.y = (const int32_t*)(ws + lo.y);
+  nd.WT = (L == 3) ? (float*)(ws + lo.wt) : nullptr;
+  ctx->pslab = (L == 3) ? (float*)(ws + lo.pslab) : nullptr;
   ctx->cands = (mca_cand*)(ws + lo.cands);
   ctx->aux = (Aux*)(ws + lo.aux);
   ctx->partial = (float*)(ws + lo.partial);
@@ -445,8 +483,8 @@ int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double*
   if (rc != MCA_OK) return rc;
   MCA_HIP(ctx, hipMemcpyAsync(ctx->cands, cands_host, (size_t)K * sizeof(mca_cand), hipMemcpyHostToDevice, ctx->stream));
   MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream); }));
-  MCA_HIP(ctx, timed(ctx, 1, [&] { return mca::launch_eval(ctx->net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream); }));
-  MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(ctx->net, ctx->partial, ctx->lo.ntiles, ctx->aux, K, ctx->dl, ctx->st, false, nullptr, nullptr, 0, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, ctx->net, K); }));
+  MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(ctx->net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab, ctx->lo.nslab, ctx->aux, K, ctx->dl, ctx->st, false, nullptr, nullptr, 0, ctx->stream); }));
   std::vector<double> dl(K);
   DevState s{};
   MCA_HIP(ctx, hipMemcpyAsync(dl.data(), ctx->dl, (size_t)K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
@@ -465,7 +503,7 @@ int mca_commit(mca_ctx* ctx, int32_t k) {
   MCA_LIVE(ctx);
   if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
   if (k < 0 || k >= ctx->pending_K) return fail(ctx, MCA_EINVAL, "k outside the pending batch");
-  MCA_HIP(ctx, timed(ctx, 3, [&] { return mca::launch_commit(ctx->net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, ctx->net, k); }));
   ctx->pending = false;
   ctx->pending_K = 0;
   return MCA_OK;
@@ -567,9 +605,9 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     }
     for (uint64_t s = 0; s < chunk; ++s) {
       MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(net, 0, true, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
-      MCA_HIP(ctx, timed(ctx, 1, [&] { return mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream); }));
-      MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->aux, K, ctx->dl, ctx->st, true, trc, trd, kTraceCap, ctx->stream); }));
-      MCA_HIP(ctx, timed(ctx, 3, [&] { return mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, -1, ctx->lo.ntiles, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K); }));
+      MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab, ctx->lo.nslab, ctx->aux, K, ctx->dl, ctx->st, true, trc, trd, kTraceCap, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1); }));
     }
     if (trace != nullptr) {
       MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));

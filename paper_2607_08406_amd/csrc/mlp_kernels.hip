@@ -52,43 +52,42 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
                                                float de, int64_t n) {
   const int L = net.L, C = net.C;
   const int64_t Ns = net.Ns;
-  const float ain = (l == 0) ? net.XT[(int64_t)i * Ns + n]
-                             : act_fn(net.Z[l - 1][(int64_t)i * Ns + n], net.act, net.gamma);
+  const float ain = (l == 0) ? gload(&net.XT[(int64_t)i * Ns + n])
+                             : act_fn(gload(&net.Z[l - 1][(int64_t)i * Ns + n]), net.act, net.gamma);
   if (ain == 0.f) return 0.f;  // z' == z for this sample
   float* zrow = net.Z[l] + (int64_t)j * Ns;
-  const float zl = zrow[n];
+  const float zl = gload(&zrow[n]);
   const float zn = zl + de * ain;
-  const float* ZL = net.Z[L - 1];
+  float* ZL = net.Z[L - 1];
   float z[kCMax];
   if (l == L - 1) {
     // the mutated weight feeds logit j directly
 #pragma unroll
     for (int c = 0; c < kCMax; ++c)
-      z[c] = (c < C) ? ((c == j) ? zn : ZL[(int64_t)c * Ns + n]) : 0.f;
+      z[c] = (c < C) ? ((c == j) ? zn : gload(&ZL[(int64_t)c * Ns + n])) : 0.f;
   } else {
     // last hidden layer: rank-1 update of the logits through W_L[:, j]
     const float da = act_fn(zn, net.act, net.gamma) - act_fn(zl, net.act, net.gamma);
     if (da == 0.f) {
-      if (STORE) zrow[n] = zn;
+      if (STORE) gstore(&zrow[n], zn);
       return 0.f;
     }
     const float* WL = net.W[L - 1];
     const int nh = net.widths[L - 1];
 #pragma unroll
     for (int c = 0; c < kCMax; ++c)
-      z[c] = (c < C) ? fmaf(da, WL[(int64_t)c * nh + j], ZL[(int64_t)c * Ns + n]) : 0.f;
+      z[c] = (c < C) ? fmaf(da, gload(&WL[(int64_t)c * nh + j]), gload(&ZL[(int64_t)c * Ns + n])) : 0.f;
   }
-  const float ln = ce_loss(z, C, net.y[n]);
-  const float dl = ln - net.ell[n];
+  const float ln = ce_loss(z, C, gload(&net.y[n]));
+  const float dl = ln - gload(&net.ell[n]);
   if (STORE) {
-    zrow[n] = zn;
+    gstore(&zrow[n], zn);
     if (l != L - 1) {
-      float* ZLw = net.Z[L - 1];
 #pragma unroll
       for (int c = 0; c < kCMax; ++c)
-        if (c < C) ZLw[(int64_t)c * Ns + n] = z[c];
+        if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
     }
-    net.ell[n] = ln;
+    gstore(&net.ell[n], ln);
   }
   return dl;
 }
@@ -106,6 +105,8 @@ __global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca
   const Aux a = aux[k];
   const int64_t n = (int64_t)tile * kTile + threadIdx.x;
   float dl = 0.f;
+  // candidates below layer L-2 are scored by their own kernel
+  if (c.layer < net.L - 2) return;  // uniform over the block
   if (a.valid && n < net.N) dl = column_sample<false>(net, c.layer, c.j, c.i, a.de, n);
   const float s = block_sum_256(dl, red);
   if (threadIdx.x == 0) partial[(int64_t)k * ntiles + tile] = s;
@@ -115,7 +116,11 @@ __global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca
 // selection (Eq. 6): one block, thread k owns candidate k
 // ---------------------------------------------------------------------------
 
+// A candidate in layer slab_layer (>= 0 for three-layer nets) takes its tile
+// sums from pslab[k * nslab + b] instead.
 __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float* partial, int ntiles,
+                                                  const mca_cand* cands, const float* pslab,
+                                                  int nslab, int slab_layer,
                                                   const Aux* aux, int K, double* dL,
                                                   DevState* st, int do_select,
                                                   int32_t* tr_chosen, double* tr_dl,
@@ -128,8 +133,10 @@ __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float*
   double v = 0.0;
   if (k < K) {
     double s = 0.0;
-    const float* p = partial + (int64_t)k * ntiles;
-    for (int t = 0; t < ntiles; ++t) s += (double)p[t];
+    const bool slab = cands[k].layer == slab_layer;
+    const float* p = slab ? pslab + (int64_t)k * nslab : partial + (int64_t)k * ntiles;
+    const int nt = slab ? nslab : ntiles;
+    for (int t = 0; t < nt; ++t) s += (double)p[t];
     v = aux[k].valid ? s / (double)net.N : __builtin_huge_val();
     dL[k] = v;
     if (do_select && accepts(v, net.ties)) atomicMin(&first, k);
@@ -169,12 +176,16 @@ __global__ __launch_bounds__(kTile) void k_commit_column(NetDev net_arg, const m
   const int k = (k_host >= 0) ? k_host : st->chosen;
   if (k < 0) return;
   const mca_cand c = cands[k];
+  if (c.layer < net.L - 2) return;  // committed by the kernel that scored it
   const Aux a = aux[k];
   const int64_t n = (int64_t)blockIdx.x * kTile + threadIdx.x;
   if (n < net.N) (void)column_sample<true>(net, c.layer, c.j, c.i, a.de, n);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     net.W[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = a.w_new;
     if (net.ternary) net.codes[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = (int8_t)c.code;
+    // the transposed copy of W_{L-2}: W_T[i][j] = W[j][i]
+    if (net.WT != nullptr && c.layer == net.L - 2)
+      net.WT[(int64_t)c.i * net.widths[c.layer + 1] + c.j] = a.w_new;
     st->L += dL[k];
     st->accepted += 1;
   }
@@ -255,9 +266,9 @@ __global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net_arg, double* bs
   if (n < net.N) {
     float z[kCMax];
 #pragma unroll
-    for (int c = 0; c < kCMax; ++c) z[c] = (c < net.C) ? net.Z[net.L - 1][(int64_t)c * net.Ns + n] : 0.f;
-    const float l = ce_loss(z, net.C, net.y[n]);
-    net.ell[n] = l;
+    for (int c = 0; c < kCMax; ++c) z[c] = (c < net.C) ? gload(&net.Z[net.L - 1][(int64_t)c * net.Ns + n]) : 0.f;
+    const float l = ce_loss(z, net.C, gload(&net.y[n]));
+    gstore(&net.ell[n], l);
     v = (double)l;
   }
   red[threadIdx.x] = v;
@@ -300,11 +311,14 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   return hipGetLastError();
 }
 
-hipError_t launch_select(const NetDev& net, const float* partial, int ntiles, const Aux* aux,
+hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
+                         const mca_cand* cands, const float* pslab, int nslab, const Aux* aux,
                          int K, double* dL, DevState* st, bool do_select, int32_t* tr_chosen,
                          double* tr_dl, int64_t tr_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, partial, ntiles, aux, K, dL, st,
-                     do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
+  const int slab_layer = (net.WT != nullptr) ? net.L - 3 : -1;
+  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, partial, ntiles, cands, pslab,
+                     nslab, slab_layer, aux, K, dL, st, do_select ? 1 : 0, tr_chosen, tr_dl,
+                     tr_cap);
   return hipGetLastError();
 }
 

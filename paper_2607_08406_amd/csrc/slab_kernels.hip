@@ -1,0 +1,250 @@
+// Evaluation and commit of mutations of a first-layer weight in a
+// three-layer MLP ("MCA Training of Shallow Wide Networks", the two-hidden-
+// layer case): changing W_0[j, i] moves z_1[n, j] by de * x[n, i] for every
+// sample whose input x[n, i] is nonzero; its activation change da[n] moves
+// every unit m of the second hidden layer by da[n] * W_1[m, j] (the O(n_2)
+// multiplications per sample the paper describes), and the logits then change
+// by W_2 (phi(z_2') - phi(z_2)) for that sample.
+//
+// A block owns T consecutive samples.  It stages their second-hidden-layer
+// local fields ([n_2][T], unit-major as in HBM) and the logit-layer weights
+// transposed ([n_2][C]) in LDS, lists every affected (candidate, sample) pair,
+// and scores each pair with 32 lanes: lane g adds the units m = g, g+32, ...
+// in order, then the 32 lane sums meet in a fixed butterfly.  The column
+// W_1[:, j] comes from a transposed copy of W_1 (row j contiguous).  The
+// commit runs the same expressions in the same order for the chosen
+// candidate, so the caches hold exactly the values that were scored.
+#include "device_common.hpp"
+#include "slab_kernels.hpp"
+
+namespace mca {
+
+namespace {
+
+constexpr int kSlabThreads = 1024;
+constexpr int kGroupK = 64;                         // candidates listed at a time
+constexpr int kLanesPerPair = 32;
+constexpr int kPairsPerPass = kSlabThreads / kLanesPerPair;
+
+template <int CM>
+struct SlabTile;
+template <>
+struct SlabTile<10> { static constexpr int T = 24; };
+template <>
+struct SlabTile<kCMax> { static constexpr int T = 16; };
+
+// Loss change of one (candidate, sample) pair; the 32 lanes of a half-wave
+// share the pair.  zt: the block's [n2][T] tile; w2: [n2][CM]; w1: row j of
+// W_1 transposed.  With STORE each lane writes its units' new local fields
+// into the tile.  All 64 lanes of the wave must call this (it shuffles).
+template <int CM, int T, bool STORE>
+__device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, const float* w1,
+                                                 int n2, int t, float da, int act, float gamma,
+                                                 bool active, float (&acc)[CM]) {
+  const int g = threadIdx.x & (kLanesPerPair - 1);
+#pragma unroll
+  for (int c = 0; c < CM; ++c) acc[c] = 0.f;
+  if (active) {
+    for (int m = g; m < n2; m += kLanesPerPair) {
+      const float zo = zt[m * T + t];
+      const float zn = zo + da * gload(&w1[m]);
+      const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
+      if (STORE) zt[m * T + t] = zn;
+#pragma unroll
+      for (int c = 0; c < CM; ++c) acc[c] = fmaf(d, w2[m * CM + c], acc[c]);
+    }
+  }
+#pragma unroll
+  for (int o = kLanesPerPair / 2; o > 0; o >>= 1)
+#pragma unroll
+    for (int c = 0; c < CM; ++c) acc[c] += __shfl_xor(acc[c], o, 64);
+}
+
+}  // namespace
+
+// k_mode: -2 evaluate every listed candidate of layer L-3; -1 commit the
+// device decision st->chosen; >= 0 commit that candidate.  A commit is a no-op
+// here unless the candidate is in layer L-3.
+template <int CM>
+__global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca_cand* cands,
+                                                       const Aux* aux, int K, float* partial,
+                                                       int nblk, int k_mode, DevState* st,
+                                                       const double* dL) {
+  constexpr int T = SlabTile<CM>::T;
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
+  __shared__ float zt[kSlabMaxUnits * T];
+  __shared__ float w2[kSlabMaxUnits * CM];
+  __shared__ uint16_t pcode[kGroupK * T];
+  __shared__ float pda[kGroupK * T];
+  __shared__ float dlp[kGroupK * T];
+  __shared__ int gk[kGroupK], gj[kGroupK], gi[kGroupK];
+  __shared__ float gde[kGroupK];
+  __shared__ int ngroup, npairs;
+  __shared__ uint32_t touched;  // commit: samples of the tile whose fields changed
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = net.L, C = (CM < kCMax) ? CM : net.C;
+  const int l = L - 3;  // the layer whose weights this kernel mutates
+  const int act = net.act;
+  const float gamma = net.gamma;
+  const int n2 = net.widths[L - 1];
+  const int64_t Ns = net.Ns, N = net.N;
+  const int64_t n0 = (int64_t)blockIdx.x * T;
+  const bool commit = k_mode != -2;
+  int kc = -1;
+  if (commit) {
+    kc = (k_mode >= 0) ? k_mode : st->chosen;
+    if (kc < 0 || cands[kc].layer != l) return;  // uniform over the block
+  }
+  float* const Z1 = net.Z[l];       // fields of the mutated unit's layer
+  float* const Z2 = net.Z[l + 1];   // the next hidden layer (the tile)
+  float* const ZL = net.Z[L - 1];   // logits
+  const float* in = (l == 0) ? net.XT : net.Z[l - 1];
+
+  // the tile and the logit-layer weights
+  for (int e = tid; e < n2 * T; e += kSlabThreads) {
+    const int m = e / T, t = e - m * T;
+    zt[e] = (n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
+  }
+  for (int e = tid; e < CM * n2; e += kSlabThreads) {
+    const int c = e / n2, m = e - c * n2;
+    w2[m * CM + c] = (c < C) ? gload(&net.W[L - 1][(int64_t)c * n2 + m]) : 0.f;
+  }
+  if (tid == 0) touched = 0u;
+
+  for (int g0 = 0; g0 < (commit ? 1 : K); g0 += kGroupK) {
+    // 1. the group's candidates in layer l (wave 0 lists them in order)
+    if (wave == 0) {
+      const int k = commit ? kc : g0 + lane;
+      const bool in_l = commit ? lane == 0
+                               : (k < K && cands[k].layer == l && aux[k].valid);
+      const uint64_t m = __ballot(in_l);
+      if (in_l) {
+        const int s = (int)__popcll(m & ((1ull << lane) - 1ull));
+        gk[s] = k;
+        gj[s] = cands[k].j;
+        gi[s] = cands[k].i;
+        gde[s] = aux[k].de;
+      }
+      if (lane == 0) {
+        ngroup = (int)__popcll(m);
+        npairs = 0;
+      }
+    }
+    __syncthreads();
+    const int ng = ngroup;
+    if (ng == 0) continue;
+    // 2. the affected pairs: a nonzero input and a changed activation
+    for (int e = tid; e < ng * T; e += kSlabThreads) {
+      const int s = e / T, t = e - s * T;
+      const int64_t n = n0 + t;
+      dlp[s * T + t] = 0.f;
+      float da = 0.f;
+      if (n < N) {
+        const float xr = gload(&in[(int64_t)gi[s] * Ns + n]);
+        const float x = (l == 0) ? xr : act_fn(xr, act, gamma);
+        if (x != 0.f) {
+          const float zl = gload(&Z1[(int64_t)gj[s] * Ns + n]);
+          const float zn = zl + gde[s] * x;
+          da = act_fn(zn, act, gamma) - act_fn(zl, act, gamma);
+          if (commit) gstore(&Z1[(int64_t)gj[s] * Ns + n], zn);
+        }
+      }
+      if (da != 0.f) {
+        const int p = atomicAdd(&npairs, 1);
+        pcode[p] = (uint16_t)(s * T + t);
+        pda[p] = da;
+      }
+    }
+    __syncthreads();
+    // 3. score the pairs, kPairsPerPass at a time
+    const int np = npairs;
+    for (int p0 = 0; p0 < np; p0 += kPairsPerPass) {
+      const int p = p0 + (tid >> 5);
+      const bool active = p < np;
+      const int code = active ? pcode[p] : 0;
+      const int s = code / T, t = code - s * T;
+      float acc[CM];
+      const float* w1 = net.WT + (int64_t)gj[s] * n2;
+      const float da = active ? pda[p] : 0.f;
+      if (commit)  // the commit also writes the new fields into the tile
+        pair_logit_delta<CM, T, true>(zt, w2, w1, n2, t, da, act, gamma, active, acc);
+      else
+        pair_logit_delta<CM, T, false>(zt, w2, w1, n2, t, da, act, gamma, active, acc);
+      if (active && (tid & (kLanesPerPair - 1)) == 0) {
+        const int64_t n = n0 + t;
+        float z[CM];
+#pragma unroll
+        for (int c = 0; c < CM; ++c) z[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) + acc[c] : 0.f;
+        const float ln = ce_loss<CM>(z, C, gload(&net.y[n]));
+        dlp[s * T + t] = ln - gload(&net.ell[n]);
+        if (commit) {
+#pragma unroll
+          for (int c = 0; c < CM; ++c)
+            if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+          gstore(&net.ell[n], ln);
+          atomicOr(&touched, 1u << t);
+        }
+      }
+    }
+    __syncthreads();
+    // 4. each candidate's partial sum over the tile, in sample order
+    if (!commit && tid < ng) {
+      float v = 0.f;
+      for (int t = 0; t < T; ++t) v += dlp[tid * T + t];
+      partial[(int64_t)gk[tid] * nblk + blockIdx.x] = v;
+    }
+    __syncthreads();
+  }
+  if (!commit) return;
+  // the changed samples' new second-layer fields go back to HBM
+  const uint32_t tm = touched;
+  for (int e = tid; e < n2 * T; e += kSlabThreads) {
+    const int m = e / T, t = e - m * T;
+    if ((tm >> t) & 1u) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[e]);
+  }
+  if (blockIdx.x == 0 && tid == 0) {
+    const mca_cand c = cands[kc];
+    const Aux a = aux[kc];
+    const int64_t idx = (int64_t)c.j * net.widths[l] + c.i;
+    gstore(&net.W[l][idx], a.w_new);
+    if (net.ternary) gstore(&net.codes[l][idx], (int8_t)c.code);
+    st->L += dL[kc];
+    st->accepted += 1;
+  }
+}
+
+// dst[c][r] = src[r][c]
+__global__ void k_transpose(const float* src, int rows, int cols, float* dst) {
+  __shared__ float tile[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
+  for (int r = ty; r < 32; r += 8)
+    if (r0 + r < rows && c0 + tx < cols) tile[r][tx] = src[(int64_t)(r0 + r) * cols + c0 + tx];
+  __syncthreads();
+  for (int c = ty; c < 32; c += 8)
+    if (c0 + c < cols && r0 + tx < rows) dst[(int64_t)(c0 + c) * rows + r0 + tx] = tile[tx][c];
+}
+
+int slab_tile(int C) { return C <= 10 ? SlabTile<10>::T : SlabTile<kCMax>::T; }
+
+hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
+                       float* partial, int nblk, int k_mode, DevState* st, const double* dL,
+                       hipStream_t s) {
+  if (net.C <= 10)
+    hipLaunchKernelGGL(k_slab<10>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
+                       partial, nblk, k_mode, st, dL);
+  else
+    hipLaunchKernelGGL(k_slab<kCMax>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
+                       partial, nblk, k_mode, st, dL);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose(const float* src, int rows, int cols, float* dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_transpose, dim3((cols + 31) / 32, (rows + 31) / 32), dim3(256), 0, s, src,
+                     rows, cols, dst);
+  return hipGetLastError();
+}
+
+}  // namespace mca

@@ -74,6 +74,21 @@ def test_plan_rejects_bad_descriptions(binding, mutate, code):
     assert code in str(e.value)
 
 
+def test_plan_layer_limits(binding):
+    """Three-layer MLPs up to a 1024-unit second hidden layer are planned;
+    deeper nets and wider second layers are reported as unsupported."""
+    d3 = binding.mlp_desc((784, 1024, 1024, 10), "gauss", delta=0.0)
+    b3 = binding.mca_plan(d3, 8192, 64)
+    # X^T, W_0..W_2, W_1 transposed, Z_0..Z_2 dominate
+    core = 4 * (784 * 8192 + 784 * 1024 + 2 * 1024 * 1024 + 10240 + (1024 + 1024 + 10) * 8192)
+    assert core < b3 < core + 16 * 2 ** 20
+    for widths in [(784, 1024, 2048, 10), (64, 32, 32, 32, 10)]:
+        d = binding.mlp_desc(widths, "tanh", delta=0.1)
+        with pytest.raises(binding.MCAError) as e:
+            binding.mca_plan(d, 1024, 8)
+        assert "MCA_EUNSUPPORTED" in str(e.value)
+
+
 def test_plan_rejects_bad_sizes(binding):
     d = binding.mlp_desc((64, 32, 10), "tanh", delta=0.1)
     for N, K in [(0, 1), (1024, 0), (1024, 1025)]:
