@@ -56,12 +56,24 @@ struct NetDev {
 // dependent vector load; the block therefore copies the descriptor to LDS
 // once (one word per thread) and every lane indexes the LDS copy.  Every
 // thread of the block must call this (it synchronises the block).
+// Blocks have at least 64 threads; every load is issued before the stores.
 __device__ __forceinline__ void stage_net(NetDev& dst, const NetDev& src) {
   static_assert(sizeof(NetDev) % 4 == 0, "descriptor copied in words");
   constexpr int kWords = (int)(sizeof(NetDev) / 4);
+  constexpr int kPer = (kWords + 63) / 64;
   const uint32_t* s = reinterpret_cast<const uint32_t*>(&src);
   uint32_t* d = reinterpret_cast<uint32_t*>(&dst);
-  for (int w = (int)threadIdx.x; w < kWords; w += (int)blockDim.x) d[w] = s[w];
+  uint32_t v[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int w = (int)threadIdx.x + u * (int)blockDim.x;
+    v[u] = (w < kWords) ? s[w] : 0u;
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int w = (int)threadIdx.x + u * (int)blockDim.x;
+    if (w < kWords) d[w] = v[u];
+  }
   __syncthreads();
 }
 

@@ -38,6 +38,7 @@ struct Layout {
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
+  size_t cols = 0, nnz = 0;  // three-layer nets: nonzero entries of candidates' W_1 columns
   int nslab = 0;
   int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
@@ -117,6 +118,8 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     const int T = mca::slab_tile(net->widths[L]);
     lo.nslab = (int)((N + T - 1) / T);
     lo.pslab = take((size_t)k_max * lo.nslab * sizeof(float));
+    lo.cols = take((size_t)k_max * net->widths[2] * sizeof(uint64_t));
+    lo.nnz = take((size_t)k_max * sizeof(int32_t));
   }
   // persistent loop: tiles of T samples (16..64), one workgroup each; the
   // partial sums are sized for the smallest tile
@@ -147,6 +150,8 @@ struct mca_ctx {
   Aux* aux = nullptr;
   float* partial = nullptr;
   float* pslab = nullptr;
+  uint64_t* cols = nullptr;
+  int* nnz = nullptr;
   double* dl = nullptr;
   double* bsum = nullptr;
   DevState* st = nullptr;
@@ -314,8 +319,8 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
 hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
   hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.WT != nullptr)
-    e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->pslab, ctx->lo.nslab, -2, ctx->st,
-                         ctx->dl, ctx->stream);
+    e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
+                         ctx->lo.nslab, -2, ctx->st, ctx->dl, ctx->stream);
   return e;
 }
 
@@ -324,8 +329,8 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
 hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
   hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.WT != nullptr)
-    e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->pslab, ctx->lo.nslab, k, ctx->st,
-                         ctx->dl, ctx->stream);
+    e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
+                         ctx->lo.nslab, k, ctx->st, ctx->dl, ctx->stream);
   return e;
 }
 
@@ -417,6 +422,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.y = (const int32_t*)(ws + lo.y);
   nd.WT = (L == 3) ? (float*)(ws + lo.wt) : nullptr;
   ctx->pslab = (L == 3) ? (float*)(ws + lo.pslab) : nullptr;
+  ctx->cols = (L == 3) ? (uint64_t*)(ws + lo.cols) : nullptr;
+  ctx->nnz = (L == 3) ? (int*)(ws + lo.nnz) : nullptr;
   ctx->cands = (mca_cand*)(ws + lo.cands);
   ctx->aux = (Aux*)(ws + lo.aux);
   ctx->partial = (float*)(ws + lo.partial);

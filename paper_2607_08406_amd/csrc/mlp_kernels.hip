@@ -117,7 +117,9 @@ __global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca
 // ---------------------------------------------------------------------------
 
 // A candidate in layer slab_layer (>= 0 for three-layer nets) takes its tile
-// sums from pslab[k * nslab + b] instead.
+// sums from pslab[k * nslab + b] instead.  Sixteen threads add a candidate's
+// tile sums: thread r takes tiles r, r+16, ... in order, then a fixed
+// butterfly joins the sixteen (fp64).
 __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float* partial, int ntiles,
                                                   const mca_cand* cands, const float* pslab,
                                                   int nslab, int slab_layer,
@@ -127,17 +129,35 @@ __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float*
                                                   int64_t tr_cap) {
   __shared__ int first;
   __shared__ int ntie;
-  const int k = threadIdx.x;
-  if (k == 0) { first = K; ntie = 0; }
+  __shared__ double vals[kMaxK];
+  const int tid = threadIdx.x;
+  if (tid == 0) { first = K; ntie = 0; }
+  for (int k0 = 0; k0 < K; k0 += kMaxK / 16) {
+    const int k = k0 + (tid >> 4), r = tid & 15;
+    double s = 0.0;
+    if (k < K) {
+      const bool slab = cands[k].layer == slab_layer;
+      const float* p = slab ? pslab + (int64_t)k * nslab : partial + (int64_t)k * ntiles;
+      const int nt = slab ? nslab : ntiles;
+      // eight loads in flight, added in order
+      for (int t0 = r; t0 < nt; t0 += 16 * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = (t0 + 16 * u < nt) ? p[t0 + 16 * u] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (t0 + 16 * u < nt) s += (double)v[u];
+      }
+    }
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (k < K && r == 0) vals[k] = aux[k].valid ? s / (double)net.N : __builtin_huge_val();
+  }
   __syncthreads();
+  const int k = tid;
   double v = 0.0;
   if (k < K) {
-    double s = 0.0;
-    const bool slab = cands[k].layer == slab_layer;
-    const float* p = slab ? pslab + (int64_t)k * nslab : partial + (int64_t)k * ntiles;
-    const int nt = slab ? nslab : ntiles;
-    for (int t = 0; t < nt; ++t) s += (double)p[t];
-    v = aux[k].valid ? s / (double)net.N : __builtin_huge_val();
+    v = vals[k];
     dL[k] = v;
     if (do_select && accepts(v, net.ties)) atomicMin(&first, k);
   }

@@ -6,14 +6,16 @@
 // multiplications per sample the paper describes), and the logits then change
 // by W_2 (phi(z_2') - phi(z_2)) for that sample.
 //
-// A block owns T consecutive samples.  It stages their second-hidden-layer
-// local fields ([n_2][T], unit-major as in HBM) and the logit-layer weights
+// Per step, k_columns lists the nonzero entries (m, W_1[m, j]) of each such
+// candidate's column in increasing m (a unit with W_1[m, j] = 0 does not move;
+// about half of a ternary column).  A block of k_slab owns T consecutive
+// samples.  It stages their second-hidden-layer local fields ([n_2][T],
+// unit-major as in HBM, rows padded to T+1 floats) and the logit-layer weights
 // transposed ([n_2][C]) in LDS, lists every affected (candidate, sample) pair,
-// and scores each pair with 32 lanes: lane g adds the units m = g, g+32, ...
-// in order, then the 32 lane sums meet in a fixed butterfly.  The column
-// W_1[:, j] comes from a transposed copy of W_1 (row j contiguous).  The
-// commit runs the same expressions in the same order for the chosen
-// candidate, so the caches hold exactly the values that were scored.
+// and scores each pair with 32 lanes: lane g adds the list entries g, g+32,
+// ... in order, then the 32 lane sums meet in a fixed butterfly.  The commit
+// runs the same expressions in the same order for the chosen candidate, so the
+// caches hold exactly the values that were scored.
 #include "device_common.hpp"
 #include "slab_kernels.hpp"
 
@@ -22,36 +24,54 @@ namespace mca {
 namespace {
 
 constexpr int kSlabThreads = 1024;
-constexpr int kGroupK = 64;                         // candidates listed at a time
+constexpr int kGroupK = 64;  // candidate slots listed at a time
 constexpr int kLanesPerPair = 32;
 constexpr int kPairsPerPass = kSlabThreads / kLanesPerPair;
+constexpr int kChunk = 8;    // list entries a lane loads at once
+constexpr int kStageU = 8;   // tile elements a thread loads at once
 
 template <int CM>
 struct SlabTile;
 template <>
-struct SlabTile<10> { static constexpr int T = 24; };
+struct SlabTile<10> { static constexpr int T = 16; };
 template <>
-struct SlabTile<kCMax> { static constexpr int T = 16; };
+struct SlabTile<kCMax> { static constexpr int T = 12; };
 
 // Loss change of one (candidate, sample) pair; the 32 lanes of a half-wave
-// share the pair.  zt: the block's [n2][T] tile; w2: [n2][CM]; w1: row j of
-// W_1 transposed.  With STORE each lane writes its units' new local fields
-// into the tile.  All 64 lanes of the wave must call this (it shuffles).
-template <int CM, int T, bool STORE>
-__device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, const float* w1,
-                                                 int n2, int t, float da, int act, float gamma,
+// share the pair.  zt: the block's tile (row stride TS); w2: [n2][CM]; col:
+// the candidate's nnz column entries (m in the low word, the bits of
+// W_1[m, j] in the high word).  With STORE each lane writes its units' new
+// local fields into the tile.  All 64 lanes of the wave must call this (it
+// shuffles).
+template <int CM, int TS, bool STORE>
+__device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, const uint64_t* col,
+                                                 int nnz, int t, float da, int act, float gamma,
                                                  bool active, float (&acc)[CM]) {
   const int g = threadIdx.x & (kLanesPerPair - 1);
 #pragma unroll
   for (int c = 0; c < CM; ++c) acc[c] = 0.f;
   if (active) {
-    for (int m = g; m < n2; m += kLanesPerPair) {
-      const float zo = zt[m * T + t];
-      const float zn = zo + da * gload(&w1[m]);
-      const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
-      if (STORE) zt[m * T + t] = zn;
+#pragma unroll 1
+    for (int e0 = g; e0 < nnz; e0 += kLanesPerPair * kChunk) {
+      uint64_t ent[kChunk];
 #pragma unroll
-      for (int c = 0; c < CM; ++c) acc[c] = fmaf(d, w2[m * CM + c], acc[c]);
+      for (int u = 0; u < kChunk; ++u) {
+        const int e = e0 + kLanesPerPair * u;
+        ent[u] = (e < nnz) ? gload(&col[e]) : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < kChunk; ++u) {
+        const int e = e0 + kLanesPerPair * u;
+        if (e < nnz) {
+          const int m = (int)(uint32_t)ent[u];
+          const float zo = zt[m * TS + t];
+          const float zn = zo + da * __uint_as_float((uint32_t)(ent[u] >> 32));
+          const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
+          if (STORE) zt[m * TS + t] = zn;
+#pragma unroll
+          for (int c = 0; c < CM; ++c) acc[c] = fmaf(d, w2[m * CM + c], acc[c]);
+        }
+      }
     }
   }
 #pragma unroll
@@ -62,18 +82,61 @@ __device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, con
 
 }  // namespace
 
+// Block k lists the nonzero entries of column j of W_1 for candidate k when it
+// is in layer L-3 (and valid), in increasing unit order: cols[k * n2 + e] =
+// m | bits(W_1[m, j]) << 32, nnz[k] = their count; otherwise nnz[k] = 0.
+__global__ __launch_bounds__(kSlabThreads) void k_columns(NetDev net_arg, const mca_cand* cands,
+                                                          const Aux* aux, int k_mode,
+                                                          const DevState* st, uint64_t* cols,
+                                                          int* nnz) {
+  __shared__ int wave_n[kSlabThreads / 64];
+  const int k = (k_mode >= 0) ? k_mode : (k_mode == -1 ? st->chosen : (int)blockIdx.x);
+  if (k < 0) return;
+  const int L = net_arg.L;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const mca_cand c = cands[k];
+  const bool take = c.layer == L - 3 && (k_mode != -2 || aux[k].valid);
+  if (!take) {
+    if (tid == 0) nnz[k] = 0;
+    return;
+  }
+  const int n2 = net_arg.widths[L - 1];
+  const float* row = net_arg.WT + (int64_t)c.j * n2;
+  int base = 0;
+  for (int m0 = 0; m0 < n2; m0 += kSlabThreads) {
+    const int m = m0 + tid;
+    const float w = (m < n2) ? gload(&row[m]) : 0.f;
+    const bool nz = w != 0.f;
+    const uint64_t b = __ballot(nz);
+    if (lane == 0) wave_n[wave] = (int)__popcll(b);
+    __syncthreads();
+    int off = base;
+    for (int v = 0; v < wave; ++v) off += wave_n[v];
+    int tot = 0;
+    for (int v = 0; v < kSlabThreads / 64; ++v) tot += wave_n[v];
+    if (nz) {
+      const int e = off + (int)__popcll(b & ((1ull << lane) - 1ull));
+      gstore(&cols[(int64_t)k * n2 + e], (uint64_t)m | ((uint64_t)__float_as_uint(w) << 32));
+    }
+    base += tot;
+    __syncthreads();
+  }
+  if (tid == 0) nnz[k] = base;
+}
+
 // k_mode: -2 evaluate every listed candidate of layer L-3; -1 commit the
 // device decision st->chosen; >= 0 commit that candidate.  A commit is a no-op
 // here unless the candidate is in layer L-3.
 template <int CM>
 __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca_cand* cands,
-                                                       const Aux* aux, int K, float* partial,
-                                                       int nblk, int k_mode, DevState* st,
+                                                       const Aux* aux, int K, const uint64_t* cols,
+                                                       const int* nnz, float* partial, int nblk,
+                                                       int k_mode, DevState* st,
                                                        const double* dL) {
-  constexpr int T = SlabTile<CM>::T;
+  constexpr int T = SlabTile<CM>::T, TS = T + 1;
   __shared__ NetDev net;
   stage_net(net, net_arg);
-  __shared__ float zt[kSlabMaxUnits * T];
+  __shared__ float zt[kSlabMaxUnits * TS];
   __shared__ float w2[kSlabMaxUnits * CM];
   __shared__ uint16_t pcode[kGroupK * T];
   __shared__ float pda[kGroupK * T];
@@ -101,17 +164,8 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   float* const Z2 = net.Z[l + 1];   // the next hidden layer (the tile)
   float* const ZL = net.Z[L - 1];   // logits
   const float* in = (l == 0) ? net.XT : net.Z[l - 1];
-
-  // the tile and the logit-layer weights
-  for (int e = tid; e < n2 * T; e += kSlabThreads) {
-    const int m = e / T, t = e - m * T;
-    zt[e] = (n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
-  }
-  for (int e = tid; e < CM * n2; e += kSlabThreads) {
-    const int c = e / n2, m = e - c * n2;
-    w2[m * CM + c] = (c < C) ? gload(&net.W[L - 1][(int64_t)c * n2 + m]) : 0.f;
-  }
   if (tid == 0) touched = 0u;
+  bool staged = false;  // the tile and the logit-layer weights are in LDS
 
   for (int g0 = 0; g0 < (commit ? 1 : K); g0 += kGroupK) {
     // 1. the group's candidates in layer l (wave 0 lists them in order)
@@ -158,20 +212,58 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       }
     }
     __syncthreads();
-    // 3. score the pairs, kPairsPerPass at a time
     const int np = npairs;
+    if (np > 0 && !staged) {  // uniform: staged once, when a pair needs it
+      // kStageU loads in flight per thread before their LDS stores
+      for (int e0 = tid; e0 < n2 * T; e0 += kStageU * kSlabThreads) {
+        float v[kStageU];
+#pragma unroll
+        for (int u = 0; u < kStageU; ++u) {
+          const int e = e0 + u * kSlabThreads;
+          const int m = e / T, t = e - m * T;
+          v[u] = (e < n2 * T && n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kStageU; ++u) {
+          const int e = e0 + u * kSlabThreads;
+          const int m = e / T, t = e - m * T;
+          if (e < n2 * T) zt[m * TS + t] = v[u];
+        }
+      }
+      const float* WL = net.W[L - 1];
+      for (int e0 = tid; e0 < CM * n2; e0 += kStageU * kSlabThreads) {
+        float v[kStageU];
+#pragma unroll
+        for (int u = 0; u < kStageU; ++u) {
+          const int e = e0 + u * kSlabThreads;
+          const int c = e / n2, m = e - c * n2;
+          v[u] = (e < CM * n2 && c < C) ? gload(&WL[(int64_t)c * n2 + m]) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kStageU; ++u) {
+          const int e = e0 + u * kSlabThreads;
+          const int c = e / n2, m = e - c * n2;
+          if (e < CM * n2) w2[m * CM + c] = v[u];
+        }
+      }
+      staged = true;
+      __syncthreads();
+    }
+    // 3. score the pairs, kPairsPerPass at a time
     for (int p0 = 0; p0 < np; p0 += kPairsPerPass) {
       const int p = p0 + (tid >> 5);
       const bool active = p < np;
       const int code = active ? pcode[p] : 0;
       const int s = code / T, t = code - s * T;
-      float acc[CM];
-      const float* w1 = net.WT + (int64_t)gj[s] * n2;
+      const int k = gk[s];
+      const uint64_t* col = cols + (int64_t)k * n2;
+      const int cnt = active ? gload(&nnz[k]) : 0;
       const float da = active ? pda[p] : 0.f;
+      float acc[CM];
       if (commit)  // the commit also writes the new fields into the tile
-        pair_logit_delta<CM, T, true>(zt, w2, w1, n2, t, da, act, gamma, active, acc);
+        pair_logit_delta<CM, TS, true>(zt, w2, col, cnt, t, da, act, gamma, active, acc);
       else
-        pair_logit_delta<CM, T, false>(zt, w2, w1, n2, t, da, act, gamma, active, acc);
+        pair_logit_delta<CM, TS, false>(zt, w2, col, cnt, t, da, act, gamma, active, acc);
       if (active && (tid & (kLanesPerPair - 1)) == 0) {
         const int64_t n = n0 + t;
         float z[CM];
@@ -202,7 +294,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   const uint32_t tm = touched;
   for (int e = tid; e < n2 * T; e += kSlabThreads) {
     const int m = e / T, t = e - m * T;
-    if ((tm >> t) & 1u) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[e]);
+    if ((tm >> t) & 1u) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[m * TS + t]);
   }
   if (blockIdx.x == 0 && tid == 0) {
     const mca_cand c = cands[kc];
@@ -230,14 +322,20 @@ __global__ void k_transpose(const float* src, int rows, int cols, float* dst) {
 int slab_tile(int C) { return C <= 10 ? SlabTile<10>::T : SlabTile<kCMax>::T; }
 
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
-                       float* partial, int nblk, int k_mode, DevState* st, const double* dL,
-                       hipStream_t s) {
+                       uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
+                       const double* dL, hipStream_t s) {
+  // the column lists: every candidate for an evaluation, the one committed
+  // candidate otherwise
+  hipLaunchKernelGGL(k_columns, dim3(k_mode == -2 ? K : 1), dim3(kSlabThreads), 0, s, net, cands,
+                     aux, k_mode, st, cols, nnz);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (net.C <= 10)
     hipLaunchKernelGGL(k_slab<10>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
-                       partial, nblk, k_mode, st, dL);
+                       cols, nnz, partial, nblk, k_mode, st, dL);
   else
     hipLaunchKernelGGL(k_slab<kCMax>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
-                       partial, nblk, k_mode, st, dL);
+                       cols, nnz, partial, nblk, k_mode, st, dL);
   return hipGetLastError();
 }
 

@@ -15,10 +15,11 @@ int slab_tile(int C);
 
 // k_mode -2: write partial[k * nblk + block] for every candidate k in layer
 // L-3 (others untouched); -1: commit st->chosen if it is in layer L-3;
-// >= 0: commit that candidate if it is in layer L-3.
+// >= 0: commit that candidate if it is in layer L-3.  cols (k_max * n_2
+// entries) and nnz (k_max) are scratch for the candidates' column lists.
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
-                       float* partial, int nblk, int k_mode, DevState* st, const double* dL,
-                       hipStream_t s);
+                       uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
+                       const double* dL, hipStream_t s);
 
 // dst[c][r] = src[r][c] for a rows x cols matrix.
 hipError_t launch_transpose(const float* src, int rows, int cols, float* dst, hipStream_t s);
