@@ -152,9 +152,10 @@ size_t mca_struct_size(int32_t which);
 
 /* Device workspace bytes for a net, n_samples and at most k_max candidates per
  * step.  Pure: touches no device.  Returns MCA_EINVAL on a bad description and
- * MCA_EUNSUPPORTED for a valid net this build does not run: Transformers, MLPs
- * with four or more weight matrices, and three-layer MLPs whose second hidden
- * layer has more than 1024 units. */
+ * MCA_EUNSUPPORTED for a valid net this build does not run: Transformers,
+ * MLPs of three or more layers whose last hidden layer has more than 1024
+ * units, and MLPs of four or more layers whose hidden layers are not all 256
+ * units wide. */
 int mca_plan(const mca_net_desc* net, int64_t n_samples, int32_t k_max,
              size_t* workspace_bytes);
 

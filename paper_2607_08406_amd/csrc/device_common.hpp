@@ -47,7 +47,7 @@ struct NetDev {
   const float* XT;
   float* ell;                         // per-sample loss cache
   const int32_t* y;
-  float* WT;                          // three-layer nets: W_1 transposed ([n_1][n_2]), else null
+  float* WT;                          // L >= 3: W_{L-2} transposed ([n_{L-2}][n_{L-1}]), else null
 };
 
 // Kernels index the pointer and size arrays of NetDev with runtime values (the

@@ -16,6 +16,7 @@
 #include "loop_kernel.hpp"
 #include "mlp_kernels.hpp"
 #include "slab_kernels.hpp"
+#include "chain_kernels.hpp"
 
 using mca::Aux;
 using mca::DevState;
@@ -38,7 +39,9 @@ struct Layout {
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
-  size_t cols = 0, nnz = 0;  // three-layer nets: nonzero entries of candidates' W_1 columns
+  size_t cols = 0, nnz = 0;  // nonzero entries of layer L-3 candidates' W_{L-2} columns
+  size_t rows = 0, rda = 0, rcnt = 0, pchain = 0;  // deep nets: affected samples, tile sums
+  int nchain = 0;
   int nslab = 0;
   int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
@@ -75,14 +78,16 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   if (!std::isfinite(net->bound)) return "bound must be finite (<= 0 disables it)";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31)) return "n_samples out of range";
   if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
-  if (L >= 4) {
+  if (L >= 3 && net->widths[L - 1] > mca::kSlabMaxUnits) {
     *code = MCA_EUNSUPPORTED;
-    return "MLPs with four or more weight matrices are not implemented by this build";
+    return "MLPs with three or more layers need a last hidden layer of at most 1024 units";
   }
-  if (L == 3 && net->widths[2] > mca::kSlabMaxUnits) {
-    *code = MCA_EUNSUPPORTED;
-    return "three-layer MLPs need a second hidden layer of at most 1024 units";
-  }
+  if (L >= 4)
+    for (int l = 1; l < L; ++l)
+      if (net->widths[l] != mca::kChainUnits) {
+        *code = MCA_EUNSUPPORTED;
+        return "MLPs with four or more layers need every hidden layer 256 units wide";
+      }
   *code = MCA_OK;
   return "";
 }
@@ -113,13 +118,20 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.state = take(sizeof(DevState));
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
-  if (L == 3) {
-    lo.wt = take((size_t)net->widths[1] * net->widths[2] * sizeof(float));
+  if (L >= 3) {
+    lo.wt = take((size_t)net->widths[L - 2] * net->widths[L - 1] * sizeof(float));
     const int T = mca::slab_tile(net->widths[L]);
     lo.nslab = (int)((N + T - 1) / T);
     lo.pslab = take((size_t)k_max * lo.nslab * sizeof(float));
-    lo.cols = take((size_t)k_max * net->widths[2] * sizeof(uint64_t));
+    lo.cols = take((size_t)k_max * net->widths[L - 1] * sizeof(uint64_t));
     lo.nnz = take((size_t)k_max * sizeof(int32_t));
+  }
+  if (L >= 4) {
+    lo.nchain = (int)((N + mca::kChainT - 1) / mca::kChainT);
+    lo.rows = take((size_t)k_max * N * sizeof(int32_t));
+    lo.rda = take((size_t)k_max * N * sizeof(float));
+    lo.rcnt = take((size_t)k_max * sizeof(int32_t));
+    lo.pchain = take((size_t)k_max * lo.nchain * sizeof(float));
   }
   // persistent loop: tiles of T samples (16..64), one workgroup each; the
   // partial sums are sized for the smallest tile
@@ -152,6 +164,10 @@ struct mca_ctx {
   float* pslab = nullptr;
   uint64_t* cols = nullptr;
   int* nnz = nullptr;
+  int* rows = nullptr;
+  float* rda = nullptr;
+  int* rcnt = nullptr;
+  float* pchain = nullptr;
   double* dl = nullptr;
   double* bsum = nullptr;
   DevState* st = nullptr;
@@ -273,8 +289,9 @@ int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const*
     MCA_HIP(ctx, hipMemcpyAsync(ctx->net.W[l], params[l], n * sizeof(float), hipMemcpyHostToDevice, ctx->stream));
     if (tern) MCA_HIP(ctx, hipMemcpyAsync(ctx->net.codes[l], codes[l], n, hipMemcpyHostToDevice, ctx->stream));
   }
-  if (ctx->net.WT != nullptr)  // W_1 [n_2][n_1] -> W_T [n_1][n_2]
-    MCA_HIP(ctx, mca::launch_transpose(ctx->net.W[1], d.widths[2], d.widths[1], ctx->net.WT, ctx->stream));
+  if (ctx->net.WT != nullptr)  // W_{L-2} [n_{L-1}][n_{L-2}] -> W_T [n_{L-2}][n_{L-1}]
+    MCA_HIP(ctx, mca::launch_transpose(ctx->net.W[L - 2], d.widths[L - 1], d.widths[L - 2],
+                                       ctx->net.WT, ctx->stream));
   MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
   return MCA_OK;
 }
@@ -315,22 +332,35 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
 }
 
 // Scores the K staged candidates: the column kernel for the last two layers,
-// the tile kernel for the first layer of a three-layer net.
+// the tile kernel for layer L-3, the dense chain for layers 0..L-4.
 hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
   hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream);
-  if (e == hipSuccess && net.WT != nullptr)
+  if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
                          ctx->lo.nslab, -2, ctx->st, ctx->dl, ctx->stream);
+  if (e == hipSuccess && net.L >= 4)
+    e = mca::launch_chain(net, ctx->cands, ctx->aux, K, ctx->rows, ctx->rda, ctx->rcnt,
+                          ctx->pchain, ctx->lo.nchain, -2, ctx->st, ctx->dl, ctx->stream);
   return e;
+}
+
+hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, int32_t* trc,
+                      double* trd) {
+  return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab,
+                            ctx->lo.nslab, ctx->pchain, ctx->lo.nchain, ctx->aux, K, ctx->dl,
+                            ctx->st, do_select, trc, trd, kTraceCap, ctx->stream);
 }
 
 // Commits candidate k (k < 0: the device decision); each kernel applies only
 // the candidates of the layers it scores.
 hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
   hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
-  if (e == hipSuccess && net.WT != nullptr)
+  if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
                          ctx->lo.nslab, k, ctx->st, ctx->dl, ctx->stream);
+  if (e == hipSuccess && net.L >= 4)
+    e = mca::launch_chain(net, ctx->cands, ctx->aux, 0, ctx->rows, ctx->rda, ctx->rcnt,
+                          ctx->pchain, ctx->lo.nchain, k, ctx->st, ctx->dl, ctx->stream);
   return e;
 }
 
@@ -420,10 +450,14 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.XT = (const float*)(ws + lo.xt);
   nd.ell = (float*)(ws + lo.ell);
   nd.y = (const int32_t*)(ws + lo.y);
-  nd.WT = (L == 3) ? (float*)(ws + lo.wt) : nullptr;
-  ctx->pslab = (L == 3) ? (float*)(ws + lo.pslab) : nullptr;
-  ctx->cols = (L == 3) ? (uint64_t*)(ws + lo.cols) : nullptr;
-  ctx->nnz = (L == 3) ? (int*)(ws + lo.nnz) : nullptr;
+  nd.WT = (L >= 3) ? (float*)(ws + lo.wt) : nullptr;
+  ctx->pslab = (L >= 3) ? (float*)(ws + lo.pslab) : nullptr;
+  ctx->cols = (L >= 3) ? (uint64_t*)(ws + lo.cols) : nullptr;
+  ctx->nnz = (L >= 3) ? (int*)(ws + lo.nnz) : nullptr;
+  ctx->rows = (L >= 4) ? (int*)(ws + lo.rows) : nullptr;
+  ctx->rda = (L >= 4) ? (float*)(ws + lo.rda) : nullptr;
+  ctx->rcnt = (L >= 4) ? (int*)(ws + lo.rcnt) : nullptr;
+  ctx->pchain = (L >= 4) ? (float*)(ws + lo.pchain) : nullptr;
   ctx->cands = (mca_cand*)(ws + lo.cands);
   ctx->aux = (Aux*)(ws + lo.aux);
   ctx->partial = (float*)(ws + lo.partial);
@@ -491,7 +525,7 @@ int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double*
   MCA_HIP(ctx, hipMemcpyAsync(ctx->cands, cands_host, (size_t)K * sizeof(mca_cand), hipMemcpyHostToDevice, ctx->stream));
   MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream); }));
   MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, ctx->net, K); }));
-  MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(ctx->net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab, ctx->lo.nslab, ctx->aux, K, ctx->dl, ctx->st, false, nullptr, nullptr, 0, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, ctx->net, K, false, nullptr, nullptr); }));
   std::vector<double> dl(K);
   DevState s{};
   MCA_HIP(ctx, hipMemcpyAsync(dl.data(), ctx->dl, (size_t)K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
@@ -613,7 +647,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     for (uint64_t s = 0; s < chunk; ++s) {
       MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(net, 0, true, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
       MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K); }));
-      MCA_HIP(ctx, timed(ctx, 2, [&] { return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab, ctx->lo.nslab, ctx->aux, K, ctx->dl, ctx->st, true, trc, trd, kTraceCap, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, net, K, true, trc, trd); }));
       MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1); }));
     }
     if (trace != nullptr) {

@@ -116,13 +116,15 @@ __global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca
 // selection (Eq. 6): one block, thread k owns candidate k
 // ---------------------------------------------------------------------------
 
-// A candidate in layer slab_layer (>= 0 for three-layer nets) takes its tile
-// sums from pslab[k * nslab + b] instead.  Sixteen threads add a candidate's
+// A candidate in layer slab_layer (L-3 for nets of three or more layers)
+// takes its tile sums from pslab[k * nslab + b], one in layers 0..chain_top
+// (L-4 for deeper nets) from pchain[k * nchain + b].  Sixteen threads add a candidate's
 // tile sums: thread r takes tiles r, r+16, ... in order, then a fixed
 // butterfly joins the sixteen (fp64).
 __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float* partial, int ntiles,
                                                   const mca_cand* cands, const float* pslab,
-                                                  int nslab, int slab_layer,
+                                                  int nslab, int slab_layer, const float* pchain,
+                                                  int nchain, int chain_top,
                                                   const Aux* aux, int K, double* dL,
                                                   DevState* st, int do_select,
                                                   int32_t* tr_chosen, double* tr_dl,
@@ -136,9 +138,16 @@ __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float*
     const int k = k0 + (tid >> 4), r = tid & 15;
     double s = 0.0;
     if (k < K) {
-      const bool slab = cands[k].layer == slab_layer;
-      const float* p = slab ? pslab + (int64_t)k * nslab : partial + (int64_t)k * ntiles;
-      const int nt = slab ? nslab : ntiles;
+      const int layer = cands[k].layer;
+      const float* p = partial + (int64_t)k * ntiles;
+      int nt = ntiles;
+      if (layer <= chain_top) {
+        p = pchain + (int64_t)k * nchain;
+        nt = nchain;
+      } else if (layer == slab_layer) {
+        p = pslab + (int64_t)k * nslab;
+        nt = nslab;
+      }
       // eight loads in flight, added in order
       for (int t0 = r; t0 < nt; t0 += 16 * 8) {
         float v[8];
@@ -332,13 +341,15 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
 }
 
 hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
-                         const mca_cand* cands, const float* pslab, int nslab, const Aux* aux,
-                         int K, double* dL, DevState* st, bool do_select, int32_t* tr_chosen,
-                         double* tr_dl, int64_t tr_cap, hipStream_t s) {
-  const int slab_layer = (net.WT != nullptr) ? net.L - 3 : -1;
+                         const mca_cand* cands, const float* pslab, int nslab,
+                         const float* pchain, int nchain, const Aux* aux, int K, double* dL,
+                         DevState* st, bool do_select, int32_t* tr_chosen, double* tr_dl,
+                         int64_t tr_cap, hipStream_t s) {
+  const int slab_layer = (net.L >= 3) ? net.L - 3 : -1;
+  const int chain_top = (net.L >= 4) ? net.L - 4 : -1;
   hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, partial, ntiles, cands, pslab,
-                     nslab, slab_layer, aux, K, dL, st, do_select ? 1 : 0, tr_chosen, tr_dl,
-                     tr_cap);
+                     nslab, slab_layer, pchain, nchain, chain_top, aux, K, dL, st,
+                     do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
   return hipGetLastError();
 }
 

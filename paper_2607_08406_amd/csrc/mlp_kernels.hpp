@@ -14,9 +14,10 @@ hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* 
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        float* partial, int ntiles, hipStream_t s);
 hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
-                         const mca_cand* cands, const float* pslab, int nslab, const Aux* aux,
-                         int K, double* dL, DevState* st, bool do_select, int32_t* tr_chosen,
-                         double* tr_dl, int64_t tr_cap, hipStream_t s);
+                         const mca_cand* cands, const float* pslab, int nslab,
+                         const float* pchain, int nchain, const Aux* aux, int K, double* dL,
+                         DevState* st, bool do_select, int32_t* tr_chosen, double* tr_dl,
+                         int64_t tr_cap, hipStream_t s);
 hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* aux,
                          const double* dL, DevState* st, int k_host, int ntiles, hipStream_t s);
 hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s);

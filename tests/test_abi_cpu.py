@@ -82,7 +82,9 @@ def test_plan_layer_limits(binding):
     # X^T, W_0..W_2, W_1 transposed, Z_0..Z_2 dominate
     core = 4 * (784 * 8192 + 784 * 1024 + 2 * 1024 * 1024 + 10240 + (1024 + 1024 + 10) * 8192)
     assert core < b3 < core + 16 * 2 ** 20
-    for widths in [(784, 1024, 2048, 10), (64, 32, 32, 32, 10)]:
+    deep = binding.mlp_desc((784,) + (256,) * 24 + (10,), "tanh", delta=0.01)
+    assert binding.mca_plan(deep, 4096, 32) > 4 * 4096 * 256 * 24
+    for widths in [(784, 1024, 2048, 10), (64, 32, 32, 32, 10), (64, 256, 512, 256, 10)]:
         d = binding.mlp_desc(widths, "tanh", delta=0.1)
         with pytest.raises(binding.MCAError) as e:
             binding.mca_plan(d, 1024, 8)
