@@ -24,6 +24,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+MFMA_FP32_PEAK_TFS = 157.3  # MI355X dense fp32 matrix
+VALU_FP32_PEAK_TFS = 157.3  # MI355X fp32 vector (256 CUs x 2.4 GHz x 256 flop/clk, packed FMA)
 
 
 def algorithmic_bytes_per_step(cfg) -> float:
@@ -45,6 +47,32 @@ def algorithmic_bytes_per_step(cfg) -> float:
     for l, s in enumerate(sizes):
         per_cand += (s / P) * (8.0 * N if l == L - 2 else 4.0 * N)
     return shared + K * per_cand
+
+
+def candidate_flops(cfg, w, cands, params):
+    """Algorithmic flops of scoring one step's candidates on the deep or the
+    three-layer net (an FMA counts 2).  A mutation in layers 0..L-4 recomputes,
+    for each sample whose activation changes, the rank-1 update of the next
+    layer (2 n), the dense layers after it (2 n^2 each) and the logits (2 n C);
+    one in layer L-3 moves, per affected sample and per nonzero entry of the
+    W_{L-2} column, one unit of the last hidden layer (2) and the C logits
+    (2 C).  Affected samples: those with a nonzero input (for layer 0 a pixel
+    column of the data; for deeper layers the tanh or Gaussian activation,
+    nonzero for every sample)."""
+    import numpy as np
+    L, C, N = cfg.n_layers, cfg.n_classes, cfg.n_samples
+    X = w["X"]
+    total = 0.0
+    for c in cands:
+        l, j, i = int(c["layer"]), int(c["j"]), int(c["i"])
+        rows = float(np.count_nonzero(X[:, i])) if l == 0 else float(N)
+        if l <= L - 4:
+            n = cfg.widths[l + 1]
+            total += rows * (2 * n + (L - 3 - l) * 2 * n * n + 2 * n * C)
+        elif l == L - 3:
+            nnz = float(np.count_nonzero(params[L - 2][:, j]))
+            total += rows * nnz * (2 + 2 * C)
+    return total
 
 
 def measured_traffic(kernel: str, workload: str, steps: int):
@@ -167,12 +195,35 @@ def main():
 
     loop = launches[mca.PHASES.index("step_loop")] > 0
     dominant = mca.PHASES.index("step_loop" if loop else "eval")
-    kernel = "k_step_loop" if loop else "k_eval_column"
     n_launch = max(int(launches[dominant]), 1)
     avg_s = ms[dominant] / 1e3 / n_launch
-    # one loop launch covers all timed steps; one eval launch covers one step
-    bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
-    achieved = bytes_launch / avg_s / 1e9
+    if cfg.n_layers <= 2:
+        kernel = "k_step_loop" if loop else "k_eval_column"
+        # one loop launch covers all timed steps; one eval launch covers one step
+        bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
+        achieved = bytes_launch / avg_s / 1e9
+        roof = {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                "traffic": (measured_traffic(kernel, "wide_784-16384-10_K64", args.steps)
+                            if loop and cfg.name == "wide" else None),
+                "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
+                "launches": int(launches[dominant]),
+                "bytes_per_step": algorithmic_bytes_per_step(cfg)}
+    else:
+        # the evaluation phase of one step: its candidates' algorithmic flops
+        params, _ = ctx.params()
+        t_first = st.next_step - args.steps
+        flops = [candidate_flops(cfg, w, ctx.propose(t_first + n, cfg.K), params)
+                 for n in range(0, args.steps, max(args.steps // 50, 1))]
+        per_step = float(np.mean(flops))
+        achieved = per_step / avg_s / 1e12
+        deep = cfg.n_layers >= 4
+        peak = MFMA_FP32_PEAK_TFS if deep else VALU_FP32_PEAK_TFS
+        roof = {"bound": "mfma" if deep else "alu",
+                "kernel": "eval phase (k_chain dominant)" if deep else "eval phase (k_slab dominant)",
+                "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": None, "flops_per_launch": per_step, "avg_launch_us": avg_s * 1e6,
+                "launches": int(launches[dominant])}
     result = {
         "metric": "candidate loss evals/sec + accepted mutations/sec at 1 GPU; % HBM/MFMA roofline",
         "value": st.evaluated / wall,
@@ -192,14 +243,7 @@ def main():
                                 f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}"),
                    "K": cfg.K, "n_samples": cfg.n_samples, "widths": list(cfg.widths),
                    "n_params": cfg.n_params},
-        "roofline": {"bound": "hbm", "kernel": kernel,
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": (measured_traffic(kernel, "wide_784-16384-10_K64", args.steps)
-                                 if loop and cfg.name == "wide" else None),
-                     "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
-                     "launches": int(launches[dominant]),
-                     "bytes_per_step": algorithmic_bytes_per_step(cfg)},
+        "roofline": roof,
         "final_loss": st.loss,
     }
     ctx.close()
