@@ -6,6 +6,6 @@ The computation lives in the HIP library ``libmca.so`` (C ABI in
 ``include/mca.h``); ``paper_2607_08406_amd.mca`` is its ctypes binding.
 """
 from . import mca  # noqa: F401
-from .mca import Context, MCAError, mlp_desc  # noqa: F401
+from .mca import Context, MCAError, TransformerContext, mlp_desc, transformer_desc  # noqa: F401
 
-__all__ = ["mca", "Context", "MCAError", "mlp_desc"]
+__all__ = ["mca", "Context", "MCAError", "TransformerContext", "mlp_desc", "transformer_desc"]

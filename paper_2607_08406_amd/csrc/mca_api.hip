@@ -17,6 +17,7 @@
 #include "mlp_kernels.hpp"
 #include "slab_kernels.hpp"
 #include "chain_kernels.hpp"
+#include "tf_kernels.hpp"
 
 using mca::Aux;
 using mca::DevState;
@@ -51,10 +52,6 @@ struct Layout {
 std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max, int* code) {
   *code = MCA_EINVAL;
   if (net == nullptr) return "net description is NULL";
-  if (net->kind == MCA_NET_TRANSFORMER) {
-    *code = MCA_EUNSUPPORTED;
-    return "Transformer nets are not implemented by this build";
-  }
   if (net->kind != MCA_NET_MLP) return "unknown net kind";
   const int L = net->n_layers;
   if (L < 1 || L > MCA_MAX_LAYERS) return "n_layers out of range [1, 32]";
@@ -90,6 +87,114 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
       }
   *code = MCA_OK;
   return "";
+}
+
+// ---------------------------------------------------------------------------
+// Transformer nets: shapes, validation and workspace layout
+// ---------------------------------------------------------------------------
+
+struct TfShape {
+  int64_t rows, cols;  // 1-D tensors: cols = 1
+};
+
+// Canonical parameter order: tok_emb, pos_emb, per block ln1.g, ln1.b, wq, bq,
+// wk, bk, wv, bv, wo, bo, ln2.g, ln2.b, wfc, bfc, wproj, bproj, then lnf.g,
+// lnf.b, wout, bout; linear weights [out][in].
+std::vector<TfShape> tf_shapes(const mca_net_desc* d) {
+  const int64_t V = d->vocab, T = d->ctx, D = d->d_model, M = d->d_mlp;
+  std::vector<TfShape> s = {{V, D}, {T, D}};
+  for (int b = 0; b < d->n_block; ++b) {
+    const TfShape blk[mca::kBlockTensors] = {{D, 1}, {D, 1}, {D, D}, {D, 1}, {D, D}, {D, 1},
+                                             {D, D}, {D, 1}, {D, D}, {D, 1}, {D, 1}, {D, 1},
+                                             {M, D}, {M, 1}, {D, M}, {D, 1}};
+    s.insert(s.end(), blk, blk + mca::kBlockTensors);
+  }
+  s.push_back({D, 1});
+  s.push_back({D, 1});
+  s.push_back({V, D});
+  s.push_back({V, 1});
+  return s;
+}
+
+std::string tf_check_desc(const mca_net_desc* d, int64_t n_samples, int32_t k_max, int* code) {
+  *code = MCA_EINVAL;
+  if (d->vocab < 2 || d->ctx < 1 || d->d_model < 1 || d->n_block < 1 || d->n_head < 1 ||
+      d->d_mlp < 1)
+    return "transformer sizes must be positive (vocab >= 2)";
+  if (!(std::isfinite(d->ln_eps) && d->ln_eps > 0.f)) return "ln_eps must be finite and positive";
+  if (!std::isfinite(d->delta) || d->delta < 0.f) return "delta must be finite and >= 0";
+  if (!std::isfinite(d->bound)) return "bound must be finite (<= 0 disables it)";
+  if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
+  if (n_samples < 1 || n_samples > ((int64_t)1 << 31) || n_samples % d->ctx != 0)
+    return "n_samples must be a positive multiple of ctx";
+  *code = MCA_EUNSUPPORTED;
+  if (d->weight_mode != MCA_WEIGHTS_FP32) return "Transformer nets take continuous weights only";
+  if (d->pick != MCA_PICK_WEIGHT) return "Transformer nets draw uniformly over all parameters only";
+  if (d->d_model != mca::kTfHeadDim * d->n_head) return "d_model must be 32 * n_head";
+  if (d->d_model > 256) return "d_model must be at most 256";
+  if (d->d_mlp % 16 != 0) return "d_mlp must be a multiple of 16";
+  if (d->ctx > mca::kTfMaxCtx) return "ctx must be at most 128";
+  if (d->n_block > mca::kTfMaxBlocks) return "at most 8 blocks";
+  *code = MCA_OK;
+  return "";
+}
+
+struct TfLayout {
+  size_t param[mca::kTfMaxTensors] = {};
+  size_t tok = 0, tgt = 0, x = 0, ell = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0;
+  size_t state = 0, tr_chosen = 0, tr_dl = 0;
+  size_t sx = 0, sh = 0, sln = 0, sqkv = 0, satt = 0, sfc = 0, sell = 0, scopy = 0;
+  size_t table = 0, start = 0, dev = 0;
+  int64_t copy_stride = 0;
+  int nblk = 0, n_tensors = 0;
+  size_t total = 0;
+};
+
+TfLayout tf_make_layout(const mca_net_desc* d, int64_t N, int32_t k_max) {
+  TfLayout lo;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const std::vector<TfShape> shapes = tf_shapes(d);
+  lo.n_tensors = (int)shapes.size();
+  int64_t maxsz = 0;
+  for (size_t t = 0; t < shapes.size(); ++t) {
+    const int64_t n = shapes[t].rows * shapes[t].cols;
+    lo.param[t] = take((size_t)n * sizeof(float));
+    maxsz = std::max(maxsz, n);
+  }
+  const size_t K = (size_t)k_max, n = (size_t)N, D = (size_t)d->d_model;
+  const size_t NB = (size_t)d->n_block, FCW = (size_t)std::max(d->d_mlp, d->vocab);
+  lo.nblk = mca::tf_loss_blocks(N);
+  lo.tok = take(n * sizeof(int32_t));
+  lo.tgt = take(n * sizeof(int32_t));
+  lo.x = take((NB + 1) * n * D * sizeof(float));
+  lo.ell = take(n * sizeof(float));
+  lo.cands = take(K * sizeof(mca_cand));
+  lo.aux = take(K * sizeof(Aux));
+  lo.partial = take(K * lo.nblk * sizeof(float));
+  lo.dl = take(K * sizeof(double));
+  lo.bsum = take((size_t)lo.nblk * sizeof(double));
+  lo.state = take(sizeof(DevState));
+  lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
+  lo.tr_dl = take((size_t)kTraceCap * K * sizeof(double));
+  lo.sx = take(K * (NB + 1) * n * D * sizeof(float));
+  lo.sh = take(K * n * D * sizeof(float));
+  lo.sln = take(K * n * D * sizeof(float));
+  lo.satt = take(K * n * D * sizeof(float));
+  lo.sqkv = take(K * n * 3 * D * sizeof(float));
+  lo.sfc = take(K * n * FCW * sizeof(float));
+  lo.sell = take(K * n * sizeof(float));
+  lo.copy_stride = (maxsz + 63) / 64 * 64;
+  lo.scopy = take(K * (size_t)lo.copy_stride * sizeof(float));
+  lo.table = take(K * (size_t)lo.n_tensors * sizeof(float*));
+  lo.start = take(K * sizeof(int32_t));
+  lo.dev = take(sizeof(mca::TfDev));
+  lo.total = off;
+  return lo;
 }
 
 Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
@@ -177,6 +282,11 @@ struct mca_ctx {
   uint64_t* loop_dls = nullptr;
   mca::LoopSync* loop_sync = nullptr;
   bool use_loop = true;
+  // Transformer nets
+  bool tf = false;
+  mca::TfDev tfh{};           // host copy of the device description
+  mca::TfDev* tfd = nullptr;  // device copy, in the workspace
+  int tf_nblk = 0;            // loss tiles of 256 positions
   bool pending = false;
   int32_t pending_K = 0;
   bool poisoned = false;
@@ -257,11 +367,41 @@ int flush_timing(mca_ctx* ctx) {
 }
 
 int run_forward(mca_ctx* ctx) {
+  if (ctx->tf) {
+    // one unmutated pass in slot 0, copied into the committed state
+    MCA_HIP(ctx, timed(ctx, 5, [&] {
+      hipError_t e = mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, 0, true,
+                                         ctx->partial, ctx->tf_nblk, ctx->stream);
+      if (e == hipSuccess)
+        e = mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, 0,
+                                  true, ctx->bsum, ctx->stream);
+      return e;
+    }));
+    return MCA_OK;
+  }
   MCA_HIP(ctx, timed(ctx, 5, [&] { return mca::launch_forward(ctx->net, ctx->bsum, ctx->st, ctx->stream); }));
   return MCA_OK;
 }
 
+int tf_upload_params(mca_ctx* ctx, const float* const* params) {
+  if (params == nullptr) return fail(ctx, MCA_EINVAL, "params is NULL");
+  const std::vector<TfShape> shapes = tf_shapes(&ctx->desc);
+  for (size_t t = 0; t < shapes.size(); ++t) {
+    if (params[t] == nullptr) return fail(ctx, MCA_EINVAL, "a parameter pointer is NULL");
+    const int64_t n = shapes[t].rows * shapes[t].cols;
+    for (int64_t e = 0; e < n; ++e)
+      if (!std::isfinite(params[t][e])) return fail(ctx, MCA_EINVAL, "non-finite parameter");
+  }
+  for (size_t t = 0; t < shapes.size(); ++t) {
+    const size_t n = (size_t)(shapes[t].rows * shapes[t].cols);
+    MCA_HIP(ctx, hipMemcpyAsync(ctx->tfh.param[t], params[t], n * sizeof(float), hipMemcpyHostToDevice, ctx->stream));
+  }
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
 int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const* codes) {
+  if (ctx->tf) return tf_upload_params(ctx, params);
   const mca_net_desc& d = ctx->desc;
   const int L = d.n_layers;
   if (params == nullptr) return fail(ctx, MCA_EINVAL, "params is NULL");
@@ -317,6 +457,16 @@ int read_state(mca_ctx* ctx, DevState* s) {
 
 int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
   const mca_net_desc& d = ctx->desc;
+  if (ctx->tf) {
+    for (int k = 0; k < K; ++k) {
+      const int l = c[k].layer;
+      if (l < 0 || l >= ctx->tfh.n_tensors) return fail(ctx, MCA_EINVAL, "candidate tensor out of range");
+      if (c[k].j < 0 || c[k].j >= ctx->tfh.rows[l] || c[k].i < 0 || c[k].i >= ctx->tfh.cols[l])
+        return fail(ctx, MCA_EINVAL, "candidate index out of range");
+      if (!std::isfinite(c[k].d)) return fail(ctx, MCA_EINVAL, "candidate increment is not finite");
+    }
+    return MCA_OK;
+  }
   for (int k = 0; k < K; ++k) {
     const int l = c[k].layer;
     if (l < 0 || l >= d.n_layers) return fail(ctx, MCA_EINVAL, "candidate layer out of range");
@@ -331,9 +481,25 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
   return MCA_OK;
 }
 
+hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
+  if (ctx->tf)
+    return mca::tf_launch_propose(ctx->tfd, ctx->tfh, step, use_dev_t, ctx->st, K, ctx->cands,
+                                  ctx->aux, ctx->stream);
+  return mca::launch_propose(ctx->net, step, use_dev_t, ctx->st, K, ctx->cands, ctx->aux,
+                             ctx->stream);
+}
+
+hipError_t prepare_dev(mca_ctx* ctx, int K) {
+  if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, ctx->cands, K, ctx->aux, ctx->stream);
+  return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream);
+}
+
 // Scores the K staged candidates: the column kernel for the last two layers,
 // the tile kernel for layer L-3, the dense chain for layers 0..L-4.
 hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
+  if (ctx->tf)
+    return mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, K, false, ctx->partial,
+                               ctx->tf_nblk, ctx->stream);
   hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
@@ -346,6 +512,10 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
 
 hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, int32_t* trc,
                       double* trd) {
+  if (ctx->tf)
+    return mca::launch_select(net, ctx->partial, ctx->tf_nblk, ctx->cands, nullptr, 0, nullptr, 0,
+                              ctx->aux, K, ctx->dl, ctx->st, do_select, trc, trd, kTraceCap,
+                              ctx->stream);
   return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab,
                             ctx->lo.nslab, ctx->pchain, ctx->lo.nchain, ctx->aux, K, ctx->dl,
                             ctx->st, do_select, trc, trd, kTraceCap, ctx->stream);
@@ -354,6 +524,9 @@ hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, in
 // Commits candidate k (k < 0: the device decision); each kernel applies only
 // the candidates of the layers it scores.
 hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
+  if (ctx->tf)
+    return mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, k,
+                                 false, ctx->bsum, ctx->stream);
   hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
@@ -362,6 +535,124 @@ hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
     e = mca::launch_chain(net, ctx->cands, ctx->aux, 0, ctx->rows, ctx->rda, ctx->rcnt,
                           ctx->pchain, ctx->lo.nchain, k, ctx->st, ctx->dl, ctx->stream);
   return e;
+}
+
+// Transformer context: validate, lay out, upload, fill the caches.
+int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, int32_t n_params,
+            const mca_data* data, int32_t k_max, void* workspace, size_t workspace_bytes,
+            void* hip_stream) {
+  int code;
+  std::string msg = tf_check_desc(net, data->n_samples, k_max, &code);
+  if (code != MCA_OK) return fail(nullptr, code, msg);
+  const TfLayout lo = tf_make_layout(net, data->n_samples, k_max);
+  if (n_params != lo.n_tensors) return fail(nullptr, MCA_EINVAL, "n_params must equal the number of Transformer tensors");
+  if (data->tokens == nullptr || data->y == nullptr) return fail(nullptr, MCA_EINVAL, "data.tokens or data.y is NULL");
+  if (data->n_seq < 1 || (int64_t)data->n_seq * net->ctx != data->n_samples)
+    return fail(nullptr, MCA_EINVAL, "n_samples must equal n_seq * ctx");
+  if (workspace == nullptr) return fail(nullptr, MCA_EINVAL, "workspace is NULL");
+  if (((uintptr_t)workspace) % kAlign != 0) return fail(nullptr, MCA_EINVAL, "workspace is not 256-byte aligned");
+  if (workspace_bytes < lo.total) return fail(nullptr, MCA_ENOSPACE, "workspace smaller than mca_plan()");
+  const int64_t N = data->n_samples;
+  for (int64_t n = 0; n < N; ++n) {
+    if (data->tokens[n] < 0 || data->tokens[n] >= net->vocab) return fail(nullptr, MCA_EINVAL, "token out of range");
+    if (data->y[n] < 0 || data->y[n] >= net->vocab) return fail(nullptr, MCA_EINVAL, "target out of range");
+  }
+  mca_ctx* ctx = new (std::nothrow) mca_ctx();
+  if (ctx == nullptr) return fail(nullptr, MCA_EINVAL, "out of host memory");
+  ctx->tf = true;
+  ctx->use_loop = false;
+  ctx->desc = *net;
+  ctx->k_max = k_max;
+  ctx->stream = (hipStream_t)hip_stream;
+  ctx->ws = (char*)workspace;
+  char* ws = ctx->ws;
+  mca::TfDev& h = ctx->tfh;
+  h.V = net->vocab;
+  h.T = net->ctx;
+  h.D = net->d_model;
+  h.NB = net->n_block;
+  h.H = net->n_head;
+  h.M = net->d_mlp;
+  h.S = data->n_seq;
+  h.n_tensors = lo.n_tensors;
+  h.N = N;
+  h.eps = net->ln_eps;
+  h.delta = net->delta;
+  h.bound = net->bound;
+  h.ties = net->accept_ties ? 1 : 0;
+  h.seed = net->seed;
+  h.tag = net->stream_tag;
+  const std::vector<TfShape> shapes = tf_shapes(net);
+  int64_t off = 0;
+  for (int t = 0; t < lo.n_tensors; ++t) {
+    h.offs[t] = off;
+    h.rows[t] = (int32_t)shapes[t].rows;
+    h.cols[t] = (int32_t)shapes[t].cols;
+    off += shapes[t].rows * shapes[t].cols;
+    h.param[t] = (float*)(ws + lo.param[t]);
+  }
+  h.offs[lo.n_tensors] = off;
+  h.P = off;
+  h.tok = (const int32_t*)(ws + lo.tok);
+  h.tgt = (const int32_t*)(ws + lo.tgt);
+  const int64_t ND = N * h.D;
+  for (int b = 0; b <= h.NB; ++b) h.x[b] = (float*)(ws + lo.x) + (int64_t)b * ND;
+  h.ell = (float*)(ws + lo.ell);
+  h.sx = (float*)(ws + lo.sx);
+  h.sh = (float*)(ws + lo.sh);
+  h.sln = (float*)(ws + lo.sln);
+  h.sqkv = (float*)(ws + lo.sqkv);
+  h.satt = (float*)(ws + lo.satt);
+  h.sfc = (float*)(ws + lo.sfc);
+  h.sell = (float*)(ws + lo.sell);
+  h.scopy = (float*)(ws + lo.scopy);
+  h.copy_stride = lo.copy_stride;
+  h.table = (float**)(ws + lo.table);
+  h.start = (int32_t*)(ws + lo.start);
+  ctx->tfd = (mca::TfDev*)(ws + lo.dev);
+  ctx->tf_nblk = lo.nblk;
+  ctx->cands = (mca_cand*)(ws + lo.cands);
+  ctx->aux = (Aux*)(ws + lo.aux);
+  ctx->partial = (float*)(ws + lo.partial);
+  ctx->dl = (double*)(ws + lo.dl);
+  ctx->bsum = (double*)(ws + lo.bsum);
+  ctx->st = (DevState*)(ws + lo.state);
+  ctx->tr_chosen = (int32_t*)(ws + lo.tr_chosen);
+  ctx->tr_dl = (double*)(ws + lo.tr_dl);
+  // what the shared selection and state calls read
+  NetDev& nd = ctx->net;
+  nd.L = 0;
+  nd.C = h.V;
+  nd.ties = h.ties;
+  nd.N = N;
+  nd.Ns = N;
+  nd.P = h.P;
+  nd.ell = h.ell;
+  {
+    hipError_t e = hipMemcpyAsync((void*)h.tok, data->tokens, (size_t)N * sizeof(int32_t), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync((void*)h.tgt, data->y, (size_t)N * sizeof(int32_t), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(ctx->tfd, &h, sizeof h, hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) {
+      device_fail(nullptr, e, "upload of the data set");
+      delete ctx;
+      return MCA_EDEVICE;
+    }
+  }
+  int rc = upload_params(ctx, params, nullptr);
+  if (rc == MCA_OK) rc = write_state(ctx, 0, false);
+  if (rc == MCA_OK) rc = run_forward(ctx);
+  if (rc == MCA_OK) {
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) rc = device_fail(ctx, e, "forward pass");
+  }
+  if (rc != MCA_OK) {
+    g_thread_error = ctx->err;
+    delete ctx;
+    return rc;
+  }
+  *out = ctx;
+  return MCA_OK;
 }
 
 }  // namespace
@@ -384,6 +675,13 @@ size_t mca_struct_size(int32_t which) {
 
 int mca_plan(const mca_net_desc* net, int64_t n_samples, int32_t k_max, size_t* workspace_bytes) {
   int code;
+  if (net != nullptr && net->kind == MCA_NET_TRANSFORMER) {
+    std::string msg = tf_check_desc(net, n_samples, k_max, &code);
+    if (code != MCA_OK) return fail(nullptr, code, msg);
+    if (workspace_bytes == nullptr) return fail(nullptr, MCA_EINVAL, "workspace_bytes is NULL");
+    *workspace_bytes = tf_make_layout(net, n_samples, k_max).total;
+    return MCA_OK;
+  }
   std::string msg = check_desc(net, n_samples, k_max, &code);
   if (code != MCA_OK) return fail(nullptr, code, msg);
   if (workspace_bytes == nullptr) return fail(nullptr, MCA_EINVAL, "workspace_bytes is NULL");
@@ -397,6 +695,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   if (out == nullptr) return fail(nullptr, MCA_EINVAL, "out is NULL");
   *out = nullptr;
   if (data == nullptr) return fail(nullptr, MCA_EINVAL, "data is NULL");
+  if (net != nullptr && net->kind == MCA_NET_TRANSFORMER)
+    return tf_init(out, net, params, n_params, data, k_max, workspace, workspace_bytes, hip_stream);
   int code;
   std::string msg = check_desc(net, data->n_samples, k_max, &code);
   if (code != MCA_OK) return fail(nullptr, code, msg);
@@ -508,7 +808,7 @@ int mca_propose(mca_ctx* ctx, uint64_t step, int32_t K, mca_cand* out_host) {
   if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
   // the proposal reuses the candidate buffers of a pending batch
   if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
-  MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(ctx->net, step, false, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_dev(ctx, step, false, K); }));
   MCA_HIP(ctx, hipMemcpyAsync(out_host, ctx->cands, (size_t)K * sizeof(mca_cand), hipMemcpyDeviceToHost, ctx->stream));
   MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
   return MCA_OK;
@@ -523,7 +823,7 @@ int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double*
   int rc = check_cands(ctx, cands_host, K);
   if (rc != MCA_OK) return rc;
   MCA_HIP(ctx, hipMemcpyAsync(ctx->cands, cands_host, (size_t)K * sizeof(mca_cand), hipMemcpyHostToDevice, ctx->stream));
-  MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream); }));
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return prepare_dev(ctx, K); }));
   MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, ctx->net, K); }));
   MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, ctx->net, K, false, nullptr, nullptr); }));
   std::vector<double> dl(K);
@@ -566,6 +866,7 @@ int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value) {
     return MCA_OK;
   }
   if (option == MCA_OPT_LOOP_TILE) {
+    if (ctx->tf) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_TILE applies to MLP contexts");
     if (value < kMinLoopTile || value > 64) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_TILE takes 16..64");
     ctx->lo.loop_T = (int)value;
     ctx->lo.loop_G = (int)((ctx->net.N + value - 1) / value);
@@ -593,10 +894,11 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   const NetDev& net = ctx->net;
   uint64_t done = 0;
   int max_blocks = 0;
-  if (ctx->use_loop && net.L <= 2 && K <= mca::kLoopMaxK)
+  const bool mlp2 = !ctx->tf && net.L <= 2;
+  if (ctx->use_loop && mlp2 && K <= mca::kLoopMaxK)
     MCA_HIP(ctx, mca::step_loop_max_blocks(K, net.C, &max_blocks));
   // G tile workgroups plus the candidate reducers must all be resident at once
-  const bool loop_ok = ctx->use_loop && net.L <= 2 && K <= mca::kLoopMaxK &&
+  const bool loop_ok = ctx->use_loop && mlp2 && K <= mca::kLoopMaxK &&
                        ctx->lo.loop_G <= mca::kLoopMaxTiles &&
                        ctx->lo.loop_G + mca::step_loop_reducers(K) <= max_blocks;
   while (loop_ok && done < n_steps) {
@@ -645,7 +947,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
       trd = trace->dloss ? ctx->tr_dl : nullptr;
     }
     for (uint64_t s = 0; s < chunk; ++s) {
-      MCA_HIP(ctx, timed(ctx, 0, [&] { return mca::launch_propose(net, 0, true, ctx->st, K, ctx->cands, ctx->aux, ctx->stream); }));
+      MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_dev(ctx, 0, true, K); }));
       MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K); }));
       MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, net, K, true, trc, trd); }));
       MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1); }));
@@ -677,6 +979,15 @@ int mca_get_params(mca_ctx* ctx, float* const* params_out, int8_t* const* codes_
   MCA_LIVE(ctx);
   if (params_out == nullptr) return fail(ctx, MCA_EINVAL, "params_out is NULL");
   const mca_net_desc& d = ctx->desc;
+  if (ctx->tf) {
+    for (int t = 0; t < ctx->tfh.n_tensors; ++t) {
+      if (params_out[t] == nullptr) return fail(ctx, MCA_EINVAL, "a params_out pointer is NULL");
+      const size_t n = (size_t)ctx->tfh.rows[t] * ctx->tfh.cols[t];
+      MCA_HIP(ctx, hipMemcpyAsync(params_out[t], ctx->tfh.param[t], n * sizeof(float), hipMemcpyDeviceToHost, ctx->stream));
+    }
+    MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    return MCA_OK;
+  }
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
     if (params_out[l] == nullptr) return fail(ctx, MCA_EINVAL, "a params_out pointer is NULL");

@@ -174,6 +174,25 @@ def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta
     return d
 
 
+def transformer_desc(vocab: int, ctx: int, d_model: int, n_block: int, n_head: int,
+                     d_mlp: int, delta: float = 0.0, ln_eps: float = 1e-5, bound: float = 0.0,
+                     accept_ties: bool = False, seed: int = 0,
+                     stream_tag: int = 0) -> mca_net_desc:
+    d = mca_net_desc()
+    d.kind = MCA_NET_TRANSFORMER
+    d.vocab, d.ctx, d.d_model = int(vocab), int(ctx), int(d_model)
+    d.n_block, d.n_head, d.d_mlp = int(n_block), int(n_head), int(d_mlp)
+    d.ln_eps = float(np.float32(ln_eps))
+    d.weight_mode = MCA_WEIGHTS_FP32
+    d.pick = MCA_PICK_WEIGHT
+    d.delta = float(np.float32(delta))
+    d.bound = bound
+    d.accept_ties = int(accept_ties)
+    d.seed = seed
+    d.stream_tag = stream_tag
+    return d
+
+
 # ---------------------------------------------------------------------------
 # the calls, with the C names
 # ---------------------------------------------------------------------------
@@ -203,6 +222,26 @@ def mca_init(desc, params: List[np.ndarray], codes, X: np.ndarray, y: np.ndarray
     rc = lib.mca_init(ctypes.byref(out), ctypes.byref(desc), _ptr_array(params, ctypes.c_float),
                       len(params), None if codes_c is None else _ptr_array(codes_c, ctypes.c_int8),
                       ctypes.byref(data), k_max, workspace.data_ptr(), workspace.numel(), stream_ptr)
+    _check(rc)
+    return out
+
+
+def mca_init_transformer(desc, params: List[np.ndarray], tokens: np.ndarray, targets: np.ndarray,
+                         k_max: int, workspace: torch.Tensor, stream_ptr: int):
+    """mca_init for a Transformer: tokens and targets are [n_seq][ctx] int32."""
+    lib = load_library()
+    params = [np.ascontiguousarray(p, dtype=np.float32) for p in params]
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    targets = np.ascontiguousarray(targets, dtype=np.int32)
+    data = mca_data()
+    data.n_samples = tokens.size
+    data.n_seq = tokens.shape[0]
+    data.tokens = tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    data.y = targets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    out = ctypes.c_void_p()
+    rc = lib.mca_init(ctypes.byref(out), ctypes.byref(desc), _ptr_array(params, ctypes.c_float),
+                      len(params), None, ctypes.byref(data), k_max, workspace.data_ptr(),
+                      workspace.numel(), stream_ptr)
     _check(rc)
     return out
 
@@ -380,3 +419,22 @@ class Context:
             self.close()
         except Exception:
             pass
+
+
+class TransformerContext(Context):
+    """An MCA context of the decoder Transformer; params in canonical order."""
+
+    def __init__(self, desc: mca_net_desc, params, tokens, targets, k_max: int,
+                 device: str = "cuda:0", stream: Optional[torch.cuda.Stream] = None):
+        if not torch.cuda.is_available():
+            raise MCAError(MCA_EDEVICE, "no GPU visible: the MCA library runs only on the GPU")
+        self.desc = desc
+        self.shapes = [np.shape(p) for p in params]
+        self.ternary = False
+        self.n_samples = int(np.size(tokens))
+        self.device = torch.device(device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = mca_plan(desc, self.n_samples, k_max)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.ctx = mca_init_transformer(desc, params, tokens, targets, k_max, self.workspace,
+                                        self.stream.cuda_stream)

@@ -61,7 +61,7 @@ def test_plan_sizes(binding):
     (dict(n_layers=0), "MCA_EINVAL"),
     (dict(act=7), "MCA_EINVAL"),
     (dict(pick=3), "MCA_EINVAL"),
-    (dict(kind=1), "MCA_EUNSUPPORTED"),
+    (dict(kind=1), "MCA_EINVAL"),  # a Transformer kind without Transformer sizes
     (dict(kind=5), "MCA_EINVAL"),
     (dict(delta=float("nan")), "MCA_EINVAL"),
 ])
@@ -89,6 +89,26 @@ def test_plan_layer_limits(binding):
         with pytest.raises(binding.MCAError) as e:
             binding.mca_plan(d, 1024, 8)
         assert "MCA_EUNSUPPORTED" in str(e.value)
+
+
+def test_plan_transformer(binding):
+    """The char-level decoder plans; shapes its kernels do not take are
+    reported as unsupported, inconsistent sizes as invalid."""
+    d = binding.transformer_desc(65, 128, 128, 2, 4, 512, delta=0.02)
+    b = binding.mca_plan(d, 64 * 128, 16)
+    # committed streams x_0..x_2 and 16 slots of activations dominate
+    assert b > 16 * 64 * 128 * 4 * (3 * 128 + 128 * 3 + 3 * 128 + 512)
+    for kw, code in [(dict(d_model=96), "MCA_EUNSUPPORTED"), (dict(ctx=256), "MCA_EUNSUPPORTED"),
+                     (dict(d_mlp=100), "MCA_EUNSUPPORTED"), (dict(vocab=1), "MCA_EINVAL")]:
+        args = dict(vocab=65, ctx=128, d_model=128, n_block=2, n_head=4, d_mlp=512)
+        args.update(kw)
+        dd = binding.transformer_desc(**args, delta=0.02)
+        with pytest.raises(binding.MCAError) as e:
+            binding.mca_plan(dd, 64 * args["ctx"], 16)
+        assert code in str(e.value)
+    with pytest.raises(binding.MCAError) as e:
+        binding.mca_plan(d, 64 * 128 + 1, 16)  # not a whole number of sequences
+    assert "MCA_EINVAL" in str(e.value)
 
 
 def test_plan_rejects_bad_sizes(binding):

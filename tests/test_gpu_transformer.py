@@ -1,0 +1,171 @@
+"""GPU parity of the decoder Transformer path against the fp64 oracle.
+
+Each candidate's loss is the full loss of the net with one parameter changed
+(the definition; the oracle recomputes everything in fp64); the device runs
+each candidate's forward pass from the first stage its parameter changes.
+Workloads: a reduced model (ctx 32, d 64, 2 heads, 2 blocks, 4 sequences)
+for explicit steps and a replayed device run, and the full char-level model
+(vocab 65, ctx 128, d 128, 4 heads, MLP 512, 2 blocks, 64 sequences) at
+K = 16.  Candidate records bit-exact, losses within relative 1e-5, decisions
+equal outside the tie band |dL| < 1e-6, committed parameters bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mca as omca
+from oracle.transformer import TransformerModel
+from parity_util import REL_TOL, TIE, assert_cands_equal, check_losses
+from workloads import CONFIGS, transformer_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def banner(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def mca():
+    from paper_2607_08406_amd import mca as m
+    m.load_library()
+    assert torch.cuda.is_available()
+    return m
+
+
+def make_pair(mca, cfg, k_max):
+    w = transformer_workload(cfg)
+    desc = mca.transformer_desc(cfg.vocab, cfg.ctx, cfg.d_model, cfg.n_layer, cfg.n_head,
+                                cfg.d_mlp, delta=cfg.delta, ln_eps=cfg.ln_eps,
+                                accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                                stream_tag=cfg.stream_tag)
+    ctx = mca.TransformerContext(desc, w["params"], w["tokens"], w["targets"], k_max=k_max)
+    ref = TransformerModel(w["params"], w["tokens"], w["targets"], cfg.vocab, cfg.ctx,
+                           cfg.d_model, cfg.n_layer, cfg.n_head, cfg.d_mlp, cfg.ln_eps)
+    return ctx, ref, w
+
+
+def assert_params_equal(ctx, ref):
+    got, _ = ctx.params()
+    for t, (a, b) in enumerate(zip(got, ref.params)):
+        assert a.tobytes() == b.tobytes(), f"tensor {t} differs"
+
+
+def explicit_steps(ctx, ref, cfg, t0, n, K):
+    accepted = 0
+    for t in range(t0, t0 + n):
+        cands = ctx.propose(t, K)
+        L_t, rc, rl, chosen = omca.evaluate(ref, t, K, cfg.seed_stream, cfg.stream_tag,
+                                            cfg.delta, "weight", cfg.accept_ties)
+        assert_cands_equal(cands, rc)
+        losses, _ = ctx.eval_losses(cands)
+        check_losses(losses, L_t, rl, cfg.accept_ties)
+        if chosen >= 0:
+            ctx.commit(chosen)
+            ref.commit(rc[chosen], rl[chosen])
+            accepted += 1
+        else:
+            ctx.rollback()
+    return accepted
+
+
+def replay(ref, cfg, t0, chosen, dloss, K):
+    for n in range(len(chosen)):
+        t = t0 + n
+        L_t, rc, rl, orc = omca.evaluate(ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
+                                         "weight", cfg.accept_ties)
+        for k in range(K):
+            g = L_t + dloss[n, k]
+            assert abs(g - rl[k]) <= REL_TOL * abs(rl[k]), (t, k, g, rl[k])
+        g = int(chosen[n])
+        if g != orc:
+            m = min(x if x >= 0 else K for x in (g, orc))
+            assert abs(rl[m] - L_t) < TIE, (t, m, g, orc, rl[m] - L_t)
+        if g >= 0:
+            ref.commit(rc[g], rl[g])
+
+
+def small_cfg(**kw):
+    base = dict(name="tf_small", ctx=32, d_model=64, n_layer=2, n_head=2, d_mlp=128, n_seq=4,
+                K=8)
+    base.update(kw)
+    return CONFIGS["transformer"].scaled(**base)
+
+
+def test_transformer_small_explicit_and_device(mca):
+    cfg = small_cfg()
+    banner(f"{cfg.name} ctx={cfg.ctx} d={cfg.d_model} heads={cfg.n_head}")
+    ctx, ref, _ = make_pair(mca, cfg, k_max=8)
+    L, t = ctx.loss()
+    assert t == 0 and abs(L - ref.loss()) <= REL_TOL * ref.loss(), (L, ref.loss())
+    acc = explicit_steps(ctx, ref, cfg, 0, 25, 8)
+    assert acc > 3
+    assert_params_equal(ctx, ref)
+    ctx.set_step(25)
+    st, ch, dl = ctx.run_steps(25, 8, trace=True, trace_dloss=True)
+    assert st.steps == 25 and st.evaluated == 25 * 8
+    replay(ref, cfg, 25, ch, dl, 8)
+    assert_params_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss_of(ref.params)) <= REL_TOL * L
+    ctx.close()
+
+
+def test_position_embedding_change_is_causal(mca):
+    """A change of pos_emb[p] leaves the loss of every position before p
+    bit-identical, and moves the loss by what the oracle says."""
+    cfg = small_cfg(name="tf_causal", n_seq=3)
+    ctx, ref, _ = make_pair(mca, cfg, k_max=1)
+    before = ctx.sample_losses().reshape(cfg.n_seq, cfg.ctx)
+    p, c = 11, 5
+    cand = np.zeros(1, dtype=mca.CAND_DTYPE)
+    cand[0]["layer"], cand[0]["j"], cand[0]["i"] = 1, p, c
+    cand[0]["flat"] = cfg.vocab * cfg.d_model + p * cfg.d_model + c
+    cand[0]["d"] = np.float32(0.05)
+    losses, _ = ctx.eval_losses(cand)
+    from oracle.philox import Candidate
+    oc = Candidate(int(cand[0]["flat"]), 1, p, c, np.float32(0.05), 0)
+    exp = ref.eval(oc)
+    assert abs(losses[0] - exp) <= REL_TOL * exp
+    ctx.commit(0)
+    after = ctx.sample_losses().reshape(cfg.n_seq, cfg.ctx)
+    assert after[:, :p].tobytes() == before[:, :p].tobytes()
+    assert not np.array_equal(after[:, p:], before[:, p:])
+    ctx.close()
+
+
+def test_transformer_rejects_unsupported(mca):
+    cfg = small_cfg()
+    w = transformer_workload(cfg)
+    for kw, code in [(dict(d_model=48), "MCA_EUNSUPPORTED"), (dict(ctx=256), "MCA_EUNSUPPORTED")]:
+        args = dict(vocab=cfg.vocab, ctx=cfg.ctx, d_model=cfg.d_model, n_block=cfg.n_layer,
+                    n_head=cfg.n_head, d_mlp=cfg.d_mlp)
+        args.update(kw)
+        d = mca.transformer_desc(**args, delta=cfg.delta)
+        with pytest.raises(mca.MCAError) as e:
+            mca.mca_plan(d, cfg.n_seq * args["ctx"], 4)
+        assert code in str(e.value)
+    bad = w["tokens"].copy()
+    bad[0, 0] = cfg.vocab
+    desc = mca.transformer_desc(cfg.vocab, cfg.ctx, cfg.d_model, cfg.n_layer, cfg.n_head,
+                                cfg.d_mlp, delta=cfg.delta)
+    with pytest.raises(mca.MCAError) as e:
+        mca.TransformerContext(desc, w["params"], bad, w["targets"], k_max=2)
+    assert "MCA_EINVAL" in str(e.value)
+
+
+def test_full_transformer_workload(mca):
+    """vocab 65, ctx 128, d 128, 4 heads, MLP 512, 2 blocks, 64 sequences, K=16:
+    init loss, one explicit step against the oracle, one device step replayed."""
+    cfg = CONFIGS["transformer"]
+    banner("transformer char-LM 64x128 K=16")
+    ctx, ref, _ = make_pair(mca, cfg, k_max=16)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    explicit_steps(ctx, ref, cfg, 0, 1, 16)
+    assert_params_equal(ctx, ref)
+    ctx.set_step(1)
+    st, ch, dl = ctx.run_steps(1, 16, trace=True, trace_dloss=True)
+    replay(ref, cfg, 1, ch, dl, 16)
+    assert_params_equal(ctx, ref)
+    ctx.close()
