@@ -75,6 +75,32 @@ def candidate_flops(cfg, w, cands, params):
     return total
 
 
+def transformer_flops(cfg, cands):
+    """Algorithmic flops of one step's Transformer candidates: each runs the
+    forward pass from the stage of its tensor (an embedding change: every
+    block; a change in block b: blocks b..; the final LayerNorm or output
+    layer: only the output layer).  Per block: Q, K, V and output projections
+    (4 x 2 N d^2), causal attention (scores and weighted values over the
+    T (T+1) / 2 visible pairs per sequence and head), and the MLP (2 x 2 N d m);
+    the output layer 2 N d V."""
+    N, D, M, V = cfg.n_samples, cfg.d_model, cfg.d_mlp, cfg.vocab
+    T, H, S, NB = cfg.ctx, cfg.n_head, cfg.n_seq, cfg.n_layer
+    attn = 2 * 2 * S * H * (T * (T + 1) / 2) * (D // H)
+    block = 4 * 2 * N * D * D + attn + 2 * 2 * N * D * M
+    out = 2 * N * D * V
+    total = 0.0
+    for c in cands:
+        t = int(c["layer"])
+        if t < 2:
+            nb = NB
+        elif t < 2 + 16 * NB:
+            nb = NB - (t - 2) // 16
+        else:
+            nb = 0
+        total += nb * block + out
+    return total
+
+
 def measured_traffic(kernel: str, workload: str, steps: int):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
     summary (calibrated against a plain copy), or None when the kernel source
@@ -92,17 +118,37 @@ def measured_traffic(kernel: str, workload: str, steps: int):
     return rec["hbm_bytes_per_step"] * steps
 
 
+def workload_config(cfg):
+    if cfg.kind == "transformer":
+        return {"workload": (f"{cfg.name} decoder vocab {cfg.vocab}, ctx {cfg.ctx}, "
+                             f"d {cfg.d_model}, {cfg.n_head} heads, MLP {cfg.d_mlp}, "
+                             f"{cfg.n_layer} blocks, {cfg.n_seq} sequences, K={cfg.K}, "
+                             f"delta={cfg.delta}"),
+                "K": cfg.K, "n_samples": cfg.n_samples, "n_params": cfg.n_params}
+    return {"workload": (f"{cfg.name} MLP {'-'.join(map(str, cfg.widths))} {cfg.act}, "
+                         f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}"),
+            "K": cfg.K, "n_samples": cfg.n_samples, "widths": list(cfg.widths),
+            "n_params": cfg.n_params}
+
+
 def cpu_baseline(cfg, w, seconds: float):
-    """The fp64 oracle (incremental mode, all K candidates scored per step, as
-    the device does) on the host cores, for about `seconds` of work."""
+    """The fp64 oracle (incremental mode for MLPs, full recomputation for the
+    Transformer; all K candidates scored per step, as the device does) on the
+    host cores, for about `seconds` of work."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import mca as omca
-    from oracle.mlp import IncrementalMLP, MLPState
     t0 = time.perf_counter()
-    ref = IncrementalMLP(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"],
-                         cfg.act, cfg.gamma)
+    if cfg.kind == "transformer":
+        from oracle.transformer import TransformerModel
+        ref = TransformerModel(w["params"], w["tokens"], w["targets"], cfg.vocab, cfg.ctx,
+                               cfg.d_model, cfg.n_layer, cfg.n_head, cfg.d_mlp, cfg.ln_eps)
+        ref.loss()
+    else:
+        from oracle.mlp import IncrementalMLP, MLPState
+        ref = IncrementalMLP(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"],
+                             cfg.act, cfg.gamma)
     t_init = time.perf_counter() - t0
     n_steps = 0
     evals = 0
@@ -110,18 +156,19 @@ def cpu_baseline(cfg, w, seconds: float):
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         rec = omca.step(ref, n_steps, cfg.K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-                        cfg.layer_pick, cfg.accept_ties, scan_all=True)
+                        getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, scan_all=True)
         n_steps += 1
         evals += len(rec.losses)
         acc += rec.chosen >= 0
     el = time.perf_counter() - t0
     blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
+    mode = "full-recompute" if cfg.kind == "transformer" else "incremental"
     return {"value": evals / el, "unit": "candidate evals/s", "cores": 1,
             "kind": "oracle",
-            "sample": (f"fp64 incremental oracle, first {n_steps} steps x K={cfg.K} of the "
+            "sample": (f"fp64 {mode} oracle, first {n_steps} steps x K={cfg.K} of the "
                        f"same workload from the same seeded init ({el:.1f} s; numpy "
-                       f"element-wise work on one thread, BLAS threads {blas} used only "
-                       f"by its {t_init:.1f} s forward pass, not timed)"),
+                       f"element-wise work on one thread, BLAS threads {blas} for its "
+                       f"matrix products; {t_init:.1f} s setup not timed)"),
             "accepted_per_s": acc / el}
 
 
@@ -164,15 +211,23 @@ def main():
     import torch
 
     from paper_2607_08406_amd import mca
-    from workloads import CONFIGS, mlp_workload
+    from workloads import CONFIGS, mlp_workload, transformer_workload
 
     cfg = CONFIGS[args.workload]
-    w = mlp_workload(cfg)
-    desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
-                        ternary_scales=w["scales"], pick=cfg.layer_pick,
-                        accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
-                        stream_tag=cfg.stream_tag)
-    ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=cfg.K, codes=w["codes"])
+    if cfg.kind == "transformer":
+        w = transformer_workload(cfg)
+        desc = mca.transformer_desc(cfg.vocab, cfg.ctx, cfg.d_model, cfg.n_layer, cfg.n_head,
+                                    cfg.d_mlp, delta=cfg.delta, ln_eps=cfg.ln_eps,
+                                    accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                                    stream_tag=cfg.stream_tag)
+        ctx = mca.TransformerContext(desc, w["params"], w["tokens"], w["targets"], k_max=cfg.K)
+    else:
+        w = mlp_workload(cfg)
+        desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
+                            ternary_scales=w["scales"], pick=cfg.layer_pick,
+                            accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                            stream_tag=cfg.stream_tag)
+        ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=cfg.K, codes=w["codes"])
     if args.tile:
         ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
     if args.per_phase:
@@ -197,7 +252,18 @@ def main():
     dominant = mca.PHASES.index("step_loop" if loop else "eval")
     n_launch = max(int(launches[dominant]), 1)
     avg_s = ms[dominant] / 1e3 / n_launch
-    if cfg.n_layers <= 2:
+    if cfg.kind == "transformer":
+        t_first = st.next_step - args.steps
+        flops = [transformer_flops(cfg, ctx.propose(t_first + n, cfg.K))
+                 for n in range(0, args.steps, max(args.steps // 50, 1))]
+        per_step = float(np.mean(flops))
+        achieved = per_step / avg_s / 1e12
+        roof = {"bound": "mfma", "kernel": "eval phase (k_tf_gemm dominant)",
+                "achieved": achieved, "peak": MFMA_FP32_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
+                "flops_per_launch": per_step, "avg_launch_us": avg_s * 1e6,
+                "launches": int(launches[dominant])}
+    elif cfg.n_layers <= 2:
         kernel = "k_step_loop" if loop else "k_eval_column"
         # one loop launch covers all timed steps; one eval launch covers one step
         bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
@@ -239,10 +305,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": (f"{cfg.name} MLP {'-'.join(map(str, cfg.widths))} {cfg.act}, "
-                                f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}"),
-                   "K": cfg.K, "n_samples": cfg.n_samples, "widths": list(cfg.widths),
-                   "n_params": cfg.n_params},
+        "config": workload_config(cfg),
         "roofline": roof,
         "final_loss": st.loss,
     }

@@ -132,7 +132,8 @@ std::string tf_check_desc(const mca_net_desc* d, int64_t n_samples, int32_t k_ma
   if (d->pick != MCA_PICK_WEIGHT) return "Transformer nets draw uniformly over all parameters only";
   if (d->d_model != mca::kTfHeadDim * d->n_head) return "d_model must be 32 * n_head";
   if (d->d_model > 256) return "d_model must be at most 256";
-  if (d->d_mlp % 16 != 0) return "d_mlp must be a multiple of 16";
+  if (d->d_mlp % 32 != 0) return "d_mlp must be a multiple of 32";
+  if (d->vocab > mca::kTfMaxVocab) return "vocab must be at most 128";
   if (d->ctx > mca::kTfMaxCtx) return "ctx must be at most 128";
   if (d->n_block > mca::kTfMaxBlocks) return "at most 8 blocks";
   *code = MCA_OK;

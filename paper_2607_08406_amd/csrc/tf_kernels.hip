@@ -27,10 +27,16 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGemmThreads = 256;  // 4 waves, a 64 x 64 output tile
-constexpr int kLnThreads = 256;    // a wave per row
+constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 64 output tile
+constexpr int kGemmRows = 128;     // rows (positions) per block, 32 per wave
+constexpr int kGemmCols = 64;      // output columns per block
+constexpr int kChunkK = 32;        // reduction chunk staged in LDS
+constexpr int kLnThreads = 256;    // a wave per row, kLnRows rows per wave
+constexpr int kLnRows = 16;
 constexpr int kLossThreads = 256;
 constexpr int kCopyThreads = 256;
+constexpr int kCopyChunk = 4096;   // floats of a private tensor copy per block
+constexpr int kEmbedPer = 4;       // embedding elements per thread
 
 __device__ __forceinline__ int64_t fc_width(const TfDev* tf) {
   return tf->M > tf->V ? tf->M : tf->V;
@@ -95,49 +101,59 @@ __global__ void k_tf_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
   aux[k] = a;
 }
 
-// Block k: the candidate's tensor table, its first stage, and the patched
-// private copy of its tensor.  identity: slot 0 with the committed tensors.
+// Blocks (x, k): candidate k's patched private copy of its tensor, a chunk of
+// kCopyChunk floats per block; block (0, k) also writes the tensor table and
+// the candidate's first stage.  identity: slot 0 with the committed tensors.
 __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const mca_cand* cands,
                                                           const Aux* aux, int identity) {
-  const int k = blockIdx.x;
+  const int k = blockIdx.y;
   const int nt = tf->n_tensors;
   float** tab = tf->table + (int64_t)k * nt;
-  for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = tf->param[t];
   if (identity) {
-    if (threadIdx.x == 0) tf->start[k] = 0;
+    if (blockIdx.x == 0) {
+      for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = tf->param[t];
+      if (threadIdx.x == 0) tf->start[k] = 0;
+    }
     return;
   }
   const mca_cand c = cands[k];
   const Aux a = aux[k];
-  if (!a.valid) {
-    if (threadIdx.x == 0) tf->start[k] = tf->NB + 2;
-    return;
-  }
   const int l = c.layer;
-  const int64_t n = (int64_t)tf->rows[l] * tf->cols[l];
   float* cp = tf->scopy + (int64_t)k * tf->copy_stride;
-  const float* src = tf->param[l];
-  for (int64_t e = threadIdx.x; e < n; e += blockDim.x) cp[e] = src[e];
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    cp[(int64_t)c.j * tf->cols[l] + c.i] = a.w_new;
-    tab[l] = cp;
-    tf->start[k] = tf_stage(l, tf->NB);
+  if (blockIdx.x == 0) {
+    for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = (t == l && a.valid) ? cp : tf->param[t];
+    if (threadIdx.x == 0) tf->start[k] = a.valid ? tf_stage(l, tf->NB) : tf->NB + 2;
   }
+  if (!a.valid) return;
+  const int64_t n = (int64_t)tf->rows[l] * tf->cols[l];
+  const int64_t at = (int64_t)c.j * tf->cols[l] + c.i;
+  const float* src = tf->param[l];
+  const int64_t e0 = (int64_t)blockIdx.x * kCopyChunk;
+  for (int64_t e = e0 + threadIdx.x; e < n && e < e0 + kCopyChunk; e += blockDim.x)
+    cp[e] = (e == at) ? a.w_new : src[e];
 }
 
 // x_0 = tok_emb[token] + pos_emb[position] for the candidates of stage 0
 __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf) {
   const int k = blockIdx.y;
   if (tf->start[k] != 0) return;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int D = tf->D;
-  if (e >= tf->N * D) return;
-  const int64_t n = e / D;
-  const int c = (int)(e - n * D);
+  const int64_t ND = tf->N * D;
   float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
-  const int pos = (int)(n % tf->T);
-  slot_x(tf, k, 0)[e] = tab[0][(int64_t)tf->tok[n] * D + c] + tab[1][(int64_t)pos * D + c];
+  const float* te = tab[0];
+  const float* pe = tab[1];
+  float* x0 = slot_x(tf, k, 0);
+  const int64_t e0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kEmbedPer;
+#pragma unroll
+  for (int u = 0; u < kEmbedPer; ++u) {
+    const int64_t e = e0 + u;
+    if (e < ND) {
+      const int64_t n = e / D;
+      const int c = (int)(e - n * D);
+      const int pos = (int)(n % tf->T);
+      x0[e] = te[(int64_t)tf->tok[n] * D + c] + pe[(int64_t)pos * D + c];
+    }
+  }
 }
 
 // LayerNorm (biased variance, eps inside the root, affine), a wave per row.
@@ -148,8 +164,6 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
   if (tf->start[k] > stage) return;
   const int D = tf->D;
   const int64_t N = tf->N, ND = N * D;
-  const int64_t n = (int64_t)blockIdx.x * (kLnThreads / 64) + (threadIdx.x >> 6);
-  if (n >= N) return;
   const int lane = threadIdx.x & 63;
   float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
   const int tb = 2 + kBlockTensors * (stage - 1);
@@ -168,42 +182,57 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
     g = tab[tf->n_tensors - 4];
     bb = tab[tf->n_tensors - 3];
   }
-  in += n * D;
+  const float eps = tf->eps;
+  float* const outk = tf->sln + k * ND;
   constexpr int kMaxPer = 4;  // D <= 256
-  float v[kMaxPer];
-  float s = 0.f;
+  float gv[kMaxPer], bv[kMaxPer];
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
     const int c = lane + 64 * u;
-    v[u] = (c < D) ? in[c] : 0.f;
-    s += v[u];
+    gv[u] = (c < D) ? g[c] : 0.f;
+    bv[u] = (c < D) ? bb[c] : 0.f;
   }
+  const int64_t r0 = ((int64_t)blockIdx.x * (kLnThreads / 64) + (threadIdx.x >> 6)) * kLnRows;
+  for (int64_t n = r0; n < r0 + kLnRows && n < N; ++n) {
+    const float* inr = in + n * D;
+    float v[kMaxPer];
+    float s = 0.f;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-  const float mean = s / (float)D;
-  float q = 0.f;
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int c = lane + 64 * u;
+      v[u] = (c < D) ? inr[c] : 0.f;
+      s += v[u];
+    }
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    const float dv = (c < D) ? v[u] - mean : 0.f;
-    q += dv * dv;
-  }
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    const float mean = s / (float)D;
+    float q = 0.f;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  const float rstd = 1.0f / sqrtf(q / (float)D + tf->eps);
-  float* out = tf->sln + k * ND + n * D;
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int c = lane + 64 * u;
+      const float dv = (c < D) ? v[u] - mean : 0.f;
+      q += dv * dv;
+    }
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    if (c < D) out[c] = (v[u] - mean) * rstd * g[c] + bb[c];
+    for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+    const float rstd = 1.0f / sqrtf(q / (float)D + eps);
+    float* out = outk + n * D;
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int c = lane + 64 * u;
+      if (c < D) out[c] = (v[u] - mean) * rstd * gv[u] + bv[u];
+    }
   }
 }
 
 // Y = X W^T + b with an epilogue, for the candidates active in `stage`.
-// A 64 x 64 output tile per block: wave w takes rows 16w.., as four 16 x 16
-// MFMA tiles.  The reduction dimension runs in blocks of 16; lane group q
-// holds k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn, so each
-// lane loads its operands as float4.  Requires Kd % 16 == 0.
+// A 128 x 64 output tile per block: wave w takes rows 32w.. as two by four
+// 16 x 16 MFMA tiles.  The reduction dimension runs in chunks of 32 staged in
+// LDS (double-buffered: the next chunk's global loads are in flight while the
+// current one is multiplied).  Inside a chunk, k runs in blocks of 16; lane
+// group q holds k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn,
+// so each lane reads its operands as float4.  Rows beyond the matrix are
+// clamped on load and dropped on store.  Requires Kd % 32 == 0.
 __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int stage, int role) {
   const int k = blockIdx.z;
   if (tf->start[k] > stage) return;
@@ -242,138 +271,267 @@ __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int s
       Nout = V;
       break;
   }
-  const int n0 = blockIdx.y * 64;
+  const int n0 = blockIdx.y * kGemmCols;
   if (n0 >= Nout) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, li = lane & 15;
-  const int64_t m0 = (int64_t)blockIdx.x * 64;
-  const int64_t arow = m0 + 16 * wave + li;
-  const bool aok = arow < N;
-  const float* Xr = X + arow * ldX + 4 * q;
-  const float* Wr[4];
-  bool bok[4];
+  __shared__ __attribute__((aligned(16))) float As[2][kGemmRows][kChunkK + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kGemmCols][kChunkK + 4];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
+  const int64_t m0 = (int64_t)blockIdx.x * kGemmRows;
+  // staging: thread tid loads float4 number tid + 256 u of the A chunk
+  // (128 rows x 8 float4) and of the B chunk (64 rows x 8 float4)
+  constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 4
+  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 2
+  const float* ga[kA4];
+  const float* gb[kB4];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) {
-    const int n = n0 + 16 * cb + li;
-    bok[cb] = n < Nout;
-    Wr[cb] = W + (int64_t)(bok[cb] ? n : 0) * Kd + 4 * q;
+  for (int u = 0; u < kA4; ++u) {
+    const int e = tid + kGemmThreads * u;
+    const int64_t r = m0 + e / (kChunkK / 4);
+    ga[u] = X + (r < N ? r : N - 1) * ldX + 4 * (e % (kChunkK / 4));
   }
+#pragma unroll
+  for (int u = 0; u < kB4; ++u) {
+    const int e = tid + kGemmThreads * u;
+    const int n = n0 + e / (kChunkK / 4);
+    gb[u] = W + (int64_t)(n < Nout ? n : Nout - 1) * Kd + 4 * (e % (kChunkK / 4));
+  }
+  floatx4 ra[kA4], rb[kB4];
+  auto fetch = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kA4; ++u) ra[u] = gload(reinterpret_cast<const floatx4*>(ga[u] + kChunkK * c));
+#pragma unroll
+    for (int u = 0; u < kB4; ++u) rb[u] = gload(reinterpret_cast<const floatx4*>(gb[u] + kChunkK * c));
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < kA4; ++u) {
+      const int e = tid + kGemmThreads * u;
+      *reinterpret_cast<floatx4*>(&As[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = ra[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kB4; ++u) {
+      const int e = tid + kGemmThreads * u;
+      *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = rb[u];
+    }
+  };
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-  floatx4 acc[4];
+  floatx4 acc[2][4];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) acc[cb] = zero;
-  floatx4 a = aok ? *reinterpret_cast<const floatx4*>(Xr) : zero;
-  floatx4 bv[4];
+  for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) bv[cb] = bok[cb] ? *reinterpret_cast<const floatx4*>(Wr[cb]) : zero;
-  const int nkb = Kd / 16;
-  for (int kb = 0; kb < nkb; ++kb) {
-    floatx4 an = zero, bn[4] = {zero, zero, zero, zero};
-    if (kb + 1 < nkb) {
-      an = aok ? *reinterpret_cast<const floatx4*>(Xr + 16 * (kb + 1)) : zero;
+    for (int cb = 0; cb < 4; ++cb) acc[sb][cb] = zero;
+  const int nc = Kd / kChunkK;
+  fetch(0);
+  store(0);
+  __syncthreads();
+  for (int c = 0; c < nc; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nc) fetch(c + 1);
+#pragma unroll
+    for (int kb = 0; kb < kChunkK / 16; ++kb) {
+      floatx4 a[2], bv[4];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+        a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][32 * wave + 16 * sb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
-        bn[cb] = bok[cb] ? *reinterpret_cast<const floatx4*>(Wr[cb] + 16 * (kb + 1)) : zero;
+        bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][16 * cb + li][16 * kb + 4 * q]);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb)
+            acc[sb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sb][t], bv[cb][t], acc[sb][cb], 0, 0, 0);
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t], bv[cb][t], acc[cb], 0, 0, 0);
-    a = an;
-#pragma unroll
-    for (int cb = 0; cb < 4; ++cb) bv[cb] = bn[cb];
+    if (c + 1 < nc) store(buf ^ 1);
+    __syncthreads();
   }
-  // D layout: lane (q, li), element v -> row 16 w + 4 q + v, column 16 cb + li
+  // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb)
+  for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t m = m0 + 16 * wave + 4 * q + v;
-      const int n = n0 + 16 * cb + li;
-      if (m < N && n < Nout) {
-        float y = acc[cb][v] + bias[n];
-        if (epi == 1) y = gelu(y);
-        if (epi == 2) y = R[m * D + n] + y;
-        Y[m * ldY + n] = y;
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t m = m0 + 32 * wave + 16 * sb + 4 * q + v;
+        const int n = n0 + 16 * cb + li;
+        if (m < N && n < Nout) {
+          float y = acc[sb][cb][v] + bias[n];
+          if (epi == 1) y = gelu(y);
+          if (epi == 2) y = R[m * D + n] + y;
+          Y[m * ldY + n] = y;
+        }
       }
-    }
 }
 
-// Causal softmax attention, scale 1/sqrt(32): block (sequence, head) of one
-// candidate, a thread per query position.
-__global__ __launch_bounds__(kTfMaxCtx) void k_tf_attn(const TfDev* tf, int stage) {
+// Causal softmax attention, scale 1/sqrt(32), on the matrix cores: a block
+// of 4 waves per (sequence, head) of one candidate.  Q, K and V of the
+// sequence and head sit in LDS (rows padded).  Row block rb (16 queries)
+// takes key blocks 0..rb: the scores S = Q K^T tile by tile (16 x 16, two
+// k-blocks of 16 over the head dimension, operands read as float4), the row
+// maximum and the sum of exponentials by a fixed butterfly over the 16 lanes
+// that hold a row, then O = P V with P re-laid out through LDS into the
+// A-operand layout.  Wave w takes row blocks w and 7-w (T = 128: every wave
+// walks 9 tiles); keys after the query are masked.
+__global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage) {
   const int k = blockIdx.y;
   if (tf->start[k] > stage) return;
-  __shared__ float Ks[kTfMaxCtx][kTfHeadDim + 1];
-  __shared__ float Vs[kTfMaxCtx][kTfHeadDim + 1];
+  constexpr int kS = kTfHeadDim + 4;  // padded row
+  __shared__ __attribute__((aligned(16))) float Qs[kTfMaxCtx][kS];
+  __shared__ __attribute__((aligned(16))) float Ks[kTfMaxCtx][kS];
+  __shared__ __attribute__((aligned(16))) float Vs[kTfMaxCtx][kS];
+  __shared__ float Ps[4][16][17];
   const int T = tf->T, D = tf->D, H = tf->H;
   const int s = blockIdx.x / H, h = blockIdx.x - (blockIdx.x / H) * H;
-  const int t = threadIdx.x;
   const int64_t ND = tf->N * D;
   const float* base = tf->sqkv + 3 * k * ND + (int64_t)s * T * 3 * D + h * kTfHeadDim;
-  float qv[kTfHeadDim];
-  if (t < T) {
-    const float* row = base + (int64_t)t * 3 * D;
+  {
+    // 128 rows x 8 float4 per tensor: four float4 of each per thread, every
+    // load issued before the LDS stores
+    constexpr int kPer = kTfMaxCtx * kTfHeadDim / 4 / 256;
+    floatx4 rq[kPer], rk[kPer], rv[kPer];
 #pragma unroll
-    for (int c = 0; c < kTfHeadDim; ++c) {
-      qv[c] = row[c];
-      Ks[t][c] = row[D + c];
-      Vs[t][c] = row[2 * D + c];
+    for (int u = 0; u < kPer; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int t = e / (kTfHeadDim / 4), c4 = e - t * (kTfHeadDim / 4);
+      const bool ok = t < T;
+      const float* row = base + (int64_t)(ok ? t : 0) * 3 * D + 4 * c4;
+      const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+      rq[u] = ok ? gload(reinterpret_cast<const floatx4*>(row)) : z;
+      rk[u] = ok ? gload(reinterpret_cast<const floatx4*>(row + D)) : z;
+      rv[u] = ok ? gload(reinterpret_cast<const floatx4*>(row + 2 * D)) : z;
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int t = e / (kTfHeadDim / 4), c4 = e - t * (kTfHeadDim / 4);
+      *reinterpret_cast<floatx4*>(&Qs[t][4 * c4]) = rq[u];
+      *reinterpret_cast<floatx4*>(&Ks[t][4 * c4]) = rk[u];
+      *reinterpret_cast<floatx4*>(&Vs[t][4 * c4]) = rv[u];
     }
   }
   __syncthreads();
-  if (t >= T) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, q = lane >> 4, li = lane & 15;
+  const int nrb = (T + 15) / 16;
   const float scale = 0.17677669529663687f;  // 1/sqrt(32)
-  float mx = -__builtin_huge_valf();
-  for (int j = 0; j <= t; ++j) {
-    float dot = 0.f;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  float* outb = tf->satt + k * ND + (int64_t)s * T * D + h * kTfHeadDim;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int rb = (pass == 0) ? wave : 7 - wave;
+    if (rb >= nrb || (pass == 1 && rb == wave)) continue;
+    // scores of row block rb against key blocks 0..rb
+    floatx4 sc[kTfMaxCtx / 16];
+    floatx4 qa[2];
 #pragma unroll
-    for (int c = 0; c < kTfHeadDim; ++c) dot = fmaf(qv[c], Ks[j][c], dot);
-    mx = fmaxf(mx, dot * scale);
+    for (int kb = 0; kb < 2; ++kb)
+      qa[kb] = *reinterpret_cast<const floatx4*>(&Qs[16 * rb + li][16 * kb + 4 * q]);
+#pragma unroll
+    for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
+      sc[cb] = zero;
+      if (cb <= rb) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const floatx4 kk = *reinterpret_cast<const floatx4*>(&Ks[16 * cb + li][16 * kb + 4 * q]);
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            sc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[kb][t], kk[t], sc[cb], 0, 0, 0);
+        }
+      }
+    }
+    // lane (q, li) holds scores of rows 16 rb + 4 q + v, keys 16 cb + li
+    float mx[4], sm[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = 16 * rb + 4 * q + v;
+      float m = -__builtin_huge_valf();
+#pragma unroll
+      for (int cb = 0; cb < kTfMaxCtx / 16; ++cb)
+        if (cb <= rb && 16 * cb + li <= row) m = fmaxf(m, sc[cb][v] * scale);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+      mx[v] = m;
+      float sum = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
+        const float p = (cb <= rb && 16 * cb + li <= row) ? fast_exp(sc[cb][v] * scale - m) : 0.f;
+        sc[cb][v] = p;
+        sum += p;
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, 64);
+      sm[v] = sum;
+    }
+    // O = P V: per key block, P through LDS into the A layout (row li, key 4 t + q)
+    floatx4 oc[2] = {zero, zero};
+#pragma unroll
+    for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
+      if (cb > rb) break;  // uniform over the wave
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Ps[wave][4 * q + v][li] = sc[cb][v];
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float pa = Ps[wave][li][4 * t + q];
+        const int key = 16 * cb + 4 * t + q;
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+          oc[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[key][16 * db + li], oc[db], 0, 0, 0);
+      }
+      __builtin_amdgcn_wave_barrier();  // every lane read Ps before the next tile rewrites it
+    }
+    // lane (q, li) holds O rows 16 rb + 4 q + v, columns 16 db + li
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = 16 * rb + 4 * q + v;
+      if (row < T) {
+#pragma unroll
+        for (int db = 0; db < 2; ++db) outb[(int64_t)row * D + 16 * db + li] = oc[db][v] / sm[v];
+      }
+    }
   }
-  float sum = 0.f, o[kTfHeadDim];
-#pragma unroll
-  for (int c = 0; c < kTfHeadDim; ++c) o[c] = 0.f;
-  for (int j = 0; j <= t; ++j) {
-    float dot = 0.f;
-#pragma unroll
-    for (int c = 0; c < kTfHeadDim; ++c) dot = fmaf(qv[c], Ks[j][c], dot);
-    const float p = fast_exp(dot * scale - mx);
-    sum += p;
-#pragma unroll
-    for (int c = 0; c < kTfHeadDim; ++c) o[c] = fmaf(p, Vs[j][c], o[c]);
-  }
-  float* out = tf->satt + k * ND + ((int64_t)s * T + t) * D + h * kTfHeadDim;
-#pragma unroll
-  for (int c = 0; c < kTfHeadDim; ++c) out[c] = o[c] / sum;
 }
 
 // Per-position cross-entropy of the candidate's logits, its change against
-// the committed loss, and the block's sum of changes (fixed order).
+// the committed loss, and the block's sum of changes over its 256 positions
+// (in order).  The block's logits are contiguous; they are staged in LDS with
+// coalesced loads and each thread then takes one position (row stride V).
 __global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, float* partial, int nblk) {
-  __shared__ float red[kLossThreads];
+  __shared__ float zl[kLossThreads * kTfMaxVocab];
+  __shared__ float dl[kLossThreads];
   const int k = blockIdx.y;
   const bool active = tf->start[k] <= tf->NB + 1;
-  const int64_t n = (int64_t)blockIdx.x * kLossThreads + threadIdx.x;
   const int V = tf->V;
+  const int64_t n0 = (int64_t)blockIdx.x * kLossThreads;
+  const int64_t nrows = (tf->N - n0 < kLossThreads) ? tf->N - n0 : kLossThreads;
+  if (active) {
+    const float* zk = tf->sfc + k * tf->N * fc_width(tf) + n0 * V;
+    for (int64_t e = threadIdx.x; e < nrows * V; e += kLossThreads) zl[e] = zk[e];
+  }
+  __syncthreads();
+  const int r = threadIdx.x;
   float d = 0.f;
-  if (active && n < tf->N) {
-    const float* z = tf->sfc + k * tf->N * fc_width(tf) + n * V;
+  if (active && r < nrows) {
+    const float* z = zl + r * V;
     float m = z[0];
     for (int v = 1; v < V; ++v) m = fmaxf(m, z[v]);
-    float s = 0.f;
-    for (int v = 0; v < V; ++v) s += fast_exp(z[v] - m);
-    const float ln = (fast_log(s) + m) - z[tf->tgt[n]];
+    float sum = 0.f;
+    for (int v = 0; v < V; ++v) sum += fast_exp(z[v] - m);
+    const int64_t n = n0 + r;
+    const float ln = (fast_log(sum) + m) - z[tf->tgt[n]];
     tf->sell[k * tf->N + n] = ln;
     d = ln - tf->ell[n];
   }
-  red[threadIdx.x] = d;
+  dl[r] = d;
   __syncthreads();
   for (int o = kLossThreads / 2; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    if (threadIdx.x < o) dl[threadIdx.x] += dl[threadIdx.x + o];
     __syncthreads();
   }
-  if (threadIdx.x == 0) partial[(int64_t)k * nblk + blockIdx.x] = red[0];
+  if (threadIdx.x == 0) partial[(int64_t)k * nblk + blockIdx.x] = dl[0];
 }
 
 // The winner's (or slot 0's, fill) residual streams from its first stage on
@@ -443,31 +601,33 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
                           hipStream_t s) {
   const unsigned KK = identity ? 1u : (unsigned)K;
   const int64_t N = h.N;
-  const unsigned mt = (unsigned)((N + 63) / 64);
-  hipLaunchKernelGGL(k_tf_prep, dim3(KK), dim3(kCopyThreads), 0, s, tf, cands, aux,
-                     identity ? 1 : 0);
-  hipLaunchKernelGGL(k_tf_embed, dim3((unsigned)((N * h.D + kCopyThreads - 1) / kCopyThreads), KK),
+  const unsigned mt = (unsigned)((N + kGemmRows - 1) / kGemmRows);
+  hipLaunchKernelGGL(k_tf_prep,
+                     dim3((unsigned)((h.copy_stride + kCopyChunk - 1) / kCopyChunk), KK),
+                     dim3(kCopyThreads), 0, s, tf, cands, aux, identity ? 1 : 0);
+  hipLaunchKernelGGL(k_tf_embed,
+                     dim3((unsigned)((N * h.D + kCopyThreads * kEmbedPer - 1) / (kCopyThreads * kEmbedPer)), KK),
                      dim3(kCopyThreads), 0, s, tf);
-  const dim3 lng((unsigned)((N + kLnThreads / 64 - 1) / (kLnThreads / 64)), KK);
+  const int64_t ln_rows = (int64_t)(kLnThreads / 64) * kLnRows;
+  const dim3 lng((unsigned)((N + ln_rows - 1) / ln_rows), KK);
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 0);
     for (int role : {kGemmQ, kGemmK, kGemmV})
-      hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + 63) / 64), KK), dim3(kGemmThreads),
-                         0, s, tf, stage, role);
-    hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), KK), dim3(kTfMaxCtx), 0, s, tf,
-                       stage);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + 63) / 64), KK), dim3(kGemmThreads), 0,
+      hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK),
+                         dim3(kGemmThreads), 0, s, tf, stage, role);
+    hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), KK), dim3(256), 0, s, tf, stage);
+    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmO);
     hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 1);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.M + 63) / 64), KK), dim3(kGemmThreads), 0,
+    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.M + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmFc);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + 63) / 64), KK), dim3(kGemmThreads), 0,
+    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmProj);
   }
   const int fin = h.NB + 1;
   hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, fin, 2);
-  hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.V + 63) / 64), KK), dim3(kGemmThreads), 0,
+  hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.V + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                      s, tf, fin, (int)kGemmOut);
   hipLaunchKernelGGL(k_tf_ce, dim3((unsigned)nblk, KK), dim3(kLossThreads), 0, s, tf, partial,
                      nblk);

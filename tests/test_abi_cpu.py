@@ -99,7 +99,7 @@ def test_plan_transformer(binding):
     # committed streams x_0..x_2 and 16 slots of activations dominate
     assert b > 16 * 64 * 128 * 4 * (3 * 128 + 128 * 3 + 3 * 128 + 512)
     for kw, code in [(dict(d_model=96), "MCA_EUNSUPPORTED"), (dict(ctx=256), "MCA_EUNSUPPORTED"),
-                     (dict(d_mlp=100), "MCA_EUNSUPPORTED"), (dict(vocab=1), "MCA_EINVAL")]:
+                     (dict(d_mlp=100), "MCA_EUNSUPPORTED"), (dict(vocab=200), "MCA_EUNSUPPORTED"), (dict(vocab=1), "MCA_EINVAL")]:
         args = dict(vocab=65, ctx=128, d_model=128, n_block=2, n_head=4, d_mlp=512)
         args.update(kw)
         dd = binding.transformer_desc(**args, delta=0.02)
