@@ -152,10 +152,12 @@ size_t mca_struct_size(int32_t which);
 
 /* Device workspace bytes for a net, n_samples and at most k_max candidates per
  * step.  Pure: touches no device.  Returns MCA_EINVAL on a bad description and
- * MCA_EUNSUPPORTED for a valid net this build does not run: Transformers,
- * MLPs of three or more layers whose last hidden layer has more than 1024
- * units, and MLPs of four or more layers whose hidden layers are not all 256
- * units wide. */
+ * MCA_EUNSUPPORTED for a valid net this build does not run: MLPs of three or
+ * more layers whose last hidden layer has more than 1024 units, MLPs of four
+ * or more layers whose hidden layers are not all 256 units wide, and
+ * Transformers outside d_model = 32 * n_head <= 256, d_mlp a multiple of 32,
+ * ctx <= 128, vocab <= 128, n_block <= 8, fp32 weights with the uniform
+ * parameter pick. */
 int mca_plan(const mca_net_desc* net, int64_t n_samples, int32_t k_max,
              size_t* workspace_bytes);
 
