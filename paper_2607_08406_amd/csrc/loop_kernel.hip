@@ -163,10 +163,9 @@ __device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, 
 // branches on the candidate's layer (pairs of different candidates share a
 // wave).
 template <int CM>
-__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
-                                           float de, const float* wcol, float ain, float zh,
-                                           const float* zL, float ell, int y, float& zn,
-                                           float (&z)[CM], float& ln) {
+__device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
+                                            float de, const float* wcol, float ain, float zh,
+                                            const float* zL, float& zn, float (&z)[CM]) {
   const bool logit = layer == L - 1;
   // every operand is loaded unconditionally (the LDS rows hold CM entries,
   // zero beyond C) so the loads issue together
@@ -185,8 +184,17 @@ __device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, i
     const float hid = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
     z[cc] = logit ? ((cc == j) ? zn : zc[cc]) : hid;
   }
+  return logit || da != 0.f;  // the logits changed
+}
+
+// The pair's new loss ln; returns its loss change.
+template <int CM>
+__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
+                                           float de, const float* wcol, float ain, float zh,
+                                           const float* zL, float ell, int y, float& ln) {
+  float zn, z[CM];
+  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, z);
   ln = ce_loss<CM>(z, C, y);
-  const bool changed = logit || da != 0.f;
   return changed ? ln - ell : 0.f;
 }
 
@@ -214,6 +222,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
   __shared__ float zh_lds[2][kLoopMaxK][64];
   __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
+  __shared__ float lnp_lds[kLoopMaxK][64];  // each pair's new loss, which a commit reuses
   __shared__ uint16_t list_lds[kLoopMaxK * 64];
   __shared__ int list_n;
   __shared__ LastCommit last[2];     // commits of the last two steps, by step parity
@@ -484,22 +493,30 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     MCA_TILE_PROBE(5);
     __syncthreads();
     MCA_TILE_PROBE(1);
-    // 2a. compact the pairs whose input is non-zero into the work list
+    // 2a. compact the pairs whose input is non-zero into the work list: one
+    // slot reservation per wave for all its candidates
+    {
+      float ainv[KW];
 #pragma unroll
-    for (int q = 0; q < KW; ++q) {
-      const int k = wave + kWaves * q;
-      if (k < K) {
-        const float ain = ain_lds[buf][k][lane];
-        dlp_lds[k][lane] = 0.f;
-        const bool act = live && ain != 0.f;
-        const uint64_t m = __ballot(act);
-        int base = 0;
-        if (lane == 0 && m) base = atomicAdd(&list_n, (int)__popcll(m));
-        base = __shfl(base, 0, 64);
-        if (act) {
-          const int pos = base + (int)__popcll(m & ((1ull << lane) - 1ull));
-          list_lds[pos] = (uint16_t)((k << 6) | lane);
-        }
+      for (int q = 0; q < KW; ++q) ainv[q] = ain_lds[buf][wave + kWaves * q][lane];
+      uint64_t m[KW];
+      int tot = 0;
+#pragma unroll
+      for (int q = 0; q < KW; ++q) {
+        const int k = wave + kWaves * q;
+        if (k < K) dlp_lds[k][lane] = 0.f;
+        m[q] = __ballot(k < K && live && ainv[q] != 0.f);
+        tot += (int)__popcll(m[q]);
+      }
+      int base = 0;
+      if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
+      base = __shfl(base, 0, 64);
+      const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+      for (int q = 0; q < KW; ++q) {
+        if ((m[q] >> lane) & 1ull)
+          list_lds[base + (int)__popcll(m[q] & below)] = (uint16_t)(((wave + kWaves * q) << 6) | lane);
+        base += (int)__popcll(m[q]);
       }
     }
     __syncthreads();
@@ -509,11 +526,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int code = list_lds[e];
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
-      float zn, z[CM], ln;
+      float ln;
       dlp_lds[k][sl] = pair_eval<CM>(L, C, act, gamma, c.layer, c.j, prep_lds[buf][k].de,
                                      wcol_lds[buf][k],
                                      ain_lds[buf][k][sl], zh_lds[buf][k][sl], &zl_lds[sl],
-                                     ell_lds[sl], y_lds[sl], zn, z, ln);
+                                     ell_lds[sl], y_lds[sl], ln);
+      lnp_lds[k][sl] = ln;
     }
     // last step's commit stores land before this step's staging reads HBM
     if (committed) wait_own_memory();
@@ -605,12 +623,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     if (kc >= 0 && wave == 1) {
       const mca_cand c = cands[kc];
       const Prep au = prep_lds[buf][kc];
+      // the same logits the scoring computed; its loss was kept
       const float ain = ain_lds[buf][kc][lane];
       const float z_raw = zh_lds[buf][kc][lane];
-      float zn, z[CM], ln;
-      (void)pair_eval<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
-                          &zl_lds[lane],
-                          ell_lds[lane], y_lds[lane], zn, z, ln);
+      const float ln = lnp_lds[kc][lane];
+      float zn, z[CM];
+      (void)pair_logits<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
+                            &zl_lds[lane], zn, z);
       const bool ch = live && ain != 0.f;
       if (ch) {
         if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
