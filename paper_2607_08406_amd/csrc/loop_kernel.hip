@@ -11,9 +11,9 @@
 // (+inf for a candidate rejected by the weight bound).  The reduction is
 // sharded by candidate: wave w < 4 of reducer workgroup r owns candidate 4r + w,
 // adds its G partial sums in a fixed order (fp64) and publishes the loss
-// change dL_k.  Every tile workgroup reads all K loss changes and takes the
-// same decision itself: the first candidate in stream order that passes the
-// test (Eq. 6).  It then applies the commit to its own tile with the same
+// change dL_k.  Every tile workgroup reads the loss changes of the
+// candidates up to the first that passes the test (Eq. 6) and takes the same
+// decision itself: that candidate.  It then applies the commit to its own tile with the same
 // expressions the evaluation used.  Tile 0 also keeps the committed loss and
 // the counters.  While wave 0 of a tile workgroup waits for the loss changes,
 // the other waves work ahead (the draw needs no state): wave 1 draws the
@@ -38,7 +38,8 @@
 // Cross-workgroup words carry their own step tag, so no separate flag, fence
 // or L2 writeback is needed: a partial sum is one 64-bit word (fp32 value |
 // 32-bit step tag), stored candidate-major so a reducer polls one candidate's
-// G contiguous words; a loss change is one fp64 word whose 16 low
+// G contiguous words, in one of two sets by step parity; a loss change is one
+// fp64 word whose 16 low
 // mantissa bits are replaced by the step tag (2^-36 relative truncation, the
 // same bits for every reader).  They are written and read with relaxed
 // agent-scope atomics, which the compiler emits as coherent (sc1) accesses.
@@ -106,6 +107,32 @@ __device__ __forceinline__ uint64_t pack_dl(double v, uint32_t tag) {
 }
 __device__ __forceinline__ double unpack_dl(uint64_t w) {
   return __longlong_as_double((long long)(w & ~0xFFFFull));
+}
+
+// Sum over the 64 lanes in one fixed order, the same bits in every lane: a
+// butterfly within rows of 16 (DPP on both halves of the double; both lanes of
+// a pair add the same two values, and after the quad steps the mirrored
+// partners hold equal sums), then across the two rows of each half, then the
+// two halves read into scalars and added once.
+template <int kCtrl>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)u, kCtrl, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), kCtrl, 0xF, 0xF, true);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  v += dpp_f64<0xB1>(v);   // quad_perm [1,0,3,2]: lane ^ 1
+  v += dpp_f64<0x4E>(v);   // quad_perm [2,3,0,1]: lane ^ 2
+  v += dpp_f64<0x141>(v);  // row_half_mirror: lane 7 - i within eight
+  v += dpp_f64<0x140>(v);  // row_mirror: lane 15 - i within sixteen
+  v += __shfl_xor(v, 16, 64);
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint64_t a0 = ((uint64_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 0) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 0);
+  const uint64_t a1 = ((uint64_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 32) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 32);
+  return __longlong_as_double((long long)a0) + __longlong_as_double((long long)a1);
 }
 
 // Bounded spin helper: returns true when the grid must abort.
@@ -227,7 +254,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ int list_n;
   __shared__ LastCommit last[2];     // commits of the last two steps, by step parity
   __shared__ float zrow_lds[2][64];  // their committed hidden rows of this tile
-  __shared__ double red_lds[kReducerWaves][64];  // reducer lane sums
   __shared__ int dec_k;
   __shared__ int aborted;
 
@@ -248,9 +274,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     if (wave >= kReducerWaves) return;  // no block barrier follows in the reducers
     const int k = (g - G) * kReducerWaves + wave;
     if (k >= K) return;
-    const uint64_t* mine = a.partials + (size_t)k * a.gpad;  // candidate-major: G words
-    double* sums = red_lds[wave];
     for (uint64_t s = 0; s < a.n_steps; ++s) {
+      // candidate-major: G words of step s's set
+      const uint64_t* mine = a.partials + ((s & 1) * (size_t)K + (size_t)k) * a.gpad;
       const uint32_t tag = (uint32_t)(s + 1);
       // lane l adds tiles l, l+64, ... in that order
       uint64_t w[kMaxTilesPerLane];
@@ -279,29 +305,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
       for (int b = 0; b < kMaxTilesPerLane; ++b)
         if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
-      // the 64 lane sums go through LDS (this wave only)
-      sums[lane] = acc;
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // lanes 0-7 add eight lane sums each in order, then every lane adds
-      // those eight in order
-      double s8 = 0.0;
-      if (lane < 8) {
-#pragma unroll
-        for (int r = 0; r < 8; ++r) s8 += sums[lane * 8 + r];
-      }
-      double p8[8];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) p8[r] = __shfl(s8, r, 64);
-      double tot = p8[0];
-#pragma unroll
-      for (int r = 1; r < 8; ++r) tot += p8[r];
+      const double tot = wave_sum_f64(acc);
       const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
       if (lane < kReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
       if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 1);
       if (lane == 0 && s < 256) MCA_PROBE(kProbeRedAll + (int64_t)s * 64 + k);
-      __builtin_amdgcn_wave_barrier();  // lanes 0-7 read every slot before they are rewritten
     }
     return;
   }
@@ -541,7 +549,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     // consecutive samples, then the runs pairwise) and publish the tile's
     // partial sum.  Only wave 0 stores here: a store still in flight would
     // make the staging waves' waits for their own loads wait for it too.
-    uint64_t* part = a.partials + g;  // candidate k's word: part[k * gpad]
+    uint64_t* part = a.partials + (size_t)buf * K * a.gpad + g;  // candidate k: part[k * gpad]
     if (wave == 0 && lane < K) {
       float r0 = 0.f, r1 = 0.f, r2 = 0.f, r3 = 0.f;
 #pragma unroll
@@ -576,9 +584,24 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       uint32_t spins = 0;
       bool ab = false;
       if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 2);
+      // The decision needs the loss changes of candidates 0 .. kc only (kc
+      // the first that passes, or all K when none does, or when every dL is
+      // traced).  Before the set of step s-1 can be overwritten (next step),
+      // every reducer must be done with it: its word carries the tag of step
+      // s-1 or s.
+      const uint32_t t16p = tag16(s + 65534u);  // tag of step s-1
+      const bool need_all = g == 0 && a.tr_dl != nullptr;
+      uint64_t fm = 0, am = 0;
       while (true) {
         if (lane < K && (uint32_t)(d & 0xFFFFu) != t16) d = ld_agent(&dls[lane]);
-        if (__all(lane >= K || (uint32_t)(d & 0xFFFFu) == t16)) break;
+        const uint32_t tg = (uint32_t)(d & 0xFFFFu);
+        const bool fresh = lane >= K || tg == t16;
+        const bool done_prev = fresh || s == 0 || tg == t16p;
+        fm = __ballot(fresh);
+        am = __ballot(lane < K && tg == t16 && accepts(unpack_dl(d), net.ties));
+        const int pre = (~fm) ? (int)__ffsll((unsigned long long)~fm) - 1 : 64;  // first stale
+        const int fa = am ? (int)__ffsll((unsigned long long)am) - 1 : 64;
+        if (__all(done_prev) && (pre >= 64 || (!need_all && fa < pre))) break;
         if ((ab = __any(spin_step(spins, a)))) break;
       }
       if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 3);
@@ -586,8 +609,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       if (g == 0 && lane == 0 && s < 256 && probes) probes[kProbeRedAll + 256 * 64 + (int64_t)s] = spins;
 #endif
       const double v = unpack_dl(d);
-      const uint64_t acc_mask = __ballot(!ab && lane < K && accepts(v, net.ties));
-      const int kc = acc_mask ? (int)__ffsll((unsigned long long)acc_mask) - 1 : -1;
+      const int kc = (!ab && am) ? (int)__ffsll((unsigned long long)am) - 1 : -1;
       if (lane == 0) {
         aborted = ab ? 1 : 0;
         dec_k = ab ? -1 : kc;
@@ -702,7 +724,7 @@ const void* pick_loop(int K, int C) {
 int step_loop_reducers(int K) { return (K + kReducerWaves - 1) / kReducerWaves; }
 
 hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s) {
-  const int64_t words = (int64_t)a.K * a.gpad;
+  const int64_t words = 2 * (int64_t)a.K * a.gpad;
   const int64_t n = words > (int64_t)kReplicas * kLoopMaxK ? words : (int64_t)kReplicas * kLoopMaxK;
   hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sync,
                      a.partials, words, a.dls, a.K);

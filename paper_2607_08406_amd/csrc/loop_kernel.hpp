@@ -23,7 +23,7 @@ struct LoopArgs {
   int gpad;             // words per candidate row of partials: G rounded up to 16
   uint64_t t0;          // first step index
   uint64_t n_steps;     // steps in this launch (< 2^32)
-  uint64_t* partials;   // [K][gpad] tagged per-tile loss-change sums
+  uint64_t* partials;   // [2][K][gpad] tagged per-tile loss-change sums, by step parity
   uint64_t* dls;        // [8][kLoopMaxK] tagged loss changes, 8 replicas
   LoopSync* sync;
   DevState* st;
