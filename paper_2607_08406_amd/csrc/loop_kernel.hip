@@ -192,7 +192,8 @@ __device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, 
 template <int CM>
 __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
                                             float de, const float* wcol, float ain, float zh,
-                                            const float* zL, float& zn, float (&z)[CM]) {
+                                            const float* zL, float& zn, float& da,
+                                            float (&z)[CM]) {
   const bool logit = layer == L - 1;
   // every operand is loaded unconditionally (the LDS rows hold CM entries,
   // zero beyond C) so the loads issue together
@@ -202,15 +203,15 @@ __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, 
     zc[cc] = zL[cc * 64];
     wc[cc] = wcol[cc];
   }
-  const float zj = zL[(logit ? j : 0) * 64];
-  const float zb = logit ? zj : zh;
-  zn = zb + de * ain;
-  const float da = act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
+  const float zb = logit ? zL[j * 64] : zh;
+  const float dz = de * ain;
+  zn = zb + dz;
+  // A logit-layer candidate's staged column is one-hot at its logit j, which
+  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
+  // exactly, so one expression serves both kinds of candidate.
+  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
 #pragma unroll
-  for (int cc = 0; cc < CM; ++cc) {
-    const float hid = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
-    z[cc] = logit ? ((cc == j) ? zn : zc[cc]) : hid;
-  }
+  for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
   return logit || da != 0.f;  // the logits changed
 }
 
@@ -219,9 +220,20 @@ template <int CM>
 __device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
                                            float de, const float* wcol, float ain, float zh,
                                            const float* zL, float ell, int y, float& ln) {
-  float zn, z[CM];
-  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, z);
-  ln = ce_loss<CM>(z, C, y);
+  float zn, da, z[CM];
+  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
+  // ce_loss() with the label's logit computed by the same fma instead of
+  // selected from z: the same bits, without a compare per class
+  const float zy = fmaf(da, wcol[y], zL[y * 64]);
+  float m = z[0];
+#pragma unroll
+  for (int c = 1; c < CM; ++c)
+    if (c < C) m = fmaxf(m, z[c]);
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < CM; ++c)
+    if (c < C) s += fast_exp(z[c] - m);
+  ln = (fast_log(s) + m) - zy;
   return changed ? ln - ell : 0.f;
 }
 
@@ -245,7 +257,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ int y_lds[64];
   __shared__ mca_cand cand_lds[4][kLoopMaxK];  // draws of steps s .. s+3, by step mod 4
   __shared__ Prep prep_lds[2][kLoopMaxK];       // staged per step parity
-  __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column of a hidden unit
+  __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column (one-hot for a logit weight)
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
   __shared__ float zh_lds[2][kLoopMaxK][64];
   __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
@@ -379,9 +391,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int64_t idx = (int64_t)c.j * (hid ? nin_hid : nin_log) + c.i;
       w_reg = gload(hid ? &a.net.W[0][idx] : &w_log[idx]);
       code_reg = ternary ? (int)gload(hid ? &a.net.codes[0][idx] : &c_log[idx]) : 0;
+      // a logit-layer candidate's column is one-hot at its logit
 #pragma unroll
       for (int cc = 0; cc < CM; ++cc)
-        col_reg[cc] = (hid && cc < C) ? gload(&w_log[(int64_t)cc * nh + c.j]) : 0.f;
+        col_reg[cc] = hid ? ((cc < C) ? gload(&w_log[(int64_t)cc * nh + c.j]) : 0.f)
+                          : ((cc == c.j) ? 1.f : 0.f);
     }
   };
   // slot: the commit applied while landing
@@ -649,9 +663,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const float ain = ain_lds[buf][kc][lane];
       const float z_raw = zh_lds[buf][kc][lane];
       const float ln = lnp_lds[kc][lane];
-      float zn, z[CM];
+      float zn, da, z[CM];
       (void)pair_logits<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
-                            &zl_lds[lane], zn, z);
+                            &zl_lds[lane], zn, da, z);
       const bool ch = live && ain != 0.f;
       if (ch) {
         if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
