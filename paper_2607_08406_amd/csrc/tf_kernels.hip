@@ -27,9 +27,9 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 64 output tile
-constexpr int kGemmRows = 128;     // rows (positions) per block, 32 per wave
-constexpr int kGemmCols = 64;      // output columns per block
+constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 per wave
+constexpr int kGemmRows = 128;     // rows (positions) per block
+constexpr int kGemmCols = 128;     // output columns per block
 constexpr int kChunkK = 32;        // reduction chunk staged in LDS
 constexpr int kLnThreads = 256;    // a wave per row, kLnRows rows per wave
 constexpr int kLnRows = 16;
@@ -226,14 +226,17 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
 }
 
 // Y = X W^T + b with an epilogue, for the candidates active in `stage`.
-// A 128 x 64 output tile per block: wave w takes rows 32w.. as two by four
-// 16 x 16 MFMA tiles.  The reduction dimension runs in chunks of 32 staged in
-// LDS (double-buffered: the next chunk's global loads are in flight while the
-// current one is multiplied).  Inside a chunk, k runs in blocks of 16; lane
-// group q holds k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn,
-// so each lane reads its operands as float4.  Rows beyond the matrix are
-// clamped on load and dropped on store.  Requires Kd % 32 == 0.
-__global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int stage, int role) {
+// A 128 x 128 output tile per block; wave (wr, wc) takes the 64 x 64
+// quarter (wr, wc) as four by four 16 x 16 MFMA tiles, so each operand
+// fragment read from LDS feeds four MFMAs.  The reduction dimension runs in
+// chunks of 32 staged in LDS (double-buffered: the next chunk's global loads
+// are in flight while the current one is multiplied).  Inside a chunk, k runs in blocks of 16; lane group q holds
+// k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn, so each lane
+// reads its operands as float4.  Rows and columns beyond the matrix are
+// clamped on load and dropped on store.  Requires Kd % 32 == 0.  The Q, K and
+// V projections are one product with 3 D output columns: column n takes its
+// weight row and bias from tensor n / D of the three.
+__global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, int stage, int role) {
   const int k = blockIdx.z;
   if (tf->start[k] > stage) return;
   const int D = tf->D, M = tf->M, V = tf->V;
@@ -243,17 +246,12 @@ __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int s
   const int tb = 2 + kBlockTensors * b;
   const float* X = tf->sln + k * ND;
   int ldX = D, Kd = D, ldY = D, Nout = D, epi = 0;
+  bool qkv = false;
   const float *W = nullptr, *bias = nullptr, *R = nullptr;
   float* Y = nullptr;
   switch (role) {
-    case kGemmQ:
-      W = tab[tb + kWq]; bias = tab[tb + kBq]; Y = tf->sqkv + 3 * k * ND; ldY = 3 * D;
-      break;
-    case kGemmK:
-      W = tab[tb + kWk]; bias = tab[tb + kBk]; Y = tf->sqkv + 3 * k * ND + D; ldY = 3 * D;
-      break;
-    case kGemmV:
-      W = tab[tb + kWv]; bias = tab[tb + kBv]; Y = tf->sqkv + 3 * k * ND + 2 * D; ldY = 3 * D;
+    case kGemmQKV:
+      Y = tf->sqkv + 3 * k * ND; ldY = 3 * D; Nout = 3 * D; qkv = true;
       break;
     case kGemmO:
       X = tf->satt + k * ND; W = tab[tb + kWo]; bias = tab[tb + kBo]; Y = tf->sh + k * ND;
@@ -273,15 +271,27 @@ __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int s
   }
   const int n0 = blockIdx.y * kGemmCols;
   if (n0 >= Nout) return;
+  // weight row and bias of output column n
+  auto wrow = [&](int n) -> const float* {
+    if (!qkv) return W + (int64_t)n * Kd;
+    const int w = n / D;
+    return tab[tb + kWq + 2 * w] + (int64_t)(n - w * D) * Kd;
+  };
+  auto bias_of = [&](int n) -> float {
+    if (!qkv) return bias[n];
+    const int w = n / D;
+    return tab[tb + kBq + 2 * w][n - w * D];
+  };
   __shared__ __attribute__((aligned(16))) float As[2][kGemmRows][kChunkK + 4];
   __shared__ __attribute__((aligned(16))) float Bs[2][kGemmCols][kChunkK + 4];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
+  const int wr = wave >> 1, wc = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.x * kGemmRows;
   // staging: thread tid loads float4 number tid + 256 u of the A chunk
-  // (128 rows x 8 float4) and of the B chunk (64 rows x 8 float4)
+  // (128 rows x 8 float4) and of the B chunk (128 rows x 8 float4)
   constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 4
-  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 2
+  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 4
   const float* ga[kA4];
   const float* gb[kB4];
 #pragma unroll
@@ -294,16 +304,16 @@ __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int s
   for (int u = 0; u < kB4; ++u) {
     const int e = tid + kGemmThreads * u;
     const int n = n0 + e / (kChunkK / 4);
-    gb[u] = W + (int64_t)(n < Nout ? n : Nout - 1) * Kd + 4 * (e % (kChunkK / 4));
+    gb[u] = wrow(n < Nout ? n : Nout - 1) + 4 * (e % (kChunkK / 4));
   }
-  floatx4 ra[kA4], rb[kB4];
-  auto fetch = [&](int c) {
+  floatx4 ra0[kA4], rb0[kB4];
+  auto fetch = [&](int c, floatx4 (&ra)[kA4], floatx4 (&rb)[kB4]) {
 #pragma unroll
     for (int u = 0; u < kA4; ++u) ra[u] = gload(reinterpret_cast<const floatx4*>(ga[u] + kChunkK * c));
 #pragma unroll
     for (int u = 0; u < kB4; ++u) rb[u] = gload(reinterpret_cast<const floatx4*>(gb[u] + kChunkK * c));
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const floatx4 (&ra)[kA4], const floatx4 (&rb)[kB4]) {
 #pragma unroll
     for (int u = 0; u < kA4; ++u) {
       const int e = tid + kGemmThreads * u;
@@ -316,51 +326,76 @@ __global__ __launch_bounds__(kGemmThreads) void k_tf_gemm(const TfDev* tf, int s
     }
   };
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-  floatx4 acc[2][4];
+  floatx4 acc[4][4];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
+  for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) acc[sb][cb] = zero;
-  const int nc = Kd / kChunkK;
-  fetch(0);
-  store(0);
-  __syncthreads();
-  for (int c = 0; c < nc; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < nc) fetch(c + 1);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kb = 0; kb < kChunkK / 16; ++kb) {
-      floatx4 a[2], bv[4];
+      floatx4 a[4], bv[4];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-        a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][32 * wave + 16 * sb + li][16 * kb + 4 * q]);
+      for (int sb = 0; sb < 4; ++sb)
+        a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][64 * wr + 16 * sb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
-        bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][16 * cb + li][16 * kb + 4 * q]);
+        bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][64 * wc + 16 * cb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
           for (int cb = 0; cb < 4; ++cb)
             acc[sb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sb][t], bv[cb][t], acc[sb][cb], 0, 0, 0);
     }
-    if (c + 1 < nc) store(buf ^ 1);
+  };
+  // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li.
+  // The residual a lane adds is loaded before the last chunk's products, so
+  // its latency hides behind them.
+  float res[4][4][4];
+  auto load_residual = [&]() {
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
+          const int n = n0 + 64 * wc + 16 * cb + li;
+          res[sb][cb][v] = (m < N && n < Nout) ? R[m * D + n] : 0.f;
+        }
+  };
+  const int nc = Kd / kChunkK;
+  fetch(0, ra0, rb0);
+  store(0, ra0, rb0);
+  __syncthreads();
+  for (int c = 0; c < nc; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nc) fetch(c + 1, ra0, rb0);
+    if (c + 1 == nc && epi == 2) load_residual();
+    compute(buf);
+    if (c + 1 < nc) store(buf ^ 1, ra0, rb0);
     __syncthreads();
   }
-  // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li
+  float bvv[4];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
+  for (int cb = 0; cb < 4; ++cb) {
+    const int n = n0 + 64 * wc + 16 * cb + li;
+    bvv[cb] = (n < Nout) ? bias_of(n) : 0.f;
+  }
+#pragma unroll
+  for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t m = m0 + 32 * wave + 16 * sb + 4 * q + v;
-        const int n = n0 + 16 * cb + li;
+        const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
+        const int n = n0 + 64 * wc + 16 * cb + li;
         if (m < N && n < Nout) {
-          float y = acc[sb][cb][v] + bias[n];
+          float y = acc[sb][cb][v] + bvv[cb];
           if (epi == 1) y = gelu(y);
-          if (epi == 2) y = R[m * D + n] + y;
+          if (epi == 2) y = res[sb][cb][v] + y;
           Y[m * ldY + n] = y;
         }
       }
@@ -613,9 +648,8 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 0);
-    for (int role : {kGemmQ, kGemmK, kGemmV})
-      hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK),
-                         dim3(kGemmThreads), 0, s, tf, stage, role);
+    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((3 * h.D + kGemmCols - 1) / kGemmCols), KK),
+                       dim3(kGemmThreads), 0, s, tf, stage, (int)kGemmQKV);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), KK), dim3(256), 0, s, tf, stage);
     hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmO);

@@ -63,7 +63,7 @@ __host__ __device__ inline int tf_stage(int t, int NB) {
 }
 
 // GEMM roles inside a stage.
-enum TfGemmRole { kGemmQ, kGemmK, kGemmV, kGemmO, kGemmFc, kGemmProj, kGemmOut };
+enum TfGemmRole { kGemmQKV, kGemmO, kGemmFc, kGemmProj, kGemmOut };
 
 // Candidates k < K of step t (t from st->t when use_dev_t): records and new values.
 hipError_t tf_launch_propose(const TfDev* tf, const TfDev& h, uint64_t t, bool use_dev_t,
