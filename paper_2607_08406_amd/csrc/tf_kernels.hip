@@ -48,8 +48,26 @@ __device__ __forceinline__ float* slot_x(const TfDev* tf, int k, int b) {
 __device__ __forceinline__ const float* stage_input(const TfDev* tf, int k, int stage) {
   return (tf->start[k] == stage) ? tf->x[stage - 1] : slot_x(tf, k, stage - 1);
 }
+// erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf x = 1 - (a1 t + ... + a5 t^5) e^{-x^2}, t = 1 / (1 + p x), x >= 0,
+// absolute error at most 1.5e-7 (odd extension for x < 0).
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  float p = 1.061405429f;
+  p = fmaf(p, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  p *= t;
+  const float e = __builtin_amdgcn_exp2f(-(ax * ax) * 1.4426950408889634f);
+  const float r = 1.0f - p * e;
+  return copysignf(r, x);
+}
+// GELU with the exact (erf) form; the erf error above is about one fp32 ulp
+// of the result.
 __device__ __forceinline__ float gelu(float y) {
-  return 0.5f * y * (1.0f + erff(y * 0.70710678118654752f));
+  return 0.5f * y * (1.0f + erf_as(y * 0.70710678118654752f));
 }
 
 }  // namespace
@@ -236,6 +254,9 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
 // clamped on load and dropped on store.  Requires Kd % 32 == 0.  The Q, K and
 // V projections are one product with 3 D output columns: column n takes its
 // weight row and bias from tensor n / D of the three.
+// EPI: 0 bias only (Q, K, V; output layer), 1 GELU (MLP up), 2 residual
+// (attention output, MLP down): each epilogue gets its own register budget.
+template <int EPI>
 __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, int stage, int role) {
   const int k = blockIdx.z;
   if (tf->start[k] > stage) return;
@@ -245,7 +266,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, in
   const int b = stage - 1;
   const int tb = 2 + kBlockTensors * b;
   const float* X = tf->sln + k * ND;
-  int ldX = D, Kd = D, ldY = D, Nout = D, epi = 0;
+  int ldX = D, Kd = D, ldY = D, Nout = D;
   bool qkv = false;
   const float *W = nullptr, *bias = nullptr, *R = nullptr;
   float* Y = nullptr;
@@ -255,14 +276,14 @@ __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, in
       break;
     case kGemmO:
       X = tf->satt + k * ND; W = tab[tb + kWo]; bias = tab[tb + kBo]; Y = tf->sh + k * ND;
-      R = stage_input(tf, k, stage); epi = 2;
+      R = stage_input(tf, k, stage);
       break;
     case kGemmFc:
-      W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = tf->sfc + k * FC; ldY = M; Nout = M; epi = 1;
+      W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = tf->sfc + k * FC; ldY = M; Nout = M;
       break;
     case kGemmProj:
       X = tf->sfc + k * FC; ldX = M; Kd = M; W = tab[tb + kWproj]; bias = tab[tb + kBproj];
-      Y = slot_x(tf, k, b + 1); R = tf->sh + k * ND; epi = 2;
+      Y = slot_x(tf, k, b + 1); R = tf->sh + k * ND;
       break;
     default:  // kGemmOut: logits of the final stage
       W = tab[tf->n_tensors - 2]; bias = tab[tf->n_tensors - 1]; Y = tf->sfc + k * FC; ldY = V;
@@ -354,6 +375,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, in
   // The residual a lane adds is loaded before the last chunk's products, so
   // its latency hides behind them.
   float res[4][4][4];
+  (void)res;
   auto load_residual = [&]() {
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb)
@@ -373,7 +395,8 @@ __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, in
   for (int c = 0; c < nc; ++c) {
     const int buf = c & 1;
     if (c + 1 < nc) fetch(c + 1, ra0, rb0);
-    if (c + 1 == nc && epi == 2) load_residual();
+    if constexpr (EPI == 2)
+      if (c + 1 == nc) load_residual();
     compute(buf);
     if (c + 1 < nc) store(buf ^ 1, ra0, rb0);
     __syncthreads();
@@ -394,8 +417,8 @@ __global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, in
         const int n = n0 + 64 * wc + 16 * cb + li;
         if (m < N && n < Nout) {
           float y = acc[sb][cb][v] + bvv[cb];
-          if (epi == 1) y = gelu(y);
-          if (epi == 2) y = res[sb][cb][v] + y;
+          if constexpr (EPI == 1) y = gelu(y);
+          if constexpr (EPI == 2) y = res[sb][cb][v] + y;
           Y[m * ldY + n] = y;
         }
       }
@@ -648,20 +671,20 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 0);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((3 * h.D + kGemmCols - 1) / kGemmCols), KK),
+    hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, (unsigned)((3 * h.D + kGemmCols - 1) / kGemmCols), KK),
                        dim3(kGemmThreads), 0, s, tf, stage, (int)kGemmQKV);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), KK), dim3(256), 0, s, tf, stage);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
+    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmO);
     hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 1);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.M + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
+    hipLaunchKernelGGL(k_tf_gemm<1>, dim3(mt, (unsigned)((h.M + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmFc);
-    hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
+    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                        s, tf, stage, (int)kGemmProj);
   }
   const int fin = h.NB + 1;
   hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, fin, 2);
-  hipLaunchKernelGGL(k_tf_gemm, dim3(mt, (unsigned)((h.V + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
+  hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, (unsigned)((h.V + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                      s, tf, fin, (int)kGemmOut);
   hipLaunchKernelGGL(k_tf_ce, dim3((unsigned)nblk, KK), dim3(kLossThreads), 0, s, tf, partial,
                      nblk);
