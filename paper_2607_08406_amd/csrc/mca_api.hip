@@ -331,8 +331,10 @@ hipEvent_t get_event(mca_ctx* ctx) {
     ctx->pool.pop_back();
     return e;
   }
+  // Phase timers only order work on this stream: without the system-scope
+  // fence on completion a record adds no idle gap between the kernels.
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 

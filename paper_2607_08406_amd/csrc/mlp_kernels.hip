@@ -148,13 +148,15 @@ __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float*
         p = pslab + (int64_t)k * nslab;
         nt = nslab;
       }
-      // eight loads in flight, added in order
-      for (int t0 = r; t0 < nt; t0 += 16 * 8) {
-        float v[8];
+      // 32 loads in flight (up to 512 partials in one round trip), added in
+      // order: thread r adds partials r, r+16, r+32, ...
+      constexpr int kLoads = 32;
+      for (int t0 = r; t0 < nt; t0 += 16 * kLoads) {
+        float v[kLoads];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = (t0 + 16 * u < nt) ? p[t0 + 16 * u] : 0.f;
+        for (int u = 0; u < kLoads; ++u) v[u] = (t0 + 16 * u < nt) ? gload(&p[t0 + 16 * u]) : 0.f;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < kLoads; ++u)
           if (t0 + 16 * u < nt) s += (double)v[u];
       }
     }

@@ -25,9 +25,10 @@ namespace {
 
 constexpr int kSlabThreads = 1024;
 constexpr int kGroupK = 64;  // candidate slots listed at a time
-constexpr int kLanesPerPair = 32;
-constexpr int kPairsPerPass = kSlabThreads / kLanesPerPair;
-constexpr int kChunk = 8;    // list entries a lane loads at once
+constexpr int kLanesPerPair = 32;    // a half-wave scores one candidate's pairs
+constexpr int kHalves = kSlabThreads / kLanesPerPair;
+constexpr int kPairChunk = 2;        // pairs of one candidate scored together
+constexpr int kChunk = 4;    // list entries a lane loads at once
 constexpr int kStageU = 8;   // tile elements a thread loads at once
 
 template <int CM>
@@ -36,20 +37,43 @@ template <>
 struct SlabTile<10> { static constexpr int T = 16; };
 template <>
 struct SlabTile<kCMax> { static constexpr int T = 12; };
+constexpr int kSlabTileMax = 16;
 
-// Loss change of one (candidate, sample) pair; the 32 lanes of a half-wave
-// share the pair.  zt: the block's tile (row stride TS); w2: [n2][CM]; col:
-// the candidate's nnz column entries (m in the low word, the bits of
-// W_1[m, j] in the high word).  With STORE each lane writes its units' new
-// local fields into the tile.  All 64 lanes of the wave must call this (it
-// shuffles).
+template <int kCtrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), kCtrl, 0xF, 0xF, true));
+}
+// Sum over the 32 lanes of a half-wave in one fixed order, valid in its lane
+// 0: DPP within rows of 16 (lane ^ 1, ^ 2, then the mirrored partners), then
+// the other row.
+__device__ __forceinline__ float half_sum(float v) {
+  v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  v += dpp_mov<0x140>(v);  // row_mirror
+  return v + __shfl_xor(v, 16, 64);
+}
+
+// Logit changes of up to kPairChunk pairs of one candidate (samples tp[p],
+// activation changes dp[p] of its first-hidden-layer unit, p < np); the 32
+// lanes of a half-wave share them: lane g takes the list entries g, g+32, ...
+// in order, reads each entry's logit-layer weights once for all the pairs,
+// and the lane sums meet in half_sum().  zt: the block's tile (row stride
+// TS); w2: [n2][CM]; col: the candidate's nnz column entries (m in the low
+// word, the bits of W_1[m, j] in the high word).  With STORE each lane writes
+// its units' new local fields into the tile.  All 64 lanes of the wave must
+// call this.
 template <int CM, int TS, bool STORE>
-__device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, const uint64_t* col,
-                                                 int nnz, int t, float da, int act, float gamma,
-                                                 bool active, float (&acc)[CM]) {
+__device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, const uint64_t* col,
+                                                  int nnz, const int (&tp)[kPairChunk],
+                                                  const float (&dp)[kPairChunk], int np, int act,
+                                                  float gamma, bool active,
+                                                  float (&acc)[kPairChunk][CM]) {
   const int g = threadIdx.x & (kLanesPerPair - 1);
 #pragma unroll
-  for (int c = 0; c < CM; ++c) acc[c] = 0.f;
+  for (int p = 0; p < kPairChunk; ++p)
+#pragma unroll
+    for (int c = 0; c < CM; ++c) acc[p][c] = 0.f;
   if (active) {
 #pragma unroll 1
     for (int e0 = g; e0 < nnz; e0 += kLanesPerPair * kChunk) {
@@ -64,20 +88,29 @@ __device__ __forceinline__ void pair_logit_delta(float* zt, const float* w2, con
         const int e = e0 + kLanesPerPair * u;
         if (e < nnz) {
           const int m = (int)(uint32_t)ent[u];
-          const float zo = zt[m * TS + t];
-          const float zn = zo + da * __uint_as_float((uint32_t)(ent[u] >> 32));
-          const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
-          if (STORE) zt[m * TS + t] = zn;
+          const float w = __uint_as_float((uint32_t)(ent[u] >> 32));
+          float wr[CM];
 #pragma unroll
-          for (int c = 0; c < CM; ++c) acc[c] = fmaf(d, w2[m * CM + c], acc[c]);
+          for (int c = 0; c < CM; ++c) wr[c] = w2[m * CM + c];
+#pragma unroll
+          for (int p = 0; p < kPairChunk; ++p) {
+            if (p < np) {
+              const float zo = zt[m * TS + tp[p]];
+              const float zn = zo + dp[p] * w;
+              const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
+              if (STORE) zt[m * TS + tp[p]] = zn;
+#pragma unroll
+              for (int c = 0; c < CM; ++c) acc[p][c] = fmaf(d, wr[c], acc[p][c]);
+            }
+          }
         }
       }
     }
   }
 #pragma unroll
-  for (int o = kLanesPerPair / 2; o > 0; o >>= 1)
+  for (int p = 0; p < kPairChunk; ++p)
 #pragma unroll
-    for (int c = 0; c < CM; ++c) acc[c] += __shfl_xor(acc[c], o, 64);
+    for (int c = 0; c < CM; ++c) acc[p][c] = half_sum(acc[p][c]);
 }
 
 }  // namespace
@@ -138,12 +171,13 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   stage_net(net, net_arg);
   __shared__ float zt[kSlabMaxUnits * TS];
   __shared__ float w2[kSlabMaxUnits * CM];
-  __shared__ uint16_t pcode[kGroupK * T];
-  __shared__ float pda[kGroupK * T];
+  __shared__ float pdt[kGroupK * T];       // activation change of slot s at sample t
+  __shared__ uint32_t pmask[kGroupK];      // slot s's samples with a change
+  __shared__ uint16_t items[kGroupK * ((kSlabTileMax + kPairChunk - 1) / kPairChunk)];
   __shared__ float dlp[kGroupK * T];
   __shared__ int gk[kGroupK], gj[kGroupK], gi[kGroupK];
   __shared__ float gde[kGroupK];
-  __shared__ int ngroup, npairs;
+  __shared__ int ngroup, nitems;
   __shared__ uint32_t touched;  // commit: samples of the tile whose fields changed
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -165,7 +199,43 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   float* const ZL = net.Z[L - 1];   // logits
   const float* in = (l == 0) ? net.XT : net.Z[l - 1];
   if (tid == 0) touched = 0u;
-  bool staged = false;  // the tile and the logit-layer weights are in LDS
+  // The tile and the logit-layer weights go to LDS: in an evaluation first
+  // (their loads are independent of the candidates, so their latency overlaps
+  // the listing); in a commit only when the block has a pair to score.
+  auto stage = [&]() {
+    for (int e0 = tid; e0 < n2 * T; e0 += kStageU * kSlabThreads) {
+      float v[kStageU];
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int m = e / T, t = e - m * T;
+        v[u] = (e < n2 * T && n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int m = e / T, t = e - m * T;
+        if (e < n2 * T) zt[m * TS + t] = v[u];
+      }
+    }
+    const float* WL = net.W[L - 1];
+    for (int e0 = tid; e0 < CM * n2; e0 += kStageU * kSlabThreads) {
+      float v[kStageU];
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int c = e / n2, m = e - c * n2;
+        v[u] = (e < CM * n2 && c < C) ? gload(&WL[(int64_t)c * n2 + m]) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int c = e / n2, m = e - c * n2;
+        if (e < CM * n2) w2[m * CM + c] = v[u];
+      }
+    }
+  };
+  if (!commit) stage();
 
   for (int g0 = 0; g0 < (commit ? 1 : K); g0 += kGroupK) {
     // 1. the group's candidates in layer l (wave 0 lists them in order)
@@ -181,10 +251,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
         gi[s] = cands[k].i;
         gde[s] = aux[k].de;
       }
-      if (lane == 0) {
-        ngroup = (int)__popcll(m);
-        npairs = 0;
-      }
+      if (lane == 0) ngroup = (int)__popcll(m);
     }
     __syncthreads();
     const int ng = ngroup;
@@ -205,83 +272,91 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
           if (commit) gstore(&Z1[(int64_t)gj[s] * Ns + n], zn);
         }
       }
-      if (da != 0.f) {
-        const int p = atomicAdd(&npairs, 1);
-        pcode[p] = (uint16_t)(s * T + t);
-        pda[p] = da;
-      }
+      pdt[s * T + t] = da;
     }
     __syncthreads();
-    const int np = npairs;
-    if (np > 0 && !staged) {  // uniform: staged once, when a pair needs it
-      // kStageU loads in flight per thread before their LDS stores
-      for (int e0 = tid; e0 < n2 * T; e0 += kStageU * kSlabThreads) {
-        float v[kStageU];
-#pragma unroll
-        for (int u = 0; u < kStageU; ++u) {
-          const int e = e0 + u * kSlabThreads;
-          const int m = e / T, t = e - m * T;
-          v[u] = (e < n2 * T && n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < kStageU; ++u) {
-          const int e = e0 + u * kSlabThreads;
-          const int m = e / T, t = e - m * T;
-          if (e < n2 * T) zt[m * TS + t] = v[u];
-        }
+    // 3. the work items: each slot's changed samples in chunks of kPairChunk
+    // (wave 0: lane s counts its slot's, the offsets by a prefix sum)
+    if (wave == 0) {
+      uint32_t pm = 0u;
+      int nch = 0;
+      if (lane < ng) {
+        for (int t = 0; t < T; ++t)
+          if (pdt[lane * T + t] != 0.f) pm |= 1u << t;
+        nch = ((int)__popc(pm) + kPairChunk - 1) / kPairChunk;
+        pmask[lane] = pm;
       }
-      const float* WL = net.W[L - 1];
-      for (int e0 = tid; e0 < CM * n2; e0 += kStageU * kSlabThreads) {
-        float v[kStageU];
+      int incl = nch;
 #pragma unroll
-        for (int u = 0; u < kStageU; ++u) {
-          const int e = e0 + u * kSlabThreads;
-          const int c = e / n2, m = e - c * n2;
-          v[u] = (e < CM * n2 && c < C) ? gload(&WL[(int64_t)c * n2 + m]) : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < kStageU; ++u) {
-          const int e = e0 + u * kSlabThreads;
-          const int c = e / n2, m = e - c * n2;
-          if (e < CM * n2) w2[m * CM + c] = v[u];
-        }
+      for (int o = 1; o < 64; o <<= 1) {
+        const int v = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += v;
       }
-      staged = true;
+      for (int c = 0; c < nch; ++c) items[incl - nch + c] = (uint16_t)((lane << 4) | c);
+      if (lane == 63) nitems = incl;
+    }
+    __syncthreads();
+    const int ni = nitems;
+    if (commit && ni > 0) {  // uniform over the block
+      stage();
       __syncthreads();
     }
-    // 3. score the pairs, kPairsPerPass at a time
-    for (int p0 = 0; p0 < np; p0 += kPairsPerPass) {
-      const int p = p0 + (tid >> 5);
-      const bool active = p < np;
-      const int code = active ? pcode[p] : 0;
-      const int s = code / T, t = code - s * T;
+    // 4. score: half-wave h takes items h, h + kHalves, ...; every half-wave
+    // runs the same rounds (the wave shares its shuffles)
+    for (int i0 = 0; i0 < ni; i0 += kHalves) {
+      const int it = i0 + (tid >> 5);
+      const bool active = it < ni;
+      const int code = active ? items[it] : 0;
+      const int s = code >> 4, ch = code & 15;
+      uint32_t pm = active ? pmask[s] : 0u;
+      for (int r = 0; r < kPairChunk * ch; ++r) pm &= pm - 1u;  // the earlier chunks' samples
+      int tp[kPairChunk];
+      float dp[kPairChunk];
+      int np = 0;
+#pragma unroll
+      for (int p = 0; p < kPairChunk; ++p) {
+        tp[p] = 0;
+        dp[p] = 0.f;
+        if (pm) {
+          const int t = __ffs(pm) - 1;
+          pm &= pm - 1u;
+          tp[p] = t;
+          dp[p] = pdt[s * T + t];
+          np = p + 1;
+        }
+      }
       const int k = gk[s];
       const uint64_t* col = cols + (int64_t)k * n2;
       const int cnt = active ? gload(&nnz[k]) : 0;
-      const float da = active ? pda[p] : 0.f;
-      float acc[CM];
+      float acc[kPairChunk][CM];
       if (commit)  // the commit also writes the new fields into the tile
-        pair_logit_delta<CM, TS, true>(zt, w2, col, cnt, t, da, act, gamma, active, acc);
+        chunk_logit_delta<CM, TS, true>(zt, w2, col, cnt, tp, dp, np, act, gamma, active, acc);
       else
-        pair_logit_delta<CM, TS, false>(zt, w2, col, cnt, t, da, act, gamma, active, acc);
+        chunk_logit_delta<CM, TS, false>(zt, w2, col, cnt, tp, dp, np, act, gamma, active, acc);
       if (active && (tid & (kLanesPerPair - 1)) == 0) {
-        const int64_t n = n0 + t;
-        float z[CM];
 #pragma unroll
-        for (int c = 0; c < CM; ++c) z[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) + acc[c] : 0.f;
-        const float ln = ce_loss<CM>(z, C, gload(&net.y[n]));
-        dlp[s * T + t] = ln - gload(&net.ell[n]);
-        if (commit) {
+        for (int p = 0; p < kPairChunk; ++p) {
+          if (p < np) {
+            const int t = tp[p];
+            const int64_t n = n0 + t;
+            float z[CM];
 #pragma unroll
-          for (int c = 0; c < CM; ++c)
-            if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
-          gstore(&net.ell[n], ln);
-          atomicOr(&touched, 1u << t);
+            for (int c = 0; c < CM; ++c) z[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) + acc[p][c] : 0.f;
+            const float ln = ce_loss<CM>(z, C, gload(&net.y[n]));
+            dlp[s * T + t] = ln - gload(&net.ell[n]);
+            if (commit) {
+#pragma unroll
+              for (int c = 0; c < CM; ++c)
+                if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+              gstore(&net.ell[n], ln);
+              atomicOr(&touched, 1u << t);
+            }
+          }
         }
       }
     }
     __syncthreads();
-    // 4. each candidate's partial sum over the tile, in sample order
+    // 5. each candidate's partial sum over the tile, in sample order
     if (!commit && tid < ng) {
       float v = 0.f;
       for (int t = 0; t < T; ++t) v += dlp[tid * T + t];
@@ -290,11 +365,14 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
     __syncthreads();
   }
   if (!commit) return;
-  // the changed samples' new second-layer fields go back to HBM
-  const uint32_t tm = touched;
-  for (int e = tid; e < n2 * T; e += kSlabThreads) {
-    const int m = e / T, t = e - m * T;
-    if ((tm >> t) & 1u) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[m * TS + t]);
+  // the tile's second-layer fields go back to HBM when any sample changed:
+  // whole rows of T samples (the unchanged ones are rewritten with the values
+  // they hold), so each unit is one contiguous store instead of scattered ones
+  if (touched != 0u) {
+    for (int e = tid; e < n2 * T; e += kSlabThreads) {
+      const int m = e / T, t = e - m * T;
+      if (n0 + t < N) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[m * TS + t]);
+    }
   }
   if (blockIdx.x == 0 && tid == 0) {
     const mca_cand c = cands[kc];
