@@ -107,15 +107,16 @@ __global__ __launch_bounds__(kRowsThreads) void k_rows(NetDev net_arg, const mca
 
 // grid (ceil(N / 64), K) for an evaluation, (ceil(N / 64), 1) for a commit.
 template <int CM>
-__global__ __launch_bounds__(kChainThreads) void k_chain(NetDev net_arg, const mca_cand* cands,
+__global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, const mca_cand* cands,
                                                          const Aux* aux, const int* rows,
                                                          const float* rda, const int* cnt,
                                                          float* partial, int nchain, int k_mode,
                                                          const DevState* st) {
   __shared__ NetDev net;
   stage_net(net, net_arg);
-  __shared__ float ta[kChainT * kRowStride];  // activations, [sample][unit]
-  __shared__ float tb[kChainT * kRowStride];
+  // activations, [sample][unit], rewritten in place layer by layer (one tile
+  // keeps two blocks resident per CU)
+  __shared__ float ta[kChainT * kRowStride];
   __shared__ float wcol[kChainUnits];
   __shared__ int rown[kChainT];
   __shared__ float rowda[kChainT];
@@ -169,9 +170,9 @@ __global__ __launch_bounds__(kChainThreads) void k_chain(NetDev net_arg, const m
     }
   }
   __syncthreads();
-  // 3. dense layers m = s+1 .. L-2: tout = phi(tin W_m^T)
-  float* tin = ta;
-  float* tout = tb;
+  // 3. dense layers m = s+1 .. L-2: tile = phi(tile W_m^T); every wave has
+  // read the whole tile before any writes its new values
+  float* const tin = ta;
   const int q = lane >> 4, li = lane & 15;
   for (int m = s + 1; m <= L - 2; ++m) {
     const float* Wm = net.W[m];
@@ -209,6 +210,7 @@ __global__ __launch_bounds__(kChainThreads) void k_chain(NetDev net_arg, const m
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) bcur[cb] = bnext[cb];
     }
+    __syncthreads();
     // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, unit 64 w + 16 cb + li
     float* Zm = net.Z[m];
 #pragma unroll
@@ -220,12 +222,9 @@ __global__ __launch_bounds__(kChainThreads) void k_chain(NetDev net_arg, const m
           const int r = 16 * sb + 4 * q + v, u = 64 * wave + 16 * cb + li;
           const float z = acc[sb][cb][v];
           if (commit && rown[r] >= 0) gstore(&Zm[(int64_t)u * Ns + rown[r]], z);
-          tout[r * kRowStride + u] = act_fn(z, act, gamma);
+          tin[r * kRowStride + u] = act_fn(z, act, gamma);
         }
     __syncthreads();
-    float* tt = tin;
-    tin = tout;
-    tout = tt;
   }
   // 4. logits z_{L-1} = W_{L-1} a_{L-2}: thread (r, cq) takes classes cq, cq+4, ...
   {
