@@ -30,7 +30,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 per wave
 constexpr int kGemmRows = 128;     // rows (positions) per block
 constexpr int kGemmCols = 128;     // output columns per block
-constexpr int kChunkK = 32;        // reduction chunk staged in LDS
+constexpr int kChunkK = 16;        // reduction chunk staged in LDS
 constexpr int kLnThreads = 256;    // a wave per row, kLnRows rows per wave
 constexpr int kLnRows = 16;
 constexpr int kLossThreads = 256;
@@ -247,17 +247,18 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
 // A 128 x 128 output tile per block; wave (wr, wc) takes the 64 x 64
 // quarter (wr, wc) as four by four 16 x 16 MFMA tiles, so each operand
 // fragment read from LDS feeds four MFMAs.  The reduction dimension runs in
-// chunks of 32 staged in LDS (double-buffered: the next chunk's global loads
+// chunks of 16 staged in LDS (double-buffered: the next chunk's global loads
 // are in flight while the current one is multiplied).  Inside a chunk, k runs in blocks of 16; lane group q holds
 // k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn, so each lane
 // reads its operands as float4.  Rows and columns beyond the matrix are
-// clamped on load and dropped on store.  Requires Kd % 32 == 0.  The Q, K and
+// clamped on load and dropped on store.  Requires Kd % 16 == 0.  The Q, K and
 // V projections are one product with 3 D output columns: column n takes its
 // weight row and bias from tensor n / D of the three.
 // EPI: 0 bias only (Q, K, V; output layer), 1 GELU (MLP up), 2 residual
-// (attention output, MLP down): each epilogue gets its own register budget.
+// (attention output, MLP down): each epilogue gets its own register budget;
+// without a residual to hold, three blocks share a CU (40 KB of LDS each).
 template <int EPI>
-__global__ __launch_bounds__(kGemmThreads, 2) void k_tf_gemm(const TfDev* tf, int stage, int role) {
+__global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(const TfDev* tf, int stage, int role) {
   const int k = blockIdx.z;
   if (tf->start[k] > stage) return;
   const int D = tf->D, M = tf->M, V = tf->V;
