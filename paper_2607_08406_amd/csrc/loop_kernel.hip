@@ -391,11 +391,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int64_t idx = (int64_t)c.j * (hid ? nin_hid : nin_log) + c.i;
       w_reg = gload(hid ? &a.net.W[0][idx] : &w_log[idx]);
       code_reg = ternary ? (int)gload(hid ? &a.net.codes[0][idx] : &c_log[idx]) : 0;
-      // a logit-layer candidate's column is one-hot at its logit
+      // Every lane loads a column (a logit-layer candidate the first, unused:
+      // landing makes its column one-hot at its logit).  A load under a
+      // per-lane branch would make the other branch's write of the same
+      // register wait for every load in flight.
+      const int64_t jc = hid ? c.j : 0;
 #pragma unroll
-      for (int cc = 0; cc < CM; ++cc)
-        col_reg[cc] = hid ? ((cc < C) ? gload(&w_log[(int64_t)cc * nh + c.j]) : 0.f)
-                          : ((cc == c.j) ? 1.f : 0.f);
+      for (int cc = 0; cc < CM; ++cc) col_reg[cc] = (cc < C) ? gload(&w_log[(int64_t)cc * nh + jc]) : 0.f;
     }
   };
   // slot: the commit applied while landing
@@ -409,9 +411,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         w = lc.w_new;
         cur = lc.code;
       }
-      const bool colhit = lc.valid && lc.layer == Lk - 1 && c.layer == Lk - 2 && lc.i == c.j;
+      const bool hid = c.layer == Lk - 2;
+      const bool colhit = lc.valid && lc.layer == Lk - 1 && hid && lc.i == c.j;
 #pragma unroll
-      for (int cc = 0; cc < CM; ++cc) wcol_lds[b][lane][cc] = (colhit && cc == lc.j) ? lc.w_new : col_reg[cc];
+      for (int cc = 0; cc < CM; ++cc)
+        wcol_lds[b][lane][cc] = !hid ? ((cc == c.j) ? 1.f : 0.f)
+                                     : ((colhit && cc == lc.j) ? lc.w_new : col_reg[cc]);
       prep_lds[b][lane] = make_prep(net, c, w, cur);
     }
   };
