@@ -82,8 +82,8 @@ namespace {
 constexpr int kWaves = 16;  // 1024 threads: four waves per SIMD hide the list's latencies
 constexpr int kLoopThreads = 64 * kWaves;
 constexpr int kReducerWaves = 4;      // candidates per reducer workgroup
-constexpr int kMaxTilesPerLane = 8;   // G <= 64 * 8 tiles in the persistent loop
-constexpr int kReplicas = 8;          // copies of each published loss change
+constexpr int kMaxTilesPerLane = kLoopMaxTiles / 64;
+constexpr int kPollWindow = 16;  // candidates a tile polls first
 
 template <class T>
 __device__ __forceinline__ T ld_agent(const T* p) {
@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
       const double tot = wave_sum_f64(acc);
       const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
-      if (lane < kReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
+      if (lane < kLoopReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
       if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 1);
       if (lane == 0 && s < 256) MCA_PROBE(kProbeRedAll + (int64_t)s * 64 + k);
     }
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (tid == 64 ? 6 : 7));
     if (wave == 0) {
       const uint32_t t16 = tag16(s);
-      const uint64_t* dls = a.dls + (g % kReplicas) * kLoopMaxK;
+      const uint64_t* dls = a.dls + (g % kLoopReplicas) * kLoopMaxK;
       uint64_t d = 0;
       uint32_t spins = 0;
       bool ab = false;
@@ -611,8 +611,16 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const uint32_t t16p = tag16(s + 65534u);  // tag of step s-1
       const bool need_all = g == 0 && a.tr_dl != nullptr;
       uint64_t fm = 0, am = 0;
+      // Polls read the first kPollWindow candidates (one line of words) and
+      // widen to all K only when those hold no improver; every lane reads
+      // until its reducer is past step s-1.  Fewer coherent loads in flight
+      // make each of them return sooner.
+      int lim = need_all ? 64 : kPollWindow;
       while (true) {
-        if (lane < K && (uint32_t)(d & 0xFFFFu) != t16) d = ld_agent(&dls[lane]);
+        {
+          const uint32_t tg0 = (uint32_t)(d & 0xFFFFu);
+          if (lane < K && tg0 != t16 && (lane < lim || !(s == 0 || tg0 == t16p))) d = ld_agent(&dls[lane]);
+        }
         const uint32_t tg = (uint32_t)(d & 0xFFFFu);
         const bool fresh = lane >= K || tg == t16;
         const bool done_prev = fresh || s == 0 || tg == t16p;
@@ -621,6 +629,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const int pre = (~fm) ? (int)__ffsll((unsigned long long)~fm) - 1 : 64;  // first stale
         const int fa = am ? (int)__ffsll((unsigned long long)am) - 1 : 64;
         if (__all(done_prev) && (pre >= 64 || (!need_all && fa < pre))) break;
+        if (fa >= pre && pre >= lim) lim = 64;
         if ((ab = __any(spin_step(spins, a)))) break;
       }
       if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 3);
@@ -722,7 +731,7 @@ __global__ void k_reset_loop(LoopSync* s, uint64_t* partials, int64_t n_words, u
                              int K) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_words) partials[i] = 0;
-  if (i < (int64_t)kReplicas * kLoopMaxK) dls[i] = 0;
+  if (i < (int64_t)kLoopReplicas * kLoopMaxK) dls[i] = 0;
   if (i == 0) s->abort = 0;
 }
 
@@ -744,7 +753,7 @@ int step_loop_reducers(int K) { return (K + kReducerWaves - 1) / kReducerWaves; 
 
 hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s) {
   const int64_t words = 2 * (int64_t)a.K * a.gpad;
-  const int64_t n = words > (int64_t)kReplicas * kLoopMaxK ? words : (int64_t)kReplicas * kLoopMaxK;
+  const int64_t n = words > (int64_t)kLoopReplicas * kLoopMaxK ? words : (int64_t)kLoopReplicas * kLoopMaxK;
   hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sync,
                      a.partials, words, a.dls, a.K);
   hipError_t e = hipGetLastError();

@@ -8,6 +8,10 @@
 namespace mca {
 
 constexpr int kLoopMaxK = 64;  // candidates per step in the persistent loop
+#ifndef MCA_LOOP_REPLICAS
+#define MCA_LOOP_REPLICAS 32
+#endif
+constexpr int kLoopReplicas = MCA_LOOP_REPLICAS;  // copies of each published loss change (<= 64)
 
 // Abort word of the step loop, on its own 256-byte line.
 struct LoopSync {
@@ -24,7 +28,7 @@ struct LoopArgs {
   uint64_t t0;          // first step index
   uint64_t n_steps;     // steps in this launch (< 2^32)
   uint64_t* partials;   // [2][K][gpad] tagged per-tile loss-change sums, by step parity
-  uint64_t* dls;        // [8][kLoopMaxK] tagged loss changes, 8 replicas
+  uint64_t* dls;        // [kLoopReplicas][kLoopMaxK] tagged loss changes
   LoopSync* sync;
   DevState* st;
   int32_t* tr_chosen;   // trace (nullable)
@@ -34,7 +38,7 @@ struct LoopArgs {
   uint32_t spin_limit;  // polls before a wait gives up and aborts the grid
 };
 
-constexpr int kLoopMaxTiles = 64 * 8;
+constexpr int kLoopMaxTiles = 64 * 4;  // one workgroup per CU: at most the CU count
 
 // Workgroups of the candidate reducers for K candidates (four candidates each).
 int step_loop_reducers(int K);

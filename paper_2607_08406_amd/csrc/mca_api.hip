@@ -246,7 +246,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   const int64_t g_max = (N + kMinLoopTile - 1) / kMinLoopTile;
   const int64_t gpad = (g_max + 15) / 16 * 16;
   lo.loop_partials = take((size_t)2 * std::min<int32_t>(k_max, mca::kLoopMaxK) * gpad * sizeof(uint64_t));
-  lo.loop_dls = take((size_t)8 * mca::kLoopMaxK * sizeof(uint64_t));  // 8 replicas
+  lo.loop_dls = take((size_t)mca::kLoopReplicas * mca::kLoopMaxK * sizeof(uint64_t));
   lo.loop_sync = take(sizeof(mca::LoopSync));
   lo.total = off;
   return lo;
