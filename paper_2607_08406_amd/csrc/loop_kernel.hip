@@ -11,28 +11,31 @@
 // (+inf for a candidate rejected by the weight bound).  The reduction is
 // sharded by candidate: wave w < 4 of reducer workgroup r owns candidate 4r + w,
 // adds its G partial sums in a fixed order (fp64) and publishes the loss
-// change dL_k.  Every tile workgroup reads the loss changes of the
+// change dL_k.  Wave 0 of every tile workgroup reads the loss changes of the
 // candidates up to the first that passes the test (Eq. 6) and takes the same
-// decision itself: that candidate.  It then applies the commit to its own tile with the same
-// expressions the evaluation used.  Tile 0 also keeps the committed loss and
-// the counters.  While wave 0 of a tile workgroup waits for the loss changes,
+// decision itself: that candidate.  It then applies the commit to its own
+// tile with the same expressions the evaluation used.  Tile 0 also keeps the
+// committed loss and the counters.  While wave 0 waits for the loss changes,
 // the other waves work ahead (the draw needs no state): wave 1 draws the
 // candidates of step s+3, the staging waves write the operands and weights of
-// step s+1 to a second LDS buffer and start the loads of step s+2; what the
-// commits made since those loads (one hidden row of the tile, one weight,
-// code or logit-layer column entry each) is patched in LDS before use.
+// step s+1 to a second LDS buffer, list its pairs and start the loads of step
+// s+2.  The commit made after those loads were issued (one hidden row of the
+// tile, one weight, code or logit-layer column entry) is applied at landing;
+// the commit of the step just before, by wave 0 right after it commits, in
+// the rare case that it touches a candidate.  A step thus takes two
+// workgroup barriers: after the scoring, and at its end.
 //
 // Sparse inputs: a sample whose input to the mutated weight is zero does not
-// change (about 81 % of an image column), so a workgroup first compacts the
-// (candidate, sample) pairs with a non-zero input into an LDS work list and
-// spreads that list over all its lanes.  Each pair writes its loss change to
+// change (about 81 % of an image column), so the (candidate, sample) pairs
+// with a non-zero input are compacted into an LDS work list, which the whole
+// workgroup then shares out over its lanes.  Each pair writes its loss change to
 // its own (candidate, sample) slot and the slots are summed in sample order,
 // so the order in which the list was built does not change any result.
 //
 // Weights are read with ordinary cached loads.  Every tile workgroup writes
 // every committed weight itself, so each CU's L1 and each XCD's L2 that may
-// hold the old value is updated by a local store; the committing wave waits
-// for its stores during the next step, before any wave reads them again, and
+// hold the old value is updated by a local store; wave 0 waits for its
+// commit stores during the next step, before any wave issues loads again, and
 // until then the value comes from LDS.
 //
 // Cross-workgroup words carry their own step tag, so no separate flag, fence
@@ -212,7 +215,7 @@ __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, 
   da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
-  return logit || da != 0.f;  // the logits changed
+  return logit ? dz != 0.f : da != 0.f;  // the logits changed
 }
 
 // The pair's new loss ln; returns its loss change.
@@ -243,9 +246,8 @@ __device__ __forceinline__ float input_of(const NetDev& net, int layer, float a_
 
 }  // namespace
 
-// KW = candidates per wave (K <= 4 KW), a compile-time bound so the operands
-// of a wave's candidates stay in registers; CM = bound on the class count.
-template <int KW, int CM>
+// CM = bound on the class count (a compile-time count for C = 10).
+template <int CM>
 __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ NetDev net;
   stage_net(net, a.net);
@@ -262,11 +264,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float zh_lds[2][kLoopMaxK][64];
   __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
   __shared__ float lnp_lds[kLoopMaxK][64];  // each pair's new loss, which a commit reuses
-  __shared__ uint16_t list_lds[kLoopMaxK * 64];
-  __shared__ int list_n;
+  __shared__ uint16_t list_lds[2][kLoopMaxK * 64];  // work lists, by step parity
+  __shared__ int list_n[2];
+  __shared__ uint32_t stage_cnt;  // waves 1-15 that have landed a step (15 per step)
   __shared__ LastCommit last[2];     // commits of the last two steps, by step parity
   __shared__ float zrow_lds[2][64];  // their committed hidden rows of this tile
-  __shared__ int dec_k;
   __shared__ int aborted;
 
   const int K = a.K, T = a.T, G = a.G;
@@ -379,6 +381,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   float a_raw[kPer], z_raw[kPer];  // per-sample loads in flight
   float w_reg = 0.f, col_reg[CM];  // per-candidate loads in flight (wave 1)
   int code_reg = 0;
+
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) col_reg[cc] = 0.f;
   auto draw = [&](uint64_t t, int cb) {
@@ -439,15 +442,23 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
     }
   };
+  // Landing also lists the (candidate, sample) pairs of the wave's
+  // candidates that can change: a non-zero input; for a logit-layer weight
+  // fed by a hidden layer every live sample, since the commit of the step
+  // before may still change that input (a pair whose input is zero adds
+  // exactly 0).  Results do not depend on the order of the list.
   auto land_samples = [&](int cb, int b, int slot) {
     const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
     const int lvalid = __builtin_amdgcn_readfirstlane(last[slot].valid);
     const int llayer = __builtin_amdgcn_readfirstlane(last[slot].layer);
     const int lj = __builtin_amdgcn_readfirstlane(last[slot].j);
     const bool row = lvalid && llayer == Lk - 2;  // a hidden row of this tile changed
+    uint64_t m[kPer];
+    int tot = 0;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
+      m[q] = 0;
       if (k < K) {
         const int l = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].layer);
         const int ci = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].i);
@@ -460,9 +471,32 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const float in = (!hid && two) ? act_fn(ar, act, gamma) : ar;
         ain_lds[b][k][lane] = live ? in : 0.f;
         zh_lds[b][k][lane] = zz;
+        m[q] = __ballot(live && (in != 0.f || (two && !hid)));
+        tot += (int)__popcll(m[q]);
       }
     }
+    int base = 0;
+    if (lane == 0 && tot) base = atomicAdd(&list_n[b], tot);
+    base = __shfl(base, 0, 64);
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      if ((m[q] >> lane) & 1ull)
+        list_lds[b][base + (int)__popcll(m[q] & below)] = (uint16_t)(((w + kStagers * q) << 6) | lane);
+      base += (int)__popcll(m[q]);
+    }
   };
+  // Waves 1-15 count the steps they have landed, so that wave 0 can patch a
+  // landed step (rarely) once they are done with it.
+  auto landed = [&]() {
+    __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (lane == 0) atomicAdd(&stage_cnt, 1u);
+  };
+
+  if (tid < 2) list_n[tid] = 0;
+  if (tid == 0) stage_cnt = 0;
+  // pair slots start clear; after each step wave 0 clears those it summed
+  for (int i = tid; i < kLoopMaxK * 65; i += kLoopThreads) (&dlp_lds[0][0])[i] = 0.f;
   if (wave == 1)
     for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(a.t0 + d, (int)d);
   __syncthreads();
@@ -480,77 +514,20 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   const int psel = (g == 0) ? 0 : ((g == G - 1) ? 1 : -1);
 #define MCA_TILE_PROBE(p) \
   if (psel >= 0 && tid == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (p))
+  // A step takes two workgroup barriers: after the scoring, and at its end,
+  // when wave 0 has decided and committed and waves 1-15 have staged and
+  // listed the next step.
   for (uint64_t s = 0; s < a.n_steps; ++s) {
     const uint32_t tag = (uint32_t)(s + 1);
     const int buf = (int)(s & 1);
     const int cb = (int)(s & 3);
     mca_cand* cands = cand_lds[cb];
     MCA_TILE_PROBE(0);
-    // 1. the staged values include every commit up to step s-2; apply the
-    // commit of step s-1 where it touches a candidate (its weight, its
-    // unit's row of this tile, or its logit-layer column), which is rare
-    {
-      const int slot = buf ^ 1;
-      const LastCommit lc = last[slot];
-      if (lc.valid && wave == 0) {
-        bool row = false;
-        mca_cand c;
-        if (lane < K) {
-          c = cands[lane];
-          const bool hid = c.layer == L - 2;
-          if (lc.layer == c.layer && lc.j == c.j && lc.i == c.i)
-            prep_lds[buf][lane] = make_prep(net, c, lc.w_new, lc.code);
-          if (lc.layer == L - 1 && hid && lc.i == c.j) wcol_lds[buf][lane][lc.j] = lc.w_new;
-          row = lc.layer == L - 2 && ((hid && c.j == lc.j) || (c.layer == L - 1 && c.i == lc.j));
-        }
-        uint64_t rows = __ballot(row);
-        if (rows) {
-          const float zr = zrow_lds[slot][lane];
-          while (rows) {
-            const int k = (int)__ffsll((unsigned long long)rows) - 1;
-            rows &= rows - 1;
-            const int l = __shfl(c.layer, k, 64);
-            if (l == L - 2) zh_lds[buf][k][lane] = zr;
-            else ain_lds[buf][k][lane] = live ? input_of(net, l, zr) : 0.f;
-          }
-        }
-      }
-    }
-    if (tid == 0) list_n = 0;
-    MCA_TILE_PROBE(5);
-    __syncthreads();
-    MCA_TILE_PROBE(1);
-    // 2a. compact the pairs whose input is non-zero into the work list: one
-    // slot reservation per wave for all its candidates
-    {
-      float ainv[KW];
-#pragma unroll
-      for (int q = 0; q < KW; ++q) ainv[q] = ain_lds[buf][wave + kWaves * q][lane];
-      uint64_t m[KW];
-      int tot = 0;
-#pragma unroll
-      for (int q = 0; q < KW; ++q) {
-        const int k = wave + kWaves * q;
-        if (k < K) dlp_lds[k][lane] = 0.f;
-        m[q] = __ballot(k < K && live && ainv[q] != 0.f);
-        tot += (int)__popcll(m[q]);
-      }
-      int base = 0;
-      if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
-      base = __shfl(base, 0, 64);
-      const uint64_t below = (1ull << lane) - 1ull;
-#pragma unroll
-      for (int q = 0; q < KW; ++q) {
-        if ((m[q] >> lane) & 1ull)
-          list_lds[base + (int)__popcll(m[q] & below)] = (uint16_t)(((wave + kWaves * q) << 6) | lane);
-        base += (int)__popcll(m[q]);
-      }
-    }
-    __syncthreads();
-    // 2b. every lane of the workgroup scores list entries
-    const int n_list = list_n;
+    // 1. every lane of the workgroup scores list entries (the list of step s
+    // was built during step s-1); the list of step s+1 starts empty
+    const int n_list = list_n[buf];
     for (int e = tid; e < n_list; e += kLoopThreads) {
-      const int code = list_lds[e];
+      const int code = list_lds[buf][e];
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
       float ln;
@@ -560,14 +537,17 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
                                      ell_lds[sl], y_lds[sl], ln);
       lnp_lds[k][sl] = ln;
     }
+    if (tid == 0) list_n[buf ^ 1] = 0;
     // last step's commit stores land before this step's staging reads HBM
     if (committed) wait_own_memory();
     committed = false;
     __syncthreads();
-    // 2c. wave 0, lane k: sum candidate k's 64 slots (four runs of 16
-    // consecutive samples, then the runs pairwise) and publish the tile's
-    // partial sum.  Only wave 0 stores here: a store still in flight would
-    // make the staging waves' waits for their own loads wait for it too.
+    MCA_TILE_PROBE(1);
+    // 2. wave 0, lane k: sum candidate k's 64 slots (four runs of 16
+    // consecutive samples, then the runs pairwise), publish the tile's
+    // partial sum and clear the slots for the next step.  Only wave 0 stores
+    // to global memory here: a store still in flight would make the staging
+    // waves' waits for their own loads wait for it too.
     uint64_t* part = a.partials + (size_t)buf * K * a.gpad + g;  // candidate k: part[k * gpad]
     if (wave == 0 && lane < K) {
       float r0 = 0.f, r1 = 0.f, r2 = 0.f, r3 = 0.f;
@@ -580,22 +560,26 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
       const float v = (r0 + r1) + (r2 + r3);
       st_agent(&part[(size_t)lane * a.gpad], pack(prep_lds[buf][lane].valid ? v : __builtin_huge_valf(), tag));
+#pragma unroll
+      for (int i = 0; i < 64; ++i) dlp_lds[lane][i] = 0.f;
     }
-    // 3. wave 0 gathers the K loss changes and decides (every tile takes the
-    // same decision from the same words); wave 1 draws step s+3, waves 2-15 land
-    // step s+1 and issue step s+2
     MCA_TILE_PROBE(2);
     if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
+    // 3. wave 1 draws step s+3, waves 2-15 land and list step s+1 and issue
+    // step s+2
     if (wave == 1) {
       if (s + 1 < a.n_steps) land_cand((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      landed();
       if (s + 2 < a.n_steps) issue_cand((int)((s + 2) & 3));
       if (s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
+      if (psel >= 0 && lane == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 6);
     } else if (wave >= 2) {
       if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      landed();
       if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
+      if (psel >= 0 && wave == 15 && lane == 0 && s < 256)
+        MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 7);
     }
-    if (psel >= 0 && (tid == 64 || tid == 64 * 15) && s < 256)
-      MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (tid == 64 ? 6 : 7));
     if (wave == 0) {
       const uint32_t t16 = tag16(s);
       const uint64_t* dls = a.dls + (g % kLoopReplicas) * kLoopMaxK;
@@ -638,10 +622,80 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #endif
       const double v = unpack_dl(d);
       const int kc = (!ab && am) ? (int)__ffsll((unsigned long long)am) - 1 : -1;
-      if (lane == 0) {
-        aborted = ab ? 1 : 0;
-        dec_k = ab ? -1 : kc;
+      // 4. commit on this tile (lane = sample; the winner's operands are
+      // staged in LDS); every workgroup writes the new weight
+      const mca_cand c = cands[kc >= 0 ? kc : 0];
+      const Prep au = prep_lds[buf][kc >= 0 ? kc : 0];
+      float zr = 0.f;  // the committed unit's row of this tile, lane = sample
+      if (kc >= 0) {
+        // the same logits the scoring computed; its loss was kept
+        const float ain = ain_lds[buf][kc][lane];
+        const float z_raw = zh_lds[buf][kc][lane];
+        const float ln = lnp_lds[kc][lane];
+        float zn, da, z[CM];
+        (void)pair_logits<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
+                              &zl_lds[lane], zn, da, z);
+        const bool ch = live && ain != 0.f;
+        if (ch) {
+          if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
+#pragma unroll
+          for (int cc = 0; cc < CM; ++cc)
+            if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
+          ell_lds[lane] = ln;
+        }
+        zr = ch ? zn : z_raw;
+        zrow_lds[buf][lane] = zr;
+        if (lane == 0) {
+          const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+          gstore(&net.W[c.layer][idx], au.w_new);
+          if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)au.code);
+          LastCommit& lc = last[buf];
+          lc.layer = c.layer;
+          lc.j = c.j;
+          lc.i = c.i;
+          lc.code = au.code;
+          lc.w_new = au.w_new;
+          lc.valid = 1;
+        }
+        committed = true;
+      } else if (lane == 0) {
+        last[buf].valid = 0;
       }
+      // 5. the commit may touch a candidate of step s+1 (its weight, its
+      // unit's row of this tile, or its logit-layer column), which is rare:
+      // once waves 1-15 have landed step s+1, patch it (lane = candidate for
+      // its value and column, lane = sample for rows)
+      if (kc >= 0 && s + 1 < a.n_steps) {
+        const mca_cand* const next = cand_lds[(s + 1) & 3];
+        bool row = false, same = false, col = false;
+        mca_cand c1{};
+        if (lane < K) {
+          c1 = next[lane];
+          const bool hid = c1.layer == L - 2;
+          same = c.layer == c1.layer && c.j == c1.j && c.i == c1.i;
+          col = c.layer == L - 1 && hid && c.i == c1.j;
+          row = c.layer == L - 2 && ((hid && c1.j == c.j) || (c1.layer == L - 1 && c1.i == c.j));
+        }
+        if (__any(row || same || col)) {
+          const uint32_t want = (uint32_t)(kWaves - 1) * (uint32_t)(s + 1);
+          while (__hip_atomic_load(&stage_cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != want)
+            __builtin_amdgcn_s_sleep(1);
+          __asm__ volatile("" ::: "memory");
+          if (same) prep_lds[buf ^ 1][lane] = make_prep(net, c1, au.w_new, au.code);
+          if (col) wcol_lds[buf ^ 1][lane][c.j] = au.w_new;
+          uint64_t rows = __ballot(row);
+          while (rows) {
+            const int k = (int)__ffsll((unsigned long long)rows) - 1;
+            rows &= rows - 1;
+            const int l = __shfl(c1.layer, k, 64);
+            if (l == L - 2) zh_lds[buf ^ 1][k][lane] = zr;
+            else ain_lds[buf ^ 1][k][lane] = live ? input_of(net, l, zr) : 0.f;
+          }
+        }
+      }
+      if (lane == 0) aborted = ab ? 1 : 0;
+      MCA_TILE_PROBE(3);
+      // tile 0 keeps the committed loss, the counters and the trace
       if (g == 0 && !ab) {
         const uint64_t tie_mask = __ballot(lane < K && fabs(v) < 1e-6);
         const double vk = __shfl(v, kc < 0 ? 0 : kc, 64);
@@ -665,47 +719,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
     }
     __syncthreads();
-    MCA_TILE_PROBE(3);
-    if (aborted) break;
-    // 4. commit on this tile (wave 1; the winner's operands are staged in
-    // LDS); every workgroup writes the new weight
-    const int kc = dec_k;
-    if (kc >= 0 && wave == 1) {
-      const mca_cand c = cands[kc];
-      const Prep au = prep_lds[buf][kc];
-      // the same logits the scoring computed; its loss was kept
-      const float ain = ain_lds[buf][kc][lane];
-      const float z_raw = zh_lds[buf][kc][lane];
-      const float ln = lnp_lds[kc][lane];
-      float zn, da, z[CM];
-      (void)pair_logits<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
-                            &zl_lds[lane], zn, da, z);
-      const bool ch = live && ain != 0.f;
-      if (ch) {
-        if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
-#pragma unroll
-        for (int cc = 0; cc < CM; ++cc)
-          if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
-        ell_lds[lane] = ln;
-      }
-      zrow_lds[buf][lane] = ch ? zn : z_raw;
-      if (lane == 0) {
-        const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
-        gstore(&net.W[c.layer][idx], au.w_new);
-        if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)au.code);
-        LastCommit& lc = last[buf];
-        lc.layer = c.layer;
-        lc.j = c.j;
-        lc.i = c.i;
-        lc.code = au.code;
-        lc.w_new = au.w_new;
-        lc.valid = 1;
-      }
-      committed = true;
-    }
-    if (kc < 0 && tid == 0) last[buf].valid = 0;
-    __syncthreads();
     MCA_TILE_PROBE(4);
+    if (aborted) break;
   }
 #undef MCA_TILE_PROBE
   // the tile's logits and losses go back to HBM; tile 0 writes the state
@@ -736,16 +751,9 @@ __global__ void k_reset_loop(LoopSync* s, uint64_t* partials, int64_t n_words, u
 }
 
 namespace {
-template <int KW>
-const void* loop_fn(int C) {
-  return C == 10 ? (const void*)k_step_loop<KW, 10> : (const void*)k_step_loop<KW, kCMax>;
-}
-
 const void* pick_loop(int K, int C) {
-  const int kw = (K + kWaves - 1) / kWaves;
-  if (kw <= 1) return loop_fn<1>(C);
-  if (kw <= 2) return loop_fn<2>(C);
-  return loop_fn<4>(C);
+  (void)K;
+  return C == 10 ? (const void*)k_step_loop<10> : (const void*)k_step_loop<kCMax>;
 }
 }  // namespace
 
