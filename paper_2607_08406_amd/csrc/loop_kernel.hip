@@ -192,6 +192,23 @@ __device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, 
 // expressions as column_sample() of the multi-kernel path, written without
 // branches on the candidate's layer (pairs of different candidates share a
 // wave).
+// pair_logits_of takes the sample's logits zc and the column wc as values.
+template <int CM>
+__device__ __forceinline__ bool pair_logits_of(int C, int act, float gamma, bool logit, float zb,
+                                               float de, const float (&wc)[CM], float ain,
+                                               const float (&zc)[CM], float& zn, float& da,
+                                               float (&z)[CM]) {
+  const float dz = de * ain;
+  zn = zb + dz;
+  // A logit-layer candidate's staged column is one-hot at its logit j, which
+  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
+  // exactly, so one expression serves both kinds of candidate.
+  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
+  return logit ? dz != 0.f : da != 0.f;  // the logits changed
+}
+
 template <int CM>
 __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
                                             float de, const float* wcol, float ain, float zh,
@@ -207,15 +224,7 @@ __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, 
     wc[cc] = wcol[cc];
   }
   const float zb = logit ? zL[j * 64] : zh;
-  const float dz = de * ain;
-  zn = zb + dz;
-  // A logit-layer candidate's staged column is one-hot at its logit j, which
-  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
-  // exactly, so one expression serves both kinds of candidate.
-  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
-#pragma unroll
-  for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
-  return logit ? dz != 0.f : da != 0.f;  // the logits changed
+  return pair_logits_of<CM>(C, act, gamma, logit, zb, de, wc, ain, zc, zn, da, z);
 }
 
 // The pair's new loss ln; returns its loss change.
@@ -423,17 +432,33 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       prep_lds[b][lane] = make_prep(net, c, w, cur);
     }
   };
+  // Lane q < kPer of a staging wave reads the layer, input and unit of the
+  // wave's q-th candidate of draw buffer cb (one LDS round trip for all of
+  // them); the wave then takes them into scalars lane by lane.
+  auto stage_fields = [&](int cb, int& lv, int& iv, int& jv) {
+    const int kq = __builtin_amdgcn_readfirstlane(wave) - 2 + kStagers * lane;
+    lv = -1;
+    iv = jv = 0;
+    if (lane < kPer && kq < K) {
+      const mca_cand c = cand_lds[cb][kq];
+      lv = c.layer;
+      iv = c.i;
+      jv = c.j;
+    }
+  };
   auto issue_samples = [&](int cb) {
     const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
+    int lv, iv, jv;
+    stage_fields(cb, lv, iv, jv);
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
       a_raw[q] = 0.f;
       z_raw[q] = 0.f;
       if (k < K) {
-        const int l = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].layer);
-        const int ci = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].i);
-        const int cj = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].j);
+        const int l = __builtin_amdgcn_readlane(lv, q);
+        const int ci = __builtin_amdgcn_readlane(iv, q);
+        const int cj = __builtin_amdgcn_readlane(jv, q);
         const bool hid = l == Lk - 2;
         if (live) {
           a_raw[q] = gload(&(hid ? in_hid : in_log)[(int64_t)ci * Ns + n]);
@@ -453,6 +478,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     const int llayer = __builtin_amdgcn_readfirstlane(last[slot].layer);
     const int lj = __builtin_amdgcn_readfirstlane(last[slot].j);
     const bool row = lvalid && llayer == Lk - 2;  // a hidden row of this tile changed
+    int lv, iv, jv;
+    stage_fields(cb, lv, iv, jv);
     uint64_t m[kPer];
     int tot = 0;
 #pragma unroll
@@ -460,9 +487,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int k = w + kStagers * q;
       m[q] = 0;
       if (k < K) {
-        const int l = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].layer);
-        const int ci = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].i);
-        const int cj = __builtin_amdgcn_readfirstlane(cand_lds[cb][k].j);
+        const int l = __builtin_amdgcn_readlane(lv, q);
+        const int ci = __builtin_amdgcn_readlane(iv, q);
+        const int cj = __builtin_amdgcn_readlane(jv, q);
         const bool hid = l == Lk - 2;
         float ar = a_raw[q], zz = z_raw[q];
         if (row && hid && cj == lj) zz = zrow_lds[slot][lane];
@@ -581,6 +608,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 7);
     }
     if (wave == 0) {
+      // what the commit and the patch check need whichever candidate wins:
+      // the lane's logits, and the candidates of step s+1 (lane = candidate)
+      float zc[CM];
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc) zc[cc] = zl_lds[cc * 64 + lane];
+      mca_cand c1{};
+      if (lane < K) c1 = cand_lds[(s + 1) & 3][lane];
       const uint32_t t16 = tag16(s);
       const uint64_t* dls = a.dls + (g % kLoopReplicas) * kLoopMaxK;
       uint64_t d = 0;
@@ -632,9 +666,15 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const float ain = ain_lds[buf][kc][lane];
         const float z_raw = zh_lds[buf][kc][lane];
         const float ln = lnp_lds[kc][lane];
+        float wc[CM];
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc) wc[cc] = wcol_lds[buf][kc][cc];
+        const bool logit = c.layer == L - 1;
+        float zb = z_raw;
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc) zb = (logit && cc == c.j) ? zc[cc] : zb;
         float zn, da, z[CM];
-        (void)pair_logits<CM>(L, C, act, gamma, c.layer, c.j, au.de, wcol_lds[buf][kc], ain, z_raw,
-                              &zl_lds[lane], zn, da, z);
+        (void)pair_logits_of<CM>(C, act, gamma, logit, zb, au.de, wc, ain, zc, zn, da, z);
         const bool ch = live && ain != 0.f;
         if (ch) {
           if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
@@ -666,11 +706,8 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       // once waves 1-15 have landed step s+1, patch it (lane = candidate for
       // its value and column, lane = sample for rows)
       if (kc >= 0 && s + 1 < a.n_steps) {
-        const mca_cand* const next = cand_lds[(s + 1) & 3];
         bool row = false, same = false, col = false;
-        mca_cand c1{};
         if (lane < K) {
-          c1 = next[lane];
           const bool hid = c1.layer == L - 2;
           same = c.layer == c1.layer && c.j == c1.j && c.i == c1.i;
           col = c.layer == L - 1 && hid && c.i == c1.j;
