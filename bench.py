@@ -49,6 +49,42 @@ def algorithmic_bytes_per_step(cfg) -> float:
     return shared + K * per_cand
 
 
+def eval_bytes(cfg, cands) -> float:
+    """Algorithmic bytes of one batched evaluation launch: the shared logits,
+    per-sample losses and labels once, plus each candidate's rows (8 N for a
+    last-hidden-layer weight, 4 N for a logit-layer weight)."""
+    N, C, L = cfg.n_samples, cfg.n_classes, cfg.n_layers
+    rows = sum(8.0 * N if int(c["layer"]) == L - 2 else 4.0 * N for c in cands)
+    return 4.0 * N * C + 4.0 * N + N + rows
+
+
+def incremental_phase(ctx, cfg, step: int, batch: int, reps: int):
+    """The incremental phases alone (column update, transfer, rank-1 update of
+    the logits, fused cross-entropy and per-tile loss-change sums): the batched
+    evaluation kernel scoring `batch` candidates of the stream against one
+    committed state, timed with HIP events on the library's stream; every
+    batch is rolled back."""
+    from paper_2607_08406_amd import mca
+    cands = ctx.propose(step, batch)
+    ctx.eval_losses(cands)
+    ctx.rollback()
+    mca.mca_get_timing(ctx.ctx, reset=True)
+    mca.mca_set_timing(ctx.ctx, 1 << mca.PHASES.index("eval"))
+    for _ in range(reps):
+        ctx.eval_losses(cands)
+        ctx.rollback()
+    ms, launches = mca.mca_get_timing(ctx.ctx, reset=True)
+    mca.mca_set_timing(ctx.ctx, 0)
+    n = int(launches[mca.PHASES.index("eval")])
+    avg_s = ms[mca.PHASES.index("eval")] / 1e3 / max(n, 1)
+    b = eval_bytes(cfg, cands)
+    achieved = b / avg_s / 1e9
+    return {"kernel": "k_eval_tiles", "batch": batch, "launches": n,
+            "avg_launch_us": avg_s * 1e6, "candidate_evals_per_s": batch / avg_s,
+            "bound": "hbm", "bytes_per_launch": b, "achieved": achieved, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS}
+
+
 def candidate_flops(cfg, w, cands, params):
     """Algorithmic flops of scoring one step's candidates on the deep or the
     three-layer net (an FMA counts 2).  A mutation in layers 0..L-4 recomputes,
@@ -194,6 +230,10 @@ def main():
     ap.add_argument("--tile", type=int, default=0, help="samples per workgroup (16..64)")
     ap.add_argument("--per-phase", action="store_true",
                     help="one launch per phase per step instead of the persistent loop")
+    ap.add_argument("--eval-batch", type=int, default=1024,
+                    help="candidates per launch of the incremental-phase measurement "
+                         "(one- and two-layer MLPs; 0 skips it)")
+    ap.add_argument("--eval-reps", type=int, default=50)
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (5 times): the "
                          "reference kernel that calibrates FETCH_SIZE / WRITE_SIZE counters")
@@ -227,7 +267,9 @@ def main():
                             ternary_scales=w["scales"], pick=cfg.layer_pick,
                             accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
                             stream_tag=cfg.stream_tag)
-        ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=cfg.K, codes=w["codes"])
+        eval_batch = args.eval_batch if cfg.n_layers <= 2 else 0
+        ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=max(cfg.K, eval_batch),
+                          codes=w["codes"])
     if args.tile:
         ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
     if args.per_phase:
@@ -264,7 +306,7 @@ def main():
                 "flops_per_launch": per_step, "avg_launch_us": avg_s * 1e6,
                 "launches": int(launches[dominant])}
     elif cfg.n_layers <= 2:
-        kernel = "k_step_loop" if loop else "k_eval_column"
+        kernel = "k_step_loop" if loop else "k_eval_tiles"
         # one loop launch covers all timed steps; one eval launch covers one step
         bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
         achieved = bytes_launch / avg_s / 1e9
@@ -309,6 +351,11 @@ def main():
         "roofline": roof,
         "final_loss": st.loss,
     }
+    if cfg.kind != "transformer" and eval_batch > 0:
+        print(f"[bench] incremental phases: {args.eval_reps} batches of {eval_batch}",
+              file=sys.stderr, flush=True)
+        result["incremental_phase"] = incremental_phase(ctx, cfg, st.next_step, eval_batch,
+                                                        args.eval_reps)
     ctx.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

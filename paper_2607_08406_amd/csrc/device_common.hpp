@@ -158,6 +158,74 @@ __device__ __forceinline__ float ce_loss(const float (&z)[CM], int C, int y) {
 }
 
 // ---------------------------------------------------------------------------
+// one (candidate, sample) pair of a mutation in the last two layers
+// ---------------------------------------------------------------------------
+
+// One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
+// the activation feeding it); zh: the cached local field of the mutated unit
+// when it is a hidden unit; zL: the sample's logits in LDS (stride 64).  The
+// new local field, logits and loss come back for a commit.  Written without
+// branches on the candidate's layer (pairs of different candidates share a
+// wave); the step loop and the batched evaluation both score pairs with
+// these expressions, and the column commit applies the same arithmetic.
+// pair_logits_of takes the sample's logits zc and the column wc as values.
+template <int CM>
+__device__ __forceinline__ bool pair_logits_of(int C, int act, float gamma, bool logit, float zb,
+                                               float de, const float (&wc)[CM], float ain,
+                                               const float (&zc)[CM], float& zn, float& da,
+                                               float (&z)[CM]) {
+  const float dz = de * ain;
+  zn = zb + dz;
+  // A logit-layer candidate's staged column is one-hot at its logit j, which
+  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
+  // exactly, so one expression serves both kinds of candidate.
+  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
+  return logit ? dz != 0.f : da != 0.f;  // the logits changed
+}
+
+template <int CM>
+__device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
+                                            float de, const float* wcol, float ain, float zh,
+                                            const float* zL, float& zn, float& da,
+                                            float (&z)[CM]) {
+  const bool logit = layer == L - 1;
+  // every operand is loaded unconditionally (the LDS rows hold CM entries,
+  // zero beyond C) so the loads issue together
+  float zc[CM], wc[CM];
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) {
+    zc[cc] = zL[cc * 64];
+    wc[cc] = wcol[cc];
+  }
+  const float zb = logit ? zL[j * 64] : zh;
+  return pair_logits_of<CM>(C, act, gamma, logit, zb, de, wc, ain, zc, zn, da, z);
+}
+
+// The pair's new loss ln; returns its loss change.
+template <int CM>
+__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
+                                           float de, const float* wcol, float ain, float zh,
+                                           const float* zL, float ell, int y, float& ln) {
+  float zn, da, z[CM];
+  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
+  // ce_loss() with the label's logit computed by the same fma instead of
+  // selected from z: the same bits, without a compare per class
+  const float zy = fmaf(da, wcol[y], zL[y * 64]);
+  float m = z[0];
+#pragma unroll
+  for (int c = 1; c < CM; ++c)
+    if (c < C) m = fmaxf(m, z[c]);
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < CM; ++c)
+    if (c < C) s += fast_exp(z[c] - m);
+  ln = (fast_log(s) + m) - zy;
+  return changed ? ln - ell : 0.f;
+}
+
+// ---------------------------------------------------------------------------
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)
 // ---------------------------------------------------------------------------
 
@@ -251,6 +319,23 @@ __device__ __forceinline__ Aux prepare_candidate(const NetDev& net, const mca_ca
 __device__ __forceinline__ bool accepts(double dL, int ties) {
   // NaN compares false either way, +inf never passes
   return ties ? (dL <= 0.0) : (dL < 0.0);
+}
+
+// Sum of v over the 64 lanes of a wave in one fixed order (a butterfly within
+// rows of 16 by DPP, then across rows), returned in every lane.  All 64
+// lanes must be active.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), kCtrl, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  v += dpp_f32<0xB1>(v);   // lane ^ 1
+  v += dpp_f32<0x4E>(v);   // lane ^ 2
+  v += dpp_f32<0x141>(v);  // mirror within eight
+  v += dpp_f32<0x140>(v);  // mirror within sixteen
+  v += __shfl_xor(v, 16, 64);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+         __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
 }
 
 // Sum of v over a block of kTile threads (4 waves of 64), fixed order.

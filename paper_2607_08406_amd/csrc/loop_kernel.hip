@@ -185,70 +185,6 @@ __device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, 
   return x;
 }
 
-// One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
-// the activation feeding it); zh: the cached local field of the mutated unit
-// when it is a hidden unit; zL: the sample's logits in LDS (stride 64).  The
-// new local field, logits and loss come back for a commit.  The same
-// expressions as column_sample() of the multi-kernel path, written without
-// branches on the candidate's layer (pairs of different candidates share a
-// wave).
-// pair_logits_of takes the sample's logits zc and the column wc as values.
-template <int CM>
-__device__ __forceinline__ bool pair_logits_of(int C, int act, float gamma, bool logit, float zb,
-                                               float de, const float (&wc)[CM], float ain,
-                                               const float (&zc)[CM], float& zn, float& da,
-                                               float (&z)[CM]) {
-  const float dz = de * ain;
-  zn = zb + dz;
-  // A logit-layer candidate's staged column is one-hot at its logit j, which
-  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
-  // exactly, so one expression serves both kinds of candidate.
-  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
-#pragma unroll
-  for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
-  return logit ? dz != 0.f : da != 0.f;  // the logits changed
-}
-
-template <int CM>
-__device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
-                                            float de, const float* wcol, float ain, float zh,
-                                            const float* zL, float& zn, float& da,
-                                            float (&z)[CM]) {
-  const bool logit = layer == L - 1;
-  // every operand is loaded unconditionally (the LDS rows hold CM entries,
-  // zero beyond C) so the loads issue together
-  float zc[CM], wc[CM];
-#pragma unroll
-  for (int cc = 0; cc < CM; ++cc) {
-    zc[cc] = zL[cc * 64];
-    wc[cc] = wcol[cc];
-  }
-  const float zb = logit ? zL[j * 64] : zh;
-  return pair_logits_of<CM>(C, act, gamma, logit, zb, de, wc, ain, zc, zn, da, z);
-}
-
-// The pair's new loss ln; returns its loss change.
-template <int CM>
-__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
-                                           float de, const float* wcol, float ain, float zh,
-                                           const float* zL, float ell, int y, float& ln) {
-  float zn, da, z[CM];
-  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
-  // ce_loss() with the label's logit computed by the same fma instead of
-  // selected from z: the same bits, without a compare per class
-  const float zy = fmaf(da, wcol[y], zL[y * 64]);
-  float m = z[0];
-#pragma unroll
-  for (int c = 1; c < CM; ++c)
-    if (c < C) m = fmaxf(m, z[c]);
-  float s = 0.f;
-#pragma unroll
-  for (int c = 0; c < CM; ++c)
-    if (c < C) s += fast_exp(z[c] - m);
-  ln = (fast_log(s) + m) - zy;
-  return changed ? ln - ell : 0.f;
-}
-
 __device__ __forceinline__ float input_of(const NetDev& net, int layer, float a_raw) {
   return (layer == 0) ? a_raw : act_fn(a_raw, net.act, net.gamma);
 }

@@ -36,7 +36,8 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // Byte offsets of every buffer inside the caller's workspace.
 struct Layout {
   int64_t Ns = 0;
-  int ntiles = 0;
+  int ntiles = 0;     // blocks of the column commit (kTile samples each)
+  int ntiles_ev = 0;  // tiles of the batched evaluation (partial sums per candidate)
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
@@ -202,6 +203,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   Layout lo;
   lo.Ns = (N + 63) / 64 * 64;
   lo.ntiles = (int)((N + mca::kTile - 1) / mca::kTile);
+  lo.ntiles_ev = mca::eval_tiles(N);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -218,7 +220,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.y = take(lo.Ns * sizeof(int32_t));
   lo.cands = take((size_t)k_max * sizeof(mca_cand));
   lo.aux = take((size_t)k_max * sizeof(Aux));
-  lo.partial = take((size_t)k_max * lo.ntiles * sizeof(float));
+  lo.partial = take((size_t)k_max * lo.ntiles_ev * sizeof(float));
   lo.dl = take((size_t)k_max * sizeof(double));
   lo.bsum = take((size_t)lo.ntiles * sizeof(double));
   lo.state = take(sizeof(DevState));
@@ -503,7 +505,7 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
   if (ctx->tf)
     return mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, K, false, ctx->partial,
                                ctx->tf_nblk, ctx->stream);
-  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles, ctx->stream);
+  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles_ev, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
                          ctx->lo.nslab, -2, ctx->st, ctx->dl, ctx->stream);
@@ -519,7 +521,7 @@ hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, in
     return mca::launch_select(net, ctx->partial, ctx->tf_nblk, ctx->cands, nullptr, 0, nullptr, 0,
                               ctx->aux, K, ctx->dl, ctx->st, do_select, trc, trd, kTraceCap,
                               ctx->stream);
-  return mca::launch_select(net, ctx->partial, ctx->lo.ntiles, ctx->cands, ctx->pslab,
+  return mca::launch_select(net, ctx->partial, ctx->lo.ntiles_ev, ctx->cands, ctx->pslab,
                             ctx->lo.nslab, ctx->pchain, ctx->lo.nchain, ctx->aux, K, ctx->dl,
                             ctx->st, do_select, trc, trd, kTraceCap, ctx->stream);
 }

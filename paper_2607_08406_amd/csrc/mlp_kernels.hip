@@ -92,77 +92,268 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
   return dl;
 }
 
-// grid (tiles, K): block (tile, k) sums the loss change of candidate k over
-// the tile's kTile samples; partial[k * ntiles + tile].
-__global__ __launch_bounds__(kTile) void k_eval_column(NetDev net_arg, const mca_cand* cands,
-                                                       const Aux* aux, float* partial,
-                                                       int ntiles) {
-  __shared__ float red[4];
-  __shared__ NetDev net;
-  stage_net(net, net_arg);
-  const int k = blockIdx.y, tile = blockIdx.x;
-  const mca_cand c = cands[k];
-  const Aux a = aux[k];
-  const int64_t n = (int64_t)tile * kTile + threadIdx.x;
-  float dl = 0.f;
-  // candidates below layer L-2 are scored by their own kernel
-  if (c.layer < net.L - 2) return;  // uniform over the block
-  if (a.valid && n < net.N) dl = column_sample<false>(net, c.layer, c.j, c.i, a.de, n);
-  const float s = block_sum_256(dl, red);
-  if (threadIdx.x == 0) partial[(int64_t)k * ntiles + tile] = s;
+// Batched scoring of the candidates whose weight is in the last two layers
+// (a mutated hidden unit of layer L-2 moves the logits by a rank-1 update; a
+// logit-layer weight moves one logit), against the committed state.
+// Block (tile, chunk) scores the kEvK candidates of the chunk on the kEvT
+// samples of the tile:
+//  - the tile's logits, per-sample losses and labels go to LDS;
+//  - wave w takes candidates w, w+8, ... (lane = sample): of the input of the
+//    mutated weight over the tile and, for a hidden unit, its local field
+//    (two coalesced 256-byte rows from HBM per candidate) only the samples
+//    whose input is non-zero can change (about 81 % of an image column is
+//    zero); those pairs are appended to an LDS list with their operands, one
+//    contiguous run per candidate in sample order;
+//  - the whole block scores the list with the pair expressions of the step
+//    loop, each pair writing its loss change beside its operands;
+//  - wave w adds the run of each of its candidates (lane = position in the
+//    run, one fixed butterfly) and writes the tile's partial sum
+//    partial[k * ntiles + tile], which the selection kernel adds over the
+//    tiles in fp64.
+// A run holds the candidate's changed samples in increasing order wherever
+// the list puts it, so the sums do not depend on the order of the appends.
+// Small blocks (about 32 KB of LDS) let several run on a CU at once, so one
+// block's loads overlap the others' scoring.
+constexpr int kEvT = 64;                 // samples per block (one per lane)
+constexpr int kEvK = 32;                 // candidates per block
+constexpr int kEvWaves = 8;
+constexpr int kEvThreads = 64 * kEvWaves;
+constexpr int kEvPer = kEvK / kEvWaves;  // candidates per wave
+static_assert(kEvPer * kEvWaves == kEvK, "candidates split evenly over the waves");
+
+// The caches the batched evaluation reads, resolved on the host.
+struct EvArgs {
+  const float* in_hid;   // input rows of layer L-2: XT (L = 2) or Z[L-3]
+  const float* in_log;   // input rows of layer L-1: XT (L = 1) or Z[L-2]
+  const float* z_hid;    // local fields of layer L-2 (L >= 2)
+  const float* z_log;    // logits, [C][Ns]
+  const float* w_log;    // W[L-1], [C][n_{L-1}]
+  const float* ell;
+  const int32_t* y;
+  const mca_cand* cands;
+  const Aux* aux;
+  float* partial;
+  int64_t N, Ns;
+  int L, C, act, nh, K, ntiles;
+  float gamma;
+};
+
+template <int CM>
+__global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
+  __shared__ float zl_lds[CM * kEvT];       // logits, [class][sample]
+  __shared__ float ell_lds[kEvT];
+  __shared__ int y_lds[kEvT];
+  __shared__ float wcol_lds[kEvK][CM];      // logit-layer column (one-hot for a logit weight)
+  __shared__ float de_lds[kEvK];
+  __shared__ int layer_lds[kEvK], j_lds[kEvK];
+  __shared__ uint16_t code_lds[kEvK * kEvT];  // pair: candidate << 6 | sample
+  __shared__ float ain_lds[kEvK * kEvT];      // pair: input of the mutated weight
+  __shared__ float zh_lds[kEvK * kEvT];       // pair: local field of a mutated hidden unit
+  __shared__ float dl_lds[kEvK * kEvT];       // pair: loss change
+  __shared__ int list_n;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int C = (CM < kCMax) ? CM : a.C, L = a.L;
+  const int act = a.act;
+  const float gamma = a.gamma;
+  const int64_t Ns = a.Ns;
+  const int b = blockIdx.x, k0 = blockIdx.y * kEvK;
+  const int64_t n = (int64_t)b * kEvT + lane;
+  const bool live = n < a.N;
+  if (tid == 0) list_n = 0;
+  // lane q < kEvPer reads the fields of the wave's candidate q (k >= K or a
+  // weight below layer L-2 or beyond the bound: not scored here)
+  int f_layer = -1, f_j = 0, f_i = 0;
+  float f_de = 0.f;
+  {
+    const int k = k0 + wave + kEvWaves * lane;
+    if (lane < kEvPer && k < a.K) {
+      const mca_cand c = a.cands[k];
+      const Aux au = a.aux[k];
+      f_layer = (c.layer >= L - 2 && au.valid) ? c.layer : -1;
+      f_j = c.j;
+      f_i = c.i;
+      f_de = au.de;
+    }
+  }
+  float zl_r[CM], ell_r = 0.f;
+  int y_r = 0;
+  if (wave == 0) {
+#pragma unroll
+    for (int c = 0; c < CM; ++c) zl_r[c] = (live && c < C) ? a.z_log[(int64_t)c * Ns + n] : 0.f;
+    ell_r = live ? a.ell[n] : 0.f;
+    y_r = live ? a.y[n] : 0;
+  }
+  // every row load of the wave is issued before any is used
+  float a_raw[kEvPer], z_raw[kEvPer], wc[kEvPer];
+  int lay[kEvPer], jj[kEvPer];
+#pragma unroll
+  for (int q = 0; q < kEvPer; ++q) {
+    lay[q] = __builtin_amdgcn_readlane(f_layer, q);
+    jj[q] = __builtin_amdgcn_readlane(f_j, q);
+    a_raw[q] = 0.f;
+    z_raw[q] = 0.f;
+    wc[q] = 0.f;
+    if (lay[q] >= 0) {
+      const int i = __builtin_amdgcn_readlane(f_i, q);
+      const bool hid = lay[q] == L - 2;
+      if (live) a_raw[q] = (hid ? a.in_hid : a.in_log)[(int64_t)i * Ns + n];
+      if (live && hid) z_raw[q] = a.z_hid[(int64_t)jj[q] * Ns + n];
+      if (hid && lane < C) wc[q] = a.w_log[(int64_t)lane * a.nh + jj[q]];
+    }
+  }
+  if (wave == 0) {
+#pragma unroll
+    for (int c = 0; c < CM; ++c) zl_lds[c * kEvT + lane] = zl_r[c];
+    ell_lds[lane] = ell_r;
+    y_lds[lane] = y_r;
+  }
+  __syncthreads();  // list_n is clear
+  // each candidate's pairs with a non-zero input are appended as one run, in
+  // sample order, with their operands
+  uint64_t m[kEvPer];
+  float in[kEvPer];
+  int tot = 0;
+#pragma unroll
+  for (int q = 0; q < kEvPer; ++q) {
+    const int kq = wave + kEvWaves * q;
+    m[q] = 0;
+    in[q] = 0.f;
+    if (lay[q] >= 0) {
+      const bool hid = lay[q] == L - 2;
+      in[q] = (lay[q] == 0) ? a_raw[q] : act_fn(a_raw[q], act, gamma);
+      if (lane < CM) wcol_lds[kq][lane] = hid ? wc[q] : ((lane == jj[q]) ? 1.f : 0.f);
+      if (lane == 0) {
+        de_lds[kq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f_de), q));
+        layer_lds[kq] = lay[q];
+        j_lds[kq] = jj[q];
+      }
+      m[q] = __ballot(live && in[q] != 0.f);
+      tot += (int)__popcll(m[q]);
+    }
+  }
+  int base = 0;
+  if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
+  base = __builtin_amdgcn_readfirstlane(__shfl(base, 0, 64));
+  const uint64_t below = (1ull << lane) - 1ull;
+  int run_base[kEvPer], run_len[kEvPer];
+#pragma unroll
+  for (int q = 0; q < kEvPer; ++q) {
+    const int cnt = (int)__popcll(m[q]);
+    run_base[q] = base;
+    run_len[q] = cnt;
+    if ((m[q] >> lane) & 1ull) {
+      const int e = base + (int)__popcll(m[q] & below);
+      code_lds[e] = (uint16_t)(((wave + kEvWaves * q) << 6) | lane);
+      ain_lds[e] = in[q];
+      zh_lds[e] = z_raw[q];
+    }
+    base += cnt;
+  }
+  __syncthreads();
+  // scoring: the whole block shares out the list
+  const int n_list = list_n;
+  for (int e = tid; e < n_list; e += kEvThreads) {
+    const int code = code_lds[e];
+    const int kq = code >> 6, sl = code & 63;
+    float ln;
+    dl_lds[e] = pair_eval<CM>(L, C, act, gamma, layer_lds[kq], j_lds[kq], de_lds[kq], wcol_lds[kq],
+                              ain_lds[e], zh_lds[e], &zl_lds[sl], ell_lds[sl], y_lds[sl], ln);
+  }
+  __syncthreads();
+  // the tile's partial sum of each of the wave's candidates
+#pragma unroll
+  for (int q = 0; q < kEvPer; ++q) {
+    if (lay[q] >= 0) {
+      const float v = wave_sum_f32(lane < run_len[q] ? dl_lds[run_base[q] + lane] : 0.f);
+      if (lane == 0) a.partial[(int64_t)(k0 + wave + kEvWaves * q) * a.ntiles + b] = v;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
 // selection (Eq. 6): one block, thread k owns candidate k
 // ---------------------------------------------------------------------------
 
-// A candidate in layer slab_layer (L-3 for nets of three or more layers)
-// takes its tile sums from pslab[k * nslab + b], one in layers 0..chain_top
-// (L-4 for deeper nets) from pchain[k * nchain + b].  Sixteen threads add a candidate's
-// tile sums: thread r takes tiles r, r+16, ... in order, then a fixed
-// butterfly joins the sixteen (fp64).
-__global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, const float* partial, int ntiles,
-                                                  const mca_cand* cands, const float* pslab,
-                                                  int nslab, int slab_layer, const float* pchain,
-                                                  int nchain, int chain_top,
-                                                  const Aux* aux, int K, double* dL,
-                                                  DevState* st, int do_select,
-                                                  int32_t* tr_chosen, double* tr_dl,
-                                                  int64_t tr_cap) {
+// Where candidate k's tile sums are.
+struct PartialSrc {
+  const float* partial;  // last two layers: partial[k * ntiles + b]
+  int ntiles;
+  const float* pslab;    // layer slab_layer (L-3 for nets of three or more layers)
+  int nslab, slab_layer;
+  const float* pchain;   // layers 0..chain_top (L-4 for deeper nets)
+  int nchain, chain_top;
+};
+
+// The loss change of candidate k (+inf when rejected by the bound) from its
+// tile sums, by sixteen lanes: lane r adds tiles r, r+16, ... in order, then
+// a fixed butterfly joins the sixteen (fp64).  Valid in lane r = 0; every
+// lane of the sixteen must call it.
+__device__ __forceinline__ double candidate_dl(const NetDev& net, const PartialSrc& src,
+                                               const mca_cand* cands, const Aux* aux, int K,
+                                               int k, int r) {
+  double s = 0.0;
+  if (k < K) {
+    const int layer = cands[k].layer;
+    const float* p = src.partial + (int64_t)k * src.ntiles;
+    int nt = src.ntiles;
+    if (layer <= src.chain_top) {
+      p = src.pchain + (int64_t)k * src.nchain;
+      nt = src.nchain;
+    } else if (layer == src.slab_layer) {
+      p = src.pslab + (int64_t)k * src.nslab;
+      nt = src.nslab;
+    }
+    // 32 loads in flight (up to 512 partials in one round trip), added in
+    // order: lane r adds partials r, r+16, r+32, ...
+    constexpr int kLoads = 32;
+    for (int t0 = r; t0 < nt; t0 += 16 * kLoads) {
+      float v[kLoads];
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u) v[u] = (t0 + 16 * u < nt) ? gload(&p[t0 + 16 * u]) : 0.f;
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u)
+        if (t0 + 16 * u < nt) s += (double)v[u];
+    }
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  return (k < K && aux[k].valid) ? s / (double)net.N : __builtin_huge_val();
+}
+
+// Loss changes of many candidates: block b adds the tile sums of candidates
+// 16b .. 16b+15 into dL (the same arithmetic as the one-block selection).
+constexpr int kReduceThreads = 256;
+__global__ __launch_bounds__(kReduceThreads) void k_reduce_dl(const NetDev net, PartialSrc src,
+                                                             const mca_cand* cands,
+                                                             const Aux* aux, int K, double* dL) {
+  const int k = blockIdx.x * (kReduceThreads / 16) + (threadIdx.x >> 4), r = threadIdx.x & 15;
+  const double v = candidate_dl(net, src, cands, aux, K, k, r);
+  if (k < K && r == 0) dL[k] = v;
+}
+
+// The selection proper: the first candidate that passes the test, the trace
+// and the counters.  With summed = 0 it also adds the tile sums (one block
+// for all K: the few-candidate steps of the per-phase loop); with summed = 1
+// k_reduce_dl has already written dL.
+__global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, PartialSrc src,
+                                                  const mca_cand* cands, const Aux* aux, int K,
+                                                  int summed, double* dL, DevState* st,
+                                                  int do_select, int32_t* tr_chosen,
+                                                  double* tr_dl, int64_t tr_cap) {
   __shared__ int first;
   __shared__ int ntie;
   __shared__ double vals[kMaxK];
   const int tid = threadIdx.x;
   if (tid == 0) { first = K; ntie = 0; }
-  for (int k0 = 0; k0 < K; k0 += kMaxK / 16) {
-    const int k = k0 + (tid >> 4), r = tid & 15;
-    double s = 0.0;
-    if (k < K) {
-      const int layer = cands[k].layer;
-      const float* p = partial + (int64_t)k * ntiles;
-      int nt = ntiles;
-      if (layer <= chain_top) {
-        p = pchain + (int64_t)k * nchain;
-        nt = nchain;
-      } else if (layer == slab_layer) {
-        p = pslab + (int64_t)k * nslab;
-        nt = nslab;
-      }
-      // 32 loads in flight (up to 512 partials in one round trip), added in
-      // order: thread r adds partials r, r+16, r+32, ...
-      constexpr int kLoads = 32;
-      for (int t0 = r; t0 < nt; t0 += 16 * kLoads) {
-        float v[kLoads];
-#pragma unroll
-        for (int u = 0; u < kLoads; ++u) v[u] = (t0 + 16 * u < nt) ? gload(&p[t0 + 16 * u]) : 0.f;
-#pragma unroll
-        for (int u = 0; u < kLoads; ++u)
-          if (t0 + 16 * u < nt) s += (double)v[u];
-      }
+  if (summed) {
+    if (tid < K) vals[tid] = dL[tid];
+  } else {
+    for (int k0 = 0; k0 < K; k0 += kMaxK / 16) {
+      const int k = k0 + (tid >> 4), r = tid & 15;
+      const double v = candidate_dl(net, src, cands, aux, K, k, r);
+      if (k < K && r == 0) vals[k] = v;
     }
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-    if (k < K && r == 0) vals[k] = aux[k].valid ? s / (double)net.N : __builtin_huge_val();
   }
   __syncthreads();
   const int k = tid;
@@ -335,10 +526,36 @@ hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* 
   return hipGetLastError();
 }
 
+int eval_tiles(int64_t n_samples) { return (int)((n_samples + kEvT - 1) / kEvT); }
+
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        float* partial, int ntiles, hipStream_t s) {
-  hipLaunchKernelGGL(k_eval_column, dim3(ntiles, K), dim3(kTile), 0, s, net, cands, aux,
-                     partial, ntiles);
+  const int L = net.L;
+  EvArgs a{};
+  a.in_hid = (L >= 3) ? net.Z[L - 3] : net.XT;
+  a.in_log = (L >= 2) ? net.Z[L - 2] : net.XT;
+  a.z_hid = (L >= 2) ? net.Z[L - 2] : nullptr;
+  a.z_log = net.Z[L - 1];
+  a.w_log = net.W[L - 1];
+  a.ell = net.ell;
+  a.y = net.y;
+  a.cands = cands;
+  a.aux = aux;
+  a.partial = partial;
+  a.N = net.N;
+  a.Ns = net.Ns;
+  a.L = L;
+  a.C = net.C;
+  a.act = net.act;
+  a.nh = net.widths[L - 1];
+  a.K = K;
+  a.ntiles = ntiles;
+  a.gamma = net.gamma;
+  const dim3 grid((unsigned)ntiles, (unsigned)((K + kEvK - 1) / kEvK));
+  if (net.C == 10)
+    hipLaunchKernelGGL(k_eval_tiles<10>, grid, dim3(kEvThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_eval_tiles<kCMax>, grid, dim3(kEvThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -347,11 +564,26 @@ hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
                          const float* pchain, int nchain, const Aux* aux, int K, double* dL,
                          DevState* st, bool do_select, int32_t* tr_chosen, double* tr_dl,
                          int64_t tr_cap, hipStream_t s) {
-  const int slab_layer = (net.L >= 3) ? net.L - 3 : -1;
-  const int chain_top = (net.L >= 4) ? net.L - 4 : -1;
-  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, partial, ntiles, cands, pslab,
-                     nslab, slab_layer, pchain, nchain, chain_top, aux, K, dL, st,
-                     do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
+  PartialSrc src;
+  src.partial = partial;
+  src.ntiles = ntiles;
+  src.pslab = pslab;
+  src.nslab = nslab;
+  src.slab_layer = (net.L >= 3) ? net.L - 3 : -1;
+  src.pchain = pchain;
+  src.nchain = nchain;
+  src.chain_top = (net.L >= 4) ? net.L - 4 : -1;
+  // more candidates than one block sums in one pass: spread the sums
+  const int summed = K > kMaxK / 16;
+  if (summed) {
+    constexpr int per = kReduceThreads / 16;
+    hipLaunchKernelGGL(k_reduce_dl, dim3((K + per - 1) / per), dim3(kReduceThreads), 0, s, net,
+                       src, cands, aux, K, dL);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, src, cands, aux, K, summed, dL,
+                     st, do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
   return hipGetLastError();
 }
 

@@ -11,6 +11,9 @@ hipError_t launch_propose(const NetDev& net, uint64_t t, bool use_dev_t, const D
                           int K, mca_cand* cands, Aux* aux, hipStream_t s);
 hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* aux,
                           hipStream_t s);
+// Tiles of the batched evaluation for n samples; launch_eval writes
+// partial[k * ntiles + tile] for the candidates in the last two layers.
+int eval_tiles(int64_t n_samples);
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        float* partial, int ntiles, hipStream_t s);
 hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,

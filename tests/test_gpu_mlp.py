@@ -121,6 +121,49 @@ def test_full_wide_workload(mca):
     ctx.close()
 
 
+def test_wide_batched_evaluation(mca):
+    """The batched evaluation at the size the benchmark's incremental-phase
+    measurement uses: 1,000 candidates of one step of the 784-16384-10 stream
+    (15 full chunks of 64 and a ragged chunk of 40; 157 sample tiles, the last
+    holding 16 samples) scored in one launch against the committed state, every
+    loss against the fp64 oracle, then the first improver committed."""
+    cfg = CONFIGS["wide"]
+    banner("wide 784-16384-10 N=10000 batched evaluation K=1000")
+    w = mlp_workload(cfg)
+    K = 1000
+    ctx, ref = make_pair(cfg, w, k_max=K)
+    cands = ctx.propose(7, K)
+    L_t, rc, rl, chosen = omca.evaluate(ref, 7, K, cfg.seed_stream, cfg.stream_tag, cfg.delta)
+    assert_cands_equal(cands, rc)
+    assert sum(int(c["layer"]) == 1 for c in cands) > 0  # logit-layer weights too
+    losses, dl = ctx.eval_losses(cands)
+    check_losses(losses, L_t, rl)
+    assert chosen >= 0
+    ctx.commit(chosen)
+    ref.commit(rc[chosen], rl[chosen])
+    assert_state_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ctx.close()
+
+
+def test_single_layer_net(mca):
+    """A net with no hidden layer (784-10): every candidate is a logit-layer
+    weight fed straight by the pixels."""
+    cfg = CONFIGS["wide"].scaled(name="linear", widths=(784, 10), n_samples=700, K=100)
+    banner("784-10 N=700 explicit steps K=100 and device loop K=64")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=100)
+    ties, acc = explicit_steps(ctx, ref, cfg, 0, 10, 100)
+    assert acc > 3
+    assert_state_equal(ctx, ref)
+    ctx.set_step(10)
+    st, ch, dl = ctx.run_steps(20, 64, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 10, ch, dl, 64)
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
 def test_zero_increment_and_bound(mca):
     cfg = small_wide()
     w = mlp_workload(cfg)
