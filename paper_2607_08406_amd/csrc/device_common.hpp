@@ -163,7 +163,7 @@ __device__ __forceinline__ float ce_loss(const float (&z)[CM], int C, int y) {
 
 // One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
 // the activation feeding it); zh: the cached local field of the mutated unit
-// when it is a hidden unit; zL: the sample's logits in LDS (stride 64).  The
+// when it is a hidden unit; zL: the sample's logits in LDS (class stride ZS).  The
 // new local field, logits and loss come back for a commit.  Written without
 // branches on the candidate's layer (pairs of different candidates share a
 // wave); the step loop and the batched evaluation both score pairs with
@@ -185,7 +185,7 @@ __device__ __forceinline__ bool pair_logits_of(int C, int act, float gamma, bool
   return logit ? dz != 0.f : da != 0.f;  // the logits changed
 }
 
-template <int CM>
+template <int CM, int ZS = 64>
 __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
                                             float de, const float* wcol, float ain, float zh,
                                             const float* zL, float& zn, float& da,
@@ -196,23 +196,23 @@ __device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, 
   float zc[CM], wc[CM];
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) {
-    zc[cc] = zL[cc * 64];
+    zc[cc] = zL[cc * ZS];
     wc[cc] = wcol[cc];
   }
-  const float zb = logit ? zL[j * 64] : zh;
+  const float zb = logit ? zL[j * ZS] : zh;
   return pair_logits_of<CM>(C, act, gamma, logit, zb, de, wc, ain, zc, zn, da, z);
 }
 
 // The pair's new loss ln; returns its loss change.
-template <int CM>
+template <int CM, int ZS = 64>
 __device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
                                            float de, const float* wcol, float ain, float zh,
                                            const float* zL, float ell, int y, float& ln) {
   float zn, da, z[CM];
-  const bool changed = pair_logits<CM>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
+  const bool changed = pair_logits<CM, ZS>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
   // ce_loss() with the label's logit computed by the same fma instead of
   // selected from z: the same bits, without a compare per class
-  const float zy = fmaf(da, wcol[y], zL[y * 64]);
+  const float zy = fmaf(da, wcol[y], zL[y * ZS]);
   float m = z[0];
 #pragma unroll
   for (int c = 1; c < CM; ++c)

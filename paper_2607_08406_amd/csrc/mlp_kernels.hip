@@ -95,58 +95,76 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
 // Batched scoring of the candidates whose weight is in the last two layers
 // (a mutated hidden unit of layer L-2 moves the logits by a rank-1 update; a
 // logit-layer weight moves one logit), against the committed state.
-// Block (tile, chunk) scores the kEvK candidates of the chunk on the kEvT
-// samples of the tile:
-//  - the tile's logits, per-sample losses and labels go to LDS;
-//  - wave w takes candidates w, w+8, ... (lane = sample): of the input of the
-//    mutated weight over the tile and, for a hidden unit, its local field
-//    (two coalesced 256-byte rows from HBM per candidate) only the samples
-//    whose input is non-zero can change (about 81 % of an image column is
-//    zero); those pairs are appended to an LDS list with their operands, one
-//    contiguous run per candidate in sample order;
+// Work items are (tile, chunk) pairs: the kEvT = 256 samples of a tile
+// against the kEvK candidates of a chunk.  A persistent grid (as many blocks
+// as fit the GPU at once) walks the items, block g taking items g, g + G, ...;
+// per item:
+//  - the tile's logits, per-sample losses and labels land in LDS;
+//  - wave w lands candidates w, w+8, ...: lane l holds samples 4l .. 4l+3 of
+//    the input of the mutated weight and, for a hidden unit, of its local
+//    field (two 1-KB rows per candidate, one 16-byte load per lane each); of
+//    these only the samples whose input is non-zero can change (about 81 % of
+//    an image column is zero); those pairs are appended to an LDS list with
+//    their operands, one contiguous run per candidate in sample order;
 //  - the whole block scores the list with the pair expressions of the step
 //    loop, each pair writing its loss change beside its operands;
-//  - wave w adds the run of each of its candidates (lane = position in the
-//    run, one fixed butterfly) and writes the tile's partial sum
-//    partial[k * ntiles + tile], which the selection kernel adds over the
-//    tiles in fp64.
+//  - wave w adds the run of each of its candidates in one fixed order and
+//    writes the tile's partial sum partial[k * ntiles + tile], which the
+//    selection kernel adds over the tiles in fp64.
 // A run holds the candidate's changed samples in increasing order wherever
-// the list puts it, so the sums do not depend on the order of the appends.
-// Small blocks (about 32 KB of LDS) let several run on a CU at once, so one
-// block's loads overlap the others' scoring.
-constexpr int kEvT = 64;                 // samples per block (one per lane)
-constexpr int kEvK = 32;                 // candidates per block
+// the list puts it, so the sums do not depend on the order of the appends or
+// on the grid size.  The rows of the next item are requested before the
+// current item is scored and the candidates' fields one item earlier still,
+// so no memory latency sits between two items.  Every load is issued
+// unconditionally from an address inside its array (a candidate that is not
+// scored here reads row 0, a sample group past the padded rows reads the
+// tile's first group) and its value is selected where it is used: a load
+// under a branch would make the merge of the branches wait for every load in
+// flight.
+constexpr int kEvT = 256;                // samples per item (four per lane)
+constexpr int kEvK = 16;                 // candidates per item
 constexpr int kEvWaves = 8;
 constexpr int kEvThreads = 64 * kEvWaves;
 constexpr int kEvPer = kEvK / kEvWaves;  // candidates per wave
 static_assert(kEvPer * kEvWaves == kEvK, "candidates split evenly over the waves");
+static_assert(kEvK <= 16 && kEvT <= 256, "a pair code holds a candidate in 4 bits, a sample in 8");
 
 // The caches the batched evaluation reads, resolved on the host.
 struct EvArgs {
   const float* in_hid;   // input rows of layer L-2: XT (L = 2) or Z[L-3]
   const float* in_log;   // input rows of layer L-1: XT (L = 1) or Z[L-2]
-  const float* z_hid;    // local fields of layer L-2 (L >= 2)
+  const float* z_hid;    // local fields of layer L-2 (L = 1: the logits, never used)
   const float* z_log;    // logits, [C][Ns]
   const float* w_log;    // W[L-1], [C][n_{L-1}]
-  const float* ell;
-  const int32_t* y;
+  const float* ell;      // [Ns]
+  const int32_t* y;      // [Ns]
   const mca_cand* cands;
   const Aux* aux;
   float* partial;
   int64_t N, Ns;
-  int L, C, act, nh, K, ntiles;
+  int L, C, act, nh, K, ntiles, nchunks;
   float gamma;
+};
+
+// A wave's candidates of one item as loaded: lane q holds candidate
+// chunk * kEvK + wave + kEvWaves * q for q < kEvPer (read from a clamped index
+// for the other lanes and beyond K; ok() rules them out).
+struct EvFields {
+  int layer, j, i, valid, k;
+  float de;
 };
 
 template <int CM>
 __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
+  constexpr int kRows = CM + 2;                             // logits, losses, labels
+  constexpr int kRowsPer = (kRows + kEvWaves - 1) / kEvWaves;
   __shared__ float zl_lds[CM * kEvT];       // logits, [class][sample]
   __shared__ float ell_lds[kEvT];
   __shared__ int y_lds[kEvT];
   __shared__ float wcol_lds[kEvK][CM];      // logit-layer column (one-hot for a logit weight)
   __shared__ float de_lds[kEvK];
   __shared__ int layer_lds[kEvK], j_lds[kEvK];
-  __shared__ uint16_t code_lds[kEvK * kEvT];  // pair: candidate << 6 | sample
+  __shared__ uint16_t code_lds[kEvK * kEvT];  // pair: candidate << 8 | sample
   __shared__ float ain_lds[kEvK * kEvT];      // pair: input of the mutated weight
   __shared__ float zh_lds[kEvK * kEvT];       // pair: local field of a mutated hidden unit
   __shared__ float dl_lds[kEvK * kEvT];       // pair: loss change
@@ -156,118 +174,181 @@ __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
   const int C = (CM < kCMax) ? CM : a.C, L = a.L;
   const int act = a.act;
   const float gamma = a.gamma;
-  const int64_t Ns = a.Ns;
-  const int b = blockIdx.x, k0 = blockIdx.y * kEvK;
-  const int64_t n = (int64_t)b * kEvT + lane;
-  const bool live = n < a.N;
-  if (tid == 0) list_n = 0;
-  // lane q < kEvPer reads the fields of the wave's candidate q (k >= K or a
-  // weight below layer L-2 or beyond the bound: not scored here)
-  int f_layer = -1, f_j = 0, f_i = 0;
-  float f_de = 0.f;
-  {
-    const int k = k0 + wave + kEvWaves * lane;
-    if (lane < kEvPer && k < a.K) {
-      const mca_cand c = a.cands[k];
-      const Aux au = a.aux[k];
-      f_layer = (c.layer >= L - 2 && au.valid) ? c.layer : -1;
-      f_j = c.j;
-      f_i = c.i;
-      f_de = au.de;
+  const int64_t Ns = a.Ns, N = a.N;
+  const int ntiles = a.ntiles, K = a.K;
+  const int n_items = ntiles * a.nchunks;
+  const int G = (int)gridDim.x;
+
+  auto load_fields = [&](int item, EvFields& f) {
+    const int it = item < n_items ? item : n_items - 1;
+    const int k = (it / ntiles) * kEvK + wave + kEvWaves * (lane % kEvPer);
+    const int kc = k < K ? k : K - 1;
+    f.layer = a.cands[kc].layer;
+    f.j = a.cands[kc].j;
+    f.i = a.cands[kc].i;
+    f.valid = a.aux[kc].valid;
+    f.de = a.aux[kc].de;
+    f.k = (item < n_items) ? k : K;
+  };
+  // candidate q of the wave is scored here: its weight is in the last two
+  // layers and within the bound
+  auto ok = [&](const EvFields& f, int q) {
+    return __builtin_amdgcn_readlane(f.k, q) < K && __builtin_amdgcn_readlane(f.layer, q) >= L - 2 &&
+           __builtin_amdgcn_readlane(f.valid, q) != 0;
+  };
+  // first sample of the lane's group in item's tile, clamped into the rows
+  auto group0 = [&](int item) {
+    const int64_t s0 = (int64_t)(item % ntiles) * kEvT + 4 * lane;
+    return s0 < Ns ? s0 : (int64_t)(item % ntiles) * kEvT;
+  };
+  float4 a4[kEvPer], z4[kEvPer], r4[kRowsPer];
+  float wc[kEvPer];
+  auto issue_rows = [&](int item, const EvFields& f) {
+    const int64_t s0 = group0(item);
+#pragma unroll
+    for (int u = 0; u < kRowsPer; ++u) {
+      const int r = wave + kEvWaves * u;  // row r of the tile: logit r < C, then losses, labels
+      const float* row = (r < C) ? a.z_log + (int64_t)r * Ns
+                                 : ((r == kRows - 2) ? a.ell : (const float*)a.y);
+      r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
     }
-  }
-  float zl_r[CM], ell_r = 0.f;
-  int y_r = 0;
-  if (wave == 0) {
 #pragma unroll
-    for (int c = 0; c < CM; ++c) zl_r[c] = (live && c < C) ? a.z_log[(int64_t)c * Ns + n] : 0.f;
-    ell_r = live ? a.ell[n] : 0.f;
-    y_r = live ? a.y[n] : 0;
-  }
-  // every row load of the wave is issued before any is used
-  float a_raw[kEvPer], z_raw[kEvPer], wc[kEvPer];
-  int lay[kEvPer], jj[kEvPer];
-#pragma unroll
-  for (int q = 0; q < kEvPer; ++q) {
-    lay[q] = __builtin_amdgcn_readlane(f_layer, q);
-    jj[q] = __builtin_amdgcn_readlane(f_j, q);
-    a_raw[q] = 0.f;
-    z_raw[q] = 0.f;
-    wc[q] = 0.f;
-    if (lay[q] >= 0) {
-      const int i = __builtin_amdgcn_readlane(f_i, q);
-      const bool hid = lay[q] == L - 2;
-      if (live) a_raw[q] = (hid ? a.in_hid : a.in_log)[(int64_t)i * Ns + n];
-      if (live && hid) z_raw[q] = a.z_hid[(int64_t)jj[q] * Ns + n];
-      if (hid && lane < C) wc[q] = a.w_log[(int64_t)lane * a.nh + jj[q]];
+    for (int q = 0; q < kEvPer; ++q) {
+      const bool use = ok(f, q);
+      const int l = __builtin_amdgcn_readlane(f.layer, q);
+      const bool hid = use && l == L - 2;
+      const int i = use ? __builtin_amdgcn_readlane(f.i, q) : 0;
+      const int j = hid ? __builtin_amdgcn_readlane(f.j, q) : 0;
+      a4[q] = *(const float4*)&(hid ? a.in_hid : a.in_log)[(int64_t)i * Ns + s0];
+      z4[q] = *(const float4*)&(hid ? a.z_hid : a.z_log)[(int64_t)j * Ns + s0];
+      wc[q] = a.w_log[(int64_t)(lane < C ? lane : 0) * a.nh + j];
     }
-  }
-  if (wave == 0) {
-#pragma unroll
-    for (int c = 0; c < CM; ++c) zl_lds[c * kEvT + lane] = zl_r[c];
-    ell_lds[lane] = ell_r;
-    y_lds[lane] = y_r;
-  }
-  __syncthreads();  // list_n is clear
-  // each candidate's pairs with a non-zero input are appended as one run, in
-  // sample order, with their operands
-  uint64_t m[kEvPer];
-  float in[kEvPer];
-  int tot = 0;
-#pragma unroll
-  for (int q = 0; q < kEvPer; ++q) {
-    const int kq = wave + kEvWaves * q;
-    m[q] = 0;
-    in[q] = 0.f;
-    if (lay[q] >= 0) {
-      const bool hid = lay[q] == L - 2;
-      in[q] = (lay[q] == 0) ? a_raw[q] : act_fn(a_raw[q], act, gamma);
-      if (lane < CM) wcol_lds[kq][lane] = hid ? wc[q] : ((lane == jj[q]) ? 1.f : 0.f);
-      if (lane == 0) {
-        de_lds[kq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f_de), q));
-        layer_lds[kq] = lay[q];
-        j_lds[kq] = jj[q];
-      }
-      m[q] = __ballot(live && in[q] != 0.f);
-      tot += (int)__popcll(m[q]);
-    }
-  }
-  int base = 0;
-  if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
-  base = __builtin_amdgcn_readfirstlane(__shfl(base, 0, 64));
-  const uint64_t below = (1ull << lane) - 1ull;
+  };
   int run_base[kEvPer], run_len[kEvPer];
+  // the item's rows go to LDS; each candidate's pairs with a non-zero input
+  // are appended as one run, in sample order, with their operands
+  auto land = [&](int item, const EvFields& f) {
+    const int64_t s0 = (int64_t)(item % ntiles) * kEvT + 4 * lane;
 #pragma unroll
-  for (int q = 0; q < kEvPer; ++q) {
-    const int cnt = (int)__popcll(m[q]);
-    run_base[q] = base;
-    run_len[q] = cnt;
-    if ((m[q] >> lane) & 1ull) {
-      const int e = base + (int)__popcll(m[q] & below);
-      code_lds[e] = (uint16_t)(((wave + kEvWaves * q) << 6) | lane);
-      ain_lds[e] = in[q];
-      zh_lds[e] = z_raw[q];
+    for (int u = 0; u < kRowsPer; ++u) {
+      const int r = wave + kEvWaves * u;
+      if (r < kRows) {
+        float* dst = (r < CM) ? &zl_lds[r * kEvT] : ((r == kRows - 2) ? ell_lds : (float*)y_lds);
+        const float4 v = r4[u];
+        const bool keep = r >= CM || r < C;  // logit rows past C stay zero
+        float4 w;
+        w.x = (keep && s0 + 0 < N) ? v.x : 0.f;
+        w.y = (keep && s0 + 1 < N) ? v.y : 0.f;
+        w.z = (keep && s0 + 2 < N) ? v.z : 0.f;
+        w.w = (keep && s0 + 3 < N) ? v.w : 0.f;
+        *(float4*)&dst[4 * lane] = w;
+      }
     }
-    base += cnt;
-  }
-  __syncthreads();
-  // scoring: the whole block shares out the list
-  const int n_list = list_n;
-  for (int e = tid; e < n_list; e += kEvThreads) {
-    const int code = code_lds[e];
-    const int kq = code >> 6, sl = code & 63;
-    float ln;
-    dl_lds[e] = pair_eval<CM>(L, C, act, gamma, layer_lds[kq], j_lds[kq], de_lds[kq], wcol_lds[kq],
-                              ain_lds[e], zh_lds[e], &zl_lds[sl], ell_lds[sl], y_lds[sl], ln);
-  }
-  __syncthreads();
-  // the tile's partial sum of each of the wave's candidates
+    uint64_t b0[kEvPer], b1[kEvPer], b2[kEvPer], b3[kEvPer];
+    float in[kEvPer][4];
+    int tot = 0;
 #pragma unroll
-  for (int q = 0; q < kEvPer; ++q) {
-    if (lay[q] >= 0) {
-      const float v = wave_sum_f32(lane < run_len[q] ? dl_lds[run_base[q] + lane] : 0.f);
-      if (lane == 0) a.partial[(int64_t)(k0 + wave + kEvWaves * q) * a.ntiles + b] = v;
+    for (int q = 0; q < kEvPer; ++q) {
+      const int kq = wave + kEvWaves * q;
+      b0[q] = b1[q] = b2[q] = b3[q] = 0;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) in[q][t] = 0.f;
+      if (ok(f, q)) {
+        const int l = __builtin_amdgcn_readlane(f.layer, q);
+        const int j = __builtin_amdgcn_readlane(f.j, q);
+        const bool hid = l == L - 2;
+        const float av[4] = {a4[q].x, a4[q].y, a4[q].z, a4[q].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) in[q][t] = (l == 0) ? av[t] : act_fn(av[t], act, gamma);
+        if (lane < CM) wcol_lds[kq][lane] = (hid && lane < C) ? wc[q] : ((lane == j) ? 1.f : 0.f);
+        if (lane == 0) {
+          de_lds[kq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f.de), q));
+          layer_lds[kq] = l;
+          j_lds[kq] = j;
+        }
+        b0[q] = __ballot(s0 + 0 < N && in[q][0] != 0.f);
+        b1[q] = __ballot(s0 + 1 < N && in[q][1] != 0.f);
+        b2[q] = __ballot(s0 + 2 < N && in[q][2] != 0.f);
+        b3[q] = __ballot(s0 + 3 < N && in[q][3] != 0.f);
+        tot += (int)(__popcll(b0[q]) + __popcll(b1[q]) + __popcll(b2[q]) + __popcll(b3[q]));
+      }
     }
+    int base = 0;
+    if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
+    base = __builtin_amdgcn_readfirstlane(__shfl(base, 0, 64));
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int q = 0; q < kEvPer; ++q) {
+      const int cnt = (int)(__popcll(b0[q]) + __popcll(b1[q]) + __popcll(b2[q]) + __popcll(b3[q]));
+      run_base[q] = base;
+      run_len[q] = cnt;
+      // pairs of lower lanes come first, then the lane's own in sample order
+      int e = base + (int)(__popcll(b0[q] & below) + __popcll(b1[q] & below) +
+                           __popcll(b2[q] & below) + __popcll(b3[q] & below));
+      const uint64_t bt[4] = {b0[q], b1[q], b2[q], b3[q]};
+      const float zv[4] = {z4[q].x, z4[q].y, z4[q].z, z4[q].w};
+      const int kq = wave + kEvWaves * q;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if ((bt[t] >> lane) & 1ull) {
+          code_lds[e] = (uint16_t)((kq << 8) | (4 * lane + t));
+          ain_lds[e] = in[q][t];
+          zh_lds[e] = zv[t];
+          ++e;
+        }
+      }
+      base += cnt;
+    }
+  };
+
+  // One item: fn holds the fields of item + G (its rows are requested here),
+  // fnn receives those of item + 2G.  The three field sets change roles by
+  // position in the unrolled loop below, not by copies: a copy of registers
+  // still being loaded would wait for every load in flight.
+  int item = (int)blockIdx.x;
+  auto step = [&](const EvFields& f, const EvFields& fn, EvFields& fnn) {
+    load_fields(item + 2 * G, fnn);
+    if (tid == 0) list_n = 0;
+    __syncthreads();  // the last item's sums are done with the list
+    land(item, f);
+    __syncthreads();
+    if (item + G < n_items) issue_rows(item + G, fn);
+    // scoring: the whole block shares out the list
+    const int n_list = list_n;
+    for (int e = tid; e < n_list; e += kEvThreads) {
+      const int code = code_lds[e];
+      const int kq = code >> 8, sl = code & 255;
+      float ln;
+      dl_lds[e] = pair_eval<CM, kEvT>(L, C, act, gamma, layer_lds[kq], j_lds[kq], de_lds[kq],
+                                      wcol_lds[kq], ain_lds[e], zh_lds[e], &zl_lds[sl],
+                                      ell_lds[sl], y_lds[sl], ln);
+    }
+    __syncthreads();
+    // the tile's partial sum of each of the wave's candidates: lane l adds
+    // run entries l, l+64, l+128, l+192 in that order, then one butterfly
+    const int b = item % ntiles;
+#pragma unroll
+    for (int q = 0; q < kEvPer; ++q) {
+      if (ok(f, q)) {
+        float v = 0.f;
+#pragma unroll
+        for (int r = 0; r < kEvT / 64; ++r) {
+          const int idx = lane + 64 * r;
+          v += (idx < run_len[q]) ? dl_lds[run_base[q] + idx] : 0.f;
+        }
+        v = wave_sum_f32(v);
+        if (lane == 0) a.partial[(int64_t)__builtin_amdgcn_readlane(f.k, q) * ntiles + b] = v;
+      }
+    }
+    item += G;
+    return item < n_items;
+  };
+  EvFields f0, f1, f2;
+  load_fields(item, f0);
+  load_fields(item + G, f1);
+  if (item >= n_items) return;
+  issue_rows(item, f0);
+  while (step(f0, f1, f2) && step(f1, f2, f0) && step(f2, f0, f1)) {
   }
 }
 
@@ -528,13 +609,31 @@ hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* 
 
 int eval_tiles(int64_t n_samples) { return (int)((n_samples + kEvT - 1) / kEvT); }
 
+namespace {
+// Blocks of k_eval_tiles that fit the device at once (queried once per
+// device and class-count variant).
+int eval_grid(const void* kernel, int variant) {
+  static int cached[16][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return 0;
+  if (cached[dev][variant] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kEvThreads, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    cached[dev][variant] = (per_cu > 0 ? per_cu : 1) * cus;
+  }
+  return cached[dev][variant];
+}
+}  // namespace
+
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        float* partial, int ntiles, hipStream_t s) {
   const int L = net.L;
   EvArgs a{};
   a.in_hid = (L >= 3) ? net.Z[L - 3] : net.XT;
   a.in_log = (L >= 2) ? net.Z[L - 2] : net.XT;
-  a.z_hid = (L >= 2) ? net.Z[L - 2] : nullptr;
+  a.z_hid = (L >= 2) ? net.Z[L - 2] : net.Z[L - 1];
   a.z_log = net.Z[L - 1];
   a.w_log = net.W[L - 1];
   a.ell = net.ell;
@@ -550,9 +649,15 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   a.nh = net.widths[L - 1];
   a.K = K;
   a.ntiles = ntiles;
+  a.nchunks = (K + kEvK - 1) / kEvK;
   a.gamma = net.gamma;
-  const dim3 grid((unsigned)ntiles, (unsigned)((K + kEvK - 1) / kEvK));
-  if (net.C == 10)
+  const bool c10 = net.C == 10;
+  const void* kernel = c10 ? (const void*)k_eval_tiles<10> : (const void*)k_eval_tiles<kCMax>;
+  const int fit = eval_grid(kernel, c10 ? 0 : 1);
+  if (fit <= 0) return hipErrorInvalidDevice;
+  const int items = ntiles * a.nchunks;
+  const dim3 grid((unsigned)(items < fit ? items : fit));
+  if (c10)
     hipLaunchKernelGGL(k_eval_tiles<10>, grid, dim3(kEvThreads), 0, s, a);
   else
     hipLaunchKernelGGL(k_eval_tiles<kCMax>, grid, dim3(kEvThreads), 0, s, a);
