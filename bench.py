@@ -82,7 +82,9 @@ def incremental_phase(ctx, cfg, step: int, batch: int, reps: int):
     return {"kernel": "k_eval_tiles", "batch": batch, "launches": n,
             "avg_launch_us": avg_s * 1e6, "candidate_evals_per_s": batch / avg_s,
             "bound": "hbm", "bytes_per_launch": b, "achieved": achieved, "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS}
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": (measured_traffic("k_eval_tiles", f"{cfg.name}_B{batch}", 1)
+                        if cfg.name == "wide" else None)}
 
 
 def candidate_flops(cfg, w, cands, params):
@@ -137,21 +139,34 @@ def transformer_flops(cfg, cands):
     return total
 
 
-def measured_traffic(kernel: str, workload: str, steps: int):
-    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
-    summary (calibrated against a plain copy), or None when the kernel source
-    has changed since the counters were taken."""
+# Sources each measured kernel is built from: a traffic record holds only
+# while their hash is the one recorded beside the counters.
+TRAFFIC_SOURCES = {
+    "k_step_loop": ["loop_kernel.hip", "loop_kernel.hpp", "device_common.hpp"],
+    "k_eval_tiles": ["mlp_kernels.hip", "mlp_kernels.hpp", "device_common.hpp"],
+}
+
+
+def sources_sha256(kernel: str) -> str:
     import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, "paper_2607_08406_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str, units: float):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary (calibrated against a plain copy; per step or per batch, times
+    `units`), or None when the kernel source has changed since the counters
+    were taken."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    h = hashlib.sha256()
-    for f in ["loop_kernel.hip", "loop_kernel.hpp", "device_common.hpp"]:
-        h.update(open(os.path.join(ROOT, "paper_2607_08406_amd", "csrc", f), "rb").read())
-    if rec.get("source_sha256") != h.hexdigest():
+    if rec.get("source_sha256") != sources_sha256(kernel):
         return None
-    return rec["hbm_bytes_per_step"] * steps
+    return rec["hbm_bytes_per_unit"] * units
 
 
 def workload_config(cfg):
@@ -312,7 +327,7 @@ def main():
         achieved = bytes_launch / avg_s / 1e9
         roof = {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                "traffic": (measured_traffic(kernel, "wide_784-16384-10_K64", args.steps)
+                "traffic": (measured_traffic(kernel, "wide", args.steps)
                             if loop and cfg.name == "wide" else None),
                 "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
                 "launches": int(launches[dominant]),
