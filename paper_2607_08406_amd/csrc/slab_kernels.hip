@@ -10,12 +10,14 @@
 // candidate's column in increasing m (a unit with W_1[m, j] = 0 does not move;
 // about half of a ternary column).  A block of k_slab owns T consecutive
 // samples.  It stages their second-hidden-layer local fields ([n_2][T],
-// unit-major as in HBM, rows padded to T+1 floats) and the logit-layer weights
-// transposed ([n_2][C]) in LDS, lists every affected (candidate, sample) pair,
-// and scores each pair with 32 lanes: lane g adds the list entries g, g+32,
-// ... in order, then the 32 lane sums meet in a fixed butterfly.  The commit
-// runs the same expressions in the same order for the chosen candidate, so the
-// caches hold exactly the values that were scored.
+// unit-major as in HBM, rows padded to T+1 floats), the logit-layer weights
+// transposed ([n_2][C]) and the tile's logits, losses and labels in LDS, lists
+// every affected (candidate, sample) pair, and scores each pair with 32 lanes:
+// lane g adds the list entries g, g+32, ... in order (the next entries are
+// requested while the current ones are used), then the 32 lane sums meet in a
+// fixed butterfly.  The commit runs the same expressions in the same order for
+// the chosen candidate, so the caches hold exactly the values that were
+// scored.
 #include "device_common.hpp"
 #include "slab_kernels.hpp"
 
@@ -28,7 +30,7 @@ constexpr int kGroupK = 64;  // candidate slots listed at a time
 constexpr int kLanesPerPair = 32;    // a half-wave scores one candidate's pairs
 constexpr int kHalves = kSlabThreads / kLanesPerPair;
 constexpr int kPairChunk = 2;        // pairs of one candidate scored together
-constexpr int kChunk = 4;    // list entries a lane loads at once
+constexpr int kChunk = 2;    // list entries a lane loads at once (two batches in flight)
 constexpr int kStageU = 8;   // tile elements a thread loads at once
 
 template <int CM>
@@ -74,37 +76,51 @@ __device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, co
   for (int p = 0; p < kPairChunk; ++p)
 #pragma unroll
     for (int c = 0; c < CM; ++c) acc[p][c] = 0.f;
-  if (active) {
-#pragma unroll 1
-    for (int e0 = g; e0 < nnz; e0 += kLanesPerPair * kChunk) {
-      uint64_t ent[kChunk];
+  // The entries of the next batch are requested before the current batch is
+  // used (two register sets, alternating by position in the loop, so no copy
+  // waits for loads in flight); a load is issued from a clamped index and its
+  // entry is skipped where it is used.
+  auto fetch = [&](int e0, uint64_t (&ent)[kChunk]) {
 #pragma unroll
-      for (int u = 0; u < kChunk; ++u) {
-        const int e = e0 + kLanesPerPair * u;
-        ent[u] = (e < nnz) ? gload(&col[e]) : 0ull;
-      }
+    for (int u = 0; u < kChunk; ++u) {
+      const int e = e0 + kLanesPerPair * u;
+      ent[u] = gload(&col[e < nnz ? e : 0]);
+    }
+  };
+  auto use = [&](int e0, const uint64_t (&ent)[kChunk]) {
 #pragma unroll
-      for (int u = 0; u < kChunk; ++u) {
-        const int e = e0 + kLanesPerPair * u;
-        if (e < nnz) {
-          const int m = (int)(uint32_t)ent[u];
-          const float w = __uint_as_float((uint32_t)(ent[u] >> 32));
-          float wr[CM];
+    for (int u = 0; u < kChunk; ++u) {
+      const int e = e0 + kLanesPerPair * u;
+      if (e < nnz) {
+        const int m = (int)(uint32_t)ent[u];
+        const float w = __uint_as_float((uint32_t)(ent[u] >> 32));
+        float wr[CM];
 #pragma unroll
-          for (int c = 0; c < CM; ++c) wr[c] = w2[m * CM + c];
+        for (int c = 0; c < CM; ++c) wr[c] = w2[m * CM + c];
 #pragma unroll
-          for (int p = 0; p < kPairChunk; ++p) {
-            if (p < np) {
-              const float zo = zt[m * TS + tp[p]];
-              const float zn = zo + dp[p] * w;
-              const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
-              if (STORE) zt[m * TS + tp[p]] = zn;
+        for (int p = 0; p < kPairChunk; ++p) {
+          if (p < np) {
+            const float zo = zt[m * TS + tp[p]];
+            const float zn = zo + dp[p] * w;
+            const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
+            if (STORE) zt[m * TS + tp[p]] = zn;
 #pragma unroll
-              for (int c = 0; c < CM; ++c) acc[p][c] = fmaf(d, wr[c], acc[p][c]);
-            }
+            for (int c = 0; c < CM; ++c) acc[p][c] = fmaf(d, wr[c], acc[p][c]);
           }
         }
       }
+    }
+  };
+  if (active && nnz > 0) {
+    constexpr int kStride = kLanesPerPair * kChunk;
+    uint64_t ea[kChunk], eb[kChunk];
+    fetch(g, ea);
+#pragma unroll 1
+    for (int e0 = g; e0 < nnz; e0 += 2 * kStride) {
+      fetch(e0 + kStride, eb);
+      use(e0, ea);
+      fetch(e0 + 2 * kStride, ea);
+      use(e0 + kStride, eb);
     }
   }
 #pragma unroll
@@ -175,7 +191,10 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   __shared__ uint32_t pmask[kGroupK];      // slot s's samples with a change
   __shared__ uint16_t items[kGroupK * ((kSlabTileMax + kPairChunk - 1) / kPairChunk)];
   __shared__ float dlp[kGroupK * T];
-  __shared__ int gk[kGroupK], gj[kGroupK], gi[kGroupK];
+  __shared__ int gk[kGroupK], gj[kGroupK], gi[kGroupK], gnnz[kGroupK];
+  __shared__ float zlt[CM * kSlabTileMax];  // the tile's logits [class][sample]
+  __shared__ float ellt[kSlabTileMax];
+  __shared__ int yt[kSlabTileMax];
   __shared__ float gde[kGroupK];
   __shared__ int ngroup, nitems;
   __shared__ uint32_t touched;  // commit: samples of the tile whose fields changed
@@ -202,6 +221,9 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   // The tile and the logit-layer weights go to LDS: in an evaluation first
   // (their loads are independent of the candidates, so their latency overlaps
   // the listing); in a commit only when the block has a pair to score.
+  // Every load is issued from an index clamped into its array and its value
+  // selected when it is stored (a load under a branch would make the merge
+  // wait for every load in flight).
   auto stage = [&]() {
     for (int e0 = tid; e0 < n2 * T; e0 += kStageU * kSlabThreads) {
       float v[kStageU];
@@ -209,13 +231,14 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       for (int u = 0; u < kStageU; ++u) {
         const int e = e0 + u * kSlabThreads;
         const int m = e / T, t = e - m * T;
-        v[u] = (e < n2 * T && n0 + t < N) ? gload(&Z2[(int64_t)m * Ns + n0 + t]) : 0.f;
+        const bool ok = e < n2 * T && n0 + t < N;
+        v[u] = gload(&Z2[ok ? (int64_t)m * Ns + n0 + t : 0]);
       }
 #pragma unroll
       for (int u = 0; u < kStageU; ++u) {
         const int e = e0 + u * kSlabThreads;
         const int m = e / T, t = e - m * T;
-        if (e < n2 * T) zt[m * TS + t] = v[u];
+        if (e < n2 * T) zt[m * TS + t] = (n0 + t < N) ? v[u] : 0.f;
       }
     }
     const float* WL = net.W[L - 1];
@@ -225,31 +248,67 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       for (int u = 0; u < kStageU; ++u) {
         const int e = e0 + u * kSlabThreads;
         const int c = e / n2, m = e - c * n2;
-        v[u] = (e < CM * n2 && c < C) ? gload(&WL[(int64_t)c * n2 + m]) : 0.f;
+        const bool ok = e < CM * n2 && c < C;
+        v[u] = gload(&WL[ok ? (int64_t)c * n2 + m : 0]);
       }
 #pragma unroll
       for (int u = 0; u < kStageU; ++u) {
         const int e = e0 + u * kSlabThreads;
         const int c = e / n2, m = e - c * n2;
-        if (e < CM * n2) w2[m * CM + c] = v[u];
+        if (e < CM * n2) w2[m * CM + c] = (c < C) ? v[u] : 0.f;
       }
     }
   };
+  // The tile's logits, losses and labels (the cross-entropy of a pair reads
+  // them), one value per thread.
+  if (tid < (CM + 2) * T) {
+    const int r = tid / T, t = tid - r * T;
+    const bool ok = n0 + t < N && (r >= CM || r < C);
+    const int64_t n = ok ? n0 + t : 0;
+    const float v = (r < CM) ? gload(&ZL[(int64_t)(r < C ? r : 0) * Ns + n])
+                             : (r == CM ? gload(&net.ell[n]) : __int_as_float(gload(&net.y[n])));
+    if (r < CM) zlt[r * T + t] = ok ? v : 0.f;
+    else if (r == CM) ellt[t] = ok ? v : 0.f;
+    else yt[t] = ok ? __float_as_int(v) : 0;
+  }
+  // The first group's candidate fields (wave 0, lane = slot) are requested
+  // before the tile, so their latency overlaps the staging.
+  int f_layer = -1, f_j = 0, f_i = 0, f_valid = 0, f_nnz = 0;
+  float f_de = 0.f;
+  if (wave == 0) {
+    // a commit names its candidate (kc < the evaluated batch; K is 0 then)
+    const int kk = commit ? kc : (lane < K ? lane : K - 1);
+    f_layer = cands[kk].layer;
+    f_j = cands[kk].j;
+    f_i = cands[kk].i;
+    f_valid = aux[kk].valid;
+    f_de = aux[kk].de;
+    f_nnz = nnz[kk];
+  }
   if (!commit) stage();
 
   for (int g0 = 0; g0 < (commit ? 1 : K); g0 += kGroupK) {
     // 1. the group's candidates in layer l (wave 0 lists them in order)
     if (wave == 0) {
       const int k = commit ? kc : g0 + lane;
-      const bool in_l = commit ? lane == 0
-                               : (k < K && cands[k].layer == l && aux[k].valid);
+      if (g0 > 0) {  // later groups of an evaluation (K > 64)
+        const int kk = k < K ? k : K - 1;
+        f_layer = cands[kk].layer;
+        f_j = cands[kk].j;
+        f_i = cands[kk].i;
+        f_valid = aux[kk].valid;
+        f_de = aux[kk].de;
+        f_nnz = nnz[kk];
+      }
+      const bool in_l = commit ? lane == 0 : (k < K && f_layer == l && f_valid);
       const uint64_t m = __ballot(in_l);
       if (in_l) {
         const int s = (int)__popcll(m & ((1ull << lane) - 1ull));
         gk[s] = k;
-        gj[s] = cands[k].j;
-        gi[s] = cands[k].i;
-        gde[s] = aux[k].de;
+        gj[s] = f_j;
+        gi[s] = f_i;
+        gde[s] = f_de;
+        gnnz[s] = f_nnz;
       }
       if (lane == 0) ngroup = (int)__popcll(m);
     }
@@ -327,7 +386,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       }
       const int k = gk[s];
       const uint64_t* col = cols + (int64_t)k * n2;
-      const int cnt = active ? gload(&nnz[k]) : 0;
+      const int cnt = active ? gnnz[s] : 0;
       float acc[kPairChunk][CM];
       if (commit)  // the commit also writes the new fields into the tile
         chunk_logit_delta<CM, TS, true>(zt, w2, col, cnt, tp, dp, np, act, gamma, active, acc);
@@ -341,9 +400,9 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
             const int64_t n = n0 + t;
             float z[CM];
 #pragma unroll
-            for (int c = 0; c < CM; ++c) z[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) + acc[p][c] : 0.f;
-            const float ln = ce_loss<CM>(z, C, gload(&net.y[n]));
-            dlp[s * T + t] = ln - gload(&net.ell[n]);
+            for (int c = 0; c < CM; ++c) z[c] = (c < C) ? zlt[c * T + t] + acc[p][c] : 0.f;
+            const float ln = ce_loss<CM>(z, C, yt[t]);
+            dlp[s * T + t] = ln - ellt[t];
             if (commit) {
 #pragma unroll
               for (int c = 0; c < CM; ++c)
