@@ -678,8 +678,12 @@ hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
   src.pchain = pchain;
   src.nchain = nchain;
   src.chain_top = (net.L >= 4) ? net.L - 4 : -1;
-  // more candidates than one block sums in one pass: spread the sums
-  const int summed = K > kMaxK / 16;
+  // more candidates than one block sums in one pass, or many tile sums per
+  // candidate (the slab's small tiles): spread the sums over blocks
+  int max_tiles = ntiles;
+  if (src.slab_layer >= 0 && nslab > max_tiles) max_tiles = nslab;
+  if (src.chain_top >= 0 && nchain > max_tiles) max_tiles = nchain;
+  const int summed = K > kMaxK / 16 || max_tiles > 128;
   if (summed) {
     constexpr int per = kReduceThreads / 16;
     hipLaunchKernelGGL(k_reduce_dl, dim3((K + per - 1) / per), dim3(kReduceThreads), 0, s, net,
