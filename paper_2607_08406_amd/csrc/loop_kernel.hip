@@ -87,6 +87,7 @@ constexpr int kLoopThreads = 64 * kWaves;
 constexpr int kReducerWaves = 4;      // candidates per reducer workgroup
 constexpr int kMaxTilesPerLane = kLoopMaxTiles / 64;
 constexpr int kPollWindow = 16;  // candidates a tile polls first
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 template <class T>
 __device__ __forceinline__ T ld_agent(const T* p) {
@@ -207,7 +208,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column (one-hot for a logit weight)
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
   __shared__ float zh_lds[2][kLoopMaxK][64];
-  __shared__ float dlp_lds[kLoopMaxK][65];  // padded: lane k reads row k conflict-free
+  // per-pair loss changes, [candidate][sample]; rows of 68 floats keep every
+  // row 16-byte aligned and a 16-byte read of the same column by 16 lanes
+  // (rows k .. k+15) conflict-free
+  __shared__ __attribute__((aligned(16))) float dlp_lds[kLoopMaxK][68];
   __shared__ float lnp_lds[kLoopMaxK][64];  // each pair's new loss, which a commit reuses
   __shared__ uint16_t list_lds[2][kLoopMaxK * 64];  // work lists, by step parity
   __shared__ int list_n[2];
@@ -459,7 +463,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   if (tid < 2) list_n[tid] = 0;
   if (tid == 0) stage_cnt = 0;
   // pair slots start clear; after each step wave 0 clears those it summed
-  for (int i = tid; i < kLoopMaxK * 65; i += kLoopThreads) (&dlp_lds[0][0])[i] = 0.f;
+  for (int i = tid; i < kLoopMaxK * 68; i += kLoopThreads) (&dlp_lds[0][0])[i] = 0.f;
   if (wave == 1)
     for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(a.t0 + d, (int)d);
   __syncthreads();
@@ -507,24 +511,37 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     __syncthreads();
     MCA_TILE_PROBE(1);
     // 2. wave 0, lane k: sum candidate k's 64 slots (four runs of 16
-    // consecutive samples, then the runs pairwise), publish the tile's
+    // consecutive samples in order, then the runs pairwise), publish the tile's
     // partial sum and clear the slots for the next step.  Only wave 0 stores
     // to global memory here: a store still in flight would make the staging
     // waves' waits for their own loads wait for it too.
     uint64_t* part = a.partials + (size_t)buf * K * a.gpad + g;  // candidate k: part[k * gpad]
     if (wave == 0 && lane < K) {
-      float r0 = 0.f, r1 = 0.f, r2 = 0.f, r3 = 0.f;
+      // the row in two halves of eight 16-byte reads, each issued before its
+      // first add
+      const floatx4* row = reinterpret_cast<const floatx4*>(&dlp_lds[lane][0]);
+      float r[4];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        r0 += dlp_lds[lane][i];
-        r1 += dlp_lds[lane][16 + i];
-        r2 += dlp_lds[lane][32 + i];
-        r3 += dlp_lds[lane][48 + i];
+      for (int half = 0; half < 2; ++half) {
+        floatx4 q4[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) q4[i] = row[8 * half + i];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          float acc = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc += q4[4 * h + i][t];
+          r[2 * half + h] = acc;
+        }
       }
-      const float v = (r0 + r1) + (r2 + r3);
+      const float v = (r[0] + r[1]) + (r[2] + r[3]);
       st_agent(&part[(size_t)lane * a.gpad], pack(prep_lds[buf][lane].valid ? v : __builtin_huge_valf(), tag));
+      const floatx4 zero4 = {0.f, 0.f, 0.f, 0.f};
+      floatx4* wrow = reinterpret_cast<floatx4*>(&dlp_lds[lane][0]);
 #pragma unroll
-      for (int i = 0; i < 64; ++i) dlp_lds[lane][i] = 0.f;
+      for (int i = 0; i < 16; ++i) wrow[i] = zero4;
     }
     MCA_TILE_PROBE(2);
     if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
