@@ -319,9 +319,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   const bool two = Lk == 2;
   const float* const in_hid = a.net.XT;                       // input of layer 0 (L = 2)
   const float* const in_log = two ? a.net.Z[0] : a.net.XT;    // input of the logit layer
-  const float* const z_hid = a.net.Z[0];                      // hidden local fields (L = 2)
-  const float* const w_log = two ? a.net.W[1] : a.net.W[0];
-  const int8_t* const c_log = two ? a.net.codes[1] : a.net.codes[0];
+  float* const z_hid = a.net.Z[0];                      // hidden local fields (L = 2)
+  float* const w_log = two ? a.net.W[1] : a.net.W[0];
+  int8_t* const c_log = two ? a.net.codes[1] : a.net.codes[0];
   const int nin_log = two ? a.net.widths[1] : a.net.widths[0];
   const int nin_hid = a.net.widths[0];
   const bool ternary = a.net.ternary != 0;
@@ -562,12 +562,18 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     }
     if (wave == 0) {
       // what the commit and the patch check need whichever candidate wins:
-      // the lane's logits, and the candidates of step s+1 (lane = candidate)
+      // the lane's logits, this step's candidates with their new values and
+      // the candidates of step s+1 (lane = candidate)
       float zc[CM];
 #pragma unroll
       for (int cc = 0; cc < CM; ++cc) zc[cc] = zl_lds[cc * 64 + lane];
-      mca_cand c1{};
-      if (lane < K) c1 = cand_lds[(s + 1) & 3][lane];
+      mca_cand c0{}, c1{};
+      Prep p0{};
+      if (lane < K) {
+        c0 = cands[lane];
+        p0 = prep_lds[buf][lane];
+        c1 = cand_lds[(s + 1) & 3][lane];
+      }
       const uint32_t t16 = tag16(s);
       const uint64_t* dls = a.dls + (g % kLoopReplicas) * kLoopMaxK;
       uint64_t d = 0;
@@ -610,9 +616,19 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const double v = unpack_dl(d);
       const int kc = (!ab && am) ? (int)__ffsll((unsigned long long)am) - 1 : -1;
       // 4. commit on this tile (lane = sample; the winner's operands are
-      // staged in LDS); every workgroup writes the new weight
-      const mca_cand c = cands[kc >= 0 ? kc : 0];
-      const Prep au = prep_lds[buf][kc >= 0 ? kc : 0];
+      // staged in LDS, its fields come from lane kc); every workgroup writes
+      // the new weight.  The loop's layers are the last two, so the
+      // destinations are the scalar pointers of the staging code.
+      const int kq = kc >= 0 ? kc : 0;
+      mca_cand c{};
+      c.layer = __builtin_amdgcn_readlane(c0.layer, kq);
+      c.j = __builtin_amdgcn_readlane(c0.j, kq);
+      c.i = __builtin_amdgcn_readlane(c0.i, kq);
+      Prep au{};
+      au.de = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p0.de), kq));
+      au.w_new = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p0.w_new), kq));
+      au.code = __builtin_amdgcn_readlane(p0.code, kq);
+      const bool chid = c.layer == Lk - 2;  // the winner is a hidden-unit weight
       float zr = 0.f;  // the committed unit's row of this tile, lane = sample
       if (kc >= 0) {
         // the same logits the scoring computed; its loss was kept
@@ -630,7 +646,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         (void)pair_logits_of<CM>(C, act, gamma, logit, zb, au.de, wc, ain, zc, zn, da, z);
         const bool ch = live && ain != 0.f;
         if (ch) {
-          if (c.layer != L - 1) gstore(&net.Z[c.layer][(int64_t)c.j * Ns + n], zn);
+          if (chid) gstore(&z_hid[(int64_t)c.j * Ns + n], zn);
 #pragma unroll
           for (int cc = 0; cc < CM; ++cc)
             if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
@@ -639,9 +655,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         zr = ch ? zn : z_raw;
         zrow_lds[buf][lane] = zr;
         if (lane == 0) {
-          const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
-          gstore(&net.W[c.layer][idx], au.w_new);
-          if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)au.code);
+          const int64_t idx = (int64_t)c.j * (chid ? nin_hid : nin_log) + c.i;
+          gstore(&(chid ? a.net.W[0] : w_log)[idx], au.w_new);
+          if (ternary) gstore(&(chid ? a.net.codes[0] : c_log)[idx], (int8_t)au.code);
           LastCommit& lc = last[buf];
           lc.layer = c.layer;
           lc.j = c.j;
