@@ -164,6 +164,30 @@ def test_single_layer_net(mca):
     ctx.close()
 
 
+@pytest.mark.parametrize("C", [7, 16])
+def test_other_class_counts(mca, C):
+    """Class counts other than 10 run the kernels' general variants: 784-256-C
+    on 600 template images (C templates), explicit steps at K = 64 (batched
+    evaluation), then the persistent device loop replayed on the oracle."""
+    cfg = CONFIGS["wide"].scaled(name=f"wide_c{C}", widths=(784, 256, C), n_samples=600, K=64)
+    banner(f"{cfg.name} {cfg.widths} N={cfg.n_samples}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=64)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ties, acc = explicit_steps(ctx, ref, cfg, 0, 20, 64)
+    assert acc > 5
+    assert_state_equal(ctx, ref)
+    ctx.set_step(20)
+    st, ch, dl = ctx.run_steps(40, 64, trace=True, trace_dloss=True)
+    assert st.steps == 40
+    replay_trace(ref, cfg, 20, ch, dl, 64)
+    assert_state_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ctx.close()
+
+
 def test_zero_increment_and_bound(mca):
     cfg = small_wide()
     w = mlp_workload(cfg)

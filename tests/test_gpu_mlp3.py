@@ -76,6 +76,29 @@ def test_ternary_three_layer_small(mca):
     ctx.close()
 
 
+def test_three_layer_other_class_count(mca):
+    """784-64-48-13 Gaussian ternary net on 250 template images: thirteen
+    classes run the general variant of the layer-(L-3) kernel (12-sample
+    tiles) and of the column kernels."""
+    cfg = CONFIGS["ternary"].scaled(name="t3_c13", widths=(784, 64, 48, 13), n_samples=250, K=16)
+    banner(f"{cfg.name} {cfg.widths} N={cfg.n_samples}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=16)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    counts = layer_counts(ref, cfg, 0, 30, 16)
+    assert counts[0] > 20  # the first layer is exercised
+    explicit_steps(ctx, ref, cfg, 0, 30, 16)
+    assert_state_equal(ctx, ref)
+    assert_caches_match(ctx, ref)
+    ctx.set_step(30)
+    st, ch, dl = ctx.run_steps(30, 16, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 30, ch, dl, 16)
+    assert_state_equal(ctx, ref)
+    assert_caches_match(ctx, ref)
+    ctx.close()
+
+
 def test_tanh_three_layer_continuous(mca):
     """64-48-40-10 tanh net with continuous weights on 500 samples, K = 8."""
     cfg = CONFIGS["tiny"].scaled(name="tanh3", widths=(64, 48, 40, 10), n_samples=500, K=8)

@@ -80,6 +80,26 @@ def test_deep_small_every_layer_kind(mca):
     ctx.close()
 
 
+def test_deep_other_class_count(mca):
+    """64-256-256-256-12 tanh, 150 samples, K = 8, layer drawn first: twelve
+    classes run the general variant of the dense chain and the other kernels."""
+    cfg = small_deep(name="deep_c12", widths=(64, 256, 256, 256, 12), n_samples=150)
+    banner(f"{cfg.name} {cfg.widths} N={cfg.n_samples}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=8)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    explicit_steps(ctx, ref, cfg, 0, 30, 8)
+    assert_state_equal(ctx, ref)
+    assert_caches_match(ctx, ref)
+    ctx.set_step(30)
+    st, ch, dl = ctx.run_steps(30, 8, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 30, ch, dl, 8)
+    assert_state_equal(ctx, ref)
+    assert_caches_match(ctx, ref)
+    ctx.close()
+
+
 def test_deep_sparse_images(mca):
     """784-256-256-256-10 tanh on 300 template images (first-layer candidates
     change about 19 % of the samples, listed sparsely), K = 16."""
