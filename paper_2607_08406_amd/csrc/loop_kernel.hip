@@ -204,6 +204,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ float ell_lds[64];
   __shared__ int y_lds[64];
   __shared__ mca_cand cand_lds[4][kLoopMaxK];  // draws of steps s .. s+3, by step mod 4
+  // each draw's row offsets in the unit-major arrays (elements): its input
+  // row and, for a hidden unit, its field row (row 0 otherwise)
+  __shared__ uint2 soff_lds[4][kLoopMaxK];
   __shared__ Prep prep_lds[2][kLoopMaxK];       // staged per step parity
   __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column (one-hot for a logit weight)
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
@@ -334,7 +337,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) col_reg[cc] = 0.f;
   auto draw = [&](uint64_t t, int cb) {
-    if (lane < K) cand_lds[cb][lane] = decode_index(net, t, (uint64_t)lane);
+    if (lane < K) {
+      const mca_cand c = decode_index(net, t, (uint64_t)lane);
+      cand_lds[cb][lane] = c;
+      const bool hid = c.layer == Lk - 2;
+      soff_lds[cb][lane] = make_uint2((uint32_t)c.i * (uint32_t)Ns, hid ? (uint32_t)c.j * (uint32_t)Ns : 0u);
+    }
   };
   auto issue_cand = [&](int cb) {
     if (lane < K) {
@@ -375,35 +383,46 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // Lane q < kPer of a staging wave reads the layer, input and unit of the
   // wave's q-th candidate of draw buffer cb (one LDS round trip for all of
   // them); the wave then takes them into scalars lane by lane.
-  auto stage_fields = [&](int cb, int& lv, int& iv, int& jv) {
+  auto stage_fields = [&](int cb, int& lv, int& iv, int& jv, uint32_t& io, uint32_t& zo) {
     const int kq = __builtin_amdgcn_readfirstlane(wave) - 2 + kStagers * lane;
     lv = -1;
     iv = jv = 0;
+    io = zo = 0u;
     if (lane < kPer && kq < K) {
       const mca_cand c = cand_lds[cb][kq];
+      const uint2 o = soff_lds[cb][kq];
       lv = c.layer;
       iv = c.i;
       jv = c.j;
+      io = o.x;
+      zo = o.y;
     }
   };
+  // The lane's sample in each row array, as per-lane addresses (vector
+  // registers): issuing a load then needs no scalar base pointer, which the
+  // compiler would otherwise reload from the kernel arguments per candidate.
+  // A dead lane (n >= N) points at sample 0 and its value is not used.
+  const int64_t n_ld = live ? n : 0;
+  const float* const in_hid_n = in_hid + n_ld;
+  const float* const in_log_n = in_log + n_ld;
+  const float* const z_hid_n = z_hid + n_ld;
+  // Both rows of a candidate are loaded at the offsets its draw computed (a
+  // logit-layer candidate's field row is row 0, unused), so issuing takes no
+  // per-candidate address arithmetic on the scalar unit.
   auto issue_samples = [&](int cb) {
     const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
     int lv, iv, jv;
-    stage_fields(cb, lv, iv, jv);
+    uint32_t io, zo;
+    stage_fields(cb, lv, iv, jv, io, zo);
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int k = w + kStagers * q;
       a_raw[q] = 0.f;
       z_raw[q] = 0.f;
       if (k < K) {
-        const int l = __builtin_amdgcn_readlane(lv, q);
-        const int ci = __builtin_amdgcn_readlane(iv, q);
-        const int cj = __builtin_amdgcn_readlane(jv, q);
-        const bool hid = l == Lk - 2;
-        if (live) {
-          a_raw[q] = gload(&(hid ? in_hid : in_log)[(int64_t)ci * Ns + n]);
-          if (hid) z_raw[q] = gload(&z_hid[(int64_t)cj * Ns + n]);
-        }
+        const bool hid = __builtin_amdgcn_readlane(lv, q) == Lk - 2;
+        a_raw[q] = gload(&(hid ? in_hid_n : in_log_n)[(uint32_t)__builtin_amdgcn_readlane((int)io, q)]);
+        z_raw[q] = gload(&z_hid_n[(uint32_t)__builtin_amdgcn_readlane((int)zo, q)]);
       }
     }
   };
@@ -414,12 +433,18 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // exactly 0).  Results do not depend on the order of the list.
   auto land_samples = [&](int cb, int b, int slot) {
     const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
-    const int lvalid = __builtin_amdgcn_readfirstlane(last[slot].valid);
-    const int llayer = __builtin_amdgcn_readfirstlane(last[slot].layer);
-    const int lj = __builtin_amdgcn_readfirstlane(last[slot].j);
-    const bool row = lvalid && llayer == Lk - 2;  // a hidden row of this tile changed
+    // every LDS read of the landing is issued here, before any is used
+    const LastCommit lc = last[slot];
+    const float zrow_v = zrow_lds[slot][lane];
     int lv, iv, jv;
-    stage_fields(cb, lv, iv, jv);
+    uint32_t io, zo;
+    stage_fields(cb, lv, iv, jv, io, zo);
+    const bool row = lc.valid && lc.layer == Lk - 2;  // a hidden row of this tile changed
+    // per candidate (lane q): a hidden-unit weight; its field row, or its
+    // input row, is the committed row
+    const uint64_t hmask = __ballot(lv == Lk - 2);
+    const uint64_t pz = __ballot(row && lv == Lk - 2 && jv == lc.j);
+    const uint64_t pa = __ballot(row && lv == Lk - 1 && iv == lc.j);
     uint64_t m[kPer];
     int tot = 0;
 #pragma unroll
@@ -427,13 +452,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int k = w + kStagers * q;
       m[q] = 0;
       if (k < K) {
-        const int l = __builtin_amdgcn_readlane(lv, q);
-        const int ci = __builtin_amdgcn_readlane(iv, q);
-        const int cj = __builtin_amdgcn_readlane(jv, q);
-        const bool hid = l == Lk - 2;
-        float ar = a_raw[q], zz = z_raw[q];
-        if (row && hid && cj == lj) zz = zrow_lds[slot][lane];
-        if (row && !hid && ci == lj) ar = zrow_lds[slot][lane];
+        const bool hid = (hmask >> q) & 1ull;
+        const float zz = ((pz >> q) & 1ull) ? zrow_v : z_raw[q];
+        const float ar = ((pa >> q) & 1ull) ? zrow_v : a_raw[q];
         // the logit layer's input is an activation when a hidden layer feeds it
         const float in = (!hid && two) ? act_fn(ar, act, gamma) : ar;
         ain_lds[b][k][lane] = live ? in : 0.f;
@@ -554,9 +575,29 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       if (s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
       if (psel >= 0 && lane == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 6);
     } else if (wave >= 2) {
+#ifdef MCA_PHASE_PROBES
+#define MCA_STAGE_PROBE(i)                                                        \
+  if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)                     \
+    probes[160000 + (int64_t)s * 8 + (i)] = (int64_t)__builtin_amdgcn_s_memrealtime();
+#else
+#define MCA_STAGE_PROBE(i)
+#endif
+      MCA_STAGE_PROBE(0);
+#ifdef MCA_PHASE_PROBES
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)
+        probes[160000 + (int64_t)s * 8 + 4] = (int64_t)__builtin_amdgcn_s_memrealtime();
+      __builtin_amdgcn_s_waitcnt(0);
+      if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)
+        probes[160000 + (int64_t)s * 8 + 5] = (int64_t)__builtin_amdgcn_s_memrealtime();
+#endif
       if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      MCA_STAGE_PROBE(1);
       landed();
+      MCA_STAGE_PROBE(2);
       if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
+      MCA_STAGE_PROBE(3);
+#undef MCA_STAGE_PROBE
       if (psel >= 0 && wave == 15 && lane == 0 && s < 256)
         MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 7);
     }

@@ -902,8 +902,12 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   const bool mlp2 = !ctx->tf && net.L <= 2;
   if (ctx->use_loop && mlp2 && K <= mca::kLoopMaxK)
     MCA_HIP(ctx, mca::step_loop_max_blocks(K, net.C, &max_blocks));
+  // row offsets of the loop's arrays are 32-bit element counts
+  bool offsets_fit = true;
+  for (int l = 0; l < net.L; ++l)
+    if ((uint64_t)net.widths[l] * (uint64_t)net.Ns >= ((uint64_t)1 << 32)) offsets_fit = false;
   // G tile workgroups plus the candidate reducers must all be resident at once
-  const bool loop_ok = ctx->use_loop && mlp2 && K <= mca::kLoopMaxK &&
+  const bool loop_ok = ctx->use_loop && mlp2 && offsets_fit && K <= mca::kLoopMaxK &&
                        ctx->lo.loop_G <= mca::kLoopMaxTiles &&
                        ctx->lo.loop_G + mca::step_loop_reducers(K) <= max_blocks;
   while (loop_ok && done < n_steps) {
