@@ -190,12 +190,13 @@ __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
     f.de = a.aux[kc].de;
     f.k = (item < n_items) ? k : K;
   };
-  // candidate q of the wave is scored here: its weight is in the last two
-  // layers and within the bound
-  auto ok = [&](const EvFields& f, int q) {
-    return __builtin_amdgcn_readlane(f.k, q) < K && __builtin_amdgcn_readlane(f.layer, q) >= L - 2 &&
-           __builtin_amdgcn_readlane(f.valid, q) != 0;
+  // bit q: candidate q of the wave is scored here (its weight is in the last
+  // two layers and within the bound); is a hidden-unit weight; takes the raw
+  // input (layer 0).  Lane-parallel, so the per-candidate tests are bit tests.
+  auto ok_mask = [&](const EvFields& f) {
+    return __ballot(f.k < K && f.layer >= L - 2 && f.valid != 0);
   };
+  auto hid_mask = [&](const EvFields& f) { return __ballot(f.layer == L - 2); };
   // first sample of the lane's group in item's tile, clamped into the rows
   auto group0 = [&](int item) {
     const int64_t s0 = (int64_t)(item % ntiles) * kEvT + 4 * lane;
@@ -212,16 +213,28 @@ __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
                                  : ((r == kRows - 2) ? a.ell : (const float*)a.y);
       r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
     }
+    // each candidate's row offsets, lane-parallel (lane q), and the lane's
+    // sample group in each array: a load then takes no scalar arithmetic
+    const uint64_t okm = ok_mask(f), hm = hid_mask(f) & okm;
+    const int64_t io = (int64_t)f.i * Ns, jo = (int64_t)f.j * Ns;
+    const float* const ih = a.in_hid + s0;
+    const float* const il = a.in_log + s0;
+    const float* const zh = a.z_hid + s0;
+    const float* const zl = a.z_log + s0;
+    const float* const wl = a.w_log + (int64_t)(lane < C ? lane : 0) * a.nh;
 #pragma unroll
     for (int q = 0; q < kEvPer; ++q) {
-      const bool use = ok(f, q);
-      const int l = __builtin_amdgcn_readlane(f.layer, q);
-      const bool hid = use && l == L - 2;
-      const int i = use ? __builtin_amdgcn_readlane(f.i, q) : 0;
+      const bool use = (okm >> q) & 1ull, hid = (hm >> q) & 1ull;
+      const int64_t oi = use ? (int64_t)__builtin_amdgcn_readlane((int)io, q) |
+                                   ((int64_t)__builtin_amdgcn_readlane((int)(io >> 32), q) << 32)
+                             : 0;
+      const int64_t oj = hid ? (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)jo, q) |
+                                   ((int64_t)__builtin_amdgcn_readlane((int)(jo >> 32), q) << 32)
+                             : 0;
       const int j = hid ? __builtin_amdgcn_readlane(f.j, q) : 0;
-      a4[q] = *(const float4*)&(hid ? a.in_hid : a.in_log)[(int64_t)i * Ns + s0];
-      z4[q] = *(const float4*)&(hid ? a.z_hid : a.z_log)[(int64_t)j * Ns + s0];
-      wc[q] = a.w_log[(int64_t)(lane < C ? lane : 0) * a.nh + j];
+      a4[q] = *(const float4*)&(hid ? ih : il)[oi];
+      z4[q] = *(const float4*)&(hid ? zh : zl)[oj];
+      wc[q] = wl[j];
     }
   };
   int run_base[kEvPer], run_len[kEvPer];
@@ -247,19 +260,20 @@ __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
     uint64_t b0[kEvPer], b1[kEvPer], b2[kEvPer], b3[kEvPer];
     float in[kEvPer][4];
     int tot = 0;
+    const uint64_t okm = ok_mask(f), hm = hid_mask(f), rawm = __ballot(f.layer == 0);
 #pragma unroll
     for (int q = 0; q < kEvPer; ++q) {
       const int kq = wave + kEvWaves * q;
       b0[q] = b1[q] = b2[q] = b3[q] = 0;
 #pragma unroll
       for (int t = 0; t < 4; ++t) in[q][t] = 0.f;
-      if (ok(f, q)) {
-        const int l = __builtin_amdgcn_readlane(f.layer, q);
+      if ((okm >> q) & 1ull) {
+        const bool hid = (hm >> q) & 1ull, raw = (rawm >> q) & 1ull;
+        const int l = hid ? L - 2 : L - 1;
         const int j = __builtin_amdgcn_readlane(f.j, q);
-        const bool hid = l == L - 2;
         const float av[4] = {a4[q].x, a4[q].y, a4[q].z, a4[q].w};
 #pragma unroll
-        for (int t = 0; t < 4; ++t) in[q][t] = (l == 0) ? av[t] : act_fn(av[t], act, gamma);
+        for (int t = 0; t < 4; ++t) in[q][t] = raw ? av[t] : act_fn(av[t], act, gamma);
         if (lane < CM) wcol_lds[kq][lane] = (hid && lane < C) ? wc[q] : ((lane == j) ? 1.f : 0.f);
         if (lane == 0) {
           de_lds[kq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f.de), q));
@@ -327,9 +341,10 @@ __global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
     // the tile's partial sum of each of the wave's candidates: lane l adds
     // run entries l, l+64, l+128, l+192 in that order, then one butterfly
     const int b = item % ntiles;
+    const uint64_t okm = ok_mask(f);
 #pragma unroll
     for (int q = 0; q < kEvPer; ++q) {
-      if (ok(f, q)) {
+      if ((okm >> q) & 1ull) {
         float v = 0.f;
 #pragma unroll
         for (int r = 0; r < kEvT / 64; ++r) {
