@@ -11,6 +11,8 @@
 // loss change is dL = (1/N) sum_n (l'_n - l_n) over the changed samples only,
 // against the cached per-sample losses, which keeps fp32 cancellation out of
 // dL (a difference of two ~2.3 totals would drown changes of 1e-6).
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "mlp_kernels.hpp"
 
@@ -95,39 +97,33 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
 // Batched scoring of the candidates whose weight is in the last two layers
 // (a mutated hidden unit of layer L-2 moves the logits by a rank-1 update; a
 // logit-layer weight moves one logit), against the committed state.
-// Work items are (tile, chunk) pairs: the kEvT = 256 samples of a tile
-// against the kEvK candidates of a chunk.  A persistent grid (as many blocks
-// as fit the GPU at once) walks the items, block g taking items g, g + G, ...;
-// per item:
-//  - the tile's logits, per-sample losses and labels land in LDS;
-//  - wave w lands candidates w, w+8, ...: lane l holds samples 4l .. 4l+3 of
-//    the input of the mutated weight and, for a hidden unit, of its local
-//    field (two 1-KB rows per candidate, one 16-byte load per lane each); of
-//    these only the samples whose input is non-zero can change (about 81 % of
-//    an image column is zero); those pairs are appended to an LDS list with
-//    their operands, one contiguous run per candidate in sample order;
-//  - the whole block scores the list with the pair expressions of the step
-//    loop, each pair writing its loss change beside its operands;
-//  - wave w adds the run of each of its candidates in one fixed order and
-//    writes the tile's partial sum partial[k * ntiles + tile], which the
-//    selection kernel adds over the tiles in fp64.
-// A run holds the candidate's changed samples in increasing order wherever
-// the list puts it, so the sums do not depend on the order of the appends or
-// on the grid size.  The rows of the next item are requested before the
-// current item is scored and the candidates' fields one item earlier still,
-// so no memory latency sits between two items.  Every load is issued
-// unconditionally from an address inside its array (a candidate that is not
-// scored here reads row 0, a sample group past the padded rows reads the
-// tile's first group) and its value is selected where it is used: a load
-// under a branch would make the merge of the branches wait for every load in
+// The samples are cut into tiles of kEvT = 256.  Each tile is shared out to
+// bpt blocks (as many as the GPU holds at once, over the tiles): a block
+// loads its tile's logits, per-sample losses and labels into LDS once, and
+// each of its waves then walks its own candidates of the tile (wave v of the
+// tile's waves takes candidates v, v + waves, ...) with no further block
+// barrier.  Per candidate, one wave:
+//  - lands the input of the mutated weight and, for a hidden unit, its local
+//    field over the tile (lane l holds samples 4l .. 4l+3, one 16-byte load
+//    per row), requested three candidates earlier;
+//  - lists the samples whose input is non-zero (the others cannot change:
+//    about 81 % of an image column is zero) in sample order, in the wave's
+//    own LDS list, with their operands;
+//  - scores the list 64 pairs at a time with the pair expressions of the step
+//    loop, lane l adding pairs l, l+64, l+128, l+192 in that order, then one
+//    butterfly; the sum is the tile's partial sum partial[k * ntiles + tile],
+//    which the selection kernel adds over the tiles in fp64.
+// The sums depend on the candidate and the tile only, not on the grid.  Every
+// row load is issued unconditionally from an address inside its array (a
+// candidate that is not scored here reads row 0; a sample group past the
+// padded rows reads the tile's first group) and the three row sets change
+// roles by position in an unrolled loop: a load under a branch, or a copy of
+// registers still being loaded, would make the wave wait for every load in
 // flight.
-constexpr int kEvT = 256;                // samples per item (four per lane)
-constexpr int kEvK = 16;                 // candidates per item
-constexpr int kEvWaves = 8;
+constexpr int kEvT = 256;                // samples per tile (four per lane)
+constexpr int kEvWaves = 4;              // waves per block
 constexpr int kEvThreads = 64 * kEvWaves;
-constexpr int kEvPer = kEvK / kEvWaves;  // candidates per wave
-static_assert(kEvPer * kEvWaves == kEvK, "candidates split evenly over the waves");
-static_assert(kEvK <= 16 && kEvT <= 256, "a pair code holds a candidate in 4 bits, a sample in 8");
+static_assert(kEvT == 256, "lane l holds samples 4l .. 4l+3 of a tile");
 
 // The caches the batched evaluation reads, resolved on the host.
 struct EvArgs {
@@ -142,228 +138,203 @@ struct EvArgs {
   const Aux* aux;
   float* partial;
   int64_t N, Ns;
-  int L, C, act, nh, K, ntiles, nchunks;
+  int L, C, act, nh, K, ntiles, bpt;  // bpt: blocks per tile
   float gamma;
 };
 
-// A wave's candidates of one item as loaded: lane q holds candidate
-// chunk * kEvK + wave + kEvWaves * q for q < kEvPer (read from a clamped index
-// for the other lanes and beyond K; ok() rules them out).
-struct EvFields {
-  int layer, j, i, valid, k;
-  float de;
+// One candidate's rows over the tile as loaded: lane l holds samples
+// 4l .. 4l+3 of the input and of the local field, and lane c < C the
+// logit-layer weight W[L-1][c][j].
+struct EvRows {
+  float4 a4, z4;
+  float wc;
 };
 
 template <int CM>
-__global__ __launch_bounds__(kEvThreads) void k_eval_tiles(EvArgs a) {
-  constexpr int kRows = CM + 2;                             // logits, losses, labels
-  constexpr int kRowsPer = (kRows + kEvWaves - 1) / kEvWaves;
-  __shared__ float zl_lds[CM * kEvT];       // logits, [class][sample]
+__global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <= 10 ? 5 : 1))) void k_eval_tiles(EvArgs a) {
+  constexpr int kRows = CM + 2;                            // logits, losses, labels
+  __shared__ float zl_lds[CM * kEvT];                      // logits, [class][sample]
   __shared__ float ell_lds[kEvT];
   __shared__ int y_lds[kEvT];
-  __shared__ float wcol_lds[kEvK][CM];      // logit-layer column (one-hot for a logit weight)
-  __shared__ float de_lds[kEvK];
-  __shared__ int layer_lds[kEvK], j_lds[kEvK];
-  __shared__ uint16_t code_lds[kEvK * kEvT];  // pair: candidate << 8 | sample
-  __shared__ float ain_lds[kEvK * kEvT];      // pair: input of the mutated weight
-  __shared__ float zh_lds[kEvK * kEvT];       // pair: local field of a mutated hidden unit
-  __shared__ float dl_lds[kEvK * kEvT];       // pair: loss change
-  __shared__ int list_n;
+  __shared__ float wcol_lds[kEvWaves][CM];                 // logit-layer column (one-hot for a logit weight)
+  __shared__ uint16_t code_lds[kEvWaves][kEvT];            // pair e: its sample in the tile
+  __shared__ float ain_lds[kEvWaves][kEvT];                // pair e: input of the mutated weight
+  __shared__ float zh_lds[kEvWaves][kEvT];                 // pair e: local field of a mutated hidden unit
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int C = (CM < kCMax) ? CM : a.C, L = a.L;
   const int act = a.act;
   const float gamma = a.gamma;
   const int64_t Ns = a.Ns, N = a.N;
-  const int ntiles = a.ntiles, K = a.K;
-  const int n_items = ntiles * a.nchunks;
-  const int G = (int)gridDim.x;
+  const int ntiles = a.ntiles, K = a.K, bpt = a.bpt;
+  const int wpt = bpt * kEvWaves;  // waves per tile
+  const int nslots = ntiles * bpt;
+  uint16_t* const code = code_lds[wave];
+  float* const ainl = ain_lds[wave];
+  float* const zhl = zh_lds[wave];
+  float* const wcol = wcol_lds[wave];
 
-  auto load_fields = [&](int item, EvFields& f) {
-    const int it = item < n_items ? item : n_items - 1;
-    const int k = (it / ntiles) * kEvK + wave + kEvWaves * (lane % kEvPer);
-    const int kc = k < K ? k : K - 1;
-    f.layer = a.cands[kc].layer;
-    f.j = a.cands[kc].j;
-    f.i = a.cands[kc].i;
-    f.valid = a.aux[kc].valid;
-    f.de = a.aux[kc].de;
-    f.k = (item < n_items) ? k : K;
-  };
-  // bit q: candidate q of the wave is scored here (its weight is in the last
-  // two layers and within the bound); is a hidden-unit weight; takes the raw
-  // input (layer 0).  Lane-parallel, so the per-candidate tests are bit tests.
-  auto ok_mask = [&](const EvFields& f) {
-    return __ballot(f.k < K && f.layer >= L - 2 && f.valid != 0);
-  };
-  auto hid_mask = [&](const EvFields& f) { return __ballot(f.layer == L - 2); };
-  // first sample of the lane's group in item's tile, clamped into the rows
-  auto group0 = [&](int item) {
-    const int64_t s0 = (int64_t)(item % ntiles) * kEvT + 4 * lane;
-    return s0 < Ns ? s0 : (int64_t)(item % ntiles) * kEvT;
-  };
-  float4 a4[kEvPer], z4[kEvPer], r4[kRowsPer];
-  float wc[kEvPer];
-  auto issue_rows = [&](int item, const EvFields& f) {
-    const int64_t s0 = group0(item);
-#pragma unroll
-    for (int u = 0; u < kRowsPer; ++u) {
-      const int r = wave + kEvWaves * u;  // row r of the tile: logit r < C, then losses, labels
-      const float* row = (r < C) ? a.z_log + (int64_t)r * Ns
-                                 : ((r == kRows - 2) ? a.ell : (const float*)a.y);
-      r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
-    }
-    // each candidate's row offsets, lane-parallel (lane q), and the lane's
-    // sample group in each array: a load then takes no scalar arithmetic
-    const uint64_t okm = ok_mask(f), hm = hid_mask(f) & okm;
-    const int64_t io = (int64_t)f.i * Ns, jo = (int64_t)f.j * Ns;
+  for (int slot = (int)blockIdx.x; slot < nslots; slot += (int)gridDim.x) {
+    const int b = slot / bpt;
+    const int64_t t0 = (int64_t)b * kEvT;
+    const int64_t sl = t0 + 4 * lane;              // the lane's first sample
+    const int64_t s0 = sl < Ns ? sl : t0;          // ... clamped into the rows
+    // this wave's candidates of the tile: k = kw + m * wpt
+    const int kw = (slot % bpt) * kEvWaves + wave;
+    const int nu = kw < K ? (K - 1 - kw) / wpt + 1 : 0;
     const float* const ih = a.in_hid + s0;
     const float* const il = a.in_log + s0;
     const float* const zh = a.z_hid + s0;
     const float* const zl = a.z_log + s0;
     const float* const wl = a.w_log + (int64_t)(lane < C ? lane : 0) * a.nh;
-#pragma unroll
-    for (int q = 0; q < kEvPer; ++q) {
-      const bool use = (okm >> q) & 1ull, hid = (hm >> q) & 1ull;
-      const int64_t oi = use ? (int64_t)__builtin_amdgcn_readlane((int)io, q) |
-                                   ((int64_t)__builtin_amdgcn_readlane((int)(io >> 32), q) << 32)
-                             : 0;
-      const int64_t oj = hid ? (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)jo, q) |
-                                   ((int64_t)__builtin_amdgcn_readlane((int)(jo >> 32), q) << 32)
-                             : 0;
-      const int j = hid ? __builtin_amdgcn_readlane(f.j, q) : 0;
-      a4[q] = *(const float4*)&(hid ? ih : il)[oi];
-      z4[q] = *(const float4*)&(hid ? zh : zl)[oj];
-      wc[q] = wl[j];
-    }
-  };
-  int run_base[kEvPer], run_len[kEvPer];
-  // the item's rows go to LDS; each candidate's pairs with a non-zero input
-  // are appended as one run, in sample order, with their operands
-  auto land = [&](int item, const EvFields& f) {
-    const int64_t s0 = (int64_t)(item % ntiles) * kEvT + 4 * lane;
-#pragma unroll
-    for (int u = 0; u < kRowsPer; ++u) {
-      const int r = wave + kEvWaves * u;
-      if (r < kRows) {
-        float* dst = (r < CM) ? &zl_lds[r * kEvT] : ((r == kRows - 2) ? ell_lds : (float*)y_lds);
-        const float4 v = r4[u];
-        const bool keep = r >= CM || r < C;  // logit rows past C stay zero
-        float4 w;
-        w.x = (keep && s0 + 0 < N) ? v.x : 0.f;
-        w.y = (keep && s0 + 1 < N) ? v.y : 0.f;
-        w.z = (keep && s0 + 2 < N) ? v.z : 0.f;
-        w.w = (keep && s0 + 3 < N) ? v.w : 0.f;
-        *(float4*)&dst[4 * lane] = w;
-      }
-    }
-    uint64_t b0[kEvPer], b1[kEvPer], b2[kEvPer], b3[kEvPer];
-    float in[kEvPer][4];
-    int tot = 0;
-    const uint64_t okm = ok_mask(f), hm = hid_mask(f), rawm = __ballot(f.layer == 0);
-#pragma unroll
-    for (int q = 0; q < kEvPer; ++q) {
-      const int kq = wave + kEvWaves * q;
-      b0[q] = b1[q] = b2[q] = b3[q] = 0;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) in[q][t] = 0.f;
-      if ((okm >> q) & 1ull) {
-        const bool hid = (hm >> q) & 1ull, raw = (rawm >> q) & 1ull;
-        const int l = hid ? L - 2 : L - 1;
-        const int j = __builtin_amdgcn_readlane(f.j, q);
-        const float av[4] = {a4[q].x, a4[q].y, a4[q].z, a4[q].w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) in[q][t] = raw ? av[t] : act_fn(av[t], act, gamma);
-        if (lane < CM) wcol_lds[kq][lane] = (hid && lane < C) ? wc[q] : ((lane == j) ? 1.f : 0.f);
-        if (lane == 0) {
-          de_lds[kq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f.de), q));
-          layer_lds[kq] = l;
-          j_lds[kq] = j;
-        }
-        b0[q] = __ballot(s0 + 0 < N && in[q][0] != 0.f);
-        b1[q] = __ballot(s0 + 1 < N && in[q][1] != 0.f);
-        b2[q] = __ballot(s0 + 2 < N && in[q][2] != 0.f);
-        b3[q] = __ballot(s0 + 3 < N && in[q][3] != 0.f);
-        tot += (int)(__popcll(b0[q]) + __popcll(b1[q]) + __popcll(b2[q]) + __popcll(b3[q]));
-      }
-    }
-    int base = 0;
-    if (lane == 0 && tot) base = atomicAdd(&list_n, tot);
-    base = __builtin_amdgcn_readfirstlane(__shfl(base, 0, 64));
-    const uint64_t below = (1ull << lane) - 1ull;
-#pragma unroll
-    for (int q = 0; q < kEvPer; ++q) {
-      const int cnt = (int)(__popcll(b0[q]) + __popcll(b1[q]) + __popcll(b2[q]) + __popcll(b3[q]));
-      run_base[q] = base;
-      run_len[q] = cnt;
-      // pairs of lower lanes come first, then the lane's own in sample order
-      int e = base + (int)(__popcll(b0[q] & below) + __popcll(b1[q] & below) +
-                           __popcll(b2[q] & below) + __popcll(b3[q] & below));
-      const uint64_t bt[4] = {b0[q], b1[q], b2[q], b3[q]};
-      const float zv[4] = {z4[q].x, z4[q].y, z4[q].z, z4[q].w};
-      const int kq = wave + kEvWaves * q;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        if ((bt[t] >> lane) & 1ull) {
-          code_lds[e] = (uint16_t)((kq << 8) | (4 * lane + t));
-          ain_lds[e] = in[q][t];
-          zh_lds[e] = zv[t];
-          ++e;
-        }
-      }
-      base += cnt;
-    }
-  };
+    __syncthreads();  // the last slot's pairs are done with the tile
 
-  // One item: fn holds the fields of item + G (its rows are requested here),
-  // fnn receives those of item + 2G.  The three field sets change roles by
-  // position in the unrolled loop below, not by copies: a copy of registers
-  // still being loaded would wait for every load in flight.
-  int item = (int)blockIdx.x;
-  auto step = [&](const EvFields& f, const EvFields& fn, EvFields& fnn) {
-    load_fields(item + 2 * G, fnn);
-    if (tid == 0) list_n = 0;
-    __syncthreads();  // the last item's sums are done with the list
-    land(item, f);
-    __syncthreads();
-    if (item + G < n_items) issue_rows(item + G, fn);
-    // scoring: the whole block shares out the list
-    const int n_list = list_n;
-    for (int e = tid; e < n_list; e += kEvThreads) {
-      const int code = code_lds[e];
-      const int kq = code >> 8, sl = code & 255;
-      float ln;
-      dl_lds[e] = pair_eval<CM, kEvT>(L, C, act, gamma, layer_lds[kq], j_lds[kq], de_lds[kq],
-                                      wcol_lds[kq], ain_lds[e], zh_lds[e], &zl_lds[sl],
-                                      ell_lds[sl], y_lds[sl], ln);
-    }
-    __syncthreads();
-    // the tile's partial sum of each of the wave's candidates: lane l adds
-    // run entries l, l+64, l+128, l+192 in that order, then one butterfly
-    const int b = item % ntiles;
-    const uint64_t okm = ok_mask(f);
+    // One pass over up to 64 of the wave's candidates: lane q holds candidate
+    // pass + q.  The first pass (every wave makes it) also brings in the
+    // tile: its rows are requested after the candidates' fields, so both
+    // arrive within one memory latency, and land in LDS before the first
+    // candidates' rows are requested; the block barrier comes after those.
+    auto run_pass = [&](int pass, auto first_pass) {
+      constexpr bool kFirst = decltype(first_pass)::value;
+      const int n = nu - pass < 64 ? nu - pass : 64;
+      const int qk = lane < n ? lane : (n > 0 ? n - 1 : 0);
+      int k = kw + (pass + qk) * wpt;
+      k = k < K ? k : K - 1;  // read from a clamped index: no load under a branch
+      const int layer = a.cands[k].layer, j = a.cands[k].j, i = a.cands[k].i;
+      const int valid = a.aux[k].valid;
+      const float de = a.aux[k].de;
+      constexpr int kRowsPer = (kRows + kEvWaves - 1) / kEvWaves;
+      float4 r4[kRowsPer];
+      if (kFirst) {
 #pragma unroll
-    for (int q = 0; q < kEvPer; ++q) {
-      if ((okm >> q) & 1ull) {
-        float v = 0.f;
-#pragma unroll
-        for (int r = 0; r < kEvT / 64; ++r) {
-          const int idx = lane + 64 * r;
-          v += (idx < run_len[q]) ? dl_lds[run_base[q] + idx] : 0.f;
+        for (int u = 0; u < kRowsPer; ++u) {
+          const int r = wave + kEvWaves * u;  // row r: logit r < C, then losses, labels
+          const float* row = (r < C) ? a.z_log + (int64_t)r * Ns
+                                     : ((r == kRows - 2) ? a.ell : (const float*)a.y);
+          r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
         }
-        v = wave_sum_f32(v);
-        if (lane == 0) a.partial[(int64_t)__builtin_amdgcn_readlane(f.k, q) * ntiles + b] = v;
       }
-    }
-    item += G;
-    return item < n_items;
-  };
-  EvFields f0, f1, f2;
-  load_fields(item, f0);
-  load_fields(item + G, f1);
-  if (item >= n_items) return;
-  issue_rows(item, f0);
-  while (step(f0, f1, f2) && step(f1, f2, f0) && step(f2, f0, f1)) {
+      // bit q: candidate q is scored here (its weight is in the last two
+      // layers, within the bound); is a hidden-unit weight; takes the raw input
+      const uint64_t okm = __ballot(lane < n && layer >= L - 2 && valid != 0);
+      const uint64_t hm = __ballot(layer == L - 2) & okm;
+      const uint64_t rawm = __ballot(layer == 0);
+      const int64_t io = (int64_t)i * Ns, jo = (int64_t)j * Ns;
+      if (kFirst) {
+#pragma unroll
+        for (int u = 0; u < kRowsPer; ++u) {
+          const int r = wave + kEvWaves * u;
+          if (r < kRows) {
+            float* dst = (r < CM) ? &zl_lds[r * kEvT] : ((r == kRows - 2) ? ell_lds : (float*)y_lds);
+            const bool keep = r >= CM || r < C;  // logit rows past C stay zero
+            const float4 v = r4[u];
+            float4 w;
+            w.x = (keep && sl + 0 < N) ? v.x : 0.f;
+            w.y = (keep && sl + 1 < N) ? v.y : 0.f;
+            w.z = (keep && sl + 2 < N) ? v.z : 0.f;
+            w.w = (keep && sl + 3 < N) ? v.w : 0.f;
+            *(float4*)&dst[4 * lane] = w;
+          }
+        }
+      }
+      // row offsets of candidate q, zero for one not scored here (and past
+      // the pass); hidden-unit rows come from the hidden layer's arrays
+      const int64_t io_s = ((okm >> lane) & 1ull) ? io : 0;
+      const int64_t jo_s = ((hm >> lane) & 1ull) ? jo : 0;
+      const int j_s = ((hm >> lane) & 1ull) ? j : 0;
+      auto issue = [&](int q, EvRows& R) {
+        const int qq = q & 63;
+        const bool in_pass = q < 64;
+        const bool hid = in_pass && ((hm >> qq) & 1ull);
+        int64_t oi = (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)io_s, qq) |
+                     ((int64_t)__builtin_amdgcn_readlane((int)(io_s >> 32), qq) << 32);
+        int64_t oj = (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)jo_s, qq) |
+                     ((int64_t)__builtin_amdgcn_readlane((int)(jo_s >> 32), qq) << 32);
+        int jj = __builtin_amdgcn_readlane(j_s, qq);
+        oi = in_pass ? oi : 0;
+        oj = in_pass ? oj : 0;
+        jj = in_pass ? jj : 0;
+        R.a4 = *(const float4*)&(hid ? ih : il)[oi];
+        R.z4 = *(const float4*)&(hid ? zh : zl)[oj];
+        R.wc = wl[jj];
+      };
+      int q = 0;
+      float pv = 0.f;  // lane q: candidate q's partial sum
+      // candidate q: list its pairs, request candidate q + 3 into R, score.
+      // The request is made on every path (a candidate not scored here lists
+      // no pairs): a load under a branch would make the merge wait for every
+      // load in flight.
+      auto unit = [&](EvRows& R) {
+        const bool scored = (okm >> q) & 1ull;
+        const bool hid = (hm >> q) & 1ull, raw = (rawm >> q) & 1ull;
+        const int lq = hid ? L - 2 : L - 1;
+        const int jq = __builtin_amdgcn_readlane(j, q);
+        const float deq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(de), q));
+        float in[4] = {R.a4.x, R.a4.y, R.a4.z, R.a4.w};
+        if (!raw) {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) in[t] = act_fn(in[t], act, gamma);
+        }
+        const float wv = (hid && lane < C) ? R.wc : ((lane == jq) ? 1.f : 0.f);
+        if (lane < CM) wcol[lane] = wv;
+        const float zv[4] = {R.z4.x, R.z4.y, R.z4.z, R.z4.w};
+        uint64_t bt[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) bt[t] = __ballot(scored && sl + t < N && in[t] != 0.f);
+        const int npairs = (int)(__popcll(bt[0]) + __popcll(bt[1]) + __popcll(bt[2]) + __popcll(bt[3]));
+        // pairs of lower lanes come first, then the lane's own in sample order
+        const uint64_t below = (1ull << lane) - 1ull;
+        int e = (int)(__popcll(bt[0] & below) + __popcll(bt[1] & below) + __popcll(bt[2] & below) +
+                      __popcll(bt[3] & below));
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if ((bt[t] >> lane) & 1ull) {
+            code[e] = (uint16_t)(4 * lane + t);
+            ainl[e] = in[t];
+            zhl[e] = zv[t];
+            ++e;
+          }
+        }
+        issue(q + 3, R);
+        __builtin_amdgcn_wave_barrier();
+        float v = 0.f;
+        for (int e0 = 0; e0 < npairs; e0 += 64) {
+          const int ee = e0 + lane;
+          const int ec = ee < npairs ? ee : 0;
+          const int s = code[ec];
+          float ln;
+          const float dl = pair_eval<CM, kEvT>(L, C, act, gamma, lq, jq, deq, wcol, ainl[ec], zhl[ec],
+                                               &zl_lds[s], ell_lds[s], y_lds[s], ln);
+          v += (ee < npairs) ? dl : 0.f;
+        }
+        __builtin_amdgcn_wave_barrier();
+        const float tot = wave_sum_f32(v);
+        pv = (lane == q) ? tot : pv;
+        ++q;
+      };
+      // the requests go out in candidate order, as in the loop below, so the
+      // waits there hold on every path into it
+      EvRows R0, R1, R2;
+      issue(0, R0);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(1, R1);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(2, R2);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kFirst) __syncthreads();
+      // whole rounds of three (up to two units past n list no pairs): no
+      // exit between the positions, whose merged paths would blur the waits
+      for (int q3 = 0; q3 < n; q3 += 3) {
+        unit(R0);
+        unit(R1);
+        unit(R2);
+      }
+      // lane q writes candidate q's partial sum: no store among the row
+      // requests, whose waits count every memory operation in flight
+      if ((okm >> lane) & 1ull) a.partial[(int64_t)(kw + (pass + lane) * wpt) * ntiles + b] = pv;
+    };
+    run_pass(0, std::true_type{});
+    for (int pass = 64; pass < nu; pass += 64) run_pass(pass, std::false_type{});
   }
 }
 
@@ -664,14 +635,20 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   a.nh = net.widths[L - 1];
   a.K = K;
   a.ntiles = ntiles;
-  a.nchunks = (K + kEvK - 1) / kEvK;
   a.gamma = net.gamma;
   const bool c10 = net.C == 10;
   const void* kernel = c10 ? (const void*)k_eval_tiles<10> : (const void*)k_eval_tiles<kCMax>;
   const int fit = eval_grid(kernel, c10 ? 0 : 1);
   if (fit <= 0) return hipErrorInvalidDevice;
-  const int items = ntiles * a.nchunks;
-  const dim3 grid((unsigned)(items < fit ? items : fit));
+  // blocks per tile: share the resident blocks out over the tiles, no more
+  // than the candidates need
+  const int per_tile = fit / ntiles > 1 ? fit / ntiles : 1;
+  const int need = (K + kEvWaves - 1) / kEvWaves;
+  a.bpt = per_tile < need ? per_tile : need;
+  if (a.bpt < 1) a.bpt = 1;  // no candidates: one block per tile finds no work
+  if (K <= 0) return hipSuccess;  // nothing to score (the kernel reads candidate K - 1)
+  const int64_t slots = (int64_t)ntiles * a.bpt;
+  const dim3 grid((unsigned)(slots < fit ? slots : fit));
   if (c10)
     hipLaunchKernelGGL(k_eval_tiles<10>, grid, dim3(kEvThreads), 0, s, a);
   else
