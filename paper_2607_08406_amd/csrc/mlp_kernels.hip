@@ -278,22 +278,28 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         const float wv = (hid && lane < C) ? R.wc : ((lane == jq) ? 1.f : 0.f);
         if (lane < CM) wcol[lane] = wv;
         const float zv[4] = {R.z4.x, R.z4.y, R.z4.z, R.z4.w};
+        bool pr[4];  // sample 4l + t is a pair
         uint64_t bt[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) bt[t] = __ballot(scored && sl + t < N && in[t] != 0.f);
+        for (int t = 0; t < 4; ++t) {
+          pr[t] = scored && sl + t < N && in[t] != 0.f;
+          bt[t] = __ballot(pr[t]);
+        }
         const int npairs = (int)(__popcll(bt[0]) + __popcll(bt[1]) + __popcll(bt[2]) + __popcll(bt[3]));
-        // pairs of lower lanes come first, then the lane's own in sample order
-        const uint64_t below = (1ull << lane) - 1ull;
-        int e = (int)(__popcll(bt[0] & below) + __popcll(bt[1] & below) + __popcll(bt[2] & below) +
-                      __popcll(bt[3] & below));
+        // pairs of lower lanes come first (mbcnt: set bits below the lane),
+        // then the lane's own in sample order
+        uint32_t e = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          e = __builtin_amdgcn_mbcnt_hi((uint32_t)(bt[t] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bt[t], e));
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          if ((bt[t] >> lane) & 1ull) {
+          if (pr[t]) {
             code[e] = (uint16_t)(4 * lane + t);
             ainl[e] = in[t];
             zhl[e] = zv[t];
-            ++e;
           }
+          e += pr[t] ? 1u : 0u;
         }
         issue(q + 3, R);
         __builtin_amdgcn_wave_barrier();
@@ -308,7 +314,7 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
           v += (ee < npairs) ? dl : 0.f;
         }
         __builtin_amdgcn_wave_barrier();
-        const float tot = wave_sum_f32(v);
+        const float tot = npairs ? wave_sum_f32(v) : 0.f;
         pv = (lane == q) ? tot : pv;
         ++q;
       };
