@@ -39,6 +39,7 @@ struct Layout {
   int ntiles = 0;     // blocks of the column commit (kTile samples each)
   int ntiles_ev = 0;  // tiles of the batched evaluation (partial sums per candidate)
   size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
+  size_t fmask = 0, cmask = 0;  // batched evaluation: tiles where a feature / candidate can change
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
   size_t cols = 0, nnz = 0;  // nonzero entries of layer L-3 candidates' W_{L-2} columns
@@ -220,6 +221,8 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.y = take(lo.Ns * sizeof(int32_t));
   lo.cands = take((size_t)k_max * sizeof(mca_cand));
   lo.aux = take((size_t)k_max * sizeof(Aux));
+  lo.fmask = take((size_t)net->widths[0] * sizeof(uint64_t));
+  lo.cmask = take((size_t)k_max * sizeof(uint64_t));
   lo.partial = take((size_t)k_max * lo.ntiles_ev * sizeof(float));
   lo.dl = take((size_t)k_max * sizeof(double));
   lo.bsum = take((size_t)lo.ntiles * sizeof(double));
@@ -268,6 +271,8 @@ struct mca_ctx {
   char* ws = nullptr;
   mca_cand* cands = nullptr;
   Aux* aux = nullptr;
+  uint64_t* fmask = nullptr;  // null: more evaluation tiles than bits
+  uint64_t* cmask = nullptr;
   float* partial = nullptr;
   float* pslab = nullptr;
   uint64_t* cols = nullptr;
@@ -491,12 +496,12 @@ hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
     return mca::tf_launch_propose(ctx->tfd, ctx->tfh, step, use_dev_t, ctx->st, K, ctx->cands,
                                   ctx->aux, ctx->stream);
   return mca::launch_propose(ctx->net, step, use_dev_t, ctx->st, K, ctx->cands, ctx->aux,
-                             ctx->stream);
+                             ctx->fmask, ctx->cmask, ctx->stream);
 }
 
 hipError_t prepare_dev(mca_ctx* ctx, int K) {
   if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, ctx->cands, K, ctx->aux, ctx->stream);
-  return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->stream);
+  return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->fmask, ctx->cmask, ctx->stream);
 }
 
 // Scores the K staged candidates: the column kernel for the last two layers,
@@ -505,7 +510,8 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
   if (ctx->tf)
     return mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, K, false, ctx->partial,
                                ctx->tf_nblk, ctx->stream);
-  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, K, ctx->partial, ctx->lo.ntiles_ev, ctx->stream);
+  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, ctx->cmask, K, ctx->partial,
+                                  ctx->lo.ntiles_ev, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
                          ctx->lo.nslab, -2, ctx->st, ctx->dl, ctx->stream);
@@ -765,6 +771,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   ctx->pchain = (L >= 4) ? (float*)(ws + lo.pchain) : nullptr;
   ctx->cands = (mca_cand*)(ws + lo.cands);
   ctx->aux = (Aux*)(ws + lo.aux);
+  ctx->fmask = lo.ntiles_ev <= 64 ? (uint64_t*)(ws + lo.fmask) : nullptr;
+  ctx->cmask = (uint64_t*)(ws + lo.cmask);
   ctx->partial = (float*)(ws + lo.partial);
   ctx->dl = (double*)(ws + lo.dl);
   ctx->bsum = (double*)(ws + lo.bsum);
@@ -782,7 +790,15 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
       for (int i = 0; i < n0; ++i) xt[(size_t)i * lo.Ns + n] = data->x[(size_t)n * n0 + i];
     std::vector<int32_t> y((size_t)lo.Ns, 0);
     std::memcpy(y.data(), data->y, (size_t)N * sizeof(int32_t));
+    // per feature, the evaluation tiles holding a non-zero sample
+    std::vector<uint64_t> fm((size_t)n0, 0);
+    if (ctx->fmask)
+      for (int i = 0; i < n0; ++i)
+        for (int64_t n = 0; n < N; ++n)
+          if (xt[(size_t)i * lo.Ns + n] != 0.f) fm[i] |= 1ull << (n / mca::eval_tile_size());
     hipError_t e = hipMemcpyAsync((void*)nd.XT, xt.data(), xt.size() * sizeof(float), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess && ctx->fmask)
+      e = hipMemcpyAsync(ctx->fmask, fm.data(), fm.size() * sizeof(uint64_t), hipMemcpyHostToDevice, ctx->stream);
     if (e == hipSuccess) e = hipMemcpyAsync((void*)nd.y, y.data(), y.size() * sizeof(int32_t), hipMemcpyHostToDevice, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) {

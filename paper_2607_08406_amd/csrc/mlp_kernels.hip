@@ -22,8 +22,15 @@ namespace mca {
 // candidate stream
 // ---------------------------------------------------------------------------
 
+// A first-layer weight multiplies the raw input: the evaluation tiles where
+// its feature is zero throughout cannot change (fmask null: no such list).
+__device__ __forceinline__ uint64_t candidate_tiles(const mca_cand& c, const uint64_t* fmask) {
+  return (c.layer == 0 && fmask != nullptr) ? fmask[c.i] : ~0ull;
+}
+
 __global__ void k_propose(NetDev net_arg, uint64_t t_host, int use_dev_t, const DevState* st,
-                          int K, mca_cand* cands, Aux* aux) {
+                          int K, mca_cand* cands, Aux* aux, const uint64_t* fmask,
+                          uint64_t* cmask) {
   __shared__ NetDev net;
   stage_net(net, net_arg);
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
@@ -32,14 +39,18 @@ __global__ void k_propose(NetDev net_arg, uint64_t t_host, int use_dev_t, const 
   const mca_cand c = decode_candidate(net, t, (uint64_t)k);
   cands[k] = c;
   aux[k] = prepare_candidate(net, c);
+  cmask[k] = candidate_tiles(c, fmask);
 }
 
-__global__ void k_prepare(NetDev net_arg, const mca_cand* cands, int K, Aux* aux) {
+__global__ void k_prepare(NetDev net_arg, const mca_cand* cands, int K, Aux* aux,
+                          const uint64_t* fmask, uint64_t* cmask) {
   __shared__ NetDev net;
   stage_net(net, net_arg);
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= K) return;
-  aux[k] = prepare_candidate(net, cands[k]);
+  const mca_cand c = cands[k];
+  aux[k] = prepare_candidate(net, c);
+  cmask[k] = candidate_tiles(c, fmask);
 }
 
 // ---------------------------------------------------------------------------
@@ -136,6 +147,7 @@ struct EvArgs {
   const int32_t* y;      // [Ns]
   const mca_cand* cands;
   const Aux* aux;
+  const uint64_t* cmask;  // per candidate: bit b set when tile b can change
   float* partial;
   int64_t N, Ns;
   int L, C, act, nh, K, ntiles, bpt;  // bpt: blocks per tile
@@ -200,9 +212,10 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
       const int qk = lane < n ? lane : (n > 0 ? n - 1 : 0);
       int k = kw + (pass + qk) * wpt;
       k = k < K ? k : K - 1;  // read from a clamped index: no load under a branch
-      const int layer = a.cands[k].layer, j = a.cands[k].j, i = a.cands[k].i;
+      const int layer0 = a.cands[k].layer, j0 = a.cands[k].j, i0 = a.cands[k].i;
       const int valid = a.aux[k].valid;
-      const float de = a.aux[k].de;
+      const float de0 = a.aux[k].de;
+      const uint64_t tmask = a.cmask[k];
       constexpr int kRowsPer = (kRows + kEvWaves - 1) / kEvWaves;
       float4 r4[kRowsPer];
       if (kFirst) {
@@ -214,9 +227,24 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
           r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
         }
       }
-      // bit q: candidate q is scored here (its weight is in the last two
-      // layers, within the bound); is a hidden-unit weight; takes the raw input
-      const uint64_t okm = __ballot(lane < n && layer >= L - 2 && valid != 0);
+      // scored here: the weight is in the last two layers and within the
+      // bound (its partial sum is written); live: the tile can change too
+      // (a first-layer weight whose feature is zero over the tile cannot)
+      const bool scored = lane < n && layer0 >= L - 2 && valid != 0;
+      const bool live = scored && ((tmask >> b) & 1ull);
+      const uint64_t livem = __ballot(live);
+      const int nl = (int)__popcll(livem);
+      // the live candidates move to lanes 0 .. nl-1, in order (the others
+      // push to lane 63, which is live only when all are)
+      const int dst = live ? (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(livem >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)livem, 0u))
+                           : 63;
+      auto perm = [&](int v) { return __builtin_amdgcn_ds_permute(dst * 4, v); };
+      const int layer = perm(layer0), j = perm(j0), i = perm(i0), qo = perm(lane);
+      const float de = __int_as_float(perm(__float_as_int(de0)));
+      // bit q: lane q holds a live candidate; a hidden-unit weight; one
+      // taking the raw input
+      const uint64_t okm = __ballot(lane < nl);
       const uint64_t hm = __ballot(layer == L - 2) & okm;
       const uint64_t rawm = __ballot(layer == 0);
       const int64_t io = (int64_t)i * Ns, jo = (int64_t)j * Ns;
@@ -265,7 +293,7 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
       // no pairs): a load under a branch would make the merge wait for every
       // load in flight.
       auto unit = [&](EvRows& R) {
-        const bool scored = (okm >> q) & 1ull;
+        const bool use = (okm >> q) & 1ull;
         const bool hid = (hm >> q) & 1ull, raw = (rawm >> q) & 1ull;
         const int lq = hid ? L - 2 : L - 1;
         const int jq = __builtin_amdgcn_readlane(j, q);
@@ -282,7 +310,7 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         uint64_t bt[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          pr[t] = scored && sl + t < N && in[t] != 0.f;
+          pr[t] = use && sl + t < N && in[t] != 0.f;
           bt[t] = __ballot(pr[t]);
         }
         const int npairs = (int)(__popcll(bt[0]) + __popcll(bt[1]) + __popcll(bt[2]) + __popcll(bt[3]));
@@ -328,16 +356,17 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
       issue(2, R2);
       __builtin_amdgcn_sched_barrier(0);
       if (kFirst) __syncthreads();
-      // whole rounds of three (up to two units past n list no pairs): no
+      // whole rounds of three (up to two units past nl list no pairs): no
       // exit between the positions, whose merged paths would blur the waits
-      for (int q3 = 0; q3 < n; q3 += 3) {
+      for (int q3 = 0; q3 < nl; q3 += 3) {
         unit(R0);
         unit(R1);
         unit(R2);
       }
       // lane q writes candidate q's partial sum: no store among the row
       // requests, whose waits count every memory operation in flight
-      if ((okm >> lane) & 1ull) a.partial[(int64_t)(kw + (pass + lane) * wpt) * ntiles + b] = pv;
+      if (lane < nl) a.partial[(int64_t)(kw + (pass + qo) * wpt) * ntiles + b] = pv;
+      if (scored && !live) a.partial[(int64_t)(kw + (pass + lane) * wpt) * ntiles + b] = 0.f;
     };
     run_pass(0, std::true_type{});
     for (int pass = 64; pass < nu; pass += 64) run_pass(pass, std::false_type{});
@@ -587,19 +616,22 @@ __global__ void k_loss_total(NetDev net, const double* bsum, int nb, DevState* s
 // ---------------------------------------------------------------------------
 
 hipError_t launch_propose(const NetDev& net, uint64_t t, bool use_dev_t, const DevState* st,
-                          int K, mca_cand* cands, Aux* aux, hipStream_t s) {
+                          int K, mca_cand* cands, Aux* aux, const uint64_t* fmask,
+                          uint64_t* cmask, hipStream_t s) {
   hipLaunchKernelGGL(k_propose, dim3((K + 63) / 64), dim3(64), 0, s, net, t, use_dev_t ? 1 : 0,
-                     st, K, cands, aux);
+                     st, K, cands, aux, fmask, cmask);
   return hipGetLastError();
 }
 
 hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* aux,
-                          hipStream_t s) {
-  hipLaunchKernelGGL(k_prepare, dim3((K + 63) / 64), dim3(64), 0, s, net, cands, K, aux);
+                          const uint64_t* fmask, uint64_t* cmask, hipStream_t s) {
+  hipLaunchKernelGGL(k_prepare, dim3((K + 63) / 64), dim3(64), 0, s, net, cands, K, aux, fmask,
+                     cmask);
   return hipGetLastError();
 }
 
 int eval_tiles(int64_t n_samples) { return (int)((n_samples + kEvT - 1) / kEvT); }
+int eval_tile_size() { return kEvT; }
 
 namespace {
 // Blocks of k_eval_tiles that fit the device at once (queried once per
@@ -619,8 +651,8 @@ int eval_grid(const void* kernel, int variant) {
 }
 }  // namespace
 
-hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
-                       float* partial, int ntiles, hipStream_t s) {
+hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
+                       const uint64_t* cmask, int K, float* partial, int ntiles, hipStream_t s) {
   const int L = net.L;
   EvArgs a{};
   a.in_hid = (L >= 3) ? net.Z[L - 3] : net.XT;
@@ -632,6 +664,7 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   a.y = net.y;
   a.cands = cands;
   a.aux = aux;
+  a.cmask = cmask;
   a.partial = partial;
   a.N = net.N;
   a.Ns = net.Ns;

@@ -8,14 +8,19 @@
 namespace mca {
 
 hipError_t launch_propose(const NetDev& net, uint64_t t, bool use_dev_t, const DevState* st,
-                          int K, mca_cand* cands, Aux* aux, hipStream_t s);
+                          int K, mca_cand* cands, Aux* aux, const uint64_t* fmask,
+                          uint64_t* cmask, hipStream_t s);
+// fmask (may be null): per input feature, bit b set when tile b of the
+// batched evaluation holds a non-zero input sample; cmask[k] receives
+// candidate k's tiles that can change (all ones but for first-layer weights).
 hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* aux,
-                          hipStream_t s);
+                          const uint64_t* fmask, uint64_t* cmask, hipStream_t s);
 // Tiles of the batched evaluation for n samples; launch_eval writes
 // partial[k * ntiles + tile] for the candidates in the last two layers.
 int eval_tiles(int64_t n_samples);
-hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
-                       float* partial, int ntiles, hipStream_t s);
+int eval_tile_size();
+hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
+                       const uint64_t* cmask, int K, float* partial, int ntiles, hipStream_t s);
 hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
                          const mca_cand* cands, const float* pslab, int nslab,
                          const float* pchain, int nchain, const Aux* aux, int K, double* dL,
