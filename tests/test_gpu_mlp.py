@@ -124,9 +124,9 @@ def test_full_wide_workload(mca):
 def test_wide_batched_evaluation(mca):
     """The batched evaluation at the size the benchmark's incremental-phase
     measurement uses: 1,000 candidates of one step of the 784-16384-10 stream
-    (15 full chunks of 64 and a ragged chunk of 40; 157 sample tiles, the last
-    holding 16 samples) scored in one launch against the committed state, every
-    loss against the fp64 oracle, then the first improver committed."""
+    (40 sample tiles of 256, the last holding 16 samples; 7 or 8 candidates per
+    wave) scored in one launch against the committed state, every loss against
+    the fp64 oracle, then the first improver committed."""
     cfg = CONFIGS["wide"]
     banner("wide 784-16384-10 N=10000 batched evaluation K=1000")
     w = mlp_workload(cfg)
@@ -144,6 +144,36 @@ def test_wide_batched_evaluation(mca):
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ctx.close()
+
+
+@pytest.mark.parametrize("N", [16384, 16424])
+def test_batched_evaluation_tile_masks(mca, N):
+    """The batched evaluation skips the tiles where a first-layer candidate's
+    pixel is zero in every sample, from per-feature masks of up to 64 tiles:
+    at 16,384 samples every one of the 64 tiles has its bit (the last is bit
+    63); at 16,424 (65 tiles, the last holding 40 samples) there are no masks
+    and every tile is scored.  Both against the fp64 oracle."""
+    cfg = CONFIGS["wide"].scaled(name="wide_tiles", widths=(784, 64, 10), n_samples=N)
+    banner(f"wide 784-64-10 N={N} batched evaluation K=256")
+    w = mlp_workload(cfg)
+    X = w["X"].copy()
+    # a lit pixel of these images is lit somewhere in every tile: blank every
+    # third pixel on the odd tiles so that the masks select tiles per feature
+    for t in range(1, (N + 255) // 256, 2):
+        X[t * 256:(t + 1) * 256, 0::3] = 0.0
+    w["X"] = X
+    nz = np.array([[np.any(X[t * 256:(t + 1) * 256, i] != 0) for t in range(64)] for i in range(784)])
+    assert (nz.any(axis=1) & ~nz.all(axis=1)).sum() > 100
+    K = 256
+    ctx, ref = make_pair(cfg, w, k_max=K)
+    for step in (0, 5):
+        cands = ctx.propose(step, K)
+        L_t, rc, rl, chosen = omca.evaluate(ref, step, K, cfg.seed_stream, cfg.stream_tag, cfg.delta)
+        assert_cands_equal(cands, rc)
+        losses, dl = ctx.eval_losses(cands)
+        check_losses(losses, L_t, rl)
+        ctx.rollback()
     ctx.close()
 
 
