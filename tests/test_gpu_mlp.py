@@ -177,6 +177,29 @@ def test_batched_evaluation_tile_masks(mca, N):
     ctx.close()
 
 
+def test_batched_evaluation_many_tiles(mca):
+    """400,000 samples: 1,563 tiles, more than the blocks the GPU holds at
+    once, so blocks walk several tiles, one block per tile, and there are no
+    tile masks; 264 candidates, so each of a tile's four waves holds 66: two
+    passes.  Sampled candidates (both passes, every wave) against the fp64
+    oracle one by one."""
+    cfg = CONFIGS["wide"].scaled(name="wide_long", widths=(16, 8, 10), n_samples=400_000,
+                                 data="sparse_uniform")
+    banner("16-8-10 N=400000 batched evaluation K=264")
+    w = mlp_workload(cfg)
+    K, t = 264, 3
+    ctx, ref = make_pair(cfg, w, k_max=K)
+    cands = ctx.propose(t, K)
+    losses, _ = ctx.eval_losses(cands)
+    L_t = ref.loss()
+    sample = sorted(set(range(8)) | set(range(248, K)) | set(range(0, K, 17)))
+    rc = [ref.candidate(cfg.seed_stream, cfg.stream_tag, t, k, cfg.delta) for k in sample]
+    assert_cands_equal([cands[k] for k in sample], rc)
+    check_losses([losses[k] for k in sample], L_t, [ref.eval(c) for c in rc])
+    ctx.rollback()
+    ctx.close()
+
+
 def test_single_layer_net(mca):
     """A net with no hidden layer (784-10): every candidate is a logit-layer
     weight fed straight by the pixels."""
