@@ -575,29 +575,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       if (s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
       if (psel >= 0 && lane == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 6);
     } else if (wave >= 2) {
-#ifdef MCA_PHASE_PROBES
-#define MCA_STAGE_PROBE(i)                                                        \
-  if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)                     \
-    probes[160000 + (int64_t)s * 8 + (i)] = (int64_t)__builtin_amdgcn_s_memrealtime();
-#else
-#define MCA_STAGE_PROBE(i)
-#endif
-      MCA_STAGE_PROBE(0);
-#ifdef MCA_PHASE_PROBES
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-      if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)
-        probes[160000 + (int64_t)s * 8 + 4] = (int64_t)__builtin_amdgcn_s_memrealtime();
-      __builtin_amdgcn_s_waitcnt(0);
-      if (g == 0 && wave == 15 && lane == 0 && s < 256 && probes)
-        probes[160000 + (int64_t)s * 8 + 5] = (int64_t)__builtin_amdgcn_s_memrealtime();
-#endif
       if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
-      MCA_STAGE_PROBE(1);
       landed();
-      MCA_STAGE_PROBE(2);
       if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
-      MCA_STAGE_PROBE(3);
-#undef MCA_STAGE_PROBE
       if (psel >= 0 && wave == 15 && lane == 0 && s < 256)
         MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 7);
     }
