@@ -15,10 +15,15 @@ Contents (each function cites the passage of the paper it follows):
 * ``mlp``        fp64 forward pass and average cross-entropy (Eq. 2) of a
                  bias-free MLP, by full recomputation (the definition), and an
                  fp64 incremental evaluator (Sec. 2.4: only the changed local
-                 fields are recomputed) pinned against the full recompute.
+                 fields move) that carries the field changes layer to layer
+                 and forms each sample's loss change from its logit change
+                 by exact identities (so a change of 1e-11 on a loss of 2.3
+                 keeps its digits), pinned against the definition in fp64
+                 where changes are large and in long double where small.
 * ``transformer`` fp64 forward pass and loss of the pre-LN causal decoder.
-* ``mca``        the greedy selection loop (Eq. 1, Eq. 5, Eq. 6) over K
-                 candidates per step in stream order.
+* ``mca``        the selection loop (Eq. 1, Eq. 5, Eq. 6, and the Metropolis
+                 rule of Eq. 7 as a per-candidate threshold) over K candidates
+                 per step in stream order.
 
 Every function computes in float64 from fp32 state; the mutated parameter
 itself is formed in fp32 exactly as a single-precision implementation would

@@ -7,6 +7,15 @@ later candidates of the step are discarded.  With K = 1 this is the paper's
 sequential rule (mutate one parameter, keep it if the loss does not increase,
 otherwise retry).  Acceptance (Eq. 6 with the ties reading): dL < 0 by default,
 dL <= 0 when ties are accepted.  A NaN or infinite dL is never accepted.
+
+The Metropolis rule (Eq. 7) accepts with probability min{1, exp(-beta dL)}:
+with the candidate's own uniform U (philox.accept_uniform), U < exp(-beta dL)
+holds exactly when dL < theta = -ln(U) / beta, so it is the greedy test
+against a per-candidate threshold theta > 0 (a zero change always passes).
+
+Each candidate's loss change comes from the model's ``delta`` (the
+difference form of the incremental oracle, the definition for the full
+one); the decision is taken on dL itself, never on L + dL - L.
 """
 from __future__ import annotations
 
@@ -16,12 +25,29 @@ from typing import List, Optional
 
 import numpy as np
 
+from .philox import accept_uniform
 
-def accepts(dL: float, accept_ties: bool) -> bool:
-    """Greedy selection test of Eq. 6 (strict unless ties are accepted)."""
+
+def accepts(dL: float, accept_ties: bool, theta: float = 0.0) -> bool:
+    """Selection test: Eq. 6 (strict unless ties are accepted) when theta is
+    0, else the Metropolis test of Eq. 7 written as dL < theta."""
     if not math.isfinite(dL):
         return False
+    if theta > 0.0:
+        return dL < theta
     return dL <= 0.0 if accept_ties else dL < 0.0
+
+
+def metropolis_threshold(u: float, beta: float) -> float:
+    """theta with (U < exp(-beta dL)) == (dL < theta): -ln(U) / beta (+inf at U = 0)."""
+    return math.inf if u == 0.0 else -math.log(u) / beta
+
+
+def thresholds(seed: int, tag: int, t: int, K: int, beta: float = 0.0):
+    """Per-candidate thresholds of step t: 0 for the greedy rule (beta = 0)."""
+    if not beta:
+        return [0.0] * K
+    return [metropolis_threshold(accept_uniform(seed, tag, t, k), beta) for k in range(K)]
 
 
 @dataclass
@@ -32,31 +58,58 @@ class StepRecord:
     losses: List[float]          # L_k for every evaluated candidate
     chosen: int                  # index of the committed candidate or -1
     L_after: float
+    dls: List[float] = field(default_factory=list)     # dL_k
+    mags: List[float] = field(default_factory=list)    # size of dL_k's first-order terms
+    thetas: List[float] = field(default_factory=list)  # acceptance thresholds (Eq. 7)
 
 
-def evaluate(model, t: int, K: int, seed: int, tag: int, delta: float,
-             mode: str = "weight", accept_ties: bool = False, scan_all: bool = True):
+def _delta(model, c):
+    if hasattr(model, "delta"):
+        dL, mag = model.delta(c)
+        return dL, mag
+    L = model.loss()
+    return model.eval(c) - L, None
+
+
+def evaluate_all(model, t: int, K: int, seed: int, tag: int, delta: float,
+                 mode: str = "weight", accept_ties: bool = False, scan_all: bool = True,
+                 beta: float = 0.0):
     """Score candidates (t, 0..K-1) against the committed state without
-    committing.  Returns (L_t, candidates, losses, index of the first that
-    passes the test or -1).  scan_all=False stops at that first candidate."""
+    committing.  Returns (L_t, candidates, dL list, sizes list, thresholds,
+    index of the first that passes the test or -1)."""
     L_t = model.loss()
-    cands, losses = [], []
+    th = thresholds(seed, tag, t, K, beta)
+    cands, dls, mags = [], [], []
     chosen = -1
     for k in range(K):
         c = model.candidate(seed, tag, t, k, delta, mode)
-        Lk = model.eval(c)
+        dL, mag = _delta(model, c)
         cands.append(c)
-        losses.append(Lk)
-        if chosen < 0 and accepts(Lk - L_t, accept_ties):
+        dls.append(dL)
+        mags.append(mag)
+        if chosen < 0 and accepts(dL, accept_ties, th[k]):
             chosen = k
             if not scan_all:
                 break
-    return L_t, cands, losses, chosen
+    return L_t, cands, dls, mags, th[:len(dls)], chosen
+
+
+def evaluate(model, t: int, K: int, seed: int, tag: int, delta: float,
+             mode: str = "weight", accept_ties: bool = False, scan_all: bool = True,
+             beta: float = 0.0):
+    """Score candidates (t, 0..K-1) against the committed state without
+    committing.  Returns (L_t, candidates, losses L_t + dL_k, index of the
+    first that passes the test or -1).  scan_all=False stops at that first
+    candidate."""
+    L_t, cands, dls, _, _, chosen = evaluate_all(model, t, K, seed, tag, delta, mode,
+                                                 accept_ties, scan_all, beta)
+    return L_t, cands, [L_t + d for d in dls], chosen
 
 
 def step(model, t: int, K: int, seed: int, tag: int, delta: float,
          mode: str = "weight", accept_ties: bool = False,
-         scan_all: bool = True, force: Optional[int] = None) -> StepRecord:
+         scan_all: bool = True, force: Optional[int] = None,
+         beta: float = 0.0) -> StepRecord:
     """One step of K candidates: evaluate, then commit the first that passes.
 
     scan_all=False stops at the first improving candidate (the sequential
@@ -64,17 +117,19 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
     `force` (None, -1 or k) overrides the decision; used only by parity tests
     where the decision lies inside the floating-point tie band.
     """
-    L_t, cands, losses, chosen = evaluate(model, t, K, seed, tag, delta, mode,
-                                          accept_ties, scan_all)
+    L_t, cands, dls, mags, th, chosen = evaluate_all(model, t, K, seed, tag, delta, mode,
+                                                     accept_ties, scan_all, beta)
+    losses = [L_t + d for d in dls]
     if force is not None:
         chosen = force
     if chosen >= 0:
         model.commit(cands[chosen], losses[chosen])
-    return StepRecord(t, L_t, cands, losses, chosen, model.loss())
+    return StepRecord(t, L_t, cands, losses, chosen, model.loss(), dls, mags, th)
 
 
 def run(model, t0: int, n_steps: int, K: int, seed: int, tag: int, delta: float,
-        mode: str = "weight", accept_ties: bool = False, scan_all: bool = False):
+        mode: str = "weight", accept_ties: bool = False, scan_all: bool = False,
+        beta: float = 0.0):
     """n_steps consecutive steps starting at step t0; returns the records."""
-    return [step(model, t, K, seed, tag, delta, mode, accept_ties, scan_all)
+    return [step(model, t, K, seed, tag, delta, mode, accept_ties, scan_all, beta=beta)
             for t in range(t0, t0 + n_steps)]

@@ -13,8 +13,14 @@ Two evaluators of the loss after a single-weight mutation:
   of every layer from the last accepted state; a change of W_l[j, i] moves
   only column j of z_l (by d * a_{l-1}[:, i]); that changes a_l[:, j], which
   moves z_{l+1} by a rank-1 term (the fan-out column W_{l+1}[:, j], the O(N)
-  work per sample of Sec. 2.4); every later layer is recomputed densely.
-  Pinned against ``FullMLP`` to rounding.
+  work per sample of Sec. 2.4); every later layer changes densely.  It
+  carries the *changes* of the fields from layer to layer and forms the
+  loss change from them (``ce_change``), so that a loss change far below
+  the loss itself keeps its relative precision: deep nets with small
+  initial weights change the loss by 1e-11 per mutation, where L' - L of two
+  fp64 totals near 2.3 would keep only four digits.  Pinned against
+  ``FullMLP`` (where the change is large) and against a long-double full
+  recomputation (where it is small).
 
 Arrays are sample-major (N x units) here; all arithmetic is float64.
 """
@@ -32,6 +38,40 @@ def phi(z, act: str, gamma: float = 1.0):
     if act == "gauss":
         return np.exp(-gamma * z * z)
     raise ValueError(act)
+
+
+def dphi(z, dz, act: str, gamma: float = 1.0):
+    """phi(z + dz) - phi(z) without cancellation, from two textbook identities:
+    tanh a - tanh b = sinh(a - b) / (cosh a cosh b), and
+    exp(-g a^2) - exp(-g b^2) = exp(-g b^2) expm1(-g (a - b)(a + b)).
+    Exactly zero where dz is zero."""
+    if act == "tanh":
+        return np.sinh(dz) / (np.cosh(z) * np.cosh(z + dz))
+    if act == "gauss":
+        arg = -gamma * dz * (2.0 * z + dz)
+        with np.errstate(over="ignore", invalid="ignore"):
+            small = np.exp(-gamma * z * z) * np.expm1(arg)
+        # a move far out of a saturated tail: no cancellation to avoid
+        return np.where(arg > 30.0, phi(z + dz, act, gamma) - phi(z, act, gamma), small)
+    raise ValueError(act)
+
+
+def softmax(logits):
+    """Row-wise softmax (max-shifted)."""
+    e = np.exp(logits - logits.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def ce_change(p, dz, y):
+    """Change of each sample's cross-entropy when its logits move by dz (Eq. 2):
+    l(z + dz) - l(z) = log(sum_c p_c e^{dz_c}) - dz_y
+                     = log1p(sum_c p_c expm1(dz_c)) - dz_y,  p = softmax(z).
+    Returns (per-sample change, per-sample size of its first-order terms
+    sum_c p_c |dz_c| + |dz_y|, the scale of the rounding of any evaluation)."""
+    rows = np.arange(dz.shape[0])
+    dl = np.log1p((p * np.expm1(dz)).sum(axis=1)) - dz[rows, y]
+    mag = (p * np.abs(dz)).sum(axis=1) + np.abs(dz[rows, y])
+    return dl, mag
 
 
 def per_sample_ce(logits, y):
@@ -117,6 +157,20 @@ class FullMLP(_Base):
         ws[c.layer] = wl
         return self.loss_of(ws)
 
+    def delta(self, c: Candidate):
+        """(L(W') - L(W), A): the definition of the loss change, and the size
+        A of its first-order terms over the logit change (see ce_change)."""
+        ws = list(self.state.weights)
+        wl = ws[c.layer].copy()
+        wl[c.j, c.i] = self.state.new_value(c)
+        ws[c.layer] = wl
+        W0 = [w.astype(np.float64) for w in self.state.weights]
+        W1 = [w.astype(np.float64) for w in ws]
+        z0 = forward_fields(W0, self.X, self.act, self.gamma)[-1]
+        z1 = forward_fields(W1, self.X, self.act, self.gamma)[-1]
+        _, mag = ce_change(softmax(z0), z1 - z0, self.y)
+        return mean_ce(z1, self.y) - mean_ce(z0, self.y), float(np.mean(mag))
+
     def commit(self, c: Candidate, loss_after: float):
         """Apply c; the loss of the new state is the one just evaluated for it
         (the same deterministic recomputation of the same weights)."""
@@ -145,43 +199,58 @@ class IncrementalMLP(_Base):
             return self.X[:, i]
         return phi(self.Z[l - 1][:, i], self.act, self.gamma)
 
-    def _propagate(self, c: Candidate):
-        """Fields that change under candidate c.
-
-        Returns (new column j of z_l, {m: new z_m for every later layer m}).
-        """
+    def _changes(self, c: Candidate):
+        """The changes of the local fields under candidate c (Sec. 2.4):
+        (change of column j of z_l, {m: change of z_m for every later layer})."""
         l, j, i = c.layer, c.j, c.i
         nL = len(self.Z)
         d = np.float64(self.state.new_value(c)) - np.float64(self.state.weights[l][j, i])
-        col = self.Z[l][:, j] + d * self._act_in(l, i)
+        dcol = d * self._act_in(l, i)
         later = {}
         if l == nL - 1:
-            return col, later
-        da = phi(col, self.act, self.gamma) - phi(self.Z[l][:, j], self.act, self.gamma)
-        Wn = self.state.weights[l + 1].astype(np.float64)
-        z = self.Z[l + 1] + np.outer(da, Wn[:, j])
-        later[l + 1] = z
+            return dcol, later
+        # the activation change of unit j, then the rank-1 term through the
+        # fan-out column W_{l+1}[:, j]
+        da = dphi(self.Z[l][:, j], dcol, self.act, self.gamma)
+        dz = np.outer(da, self.state.weights[l + 1][:, j].astype(np.float64))
+        later[l + 1] = dz
+        # every later layer: dz_m = (phi(z_{m-1} + dz_{m-1}) - phi(z_{m-1})) W_m^T
         for m in range(l + 2, nL):
-            z = phi(z, self.act, self.gamma) @ self.state.weights[m].astype(np.float64).T
-            later[m] = z
-        return col, later
+            da = dphi(self.Z[m - 1], dz, self.act, self.gamma)
+            dz = da @ self.state.weights[m].astype(np.float64).T
+            later[m] = dz
+        return dcol, later
 
-    def _logits(self, c: Candidate, col, later):
+    def _logit_change(self, c: Candidate, dcol, later):
         nL = len(self.Z)
         if c.layer == nL - 1:
-            z = self.Z[-1].copy()
-            z[:, c.j] = col
-            return z
+            dz = np.zeros_like(self.Z[-1])
+            dz[:, c.j] = dcol
+            return dz
         return later[nL - 1]
 
+    def sample_changes(self, c: Candidate):
+        """Per-sample loss changes and their first-order sizes (ce_change)."""
+        dcol, later = self._changes(c)
+        return ce_change(softmax(self.Z[-1]), self._logit_change(c, dcol, later), self.y)
+
+    def delta(self, c: Candidate):
+        """(dL, A): the loss change of candidate c (Eq. 2 difference), from the
+        field changes, and the mean size A of its first-order terms."""
+        dl, mag = self.sample_changes(c)
+        return float(np.mean(dl)), float(np.mean(mag))
+
     def eval(self, c: Candidate) -> float:
-        col, later = self._propagate(c)
-        return mean_ce(self._logits(c, col, later), self.y)
+        return self.L + self.delta(c)[0]
 
     def commit(self, c: Candidate, loss_after: float):
-        col, later = self._propagate(c)
-        self.Z[c.layer][:, c.j] = col
-        for m, z in later.items():
-            self.Z[m] = z
+        """Apply c: every cached field moves by its change; the committed loss
+        moves by the candidate's loss change (loss_after = L + dL)."""
+        dcol, later = self._changes(c)
+        dl, _ = ce_change(softmax(self.Z[-1]), self._logit_change(c, dcol, later), self.y)
+        dL = float(np.mean(dl))
+        self.Z[c.layer][:, c.j] += dcol
+        for m, dz in later.items():
+            self.Z[m] += dz
         self.state.apply(c)
-        self.L = mean_ce(self.Z[-1], self.y)
+        self.L = self.L + dL

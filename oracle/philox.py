@@ -18,6 +18,9 @@ Decoding of one 4x64-bit block (w0, w1, w2, w3):
   fp32), d = fl32(delta * r), new value fl32(w + d);
 * ternary jump: bit b = w3 >> 63 picks the b-th of the two codes other than
   the current one, in ascending order (Eq. 12 with W_ij in {-1, 0, +1}).
+
+The Metropolis rule (Eq. 7) needs one more uniform per candidate: word w0
+of the block at counter (t, k, 1, 0), U = (w0 >> 11) * 2^-53 in [0, 1).
 """
 from __future__ import annotations
 
@@ -67,6 +70,12 @@ def unit_r(w2: int) -> np.float32:
 def draw(seed: int, tag: int, t: int, k: int):
     """The block for candidate k of step t: key (seed, tag), counter (t, k, 0, 0)."""
     return philox4x64((t, k, 0, 0), (seed, tag))
+
+
+def accept_uniform(seed: int, tag: int, t: int, k: int) -> float:
+    """The acceptance uniform of candidate k of step t (Eq. 7): exact in fp64."""
+    w0 = philox4x64((t, k, 1, 0), (seed, tag))[0]
+    return float(w0 >> 11) * 2.0 ** -53
 
 
 @dataclass(frozen=True)

@@ -191,3 +191,69 @@ def test_scan_all_and_first_improver_agree():
     assert [r.chosen for r in ra] == [r.chosen for r in rb]
     for u, v in zip(a.state.weights, b.state.weights):
         np.testing.assert_array_equal(u, v)
+
+
+@pytest.mark.parametrize("beta,dL", [(50.0, 0.01), (200.0, 0.004), (10.0, 0.2), (1e3, 1e-3)])
+def test_metropolis_acceptance_frequency(beta, dL):
+    """Eq. 7: a candidate with change dL > 0 passes with probability
+    exp(-beta dL); over 40,000 candidates of the stream the frequency is
+    within 4.5 sigma of it."""
+    n = 40000
+    hits = 0
+    for m in range(n):
+        th = mca.thresholds(9, 1, m // 64, 64, beta)[m % 64] if m % 64 == 0 else None
+        if th is None:
+            from oracle.philox import accept_uniform
+            th = mca.metropolis_threshold(accept_uniform(9, 1, m // 64, m % 64), beta)
+        hits += mca.accepts(dL, False, th)
+    p = math.exp(-beta * dL)
+    sigma = math.sqrt(p * (1 - p) / n)
+    assert abs(hits / n - p) <= 4.5 * sigma + 1e-12, (hits / n, p)
+
+
+def test_metropolis_never_rejects_downhill_or_zero():
+    from oracle.philox import accept_uniform
+    for t in range(200):
+        th = mca.metropolis_threshold(accept_uniform(3, 3, t, 0), 7.0)
+        assert th > 0
+        assert mca.accepts(0.0, False, th) and mca.accepts(-1e-9, False, th)
+        assert not mca.accepts(float("nan"), False, th)
+
+
+def test_metropolis_infinite_beta_is_greedy_with_ties():
+    """beta -> infinity: Eq. 7 becomes the greedy rule that accepts dL <= 0
+    (min{1, e^0} = 1), so the run equals the ties-accepting greedy run bit
+    for bit; the net has dead inputs, so zero changes occur."""
+    X, y, Ws = random_net((6, 5, 4), 80, 31, scale=1.0)
+    X[:, 4:] = 0.0
+    a = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    b = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    ra = mca.run(a, 0, 300, 3, 5, 6, 0.3, accept_ties=True, scan_all=True)
+    rb = mca.run(b, 0, 300, 3, 5, 6, 0.3, scan_all=True, beta=1e300)
+    zero_acc = 0
+    for p, q in zip(ra, rb):
+        assert p.chosen == q.chosen
+        assert p.dls == q.dls
+        zero_acc += p.chosen >= 0 and p.dls[p.chosen] == 0.0
+    assert zero_acc > 0
+    for u, v in zip(a.state.weights, b.state.weights):
+        assert u.tobytes() == v.tobytes()
+
+
+def test_metropolis_run_climbs_uphill_sometimes():
+    """A finite beta accepts some moves with dL > 0, each with U < exp(-beta dL)."""
+    from oracle.philox import accept_uniform
+    X, y, Ws = random_net((8, 6, 4), 100, 32, scale=1.0)
+    model = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    beta = 300.0
+    recs = mca.run(model, 0, 400, 2, 11, 12, 0.2, scan_all=True, beta=beta)
+    up = 0
+    for r in recs:
+        if r.chosen >= 0 and r.dls[r.chosen] > 0:
+            up += 1
+            u = accept_uniform(11, 12, r.t, r.chosen)
+            assert u < math.exp(-beta * r.dls[r.chosen])
+        for k in range(r.chosen if r.chosen >= 0 else len(r.dls)):
+            u = accept_uniform(11, 12, r.t, k)
+            assert not (u < math.exp(-beta * r.dls[k]))
+    assert up > 0

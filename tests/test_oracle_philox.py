@@ -152,3 +152,35 @@ def test_ternary_moves():
         assert c.code != cur and c.code in (-1, 0, 1)
         assert c.code == ternary_next(cur, w[3] >> 63)
         assert Fraction(float(c.d)) == (c.code - cur) * Fraction(float(scales[0]))
+
+
+@pytest.mark.parametrize("delta", [0.05, 0.01, 0.1])
+def test_decode_increment_from_numpy_words(delta):
+    """The continuous increment of Eq. 1 rebuilt from numpy's raw Philox words
+    and exact rationals: r = (w2 >> 40) / 2^23 - 1 (word w2, top 24 bits) and
+    d = the fp32 nearest to fl32(delta) * r.  Decoding r from any other word,
+    or other bits, fails here."""
+    shapes = [(16384, 784), (10, 16384)]
+    df = Fraction(float(np.float32(delta)))
+    for t in range(200):
+        w = numpy_block((t, 3, 0, 0), (4002, 2))
+        c = decode(draw(4002, 2, t, 3), shapes, delta, "weight")
+        r = Fraction(w[2] >> 40, 2 ** 23) - 1
+        exact = df * r  # <= 48 significant bits: exact in fp64
+        assert Fraction(float(exact)) == exact
+        want = np.float32(float(exact))  # one rounding to single precision
+        assert np.float32(c.d).tobytes() == want.tobytes(), (t, c.d, want)
+        P = sum(a * b for a, b in shapes)
+        assert c.flat == (w[0] * P) >> 64
+
+
+def test_accept_uniform_from_numpy_words():
+    """The Metropolis uniform (Eq. 7): word w0 of the block at counter
+    (t, k, 1, 0), U = (w0 >> 11) / 2^53, exact in fp64."""
+    from oracle.philox import accept_uniform
+    for t, k in [(0, 0), (7, 3), (19999, 63), (2 ** 33, 1)]:
+        w = numpy_block((t, k, 1, 0), (4001, 1))
+        u = accept_uniform(4001, 1, t, k)
+        assert Fraction(u) == Fraction(w[0] >> 11, 2 ** 53)
+        assert 0.0 <= u < 1.0
+        assert u != float(Fraction(draw(4001, 1, t, k)[0] >> 11, 2 ** 53))  # not stream 0
