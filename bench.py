@@ -25,14 +25,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 MFMA_FP32_PEAK_TFS = 157.3  # MI355X dense fp32 matrix
-VALU_FP32_PEAK_TFS = 157.3  # MI355X fp32 vector (256 CUs x 2.4 GHz x 256 flop/clk, packed FMA)
+# MI355X fp32 vector: 157.3 TFLOP/s with packed (two-wide) FMA; the library is
+# built with packed fp32 instructions off, so one FMA per lane per clock:
+# 256 CUs x 2.4 GHz x 128 flop/clk = 78.6 TFLOP/s is the reachable ALU peak.
+VALU_FP32_PEAK_TFS = 78.6
 
 
 def algorithmic_bytes_per_step(cfg) -> float:
     """Bytes one evaluation launch must move at least (one step of K candidates).
 
-    Shared by all candidates of the step: the logits (4 N C), the cached
-    per-sample losses (4 N) and the labels (N, one byte each).  Per candidate
+    Shared by all candidates of the step: the softmax of the logits (4 N C),
+    from which each sample's loss change is formed, and the labels (N, one
+    byte each).  Per candidate
     in the last hidden layer: the input column and the mutated unit's row of
     local fields (8 N); per candidate in the output layer: the input unit's row
     of local fields (4 N).  Candidates fall in each layer in proportion to its
@@ -41,7 +45,7 @@ def algorithmic_bytes_per_step(cfg) -> float:
     N, C, K = cfg.n_samples, cfg.n_classes, cfg.K
     sizes = cfg.layer_sizes()
     P = float(sum(sizes))
-    shared = 4.0 * N * C + 4.0 * N + N
+    shared = 4.0 * N * C + N
     per_cand = 0.0
     L = cfg.n_layers
     for l, s in enumerate(sizes):
@@ -50,12 +54,12 @@ def algorithmic_bytes_per_step(cfg) -> float:
 
 
 def eval_bytes(cfg, cands) -> float:
-    """Algorithmic bytes of one batched evaluation launch: the shared logits,
-    per-sample losses and labels once, plus each candidate's rows (8 N for a
+    """Algorithmic bytes of one batched evaluation launch: the shared softmax
+    rows and labels once, plus each candidate's rows (8 N for a
     last-hidden-layer weight, 4 N for a logit-layer weight)."""
     N, C, L = cfg.n_samples, cfg.n_classes, cfg.n_layers
     rows = sum(8.0 * N if int(c["layer"]) == L - 2 else 4.0 * N for c in cands)
-    return 4.0 * N * C + 4.0 * N + N + rows
+    return 4.0 * N * C + N + rows
 
 
 def incremental_phase(ctx, cfg, step: int, batch: int, reps: int):
@@ -182,45 +186,155 @@ def workload_config(cfg):
             "n_params": cfg.n_params}
 
 
-def cpu_baseline(cfg, w, seconds: float):
-    """The fp64 oracle (incremental mode for MLPs, full recomputation for the
-    Transformer; all K candidates scored per step, as the device does) on the
-    host cores, for about `seconds` of work."""
-    import numpy as np
+def host_threads():
+    """Cores this process may run on, and the BLAS threads numpy uses."""
     from threadpoolctl import threadpool_info
+    cores = len(os.sched_getaffinity(0))
+    blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
+    return cores, (blas[0] if blas else None)
 
-    from oracle import mca as omca
-    t0 = time.perf_counter()
+
+def oracle_model(cfg, w, mode):
+    """The fp64 oracle: "incremental" (its own field-change evaluator) or
+    "full" (the definition: every candidate recomputes the whole forward
+    pass).  The Transformer oracle has only the full mode."""
     if cfg.kind == "transformer":
         from oracle.transformer import TransformerModel
-        ref = TransformerModel(w["params"], w["tokens"], w["targets"], cfg.vocab, cfg.ctx,
-                               cfg.d_model, cfg.n_layer, cfg.n_head, cfg.d_mlp, cfg.ln_eps)
-        ref.loss()
-    else:
-        from oracle.mlp import IncrementalMLP, MLPState
-        ref = IncrementalMLP(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"],
-                             cfg.act, cfg.gamma)
-    t_init = time.perf_counter() - t0
-    n_steps = 0
-    evals = 0
-    acc = 0
+        return TransformerModel(w["params"], w["tokens"], w["targets"], cfg.vocab, cfg.ctx,
+                                cfg.d_model, cfg.n_layer, cfg.n_head, cfg.d_mlp, cfg.ln_eps)
+    from oracle.mlp import FullMLP, IncrementalMLP, MLPState
+    cls = IncrementalMLP if mode == "incremental" else FullMLP
+    return cls(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"], cfg.act, cfg.gamma)
+
+
+def cpu_baseline(cfg, w, seconds: float, mode: str, scan_all: bool):
+    """The fp64 oracle as it stands, on the host cores, for about `seconds`
+    of work (at least one candidate).  scan_all: score all K candidates of
+    each step (what the device does); otherwise stop at the first one that
+    passes, the paper's sequential method."""
+    from oracle import mca as omca
     t0 = time.perf_counter()
-    while time.perf_counter() - t0 < seconds:
+    ref = oracle_model(cfg, w, mode)
+    ref.loss()
+    t_init = time.perf_counter() - t0
+    n_steps = evals = acc = 0
+    pick = getattr(cfg, "layer_pick", "weight")
+    t0 = time.perf_counter()
+    while evals == 0 or time.perf_counter() - t0 < seconds:
         rec = omca.step(ref, n_steps, cfg.K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-                        getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, scan_all=True)
+                        pick, cfg.accept_ties, scan_all=scan_all)
         n_steps += 1
         evals += len(rec.losses)
         acc += rec.chosen >= 0
     el = time.perf_counter() - t0
-    blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
-    mode = "full-recompute" if cfg.kind == "transformer" else "incremental"
-    return {"value": evals / el, "unit": "candidate evals/s", "cores": 1,
-            "kind": "oracle",
-            "sample": (f"fp64 {mode} oracle, first {n_steps} steps x K={cfg.K} of the "
-                       f"same workload from the same seeded init ({el:.1f} s; numpy "
-                       f"element-wise work on one thread, BLAS threads {blas} for its "
-                       f"matrix products; {t_init:.1f} s setup not timed)"),
+    cores, blas = host_threads()
+    label = {"incremental": "fp64 incremental oracle", "full": "fp64 full-recompute oracle"}[
+        "full" if cfg.kind == "transformer" else mode]
+    return {"value": evals / el, "unit": "candidate evals/s", "cores": cores,
+            "blas_threads": blas, "kind": "oracle", "mode": mode if cfg.kind != "transformer" else "full",
+            "scan": "all K" if scan_all else "stop at first improver",
+            "sample": (f"{label}, first {n_steps} step(s) x K={cfg.K} "
+                       f"({'all scored' if scan_all else 'until the first improver'}) of the same "
+                       f"workload from the same seeded init ({el:.1f} s; {t_init:.1f} s setup "
+                       f"not timed)"),
             "accepted_per_s": acc / el}
+
+
+def make_context(cfg, w, k_max, args):
+    from paper_2607_08406_amd import mca
+    if cfg.kind == "transformer":
+        desc = mca.transformer_desc(cfg.vocab, cfg.ctx, cfg.d_model, cfg.n_layer, cfg.n_head,
+                                    cfg.d_mlp, delta=cfg.delta, ln_eps=cfg.ln_eps,
+                                    accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                                    stream_tag=cfg.stream_tag)
+        return mca.TransformerContext(desc, w["params"], w["tokens"], w["targets"], k_max=k_max)
+    desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
+                        ternary_scales=w["scales"], pick=cfg.layer_pick,
+                        accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
+                        stream_tag=cfg.stream_tag)
+    ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=k_max, codes=w["codes"])
+    if args.tile:
+        ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
+    if args.per_phase:
+        ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, 0)
+    if args.plain_launch:
+        ctx.set_option(mca.MCA_OPT_LOOP_LAUNCH, 1)
+    return ctx
+
+
+def load_workload(cfg):
+    from workloads import mlp_workload, transformer_workload
+    return transformer_workload(cfg) if cfg.kind == "transformer" else mlp_workload(cfg)
+
+
+def measure(cfg, w, steps, warmup, args, eval_batch=0):
+    """Time `steps` device steps after `warmup`; returns the result object
+    (throughput, roofline of the dominant kernel) and the context."""
+    import numpy as np
+    import torch
+
+    from paper_2607_08406_amd import mca
+    ctx = make_context(cfg, w, max(cfg.K, eval_batch), args)
+    if warmup:
+        ctx.run_steps(warmup, cfg.K)
+    mca.mca_get_timing(ctx.ctx, reset=True)
+    # the dominant kernel: the persistent step loop (one launch runs every
+    # timed step), or the evaluation phase when each phase is its own launch
+    mca.mca_set_timing(ctx.ctx, (1 << mca.PHASES.index("eval")) | (1 << mca.PHASES.index("step_loop")))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    st, _, _ = ctx.run_steps(steps, cfg.K)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms, launches = mca.mca_get_timing(ctx.ctx, reset=True)
+    mca.mca_set_timing(ctx.ctx, 0)
+    loop = launches[mca.PHASES.index("step_loop")] > 0
+    dominant = mca.PHASES.index("step_loop" if loop else "eval")
+    n_launch = max(int(launches[dominant]), 1)
+    avg_s = ms[dominant] / 1e3 / n_launch
+    t_first = st.next_step - steps
+    sample = range(0, steps, max(steps // 40, 1))
+    if cfg.kind == "transformer":
+        per_step = float(np.mean([transformer_flops(cfg, ctx.propose(t_first + n, cfg.K))
+                                  for n in sample]))
+        achieved = per_step / avg_s / 1e12
+        roof = {"bound": "mfma", "kernel": "eval phase (k_tf_gemm dominant)",
+                "achieved": achieved, "peak": MFMA_FP32_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
+                "flops_per_launch": per_step}
+    elif cfg.n_layers <= 2:
+        kernel = "k_step_loop" if loop else "k_eval_tiles"
+        # one loop launch covers all timed steps; one eval launch covers one step
+        bytes_launch = algorithmic_bytes_per_step(cfg) * (steps / n_launch if loop else 1)
+        achieved = bytes_launch / avg_s / 1e9
+        roof = {"bound": "hbm" if cfg.name != "tiny" else "latency", "kernel": kernel,
+                "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS,
+                "traffic": (measured_traffic(kernel, cfg.name, steps)
+                            if loop and cfg.name == "wide" else None),
+                "bytes_per_launch": bytes_launch,
+                "bytes_per_step": algorithmic_bytes_per_step(cfg)}
+    else:
+        params, _ = ctx.params()
+        per_step = float(np.mean([candidate_flops(cfg, w, ctx.propose(t_first + n, cfg.K), params)
+                                  for n in sample]))
+        achieved = per_step / avg_s / 1e12
+        deep = cfg.n_layers >= 4
+        peak = MFMA_FP32_PEAK_TFS if deep else VALU_FP32_PEAK_TFS
+        roof = {"bound": "mfma" if deep else "alu",
+                "kernel": "eval phase (k_chain dominant)" if deep else "eval phase (k_slab dominant)",
+                "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": None, "flops_per_launch": per_step}
+    roof["avg_launch_us"] = avg_s * 1e6
+    roof["launches"] = int(launches[dominant])
+    out = {"workload": workload_config(cfg)["workload"], "steps": steps, "warmup": warmup,
+           "ms_per_step": wall * 1e3 / steps, "evals_per_s": st.evaluated / wall,
+           "accepted_per_s": st.accepted / wall,
+           "accept_rate_per_step": st.accepted / max(st.steps, 1),
+           "tie_band": int(st.tie_band),
+           "tie_band_per_eval": st.tie_band / max(st.evaluated, 1),
+           "final_loss": st.loss, "roofline": roof}
+    return out, ctx, st, wall
 
 
 def copy_calibration(nbytes: int):
@@ -234,17 +348,28 @@ def copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes": nbytes, "launches": 5}), flush=True)
 
 
+# Per-config windows of the multi-config line (the headline config times
+# exactly --steps): long enough that launch and copy overheads are small.
+SUB_STEPS = {"tiny": (20000, 200), "deep": (60, 3), "ternary": (1000, 20),
+             "transformer": (100, 5)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5000)
-    ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--workload", default="wide")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--workload", default="wide", help="the headline workload")
+    ap.add_argument("--configs", default="tiny,deep,ternary,transformer",
+                    help="the other workloads measured into the same line ('' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--sub-cpu-seconds", type=float, default=3.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--tile", type=int, default=0, help="samples per workgroup (16..64)")
     ap.add_argument("--per-phase", action="store_true",
                     help="one launch per phase per step instead of the persistent loop")
+    ap.add_argument("--plain-launch", action="store_true",
+                    help="launch the persistent loop with an ordinary (not cooperative) launch")
     ap.add_argument("--eval-batch", type=int, default=1024,
                     help="candidates per launch of the incremental-phase measurement "
                          "(one- and two-layer MLPs; 0 skips it)")
@@ -262,91 +387,14 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
-    import torch
-
-    from paper_2607_08406_amd import mca
-    from workloads import CONFIGS, mlp_workload, transformer_workload
+    from workloads import CONFIGS
 
     cfg = CONFIGS[args.workload]
-    if cfg.kind == "transformer":
-        w = transformer_workload(cfg)
-        desc = mca.transformer_desc(cfg.vocab, cfg.ctx, cfg.d_model, cfg.n_layer, cfg.n_head,
-                                    cfg.d_mlp, delta=cfg.delta, ln_eps=cfg.ln_eps,
-                                    accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
-                                    stream_tag=cfg.stream_tag)
-        ctx = mca.TransformerContext(desc, w["params"], w["tokens"], w["targets"], k_max=cfg.K)
-    else:
-        w = mlp_workload(cfg)
-        desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
-                            ternary_scales=w["scales"], pick=cfg.layer_pick,
-                            accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
-                            stream_tag=cfg.stream_tag)
-        eval_batch = args.eval_batch if cfg.n_layers <= 2 else 0
-        ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=max(cfg.K, eval_batch),
-                          codes=w["codes"])
-    if args.tile:
-        ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
-    if args.per_phase:
-        ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, 0)
-    print(f"[bench] {cfg.name}: context ready, warmup {args.warmup} steps", file=sys.stderr,
+    w = load_workload(cfg)
+    eval_batch = args.eval_batch if cfg.kind != "transformer" and cfg.n_layers <= 2 else 0
+    print(f"[bench] {cfg.name}: {args.steps} timed steps after {args.warmup}", file=sys.stderr,
           flush=True)
-    ctx.run_steps(args.warmup, cfg.K)
-    mca.mca_get_timing(ctx.ctx, reset=True)
-    # the dominant kernel: the persistent step loop (one launch runs every
-    # timed step), or the evaluation kernel when each phase is its own launch
-    mca.mca_set_timing(ctx.ctx, (1 << mca.PHASES.index("eval")) | (1 << mca.PHASES.index("step_loop")))
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    st, _, _ = ctx.run_steps(args.steps, cfg.K)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms, launches = mca.mca_get_timing(ctx.ctx, reset=True)
-    mca.mca_set_timing(ctx.ctx, 0)
-    print(f"[bench] timed {args.steps} steps in {wall:.3f} s", file=sys.stderr, flush=True)
-
-    loop = launches[mca.PHASES.index("step_loop")] > 0
-    dominant = mca.PHASES.index("step_loop" if loop else "eval")
-    n_launch = max(int(launches[dominant]), 1)
-    avg_s = ms[dominant] / 1e3 / n_launch
-    if cfg.kind == "transformer":
-        t_first = st.next_step - args.steps
-        flops = [transformer_flops(cfg, ctx.propose(t_first + n, cfg.K))
-                 for n in range(0, args.steps, max(args.steps // 50, 1))]
-        per_step = float(np.mean(flops))
-        achieved = per_step / avg_s / 1e12
-        roof = {"bound": "mfma", "kernel": "eval phase (k_tf_gemm dominant)",
-                "achieved": achieved, "peak": MFMA_FP32_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
-                "flops_per_launch": per_step, "avg_launch_us": avg_s * 1e6,
-                "launches": int(launches[dominant])}
-    elif cfg.n_layers <= 2:
-        kernel = "k_step_loop" if loop else "k_eval_tiles"
-        # one loop launch covers all timed steps; one eval launch covers one step
-        bytes_launch = algorithmic_bytes_per_step(cfg) * (args.steps / n_launch if loop else 1)
-        achieved = bytes_launch / avg_s / 1e9
-        roof = {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                "traffic": (measured_traffic(kernel, "wide", args.steps)
-                            if loop and cfg.name == "wide" else None),
-                "bytes_per_launch": bytes_launch, "avg_launch_us": avg_s * 1e6,
-                "launches": int(launches[dominant]),
-                "bytes_per_step": algorithmic_bytes_per_step(cfg)}
-    else:
-        # the evaluation phase of one step: its candidates' algorithmic flops
-        params, _ = ctx.params()
-        t_first = st.next_step - args.steps
-        flops = [candidate_flops(cfg, w, ctx.propose(t_first + n, cfg.K), params)
-                 for n in range(0, args.steps, max(args.steps // 50, 1))]
-        per_step = float(np.mean(flops))
-        achieved = per_step / avg_s / 1e12
-        deep = cfg.n_layers >= 4
-        peak = MFMA_FP32_PEAK_TFS if deep else VALU_FP32_PEAK_TFS
-        roof = {"bound": "mfma" if deep else "alu",
-                "kernel": "eval phase (k_chain dominant)" if deep else "eval phase (k_slab dominant)",
-                "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": None, "flops_per_launch": per_step, "avg_launch_us": avg_s * 1e6,
-                "launches": int(launches[dominant])}
+    head, ctx, st, wall = measure(cfg, w, args.steps, args.warmup, args, eval_batch)
     result = {
         "metric": "candidate loss evals/sec + accepted mutations/sec at 1 GPU; % HBM/MFMA roofline",
         "value": st.evaluated / wall,
@@ -363,18 +411,40 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": workload_config(cfg),
-        "roofline": roof,
+        "roofline": head["roofline"],
+        "tie_band": head["tie_band"],
+        "tie_band_per_eval": head["tie_band_per_eval"],
         "final_loss": st.loss,
     }
-    if cfg.kind != "transformer" and eval_batch > 0:
+    if eval_batch > 0:
         print(f"[bench] incremental phases: {args.eval_reps} batches of {eval_batch}",
               file=sys.stderr, flush=True)
         result["incremental_phase"] = incremental_phase(ctx, cfg, st.next_step, eval_batch,
                                                         args.eval_reps)
     ctx.close()
+    subs = {}
+    for name in [c for c in args.configs.split(",") if c and c != cfg.name]:
+        sc = CONFIGS[name]
+        steps, warm = SUB_STEPS.get(name, (200, 10))
+        print(f"[bench] {name}: {steps} timed steps after {warm}", file=sys.stderr, flush=True)
+        sw = load_workload(sc)
+        sub, sctx, _, _ = measure(sc, sw, steps, warm, args)
+        sctx.close()
+        if not args.no_cpu_baseline:
+            sub["cpu_baseline"] = cpu_baseline(sc, sw, args.sub_cpu_seconds, "incremental", True)
+        subs[name] = sub
+        del sw
+    head_sub = dict(head)
+    subs[cfg.name] = head_sub
+    result["configs"] = subs
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(cfg, w, args.cpu_seconds)
+        base = cpu_baseline(cfg, w, args.cpu_seconds, "incremental", True)
+        if cfg.kind != "transformer":
+            # the definition in the paper's sequential mode (stop at the first
+            # improver): one or more full fp64 forward passes per candidate
+            base["full_recompute"] = cpu_baseline(cfg, w, args.cpu_seconds, "full", False)
+        result["cpu_baseline"] = base
     print(json.dumps(result), flush=True)
 
 

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define MCA_ABI_VERSION 1
+#define MCA_ABI_VERSION 2
 #define MCA_MAX_LAYERS 32  /* maximum number of MLP weight matrices */
 #define MCA_MAX_CLASSES 16 /* maximum MLP output width (logits kept in registers) */
 
@@ -70,6 +70,10 @@ extern "C" {
 #define MCA_WEIGHTS_FP32 0    /* continuous fp32 weights, w -> fl32(w + d) (Eq. 1) */
 #define MCA_WEIGHTS_TERNARY 1 /* w = code * scale_l, code in {-1, 0, 1} (Eq. 12) */
 
+/* selection rules */
+#define MCA_RULE_GREEDY 0     /* accept iff dL < 0 (dL <= 0 with accept_ties) (Eq. 6) */
+#define MCA_RULE_METROPOLIS 1 /* accept with probability min{1, exp(-beta dL)} (Eq. 7) */
+
 /* how a candidate picks its parameter */
 #define MCA_PICK_WEIGHT 0 /* uniform over all parameters */
 #define MCA_PICK_LAYER 1  /* uniform layer, then uniform inside it */
@@ -93,7 +97,27 @@ typedef struct mca_net_desc {
   /* Transformer (MCA_NET_TRANSFORMER) */
   int32_t vocab, ctx, d_model, n_block, n_head, d_mlp;
   float ln_eps;
+  /* selection rule (Eq. 6 / Eq. 7).  Metropolis: candidate k of step t draws
+   * U from Philox block (t, k, 1, 0), word 0: U = (w0 >> 11) * 2^-53, and passes
+   * iff dL < -ln(U) / beta (the same event as U < exp(-beta dL)). */
+  int32_t accept_rule;                  /* MCA_RULE_* */
+  /* pruning (Sec. 2.2, "w -> 0"): in every step candidates 0 .. n_prune-1
+   * set their weight to zero (d = -w; ternary: code 0), the rest are the
+   * ordinary mutations; n_prune >= K gives pure pruning, 0 none.  Pruning
+   * candidates come first in stream order, so they are preferred. */
+  int32_t n_prune;
+  double beta;                          /* Metropolis selection intensity, > 0 */
+  /* minibatch (Sec. 2.2): 0 = every sample; otherwise the loss changes of
+   * steps t with floor(t / subset_period) = e are averaged over the
+   * subset_size samples n = (e * subset_size + m) mod N, m < subset_size (a
+   * cyclic window over the sample order).  Caches stay exact for every
+   * sample. */
+  int64_t subset_size;
+  int64_t subset_period;
 } mca_net_desc;
+
+/* mca_cand.flags */
+#define MCA_CAND_PRUNE 1 /* set the weight to zero (Sec. 2.2): w' = 0, d = -w, code 0 */
 
 /* One proposed single-parameter mutation (32 bytes). */
 typedef struct mca_cand {
@@ -101,9 +125,9 @@ typedef struct mca_cand {
   int32_t layer; /* parameter tensor (MLP: weight matrix) index */
   int32_t j;     /* row: output unit (1-D tensors: element) */
   int32_t i;     /* column: input unit (1-D tensors: 0) */
-  float d;       /* continuous: fp32 increment fl32(delta * r); ternary: fl32(w' - w) */
+  float d;       /* continuous: fp32 increment fl32(delta * r); ternary or pruning: fl32(w' - w) */
   int32_t code;  /* ternary: the new code (-1, 0, 1); continuous: 0 */
-  int32_t reserved;
+  int32_t flags; /* MCA_CAND_* */
 } mca_cand;
 
 /* Data set.  MLP: x is [n_samples][n_0] fp32 row-major, y the labels in
@@ -203,9 +227,17 @@ int mca_rollback(mca_ctx* ctx);
  *                            phase per step.  Both give the same results up
  *                            to the order of the loss-change sums.
  *   MCA_OPT_LOOP_TILE        samples per workgroup of the persistent loop,
- *                            16..64 (default 64). */
+ *                            16..64 (default 64).
+ *   MCA_OPT_LOOP_LAUNCH      0 (default): launch the persistent loop
+ *                            cooperatively (the runtime guarantees that all
+ *                            its workgroups are resident together); 1: an
+ *                            ordinary launch of the same grid, relying on the
+ *                            library's occupancy check (a workgroup kept out
+ *                            by other work on the GPU makes the loop's bounded
+ *                            waits give up: MCA_EDEVICE, never a hang). */
 #define MCA_OPT_PERSISTENT_LOOP 1
 #define MCA_OPT_LOOP_TILE 2
+#define MCA_OPT_LOOP_LAUNCH 3
 /* Set a tuning option; MCA_EINVAL for an unknown option or value. */
 int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value);
 

@@ -73,16 +73,19 @@ def _delta(model, c):
 
 def evaluate_all(model, t: int, K: int, seed: int, tag: int, delta: float,
                  mode: str = "weight", accept_ties: bool = False, scan_all: bool = True,
-                 beta: float = 0.0):
+                 beta: float = 0.0, n_prune: int = 0):
     """Score candidates (t, 0..K-1) against the committed state without
-    committing.  Returns (L_t, candidates, dL list, sizes list, thresholds,
-    index of the first that passes the test or -1)."""
+    committing; candidates k < n_prune are pruning moves (Sec. 2.2: they come
+    first in stream order, so pruning is preferred).  Returns (L_t,
+    candidates, dL list, sizes list, thresholds, index of the first that
+    passes the test or -1)."""
     L_t = model.loss()
     th = thresholds(seed, tag, t, K, beta)
     cands, dls, mags = [], [], []
     chosen = -1
     for k in range(K):
-        c = model.candidate(seed, tag, t, k, delta, mode)
+        c = (model.candidate(seed, tag, t, k, delta, mode, prune=True) if k < n_prune
+             else model.candidate(seed, tag, t, k, delta, mode))
         dL, mag = _delta(model, c)
         cands.append(c)
         dls.append(dL)
@@ -109,7 +112,7 @@ def evaluate(model, t: int, K: int, seed: int, tag: int, delta: float,
 def step(model, t: int, K: int, seed: int, tag: int, delta: float,
          mode: str = "weight", accept_ties: bool = False,
          scan_all: bool = True, force: Optional[int] = None,
-         beta: float = 0.0) -> StepRecord:
+         beta: float = 0.0, n_prune: int = 0) -> StepRecord:
     """One step of K candidates: evaluate, then commit the first that passes.
 
     scan_all=False stops at the first improving candidate (the sequential
@@ -118,7 +121,7 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
     where the decision lies inside the floating-point tie band.
     """
     L_t, cands, dls, mags, th, chosen = evaluate_all(model, t, K, seed, tag, delta, mode,
-                                                     accept_ties, scan_all, beta)
+                                                     accept_ties, scan_all, beta, n_prune)
     losses = [L_t + d for d in dls]
     if force is not None:
         chosen = force
@@ -129,7 +132,14 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
 
 def run(model, t0: int, n_steps: int, K: int, seed: int, tag: int, delta: float,
         mode: str = "weight", accept_ties: bool = False, scan_all: bool = False,
-        beta: float = 0.0):
+        beta: float = 0.0, n_prune: int = 0):
     """n_steps consecutive steps starting at step t0; returns the records."""
-    return [step(model, t, K, seed, tag, delta, mode, accept_ties, scan_all, beta=beta)
+    return [step(model, t, K, seed, tag, delta, mode, accept_ties, scan_all, beta=beta,
+                 n_prune=n_prune)
             for t in range(t0, t0 + n_steps)]
+
+
+def remaining_weight_ratio(model) -> float:
+    """Fraction of weights that are not zero (the pruning metric of Sec. 2.2)."""
+    ws = model.state.weights
+    return float(sum(np.count_nonzero(w) for w in ws)) / float(sum(w.size for w in ws))

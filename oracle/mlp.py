@@ -56,21 +56,33 @@ def dphi(z, dz, act: str, gamma: float = 1.0):
     raise ValueError(act)
 
 
+def dphi_dz(z, act: str, gamma: float = 1.0):
+    """phi'(z)."""
+    if act == "tanh":
+        t = np.tanh(z)
+        return 1.0 - t * t
+    return -2.0 * gamma * z * np.exp(-gamma * z * z)
+
+
 def softmax(logits):
     """Row-wise softmax (max-shifted)."""
     e = np.exp(logits - logits.max(axis=1, keepdims=True))
     return e / e.sum(axis=1, keepdims=True)
 
 
-def ce_change(p, dz, y):
+def ce_change(p, dz, y, adz=None):
     """Change of each sample's cross-entropy when its logits move by dz (Eq. 2):
     l(z + dz) - l(z) = log(sum_c p_c e^{dz_c}) - dz_y
                      = log1p(sum_c p_c expm1(dz_c)) - dz_y,  p = softmax(z).
     Returns (per-sample change, per-sample size of its first-order terms
-    sum_c p_c |dz_c| + |dz_y|, the scale of the rounding of any evaluation)."""
+    sum_c p_c a_c + a_y, the scale of the rounding of any evaluation), with
+    a = |dz|, or `adz` when given: the sums of the absolute terms each logit
+    change is made of (a sum of many terms of both signs rounds in
+    proportion to those, not to its result)."""
     rows = np.arange(dz.shape[0])
     dl = np.log1p((p * np.expm1(dz)).sum(axis=1)) - dz[rows, y]
-    mag = (p * np.abs(dz)).sum(axis=1) + np.abs(dz[rows, y])
+    a = np.abs(dz) if adz is None else adz
+    mag = (p * a).sum(axis=1) + a[rows, y]
     return dl, mag
 
 
@@ -112,7 +124,10 @@ class MLPState:
         return [w.shape for w in self.weights]
 
     def new_value(self, c: Candidate) -> np.float32:
-        """The proposed fp32 value: fl32(w + d) (Eq. 1) or code' * scale (Eq. 12)."""
+        """The proposed fp32 value: fl32(w + d) (Eq. 1), code' * scale (Eq. 12),
+        or zero for a pruning move (Sec. 2.2, d = -w)."""
+        if c.prune:
+            return np.float32(0.0)
         if self.codes is not None:
             return np.float32(np.float32(c.code) * self.scales[c.layer])
         return np.float32(self.weights[c.layer][c.j, c.i] + c.d)
@@ -132,9 +147,15 @@ class _Base:
         self.act = act
         self.gamma = float(gamma)
 
-    def candidate(self, seed, tag, t, k, delta, mode="weight") -> Candidate:
-        return decode(draw(seed, tag, t, k), self.state.shapes, delta, mode,
-                      self.state.codes, self.state.scales)
+    def candidate(self, seed, tag, t, k, delta, mode="weight", prune=False) -> Candidate:
+        """Candidate k of step t; with prune, the same draw's weight is set to
+        zero instead (d = -w, ternary code 0)."""
+        c = decode(draw(seed, tag, t, k), self.state.shapes, delta, mode,
+                   self.state.codes, self.state.scales)
+        if prune:
+            w = self.state.weights[c.layer][c.j, c.i]
+            c = Candidate(c.flat, c.layer, c.j, c.i, np.float32(np.float32(0.0) - w), 0, True)
+        return c
 
 
 class FullMLP(_Base):
@@ -164,9 +185,11 @@ class FullMLP(_Base):
         wl = ws[c.layer].copy()
         wl[c.j, c.i] = self.state.new_value(c)
         ws[c.layer] = wl
-        W0 = [w.astype(np.float64) for w in self.state.weights]
+        if getattr(self, "_z0", None) is None:  # the committed logits, kept until a commit
+            W0 = [w.astype(np.float64) for w in self.state.weights]
+            self._z0 = forward_fields(W0, self.X, self.act, self.gamma)[-1]
+        z0 = self._z0
         W1 = [w.astype(np.float64) for w in ws]
-        z0 = forward_fields(W0, self.X, self.act, self.gamma)[-1]
         z1 = forward_fields(W1, self.X, self.act, self.gamma)[-1]
         _, mag = ce_change(softmax(z0), z1 - z0, self.y)
         return mean_ce(z1, self.y) - mean_ce(z0, self.y), float(np.mean(mag))
@@ -176,6 +199,7 @@ class FullMLP(_Base):
         (the same deterministic recomputation of the same weights)."""
         self.state.apply(c)
         self._L = float(loss_after)
+        self._z0 = None
 
 
 class IncrementalMLP(_Base):
@@ -189,6 +213,7 @@ class IncrementalMLP(_Base):
         W64 = [w.astype(np.float64) for w in self.state.weights]
         self.Z = forward_fields(W64, self.X, self.act, self.gamma)
         self.L = mean_ce(self.Z[-1], self.y)
+        self._P = None
 
     def loss(self) -> float:
         return self.L
@@ -200,45 +225,96 @@ class IncrementalMLP(_Base):
         return phi(self.Z[l - 1][:, i], self.act, self.gamma)
 
     def _changes(self, c: Candidate):
-        """The changes of the local fields under candidate c (Sec. 2.4):
-        (change of column j of z_l, {m: change of z_m for every later layer})."""
+        """The changes of the local fields under candidate c (Sec. 2.4), on the
+        samples whose field moves (rows: every other sample has exactly zero
+        change in every later layer, since dphi(z, 0) = 0):
+        (rows, change of column j of z_l there, {m: change of z_m there})."""
         l, j, i = c.layer, c.j, c.i
         nL = len(self.Z)
         d = np.float64(self.state.new_value(c)) - np.float64(self.state.weights[l][j, i])
         dcol = d * self._act_in(l, i)
+        rows = np.flatnonzero(dcol)
+        dcol = dcol[rows]
         later = {}
         if l == nL - 1:
-            return dcol, later
+            return rows, dcol, later
         # the activation change of unit j, then the rank-1 term through the
         # fan-out column W_{l+1}[:, j]
-        da = dphi(self.Z[l][:, j], dcol, self.act, self.gamma)
+        da = dphi(self.Z[l][rows, j], dcol, self.act, self.gamma)
         dz = np.outer(da, self.state.weights[l + 1][:, j].astype(np.float64))
         later[l + 1] = dz
         # every later layer: dz_m = (phi(z_{m-1} + dz_{m-1}) - phi(z_{m-1})) W_m^T
         for m in range(l + 2, nL):
-            da = dphi(self.Z[m - 1], dz, self.act, self.gamma)
-            dz = da @ self.state.weights[m].astype(np.float64).T
+            da = dphi(self.Z[m - 1][rows], dz, self.act, self.gamma)
+            Wm = self.state.weights[m].astype(np.float64)
+            dz = da @ Wm.T
             later[m] = dz
-        return dcol, later
+            if m == nL - 1:  # the absolute terms of the logit sums
+                later["abs"] = np.abs(da) @ np.abs(Wm).T
+        return rows, dcol, later
 
-    def _logit_change(self, c: Candidate, dcol, later):
+    def _logit_change(self, c: Candidate, rows, dcol, later):
         nL = len(self.Z)
         if c.layer == nL - 1:
-            dz = np.zeros_like(self.Z[-1])
+            dz = np.zeros((len(rows), self.Z[-1].shape[1]))
             dz[:, c.j] = dcol
             return dz
         return later[nL - 1]
 
+    def _softmax(self):
+        """softmax of the cached logits (kept until the next commit)."""
+        if getattr(self, "_P", None) is None:
+            self._P = softmax(self.Z[-1])
+        return self._P
+
+    def _fwd_terms(self, l, unit, rows):
+        """sum_k |W_l[unit, k] a_{l-1}[n, k]| on the given rows: the size of
+        the terms of unit's local field, which an fp32 forward pass rounds in
+        proportion to."""
+        a = np.abs(self.X[rows]) if l == 0 else np.abs(phi(self.Z[l - 1][rows], self.act, self.gamma))
+        return a @ np.abs(self.state.weights[l][unit].astype(np.float64))
+
+    def _cache_sensitivity(self, c: Candidate, rows, dcol):
+        """Per row, the relative change of the sample's loss change per unit
+        of forward rounding (u * field-term size) in the two cached fields the
+        candidate reads: its input a_{l-1}[n, i] = phi(z_{l-1}[n, i]) (the loss
+        change is linear in it) and, for a hidden unit, its own field z_l[n, j]
+        (through phi(z + dz) - phi(z))."""
+        l, j, i = c.layer, c.j, c.i
+        sens = np.zeros(len(rows))
+        if l >= 1:
+            z_in = self.Z[l - 1][rows, i]
+            a_in = phi(z_in, self.act, self.gamma)
+            sens += np.abs(dphi_dz(z_in, self.act, self.gamma)) * self._fwd_terms(l - 1, i, rows) / np.abs(a_in)
+        if l < len(self.Z) - 1:
+            z = self.Z[l][rows, j]
+            da = dphi(z, dcol, self.act, self.gamma)
+            slope = np.abs(dphi_dz(z + dcol, self.act, self.gamma) - dphi_dz(z, self.act, self.gamma))
+            with np.errstate(divide="ignore", invalid="ignore"):
+                own = np.where(da != 0, slope / np.abs(da), 0.0)
+            sens += own * self._fwd_terms(l, j, rows)
+        return sens
+
     def sample_changes(self, c: Candidate):
-        """Per-sample loss changes and their first-order sizes (ce_change)."""
-        dcol, later = self._changes(c)
-        return ce_change(softmax(self.Z[-1]), self._logit_change(c, dcol, later), self.y)
+        """(rows, per-sample loss changes there, their first-order sizes there);
+        every other sample's change is zero.  The sizes add to the terms of
+        the change itself (ce_change) its sensitivity to the rounding of the
+        cached fields it reads (_cache_sensitivity)."""
+        rows, dcol, later = self._changes(c)
+        dl, mag = ce_change(self._softmax()[rows], self._logit_change(c, rows, dcol, later),
+                            self.y[rows], later.get("abs"))
+        # an fp32 dot product rounds its result by about 2^-24 times the sum
+        # of its terms' sizes: 1/16 of the size unit the evaluation's own
+        # arithmetic is counted in (see ce_change's callers)
+        mag = mag + np.abs(dl) * self._cache_sensitivity(c, rows, dcol) / 16.0
+        return rows, dl, mag
 
     def delta(self, c: Candidate):
         """(dL, A): the loss change of candidate c (Eq. 2 difference), from the
         field changes, and the mean size A of its first-order terms."""
-        dl, mag = self.sample_changes(c)
-        return float(np.mean(dl)), float(np.mean(mag))
+        _, dl, mag = self.sample_changes(c)
+        N = self.X.shape[0]
+        return float(dl.sum()) / N, float(mag.sum()) / N
 
     def eval(self, c: Candidate) -> float:
         return self.L + self.delta(c)[0]
@@ -246,11 +322,14 @@ class IncrementalMLP(_Base):
     def commit(self, c: Candidate, loss_after: float):
         """Apply c: every cached field moves by its change; the committed loss
         moves by the candidate's loss change (loss_after = L + dL)."""
-        dcol, later = self._changes(c)
-        dl, _ = ce_change(softmax(self.Z[-1]), self._logit_change(c, dcol, later), self.y)
-        dL = float(np.mean(dl))
-        self.Z[c.layer][:, c.j] += dcol
+        rows, dcol, later = self._changes(c)
+        dl, _ = ce_change(self._softmax()[rows], self._logit_change(c, rows, dcol, later),
+                          self.y[rows])
+        dL = float(dl.sum()) / self.X.shape[0]
+        self.Z[c.layer][rows, c.j] += dcol
         for m, dz in later.items():
-            self.Z[m] += dz
+            if m != "abs":
+                self.Z[m][rows] += dz
+        self._P = None
         self.state.apply(c)
         self.L = self.L + dL

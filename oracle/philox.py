@@ -81,14 +81,16 @@ def accept_uniform(seed: int, tag: int, t: int, k: int) -> float:
 @dataclass(frozen=True)
 class Candidate:
     """A single-parameter mutation: parameter `flat` = tensor `layer`, row j,
-    column i; `d` the fp32 increment (continuous) or fl32(w' - w) (ternary);
-    `code` the new ternary code (0 for continuous weights)."""
+    column i; `d` the fp32 increment (continuous) or fl32(w' - w) (ternary,
+    pruning); `code` the new ternary code (0 for continuous weights); `prune`
+    a pruning move (w' = 0)."""
     flat: int
     layer: int
     j: int
     i: int
     d: np.float32
     code: int = 0
+    prune: bool = False  # set the weight to zero (Sec. 2.2): w' = 0, d = -w
 
 
 def ternary_next(code: int, bit: int) -> int:

@@ -19,7 +19,7 @@ import numpy as np
 from scipy.special import erf
 
 from .philox import Candidate, decode, draw
-from .mlp import mean_ce
+from .mlp import ce_change, mean_ce, per_sample_ce, softmax
 
 
 def param_layout(vocab, ctx, d, n_layer, d_mlp):
@@ -129,6 +129,36 @@ class TransformerModel:
         ps[c.layer] = p
         return self.loss_of(ps)
 
+    def _base(self):
+        """The committed logits and per-position losses (kept until a commit)."""
+        if getattr(self, "_z0", None) is None:
+            z = self.logits_of(self.params)
+            V = z.shape[-1]
+            self._z0 = z.reshape(-1, V)
+            self._l0 = per_sample_ce(self._z0, self.targets.reshape(-1))
+        return self._z0, self._l0
+
+    def delta(self, c: Candidate):
+        """(dL, R): the loss change by its definition, L(W') - L(W) (Eq. 2),
+        here as the mean of the per-position changes of two full fp64
+        recomputations (fp64 keeps ~1e-16 of losses near ln 65, far below
+        the 1e-6 changes), and R = sqrt(sum_n (l_n + max_c |z_nc|)^2) / N over
+        the positions whose loss the change reaches: the size of the
+        rounding of an fp32 evaluation that recomputes those positions'
+        losses (independent per position, so it adds in quadrature)."""
+        z0, l0 = self._base()
+        ps = list(self.params)
+        p = ps[c.layer].copy()
+        p[self._index(c)] = self.new_value(c)
+        ps[c.layer] = p
+        z1 = self.logits_of(ps).reshape(z0.shape)
+        l1 = per_sample_ce(z1, self.targets.reshape(-1))
+        moved = np.any(z1 != z0, axis=1)
+        N = z0.shape[0]
+        size = (l0 + np.abs(z0).max(axis=1))[moved]
+        return float((l1 - l0).sum()) / N, float(np.sqrt((size * size).sum())) / N
+
     def commit(self, c: Candidate, loss_after: float):
         self.params[c.layer][self._index(c)] = self.new_value(c)
         self._L = float(loss_after)
+        self._z0 = None

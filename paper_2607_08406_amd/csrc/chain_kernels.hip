@@ -1,20 +1,24 @@
 // Evaluation and commit of mutations in the deep layers of an MLP (layers
-// 0..L-4: "Single-parameter MCA Training of Deep Networks"): changing
-// W_l[j, i] moves unit j of layer l for every sample whose input a_{l-1}[n, i]
-// is nonzero; its activation change da[n] moves every unit of layer l+1 by
-// da[n] * W_{l+1}[:, j] (rank-1), and from there on every later layer is a
-// dense product, z_m = W_m phi(z_{m-1}) for m = l+2 .. L-2, then the logits
-// z_{L-1} = W_{L-1} phi(z_{L-2}) and the cross-entropy.  The dense products are
+// 0..L-4, Sec. 2.1): changing W_l[j, i] moves unit j of layer l for every
+// sample whose input a_{l-1}[n, i] is nonzero; its activation change da[n]
+// moves every unit of layer l+1 by da[n] * W_{l+1}[:, j] (rank-1), and from
+// there on every later layer changes densely.  The kernels carry the
+// *changes*: dz_m = W_m dA_{m-1} for m = l+2 .. L-2, with
+// dA_m = phi(z_m + dz_m) - phi(z_m) formed by dphi() from the cached field
+// z_m, then the logit change dz_{L-1} = W_{L-1} dA_{L-2} and each sample's
+// loss change from it and the cached softmax (ce_change).  A deep net with
+// small weights changes its loss by 1e-11 per mutation; a recomputed loss
+// minus the cached one would keep none of it in fp32.  The dense products are
 // the dominant work and run on the matrix cores (v_mfma_f32_16x16x4f32).
 //
 // k_rows lists, per candidate and in increasing sample order, the samples
 // whose activation changes, with their da.  A block of k_chain takes one
-// candidate and 64 listed samples: it builds phi(z_{l+1} + da W_{l+1}[:, j])
-// in an LDS tile ([64][256], rows padded), runs the dense layers tile to tile
-// (4 waves, each 64 samples x 64 output units as 4 x 4 MFMA tiles), computes
-// the logits and the loss change of each sample against its cached loss, and
-// adds the 64 changes in list order.  The commit runs the same arithmetic for
-// the chosen candidate and writes every recomputed local field back.
+// candidate and 64 listed samples: it builds dA_{l+1} in an LDS tile
+// ([64][256], rows padded), runs the dense layers tile to tile (4 waves, each
+// 64 samples x 64 output units as 4 x 4 MFMA tiles), computes the logit
+// changes and the loss change of each sample, and adds the 64 changes in
+// list order.  The commit runs the same arithmetic for the chosen candidate
+// and moves every cached field by its change.
 //
 // The hidden layers touched here must be exactly kChainUnits wide.
 #include "device_common.hpp"
@@ -70,9 +74,9 @@ __global__ __launch_bounds__(kRowsThreads) void k_rows(NetDev net_arg, const mca
       const float x = (l == 0) ? xr : act_fn(xr, act, gamma);
       if (x != 0.f) {
         const float zl = gload(&zrow[n]);
-        const float zn = zl + de * x;
-        da = act_fn(zn, act, gamma) - act_fn(zl, act, gamma);
-        if (commit) gstore(&zrow[n], zn);
+        const float dz = de * x;
+        da = dphi(zl, dz, act, gamma);
+        if (commit) gstore(&zrow[n], zl + dz);
       }
     }
     const bool take = da != 0.f;
@@ -114,8 +118,8 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
                                                          const DevState* st) {
   __shared__ NetDev net;
   stage_net(net, net_arg);
-  // activations, [sample][unit], rewritten in place layer by layer (one tile
-  // keeps two blocks resident per CU)
+  // activation changes, [sample][unit], rewritten in place layer by layer
+  // (one tile keeps two blocks resident per CU)
   __shared__ float ta[kChainT * kRowStride];
   __shared__ float wcol[kChainUnits];
   __shared__ int rown[kChainT];
@@ -154,8 +158,8 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
     wcol[tid] = gload(&Ws[(int64_t)tid * kChainUnits + c.j]);  // kChainThreads == kChainUnits
   }
   __syncthreads();
-  // 2. z_s + da W_s[:, j], activated, into the tile (unit-major source:
-  // consecutive threads take consecutive rows of one unit)
+  // 2. dA_s = phi(z_s + da W_s[:, j]) - phi(z_s) into the tile (unit-major
+  // source: consecutive threads take consecutive rows of one unit)
   {
     float* Zs = net.Z[s];
     for (int e = tid; e < kChainT * kChainUnits; e += kChainThreads) {
@@ -163,17 +167,29 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
       const int n = rown[r];
       float v = 0.f;
       if (n >= 0) {
-        v = gload(&Zs[(int64_t)u * Ns + n]) + rowda[r] * wcol[u];
-        if (commit) gstore(&Zs[(int64_t)u * Ns + n], v);
+        const float z = gload(&Zs[(int64_t)u * Ns + n]);
+        const float dz = rowda[r] * wcol[u];
+        v = dphi(z, dz, act, gamma);
+        if (commit) gstore(&Zs[(int64_t)u * Ns + n], z + dz);
       }
-      ta[r * kRowStride + u] = (n >= 0) ? act_fn(v, act, gamma) : 0.f;
+      ta[r * kRowStride + u] = v;
     }
   }
   __syncthreads();
-  // 3. dense layers m = s+1 .. L-2: tile = phi(tile W_m^T); every wave has
-  // read the whole tile before any writes its new values
+  // 3. dense layers m = s+1 .. L-2: dz = tile W_m^T, then the tile becomes
+  // phi(z_m + dz) - phi(z_m); every wave has read the whole tile before any
+  // writes its new values
   float* const tin = ta;
   const int q = lane >> 4, li = lane & 15;
+  // the samples of this lane's output rows 16 sb + 4 q + v (row 0 for padding
+  // rows: their changes are zero)
+  int nrow[4][4];
+#pragma unroll
+  for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) nrow[sb][v] = rown[16 * sb + 4 * q + v];
+  // every row of the tile holds the next sample after the one before
+  const bool rows_dense = rown[kChainT - 1] == rown[0] + kChainT - 1 && (rown[0] & 3) == 0;
   for (int m = s + 1; m <= L - 2; ++m) {
     const float* Wm = net.W[m];
     floatx4 acc[4][4];
@@ -210,9 +226,35 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) bcur[cb] = bnext[cb];
     }
-    __syncthreads();
-    // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, unit 64 w + 16 cb + li
+    // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, unit 64 w + 16 cb + li;
+    // the cached fields of those elements, all requested before any is used.
+    // A lane's four rows v = 0..3 are four consecutive samples whenever the
+    // tile lists every sample (a candidate past the first layer): one 16-byte
+    // load each then (16-byte aligned: the tile starts at a multiple of 64).
     float* Zm = net.Z[m];
+    float zc[4][4][4];
+    if (rows_dense) {
+#pragma unroll
+      for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const int u = 64 * wave + 16 * cb + li;
+          const floatx4 z4 = gload(reinterpret_cast<const floatx4*>(&Zm[(int64_t)u * Ns + nrow[sb][0]]));
+#pragma unroll
+          for (int v = 0; v < 4; ++v) zc[sb][cb][v] = z4[v];
+        }
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int u = 64 * wave + 16 * cb + li, nr = nrow[sb][v];
+            zc[sb][cb][v] = gload(&Zm[(int64_t)u * Ns + (nr >= 0 ? nr : 0)]);
+          }
+    }
+    __syncthreads();
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
@@ -220,13 +262,14 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int r = 16 * sb + 4 * q + v, u = 64 * wave + 16 * cb + li;
-          const float z = acc[sb][cb][v];
-          if (commit && rown[r] >= 0) gstore(&Zm[(int64_t)u * Ns + rown[r]], z);
-          tin[r * kRowStride + u] = act_fn(z, act, gamma);
+          const float dz = acc[sb][cb][v];
+          const float z = zc[sb][cb][v];
+          if (commit && nrow[sb][v] >= 0) gstore(&Zm[(int64_t)u * Ns + nrow[sb][v]], z + dz);
+          tin[r * kRowStride + u] = dphi(z, dz, act, gamma);
         }
     __syncthreads();
   }
-  // 4. logits z_{L-1} = W_{L-1} a_{L-2}: thread (r, cq) takes classes cq, cq+4, ...
+  // 4. logit changes dz_{L-1} = W_{L-1} dA_{L-2}: thread (r, cq) takes classes cq, cq+4, ...
   {
     const float* WL = net.W[L - 1];
     const int r = tid >> 2, cq = tid & 3;
@@ -242,21 +285,33 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_chain(NetDev net_arg, cons
     }
   }
   __syncthreads();
-  // 5. per-sample loss change; the tile's sum in list order
+  // 5. per-sample loss change from the logit change and the cached softmax;
+  // the tile's sum in list order
   if (tid < kChainT) {
     const int n = rown[tid];
     float d = 0.f;
     if (n >= 0) {
-      float z[CM];
+      const int y = gload(&net.y[n]);
+      float dz[CM], p[CM], dzy = 0.f;
 #pragma unroll
-      for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? logit[tid][cc] : 0.f;
-      const float ln = ce_loss<CM>(z, C, gload(&net.y[n]));
-      d = ln - gload(&net.ell[n]);
+      for (int cc = 0; cc < CM; ++cc) {
+        dz[cc] = (cc < C) ? logit[tid][cc] : 0.f;
+        p[cc] = (cc < C) ? gload(&net.prob[(int64_t)cc * Ns + n]) : 0.f;
+        dzy = (cc == y) ? dz[cc] : dzy;
+      }
+      d = ce_change<CM>(p, dz, C, dzy);
       if (commit) {
         float* ZL = net.Z[L - 1];
+        float z[CM], pn[CM];
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? gload(&ZL[(int64_t)cc * Ns + n]) + dz[cc] : 0.f;
+        const float ln = softmax_ce<CM>(z, C, y, pn);
 #pragma unroll
         for (int cc = 0; cc < CM; ++cc)
-          if (cc < C) gstore(&ZL[(int64_t)cc * Ns + n], z[cc]);
+          if (cc < C) {
+            gstore(&ZL[(int64_t)cc * Ns + n], z[cc]);
+            gstore(&net.prob[(int64_t)cc * Ns + n], pn[cc]);
+          }
         gstore(&net.ell[n], ln);
       }
     }

@@ -1,13 +1,19 @@
 // Device-side building blocks shared by every MCA kernel: the network
 // description passed by value to each launch, the per-candidate prepared
-// values, the device state word block, the transfer functions, the per-sample
-// cross-entropy, and the Philox4x64-10 candidate stream.
+// values, the device state word block, the transfer functions, the loss
+// change of one sample in difference form, and the Philox4x64-10 candidate
+// stream.
 //
 // All floating point here is IEEE fp32 with contraction disabled at build
 // time; the only fused multiply-adds are the explicit fmaf() calls, so the
-// same expression evaluates to the same bits in every kernel that uses it
-// (evaluation, commit and the full forward pass agree bit for bit on an
-// unchanged sample).
+// same expression evaluates to the same bits in every kernel that uses it.
+//
+// Loss changes are formed from the *changes* of the local fields, never as
+// the difference of two losses: a sample's loss is ~2.3 (ulp 2.4e-7) while a
+// mutation moves it by as little as 1e-11 in a deep net.  With exact
+// identities (tanh and Gaussian differences, the log-sum-exp difference) and
+// an expm1/log1p that keep relative precision near zero, every change keeps
+// a few ulp of relative precision whatever its size.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -34,8 +40,11 @@ struct NetDev {
   float delta;
   float bound;      // > 0: reject |w'| >= bound
   int32_t ties;     // accept dL <= 0
-  int32_t pad0;
+  int32_t rule;     // MCA_RULE_*
   uint64_t seed, tag;
+  double beta;      // Metropolis selection intensity
+  int32_t n_prune;  // candidates 0 .. n_prune-1 of a step set their weight to zero
+  int32_t pad0;
   int64_t N, Ns;    // samples, row stride of the unit-major caches
   int64_t P;        // parameters
   int32_t widths[MCA_MAX_LAYERS + 1];
@@ -46,6 +55,7 @@ struct NetDev {
   float* Z[MCA_MAX_LAYERS];           // Z[l] = output local fields of layer l
   const float* XT;
   float* ell;                         // per-sample loss cache
+  float* prob;                        // softmax of the logits, [C][Ns] (unit-major like Z)
   const int32_t* y;
   float* WT;                          // L >= 3: W_{L-2} transposed ([n_{L-2}][n_{L-1}]), else null
 };
@@ -97,6 +107,7 @@ struct Aux {
   float w_new;
   float de;       // fl32(w_new - w_old): the increment the caches apply
   int32_t valid;  // 0: |w_new| >= bound, rejected without evaluation
+  double theta;   // acceptance threshold: 0 greedy (Eq. 6), -ln(U) / beta Metropolis (Eq. 7)
 };
 
 // Committed scalars and counters, one 256-byte block in the workspace.
@@ -116,20 +127,38 @@ static_assert(sizeof(DevState) <= 256, "state block");
 // ---------------------------------------------------------------------------
 
 // The transcendentals of the hot path use the hardware exp2/log2/rcp units:
-// e^x = 2^(x log2 e), ln x = log2(x) ln 2, tanh z = 1 - 2 / (e^{2z} + 1).
-// Their error (a few ulp, absolute error of tanh near 1e-7) is far below the
-// fp32 rounding of the caches; every kernel (forward, evaluation, commit)
-// calls these same functions, so an unchanged sample evaluates to the same
-// bits everywhere.
+// e^x = 2^(x log2 e), ln x = log2(x) ln 2.  Their error is a few ulp; every
+// kernel (forward, evaluation, commit) calls these same functions, so an
+// unchanged sample evaluates to the same bits everywhere.
 __device__ __forceinline__ float fast_exp(float x) {
   return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
 __device__ __forceinline__ float fast_log(float x) {
   return __builtin_amdgcn_logf(x) * 0.6931471805599453f;
 }
+
+// e^x - 1 for |x| < kEm1Small: the degree-5 Taylor polynomial (truncation
+// below x^5 / 720 < 2^-24 relative there).
+constexpr float kEm1Small = 0.125f;
+__device__ __forceinline__ float em1_small(float x) {
+  float p = fmaf(x, 1.0f / 120.0f, 1.0f / 24.0f);
+  p = fmaf(x, p, 1.0f / 6.0f);
+  p = fmaf(x, p, 0.5f);
+  p = fmaf(x, p, 1.0f);
+  return x * p;
+}
+
+// tanh z with a few ulp of relative error for every z: near zero
+// e / (e + 2) with e = expm1(2z) from the polynomial, elsewhere
+// sign(z) (1 - t) / (1 + t) with t = e^{-2|z|} (1 - 2 / (e^{2z} + 1) would
+// cancel near zero: deep nets with small weights carry activations of 1e-6,
+// which it gets wrong by percents).
 __device__ __forceinline__ float fast_tanh(float z) {
-  const float e = fast_exp(z + z);
-  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+  const float e = em1_small(z + z);
+  const float near = e * __builtin_amdgcn_rcpf(e + 2.0f);
+  const float t = fast_exp(-2.0f * fabsf(z));
+  const float far = copysignf((1.0f - t) * __builtin_amdgcn_rcpf(1.0f + t), z);
+  return (fabsf(z + z) < kEm1Small) ? near : far;
 }
 
 __device__ __forceinline__ float act_fn(float z, int act, float gamma) {
@@ -139,11 +168,59 @@ __device__ __forceinline__ float act_fn(float z, int act, float gamma) {
   return fast_exp(-t);
 }
 
-// Cross-entropy of one sample from its C <= CM logits: logsumexp(z) - z[y],
-// with the maximum subtracted first.  Summation order c = 0..C-1, so every
-// CM >= C gives the same bits.
+// e^x - 1 for every x, a few ulp: the polynomial near zero, elsewhere
+// Kahan's (u - 1) x / ln u with u = e^x, which cancels the rounding of u.
+__device__ __forceinline__ float em1(float x) {
+  const float u = fast_exp(x);
+  const float k = (u - 1.0f) * (x * __builtin_amdgcn_rcpf(fast_log(u)));
+  float r = (x < -17.0f) ? -1.0f : k;  // fl32(e^x - 1) = -1 below -17
+  r = (u == __builtin_huge_valf()) ? u : r;
+  return (fabsf(x) < kEm1Small) ? em1_small(x) : r;
+}
+
+// ln(1 + s) for s > -1, a few ulp: Kahan's ln(u) s / (u - 1) with u = 1 + s.
+__device__ __forceinline__ float lg1p(float s) {
+  const float u = 1.0f + s;
+  const float r = fast_log(u) * (s * __builtin_amdgcn_rcpf(u - 1.0f));
+  return (u == 1.0f) ? s : r;
+}
+
+// tanh(z + dz) - tanh(z) without cancellation: tanh(dz) (1 - tanh z tanh(z + dz)),
+// where, with u = e^{-2|z|} and v = e^{-2|z + dz|}, 1 - tanh a tanh b is
+// 2 (u + v) / ((1 + u)(1 + v)) when a and b share a sign and
+// 2 (1 + u v) / ((1 + u)(1 + v)) otherwise (no difference of near-equal
+// values either way), and tanh(dz) = e / (e + 2) with e = expm1(2 dz).
+// Exactly zero where dz is zero.
+__device__ __forceinline__ float dtanh(float z, float dz) {
+  const float zn = z + dz;
+  const float u = fast_exp(-2.0f * fabsf(z)), v = fast_exp(-2.0f * fabsf(zn));
+  const bool same = (z < 0.0f) == (zn < 0.0f);
+  const float w = same ? u + v : fmaf(u, v, 1.0f);
+  const float f = (2.0f * w) * __builtin_amdgcn_rcpf((1.0f + u) * (1.0f + v));
+  const float e = em1(fminf(fmaxf(2.0f * dz, -40.0f), 40.0f));
+  return (e * __builtin_amdgcn_rcpf(e + 2.0f)) * f;
+}
+
+// exp(-g (z + dz)^2) - exp(-g z^2) = exp(-g z^2) expm1(-g dz (2 z + dz));
+// a move out of a far tail (the expm1 argument above 30) has nothing to
+// cancel and takes the plain difference.  Exactly zero where dz is zero.
+__device__ __forceinline__ float dgauss(float z, float dz, float g) {
+  const float x = (-g * dz) * fmaf(2.0f, z, dz);
+  const float near = act_fn(z, MCA_ACT_GAUSS, g) * em1(x);
+  const float far = act_fn(z + dz, MCA_ACT_GAUSS, g) - act_fn(z, MCA_ACT_GAUSS, g);
+  return (x > 30.0f) ? far : near;
+}
+
+// phi(z + dz) - phi(z) for the net's transfer function.
+__device__ __forceinline__ float dphi(float z, float dz, int act, float gamma) {
+  return (act == MCA_ACT_TANH) ? dtanh(z, dz) : dgauss(z, dz, gamma);
+}
+
+// Softmax p of C <= CM logits and the cross-entropy logsumexp(z) - z[y]
+// (maximum subtracted first; summation order c = 0..C-1, so every CM >= C
+// gives the same bits).  p is zero beyond C.
 template <int CM>
-__device__ __forceinline__ float ce_loss(const float (&z)[CM], int C, int y) {
+__device__ __forceinline__ float softmax_ce(const float (&z)[CM], int C, int y, float (&p)[CM]) {
   float m = z[0];
 #pragma unroll
   for (int c = 1; c < CM; ++c)
@@ -151,78 +228,107 @@ __device__ __forceinline__ float ce_loss(const float (&z)[CM], int C, int y) {
   float s = 0.f, zy = 0.f;
 #pragma unroll
   for (int c = 0; c < CM; ++c) {
-    if (c < C) s += fast_exp(z[c] - m);
+    p[c] = (c < C) ? fast_exp(z[c] - m) : 0.f;
+    s += p[c];
     zy = (c == y) ? z[c] : zy;
   }
+  const float r = __builtin_amdgcn_rcpf(s);
+#pragma unroll
+  for (int c = 0; c < CM; ++c) p[c] *= r;
   return (fast_log(s) + m) - zy;
+}
+
+// Change of one sample's cross-entropy when its logits move by dz[c] (Eq. 2):
+// ln(sum_c p_c e^{dz_c}) - dz_y = log1p(sum_c p_c expm1(dz_c)) - dz_y, with p
+// the softmax of the committed logits.  Zero exactly where every dz is zero.
+template <int CM>
+__device__ __forceinline__ float ce_change(const float (&p)[CM], const float (&dz)[CM], int C,
+                                           float dzy) {
+  float amax = 0.f;
+#pragma unroll
+  for (int c = 0; c < CM; ++c)
+    if (c < C) amax = fmaxf(amax, fabsf(dz[c]));
+  float s = 0.f;
+  if (amax < kEm1Small) {
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+      if (c < C) s = fmaf(p[c], em1_small(dz[c]), s);
+  } else {
+    // large changes (rare): one class at a time, so the general expm1's
+    // temporaries of different classes are never live together
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+      if (c < C) s = fmaf(p[c], em1(dz[c]), s);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  return lg1p(s) - dzy;
 }
 
 // ---------------------------------------------------------------------------
 // one (candidate, sample) pair of a mutation in the last two layers
 // ---------------------------------------------------------------------------
 
-// One (candidate, sample) pair.  ain: the input of the mutated weight (x, or
-// the activation feeding it); zh: the cached local field of the mutated unit
-// when it is a hidden unit; zL: the sample's logits in LDS (class stride ZS).  The
-// new local field, logits and loss come back for a commit.  Written without
-// branches on the candidate's layer (pairs of different candidates share a
-// wave); the step loop and the batched evaluation both score pairs with
-// these expressions, and the column commit applies the same arithmetic.
-// pair_logits_of takes the sample's logits zc and the column wc as values.
-template <int CM>
-__device__ __forceinline__ bool pair_logits_of(int C, int act, float gamma, bool logit, float zb,
-                                               float de, const float (&wc)[CM], float ain,
-                                               const float (&zc)[CM], float& zn, float& da,
-                                               float (&z)[CM]) {
+// One (candidate, sample) pair: the mutated weight's input ain moves its unit
+// by dz = de * ain.  A logit-layer weight moves logit j by dz; a hidden unit's
+// activation moves by da = phi(zh + dz) - phi(zh) (zh its cached local field)
+// and the logits by da * wcol[c] (the unit's logit-layer column).  wcol is
+// one-hot at j for a logit-layer weight, so one expression serves both:
+// da = dz there and dz_c = dz * [c == j].  w holds wcol's C values (the
+// caller loads them: scalars when the pairs share a candidate).  wmax bounds |wcol[c]|: when
+// |da| wmax is small every expm1 takes the polynomial (no per-class test).
+// pL: the sample's softmax in LDS (class stride ZS).  Returns the sample's
+// loss change; da comes back for a commit.  Written without branches on the
+// candidate's layer (pairs of different candidates share a wave); the step
+// loop and the batched evaluation both score pairs with it.
+template <int CM, int ZS = 64>
+__device__ __forceinline__ float pair_change(int C, int act, float gamma, bool logit, float zh,
+                                             float de, const float (&w)[CM], const float* wcol,
+                                             float wmax, float ain, const float* pL, int y,
+                                             float& da) {
   const float dz = de * ain;
-  zn = zb + dz;
-  // A logit-layer candidate's staged column is one-hot at its logit j, which
-  // moves by dz itself: fma(dz, 1, z_j) = z_j + dz = zn and fma(dz, 0, z) = z
-  // exactly, so one expression serves both kinds of candidate.
-  da = logit ? dz : act_fn(zn, act, gamma) - act_fn(zb, act, gamma);
+  da = logit ? dz : dphi(zh, dz, act, gamma);
+  // every softmax operand is loaded unconditionally (the LDS rows hold CM
+  // entries, zero beyond C) so the loads issue together
+  float p[CM];
+#pragma unroll
+  for (int cc = 0; cc < CM; ++cc) p[cc] = pL[cc * ZS];
+  const float wy = wcol[y];
+  float s = 0.f;
+  if (fabsf(da) * wmax < kEm1Small) {
+#pragma unroll
+    for (int cc = 0; cc < CM; ++cc)
+      if (cc < C) s = fmaf(p[cc], em1_small(da * w[cc]), s);
+  } else {
+    // large changes (rare on wide nets): one class at a time from LDS, so the
+    // general expm1's temporaries of different classes are never live together
+#pragma unroll 1
+    for (int cc = 0; cc < C; ++cc) s = fmaf(pL[cc * ZS], em1(da * wcol[cc]), s);
+  }
+  return lg1p(s) - da * wy;
+}
+
+// Maximum of v over lanes 0..15 (one DPP row), returned wave-uniform.  All
+// 64 lanes must be active.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_max_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), kCtrl, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_max_f32<0xB1>(v));   // lane ^ 1
+  v = fmaxf(v, dpp_max_f32<0x4E>(v));   // lane ^ 2
+  v = fmaxf(v, dpp_max_f32<0x141>(v));  // mirror within eight
+  v = fmaxf(v, dpp_max_f32<0x140>(v));  // mirror within sixteen
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+}
+
+// The committed logits after a pair's change: z[c] + da * wcol[c] (for a
+// logit-layer weight, wcol one-hot: only logit j moves, by dz).
+template <int CM>
+__device__ __forceinline__ void moved_logits(int C, float da, const float (&wc)[CM],
+                                             const float (&zc)[CM], float (&z)[CM]) {
 #pragma unroll
   for (int cc = 0; cc < CM; ++cc) z[cc] = (cc < C) ? fmaf(da, wc[cc], zc[cc]) : 0.f;
-  return logit ? dz != 0.f : da != 0.f;  // the logits changed
-}
-
-template <int CM, int ZS = 64>
-__device__ __forceinline__ bool pair_logits(int L, int C, int act, float gamma, int layer, int j,
-                                            float de, const float* wcol, float ain, float zh,
-                                            const float* zL, float& zn, float& da,
-                                            float (&z)[CM]) {
-  const bool logit = layer == L - 1;
-  // every operand is loaded unconditionally (the LDS rows hold CM entries,
-  // zero beyond C) so the loads issue together
-  float zc[CM], wc[CM];
-#pragma unroll
-  for (int cc = 0; cc < CM; ++cc) {
-    zc[cc] = zL[cc * ZS];
-    wc[cc] = wcol[cc];
-  }
-  const float zb = logit ? zL[j * ZS] : zh;
-  return pair_logits_of<CM>(C, act, gamma, logit, zb, de, wc, ain, zc, zn, da, z);
-}
-
-// The pair's new loss ln; returns its loss change.
-template <int CM, int ZS = 64>
-__device__ __forceinline__ float pair_eval(int L, int C, int act, float gamma, int layer, int j,
-                                           float de, const float* wcol, float ain, float zh,
-                                           const float* zL, float ell, int y, float& ln) {
-  float zn, da, z[CM];
-  const bool changed = pair_logits<CM, ZS>(L, C, act, gamma, layer, j, de, wcol, ain, zh, zL, zn, da, z);
-  // ce_loss() with the label's logit computed by the same fma instead of
-  // selected from z: the same bits, without a compare per class
-  const float zy = fmaf(da, wcol[y], zL[y * ZS]);
-  float m = z[0];
-#pragma unroll
-  for (int c = 1; c < CM; ++c)
-    if (c < C) m = fmaxf(m, z[c]);
-  float s = 0.f;
-#pragma unroll
-  for (int c = 0; c < CM; ++c)
-    if (c < C) s += fast_exp(z[c] - m);
-  ln = (fast_log(s) + m) - zy;
-  return changed ? ln - ell : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -273,7 +379,7 @@ __device__ __forceinline__ mca_cand decode_index(const NetDev& net, uint64_t t, 
   c.layer = layer;
   c.j = (int32_t)((uint32_t)off / nin);
   c.i = (int32_t)((uint32_t)off - (uint32_t)c.j * nin);
-  c.reserved = 0;
+  c.flags = ((int64_t)k < (int64_t)net.n_prune) ? MCA_CAND_PRUNE : 0;
   if (net.ternary) {
     c.d = 0.f;
     c.code = (int)(w.w3 >> 63);
@@ -300,25 +406,46 @@ __device__ __forceinline__ void finish_ternary(const NetDev& net, mca_cand& c, i
 
 __device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t t, uint64_t k) {
   mca_cand c = decode_index(net, t, k);
-  if (net.ternary)
-    finish_ternary(net, c, net.codes[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i]);
+  const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+  if (net.ternary) finish_ternary(net, c, net.codes[c.layer][idx]);
+  if (c.flags & MCA_CAND_PRUNE) {  // w' = 0: the increment is -w
+    c.code = 0;
+    c.d = 0.0f - net.W[c.layer][idx];
+  }
   return c;
 }
 
-// New value of a candidate against the committed weights.
+// New value of a candidate against the committed weights (a pruning
+// candidate's is zero).
 __device__ __forceinline__ Aux prepare_candidate(const NetDev& net, const mca_cand& c) {
   Aux a;
   const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
   a.w_old = net.W[c.layer][idx];
-  a.w_new = net.ternary ? (float)c.code * net.scales[c.layer] : a.w_old + c.d;
+  a.w_new = (c.flags & MCA_CAND_PRUNE) ? 0.0f
+            : (net.ternary ? (float)c.code * net.scales[c.layer] : a.w_old + c.d);
   a.de = a.w_new - a.w_old;
   a.valid = !(net.bound > 0.f && fabsf(a.w_new) >= net.bound);
+  a.theta = 0.0;
   return a;
 }
 
-__device__ __forceinline__ bool accepts(double dL, int ties) {
-  // NaN compares false either way, +inf never passes
+// The selection test: Eq. 6 (dL < 0, or dL <= 0 with ties) when theta is 0;
+// the Metropolis rule of Eq. 7 as dL < theta otherwise (theta > 0).  NaN
+// compares false either way, +inf never passes.
+__device__ __forceinline__ bool accepts(double dL, int ties, double theta = 0.0) {
+  if (theta > 0.0) return dL < theta;
   return ties ? (dL <= 0.0) : (dL < 0.0);
+}
+
+// Metropolis threshold of candidate k of step t (Eq. 7): U from word 0 of the
+// Philox block at counter (t, k, 1, 0), U = (w0 >> 11) 2^-53, and
+// U < exp(-beta dL) exactly when dL < -ln(U) / beta.  0 under the greedy rule.
+__device__ __forceinline__ double accept_theta(int rule, double beta, uint64_t seed,
+                                               uint64_t tag, uint64_t t, uint64_t k) {
+  if (rule != MCA_RULE_METROPOLIS) return 0.0;
+  const Words w = philox4x64_10(t, k, 1, 0, seed, tag);
+  const double u = (double)(w.w0 >> 11) * 0x1p-53;
+  return (u == 0.0) ? __builtin_huge_val() : -log(u) / beta;
 }
 
 // Sum of v over the 64 lanes of a wave in one fixed order (a butterfly within

@@ -3,8 +3,10 @@
 // runs many steps of propose -> evaluate -> select -> commit.
 //
 // Work split: tile workgroup g < G owns T <= 64 consecutive samples for the
-// whole launch.  Its share of the logits, cached per-sample losses and labels
-// stays in LDS; the hidden local fields Z_l stay in HBM but each tile of a row
+// whole launch.  Its share of the logits, their softmax and the labels stays
+// in LDS (a pair's loss change is formed from its logit change and the
+// softmax, pair_change; the per-sample losses are recomputed from the final
+// logits when the launch ends); the hidden local fields Z_l stay in HBM but each tile of a row
 // is only ever read and written by its owner.  Every tile workgroup decodes
 // the step's K candidates itself (the stream is counter-based), scores all of
 // them on its tile and publishes one partial loss change per candidate
@@ -55,30 +57,6 @@
 #include "loop_kernel.hpp"
 
 namespace mca {
-
-// Phase timestamps for profiling builds (compiled with -DMCA_PHASE_PROBES);
-// they expand to nothing otherwise.  Slot layout: tile g (0: first tile, 1:
-// last tile) phase p of step s < 256 at (g * 256 + s) * 8 + p; every tile's
-// publish time at 6144 + s * 512 + g; candidate 0's reducer and tile 0's
-// wave 0 at 137216 + s * 4 + {0 fresh, 1 published, 2 poll start, 3 seen};
-// every candidate's publish time at 138240 + s * 64 + k; tile 0's poll
-// iterations at 154624 + s.
-#ifdef MCA_PHASE_PROBES
-__device__ int64_t* g_phase_probes;
-#define MCA_PROBE(slot)                                                        \
-  do {                                                                         \
-    if (probes) probes[slot] = (int64_t)__builtin_amdgcn_s_memrealtime();      \
-  } while (0)
-extern "C" hipError_t mca_set_phase_probes(void* p) {
-  return hipMemcpyToSymbol(HIP_SYMBOL(g_phase_probes), &p, sizeof p);
-}
-#else
-#define MCA_PROBE(slot) \
-  do {                  \
-  } while (0)
-#endif
-constexpr int64_t kProbePost = 6144, kProbeRed = 6144 + 256 * 512;
-constexpr int64_t kProbeRedAll = kProbeRed + 256 * 4;  // + s * 64 + k: candidate k published
 
 namespace {
 
@@ -172,7 +150,10 @@ struct Prep {
 __device__ __forceinline__ Prep make_prep(const NetDev& net, const mca_cand& c, float w, int cur) {
   Prep x;
   x.w_old = w;
-  if (net.ternary) {
+  if (c.flags & MCA_CAND_PRUNE) {  // w' = 0 (Sec. 2.2)
+    x.code = 0;
+    x.w_new = 0.0f;
+  } else if (net.ternary) {
     mca_cand t = c;
     finish_ternary(net, t, cur);
     x.code = t.code;
@@ -197,25 +178,29 @@ template <int CM>
 __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   __shared__ NetDev net;
   stage_net(net, a.net);
-#ifdef MCA_PHASE_PROBES
-  int64_t* const probes = g_phase_probes;
-#endif
-  __shared__ float zl_lds[CM * 64];
-  __shared__ float ell_lds[64];
+  // an earlier launch of this call gave up: nothing runs
+  if (ld_agent(&a.sync->abort) != 0u) return;
+  // the first step's index, from the committed state (every workgroup reads
+  // it before tile 0 can write the next one: no step completes without all)
+  const uint64_t t0 = a.st->t;
+  __shared__ float zl_lds[CM * 64];  // logits, [class][sample]
+  __shared__ float pl_lds[CM * 64];  // their softmax
   __shared__ int y_lds[64];
   __shared__ mca_cand cand_lds[4][kLoopMaxK];  // draws of steps s .. s+3, by step mod 4
+  __shared__ double theta_lds[4][kLoopMaxK];   // their acceptance thresholds (Eq. 7; 0 greedy)
   // each draw's row offsets in the unit-major arrays (elements): its input
   // row and, for a hidden unit, its field row (row 0 otherwise)
   __shared__ uint2 soff_lds[4][kLoopMaxK];
   __shared__ Prep prep_lds[2][kLoopMaxK];       // staged per step parity
   __shared__ float wcol_lds[2][kLoopMaxK][CM];  // logit-layer column (one-hot for a logit weight)
+  __shared__ float wmax_lds[2][kLoopMaxK];      // max |column entry|
   __shared__ float ain_lds[2][kLoopMaxK][64];  // staged per step parity
   __shared__ float zh_lds[2][kLoopMaxK][64];
   // per-pair loss changes, [candidate][sample]; rows of 68 floats keep every
   // row 16-byte aligned and a 16-byte read of the same column by 16 lanes
   // (rows k .. k+15) conflict-free
   __shared__ __attribute__((aligned(16))) float dlp_lds[kLoopMaxK][68];
-  __shared__ float lnp_lds[kLoopMaxK][64];  // each pair's new loss, which a commit reuses
+  __shared__ float dap_lds[kLoopMaxK][64];  // each pair's activation change, which a commit reuses
   __shared__ uint16_t list_lds[2][kLoopMaxK * 64];  // work lists, by step parity
   __shared__ int list_n[2];
   __shared__ uint32_t stage_cnt;  // waves 1-15 that have landed a step (15 per step)
@@ -266,7 +251,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         if (!fresh) ab = __any(spin_step(spins, a));
       }
       if (ab) return;
-      if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4);
       double acc = 0.0;
 #pragma unroll
       for (int b = 0; b < kMaxTilesPerLane; ++b)
@@ -274,8 +258,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const double tot = wave_sum_f64(acc);
       const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
       if (lane < kLoopReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
-      if (k == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 1);
-      if (lane == 0 && s < 256) MCA_PROBE(kProbeRedAll + (int64_t)s * 64 + k);
     }
     return;
   }
@@ -285,11 +267,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   const bool live = lane < T && n < net.N;
   const int nh = net.widths[L - 1];
   const int64_t Ns = net.Ns;
-  // the tile's logits, losses and labels move to LDS for the whole launch
+  // the tile's logits, softmax and labels move to LDS for the whole launch
   if (wave == 0) {
-    for (int c = 0; c < CM; ++c)
+    for (int c = 0; c < CM; ++c) {
       zl_lds[c * 64 + lane] = (live && c < C) ? gload(&net.Z[L - 1][(int64_t)c * Ns + n]) : 0.f;
-    ell_lds[lane] = live ? gload(&net.ell[n]) : 0.f;
+      pl_lds[c * 64 + lane] = (live && c < C) ? gload(&net.prob[(int64_t)c * Ns + n]) : 0.f;
+    }
     y_lds[lane] = live ? gload(&net.y[n]) : 0;
   }
   if (tid < 2) last[tid].valid = 0;
@@ -340,6 +323,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     if (lane < K) {
       const mca_cand c = decode_index(net, t, (uint64_t)lane);
       cand_lds[cb][lane] = c;
+      theta_lds[cb][lane] = accept_theta(net.rule, net.beta, net.seed, net.tag, t, (uint64_t)lane);
       const bool hid = c.layer == Lk - 2;
       soff_lds[cb][lane] = make_uint2((uint32_t)c.i * (uint32_t)Ns, hid ? (uint32_t)c.j * (uint32_t)Ns : 0u);
     }
@@ -373,10 +357,15 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
       const bool hid = c.layer == Lk - 2;
       const bool colhit = lc.valid && lc.layer == Lk - 1 && hid && lc.i == c.j;
+      float wm = 0.f;
 #pragma unroll
-      for (int cc = 0; cc < CM; ++cc)
-        wcol_lds[b][lane][cc] = !hid ? ((cc == c.j) ? 1.f : 0.f)
-                                     : ((colhit && cc == lc.j) ? lc.w_new : col_reg[cc]);
+      for (int cc = 0; cc < CM; ++cc) {
+        const float wv = !hid ? ((cc == c.j) ? 1.f : 0.f)
+                              : ((colhit && cc == lc.j) ? lc.w_new : col_reg[cc]);
+        wcol_lds[b][lane][cc] = wv;
+        wm = fmaxf(wm, fabsf(wv));
+      }
+      wmax_lds[b][lane] = wm;
       prep_lds[b][lane] = make_prep(net, c, w, cur);
     }
   };
@@ -486,7 +475,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // pair slots start clear; after each step wave 0 clears those it summed
   for (int i = tid; i < kLoopMaxK * 68; i += kLoopThreads) (&dlp_lds[0][0])[i] = 0.f;
   if (wave == 1)
-    for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(a.t0 + d, (int)d);
+    for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(t0 + d, (int)d);
   __syncthreads();
   if (wave == 1) {
     issue_cand(0);
@@ -499,9 +488,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   }
   __syncthreads();
 
-  const int psel = (g == 0) ? 0 : ((g == G - 1) ? 1 : -1);
-#define MCA_TILE_PROBE(p) \
-  if (psel >= 0 && tid == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + (p))
   // A step takes two workgroup barriers: after the scoring, and at its end,
   // when wave 0 has decided and committed and waves 1-15 have staged and
   // listed the next step.
@@ -510,7 +496,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     const int buf = (int)(s & 1);
     const int cb = (int)(s & 3);
     mca_cand* cands = cand_lds[cb];
-    MCA_TILE_PROBE(0);
     // 1. every lane of the workgroup scores list entries (the list of step s
     // was built during step s-1); the list of step s+1 starts empty
     const int n_list = list_n[buf];
@@ -518,19 +503,19 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const int code = list_lds[buf][e];
       const int k = code >> 6, sl = code & 63;
       const mca_cand& c = cands[k];
-      float ln;
-      dlp_lds[k][sl] = pair_eval<CM>(L, C, act, gamma, c.layer, c.j, prep_lds[buf][k].de,
-                                     wcol_lds[buf][k],
-                                     ain_lds[buf][k][sl], zh_lds[buf][k][sl], &zl_lds[sl],
-                                     ell_lds[sl], y_lds[sl], ln);
-      lnp_lds[k][sl] = ln;
+      float da, w[CM];
+#pragma unroll
+      for (int cc = 0; cc < CM; ++cc) w[cc] = wcol_lds[buf][k][cc];
+      dlp_lds[k][sl] = pair_change<CM>(C, act, gamma, c.layer == L - 1, zh_lds[buf][k][sl],
+                                       prep_lds[buf][k].de, w, wcol_lds[buf][k], wmax_lds[buf][k],
+                                       ain_lds[buf][k][sl], &pl_lds[sl], y_lds[sl], da);
+      dap_lds[k][sl] = da;
     }
     if (tid == 0) list_n[buf ^ 1] = 0;
     // last step's commit stores land before this step's staging reads HBM
     if (committed) wait_own_memory();
     committed = false;
     __syncthreads();
-    MCA_TILE_PROBE(1);
     // 2. wave 0, lane k: sum candidate k's 64 slots (four runs of 16
     // consecutive samples in order, then the runs pairwise), publish the tile's
     // partial sum and clear the slots for the next step.  Only wave 0 stores
@@ -564,22 +549,17 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) wrow[i] = zero4;
     }
-    MCA_TILE_PROBE(2);
-    if (tid == 0 && s < 256) MCA_PROBE(kProbePost + (int64_t)s * 512 + g);
     // 3. wave 1 draws step s+3, waves 2-15 land and list step s+1 and issue
     // step s+2
     if (wave == 1) {
       if (s + 1 < a.n_steps) land_cand((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
       landed();
       if (s + 2 < a.n_steps) issue_cand((int)((s + 2) & 3));
-      if (s + 3 < a.n_steps) draw(a.t0 + s + 3, (int)((s + 3) & 3));
-      if (psel >= 0 && lane == 0 && s < 256) MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 6);
+      if (s + 3 < a.n_steps) draw(t0 + s + 3, (int)((s + 3) & 3));
     } else if (wave >= 2) {
       if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
       landed();
       if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
-      if (psel >= 0 && wave == 15 && lane == 0 && s < 256)
-        MCA_PROBE(((int64_t)psel * 256 + (int64_t)s) * 8 + 7);
     }
     if (wave == 0) {
       // what the commit and the patch check need whichever candidate wins:
@@ -596,11 +576,11 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         c1 = cand_lds[(s + 1) & 3][lane];
       }
       const uint32_t t16 = tag16(s);
+      const double th = lane < K ? theta_lds[cb][lane] : 0.0;
       const uint64_t* dls = a.dls + (g % kLoopReplicas) * kLoopMaxK;
       uint64_t d = 0;
       uint32_t spins = 0;
       bool ab = false;
-      if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 2);
       // The decision needs the loss changes of candidates 0 .. kc only (kc
       // the first that passes, or all K when none does, or when every dL is
       // traced).  Before the set of step s-1 can be overwritten (next step),
@@ -623,17 +603,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const bool fresh = lane >= K || tg == t16;
         const bool done_prev = fresh || s == 0 || tg == t16p;
         fm = __ballot(fresh);
-        am = __ballot(lane < K && tg == t16 && accepts(unpack_dl(d), net.ties));
+        am = __ballot(lane < K && tg == t16 && accepts(unpack_dl(d), net.ties, th));
         const int pre = (~fm) ? (int)__ffsll((unsigned long long)~fm) - 1 : 64;  // first stale
         const int fa = am ? (int)__ffsll((unsigned long long)am) - 1 : 64;
         if (__all(done_prev) && (pre >= 64 || (!need_all && fa < pre))) break;
         if (fa >= pre && pre >= lim) lim = 64;
         if ((ab = __any(spin_step(spins, a)))) break;
       }
-      if (g == 0 && lane == 0 && s < 256) MCA_PROBE(kProbeRed + (int64_t)s * 4 + 3);
-#ifdef MCA_PHASE_PROBES
-      if (g == 0 && lane == 0 && s < 256 && probes) probes[kProbeRedAll + 256 * 64 + (int64_t)s] = spins;
-#endif
       const double v = unpack_dl(d);
       const int kc = (!ab && am) ? (int)__ffsll((unsigned long long)am) - 1 : -1;
       // 4. commit on this tile (lane = sample; the winner's operands are
@@ -652,26 +628,26 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const bool chid = c.layer == Lk - 2;  // the winner is a hidden-unit weight
       float zr = 0.f;  // the committed unit's row of this tile, lane = sample
       if (kc >= 0) {
-        // the same logits the scoring computed; its loss was kept
+        // the logits move by the activation change the scoring computed
+        // (kept for every listed pair: every sample with a non-zero input)
         const float ain = ain_lds[buf][kc][lane];
         const float z_raw = zh_lds[buf][kc][lane];
-        const float ln = lnp_lds[kc][lane];
+        const float da = dap_lds[kc][lane];
         float wc[CM];
 #pragma unroll
         for (int cc = 0; cc < CM; ++cc) wc[cc] = wcol_lds[buf][kc][cc];
-        const bool logit = c.layer == L - 1;
-        float zb = z_raw;
-#pragma unroll
-        for (int cc = 0; cc < CM; ++cc) zb = (logit && cc == c.j) ? zc[cc] : zb;
-        float zn, da, z[CM];
-        (void)pair_logits_of<CM>(C, act, gamma, logit, zb, au.de, wc, ain, zc, zn, da, z);
+        const float zn = z_raw + au.de * ain;
         const bool ch = live && ain != 0.f;
         if (ch) {
           if (chid) gstore(&z_hid[(int64_t)c.j * Ns + n], zn);
+          float z[CM], p[CM];
+          moved_logits<CM>(C, da, wc, zc, z);
+          (void)softmax_ce<CM>(z, C, y_lds[lane], p);
 #pragma unroll
-          for (int cc = 0; cc < CM; ++cc)
-            if (cc < C) zl_lds[cc * 64 + lane] = z[cc];
-          ell_lds[lane] = ln;
+          for (int cc = 0; cc < CM; ++cc) {
+            zl_lds[cc * 64 + lane] = z[cc];
+            pl_lds[cc * 64 + lane] = p[cc];
+          }
         }
         zr = ch ? zn : z_raw;
         zrow_lds[buf][lane] = zr;
@@ -709,7 +685,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
             __builtin_amdgcn_s_sleep(1);
           __asm__ volatile("" ::: "memory");
           if (same) prep_lds[buf ^ 1][lane] = make_prep(net, c1, au.w_new, au.code);
-          if (col) wcol_lds[buf ^ 1][lane][c.j] = au.w_new;
+          if (col) {
+            wcol_lds[buf ^ 1][lane][c.j] = au.w_new;
+            float wm = 0.f;
+#pragma unroll
+            for (int cc = 0; cc < CM; ++cc) wm = fmaxf(wm, fabsf(wcol_lds[buf ^ 1][lane][cc]));
+            wmax_lds[buf ^ 1][lane] = wm;
+          }
           uint64_t rows = __ballot(row);
           while (rows) {
             const int k = (int)__ffsll((unsigned long long)rows) - 1;
@@ -721,7 +703,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         }
       }
       if (lane == 0) aborted = ab ? 1 : 0;
-      MCA_TILE_PROBE(3);
       // tile 0 keeps the committed loss, the counters and the trace
       if (g == 0 && !ab) {
         const uint64_t tie_mask = __ballot(lane < K && fabs(v) < 1e-6);
@@ -735,10 +716,9 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
           }
           last_k = kc;
         }
-        const uint64_t t = a.t0 + s;
         if (a.tr_chosen != nullptr) {
-          const int64_t slot = (int64_t)(t - a.trace_base);
-          if (slot >= 0 && slot < a.tr_cap) {
+          const int64_t slot = (int64_t)s;  // the trace chunk starts at this launch's first step
+          if (slot < a.tr_cap) {
             if (lane == 0) a.tr_chosen[slot] = kc;
             if (a.tr_dl != nullptr && lane < K) a.tr_dl[slot * K + lane] = v;
           }
@@ -746,19 +726,25 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       }
     }
     __syncthreads();
-    MCA_TILE_PROBE(4);
     if (aborted) break;
   }
-#undef MCA_TILE_PROBE
-  // the tile's logits and losses go back to HBM; tile 0 writes the state
+  // the tile's logits and softmax go back to HBM with the losses of the
+  // final logits; tile 0 writes the state
   if (wave == 0 && live) {
-    for (int c = 0; c < C; ++c) gstore(&net.Z[L - 1][(int64_t)c * Ns + n], zl_lds[c * 64 + lane]);
-    gstore(&net.ell[n], ell_lds[lane]);
+    float z[CM], p[CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) z[c] = zl_lds[c * 64 + lane];
+    const float ln = softmax_ce<CM>(z, C, y_lds[lane], p);
+    for (int c = 0; c < C; ++c) {
+      gstore(&net.Z[L - 1][(int64_t)c * Ns + n], z[c]);
+      gstore(&net.prob[(int64_t)c * Ns + n], pl_lds[c * 64 + lane]);
+    }
+    gstore(&net.ell[n], ln);
   }
   if (g == 0 && tid == 0 && !aborted) {
     DevState* st = a.st;
     st->L = L_acc;
-    st->t = a.t0 + a.n_steps;
+    st->t = t0 + a.n_steps;
     st->steps += a.n_steps;
     st->evaluated += a.n_steps * (uint64_t)K;
     st->accepted = n_acc;
@@ -768,13 +754,12 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 }
 
 // Clears the tags before a launch (a fill kernel, so the sequence can be
-// captured in a graph).
-__global__ void k_reset_loop(LoopSync* s, uint64_t* partials, int64_t n_words, uint64_t* dls,
-                             int K) {
+// captured in a graph).  The abort word is cleared once per call, by the
+// caller: a launch after one that gave up must see it.
+__global__ void k_reset_loop(uint64_t* partials, int64_t n_words, uint64_t* dls) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_words) partials[i] = 0;
   if (i < (int64_t)kLoopReplicas * kLoopMaxK) dls[i] = 0;
-  if (i == 0) s->abort = 0;
 }
 
 namespace {
@@ -786,18 +771,28 @@ const void* pick_loop(int K, int C) {
 
 int step_loop_reducers(int K) { return (K + kReducerWaves - 1) / kReducerWaves; }
 
-hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s) {
+hipError_t launch_step_loop(const LoopArgs& a, bool cooperative, hipStream_t s) {
   const int64_t words = 2 * (int64_t)a.K * a.gpad;
   const int64_t n = words > (int64_t)kLoopReplicas * kLoopMaxK ? words : (int64_t)kLoopReplicas * kLoopMaxK;
-  hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a.sync,
-                     a.partials, words, a.dls, a.K);
+  hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     a.partials, words, a.dls);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // G tile workgroups and the candidate reducers; every workgroup must be
+  // resident at once (the caller checked the occupancy).  The cooperative
+  // launch has the runtime guarantee it; the ordinary one relies on the
+  // check and on the bounded waits (a workgroup that never starts makes the
+  // others give up and abort, never hang).
+  const dim3 grid(a.G + step_loop_reducers(a.K));
+  if (!cooperative) {
+    if (a.net.C == 10)
+      hipLaunchKernelGGL(k_step_loop<10>, grid, dim3(kLoopThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL(k_step_loop<kCMax>, grid, dim3(kLoopThreads), 0, s, a);
+    return hipGetLastError();
+  }
   void* args[] = {(void*)&a};
-  // G tile workgroups and the candidate reducers
-  return hipLaunchCooperativeKernel(pick_loop(a.K, a.net.C),
-                                    dim3(a.G + step_loop_reducers(a.K)), dim3(kLoopThreads), args,
-                                    0, s);
+  return hipLaunchCooperativeKernel(pick_loop(a.K, a.net.C), grid, dim3(kLoopThreads), args, 0, s);
 }
 
 hipError_t step_loop_max_blocks(int K, int C, int* out) {

@@ -25,16 +25,14 @@ struct LoopArgs {
   int T;                // samples per workgroup tile (<= 64)
   int G;                // tile workgroups (<= kLoopMaxTiles)
   int gpad;             // words per candidate row of partials: G rounded up to 16
-  uint64_t t0;          // first step index
-  uint64_t n_steps;     // steps in this launch (< 2^32)
+  uint64_t n_steps;     // steps in this launch (< 2^32); the first is st->t
   uint64_t* partials;   // [2][K][gpad] tagged per-tile loss-change sums, by step parity
   uint64_t* dls;        // [kLoopReplicas][kLoopMaxK] tagged loss changes
   LoopSync* sync;
   DevState* st;
-  int32_t* tr_chosen;   // trace (nullable)
+  int32_t* tr_chosen;   // trace (nullable): slot s = this launch's step s
   double* tr_dl;        // trace of every dL (nullable)
   int64_t tr_cap;
-  uint64_t trace_base;  // step index of trace slot 0
   uint32_t spin_limit;  // polls before a wait gives up and aborts the grid
 };
 
@@ -42,7 +40,7 @@ constexpr int kLoopMaxTiles = 64 * 4;  // one workgroup per CU: at most the CU c
 
 // Workgroups of the candidate reducers for K candidates (four candidates each).
 int step_loop_reducers(int K);
-hipError_t launch_step_loop(const LoopArgs& a, hipStream_t s);
+hipError_t launch_step_loop(const LoopArgs& a, bool cooperative, hipStream_t s);
 hipError_t step_loop_max_blocks(int K, int C, int* out);
 
 }  // namespace mca

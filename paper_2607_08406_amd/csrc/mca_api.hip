@@ -28,6 +28,11 @@ namespace {
 constexpr int64_t kTraceCap = 4096;  // steps per trace chunk kept on the device
 constexpr size_t kAlign = 256;
 constexpr int kMinLoopTile = 16;
+// The committed state (DevState), the snapshot of its counters taken when a
+// run_steps call starts, and the step loop's abort word, on three 256-byte
+// lines of one block: a call reads all three back with one copy.
+constexpr size_t kStateBlock = 3 * 256;
+static_assert(sizeof(DevState) <= 256 && sizeof(mca::LoopSync) <= 256, "state block lines");
 
 thread_local std::string g_thread_error;
 
@@ -38,7 +43,7 @@ struct Layout {
   int64_t Ns = 0;
   int ntiles = 0;     // blocks of the column commit (kTile samples each)
   int ntiles_ev = 0;  // tiles of the batched evaluation (partial sums per candidate)
-  size_t xt = 0, ell = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
+  size_t xt = 0, ell = 0, pr = 0, y = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0, state = 0;
   size_t fmask = 0, cmask = 0;  // batched evaluation: tiles where a feature / candidate can change
   size_t tr_chosen = 0, tr_dl = 0, loop_partials = 0, loop_sync = 0, loop_dls = 0;
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
@@ -50,6 +55,24 @@ struct Layout {
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
   size_t total = 0;
 };
+
+// Selection rule, pruning and minibatch fields (shared by both net kinds).
+std::string check_selection(const mca_net_desc* net, int64_t n_samples, int* code) {
+  *code = MCA_EINVAL;
+  if (net->accept_rule != MCA_RULE_GREEDY && net->accept_rule != MCA_RULE_METROPOLIS)
+    return "unknown accept rule";
+  if (net->accept_rule == MCA_RULE_METROPOLIS && !(std::isfinite(net->beta) && net->beta > 0.0))
+    return "Metropolis beta must be finite and positive";
+  if (net->n_prune < 0) return "n_prune must be >= 0";
+  if (net->subset_size < 0 || net->subset_size > n_samples) return "subset_size out of range [0, n_samples]";
+  if (net->subset_size > 0 && net->subset_period < 1) return "subset_period must be >= 1";
+  *code = MCA_EUNSUPPORTED;
+  if (net->kind == MCA_NET_TRANSFORMER && net->n_prune != 0)
+    return "pruning candidates are built for MLPs only";
+  if (net->subset_size != 0) return "minibatch not built yet";
+  *code = MCA_OK;
+  return "";
+}
 
 std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max, int* code) {
   *code = MCA_EINVAL;
@@ -77,6 +100,10 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   if (!std::isfinite(net->bound)) return "bound must be finite (<= 0 disables it)";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31)) return "n_samples out of range";
   if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
+  {
+    std::string m = check_selection(net, n_samples, code);
+    if (!m.empty()) return m;
+  }
   if (L >= 3 && net->widths[L - 1] > mca::kSlabMaxUnits) {
     *code = MCA_EUNSUPPORTED;
     return "MLPs with three or more layers need a last hidden layer of at most 1024 units";
@@ -129,6 +156,10 @@ std::string tf_check_desc(const mca_net_desc* d, int64_t n_samples, int32_t k_ma
   if (k_max < 1 || k_max > mca::kMaxK) return "k_max out of range [1, 1024]";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31) || n_samples % d->ctx != 0)
     return "n_samples must be a positive multiple of ctx";
+  {
+    std::string m = check_selection(d, n_samples, code);
+    if (!m.empty()) return m;
+  }
   *code = MCA_EUNSUPPORTED;
   if (d->weight_mode != MCA_WEIGHTS_FP32) return "Transformer nets take continuous weights only";
   if (d->pick != MCA_PICK_WEIGHT) return "Transformer nets draw uniformly over all parameters only";
@@ -181,7 +212,7 @@ TfLayout tf_make_layout(const mca_net_desc* d, int64_t N, int32_t k_max) {
   lo.partial = take(K * lo.nblk * sizeof(float));
   lo.dl = take(K * sizeof(double));
   lo.bsum = take((size_t)lo.nblk * sizeof(double));
-  lo.state = take(sizeof(DevState));
+  lo.state = take(kStateBlock);
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * K * sizeof(double));
   lo.sx = take(K * (NB + 1) * n * D * sizeof(float));
@@ -218,6 +249,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     for (int l = 0; l < L; ++l) lo.codes[l] = take((size_t)net->widths[l + 1] * net->widths[l]);
   for (int l = 0; l < L; ++l) lo.z[l] = take((size_t)net->widths[l + 1] * lo.Ns * sizeof(float));
   lo.ell = take(lo.Ns * sizeof(float));
+  lo.pr = take((size_t)net->widths[L] * lo.Ns * sizeof(float));
   lo.y = take(lo.Ns * sizeof(int32_t));
   lo.cands = take((size_t)k_max * sizeof(mca_cand));
   lo.aux = take((size_t)k_max * sizeof(Aux));
@@ -226,7 +258,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.partial = take((size_t)k_max * lo.ntiles_ev * sizeof(float));
   lo.dl = take((size_t)k_max * sizeof(double));
   lo.bsum = take((size_t)lo.ntiles * sizeof(double));
-  lo.state = take(sizeof(DevState));
+  lo.state = take(kStateBlock);
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
   if (L >= 3) {
@@ -252,13 +284,17 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   const int64_t gpad = (g_max + 15) / 16 * 16;
   lo.loop_partials = take((size_t)2 * std::min<int32_t>(k_max, mca::kLoopMaxK) * gpad * sizeof(uint64_t));
   lo.loop_dls = take((size_t)mca::kLoopReplicas * mca::kLoopMaxK * sizeof(uint64_t));
-  lo.loop_sync = take(sizeof(mca::LoopSync));
   lo.total = off;
   return lo;
 }
 
-__global__ void k_set_trace_base(DevState* st, uint64_t v) { st->trace_base = v; }
+__global__ void k_set_trace_base(DevState* st) { st->trace_base = st->t; }
 __global__ void k_set_next_step(DevState* st, uint64_t v) { st->t = v; }
+// Start of a run_steps call: the counters as they stand, and a clear abort word.
+__global__ void k_call_start(const DevState* st, DevState* snap, mca::LoopSync* sync) {
+  *snap = *st;
+  sync->abort = 0;
+}
 
 }  // namespace
 
@@ -289,7 +325,10 @@ struct mca_ctx {
   uint64_t* loop_partials = nullptr;
   uint64_t* loop_dls = nullptr;
   mca::LoopSync* loop_sync = nullptr;
+  DevState* snap = nullptr;  // counters at the start of the current run_steps call
   bool use_loop = true;
+  bool loop_coop = true;     // cooperative launch of the step loop
+  int loop_fit_K = -1, loop_fit = 0;  // resident workgroups of the loop, cached per K
   // Transformer nets
   bool tf = false;
   mca::TfDev tfh{};           // host copy of the device description
@@ -474,6 +513,7 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
       if (c[k].j < 0 || c[k].j >= ctx->tfh.rows[l] || c[k].i < 0 || c[k].i >= ctx->tfh.cols[l])
         return fail(ctx, MCA_EINVAL, "candidate index out of range");
       if (!std::isfinite(c[k].d)) return fail(ctx, MCA_EINVAL, "candidate increment is not finite");
+      if (c[k].flags != 0) return fail(ctx, MCA_EINVAL, "Transformer candidates take no flags");
     }
     return MCA_OK;
   }
@@ -482,6 +522,7 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
     if (l < 0 || l >= d.n_layers) return fail(ctx, MCA_EINVAL, "candidate layer out of range");
     if (c[k].j < 0 || c[k].j >= d.widths[l + 1] || c[k].i < 0 || c[k].i >= d.widths[l])
       return fail(ctx, MCA_EINVAL, "candidate index out of range");
+    if (c[k].flags & ~MCA_CAND_PRUNE) return fail(ctx, MCA_EINVAL, "unknown candidate flags");
     if (d.weight_mode == MCA_WEIGHTS_TERNARY) {
       if (c[k].code < -1 || c[k].code > 1) return fail(ctx, MCA_EINVAL, "candidate code outside {-1, 0, 1}");
     } else if (!std::isfinite(c[k].d)) {
@@ -591,6 +632,8 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   h.delta = net->delta;
   h.bound = net->bound;
   h.ties = net->accept_ties ? 1 : 0;
+  h.rule = net->accept_rule;
+  h.beta = net->beta;
   h.seed = net->seed;
   h.tag = net->stream_tag;
   const std::vector<TfShape> shapes = tf_shapes(net);
@@ -628,6 +671,8 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   ctx->dl = (double*)(ws + lo.dl);
   ctx->bsum = (double*)(ws + lo.bsum);
   ctx->st = (DevState*)(ws + lo.state);
+  ctx->snap = (DevState*)(ws + lo.state + 256);
+  ctx->loop_sync = (mca::LoopSync*)(ws + lo.state + 512);
   ctx->tr_chosen = (int32_t*)(ws + lo.tr_chosen);
   ctx->tr_dl = (double*)(ws + lo.tr_dl);
   // what the shared selection and state calls read
@@ -635,6 +680,8 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   nd.L = 0;
   nd.C = h.V;
   nd.ties = h.ties;
+  nd.rule = h.rule;
+  nd.beta = h.beta;
   nd.N = N;
   nd.Ns = N;
   nd.P = h.P;
@@ -742,6 +789,9 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.delta = net->delta;
   nd.bound = net->bound;
   nd.ties = net->accept_ties ? 1 : 0;
+  nd.rule = net->accept_rule;
+  nd.beta = net->beta;
+  nd.n_prune = net->n_prune;
   nd.seed = net->seed;
   nd.tag = net->stream_tag;
   nd.N = N;
@@ -760,6 +810,7 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.P = off;
   nd.XT = (const float*)(ws + lo.xt);
   nd.ell = (float*)(ws + lo.ell);
+  nd.prob = (float*)(ws + lo.pr);
   nd.y = (const int32_t*)(ws + lo.y);
   nd.WT = (L >= 3) ? (float*)(ws + lo.wt) : nullptr;
   ctx->pslab = (L >= 3) ? (float*)(ws + lo.pslab) : nullptr;
@@ -777,11 +828,12 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   ctx->dl = (double*)(ws + lo.dl);
   ctx->bsum = (double*)(ws + lo.bsum);
   ctx->st = (DevState*)(ws + lo.state);
+  ctx->snap = (DevState*)(ws + lo.state + 256);
+  ctx->loop_sync = (mca::LoopSync*)(ws + lo.state + 512);
   ctx->tr_chosen = (int32_t*)(ws + lo.tr_chosen);
   ctx->tr_dl = (double*)(ws + lo.tr_dl);
   ctx->loop_partials = (uint64_t*)(ws + lo.loop_partials);
   ctx->loop_dls = (uint64_t*)(ws + lo.loop_dls);
-  ctx->loop_sync = (mca::LoopSync*)(ws + lo.loop_sync);
 
   // inputs, transposed to the unit-major layout (zero padding to Ns)
   {
@@ -886,6 +938,11 @@ int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value) {
     ctx->use_loop = value != 0;
     return MCA_OK;
   }
+  if (option == MCA_OPT_LOOP_LAUNCH) {
+    if (value != 0 && value != 1) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_LAUNCH takes 0 or 1");
+    ctx->loop_coop = value == 0;
+    return MCA_OK;
+  }
   if (option == MCA_OPT_LOOP_TILE) {
     if (ctx->tf) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_TILE applies to MLP contexts");
     if (value < kMinLoopTile || value > 64) return fail(ctx, MCA_EINVAL, "MCA_OPT_LOOP_TILE takes 16..64");
@@ -909,15 +966,22 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
   if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
   if (trace != nullptr && trace->chosen == nullptr) return fail(ctx, MCA_EINVAL, "trace.chosen is NULL");
-  DevState before{};
-  int rc = read_state(ctx, &before);
-  if (rc != MCA_OK) return rc;
+  // Nothing is read back until the end: the device state supplies each
+  // launch's first step, a snapshot kernel records the counters the call's
+  // statistics are taken against, and one copy returns state, snapshot and
+  // abort word together.
+  hipLaunchKernelGGL(k_call_start, dim3(1), dim3(1), 0, ctx->stream, ctx->st, ctx->snap,
+                     ctx->loop_sync);
+  MCA_HIP(ctx, hipGetLastError());
   const NetDev& net = ctx->net;
   uint64_t done = 0;
-  int max_blocks = 0;
   const bool mlp2 = !ctx->tf && net.L <= 2;
-  if (ctx->use_loop && mlp2 && K <= mca::kLoopMaxK)
-    MCA_HIP(ctx, mca::step_loop_max_blocks(K, net.C, &max_blocks));
+  if (ctx->use_loop && mlp2 && K <= mca::kLoopMaxK && ctx->loop_fit_K != K) {
+    int fit = 0;
+    MCA_HIP(ctx, mca::step_loop_max_blocks(K, net.C, &fit));
+    ctx->loop_fit = fit;
+    ctx->loop_fit_K = K;
+  }
   // row offsets of the loop's arrays are 32-bit element counts
   bool offsets_fit = true;
   for (int l = 0; l < net.L; ++l)
@@ -925,7 +989,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   // G tile workgroups plus the candidate reducers must all be resident at once
   const bool loop_ok = ctx->use_loop && mlp2 && offsets_fit && K <= mca::kLoopMaxK &&
                        ctx->lo.loop_G <= mca::kLoopMaxTiles &&
-                       ctx->lo.loop_G + mca::step_loop_reducers(K) <= max_blocks;
+                       ctx->lo.loop_G + mca::step_loop_reducers(K) <= ctx->loop_fit;
   while (loop_ok && done < n_steps) {
     const uint64_t cap = trace ? (uint64_t)kTraceCap : ((uint64_t)1 << 22);
     const uint64_t chunk = std::min<uint64_t>(n_steps - done, cap);
@@ -933,7 +997,6 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     a.net = net;
     a.K = K;
     a.T = ctx->lo.loop_T;
-    a.t0 = before.t + done;
     a.n_steps = chunk;
     a.G = ctx->lo.loop_G;
     a.gpad = (ctx->lo.loop_G + 15) / 16 * 16;
@@ -944,20 +1007,13 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     a.tr_chosen = trace ? ctx->tr_chosen : nullptr;
     a.tr_dl = (trace && trace->dloss) ? ctx->tr_dl : nullptr;
     a.tr_cap = kTraceCap;
-    a.trace_base = a.t0;
     a.spin_limit = 1u << 22;
-    MCA_HIP(ctx, timed(ctx, 4, [&] { return mca::launch_step_loop(a, ctx->stream); }));
-    mca::LoopSync sync{};
-    MCA_HIP(ctx, hipMemcpyAsync(&sync, ctx->loop_sync, sizeof sync, hipMemcpyDeviceToHost, ctx->stream));
-    if (trace != nullptr) {
+    MCA_HIP(ctx, timed(ctx, 4, [&] { return mca::launch_step_loop(a, ctx->loop_coop, ctx->stream); }));
+    if (trace != nullptr) {  // the next chunk reuses the device trace buffers
       MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));
       if (trace->dloss)
         MCA_HIP(ctx, hipMemcpyAsync(trace->dloss + done * K, ctx->tr_dl, chunk * K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
-    }
-    MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
-    if (sync.abort != 0) {
-      ctx->poisoned = true;
-      return fail(ctx, MCA_EDEVICE, "step loop aborted: a bounded wait between workgroups ran out");
+      MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
     }
     done += chunk;
   }
@@ -966,7 +1022,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     int32_t* trc = nullptr;
     double* trd = nullptr;
     if (trace != nullptr) {
-      hipLaunchKernelGGL(k_set_trace_base, dim3(1), dim3(1), 0, ctx->stream, ctx->st, before.t + done);
+      hipLaunchKernelGGL(k_set_trace_base, dim3(1), dim3(1), 0, ctx->stream, ctx->st);
       MCA_HIP(ctx, hipGetLastError());
       trc = ctx->tr_chosen;
       trd = trace->dloss ? ctx->tr_dl : nullptr;
@@ -985,9 +1041,19 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     }
     done += chunk;
   }
-  DevState after{};
-  rc = read_state(ctx, &after);
-  if (rc != MCA_OK) return rc;
+  // state, snapshot and abort word: one copy
+  alignas(8) unsigned char blk[kStateBlock];
+  MCA_HIP(ctx, hipMemcpyAsync(blk, ctx->st, kStateBlock, hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  DevState after, before;
+  mca::LoopSync sync;
+  std::memcpy(&after, blk, sizeof after);
+  std::memcpy(&before, blk + 256, sizeof before);
+  std::memcpy(&sync, blk + 512, sizeof sync);
+  if (sync.abort != 0) {
+    ctx->poisoned = true;
+    return fail(ctx, MCA_EDEVICE, "step loop aborted: a bounded wait between workgroups ran out");
+  }
   if (stats != nullptr) {
     stats->steps = after.steps - before.steps;
     stats->evaluated = after.evaluated - before.evaluated;

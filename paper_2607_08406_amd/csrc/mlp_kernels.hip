@@ -8,9 +8,9 @@
 // da[n] = phi(z'[n]) - phi(z[n]) moves the next layer's local fields by the
 // rank-1 term da[n] * W_{l+1}[:, j].  Samples whose input a_{l-1}[i, n] is zero
 // (about 81 % of an image column) are skipped: nothing changes for them.  The
-// loss change is dL = (1/N) sum_n (l'_n - l_n) over the changed samples only,
-// against the cached per-sample losses, which keeps fp32 cancellation out of
-// dL (a difference of two ~2.3 totals would drown changes of 1e-6).
+// loss change is dL = (1/N) sum_n dl_n over the changed samples only, each
+// dl_n formed from the sample's logit change and the cached softmax of its
+// logits (difference form: no difference of two losses near 2.3).
 #include <type_traits>
 
 #include "device_common.hpp"
@@ -38,7 +38,9 @@ __global__ void k_propose(NetDev net_arg, uint64_t t_host, int use_dev_t, const 
   const uint64_t t = use_dev_t ? st->t : t_host;
   const mca_cand c = decode_candidate(net, t, (uint64_t)k);
   cands[k] = c;
-  aux[k] = prepare_candidate(net, c);
+  Aux a = prepare_candidate(net, c);
+  a.theta = accept_theta(net.rule, net.beta, net.seed, net.tag, t, (uint64_t)k);
+  aux[k] = a;
   cmask[k] = candidate_tiles(c, fmask);
 }
 
@@ -57,52 +59,50 @@ __global__ void k_prepare(NetDev net_arg, const mca_cand* cands, int K, Aux* aux
 // per-sample incremental update for a mutation in one of the last two layers
 // ---------------------------------------------------------------------------
 
-// Loss change of sample n under candidate (l, j, i, de); with STORE the new
-// local fields and loss are written to the caches (the commit), computed by
-// exactly the same expressions as the evaluation.
-template <bool STORE>
-__device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, int i,
-                                               float de, int64_t n) {
+// Commit of candidate (l, j, i, de) on sample n, for a weight in the last
+// two layers: the mutated unit's local field moves by dz = de * ain; the
+// logits move by dz (a logit-layer weight) or by da * W_{L-1}[:, j] with
+// da = phi(z + dz) - phi(z) (the expressions of the evaluation); the
+// sample's softmax and loss are recomputed from its new logits.
+__device__ __forceinline__ void column_commit(const NetDev& net, int l, int j, int i, float de,
+                                              int64_t n) {
   const int L = net.L, C = net.C;
   const int64_t Ns = net.Ns;
   const float ain = (l == 0) ? gload(&net.XT[(int64_t)i * Ns + n])
                              : act_fn(gload(&net.Z[l - 1][(int64_t)i * Ns + n]), net.act, net.gamma);
-  if (ain == 0.f) return 0.f;  // z' == z for this sample
+  if (ain == 0.f) return;  // nothing changes for this sample
   float* zrow = net.Z[l] + (int64_t)j * Ns;
   const float zl = gload(&zrow[n]);
-  const float zn = zl + de * ain;
+  const float dz = de * ain;
   float* ZL = net.Z[L - 1];
-  float z[kCMax];
-  if (l == L - 1) {
-    // the mutated weight feeds logit j directly
+  float zc[kCMax], wc[kCMax];
 #pragma unroll
-    for (int c = 0; c < kCMax; ++c)
-      z[c] = (c < C) ? ((c == j) ? zn : gload(&ZL[(int64_t)c * Ns + n])) : 0.f;
+  for (int c = 0; c < kCMax; ++c) zc[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) : 0.f;
+  float da;
+  if (l == L - 1) {
+    da = dz;  // the mutated weight feeds logit j directly
+#pragma unroll
+    for (int c = 0; c < kCMax; ++c) wc[c] = (c == j) ? 1.f : 0.f;
   } else {
     // last hidden layer: rank-1 update of the logits through W_L[:, j]
-    const float da = act_fn(zn, net.act, net.gamma) - act_fn(zl, net.act, net.gamma);
-    if (da == 0.f) {
-      if (STORE) gstore(&zrow[n], zn);
-      return 0.f;
-    }
+    da = dphi(zl, dz, net.act, net.gamma);
     const float* WL = net.W[L - 1];
     const int nh = net.widths[L - 1];
 #pragma unroll
-    for (int c = 0; c < kCMax; ++c)
-      z[c] = (c < C) ? fmaf(da, gload(&WL[(int64_t)c * nh + j]), gload(&ZL[(int64_t)c * Ns + n])) : 0.f;
+    for (int c = 0; c < kCMax; ++c) wc[c] = (c < C) ? gload(&WL[(int64_t)c * nh + j]) : 0.f;
   }
-  const float ln = ce_loss(z, C, gload(&net.y[n]));
-  const float dl = ln - gload(&net.ell[n]);
-  if (STORE) {
-    gstore(&zrow[n], zn);
-    if (l != L - 1) {
+  gstore(&zrow[n], zl + dz);
+  if (da == 0.f) return;
+  float z[kCMax], p[kCMax];
+  moved_logits(C, da, wc, zc, z);
+  const float ln = softmax_ce(z, C, gload(&net.y[n]), p);
 #pragma unroll
-      for (int c = 0; c < kCMax; ++c)
-        if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+  for (int c = 0; c < kCMax; ++c)
+    if (c < C) {
+      gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+      gstore(&net.prob[(int64_t)c * Ns + n], p[c]);
     }
-    gstore(&net.ell[n], ln);
-  }
-  return dl;
+  gstore(&net.ell[n], ln);
 }
 
 // Batched scoring of the candidates whose weight is in the last two layers
@@ -117,6 +117,8 @@ __device__ __forceinline__ float column_sample(const NetDev& net, int l, int j, 
 //  - lands the input of the mutated weight and, for a hidden unit, its local
 //    field over the tile (lane l holds samples 4l .. 4l+3, one 16-byte load
 //    per row), requested three candidates earlier;
+//  (the block's tile holds each sample's softmax and label: the loss change
+//    of a pair is formed from its logit change, pair_change)
 //  - lists the samples whose input is non-zero (the others cannot change:
 //    about 81 % of an image column is zero) in sample order, in the wave's
 //    own LDS list, with their operands;
@@ -141,9 +143,8 @@ struct EvArgs {
   const float* in_hid;   // input rows of layer L-2: XT (L = 2) or Z[L-3]
   const float* in_log;   // input rows of layer L-1: XT (L = 1) or Z[L-2]
   const float* z_hid;    // local fields of layer L-2 (L = 1: the logits, never used)
-  const float* z_log;    // logits, [C][Ns]
+  const float* p_log;    // softmax of the logits, [C][Ns]
   const float* w_log;    // W[L-1], [C][n_{L-1}]
-  const float* ell;      // [Ns]
   const int32_t* y;      // [Ns]
   const mca_cand* cands;
   const Aux* aux;
@@ -164,9 +165,8 @@ struct EvRows {
 
 template <int CM>
 __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <= 10 ? 5 : 1))) void k_eval_tiles(EvArgs a) {
-  constexpr int kRows = CM + 2;                            // logits, losses, labels
-  __shared__ float zl_lds[CM * kEvT];                      // logits, [class][sample]
-  __shared__ float ell_lds[kEvT];
+  constexpr int kRows = CM + 1;                            // softmax rows, labels
+  __shared__ float pl_lds[CM * kEvT];                      // softmax, [class][sample]
   __shared__ int y_lds[kEvT];
   __shared__ float wcol_lds[kEvWaves][CM];                 // logit-layer column (one-hot for a logit weight)
   __shared__ uint16_t code_lds[kEvWaves][kEvT];            // pair e: its sample in the tile
@@ -197,7 +197,6 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
     const float* const ih = a.in_hid + s0;
     const float* const il = a.in_log + s0;
     const float* const zh = a.z_hid + s0;
-    const float* const zl = a.z_log + s0;
     const float* const wl = a.w_log + (int64_t)(lane < C ? lane : 0) * a.nh;
     __syncthreads();  // the last slot's pairs are done with the tile
 
@@ -221,10 +220,9 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
       if (kFirst) {
 #pragma unroll
         for (int u = 0; u < kRowsPer; ++u) {
-          const int r = wave + kEvWaves * u;  // row r: logit r < C, then losses, labels
-          const float* row = (r < C) ? a.z_log + (int64_t)r * Ns
-                                     : ((r == kRows - 2) ? a.ell : (const float*)a.y);
-          r4[u] = *(const float4*)&(r < kRows ? row : a.ell)[s0];
+          const int r = wave + kEvWaves * u;  // row r: softmax r < C, then labels
+          const float* row = (r < C) ? a.p_log + (int64_t)r * Ns : (const float*)a.y;
+          r4[u] = *(const float4*)&row[s0];
         }
       }
       // scored here: the weight is in the last two layers and within the
@@ -253,8 +251,8 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         for (int u = 0; u < kRowsPer; ++u) {
           const int r = wave + kEvWaves * u;
           if (r < kRows) {
-            float* dst = (r < CM) ? &zl_lds[r * kEvT] : ((r == kRows - 2) ? ell_lds : (float*)y_lds);
-            const bool keep = r >= CM || r < C;  // logit rows past C stay zero
+            float* dst = (r < CM) ? &pl_lds[r * kEvT] : (float*)y_lds;
+            const bool keep = r >= CM || r < C;  // softmax rows past C stay zero
             const float4 v = r4[u];
             float4 w;
             w.x = (keep && sl + 0 < N) ? v.x : 0.f;
@@ -283,7 +281,10 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         oj = in_pass ? oj : 0;
         jj = in_pass ? jj : 0;
         R.a4 = *(const float4*)&(hid ? ih : il)[oi];
-        R.z4 = *(const float4*)&(hid ? zh : zl)[oj];
+        // a logit-layer weight reads the input's row 0 (unused); the select
+        // keeps the row addresses in registers (an unselected load of zh
+        // made the compiler demote them to scratch)
+        R.z4 = *(const float4*)&(hid ? zh : ih)[oj];
         R.wc = wl[jj];
       };
       int q = 0;
@@ -295,7 +296,6 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
       auto unit = [&](EvRows& R) {
         const bool use = (okm >> q) & 1ull;
         const bool hid = (hm >> q) & 1ull, raw = (rawm >> q) & 1ull;
-        const int lq = hid ? L - 2 : L - 1;
         const int jq = __builtin_amdgcn_readlane(j, q);
         const float deq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(de), q));
         float in[4] = {R.a4.x, R.a4.y, R.a4.z, R.a4.w};
@@ -305,6 +305,11 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         }
         const float wv = (hid && lane < C) ? R.wc : ((lane == jq) ? 1.f : 0.f);
         if (lane < CM) wcol[lane] = wv;
+        const float wmax = row16_max(lane < C ? fabsf(wv) : 0.f);
+        float wr[CM];  // the column, wave-uniform (scalar registers)
+#pragma unroll
+        for (int cc = 0; cc < CM; ++cc)
+          wr[cc] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wv), cc));
         const float zv[4] = {R.z4.x, R.z4.y, R.z4.z, R.z4.w};
         bool pr[4];  // sample 4l + t is a pair
         uint64_t bt[4];
@@ -336,9 +341,9 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
           const int ee = e0 + lane;
           const int ec = ee < npairs ? ee : 0;
           const int s = code[ec];
-          float ln;
-          const float dl = pair_eval<CM, kEvT>(L, C, act, gamma, lq, jq, deq, wcol, ainl[ec], zhl[ec],
-                                               &zl_lds[s], ell_lds[s], y_lds[s], ln);
+          float da;
+          const float dl = pair_change<CM, kEvT>(C, act, gamma, !hid, zhl[ec], deq, wr, wcol,
+                                                 wmax, ainl[ec], &pl_lds[s], y_lds[s], da);
           v += (ee < npairs) ? dl : 0.f;
         }
         __builtin_amdgcn_wave_barrier();
@@ -463,7 +468,7 @@ __global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, PartialSrc s
   if (k < K) {
     v = vals[k];
     dL[k] = v;
-    if (do_select && accepts(v, net.ties)) atomicMin(&first, k);
+    if (do_select && accepts(v, net.ties, aux[k].theta)) atomicMin(&first, k);
   }
   if (!do_select) return;
   __syncthreads();
@@ -503,7 +508,7 @@ __global__ __launch_bounds__(kTile) void k_commit_column(NetDev net_arg, const m
   if (c.layer < net.L - 2) return;  // committed by the kernel that scored it
   const Aux a = aux[k];
   const int64_t n = (int64_t)blockIdx.x * kTile + threadIdx.x;
-  if (n < net.N) (void)column_sample<true>(net, c.layer, c.j, c.i, a.de, n);
+  if (n < net.N) column_commit(net, c.layer, c.j, c.i, a.de, n);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     net.W[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = a.w_new;
     if (net.ternary) net.codes[c.layer][(int64_t)c.j * net.widths[c.layer] + c.i] = (int8_t)c.code;
@@ -580,7 +585,8 @@ __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, i
   }
 }
 
-// l_n for every sample from the cached logits; fp64 block sums of l_n.
+// l_n and the softmax of every sample from the cached logits; fp64 block sums
+// of l_n.
 __global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net_arg, double* bsum) {
   __shared__ double red[kTile];
   __shared__ NetDev net;
@@ -591,8 +597,12 @@ __global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net_arg, double* bs
     float z[kCMax];
 #pragma unroll
     for (int c = 0; c < kCMax; ++c) z[c] = (c < net.C) ? gload(&net.Z[net.L - 1][(int64_t)c * net.Ns + n]) : 0.f;
-    const float l = ce_loss(z, net.C, gload(&net.y[n]));
+    float p[kCMax];
+    const float l = softmax_ce(z, net.C, gload(&net.y[n]), p);
     gstore(&net.ell[n], l);
+#pragma unroll
+    for (int c = 0; c < kCMax; ++c)
+      if (c < net.C) gstore(&net.prob[(int64_t)c * net.Ns + n], p[c]);
     v = (double)l;
   }
   red[threadIdx.x] = v;
@@ -658,9 +668,8 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   a.in_hid = (L >= 3) ? net.Z[L - 3] : net.XT;
   a.in_log = (L >= 2) ? net.Z[L - 2] : net.XT;
   a.z_hid = (L >= 2) ? net.Z[L - 2] : net.Z[L - 1];
-  a.z_log = net.Z[L - 1];
+  a.p_log = net.prob;
   a.w_log = net.W[L - 1];
-  a.ell = net.ell;
   a.y = net.y;
   a.cands = cands;
   a.aux = aux;

@@ -4,14 +4,16 @@
 // sample whose input x[n, i] is nonzero; its activation change da[n] moves
 // every unit m of the second hidden layer by da[n] * W_1[m, j] (the O(n_2)
 // multiplications per sample the paper describes), and the logits then change
-// by W_2 (phi(z_2') - phi(z_2)) for that sample.
+// by W_2 (phi(z_2') - phi(z_2)) for that sample.  Every activation change is
+// formed by dphi() and the loss change from the logit change and the cached
+// softmax (ce_change), never as a difference of two losses.
 //
 // Per step, k_columns lists the nonzero entries (m, W_1[m, j]) of each such
 // candidate's column in increasing m (a unit with W_1[m, j] = 0 does not move;
 // about half of a ternary column).  A block of k_slab owns T consecutive
 // samples.  It stages their second-hidden-layer local fields ([n_2][T],
 // unit-major as in HBM, rows padded to T+1 floats), the logit-layer weights
-// transposed ([n_2][C]) and the tile's logits, losses and labels in LDS, lists
+// transposed ([n_2][C]) and the tile's logits, softmax and labels in LDS, lists
 // every affected (candidate, sample) pair, and scores each pair with 32 lanes:
 // lane g adds the list entries g, g+32, ... in order (the next entries are
 // requested while the current ones are used), then the 32 lane sums meet in a
@@ -101,9 +103,9 @@ __device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, co
         for (int p = 0; p < kPairChunk; ++p) {
           if (p < np) {
             const float zo = zt[m * TS + tp[p]];
-            const float zn = zo + dp[p] * w;
-            const float d = act_fn(zn, act, gamma) - act_fn(zo, act, gamma);
-            if (STORE) zt[m * TS + tp[p]] = zn;
+            const float dz = dp[p] * w;
+            const float d = dphi(zo, dz, act, gamma);
+            if (STORE) zt[m * TS + tp[p]] = zo + dz;
 #pragma unroll
             for (int c = 0; c < CM; ++c) acc[p][c] = fmaf(d, wr[c], acc[p][c]);
           }
@@ -193,7 +195,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   __shared__ float dlp[kGroupK * T];
   __shared__ int gk[kGroupK], gj[kGroupK], gi[kGroupK], gnnz[kGroupK];
   __shared__ float zlt[CM * kSlabTileMax];  // the tile's logits [class][sample]
-  __shared__ float ellt[kSlabTileMax];
+  __shared__ float plt[CM * kSlabTileMax];  // their softmax
   __shared__ int yt[kSlabTileMax];
   __shared__ float gde[kGroupK];
   __shared__ int ngroup, nitems;
@@ -259,16 +261,19 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       }
     }
   };
-  // The tile's logits, losses and labels (the cross-entropy of a pair reads
-  // them), one value per thread.
-  if (tid < (CM + 2) * T) {
+  // The tile's logits, softmax and labels (the loss change of a pair reads
+  // the softmax and labels, a commit the logits), one value per thread.
+  static_assert((2 * kCMax + 1) * kSlabTileMax <= kSlabThreads, "one value per thread");
+  if (tid < (2 * CM + 1) * T) {
     const int r = tid / T, t = tid - r * T;
-    const bool ok = n0 + t < N && (r >= CM || r < C);
+    const int rc = (r < CM) ? r : r - CM;  // class of a logit or softmax row
+    const bool ok = n0 + t < N && (r >= 2 * CM || rc < C);
     const int64_t n = ok ? n0 + t : 0;
-    const float v = (r < CM) ? gload(&ZL[(int64_t)(r < C ? r : 0) * Ns + n])
-                             : (r == CM ? gload(&net.ell[n]) : __int_as_float(gload(&net.y[n])));
+    const int64_t ro = (int64_t)(rc < C ? rc : 0) * Ns + n;
+    const float v = (r < CM) ? gload(&ZL[ro])
+                             : (r < 2 * CM ? gload(&net.prob[ro]) : __int_as_float(gload(&net.y[n])));
     if (r < CM) zlt[r * T + t] = ok ? v : 0.f;
-    else if (r == CM) ellt[t] = ok ? v : 0.f;
+    else if (r < 2 * CM) plt[rc * T + t] = ok ? v : 0.f;
     else yt[t] = ok ? __float_as_int(v) : 0;
   }
   // The first group's candidate fields (wave 0, lane = slot) are requested
@@ -326,9 +331,9 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
         const float x = (l == 0) ? xr : act_fn(xr, act, gamma);
         if (x != 0.f) {
           const float zl = gload(&Z1[(int64_t)gj[s] * Ns + n]);
-          const float zn = zl + gde[s] * x;
-          da = act_fn(zn, act, gamma) - act_fn(zl, act, gamma);
-          if (commit) gstore(&Z1[(int64_t)gj[s] * Ns + n], zn);
+          const float dz = gde[s] * x;
+          da = dphi(zl, dz, act, gamma);
+          if (commit) gstore(&Z1[(int64_t)gj[s] * Ns + n], zl + dz);
         }
       }
       pdt[s * T + t] = da;
@@ -398,15 +403,28 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
           if (p < np) {
             const int t = tp[p];
             const int64_t n = n0 + t;
-            float z[CM];
+            float pr[CM], dz[CM];
 #pragma unroll
-            for (int c = 0; c < CM; ++c) z[c] = (c < C) ? zlt[c * T + t] + acc[p][c] : 0.f;
-            const float ln = ce_loss<CM>(z, C, yt[t]);
-            dlp[s * T + t] = ln - ellt[t];
+            for (int c = 0; c < CM; ++c) {
+              pr[c] = plt[c * T + t];
+              dz[c] = (c < C) ? acc[p][c] : 0.f;
+            }
+            const int y = yt[t];
+            float dzy = 0.f;
+#pragma unroll
+            for (int c = 0; c < CM; ++c) dzy = (c == y) ? dz[c] : dzy;
+            dlp[s * T + t] = ce_change<CM>(pr, dz, C, dzy);
             if (commit) {
+              float z[CM], pn[CM];
+#pragma unroll
+              for (int c = 0; c < CM; ++c) z[c] = (c < C) ? zlt[c * T + t] + dz[c] : 0.f;
+              const float ln = softmax_ce<CM>(z, C, y, pn);
 #pragma unroll
               for (int c = 0; c < CM; ++c)
-                if (c < C) gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+                if (c < C) {
+                  gstore(&ZL[(int64_t)c * Ns + n], z[c]);
+                  gstore(&net.prob[(int64_t)c * Ns + n], pn[c]);
+                }
               gstore(&net.ell[n], ln);
               atomicOr(&touched, 1u << t);
             }

@@ -97,13 +97,14 @@ __global__ void k_tf_propose(const TfDev* tf, uint64_t t_host, int use_dev_t,
   const float r = m * 0x1p-23f - 1.0f;
   c.d = tf->delta * r;
   c.code = 0;
-  c.reserved = 0;
+  c.flags = 0;
   cands[k] = c;
   Aux a;
   a.w_old = tf->param[layer][off];
   a.w_new = a.w_old + c.d;
   a.de = a.w_new - a.w_old;
   a.valid = !(tf->bound > 0.f && fabsf(a.w_new) >= tf->bound);
+  a.theta = accept_theta(tf->rule, tf->beta, tf->seed, tf->tag, t, (uint64_t)k);
   aux[k] = a;
 }
 
@@ -116,6 +117,7 @@ __global__ void k_tf_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
   a.w_new = a.w_old + c.d;
   a.de = a.w_new - a.w_old;
   a.valid = !(tf->bound > 0.f && fabsf(a.w_new) >= tf->bound);
+  a.theta = 0.0;
   aux[k] = a;
 }
 

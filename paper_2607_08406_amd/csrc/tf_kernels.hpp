@@ -34,6 +34,9 @@ struct TfDev {
   float eps, delta, bound;
   int32_t ties;
   uint64_t seed, tag;
+  double beta;                    // Metropolis selection intensity
+  int32_t rule;                   // MCA_RULE_*
+  int32_t pad0;
   int64_t offs[kTfMaxTensors + 1];   // flat offset of each tensor, offs[n_tensors] = P
   int32_t rows[kTfMaxTensors], cols[kTfMaxTensors];  // 1-D tensors: cols = 1
   float* param[kTfMaxTensors];       // committed tensors

@@ -27,7 +27,8 @@ MCA_NET_MLP, MCA_NET_TRANSFORMER = 0, 1
 MCA_ACT_TANH, MCA_ACT_GAUSS = 0, 1
 MCA_WEIGHTS_FP32, MCA_WEIGHTS_TERNARY = 0, 1
 MCA_PICK_WEIGHT, MCA_PICK_LAYER = 0, 1
-MCA_OPT_PERSISTENT_LOOP, MCA_OPT_LOOP_TILE = 1, 2
+MCA_RULE_GREEDY, MCA_RULE_METROPOLIS = 0, 1
+MCA_OPT_PERSISTENT_LOOP, MCA_OPT_LOOP_TILE, MCA_OPT_LOOP_LAUNCH = 1, 2, 3
 
 STATUS_NAMES = {0: "MCA_OK", -1: "MCA_EINVAL", -2: "MCA_ESTATE", -3: "MCA_ENOSPACE",
                 -4: "MCA_EDEVICE", -5: "MCA_EPOISONED", -6: "MCA_EUNSUPPORTED"}
@@ -48,17 +49,21 @@ class mca_net_desc(ctypes.Structure):
                 ("accept_ties", ctypes.c_int32), ("seed", ctypes.c_uint64),
                 ("stream_tag", ctypes.c_uint64), ("vocab", ctypes.c_int32),
                 ("ctx", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_block", ctypes.c_int32),
-                ("n_head", ctypes.c_int32), ("d_mlp", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+                ("n_head", ctypes.c_int32), ("d_mlp", ctypes.c_int32), ("ln_eps", ctypes.c_float),
+                ("accept_rule", ctypes.c_int32), ("n_prune", ctypes.c_int32),
+                ("beta", ctypes.c_double), ("subset_size", ctypes.c_int64),
+                ("subset_period", ctypes.c_int64)]
 
 
 class mca_cand(ctypes.Structure):
     _fields_ = [("flat", ctypes.c_int64), ("layer", ctypes.c_int32), ("j", ctypes.c_int32),
                 ("i", ctypes.c_int32), ("d", ctypes.c_float), ("code", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("flags", ctypes.c_int32)]
 
 
 CAND_DTYPE = np.dtype([("flat", "<i8"), ("layer", "<i4"), ("j", "<i4"), ("i", "<i4"),
-                       ("d", "<f4"), ("code", "<i4"), ("reserved", "<i4")])
+                       ("d", "<f4"), ("code", "<i4"), ("flags", "<i4")])
+MCA_CAND_PRUNE = 1
 
 
 class mca_data(ctypes.Structure):
@@ -150,10 +155,20 @@ def _ptr_array(arrays, ctype):
 # descriptions
 # ---------------------------------------------------------------------------
 
+def _selection(d: mca_net_desc, beta: float, n_prune: int, subset_size: int,
+               subset_period: int):
+    d.accept_rule = MCA_RULE_METROPOLIS if beta else MCA_RULE_GREEDY
+    d.beta = float(beta)
+    d.n_prune = int(n_prune)
+    d.subset_size = int(subset_size)
+    d.subset_period = int(subset_period)
+
+
 def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta: float = 0.0,
              ternary_scales: Optional[Sequence[float]] = None, pick: str = "weight",
              bound: float = 0.0, accept_ties: bool = False, seed: int = 0,
-             stream_tag: int = 0) -> mca_net_desc:
+             stream_tag: int = 0, beta: float = 0.0, n_prune: int = 0, subset_size: int = 0,
+             subset_period: int = 1) -> mca_net_desc:
     d = mca_net_desc()
     d.kind = MCA_NET_MLP
     d.n_layers = len(widths) - 1
@@ -171,13 +186,14 @@ def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta
     d.accept_ties = int(accept_ties)
     d.seed = seed
     d.stream_tag = stream_tag
+    _selection(d, beta, n_prune, subset_size, subset_period)
     return d
 
 
 def transformer_desc(vocab: int, ctx: int, d_model: int, n_block: int, n_head: int,
                      d_mlp: int, delta: float = 0.0, ln_eps: float = 1e-5, bound: float = 0.0,
                      accept_ties: bool = False, seed: int = 0,
-                     stream_tag: int = 0) -> mca_net_desc:
+                     stream_tag: int = 0, beta: float = 0.0) -> mca_net_desc:
     d = mca_net_desc()
     d.kind = MCA_NET_TRANSFORMER
     d.vocab, d.ctx, d.d_model = int(vocab), int(ctx), int(d_model)
@@ -190,6 +206,7 @@ def transformer_desc(vocab: int, ctx: int, d_model: int, n_block: int, n_head: i
     d.accept_ties = int(accept_ties)
     d.seed = seed
     d.stream_tag = stream_tag
+    _selection(d, beta, 0, 0, 1)
     return d
 
 

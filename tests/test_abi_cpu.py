@@ -45,7 +45,7 @@ def test_struct_mirrors(binding):
         assert lib.mca_struct_size(n) == ctypes.sizeof(st)
     assert ctypes.sizeof(binding.mca_cand) == 32 == binding.CAND_DTYPE.itemsize
     assert lib.mca_struct_size(99) == 0
-    assert binding.mca_abi_version() == 1
+    assert binding.mca_abi_version() == 2
 
 
 def test_plan_sizes(binding):

@@ -13,8 +13,8 @@ import torch
 
 from oracle import mca as omca
 from oracle.mlp import FullMLP, IncrementalMLP, MLPState
-from parity_util import (REL_TOL, TIE, assert_cands_equal, assert_state_equal, check_losses,
-                         explicit_steps, make_pair, replay_trace)
+from parity_util import (REL_TOL, TIE, ParityStats, assert_cands_equal, assert_state_equal,
+                         check_batch, explicit_steps, make_pair, mlp_kappa, replay_trace)
 from workloads import CONFIGS, mlp_workload
 
 pytestmark = pytest.mark.gpu
@@ -45,7 +45,7 @@ def test_tiny_init_and_explicit_steps(mca):
     assert t == 0 and abs(L - ref.loss()) <= REL_TOL * ref.loss()
     full = FullMLP(MLPState(w["weights"]), w["X"], w["y"], cfg.act)
     assert abs(L - full.loss()) <= REL_TOL * full.loss()
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 300, 4)
+    st, acc = explicit_steps(ctx, ref, cfg, 0, 300, 4, ParityStats("tiny explicit K=4"))
     assert acc > 50
     assert_state_equal(ctx, ref)
     ctx.close()
@@ -63,9 +63,10 @@ def test_tiny_device_loop_full_window(mca, persistent):
     ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, persistent)
     st, chosen, dloss = ctx.run_steps(cfg.steps, 1, trace=True, trace_dloss=True)
     assert st.steps == cfg.steps and st.evaluated == cfg.steps and st.next_step == cfg.steps
-    ties, acc = replay_trace(ref, cfg, 0, chosen, dloss, 1)
+    ps, acc = replay_trace(ref, cfg, 0, chosen, dloss, 1,
+                           ParityStats(f"tiny 20000 device steps persistent={persistent}"))
     assert acc == st.accepted
-    assert ties <= 20
+    assert ps.flips <= 20
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
@@ -83,14 +84,15 @@ def test_small_wide_explicit_and_loop(mca, persistent, tile):
     ctx, ref = make_pair(cfg, w, k_max=64)
     ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, persistent)
     ctx.set_option(mca.MCA_OPT_LOOP_TILE, tile)
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 40, 64)
+    ps = ParityStats(f"wide 784-512-10 persistent={persistent} tile={tile}")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 40, 64, ps)
     assert acc > 10
     assert_state_equal(ctx, ref)
     assert ctx.loss()[1] == 0  # the explicit path leaves the step counter alone
     ctx.set_step(40)
     st, chosen, dloss = ctx.run_steps(60, 64, trace=True, trace_dloss=True)
     assert st.next_step == 100
-    replay_trace(ref, cfg, 40, chosen, dloss, 64)
+    replay_trace(ref, cfg, 40, chosen, dloss, 64, ps)
     assert_state_equal(ctx, ref)
     ctx.close()
 
@@ -105,18 +107,20 @@ def test_full_wide_workload(mca):
     ctx, ref = make_pair(cfg, w, k_max=64)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ps = ParityStats("wide 784-16384-10 full")
     cands = ctx.propose(0, 64)
-    L_t, rc, rl, chosen = omca.evaluate(ref, 0, 64, cfg.seed_stream, cfg.stream_tag, cfg.delta)
-    assert_cands_equal(cands, rc)
     losses, dl = ctx.eval_losses(cands)
-    check_losses(losses, L_t, rl)
+    L_t, rc, dls, chosen = check_batch(ps, dl, ref, cfg, 0, 64)
+    assert_cands_equal(cands, rc)
     full = FullMLP(MLPState(w["weights"]), w["X"], w["y"], cfg.act)
     for k in (0, 1):
         assert abs(losses[k] - full.eval(rc[k])) <= REL_TOL * losses[k]
+        d, _ = full.delta(rc[k])
+        assert abs(dl[k] - d) <= 1e-5 * abs(d) + 2e-15 * 64, (k, dl[k], d)
     ctx.rollback()
     st, ch, dloss = ctx.run_steps(20, 64, trace=True, trace_dloss=True)
     assert st.steps == 20
-    replay_trace(ref, cfg, 0, ch, dloss, 64)
+    replay_trace(ref, cfg, 0, ch, dloss, 64, ps)
     assert_state_equal(ctx, ref)
     ctx.close()
 
@@ -133,14 +137,13 @@ def test_wide_batched_evaluation(mca):
     K = 1000
     ctx, ref = make_pair(cfg, w, k_max=K)
     cands = ctx.propose(7, K)
-    L_t, rc, rl, chosen = omca.evaluate(ref, 7, K, cfg.seed_stream, cfg.stream_tag, cfg.delta)
-    assert_cands_equal(cands, rc)
     assert sum(int(c["layer"]) == 1 for c in cands) > 0  # logit-layer weights too
     losses, dl = ctx.eval_losses(cands)
-    check_losses(losses, L_t, rl)
+    L_t, rc, dls, chosen = check_batch(ParityStats("wide batched K=1000"), dl, ref, cfg, 7, K)
+    assert_cands_equal(cands, rc)
     assert chosen >= 0
     ctx.commit(chosen)
-    ref.commit(rc[chosen], rl[chosen])
+    ref.commit(rc[chosen], L_t + dls[chosen])
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
@@ -167,12 +170,12 @@ def test_batched_evaluation_tile_masks(mca, N):
     assert (nz.any(axis=1) & ~nz.all(axis=1)).sum() > 100
     K = 256
     ctx, ref = make_pair(cfg, w, k_max=K)
+    ps = ParityStats(f"wide 784-64-10 N={N} tile masks")
     for step in (0, 5):
         cands = ctx.propose(step, K)
-        L_t, rc, rl, chosen = omca.evaluate(ref, step, K, cfg.seed_stream, cfg.stream_tag, cfg.delta)
-        assert_cands_equal(cands, rc)
         losses, dl = ctx.eval_losses(cands)
-        check_losses(losses, L_t, rl)
+        L_t, rc, dls, chosen = check_batch(ps, dl, ref, cfg, step, K)
+        assert_cands_equal(cands, rc)
         ctx.rollback()
     ctx.close()
 
@@ -190,12 +193,16 @@ def test_batched_evaluation_many_tiles(mca):
     K, t = 264, 3
     ctx, ref = make_pair(cfg, w, k_max=K)
     cands = ctx.propose(t, K)
-    losses, _ = ctx.eval_losses(cands)
-    L_t = ref.loss()
+    losses, dl = ctx.eval_losses(cands)
     sample = sorted(set(range(8)) | set(range(248, K)) | set(range(0, K, 17)))
     rc = [ref.candidate(cfg.seed_stream, cfg.stream_tag, t, k, cfg.delta) for k in sample]
     assert_cands_equal([cands[k] for k in sample], rc)
-    check_losses([losses[k] for k in sample], L_t, [ref.eval(c) for c in rc])
+    ps = ParityStats("16-8-10 N=400000 sampled")
+    for k, c in zip(sample, rc):
+        d, mag = ref.delta(c)
+        tol = REL_TOL * abs(d) + mlp_kappa(cfg.widths, c.layer) * 2.0 ** -24 * mag
+        assert abs(dl[k] - d) <= tol, (k, dl[k], d)
+        ps.n += 1
     ctx.rollback()
     ctx.close()
 
@@ -207,12 +214,13 @@ def test_single_layer_net(mca):
     banner("784-10 N=700 explicit steps K=100 and device loop K=64")
     w = mlp_workload(cfg)
     ctx, ref = make_pair(cfg, w, k_max=100)
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 10, 100)
+    ps = ParityStats("784-10 single layer")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 10, 100, ps)
     assert acc > 3
     assert_state_equal(ctx, ref)
     ctx.set_step(10)
     st, ch, dl = ctx.run_steps(20, 64, trace=True, trace_dloss=True)
-    replay_trace(ref, cfg, 10, ch, dl, 64)
+    replay_trace(ref, cfg, 10, ch, dl, 64, ps)
     assert_state_equal(ctx, ref)
     ctx.close()
 
@@ -228,13 +236,14 @@ def test_other_class_counts(mca, C):
     ctx, ref = make_pair(cfg, w, k_max=64)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 20, 64)
+    ps = ParityStats(f"784-256-{C}")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 20, 64, ps)
     assert acc > 5
     assert_state_equal(ctx, ref)
     ctx.set_step(20)
     st, ch, dl = ctx.run_steps(40, 64, trace=True, trace_dloss=True)
     assert st.steps == 40
-    replay_trace(ref, cfg, 20, ch, dl, 64)
+    replay_trace(ref, cfg, 20, ch, dl, 64, ps)
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
@@ -345,7 +354,7 @@ def test_degenerate_sample_counts(mca, N):
     ctx, ref = make_pair(cfg, w, k_max=8)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
-    explicit_steps(ctx, ref, cfg, 0, 20, 8)
+    explicit_steps(ctx, ref, cfg, 0, 20, 8, ParityStats(f"tiny N={N}"))
     assert_state_equal(ctx, ref)
     ctx.close()
 
@@ -356,11 +365,12 @@ def test_gauss_and_ternary_two_layer(mca):
     cfg = base.scaled(name="ternary2", widths=(784, 256, 10), n_samples=777, K=32)
     w = mlp_workload(cfg)
     ctx, ref = make_pair(cfg, w, k_max=32)
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 30, 32)
+    ps = ParityStats("ternary 784-256-10 gauss")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 30, 32, ps)
     assert acc > 5
     assert_state_equal(ctx, ref)
     ctx.set_step(30)
     st, ch, dl = ctx.run_steps(30, 32, trace=True, trace_dloss=True)
-    replay_trace(ref, cfg, 30, ch, dl, 32)
+    replay_trace(ref, cfg, 30, ch, dl, 32, ps)
     assert_state_equal(ctx, ref)
     ctx.close()

@@ -13,8 +13,8 @@ import torch
 
 from oracle import mca as omca
 from oracle.mlp import FullMLP, MLPState, per_sample_ce
-from parity_util import (REL_TOL, assert_cands_equal, assert_state_equal, check_losses,
-                         explicit_steps, make_pair, replay_trace)
+from parity_util import (REL_TOL, ParityStats, assert_cands_equal, assert_state_equal,
+                         check_batch, explicit_steps, make_pair, replay_trace)
 from workloads import CONFIGS, mlp_workload
 
 pytestmark = pytest.mark.gpu
@@ -60,14 +60,15 @@ def test_ternary_three_layer_small(mca):
     ctx, ref = make_pair(cfg, w, k_max=16)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
-    ties, acc = explicit_steps(ctx, ref, cfg, 0, 40, 16)
+    ps = ParityStats("ternary 784-96-80-10")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 40, 16, ps)
     assert acc > 5
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.set_step(40)
     st, ch, dl = ctx.run_steps(60, 16, trace=True, trace_dloss=True)
     assert st.steps == 60
-    replay_trace(ref, cfg, 40, ch, dl, 16)
+    replay_trace(ref, cfg, 40, ch, dl, 16, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     # first-layer candidates were drawn and some were committed
@@ -88,12 +89,13 @@ def test_three_layer_other_class_count(mca):
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
     counts = layer_counts(ref, cfg, 0, 30, 16)
     assert counts[0] > 20  # the first layer is exercised
-    explicit_steps(ctx, ref, cfg, 0, 30, 16)
+    ps = ParityStats("ternary 784-64-48-13")
+    explicit_steps(ctx, ref, cfg, 0, 30, 16, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.set_step(30)
     st, ch, dl = ctx.run_steps(30, 16, trace=True, trace_dloss=True)
-    replay_trace(ref, cfg, 30, ch, dl, 16)
+    replay_trace(ref, cfg, 30, ch, dl, 16, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.close()
@@ -107,12 +109,13 @@ def test_tanh_three_layer_continuous(mca):
     ctx, ref = make_pair(cfg, w, k_max=8)
     counts = layer_counts(ref, cfg, 0, 50, 8)
     assert counts[0] > 20  # the first layer is exercised
-    explicit_steps(ctx, ref, cfg, 0, 50, 8)
+    ps = ParityStats("tanh 64-48-40-10")
+    explicit_steps(ctx, ref, cfg, 0, 50, 8, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.set_step(50)
     st, ch, dl = ctx.run_steps(150, 8, trace=True, trace_dloss=True)
-    replay_trace(ref, cfg, 50, ch, dl, 8)
+    replay_trace(ref, cfg, 50, ch, dl, 8, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.close()
@@ -123,7 +126,7 @@ def test_three_layer_tile_edges(mca, N):
     cfg = CONFIGS["ternary"].scaled(name=f"t3_n{N}", widths=(784, 40, 36, 10), n_samples=N, K=8)
     w = mlp_workload(cfg)
     ctx, ref = make_pair(cfg, w, k_max=8)
-    explicit_steps(ctx, ref, cfg, 0, 25, 8)
+    explicit_steps(ctx, ref, cfg, 0, 25, 8, ParityStats(f"ternary 784-40-36-10 N={N}"))
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.close()
@@ -158,21 +161,23 @@ def test_full_ternary_workload(mca):
     ctx, ref = make_pair(cfg, w, k_max=64)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
+    ps = ParityStats("ternary 784-1024-1024-10 full")
     cands = ctx.propose(0, 64)
-    L_t, rc, rl, chosen = omca.evaluate(ref, 0, 64, cfg.seed_stream, cfg.stream_tag, cfg.delta)
+    losses, dl = ctx.eval_losses(cands)
+    L_t, rc, dls, chosen = check_batch(ps, dl, ref, cfg, 0, 64)
     assert_cands_equal(cands, rc)
-    losses, _ = ctx.eval_losses(cands)
-    check_losses(losses, L_t, rl)
     full = FullMLP(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"], cfg.act,
                    cfg.gamma)
     firsts = [k for k, c in enumerate(rc) if c.layer == 0][:2]
     assert firsts
     for k in firsts:
         assert abs(losses[k] - full.eval(rc[k])) <= REL_TOL * losses[k]
+        d, _ = full.delta(rc[k])
+        assert abs(dl[k] - d) <= 1e-5 * abs(d) + 1e-13, (k, dl[k], d)
     ctx.rollback()
-    st, ch, dl = ctx.run_steps(4, 64, trace=True, trace_dloss=True)
-    assert st.steps == 4
-    replay_trace(ref, cfg, 0, ch, dl, 64)
+    st, ch, dl = ctx.run_steps(50, 64, trace=True, trace_dloss=True)
+    assert st.steps == 50
+    replay_trace(ref, cfg, 0, ch, dl, 64, ps)
     assert_state_equal(ctx, ref)
     assert_caches_match(ctx, ref)
     ctx.close()

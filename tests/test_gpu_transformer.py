@@ -15,7 +15,13 @@ import torch
 
 from oracle import mca as omca
 from oracle.transformer import TransformerModel
-from parity_util import REL_TOL, TIE, assert_cands_equal, check_losses
+from parity_util import REL_TOL, TIE, ParityStats, assert_cands_equal, check_step
+
+# The device recomputes the reached positions' losses in fp32 and subtracts
+# the cached ones; each position's rounding is a few ulp of l_n + max|z| and
+# independent of the others, so the floor is 8 ulp of their root-sum-square
+# (the oracle's R).
+KAPPA_TF = 8.0
 from workloads import CONFIGS, transformer_workload
 
 pytestmark = pytest.mark.gpu
@@ -51,38 +57,37 @@ def assert_params_equal(ctx, ref):
         assert a.tobytes() == b.tobytes(), f"tensor {t} differs"
 
 
-def explicit_steps(ctx, ref, cfg, t0, n, K):
+def explicit_steps(ctx, ref, cfg, t0, n, K, stats):
     accepted = 0
     for t in range(t0, t0 + n):
         cands = ctx.propose(t, K)
-        L_t, rc, rl, chosen = omca.evaluate(ref, t, K, cfg.seed_stream, cfg.stream_tag,
-                                            cfg.delta, "weight", cfg.accept_ties)
+        L_t, rc, dls, mags, th, chosen = omca.evaluate_all(ref, t, K, cfg.seed_stream,
+                                                           cfg.stream_tag, cfg.delta, "weight",
+                                                           cfg.accept_ties)
         assert_cands_equal(cands, rc)
-        losses, _ = ctx.eval_losses(cands)
-        check_losses(losses, L_t, rl, cfg.accept_ties)
-        if chosen >= 0:
-            ctx.commit(chosen)
-            ref.commit(rc[chosen], rl[chosen])
+        _, gdl = ctx.eval_losses(cands)
+        gch = next((k for k in range(K) if omca.accepts(float(gdl[k]), cfg.accept_ties)), -1)
+        take = check_step(stats, gdl, dls, mags, [KAPPA_TF] * K, th, cfg.accept_ties, gch,
+                          chosen, tag=f"step {t}")
+        if take >= 0:
+            ctx.commit(take)
+            ref.commit(rc[take], L_t + dls[take])
             accepted += 1
         else:
             ctx.rollback()
     return accepted
 
 
-def replay(ref, cfg, t0, chosen, dloss, K):
+def replay(ref, cfg, t0, chosen, dloss, K, stats):
     for n in range(len(chosen)):
         t = t0 + n
-        L_t, rc, rl, orc = omca.evaluate(ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-                                         "weight", cfg.accept_ties)
-        for k in range(K):
-            g = L_t + dloss[n, k]
-            assert abs(g - rl[k]) <= REL_TOL * abs(rl[k]), (t, k, g, rl[k])
-        g = int(chosen[n])
-        if g != orc:
-            m = min(x if x >= 0 else K for x in (g, orc))
-            assert abs(rl[m] - L_t) < TIE, (t, m, g, orc, rl[m] - L_t)
-        if g >= 0:
-            ref.commit(rc[g], rl[g])
+        L_t, rc, dls, mags, th, orc = omca.evaluate_all(ref, t, K, cfg.seed_stream,
+                                                        cfg.stream_tag, cfg.delta, "weight",
+                                                        cfg.accept_ties)
+        take = check_step(stats, dloss[n], dls, mags, [KAPPA_TF] * K, th, cfg.accept_ties,
+                          int(chosen[n]), orc, tag=f"step {t}")
+        if take >= 0:
+            ref.commit(rc[take], L_t + dls[take])
 
 
 def small_cfg(**kw):
@@ -98,13 +103,14 @@ def test_transformer_small_explicit_and_device(mca):
     ctx, ref, _ = make_pair(mca, cfg, k_max=8)
     L, t = ctx.loss()
     assert t == 0 and abs(L - ref.loss()) <= REL_TOL * ref.loss(), (L, ref.loss())
-    acc = explicit_steps(ctx, ref, cfg, 0, 25, 8)
+    ps = ParityStats("transformer ctx 32 d 64")
+    acc = explicit_steps(ctx, ref, cfg, 0, 25, 8, ps)
     assert acc > 3
     assert_params_equal(ctx, ref)
     ctx.set_step(25)
     st, ch, dl = ctx.run_steps(25, 8, trace=True, trace_dloss=True)
     assert st.steps == 25 and st.evaluated == 25 * 8
-    replay(ref, cfg, 25, ch, dl, 8)
+    replay(ref, cfg, 25, ch, dl, 8, ps)
     assert_params_equal(ctx, ref)
     L, _ = ctx.loss()
     assert abs(L - ref.loss_of(ref.params)) <= REL_TOL * L
@@ -162,10 +168,11 @@ def test_full_transformer_workload(mca):
     ctx, ref, _ = make_pair(mca, cfg, k_max=16)
     L, _ = ctx.loss()
     assert abs(L - ref.loss()) <= REL_TOL * ref.loss()
-    explicit_steps(ctx, ref, cfg, 0, 1, 16)
+    ps = ParityStats("transformer full")
+    explicit_steps(ctx, ref, cfg, 0, 2, 16, ps)
     assert_params_equal(ctx, ref)
-    ctx.set_step(1)
-    st, ch, dl = ctx.run_steps(1, 16, trace=True, trace_dloss=True)
-    replay(ref, cfg, 1, ch, dl, 16)
+    ctx.set_step(2)
+    st, ch, dl = ctx.run_steps(4, 16, trace=True, trace_dloss=True)
+    replay(ref, cfg, 2, ch, dl, 16, ps)
     assert_params_equal(ctx, ref)
     ctx.close()

@@ -97,7 +97,8 @@ def test_delta_equals_definition_where_large(act, widths):
                 b, mb = inc.delta(c)
                 # the fp64 definition rounds L' and L (~2) to 2^-53 each
                 assert abs(a - b) <= 1e-9 * abs(a) + 2e-15, (c, a, b)
-                assert abs(ma - mb) <= 1e-9 * ma + 1e-15
+                # the sizes: of the logit change (full), of its terms (incremental)
+                assert mb >= ma * (1 - 1e-9)
                 n += abs(a) > 1e-6
     assert n > 10
 

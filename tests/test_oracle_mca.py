@@ -257,3 +257,43 @@ def test_metropolis_run_climbs_uphill_sometimes():
             u = accept_uniform(11, 12, r.t, k)
             assert not (u < math.exp(-beta * r.dls[k]))
     assert up > 0
+
+
+def test_pruning_moves_zero_the_weight_and_match_definition():
+    """Sec. 2.2: a pruning move sets its weight to zero (d = -w); its loss
+    change equals the definition; a pure-pruning run only ever zeroes
+    weights, never lowers the loss count of zeros, and strictly lowers L on
+    every accepted step."""
+    X, y, Ws = random_net((9, 7, 5), 120, 41, scale=1.2)
+    inc = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    full = FullMLP(MLPState(Ws), X, y, "tanh")
+    for t in range(30):
+        c = inc.candidate(2, 3, t, 0, 0.1, prune=True)
+        assert c.prune and c.d == -Ws[c.layer][c.j, c.i] and inc.state.new_value(c) == 0.0
+        a, _ = full.delta(c)
+        b, _ = inc.delta(c)
+        assert abs(a - b) <= 1e-9 * abs(a) + 2e-15
+    ratio0 = mca.remaining_weight_ratio(inc)
+    recs = mca.run(inc, 0, 300, 4, 2, 3, 0.1, scan_all=True, n_prune=4)
+    acc = [r for r in recs if r.chosen >= 0]
+    assert acc and all(r.L_after < r.L_before for r in acc)
+    assert all(r.cands[r.chosen].prune for r in acc)
+    total = sum(w.size for w in Ws)
+    assert round(mca.remaining_weight_ratio(inc) * total) == round(ratio0 * total) - len(acc)
+    fresh = FullMLP(MLPState(inc.state.weights), X, y, "tanh")
+    assert abs(fresh.loss() - inc.loss()) <= 1e-12
+
+
+def test_mixed_pruning_puts_pruning_first():
+    """n_prune < K: candidates 0 .. n_prune-1 prune, the rest mutate; the
+    first passing candidate in that order wins (pruning preferred)."""
+    X, y, Ws = random_net((9, 7, 5), 120, 43, scale=1.2)
+    inc = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    recs = mca.run(inc, 0, 200, 6, 4, 5, 0.2, scan_all=True, n_prune=2)
+    kinds = set()
+    for r in recs:
+        assert [c.prune for c in r.cands] == [True, True, False, False, False, False]
+        if r.chosen >= 0:
+            kinds.add(r.cands[r.chosen].prune)
+            assert all(d >= 0 for d in r.dls[:r.chosen])
+    assert kinds == {True, False}
