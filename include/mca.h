@@ -220,6 +220,23 @@ int mca_commit(mca_ctx* ctx, int32_t k);
  * byte-identical to before the evaluation.  MCA_ESTATE without a pending batch. */
 int mca_rollback(mca_ctx* ctx);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid it): mca_eval_losses
+ * without any use of the context's per-call buffers.  The per-call device
+ * buffers (the candidates' device copy, prepared values, tile sums, the
+ * three-layer and deep nets' affected-sample lists, loss changes) live in one
+ * static array per GPU of 8 MiB, held until the process ends; a request that
+ * needs more (K x (N or tiles) too large) fails with MCA_EINVAL before
+ * anything is enqueued.  The call allocates nothing, scores K candidates
+ * (1 <= K <= 1024, K not bounded by k_max) against the committed state
+ * exactly as mca_eval_losses does (same kernels, same results), leaves no
+ * pending batch and touches no pending batch's buffers, and synchronises.
+ * MLP contexts only (MCA_EUNSUPPORTED otherwise).  Every call on a GPU shares
+ * that GPU's array: calls that overlap on one GPU (several streams or
+ * threads) race on it. */
+int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
+                            double* loss_out, double* dloss_out);
+
 /* Tuning options of mca_run_steps (mca_set_option):
  *   MCA_OPT_PERSISTENT_LOOP  1 (default): run eligible nets (mutations reach
  *                            at most the last two layers, K <= 64) in one

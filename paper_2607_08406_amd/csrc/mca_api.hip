@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -23,9 +24,36 @@ using mca::Aux;
 using mca::DevState;
 using mca::NetDev;
 
+// Per-call buffers of mca_eval_losses_noalloc: one array per GPU, for the
+// process's lifetime.  Host code never uses this name as an address: it is a
+// host-side stand-in; the device address comes from hipGetSymbolAddress.
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 constexpr int64_t kTraceCap = 4096;  // steps per trace chunk kept on the device
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of this GPU's scratch array, looked up once per device
+// with that device current (mca_init calls it).  nullptr on failure.
+hipError_t scratch_for_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 constexpr size_t kAlign = 256;
 constexpr int kMinLoopTile = 16;
 // The committed state (DevState), the snapshot of its counters taken when a
@@ -328,6 +356,7 @@ struct mca_ctx {
   DevState* snap = nullptr;  // counters at the start of the current run_steps call
   bool use_loop = true;
   bool loop_coop = true;     // cooperative launch of the step loop
+  void* scratch_dev = nullptr;  // this device's static scratch array (no-allocation entry point)
   int loop_fit_K = -1, loop_fit = 0;  // resident workgroups of the loop, cached per K
   // Transformer nets
   bool tf = false;
@@ -532,6 +561,28 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
   return MCA_OK;
 }
 
+// Where one evaluation's per-call buffers live: the context's workspace, or
+// the static scratch array of the no-allocation entry point.
+struct Bufs {
+  mca_cand* cands;
+  Aux* aux;
+  uint64_t* cmask;
+  float* partial;
+  double* dl;
+  float* pslab;
+  uint64_t* cols;
+  int* nnz;
+  int* rows;
+  float* rda;
+  int* rcnt;
+  float* pchain;
+};
+
+Bufs ctx_bufs(const mca_ctx* ctx) {
+  return Bufs{ctx->cands, ctx->aux, ctx->cmask, ctx->partial, ctx->dl, ctx->pslab,
+              ctx->cols, ctx->nnz, ctx->rows, ctx->rda, ctx->rcnt, ctx->pchain};
+}
+
 hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
   if (ctx->tf)
     return mca::tf_launch_propose(ctx->tfd, ctx->tfh, step, use_dev_t, ctx->st, K, ctx->cands,
@@ -540,37 +591,45 @@ hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
                              ctx->fmask, ctx->cmask, ctx->stream);
 }
 
-hipError_t prepare_dev(mca_ctx* ctx, int K) {
-  if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, ctx->cands, K, ctx->aux, ctx->stream);
-  return mca::launch_prepare(ctx->net, ctx->cands, K, ctx->aux, ctx->fmask, ctx->cmask, ctx->stream);
+hipError_t prepare_into(mca_ctx* ctx, const Bufs& b, int K) {
+  if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, b.cands, K, b.aux, ctx->stream);
+  return mca::launch_prepare(ctx->net, b.cands, K, b.aux, ctx->fmask, b.cmask, ctx->stream);
 }
+hipError_t prepare_dev(mca_ctx* ctx, int K) { return prepare_into(ctx, ctx_bufs(ctx), K); }
 
 // Scores the K staged candidates: the column kernel for the last two layers,
 // the tile kernel for layer L-3, the dense chain for layers 0..L-4.
-hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
+hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
   if (ctx->tf)
-    return mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, K, false, ctx->partial,
+    return mca::tf_launch_eval(ctx->tfd, ctx->tfh, b.cands, b.aux, K, false, b.partial,
                                ctx->tf_nblk, ctx->stream);
-  hipError_t e = mca::launch_eval(net, ctx->cands, ctx->aux, ctx->cmask, K, ctx->partial,
+  hipError_t e = mca::launch_eval(net, b.cands, b.aux, b.cmask, K, b.partial,
                                   ctx->lo.ntiles_ev, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
-    e = mca::launch_slab(net, ctx->cands, ctx->aux, K, ctx->cols, ctx->nnz, ctx->pslab,
-                         ctx->lo.nslab, -2, ctx->st, ctx->dl, ctx->stream);
+    e = mca::launch_slab(net, b.cands, b.aux, K, b.cols, b.nnz, b.pslab, ctx->lo.nslab, -2,
+                         ctx->st, b.dl, ctx->stream);
   if (e == hipSuccess && net.L >= 4)
-    e = mca::launch_chain(net, ctx->cands, ctx->aux, K, ctx->rows, ctx->rda, ctx->rcnt,
-                          ctx->pchain, ctx->lo.nchain, -2, ctx->st, ctx->dl, ctx->stream);
+    e = mca::launch_chain(net, b.cands, b.aux, K, b.rows, b.rda, b.rcnt, b.pchain,
+                          ctx->lo.nchain, -2, ctx->st, b.dl, ctx->stream);
   return e;
 }
+hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
+  return eval_into(ctx, net, ctx_bufs(ctx), K);
+}
 
+hipError_t select_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K, bool do_select,
+                       int32_t* trc, double* trd) {
+  if (ctx->tf)
+    return mca::launch_select(net, b.partial, ctx->tf_nblk, b.cands, nullptr, 0, nullptr, 0,
+                              b.aux, K, b.dl, ctx->st, do_select, trc, trd, kTraceCap,
+                              ctx->stream);
+  return mca::launch_select(net, b.partial, ctx->lo.ntiles_ev, b.cands, b.pslab,
+                            ctx->lo.nslab, b.pchain, ctx->lo.nchain, b.aux, K, b.dl,
+                            ctx->st, do_select, trc, trd, kTraceCap, ctx->stream);
+}
 hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, int32_t* trc,
                       double* trd) {
-  if (ctx->tf)
-    return mca::launch_select(net, ctx->partial, ctx->tf_nblk, ctx->cands, nullptr, 0, nullptr, 0,
-                              ctx->aux, K, ctx->dl, ctx->st, do_select, trc, trd, kTraceCap,
-                              ctx->stream);
-  return mca::launch_select(net, ctx->partial, ctx->lo.ntiles_ev, ctx->cands, ctx->pslab,
-                            ctx->lo.nslab, ctx->pchain, ctx->lo.nchain, ctx->aux, K, ctx->dl,
-                            ctx->st, do_select, trc, trd, kTraceCap, ctx->stream);
+  return select_into(ctx, net, ctx_bufs(ctx), K, do_select, trc, trd);
 }
 
 // Commits candidate k (k < 0: the device decision); each kernel applies only
@@ -866,6 +925,10 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
     hipError_t e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) rc = device_fail(ctx, e, "forward pass");
   }
+  if (rc == MCA_OK) {
+    hipError_t e = scratch_for_current_device(&ctx->scratch_dev);
+    if (e != hipSuccess) rc = device_fail(ctx, e, "hipGetSymbolAddress(scratch)");
+  }
   if (rc != MCA_OK) {
     g_thread_error = ctx->err;
     delete ctx;
@@ -928,6 +991,75 @@ int mca_rollback(mca_ctx* ctx) {
   if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
   ctx->pending = false;
   ctx->pending_K = 0;
+  return MCA_OK;
+}
+
+int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
+                            double* loss_out, double* dloss_out) {
+  MCA_LIVE(ctx);
+  if (ctx->tf) return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes MLP contexts");
+  if (K < 1 || K > mca::kMaxK) return fail(ctx, MCA_EINVAL, "K out of range [1, 1024]");
+  if (cands_host == nullptr) return fail(ctx, MCA_EINVAL, "cands_host is NULL");
+  if (ctx->scratch_dev == nullptr) return fail(ctx, MCA_EDEVICE, "no scratch array on this device");
+  int rc = check_cands(ctx, cands_host, K);
+  if (rc != MCA_OK) return rc;
+  // the per-call buffers, carved from the scratch array in the workspace's
+  // order and alignment
+  const Layout& lo = ctx->lo;
+  const NetDev& net = ctx->net;
+  const int L = net.L;
+  const size_t kk = (size_t)K;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const size_t o_cands = take(kk * sizeof(mca_cand)), o_aux = take(kk * sizeof(Aux));
+  const size_t o_cmask = take(kk * sizeof(uint64_t));
+  const size_t o_partial = take(kk * lo.ntiles_ev * sizeof(float)), o_dl = take(kk * sizeof(double));
+  size_t o_pslab = 0, o_cols = 0, o_nnz = 0, o_rows = 0, o_rda = 0, o_rcnt = 0, o_pchain = 0;
+  if (L >= 3) {
+    o_pslab = take(kk * lo.nslab * sizeof(float));
+    o_cols = take(kk * net.widths[L - 1] * sizeof(uint64_t));
+    o_nnz = take(kk * sizeof(int32_t));
+  }
+  if (L >= 4) {
+    o_rows = take(kk * net.N * sizeof(int32_t));
+    o_rda = take(kk * net.N * sizeof(float));
+    o_rcnt = take(kk * sizeof(int32_t));
+    o_pchain = take(kk * lo.nchain * sizeof(float));
+  }
+  if (off > kScratchBytes)
+    return fail(ctx, MCA_EINVAL, "K candidates on this net need " + std::to_string(off) +
+                                     " bytes of scratch, more than the static array's " +
+                                     std::to_string(kScratchBytes));
+  char* base = (char*)ctx->scratch_dev;
+  const Bufs b{(mca_cand*)(base + o_cands), (Aux*)(base + o_aux), (uint64_t*)(base + o_cmask),
+               (float*)(base + o_partial), (double*)(base + o_dl),
+               L >= 3 ? (float*)(base + o_pslab) : nullptr,
+               L >= 3 ? (uint64_t*)(base + o_cols) : nullptr,
+               L >= 3 ? (int*)(base + o_nnz) : nullptr,
+               L >= 4 ? (int*)(base + o_rows) : nullptr,
+               L >= 4 ? (float*)(base + o_rda) : nullptr,
+               L >= 4 ? (int*)(base + o_rcnt) : nullptr,
+               L >= 4 ? (float*)(base + o_pchain) : nullptr};
+  // every scratch word a kernel reads is written earlier in this call (the
+  // prepared values, masks, lists, counts, tile sums and loss changes), so
+  // nothing is cleared; overlapping calls on one GPU would race on them
+  MCA_HIP(ctx, hipMemcpyAsync(b.cands, cands_host, kk * sizeof(mca_cand), hipMemcpyHostToDevice, ctx->stream));
+  MCA_HIP(ctx, prepare_into(ctx, b, K));
+  MCA_HIP(ctx, eval_into(ctx, net, b, K));
+  MCA_HIP(ctx, select_into(ctx, net, b, K, false, nullptr, nullptr));
+  std::vector<double> dl(K);
+  double L_c = 0.0;
+  MCA_HIP(ctx, hipMemcpyAsync(dl.data(), b.dl, kk * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipMemcpyAsync(&L_c, &ctx->st->L, sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  for (int k = 0; k < K; ++k) {
+    if (loss_out) loss_out[k] = L_c + dl[k];
+    if (dloss_out) dloss_out[k] = dl[k];
+  }
   return MCA_OK;
 }
 

@@ -99,6 +99,7 @@ _SIGNATURES = {
                                 _P, ctypes.POINTER(mca_data), ctypes.c_int32, _P, ctypes.c_size_t, _P]),
     "mca_propose": (ctypes.c_int, [_P, ctypes.c_uint64, ctypes.c_int32, _P]),
     "mca_eval_losses": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
+    "mca_eval_losses_noalloc": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
     "mca_commit": (ctypes.c_int, [_P, ctypes.c_int32]),
     "mca_rollback": (ctypes.c_int, [_P]),
     "mca_set_option": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int64]),
@@ -276,6 +277,16 @@ def mca_eval_losses(ctx, cands: np.ndarray):
     dloss = np.zeros(K)
     _check(load_library().mca_eval_losses(ctx, cands.ctypes.data, K, loss.ctypes.data,
                                           dloss.ctypes.data), ctx)
+    return loss, dloss
+
+
+def mca_eval_losses_noalloc(ctx, cands: np.ndarray):
+    cands = np.ascontiguousarray(cands, dtype=CAND_DTYPE)
+    K = len(cands)
+    loss = np.zeros(K)
+    dloss = np.zeros(K)
+    _check(load_library().mca_eval_losses_noalloc(ctx, cands.ctypes.data, K, loss.ctypes.data,
+                                                  dloss.ctypes.data), ctx)
     return loss, dloss
 
 
