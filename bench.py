@@ -257,8 +257,8 @@ def make_context(cfg, w, k_max, args):
         ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
     if args.per_phase:
         ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, 0)
-    if args.plain_launch:
-        ctx.set_option(mca.MCA_OPT_LOOP_LAUNCH, 1)
+    if args.cooperative:
+        ctx.set_option(mca.MCA_OPT_LOOP_LAUNCH, 0)
     return ctx
 
 
@@ -368,8 +368,8 @@ def main():
     ap.add_argument("--tile", type=int, default=0, help="samples per workgroup (16..64)")
     ap.add_argument("--per-phase", action="store_true",
                     help="one launch per phase per step instead of the persistent loop")
-    ap.add_argument("--plain-launch", action="store_true",
-                    help="launch the persistent loop with an ordinary (not cooperative) launch")
+    ap.add_argument("--cooperative", action="store_true",
+                    help="launch the persistent loop cooperatively (default: an ordinary launch)")
     ap.add_argument("--eval-batch", type=int, default=1024,
                     help="candidates per launch of the incremental-phase measurement "
                          "(one- and two-layer MLPs; 0 skips it)")

@@ -107,11 +107,13 @@ typedef struct mca_net_desc {
    * candidates come first in stream order, so they are preferred. */
   int32_t n_prune;
   double beta;                          /* Metropolis selection intensity, > 0 */
-  /* minibatch (Sec. 2.2): 0 = every sample; otherwise the loss changes of
-   * steps t with floor(t / subset_period) = e are averaged over the
-   * subset_size samples n = (e * subset_size + m) mod N, m < subset_size (a
-   * cyclic window over the sample order).  Caches stay exact for every
-   * sample. */
+  /* minibatch (Sec. 2.2, MLPs): 0 = every sample; otherwise the loss
+   * changes of steps t with floor(t / subset_period) = e are averaged over
+   * the subset_size samples n = ((e mod N) * subset_size + m) mod N,
+   * m < subset_size (consecutive windows of the sample order, wrapping).
+   * The explicit mca_eval_losses scores the window of the device's next step
+   * (mca_set_step).  Caches stay exact for every sample, and the committed
+   * loss is the mean over every sample. */
   int64_t subset_size;
   int64_t subset_period;
 } mca_net_desc;
@@ -245,13 +247,14 @@ int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
  *                            to the order of the loss-change sums.
  *   MCA_OPT_LOOP_TILE        samples per workgroup of the persistent loop,
  *                            16..64 (default 64).
- *   MCA_OPT_LOOP_LAUNCH      0 (default): launch the persistent loop
- *                            cooperatively (the runtime guarantees that all
- *                            its workgroups are resident together); 1: an
- *                            ordinary launch of the same grid, relying on the
- *                            library's occupancy check (a workgroup kept out
- *                            by other work on the GPU makes the loop's bounded
- *                            waits give up: MCA_EDEVICE, never a hang). */
+ *   MCA_OPT_LOOP_LAUNCH      1 (default): an ordinary launch of the
+ *                            persistent loop's grid, relying on the library's
+ *                            occupancy check for all workgroups to be resident
+ *                            together (on a GPU shared with other work, a
+ *                            workgroup kept out makes the loop's bounded waits
+ *                            give up: MCA_EDEVICE, never a hang); 0: a
+ *                            cooperative launch, where the runtime guarantees
+ *                            it (about 15 us more per call). */
 #define MCA_OPT_PERSISTENT_LOOP 1
 #define MCA_OPT_LOOP_TILE 2
 #define MCA_OPT_LOOP_LAUNCH 3

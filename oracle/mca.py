@@ -43,6 +43,19 @@ def metropolis_threshold(u: float, beta: float) -> float:
     return math.inf if u == 0.0 else -math.log(u) / beta
 
 
+def minibatch(t: int, N: int, size: int, period: int):
+    """The samples whose loss changes step t averages (Sec. 2.2's minibatch;
+    None = all): window e = floor(t / period) covers the `size` samples
+    n = (e size + m) mod N, m < size -- consecutive windows of the sample
+    order, wrapping around."""
+    if not size:
+        return None
+    start = ((t // period) % N) * size % N
+    mask = np.zeros(N, dtype=bool)
+    mask[(start + np.arange(size)) % N] = True
+    return mask
+
+
 def thresholds(seed: int, tag: int, t: int, K: int, beta: float = 0.0):
     """Per-candidate thresholds of step t: 0 for the greedy rule (beta = 0)."""
     if not beta:
@@ -73,12 +86,15 @@ def _delta(model, c):
 
 def evaluate_all(model, t: int, K: int, seed: int, tag: int, delta: float,
                  mode: str = "weight", accept_ties: bool = False, scan_all: bool = True,
-                 beta: float = 0.0, n_prune: int = 0):
+                 beta: float = 0.0, n_prune: int = 0, subset=(0, 1)):
     """Score candidates (t, 0..K-1) against the committed state without
     committing; candidates k < n_prune are pruning moves (Sec. 2.2: they come
-    first in stream order, so pruning is preferred).  Returns (L_t,
+    first in stream order, so pruning is preferred); subset = (size, period)
+    averages each change over step t's minibatch.  Returns (L_t,
     candidates, dL list, sizes list, thresholds, index of the first that
     passes the test or -1)."""
+    if subset[0]:
+        model.subset = minibatch(t, model.X.shape[0], subset[0], subset[1])
     L_t = model.loss()
     th = thresholds(seed, tag, t, K, beta)
     cands, dls, mags = [], [], []
@@ -94,6 +110,8 @@ def evaluate_all(model, t: int, K: int, seed: int, tag: int, delta: float,
             chosen = k
             if not scan_all:
                 break
+    if subset[0]:
+        model.subset = None
     return L_t, cands, dls, mags, th[:len(dls)], chosen
 
 
@@ -112,7 +130,7 @@ def evaluate(model, t: int, K: int, seed: int, tag: int, delta: float,
 def step(model, t: int, K: int, seed: int, tag: int, delta: float,
          mode: str = "weight", accept_ties: bool = False,
          scan_all: bool = True, force: Optional[int] = None,
-         beta: float = 0.0, n_prune: int = 0) -> StepRecord:
+         beta: float = 0.0, n_prune: int = 0, subset=(0, 1)) -> StepRecord:
     """One step of K candidates: evaluate, then commit the first that passes.
 
     scan_all=False stops at the first improving candidate (the sequential
@@ -121,7 +139,8 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
     where the decision lies inside the floating-point tie band.
     """
     L_t, cands, dls, mags, th, chosen = evaluate_all(model, t, K, seed, tag, delta, mode,
-                                                     accept_ties, scan_all, beta, n_prune)
+                                                     accept_ties, scan_all, beta, n_prune,
+                                                     subset)
     losses = [L_t + d for d in dls]
     if force is not None:
         chosen = force
@@ -132,10 +151,10 @@ def step(model, t: int, K: int, seed: int, tag: int, delta: float,
 
 def run(model, t0: int, n_steps: int, K: int, seed: int, tag: int, delta: float,
         mode: str = "weight", accept_ties: bool = False, scan_all: bool = False,
-        beta: float = 0.0, n_prune: int = 0):
+        beta: float = 0.0, n_prune: int = 0, subset=(0, 1)):
     """n_steps consecutive steps starting at step t0; returns the records."""
     return [step(model, t, K, seed, tag, delta, mode, accept_ties, scan_all, beta=beta,
-                 n_prune=n_prune)
+                 n_prune=n_prune, subset=subset)
             for t in range(t0, t0 + n_steps)]
 
 

@@ -309,10 +309,18 @@ class IncrementalMLP(_Base):
         mag = mag + np.abs(dl) * self._cache_sensitivity(c, rows, dcol) / 16.0
         return rows, dl, mag
 
+    # minibatch (Sec. 2.2): a boolean mask over the samples, or None for all
+    subset = None
+
     def delta(self, c: Candidate):
         """(dL, A): the loss change of candidate c (Eq. 2 difference), from the
-        field changes, and the mean size A of its first-order terms."""
-        _, dl, mag = self.sample_changes(c)
+        field changes, and the mean size A of its first-order terms; over the
+        current minibatch when one is set."""
+        rows, dl, mag = self.sample_changes(c)
+        if self.subset is not None:
+            keep = self.subset[rows]
+            n = int(self.subset.sum())
+            return float(dl[keep].sum()) / n, float(mag[keep].sum()) / n
         N = self.X.shape[0]
         return float(dl.sum()) / N, float(mag.sum()) / N
 
@@ -325,7 +333,7 @@ class IncrementalMLP(_Base):
         rows, dcol, later = self._changes(c)
         dl, _ = ce_change(self._softmax()[rows], self._logit_change(c, rows, dcol, later),
                           self.y[rows])
-        dL = float(dl.sum()) / self.X.shape[0]
+        dL = float(dl.sum()) / self.X.shape[0]  # the loss over every sample
         self.Z[c.layer][rows, c.j] += dcol
         for m, dz in later.items():
             if m != "abs":

@@ -65,6 +65,8 @@ __global__ __launch_bounds__(kRowsThreads) void k_rows(NetDev net_arg, const mca
   const int64_t N = net.N, Ns = net.Ns;
   const float* in = (l == 0) ? net.XT : net.Z[l - 1];
   float* zrow = net.Z[l] + (int64_t)c.j * Ns;
+  // an evaluation lists the step's minibatch only; a commit moves every sample
+  const int64_t sub0 = subset_start(net, commit ? 0 : st->t);
   int base = 0;
   for (int64_t n0 = 0; n0 < N; n0 += kRowsThreads) {
     const int64_t n = n0 + tid;
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(kRowsThreads) void k_rows(NetDev net_arg, const mca
         if (commit) gstore(&zrow[n], zl + dz);
       }
     }
-    const bool take = da != 0.f;
+    const bool take = da != 0.f && (commit || in_subset(net, sub0, n));
     const uint64_t b = __ballot(take);
     if (lane == 0) wave_n[wave] = (int)__popcll(b);
     __syncthreads();
@@ -103,7 +105,7 @@ __global__ __launch_bounds__(kRowsThreads) void k_rows(NetDev net_arg, const mca
       const int64_t idx = (int64_t)c.j * net.widths[l] + c.i;
       gstore(&net.W[l][idx], a.w_new);
       if (net.ternary) gstore(&net.codes[l][idx], (int8_t)c.code);
-      st->L += dL[k];
+      if (net.sub_size == 0) st->L += dL[k];
       st->accepted += 1;
     }
   }

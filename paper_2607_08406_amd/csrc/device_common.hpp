@@ -45,6 +45,7 @@ struct NetDev {
   double beta;      // Metropolis selection intensity
   int32_t n_prune;  // candidates 0 .. n_prune-1 of a step set their weight to zero
   int32_t pad0;
+  int64_t sub_size, sub_period;  // minibatch window (0: every sample)
   int64_t N, Ns;    // samples, row stride of the unit-major caches
   int64_t P;        // parameters
   int32_t widths[MCA_MAX_LAYERS + 1];
@@ -432,6 +433,24 @@ __device__ __forceinline__ Aux prepare_candidate(const NetDev& net, const mca_ca
 // The selection test: Eq. 6 (dL < 0, or dL <= 0 with ties) when theta is 0;
 // the Metropolis rule of Eq. 7 as dL < theta otherwise (theta > 0).  NaN
 // compares false either way, +inf never passes.
+// Minibatch (Sec. 2.2): step t averages its loss changes over the window of
+// sub_size samples starting at ((t / sub_period) mod N) * sub_size mod N,
+// wrapping around the sample order; without one, over every sample.
+__device__ __forceinline__ int64_t subset_start(const NetDev& net, uint64_t t) {
+  if (net.sub_size == 0) return 0;
+  const uint64_t e = t / (uint64_t)net.sub_period;
+  return (int64_t)(((e % (uint64_t)net.N) * (uint64_t)net.sub_size) % (uint64_t)net.N);
+}
+__device__ __forceinline__ bool in_subset(const NetDev& net, int64_t start, int64_t n) {
+  if (net.sub_size == 0) return true;
+  int64_t d = n - start;
+  d += (d < 0) ? net.N : 0;
+  return d < net.sub_size;
+}
+__device__ __forceinline__ double subset_count(const NetDev& net) {
+  return (double)(net.sub_size ? net.sub_size : net.N);
+}
+
 __device__ __forceinline__ bool accepts(double dL, int ties, double theta = 0.0) {
   if (theta > 0.0) return dL < theta;
   return ties ? (dL <= 0.0) : (dL < 0.0);

@@ -200,7 +200,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // row 16-byte aligned and a 16-byte read of the same column by 16 lanes
   // (rows k .. k+15) conflict-free
   __shared__ __attribute__((aligned(16))) float dlp_lds[kLoopMaxK][68];
-  __shared__ float dap_lds[kLoopMaxK][64];  // each pair's activation change, which a commit reuses
   __shared__ uint16_t list_lds[2][kLoopMaxK * 64];  // work lists, by step parity
   __shared__ int list_n[2];
   __shared__ uint32_t stage_cnt;  // waves 1-15 that have landed a step (15 per step)
@@ -256,7 +255,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       for (int b = 0; b < kMaxTilesPerLane; ++b)
         if (lane + 64 * b < G) acc += (double)__uint_as_float((uint32_t)(w[b] >> 32));
       const double tot = wave_sum_f64(acc);
-      const uint64_t word = pack_dl(tot / (double)net.N, tag16(s));  // +inf: rejected
+      const uint64_t word = pack_dl(tot / subset_count(net), tag16(s));  // +inf: rejected
       if (lane < kLoopReplicas) st_agent(&a.dls[lane * kLoopMaxK + k], word);
     }
     return;
@@ -420,8 +419,10 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   // fed by a hidden layer every live sample, since the commit of the step
   // before may still change that input (a pair whose input is zero adds
   // exactly 0).  Results do not depend on the order of the list.
-  auto land_samples = [&](int cb, int b, int slot) {
+  auto land_samples = [&](int cb, int b, int slot, uint64_t t_land) {
     const int w = __builtin_amdgcn_readfirstlane(wave) - 2;
+    // the landed step's minibatch: only its samples are listed and scored
+    const bool mem = in_subset(net, subset_start(net, t_land), n);
     // every LDS read of the landing is issued here, before any is used
     const LastCommit lc = last[slot];
     const float zrow_v = zrow_lds[slot][lane];
@@ -448,7 +449,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
         const float in = (!hid && two) ? act_fn(ar, act, gamma) : ar;
         ain_lds[b][k][lane] = live ? in : 0.f;
         zh_lds[b][k][lane] = zz;
-        m[q] = __ballot(live && (in != 0.f || (two && !hid)));
+        m[q] = __ballot(live && mem && (in != 0.f || (two && !hid)));
         tot += (int)__popcll(m[q]);
       }
     }
@@ -483,7 +484,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
     if (a.n_steps > 1) issue_cand(1);
   } else if (wave >= 2) {
     issue_samples(0);
-    land_samples(0, 0, 1);
+    land_samples(0, 0, 1, t0);
     if (a.n_steps > 1) issue_samples(1);
   }
   __syncthreads();
@@ -509,7 +510,6 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       dlp_lds[k][sl] = pair_change<CM>(C, act, gamma, c.layer == L - 1, zh_lds[buf][k][sl],
                                        prep_lds[buf][k].de, w, wcol_lds[buf][k], wmax_lds[buf][k],
                                        ain_lds[buf][k][sl], &pl_lds[sl], y_lds[sl], da);
-      dap_lds[k][sl] = da;
     }
     if (tid == 0) list_n[buf ^ 1] = 0;
     // last step's commit stores land before this step's staging reads HBM
@@ -557,7 +557,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       if (s + 2 < a.n_steps) issue_cand((int)((s + 2) & 3));
       if (s + 3 < a.n_steps) draw(t0 + s + 3, (int)((s + 3) & 3));
     } else if (wave >= 2) {
-      if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1);
+      if (s + 1 < a.n_steps) land_samples((int)((s + 1) & 3), buf ^ 1, buf ^ 1, t0 + s + 1);
       landed();
       if (s + 2 < a.n_steps) issue_samples((int)((s + 2) & 3));
     }
@@ -628,11 +628,13 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
       const bool chid = c.layer == Lk - 2;  // the winner is a hidden-unit weight
       float zr = 0.f;  // the committed unit's row of this tile, lane = sample
       if (kc >= 0) {
-        // the logits move by the activation change the scoring computed
-        // (kept for every listed pair: every sample with a non-zero input)
+        // the logits move by the activation change, by the scoring's
+        // expressions (the same bits for a scored sample; a sample outside
+        // the step's minibatch was not scored but moves all the same)
         const float ain = ain_lds[buf][kc][lane];
         const float z_raw = zh_lds[buf][kc][lane];
-        const float da = dap_lds[kc][lane];
+        const float dz0 = au.de * ain;
+        const float da = chid ? dphi(z_raw, dz0, act, gamma) : dz0;
         float wc[CM];
 #pragma unroll
         for (int cc = 0; cc < CM; ++cc) wc[cc] = wcol_lds[buf][kc][cc];
@@ -711,7 +713,7 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
           const uint64_t upto = (kc >= 0) ? ((kc == 63) ? ~0ull : ((2ull << kc) - 1ull)) : ~0ull;
           n_tie += (uint64_t)__popcll(tie_mask & upto);
           if (kc >= 0) {
-            L_acc += vk;
+            if (net.sub_size == 0) L_acc += vk;  // a minibatch's change is not the loss's
             ++n_acc;
           }
           last_k = kc;

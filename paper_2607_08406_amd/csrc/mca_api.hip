@@ -97,7 +97,8 @@ std::string check_selection(const mca_net_desc* net, int64_t n_samples, int* cod
   *code = MCA_EUNSUPPORTED;
   if (net->kind == MCA_NET_TRANSFORMER && net->n_prune != 0)
     return "pruning candidates are built for MLPs only";
-  if (net->subset_size != 0) return "minibatch not built yet";
+  if (net->kind == MCA_NET_TRANSFORMER && net->subset_size != 0)
+    return "minibatches are built for MLPs only";
   *code = MCA_OK;
   return "";
 }
@@ -355,7 +356,7 @@ struct mca_ctx {
   mca::LoopSync* loop_sync = nullptr;
   DevState* snap = nullptr;  // counters at the start of the current run_steps call
   bool use_loop = true;
-  bool loop_coop = true;     // cooperative launch of the step loop
+  bool loop_coop = false;    // cooperative launch of the step loop (default: ordinary)
   void* scratch_dev = nullptr;  // this device's static scratch array (no-allocation entry point)
   int loop_fit_K = -1, loop_fit = 0;  // resident workgroups of the loop, cached per K
   // Transformer nets
@@ -604,7 +605,7 @@ hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
     return mca::tf_launch_eval(ctx->tfd, ctx->tfh, b.cands, b.aux, K, false, b.partial,
                                ctx->tf_nblk, ctx->stream);
   hipError_t e = mca::launch_eval(net, b.cands, b.aux, b.cmask, K, b.partial,
-                                  ctx->lo.ntiles_ev, ctx->stream);
+                                  ctx->lo.ntiles_ev, ctx->st, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, b.cands, b.aux, K, b.cols, b.nnz, b.pslab, ctx->lo.nslab, -2,
                          ctx->st, b.dl, ctx->stream);
@@ -851,6 +852,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.rule = net->accept_rule;
   nd.beta = net->beta;
   nd.n_prune = net->n_prune;
+  nd.sub_size = net->subset_size;
+  nd.sub_period = net->subset_size ? net->subset_period : 1;
   nd.seed = net->seed;
   nd.tag = net->stream_tag;
   nd.N = N;
@@ -981,6 +984,8 @@ int mca_commit(mca_ctx* ctx, int32_t k) {
   if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
   if (k < 0 || k >= ctx->pending_K) return fail(ctx, MCA_EINVAL, "k outside the pending batch");
   MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, ctx->net, k); }));
+  if (!ctx->tf && ctx->net.sub_size > 0)  // the loss over every sample, from the logits
+    MCA_HIP(ctx, mca::launch_loss_refresh(ctx->net, ctx->bsum, ctx->st, ctx->stream));
   ctx->pending = false;
   ctx->pending_K = 0;
   return MCA_OK;
@@ -1173,6 +1178,8 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     }
     done += chunk;
   }
+  if (!ctx->tf && net.sub_size > 0)  // the loss over every sample, from the logits
+    MCA_HIP(ctx, mca::launch_loss_refresh(net, ctx->bsum, ctx->st, ctx->stream));
   // state, snapshot and abort word: one copy
   alignas(8) unsigned char blk[kStateBlock];
   MCA_HIP(ctx, hipMemcpyAsync(blk, ctx->st, kStateBlock, hipMemcpyDeviceToHost, ctx->stream));

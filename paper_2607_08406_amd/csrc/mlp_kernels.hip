@@ -150,6 +150,8 @@ struct EvArgs {
   const Aux* aux;
   const uint64_t* cmask;  // per candidate: bit b set when tile b can change
   float* partial;
+  const DevState* st;     // the step whose minibatch is scored (st->t)
+  int64_t sub_size, sub_period;
   int64_t N, Ns;
   int L, C, act, nh, K, ntiles, bpt;  // bpt: blocks per tile
   float gamma;
@@ -181,6 +183,12 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
   const int ntiles = a.ntiles, K = a.K, bpt = a.bpt;
   const int wpt = bpt * kEvWaves;  // waves per tile
   const int nslots = ntiles * bpt;
+  // the minibatch window of the step being scored (every sample without one)
+  NetDev sub{};
+  sub.N = N;
+  sub.sub_size = a.sub_size;
+  sub.sub_period = a.sub_period;
+  const int64_t sub0 = subset_start(sub, a.sub_size ? a.st->t : 0);
   uint16_t* const code = code_lds[wave];
   float* const ainl = ain_lds[wave];
   float* const zhl = zh_lds[wave];
@@ -315,7 +323,7 @@ __global__ __launch_bounds__(kEvThreads) __attribute__((amdgpu_waves_per_eu(CM <
         uint64_t bt[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          pr[t] = use && sl + t < N && in[t] != 0.f;
+          pr[t] = use && sl + t < N && in[t] != 0.f && in_subset(sub, sub0, sl + t);
           bt[t] = __ballot(pr[t]);
         }
         const int npairs = (int)(__popcll(bt[0]) + __popcll(bt[1]) + __popcll(bt[2]) + __popcll(bt[3]));
@@ -425,7 +433,7 @@ __device__ __forceinline__ double candidate_dl(const NetDev& net, const PartialS
   }
 #pragma unroll
   for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-  return (k < K && aux[k].valid) ? s / (double)net.N : __builtin_huge_val();
+  return (k < K && aux[k].valid) ? s / subset_count(net) : __builtin_huge_val();
 }
 
 // Loss changes of many candidates: block b adds the tile sums of candidates
@@ -515,7 +523,7 @@ __global__ __launch_bounds__(kTile) void k_commit_column(NetDev net_arg, const m
     // the transposed copy of W_{L-2}: W_T[i][j] = W[j][i]
     if (net.WT != nullptr && c.layer == net.L - 2)
       net.WT[(int64_t)c.i * net.widths[c.layer + 1] + c.j] = a.w_new;
-    st->L += dL[k];
+    if (net.sub_size == 0) st->L += dL[k];  // a minibatch's change is not the loss's
     st->accepted += 1;
   }
 }
@@ -662,7 +670,8 @@ int eval_grid(const void* kernel, int variant) {
 }  // namespace
 
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
-                       const uint64_t* cmask, int K, float* partial, int ntiles, hipStream_t s) {
+                       const uint64_t* cmask, int K, float* partial, int ntiles,
+                       const DevState* st, hipStream_t s) {
   const int L = net.L;
   EvArgs a{};
   a.in_hid = (L >= 3) ? net.Z[L - 3] : net.XT;
@@ -675,6 +684,9 @@ hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
   a.aux = aux;
   a.cmask = cmask;
   a.partial = partial;
+  a.st = st;
+  a.sub_size = net.sub_size;
+  a.sub_period = net.sub_period;
   a.N = net.N;
   a.Ns = net.Ns;
   a.L = L;
@@ -740,6 +752,13 @@ hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* au
                          const double* dL, DevState* st, int k_host, int ntiles, hipStream_t s) {
   hipLaunchKernelGGL(k_commit_column, dim3(ntiles), dim3(kTile), 0, s, net, cands, aux, dL, st,
                      k_host);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_refresh(const NetDev& net, double* bsum, DevState* st, hipStream_t s) {
+  const int nb = (int)((net.N + kTile - 1) / kTile);
+  hipLaunchKernelGGL(k_ce_forward, dim3(nb), dim3(kTile), 0, s, net, bsum);
+  hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(64), 0, s, net, bsum, nb, st);
   return hipGetLastError();
 }
 

@@ -20,7 +20,8 @@ hipError_t launch_prepare(const NetDev& net, const mca_cand* cands, int K, Aux* 
 int eval_tiles(int64_t n_samples);
 int eval_tile_size();
 hipError_t launch_eval(const NetDev& net, const mca_cand* cands, const Aux* aux,
-                       const uint64_t* cmask, int K, float* partial, int ntiles, hipStream_t s);
+                       const uint64_t* cmask, int K, float* partial, int ntiles,
+                       const DevState* st, hipStream_t s);
 hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
                          const mca_cand* cands, const float* pslab, int nslab,
                          const float* pchain, int nchain, const Aux* aux, int K, double* dL,
@@ -28,6 +29,9 @@ hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
                          int64_t tr_cap, hipStream_t s);
 hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* aux,
                          const double* dL, DevState* st, int k_host, int ntiles, hipStream_t s);
+// The committed loss from the cached logits (the losses and softmax cached
+// from them again): with a minibatch the loss is not the sum of the changes.
+hipError_t launch_loss_refresh(const NetDev& net, double* bsum, DevState* st, hipStream_t s);
 hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s);
 
 }  // namespace mca

@@ -1,6 +1,5 @@
 // Evaluation and commit of mutations of a first-layer weight in a
-// three-layer MLP ("MCA Training of Shallow Wide Networks", the two-hidden-
-// layer case): changing W_0[j, i] moves z_1[n, j] by de * x[n, i] for every
+// three-layer MLP (Sec. 2.4, the two-hidden-layer case): changing W_0[j, i] moves z_1[n, j] by de * x[n, i] for every
 // sample whose input x[n, i] is nonzero; its activation change da[n] moves
 // every unit m of the second hidden layer by da[n] * W_1[m, j] (the O(n_2)
 // multiplications per sample the paper describes), and the logits then change
@@ -320,13 +319,15 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
     __syncthreads();
     const int ng = ngroup;
     if (ng == 0) continue;
-    // 2. the affected pairs: a nonzero input and a changed activation
+    // 2. the affected pairs: a nonzero input and a changed activation (an
+    // evaluation scores the step's minibatch only; a commit moves every sample)
+    const int64_t sub0 = subset_start(net, commit ? 0 : st->t);
     for (int e = tid; e < ng * T; e += kSlabThreads) {
       const int s = e / T, t = e - s * T;
       const int64_t n = n0 + t;
       dlp[s * T + t] = 0.f;
       float da = 0.f;
-      if (n < N) {
+      if (n < N && (commit || in_subset(net, sub0, n))) {
         const float xr = gload(&in[(int64_t)gi[s] * Ns + n]);
         const float x = (l == 0) ? xr : act_fn(xr, act, gamma);
         if (x != 0.f) {
@@ -457,7 +458,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
     const int64_t idx = (int64_t)c.j * net.widths[l] + c.i;
     gstore(&net.W[l][idx], a.w_new);
     if (net.ternary) gstore(&net.codes[l][idx], (int8_t)c.code);
-    st->L += dL[kc];
+    if (net.sub_size == 0) st->L += dL[kc];
     st->accepted += 1;
   }
 }

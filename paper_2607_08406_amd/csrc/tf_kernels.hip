@@ -1,5 +1,5 @@
-// HIP kernels (gfx950) of the decoder Transformer path of MCA ("MCA Training
-// of Transformer Networks"): the candidate stream over all parameter tensors,
+// HIP kernels (gfx950) of the decoder Transformer path of MCA (Sec. 2.5):
+// the candidate stream over all parameter tensors,
 // each candidate's forward pass from the first stage its parameter changes,
 // the per-position cross-entropy and its change against the committed
 // per-position losses, and the commit.

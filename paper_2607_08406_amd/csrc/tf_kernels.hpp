@@ -1,5 +1,4 @@
-// The decoder Transformer of "MCA Training of Transformer Networks" on the
-// device: its description, and the host-side launchers of its kernels
+// The decoder Transformer of Sec. 2.5 on the device: its description, and the host-side launchers of its kernels
 // (implemented in tf_kernels.hip).
 #pragma once
 

@@ -76,13 +76,15 @@ class ParityStats:
                 f"unresolved {self.unresolved}, decision flips {self.flips}")
 
 
-def make_pair(cfg, w, k_max, oracle="incremental", bound=0.0, beta=0.0, n_prune=0):
+def make_pair(cfg, w, k_max, oracle="incremental", bound=0.0, beta=0.0, n_prune=0,
+              subset=(0, 1)):
     from paper_2607_08406_amd import mca
     scales = w["scales"]
     desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
                         ternary_scales=scales, pick=cfg.layer_pick,
                         accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
-                        stream_tag=cfg.stream_tag, bound=bound, beta=beta, n_prune=n_prune)
+                        stream_tag=cfg.stream_tag, bound=bound, beta=beta, n_prune=n_prune,
+                        subset_size=subset[0], subset_period=subset[1])
     ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=k_max, codes=w["codes"])
     cls = IncrementalMLP if oracle == "incremental" else FullMLP
     ref = cls(MLPState(w["weights"], w["codes"], scales), w["X"], w["y"], cfg.act, cfg.gamma)
@@ -156,12 +158,13 @@ def check_step(stats, gpu_dl, ref_dl, mags, kappas, thetas, accept_ties, chosen_
     return chosen_gpu
 
 
-def _oracle_step(ref, cfg, t, K, bound, beta, n_prune):
+def _oracle_step(ref, cfg, t, K, bound, beta, n_prune, subset=(0, 1)):
     """The oracle's view of step t: candidates, loss changes (+inf for those a
     weight bound rejects unevaluated, Eq. 1), sizes, thresholds, decision."""
     L_t, rc, dls, mags, th, chosen = omca.evaluate_all(
         ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-        getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune)
+        getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune,
+        subset=subset)
     bounded = [_bounded(ref, c, bound) for c in rc]
     if bound > 0:
         dls = [math.inf if b else d for b, d in zip(bounded, dls)]
@@ -170,17 +173,21 @@ def _oracle_step(ref, cfg, t, K, bound, beta, n_prune):
     return L_t, rc, dls, mags, th, chosen, (bounded if bound > 0 else None)
 
 
-def explicit_steps(ctx, ref, cfg, t0, n_steps, K, stats=None, bound=0.0, beta=0.0, n_prune=0):
+def explicit_steps(ctx, ref, cfg, t0, n_steps, K, stats=None, bound=0.0, beta=0.0, n_prune=0,
+                   subset=(0, 1)):
     """propose / eval_losses / commit-or-rollback on the GPU beside the oracle.
     Decisions follow the oracle's (the device's only inside the unresolvable
-    margin, where both are valid)."""
+    margin, where both are valid).  With a minibatch, the device's next step
+    is set to t first (the explicit evaluation scores its window)."""
     stats = stats if stats is not None else ParityStats()
     accepted = 0
     for t in range(t0, t0 + n_steps):
         cands = ctx.propose(t, K)
         L_t, rc, dls, mags, th, chosen, bounded = _oracle_step(ref, cfg, t, K, bound, beta,
-                                                               n_prune)
+                                                               n_prune, subset)
         assert_cands_equal(cands, rc)
+        if subset[0]:
+            ctx.set_step(t)
         _, gdl = ctx.eval_losses(cands)
         kap = [mlp_kappa(cfg.widths, c.layer) for c in rc]
         gch = next((k for k in range(K) if omca.accepts(float(gdl[k]), cfg.accept_ties, th[k])), -1)
@@ -196,7 +203,7 @@ def explicit_steps(ctx, ref, cfg, t0, n_steps, K, stats=None, bound=0.0, beta=0.
 
 
 def replay_trace(ref, cfg, t0, chosen, dloss, K, stats=None, beta=0.0, kappa=None, bound=0.0,
-                 n_prune=0):
+                 n_prune=0, subset=(0, 1)):
     """Replay a device run's trace on the oracle: every traced loss change
     against the oracle's, every decision against the oracle's; where only an
     unresolvable margin separates them the oracle follows the device (both
@@ -205,7 +212,8 @@ def replay_trace(ref, cfg, t0, chosen, dloss, K, stats=None, beta=0.0, kappa=Non
     accepted = 0
     for n in range(len(chosen)):
         t = t0 + n
-        L_t, rc, dls, mags, th, orc, bounded = _oracle_step(ref, cfg, t, K, bound, beta, n_prune)
+        L_t, rc, dls, mags, th, orc, bounded = _oracle_step(ref, cfg, t, K, bound, beta, n_prune,
+                                                            subset)
         if kappa is None:
             kap = [mlp_kappa(cfg.widths, c.layer) for c in rc]
         else:

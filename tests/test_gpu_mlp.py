@@ -97,6 +97,39 @@ def test_small_wide_explicit_and_loop(mca, persistent, tile):
     ctx.close()
 
 
+def test_ordinary_launch_of_the_loop(mca):
+    """The persistent loop with an ordinary launch of its grid (the default)
+    and a cooperative one: the same decisions and weights,
+    over several calls (the counters of each call, the first step of each
+    launch from device state)."""
+    cfg = small_wide()
+    w = mlp_workload(cfg)
+    a, ref = make_pair(cfg, w, k_max=64)
+    a.set_option(mca.MCA_OPT_LOOP_LAUNCH, 0)  # cooperative
+    b, _ = make_pair(cfg, w, k_max=64)
+    b.set_option(mca.MCA_OPT_LOOP_LAUNCH, 1)  # ordinary (the default)
+    ps = ParityStats("wide 784-512-10 ordinary and cooperative launch")
+    t = 0
+    for n in (1, 7, 40):
+        sa, ca, da = a.run_steps(n, 64, trace=True, trace_dloss=True)
+        sb, cb, db = b.run_steps(n, 64, trace=True, trace_dloss=True)
+        assert sa.steps == sb.steps == n and sa.next_step == sb.next_step == t + n
+        assert sa.accepted == sb.accepted and sa.evaluated == n * 64
+        np.testing.assert_array_equal(ca, cb)
+        replay_trace(ref, cfg, t, cb, db, 64, ps)
+        t += n
+    pa, _ = a.params()
+    pb, _ = b.params()
+    for x, y in zip(pa, pb):
+        assert x.tobytes() == y.tobytes()
+    assert_state_equal(b, ref)
+    for v in (2, -1):
+        with pytest.raises(mca.MCAError, match="EINVAL"):
+            b.set_option(mca.MCA_OPT_LOOP_LAUNCH, v)
+    a.close()
+    b.close()
+
+
 def test_full_wide_workload(mca):
     """784-16384-10 on 10,000 samples, K=64: init loss, 20 device steps with
     every candidate's dL, replayed on the incremental oracle; two sampled

@@ -210,10 +210,62 @@ def test_mixed_pruning_deep(mca):
     ctx.close()
 
 
+@pytest.mark.parametrize("persistent", [1, 0])
+def test_minibatch_wide(mca, persistent):
+    """Sec. 2.2's minibatch: each step's loss changes average over a window of
+    400 of the 1,000 samples (moving every 3 steps, wrapping around), pairs
+    outside it are not scored; commits still move every sample, and the
+    committed loss is the mean over all of them."""
+    cfg = small_wide(name="wide_mb")
+    sub = (400, 3)
+    banner(f"minibatch {sub} 784-512-10 persistent={persistent}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=16, subset=sub)
+    ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, persistent)
+    ps = ParityStats(f"minibatch 784-512-10 persistent={persistent}")
+    _, acc = explicit_steps(ctx, ref, cfg, 0, 15, 16, ps, subset=sub)
+    assert acc > 3
+    assert_state_equal(ctx, ref)
+    ctx.set_step(15)
+    st, ch, dl = ctx.run_steps(60, 16, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 15, ch, dl, 16, ps, subset=sub)
+    assert_state_equal(ctx, ref)
+    L, t = ctx.loss()
+    assert t == 75 and abs(L - ref.loss()) <= 1e-5 * ref.loss()
+    ctx.close()
+
+
+@pytest.mark.parametrize("kind", ["ternary3", "deep"])
+def test_minibatch_other_paths(mca, kind):
+    """The window on the three-layer slab and the deep chain paths, with
+    pruning mixed in (Sec. 2.2's setting: pruning preferred, minibatches)."""
+    if kind == "ternary3":
+        cfg = CONFIGS["ternary"].scaled(name="t3_mb", widths=(784, 96, 80, 10), n_samples=333,
+                                        K=16)
+    else:
+        cfg = CONFIGS["deep"].scaled(name="deep_mb", widths=(784, 256, 256, 256, 10),
+                                     n_samples=300, K=16, delta=0.05)
+    sub = (150, 2)
+    banner(f"minibatch {sub} {cfg.name}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=16, n_prune=4, subset=sub)
+    ps = ParityStats(f"minibatch + pruning {cfg.name}")
+    explicit_steps(ctx, ref, cfg, 0, 20, 16, ps, n_prune=4, subset=sub)
+    assert_state_equal(ctx, ref)
+    ctx.set_step(20)
+    st, ch, dl = ctx.run_steps(20, 16, trace=True, trace_dloss=True)
+    replay_trace(ref, cfg, 20, ch, dl, 16, ps, n_prune=4, subset=sub)
+    assert_state_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= 1e-5 * ref.loss()
+    ctx.close()
+
+
 def test_selection_options_validated(mca):
     cfg = small_wide()
     w = mlp_workload(cfg)
-    for kw in [dict(beta=-1.0), dict(n_prune=-1)]:
+    for kw in [dict(beta=-1.0), dict(n_prune=-1), dict(subset_size=cfg.n_samples + 1),
+               dict(subset_size=10, subset_period=0)]:
         d = mca.mlp_desc(cfg.widths, cfg.act, delta=cfg.delta, **kw)
         with pytest.raises(mca.MCAError, match="EINVAL"):
             mca.mca_plan(d, cfg.n_samples, 8)

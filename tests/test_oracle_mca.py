@@ -297,3 +297,31 @@ def test_mixed_pruning_puts_pruning_first():
             kinds.add(r.cands[r.chosen].prune)
             assert all(d >= 0 for d in r.dls[:r.chosen])
     assert kinds == {True, False}
+
+
+def test_minibatch_windows_and_means():
+    """Sec. 2.2's minibatch: step t's window e = t // period covers samples
+    (e size + m) mod N; a candidate's change is the mean over the window of
+    its samples' changes; the committed loss stays the mean over all."""
+    m = mca.minibatch(0, 10, 4, 3)
+    assert list(np.flatnonzero(m)) == [0, 1, 2, 3]
+    assert list(np.flatnonzero(mca.minibatch(2, 10, 4, 3))) == [0, 1, 2, 3]
+    assert list(np.flatnonzero(mca.minibatch(3, 10, 4, 3))) == [4, 5, 6, 7]
+    assert list(np.flatnonzero(mca.minibatch(6, 10, 4, 3))) == [0, 1, 8, 9]
+    assert mca.minibatch(5, 10, 0, 1) is None
+    X, y, Ws = random_net((9, 7, 5), 60, 47, scale=1.2)
+    inc = IncrementalMLP(MLPState(Ws), X, y, "tanh")
+    full = FullMLP(MLPState(Ws), X, y, "tanh")
+    c = inc.candidate(1, 2, 0, 0, 0.3)
+    rows, dl, _ = inc.sample_changes(c)
+    per = np.zeros(60)
+    per[rows] = dl
+    inc.subset = mca.minibatch(4, 60, 25, 2)
+    d, _ = inc.delta(c)
+    inc.subset = None
+    assert abs(d - per[mca.minibatch(4, 60, 25, 2)].mean()) <= 1e-15
+    # a run with minibatches: decisions on the window, L over every sample
+    recs = mca.run(inc, 0, 100, 4, 1, 2, 0.3, scan_all=True, subset=(25, 2))
+    assert any(r.chosen >= 0 for r in recs)
+    fresh = FullMLP(MLPState(inc.state.weights), X, y, "tanh")
+    assert abs(fresh.loss() - inc.loss()) <= 1e-12
