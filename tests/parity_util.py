@@ -160,11 +160,18 @@ def check_step(stats, gpu_dl, ref_dl, mags, kappas, thetas, accept_ties, chosen_
 
 def _oracle_step(ref, cfg, t, K, bound, beta, n_prune, subset=(0, 1)):
     """The oracle's view of step t: candidates, loss changes (+inf for those a
-    weight bound rejects unevaluated, Eq. 1), sizes, thresholds, decision."""
-    L_t, rc, dls, mags, th, chosen = omca.evaluate_all(
-        ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-        getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune,
-        subset=subset)
+    weight bound rejects unevaluated, Eq. 1), sizes, thresholds, decision.
+    `ref` is one oracle model or a pool of replicas (tests/oracle_pool.py)."""
+    if hasattr(ref, "evaluate_all"):
+        assert not subset[0]
+        L_t, rc, dls, mags, th, chosen = ref.evaluate_all(
+            t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
+            getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune)
+    else:
+        L_t, rc, dls, mags, th, chosen = omca.evaluate_all(
+            ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
+            getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune,
+            subset=subset)
     bounded = [_bounded(ref, c, bound) for c in rc]
     if bound > 0:
         dls = [math.inf if b else d for b, d in zip(bounded, dls)]
@@ -237,7 +244,8 @@ def replay_trace(ref, cfg, t0, chosen, dloss, K, stats=None, beta=0.0, kappa=Non
 
 def assert_state_equal(ctx, ref):
     params, codes = ctx.params()
-    for l, (a, b) in enumerate(zip(params, ref.state.weights)):
+    weights = ref.state_weights() if hasattr(ref, "state_weights") else ref.state.weights
+    for l, (a, b) in enumerate(zip(params, weights)):
         assert a.tobytes() == b.tobytes(), f"weights of layer {l} differ"
     if codes is not None:
         for l, (a, b) in enumerate(zip(codes, ref.state.codes)):
