@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define MCA_ABI_VERSION 2
+#define MCA_ABI_VERSION 3
 #define MCA_MAX_LAYERS 32  /* maximum number of MLP weight matrices */
 #define MCA_MAX_CLASSES 16 /* maximum MLP output width (logits kept in registers) */
 
@@ -65,6 +65,7 @@ extern "C" {
 /* transfer functions of hidden MLP layers (Sec. 2) */
 #define MCA_ACT_TANH 0
 #define MCA_ACT_GAUSS 1 /* exp(-gamma z^2) */
+#define MCA_ACT_RELU 2  /* max(0, z) */
 
 /* weight modes */
 #define MCA_WEIGHTS_FP32 0    /* continuous fp32 weights, w -> fl32(w + d) (Eq. 1) */
@@ -73,6 +74,12 @@ extern "C" {
 /* selection rules */
 #define MCA_RULE_GREEDY 0     /* accept iff dL < 0 (dL <= 0 with accept_ties) (Eq. 6) */
 #define MCA_RULE_METROPOLIS 1 /* accept with probability min{1, exp(-beta dL)} (Eq. 7) */
+
+/* what one candidate changes (MLPs) */
+#define MCA_MUTATE_SINGLE 0         /* one parameter (Eq. 1) */
+#define MCA_MUTATE_CHANNEL_REDRAW 1 /* a channel: one weight per layer on an input-to-output
+                                     * path, each re-drawn as fl32(sqrt(8 / fan_in)) * r (Sec. 2.3) */
+#define MCA_MUTATE_CHANNEL_ZERO 2   /* a channel whose weights are all set to zero (Sec. 2.3) */
 
 /* how a candidate picks its parameter */
 #define MCA_PICK_WEIGHT 0 /* uniform over all parameters */
@@ -116,6 +123,14 @@ typedef struct mca_net_desc {
    * loss is the mean over every sample. */
   int64_t subset_size;
   int64_t subset_period;
+  /* MCA_MUTATE_*.  Channel mutations (Sec. 2.3) need an MLP of fp32 weights
+   * with L >= 2 whose hidden layers are all 256, 512 or 1024 wide, every
+   * sample in each step (subset_size 0) and no pruning candidates
+   * (n_prune 0); their candidates are mca_channel records (mca_propose_channels,
+   * mca_eval_channels), scored against the committed state like single
+   * mutations and committed, rolled back and run (mca_run_steps) the same way. */
+  int32_t mutation;
+  int32_t reserved0;
 } mca_net_desc;
 
 /* mca_cand.flags */
@@ -131,6 +146,18 @@ typedef struct mca_cand {
   int32_t code;  /* ternary: the new code (-1, 0, 1); continuous: 0 */
   int32_t flags; /* MCA_CAND_* */
 } mca_cand;
+
+/* One proposed channel mutation (Sec. 2.3): units[m] is the path's unit in
+ * layer m (units[0] an input, units[L] a class; entries past L unused); the
+ * path's weight of layer m is W_m[units[m + 1]][units[m]] and becomes
+ * w_new[m].  Drawn from the Philox blocks at counters (t, k, 2 + b, 0),
+ * words in order: word m gives units[m] = floor(word * n_m / 2^64), m = 0..L;
+ * word L + 1 + m re-draws w_new[m] = fl32(fl32(sqrt(8 / n_m)) * r) with
+ * r = (word >> 40) * 2^-23 - 1 (zero for MCA_MUTATE_CHANNEL_ZERO).  260 bytes. */
+typedef struct mca_channel {
+  int32_t units[MCA_MAX_LAYERS + 1];
+  float w_new[MCA_MAX_LAYERS];
+} mca_channel;
 
 /* Data set.  MLP: x is [n_samples][n_0] fp32 row-major, y the labels in
  * [0, n_L).  Transformer: tokens is [n_seq][ctx] int32, y the next-symbol
@@ -173,7 +200,7 @@ int mca_abi_version(void);
 
 /* sizeof of the ABI structs, so bindings can check their mirrors:
  * which = 0 mca_net_desc, 1 mca_cand, 2 mca_data, 3 mca_stats, 4 mca_trace,
- * 5 mca_timing; 0 for any other value. */
+ * 5 mca_timing, 6 mca_channel; 0 for any other value. */
 size_t mca_struct_size(int32_t which);
 
 /* Device workspace bytes for a net, n_samples and at most k_max candidates per
@@ -211,6 +238,24 @@ int mca_propose(mca_ctx* ctx, uint64_t step, int32_t K, mca_cand* out_host);
  * marks the batch pending (MCA_ESTATE if one is already pending).  Synchronises. */
 int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
                     double* loss_out, double* dloss_out);
+
+/* Channel contexts (mutation MCA_MUTATE_CHANNEL_*, Sec. 2.3): candidates
+ * k = 0..K-1 of step `step` as channel records (the draw described at
+ * mca_channel), 1 <= K <= k_max.  Pure with respect to the committed state.
+ * MCA_ESTATE while a batch is pending, MCA_EINVAL on a single-mutation
+ * context.  Synchronises. */
+int mca_propose_channels(mca_ctx* ctx, uint64_t step, int32_t K, mca_channel* out_host);
+
+/* Channel contexts: score K channel records against the committed state, as
+ * mca_eval_losses does for single mutations: dL_k = L(W with every path
+ * weight of channel k replaced) - L(W), computed on every sample from the
+ * cached fields (the first field's path column, then each later layer's
+ * dense change plus its own path weight's change).  A channel with any
+ * |w_new| >= bound gets +inf.  Records are validated (units in range, finite
+ * values) before anything is enqueued.  Marks the batch pending; commit it
+ * with mca_commit(k) or drop it with mca_rollback.  Synchronises. */
+int mca_eval_channels(mca_ctx* ctx, const mca_channel* chans_host, int32_t K,
+                      double* loss_out, double* dloss_out);
 
 /* Accept candidate k of the pending batch (Eq. 6): write the new parameter and
  * update the cached local fields and per-sample losses in place; L += dL_k.

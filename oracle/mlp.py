@@ -2,7 +2,7 @@
 
 Network (Sec. 3.6 notation): z_l = W_l a_{l-1}, a_l = phi(z_l) for hidden
 layers, a_0 = x, and the last local field z_L is the logit vector.  phi is
-tanh or the Gaussian exp(-gamma z^2) (Sec. 2).  The loss is the average
+tanh, ReLU max(0, z) or the Gaussian exp(-gamma z^2) (Sec. 2).  The loss is the average
 cross-entropy over the full sample set (Sec. 2; Eq. 2 with R(W) = 0).
 
 Two evaluators of the loss after a single-weight mutation:
@@ -22,19 +22,28 @@ Two evaluators of the loss after a single-weight mutation:
   ``FullMLP`` (where the change is large) and against a long-double full
   recomputation (where it is small).
 
+Both also evaluate a channel mutation (Sec. 2.3): one weight per layer on an
+input-to-output path changes at once.  The definition replaces all of them
+and recomputes; the incremental form moves column units[1] of the first
+field, then every later field by the dense change of its input plus the
+point change of its own path weight (W'_m a'_m - W_m a_m =
+W_m (a'_m - a_m) + (w'_m - w_m) a'_m[units[m]] at unit units[m + 1]).
+
 Arrays are sample-major (N x units) here; all arithmetic is float64.
 """
 from __future__ import annotations
 
 import numpy as np
 
-from .philox import Candidate, decode, draw
+from .philox import Candidate, Channel, channel_words, decode, decode_channel, draw
 
 
 def phi(z, act: str, gamma: float = 1.0):
-    """Transfer function (Sec. 2): tanh, or the Gaussian exp(-gamma z^2)."""
+    """Transfer function (Sec. 2): tanh, ReLU max(0, z), or the Gaussian exp(-gamma z^2)."""
     if act == "tanh":
         return np.tanh(z)
+    if act == "relu":
+        return np.maximum(z, 0.0)
     if act == "gauss":
         return np.exp(-gamma * z * z)
     raise ValueError(act)
@@ -44,9 +53,14 @@ def dphi(z, dz, act: str, gamma: float = 1.0):
     """phi(z + dz) - phi(z) without cancellation, from two textbook identities:
     tanh a - tanh b = sinh(a - b) / (cosh a cosh b), and
     exp(-g a^2) - exp(-g b^2) = exp(-g b^2) expm1(-g (a - b)(a + b)).
+    For ReLU the change is dz itself where both fields are positive, zero
+    where neither is, and the one non-zero activation where they straddle 0.
     Exactly zero where dz is zero."""
     if act == "tanh":
         return np.sinh(dz) / (np.cosh(z) * np.cosh(z + dz))
+    if act == "relu":
+        zn = z + dz
+        return np.where((z > 0) & (zn > 0), dz, np.maximum(zn, 0.0) - np.maximum(z, 0.0))
     if act == "gauss":
         arg = -gamma * dz * (2.0 * z + dz)
         with np.errstate(over="ignore", invalid="ignore"):
@@ -57,10 +71,12 @@ def dphi(z, dz, act: str, gamma: float = 1.0):
 
 
 def dphi_dz(z, act: str, gamma: float = 1.0):
-    """phi'(z)."""
+    """phi'(z) (ReLU: the step function, 0 at z = 0)."""
     if act == "tanh":
         t = np.tanh(z)
         return 1.0 - t * t
+    if act == "relu":
+        return (np.asarray(z) > 0).astype(np.float64)
     return -2.0 * gamma * z * np.exp(-gamma * z * z)
 
 
@@ -132,6 +148,20 @@ class MLPState:
             return np.float32(np.float32(c.code) * self.scales[c.layer])
         return np.float32(self.weights[c.layer][c.j, c.i] + c.d)
 
+    def apply_channel(self, ch: Channel):
+        for m, w in enumerate(ch.w_new):
+            self.weights[m][ch.units[m + 1], ch.units[m]] = np.float32(w)
+
+    def with_channel(self, ch: Channel):
+        """The weight list with the channel's entries replaced (copies of the
+        changed layers only)."""
+        ws = list(self.weights)
+        for m, w in enumerate(ch.w_new):
+            wl = ws[m].copy()
+            wl[ch.units[m + 1], ch.units[m]] = np.float32(w)
+            ws[m] = wl
+        return ws
+
     def apply(self, c: Candidate):
         w = self.new_value(c)
         self.weights[c.layer][c.j, c.i] = w
@@ -147,9 +177,19 @@ class _Base:
         self.act = act
         self.gamma = float(gamma)
 
-    def candidate(self, seed, tag, t, k, delta, mode="weight", prune=False) -> Candidate:
+    @property
+    def widths(self):
+        ws = self.state.weights
+        return (ws[0].shape[1],) + tuple(w.shape[0] for w in ws)
+
+    def candidate(self, seed, tag, t, k, delta, mode="weight", prune=False):
         """Candidate k of step t; with prune, the same draw's weight is set to
-        zero instead (d = -w, ternary code 0)."""
+        zero instead (d = -w, ternary code 0).  Modes "channel_redraw" and
+        "channel_zero" draw a channel mutation (Sec. 2.3) instead."""
+        if mode.startswith("channel_"):
+            L = len(self.state.weights)
+            return decode_channel(channel_words(seed, tag, t, k, 2 * L + 1), self.widths,
+                                  mode[len("channel_"):])
         c = decode(draw(seed, tag, t, k), self.state.shapes, delta, mode,
                    self.state.codes, self.state.scales)
         if prune:
@@ -178,13 +218,17 @@ class FullMLP(_Base):
         ws[c.layer] = wl
         return self.loss_of(ws)
 
-    def delta(self, c: Candidate):
+    def delta(self, c):
         """(L(W') - L(W), A): the definition of the loss change, and the size
-        A of its first-order terms over the logit change (see ce_change)."""
-        ws = list(self.state.weights)
-        wl = ws[c.layer].copy()
-        wl[c.j, c.i] = self.state.new_value(c)
-        ws[c.layer] = wl
+        A of its first-order terms over the logit change (see ce_change).
+        c is a single-parameter Candidate or a Channel."""
+        if isinstance(c, Channel):
+            ws = self.state.with_channel(c)
+        else:
+            ws = list(self.state.weights)
+            wl = ws[c.layer].copy()
+            wl[c.j, c.i] = self.state.new_value(c)
+            ws[c.layer] = wl
         if getattr(self, "_z0", None) is None:  # the committed logits, kept until a commit
             W0 = [w.astype(np.float64) for w in self.state.weights]
             self._z0 = forward_fields(W0, self.X, self.act, self.gamma)[-1]
@@ -197,7 +241,10 @@ class FullMLP(_Base):
     def commit(self, c: Candidate, loss_after: float):
         """Apply c; the loss of the new state is the one just evaluated for it
         (the same deterministic recomputation of the same weights)."""
-        self.state.apply(c)
+        if isinstance(c, Channel):
+            self.state.apply_channel(c)
+        else:
+            self.state.apply(c)
         self._L = float(loss_after)
         self._z0 = None
 
@@ -309,13 +356,63 @@ class IncrementalMLP(_Base):
         mag = mag + np.abs(dl) * self._cache_sensitivity(c, rows, dcol) / 16.0
         return rows, dl, mag
 
+    def _channel_changes(self, ch: Channel):
+        """Field changes under channel ch on every sample (Sec. 2.3): {m: the
+        change of z_m (for the first layer: of column units[1] only)}, and
+        the absolute terms of the logit changes."""
+        W = self.state.weights
+        nL = len(self.Z)
+        u = ch.units
+        d = [np.float64(ch.w_new[m]) - np.float64(W[m][u[m + 1], u[m]]) for m in range(nL)]
+        out = {}
+        col = d[0] * self.X[:, u[0]]  # column u[1] of the first field
+        out[0] = col
+        if nL == 1:
+            dz = np.zeros(self.Z[0].shape)
+            dz[:, u[1]] = col
+            out["logits"], out["abs"] = dz, np.abs(dz)
+            return out
+        # the first layer's new activation of the path unit and its change
+        zc = self.Z[0][:, u[1]]
+        a_path = phi(zc + col, self.act, self.gamma)
+        da_col = dphi(zc, col, self.act, self.gamma)
+        da = None  # dense activation change of the layer before (m >= 2)
+        for m in range(1, nL):
+            Wm = W[m].astype(np.float64)
+            if m == 1:
+                dz = np.outer(da_col, Wm[:, u[1]])
+                absz = np.outer(np.abs(da_col), np.abs(Wm[:, u[1]]))
+            else:
+                dz = da @ Wm.T
+                absz = np.abs(da) @ np.abs(Wm).T if m == nL - 1 else None
+            point = d[m] * a_path
+            dz[:, u[m + 1]] += point
+            out[m] = dz
+            if m == nL - 1:
+                absz[:, u[m + 1]] += np.abs(point)
+                out["logits"], out["abs"] = dz, absz
+                return out
+            z = self.Z[m]
+            da = dphi(z, dz, self.act, self.gamma)
+            a_path = phi(z[:, u[m + 1]] + dz[:, u[m + 1]], self.act, self.gamma)
+
+    def channel_sample_changes(self, ch: Channel):
+        """(per-sample loss changes, their first-order sizes) of channel ch."""
+        out = self._channel_changes(ch)
+        return ce_change(self._softmax(), out["logits"], self.y, out["abs"])
+
     # minibatch (Sec. 2.2): a boolean mask over the samples, or None for all
     subset = None
 
     def delta(self, c: Candidate):
         """(dL, A): the loss change of candidate c (Eq. 2 difference), from the
         field changes, and the mean size A of its first-order terms; over the
-        current minibatch when one is set."""
+        current minibatch when one is set.  c may be a Channel (Sec. 2.3)."""
+        if isinstance(c, Channel):
+            assert self.subset is None, "channel mutations score every sample"
+            dl, mag = self.channel_sample_changes(c)
+            N = self.X.shape[0]
+            return float(dl.sum()) / N, float(mag.sum()) / N
         rows, dl, mag = self.sample_changes(c)
         if self.subset is not None:
             keep = self.subset[rows]
@@ -330,6 +427,16 @@ class IncrementalMLP(_Base):
     def commit(self, c: Candidate, loss_after: float):
         """Apply c: every cached field moves by its change; the committed loss
         moves by the candidate's loss change (loss_after = L + dL)."""
+        if isinstance(c, Channel):
+            out = self._channel_changes(c)
+            dl, _ = ce_change(self._softmax(), out["logits"], self.y)
+            self.Z[0][:, c.units[1]] += out[0]
+            for m in range(1, len(self.Z)):
+                self.Z[m] += out[m]
+            self._P = None
+            self.state.apply_channel(c)
+            self.L = self.L + float(dl.sum()) / self.X.shape[0]
+            return
         rows, dcol, later = self._changes(c)
         dl, _ = ce_change(self._softmax()[rows], self._logit_change(c, rows, dcol, later),
                           self.y[rows])

@@ -21,10 +21,21 @@ Decoding of one 4x64-bit block (w0, w1, w2, w3):
 
 The Metropolis rule (Eq. 7) needs one more uniform per candidate: word w0
 of the block at counter (t, k, 1, 0), U = (w0 >> 11) * 2^-53 in [0, 1).
+
+A channel mutation (Sec. 2.3) draws one unit per layer of the net, input to
+output, and for the re-draw scheme one value per weight on that path.  Its
+words are those of the blocks at counters (t, k, 2 + b, 0), b = 0, 1, ...,
+taken in order (four per block): word m picks the path's unit of layer m,
+units[m] = floor(word_m * n_m / 2^64), m = 0..L (units[L] a class); word
+L + 1 + m re-draws the weight of layer m on the path as
+fl32(a_m * r), r = unit_r(word), a_m = fl32(sqrt(8 / n_m)) the He amplitude
+of its fan-in (the initialisation scale of Sec. 2.2).
 """
 from __future__ import annotations
 
 from dataclasses import dataclass
+
+import math
 
 import numpy as np
 
@@ -143,3 +154,46 @@ def decode(words, shapes, delta: float, mode: str = "weight",
     s = np.float32(scales[layer])
     d = np.float32(np.float32(new) * s - np.float32(cur) * s)
     return Candidate(flat, layer, j, i, d, new)
+
+
+@dataclass(frozen=True)
+class Channel:
+    """A multi-parameter channel mutation (Sec. 2.3): one weight per layer on a
+    path from an input to an output unit.  units[m] is the path's unit in
+    layer m (units[0] an input, units[L] a class), so the path's weight of
+    layer m is W_m[units[m + 1], units[m]]; w_new[m] is its proposed fp32 value."""
+    units: tuple
+    w_new: tuple
+
+
+def channel_words(seed: int, tag: int, t: int, k: int, n: int):
+    """The first n words of channel candidate k of step t: blocks at counters
+    (t, k, 2 + b, 0) under key (seed, tag), four words each, in order."""
+    out = []
+    b = 0
+    while len(out) < n:
+        out.extend(philox4x64((t, k, 2 + b, 0), (seed, tag)))
+        b += 1
+    return out[:n]
+
+
+def he_amplitude(fan_in: int) -> np.float32:
+    """fl32(sqrt(8 / fan_in)): the amplitude of a re-drawn weight (Sec. 2.2's
+    He initialisation scale, used by Sec. 2.3's re-draw scheme)."""
+    return np.float32(math.sqrt(8.0 / fan_in))
+
+
+def decode_channel(words, widths, scheme: str) -> Channel:
+    """A channel of a net with widths (n_0 .. n_L) from 2L + 1 words: the path
+    (one unit per layer), then, for scheme "redraw", the new weights
+    fl32(a_m * r_m); for scheme "zero" every path weight becomes 0."""
+    L = len(widths) - 1
+    units = tuple(mulhi64(words[m], widths[m]) for m in range(L + 1))
+    if scheme == "zero":
+        w_new = tuple(np.float32(0.0) for _ in range(L))
+    elif scheme == "redraw":
+        w_new = tuple(np.float32(he_amplitude(widths[m]) * unit_r(words[L + 1 + m]))
+                      for m in range(L))
+    else:
+        raise ValueError(scheme)
+    return Channel(units, w_new)

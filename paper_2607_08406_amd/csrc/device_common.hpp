@@ -59,6 +59,9 @@ struct NetDev {
   float* prob;                        // softmax of the logits, [C][Ns] (unit-major like Z)
   const int32_t* y;
   float* WT;                          // L >= 3: W_{L-2} transposed ([n_{L-2}][n_{L-1}]), else null
+  int32_t mutation;                   // MCA_MUTATE_*
+  int32_t pad1;
+  float chan_amp[MCA_MAX_LAYERS];     // fl32(sqrt(8 / n_l)): amplitude of a re-drawn channel weight
 };
 
 // Kernels index the pointer and size arrays of NetDev with runtime values (the
@@ -164,6 +167,7 @@ __device__ __forceinline__ float fast_tanh(float z) {
 
 __device__ __forceinline__ float act_fn(float z, int act, float gamma) {
   if (act == MCA_ACT_TANH) return fast_tanh(z);
+  if (act == MCA_ACT_RELU) return fmaxf(z, 0.0f);
   float t = gamma * z;
   t = t * z;
   return fast_exp(-t);
@@ -212,8 +216,17 @@ __device__ __forceinline__ float dgauss(float z, float dz, float g) {
   return (x > 30.0f) ? far : near;
 }
 
+// max(0, z + dz) - max(0, z): dz itself where both fields are positive (no
+// rounding), zero where neither is, the one non-zero activation where they
+// straddle zero.  Exactly zero where dz is zero.
+__device__ __forceinline__ float drelu(float z, float dz) {
+  const float zn = z + dz;
+  return (z > 0.0f && zn > 0.0f) ? dz : fmaxf(zn, 0.0f) - fmaxf(z, 0.0f);
+}
+
 // phi(z + dz) - phi(z) for the net's transfer function.
 __device__ __forceinline__ float dphi(float z, float dz, int act, float gamma) {
+  if (act == MCA_ACT_RELU) return drelu(z, dz);
   return (act == MCA_ACT_TANH) ? dtanh(z, dz) : dgauss(z, dz, gamma);
 }
 

@@ -18,6 +18,7 @@
 #include "mlp_kernels.hpp"
 #include "slab_kernels.hpp"
 #include "chain_kernels.hpp"
+#include "channel_kernels.hpp"
 #include "tf_kernels.hpp"
 
 using mca::Aux;
@@ -77,7 +78,8 @@ struct Layout {
   size_t wt = 0, pslab = 0;  // three-layer nets: W_1 transposed, first-layer tile sums
   size_t cols = 0, nnz = 0;  // nonzero entries of layer L-3 candidates' W_{L-2} columns
   size_t rows = 0, rda = 0, rcnt = 0, pchain = 0;  // deep nets: affected samples, tile sums
-  int nchain = 0;
+  size_t chans = 0, pchan = 0;                      // channel mutations: records, tile sums
+  int nchain = 0, nchan = 0;
   int nslab = 0;
   int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
@@ -115,7 +117,11 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   for (int l = 0; l < L; ++l)
     if ((int64_t)net->widths[l] * net->widths[l + 1] >= (int64_t)1 << 31)
       return "a weight matrix has 2^31 or more entries";
-  if (net->act != MCA_ACT_TANH && net->act != MCA_ACT_GAUSS) return "unknown transfer function";
+  if (net->act != MCA_ACT_TANH && net->act != MCA_ACT_GAUSS && net->act != MCA_ACT_RELU)
+    return "unknown transfer function";
+  if (net->mutation != MCA_MUTATE_SINGLE && net->mutation != MCA_MUTATE_CHANNEL_REDRAW &&
+      net->mutation != MCA_MUTATE_CHANNEL_ZERO)
+    return "unknown mutation kind";
   if (net->act == MCA_ACT_GAUSS && !(std::isfinite(net->gamma) && net->gamma > 0.f))
     return "gamma must be finite and positive";
   if (net->weight_mode != MCA_WEIGHTS_FP32 && net->weight_mode != MCA_WEIGHTS_TERNARY)
@@ -132,6 +138,18 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   {
     std::string m = check_selection(net, n_samples, code);
     if (!m.empty()) return m;
+  }
+  if (net->mutation != MCA_MUTATE_SINGLE) {
+    *code = MCA_EUNSUPPORTED;
+    if (L < 2) return "channel mutations need at least one hidden layer";
+    if (net->weight_mode != MCA_WEIGHTS_FP32) return "channel mutations take continuous weights";
+    for (int l = 1; l < L; ++l)
+      if (net->widths[l] != net->widths[1] || !mca::channel_width_ok(net->widths[l]))
+        return "channel mutations need every hidden layer 256, 512 or 1024 units wide";
+    if (net->n_prune != 0) return "channel mutations take no pruning candidates";
+    if (net->subset_size != 0) return "channel mutations score every sample";
+    *code = MCA_OK;
+    return "";
   }
   if (L >= 3 && net->widths[L - 1] > mca::kSlabMaxUnits) {
     *code = MCA_EUNSUPPORTED;
@@ -290,6 +308,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.state = take(kStateBlock);
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
+  const bool chan = net->mutation != MCA_MUTATE_SINGLE;
   if (L >= 3) {
     lo.wt = take((size_t)net->widths[L - 2] * net->widths[L - 1] * sizeof(float));
     const int T = mca::slab_tile(net->widths[L]);
@@ -298,12 +317,17 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     lo.cols = take((size_t)k_max * net->widths[L - 1] * sizeof(uint64_t));
     lo.nnz = take((size_t)k_max * sizeof(int32_t));
   }
-  if (L >= 4) {
+  if (L >= 4 && !chan) {
     lo.nchain = (int)((N + mca::kChainT - 1) / mca::kChainT);
     lo.rows = take((size_t)k_max * N * sizeof(int32_t));
     lo.rda = take((size_t)k_max * N * sizeof(float));
     lo.rcnt = take((size_t)k_max * sizeof(int32_t));
     lo.pchain = take((size_t)k_max * lo.nchain * sizeof(float));
+  }
+  if (net->mutation != MCA_MUTATE_SINGLE) {
+    lo.nchan = mca::channel_tiles(N, net->widths[1]);
+    lo.chans = take((size_t)k_max * sizeof(mca_channel));
+    lo.pchan = take((size_t)k_max * lo.nchan * sizeof(float));
   }
   // persistent loop: tiles of T samples (16..64), one workgroup each; the
   // partial sums are sized for the smallest tile
@@ -346,6 +370,9 @@ struct mca_ctx {
   float* rda = nullptr;
   int* rcnt = nullptr;
   float* pchain = nullptr;
+  bool chan = false;             // candidates are channel mutations (Sec. 2.3)
+  mca_channel* chans = nullptr;  // their records
+  float* pchan = nullptr;        // their tile sums
   double* dl = nullptr;
   double* bsum = nullptr;
   DevState* st = nullptr;
@@ -585,6 +612,9 @@ Bufs ctx_bufs(const mca_ctx* ctx) {
 }
 
 hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
+  if (ctx->chan)
+    return mca::launch_channel_propose(ctx->net, step, use_dev_t, ctx->st, K, ctx->chans,
+                                       ctx->cands, ctx->aux, ctx->stream);
   if (ctx->tf)
     return mca::tf_launch_propose(ctx->tfd, ctx->tfh, step, use_dev_t, ctx->st, K, ctx->cands,
                                   ctx->aux, ctx->stream);
@@ -593,6 +623,8 @@ hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
 }
 
 hipError_t prepare_into(mca_ctx* ctx, const Bufs& b, int K) {
+  if (ctx->chan)
+    return mca::launch_channel_prepare(ctx->net, ctx->chans, K, b.cands, b.aux, ctx->stream);
   if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, b.cands, K, b.aux, ctx->stream);
   return mca::launch_prepare(ctx->net, b.cands, K, b.aux, ctx->fmask, b.cmask, ctx->stream);
 }
@@ -601,6 +633,9 @@ hipError_t prepare_dev(mca_ctx* ctx, int K) { return prepare_into(ctx, ctx_bufs(
 // Scores the K staged candidates: the column kernel for the last two layers,
 // the tile kernel for layer L-3, the dense chain for layers 0..L-4.
 hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
+  if (ctx->chan)
+    return mca::launch_channel(net, ctx->chans, b.aux, K, ctx->pchan, ctx->lo.nchan, -2,
+                               ctx->st, b.dl, ctx->stream);
   if (ctx->tf)
     return mca::tf_launch_eval(ctx->tfd, ctx->tfh, b.cands, b.aux, K, false, b.partial,
                                ctx->tf_nblk, ctx->stream);
@@ -620,6 +655,15 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
 
 hipError_t select_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K, bool do_select,
                        int32_t* trc, double* trd) {
+  if (ctx->chan) {
+    // every channel has one source of tile sums (an L = 0 view of the net
+    // selects it)
+    NetDev one = net;
+    one.L = 0;
+    return mca::launch_select(one, ctx->pchan, ctx->lo.nchan, b.cands, nullptr, 0, nullptr, 0,
+                              b.aux, K, b.dl, ctx->st, do_select, trc, trd, kTraceCap,
+                              ctx->stream);
+  }
   if (ctx->tf)
     return mca::launch_select(net, b.partial, ctx->tf_nblk, b.cands, nullptr, 0, nullptr, 0,
                               b.aux, K, b.dl, ctx->st, do_select, trc, trd, kTraceCap,
@@ -636,6 +680,9 @@ hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, in
 // Commits candidate k (k < 0: the device decision); each kernel applies only
 // the candidates of the layers it scores.
 hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
+  if (ctx->chan)
+    return mca::launch_channel(net, ctx->chans, ctx->aux, 0, ctx->pchan, ctx->lo.nchan, k,
+                               ctx->st, ctx->dl, ctx->stream);
   if (ctx->tf)
     return mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, k,
                                  false, ctx->bsum, ctx->stream);
@@ -787,6 +834,7 @@ size_t mca_struct_size(int32_t which) {
     case 3: return sizeof(mca_stats);
     case 4: return sizeof(mca_trace);
     case 5: return sizeof(mca_timing);
+    case 6: return sizeof(mca_channel);
     default: return 0;
   }
 }
@@ -858,6 +906,8 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.tag = net->stream_tag;
   nd.N = N;
   nd.Ns = lo.Ns;
+  nd.mutation = net->mutation;
+  for (int l = 0; l < L; ++l) nd.chan_amp[l] = (float)std::sqrt(8.0 / (double)net->widths[l]);
   int64_t off = 0;
   for (int l = 0; l <= L; ++l) nd.widths[l] = net->widths[l];
   for (int l = 0; l < L; ++l) {
@@ -878,10 +928,15 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   ctx->pslab = (L >= 3) ? (float*)(ws + lo.pslab) : nullptr;
   ctx->cols = (L >= 3) ? (uint64_t*)(ws + lo.cols) : nullptr;
   ctx->nnz = (L >= 3) ? (int*)(ws + lo.nnz) : nullptr;
-  ctx->rows = (L >= 4) ? (int*)(ws + lo.rows) : nullptr;
-  ctx->rda = (L >= 4) ? (float*)(ws + lo.rda) : nullptr;
-  ctx->rcnt = (L >= 4) ? (int*)(ws + lo.rcnt) : nullptr;
-  ctx->pchain = (L >= 4) ? (float*)(ws + lo.pchain) : nullptr;
+  ctx->chan = net->mutation != MCA_MUTATE_SINGLE;
+  const bool deep = L >= 4 && !ctx->chan;
+  ctx->rows = deep ? (int*)(ws + lo.rows) : nullptr;
+  ctx->rda = deep ? (float*)(ws + lo.rda) : nullptr;
+  ctx->rcnt = deep ? (int*)(ws + lo.rcnt) : nullptr;
+  ctx->pchain = deep ? (float*)(ws + lo.pchain) : nullptr;
+  ctx->chans = ctx->chan ? (mca_channel*)(ws + lo.chans) : nullptr;
+  ctx->pchan = ctx->chan ? (float*)(ws + lo.pchan) : nullptr;
+  if (ctx->chan) ctx->use_loop = false;
   ctx->cands = (mca_cand*)(ws + lo.cands);
   ctx->aux = (Aux*)(ws + lo.aux);
   ctx->fmask = lo.ntiles_ev <= 64 ? (uint64_t*)(ws + lo.fmask) : nullptr;
@@ -943,6 +998,7 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
 
 int mca_propose(mca_ctx* ctx, uint64_t step, int32_t K, mca_cand* out_host) {
   MCA_LIVE(ctx);
+  if (ctx->chan) return fail(ctx, MCA_EINVAL, "a channel context proposes mca_channel records (mca_propose_channels)");
   if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
   if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
   // the proposal reuses the candidate buffers of a pending batch
@@ -956,6 +1012,7 @@ int mca_propose(mca_ctx* ctx, uint64_t step, int32_t K, mca_cand* out_host) {
 int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double* loss_out,
                     double* dloss_out) {
   MCA_LIVE(ctx);
+  if (ctx->chan) return fail(ctx, MCA_EINVAL, "a channel context scores mca_channel records (mca_eval_channels)");
   if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is already pending");
   if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
   if (cands_host == nullptr) return fail(ctx, MCA_EINVAL, "cands_host is NULL");
@@ -999,10 +1056,56 @@ int mca_rollback(mca_ctx* ctx) {
   return MCA_OK;
 }
 
+int mca_propose_channels(mca_ctx* ctx, uint64_t step, int32_t K, mca_channel* out_host) {
+  MCA_LIVE(ctx);
+  if (!ctx->chan) return fail(ctx, MCA_EINVAL, "not a channel context");
+  if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
+  if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is pending: commit or roll back first");
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_dev(ctx, step, false, K); }));
+  MCA_HIP(ctx, hipMemcpyAsync(out_host, ctx->chans, (size_t)K * sizeof(mca_channel), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MCA_OK;
+}
+
+int mca_eval_channels(mca_ctx* ctx, const mca_channel* chans_host, int32_t K, double* loss_out,
+                      double* dloss_out) {
+  MCA_LIVE(ctx);
+  if (!ctx->chan) return fail(ctx, MCA_EINVAL, "not a channel context");
+  if (ctx->pending) return fail(ctx, MCA_ESTATE, "a batch is already pending");
+  if (K < 1 || K > ctx->k_max) return fail(ctx, MCA_EINVAL, "K out of range [1, k_max]");
+  if (chans_host == nullptr) return fail(ctx, MCA_EINVAL, "chans_host is NULL");
+  const mca_net_desc& d = ctx->desc;
+  for (int k = 0; k < K; ++k) {
+    for (int m = 0; m <= d.n_layers; ++m)
+      if (chans_host[k].units[m] < 0 || chans_host[k].units[m] >= d.widths[m])
+        return fail(ctx, MCA_EINVAL, "channel unit out of range");
+    for (int m = 0; m < d.n_layers; ++m)
+      if (!std::isfinite(chans_host[k].w_new[m])) return fail(ctx, MCA_EINVAL, "channel weight is not finite");
+  }
+  MCA_HIP(ctx, hipMemcpyAsync(ctx->chans, chans_host, (size_t)K * sizeof(mca_channel), hipMemcpyHostToDevice, ctx->stream));
+  MCA_HIP(ctx, timed(ctx, 0, [&] { return prepare_dev(ctx, K); }));
+  MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, ctx->net, K); }));
+  MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, ctx->net, K, false, nullptr, nullptr); }));
+  std::vector<double> dl(K);
+  DevState s{};
+  MCA_HIP(ctx, hipMemcpyAsync(dl.data(), ctx->dl, (size_t)K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipMemcpyAsync(&s, ctx->st, sizeof s, hipMemcpyDeviceToHost, ctx->stream));
+  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  for (int k = 0; k < K; ++k) {
+    if (loss_out) loss_out[k] = s.L + dl[k];
+    if (dloss_out) dloss_out[k] = dl[k];
+  }
+  ctx->pending = true;
+  ctx->pending_K = K;
+  return MCA_OK;
+}
+
 int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
                             double* loss_out, double* dloss_out) {
   MCA_LIVE(ctx);
   if (ctx->tf) return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes MLP contexts");
+  if (ctx->chan) return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes single-mutation contexts");
   if (K < 1 || K > mca::kMaxK) return fail(ctx, MCA_EINVAL, "K out of range [1, 1024]");
   if (cands_host == nullptr) return fail(ctx, MCA_EINVAL, "cands_host is NULL");
   if (ctx->scratch_dev == nullptr) return fail(ctx, MCA_EDEVICE, "no scratch array on this device");

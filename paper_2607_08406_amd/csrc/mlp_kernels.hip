@@ -774,6 +774,9 @@ hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStre
     else if (net.act == MCA_ACT_TANH)
       hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
                          net.Ns, N, net.Z[l], net.Ns, net.gamma);
+    else if (net.act == MCA_ACT_RELU)
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_RELU>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
     else
       hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
                          net.Ns, N, net.Z[l], net.Ns, net.gamma);

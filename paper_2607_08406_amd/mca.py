@@ -24,7 +24,8 @@ MCA_MAX_CLASSES = 16
 MCA_OK, MCA_EINVAL, MCA_ESTATE, MCA_ENOSPACE = 0, -1, -2, -3
 MCA_EDEVICE, MCA_EPOISONED, MCA_EUNSUPPORTED = -4, -5, -6
 MCA_NET_MLP, MCA_NET_TRANSFORMER = 0, 1
-MCA_ACT_TANH, MCA_ACT_GAUSS = 0, 1
+MCA_ACT_TANH, MCA_ACT_GAUSS, MCA_ACT_RELU = 0, 1, 2
+MCA_MUTATE_SINGLE, MCA_MUTATE_CHANNEL_REDRAW, MCA_MUTATE_CHANNEL_ZERO = 0, 1, 2
 MCA_WEIGHTS_FP32, MCA_WEIGHTS_TERNARY = 0, 1
 MCA_PICK_WEIGHT, MCA_PICK_LAYER = 0, 1
 MCA_RULE_GREEDY, MCA_RULE_METROPOLIS = 0, 1
@@ -52,7 +53,8 @@ class mca_net_desc(ctypes.Structure):
                 ("n_head", ctypes.c_int32), ("d_mlp", ctypes.c_int32), ("ln_eps", ctypes.c_float),
                 ("accept_rule", ctypes.c_int32), ("n_prune", ctypes.c_int32),
                 ("beta", ctypes.c_double), ("subset_size", ctypes.c_int64),
-                ("subset_period", ctypes.c_int64)]
+                ("subset_period", ctypes.c_int64), ("mutation", ctypes.c_int32),
+                ("reserved0", ctypes.c_int32)]
 
 
 class mca_cand(ctypes.Structure):
@@ -64,6 +66,15 @@ class mca_cand(ctypes.Structure):
 CAND_DTYPE = np.dtype([("flat", "<i8"), ("layer", "<i4"), ("j", "<i4"), ("i", "<i4"),
                        ("d", "<f4"), ("code", "<i4"), ("flags", "<i4")])
 MCA_CAND_PRUNE = 1
+
+
+class mca_channel(ctypes.Structure):
+    _fields_ = [("units", ctypes.c_int32 * (MCA_MAX_LAYERS + 1)),
+                ("w_new", ctypes.c_float * MCA_MAX_LAYERS)]
+
+
+CHANNEL_DTYPE = np.dtype([("units", "<i4", (MCA_MAX_LAYERS + 1,)),
+                          ("w_new", "<f4", (MCA_MAX_LAYERS,))])
 
 
 class mca_data(ctypes.Structure):
@@ -87,7 +98,7 @@ class mca_timing(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * 8), ("launches", ctypes.c_uint64 * 8)]
 
 
-STRUCTS = [mca_net_desc, mca_cand, mca_data, mca_stats, mca_trace, mca_timing]
+STRUCTS = [mca_net_desc, mca_cand, mca_data, mca_stats, mca_trace, mca_timing, mca_channel]
 
 _P = ctypes.c_void_p
 _SIGNATURES = {
@@ -100,6 +111,8 @@ _SIGNATURES = {
     "mca_propose": (ctypes.c_int, [_P, ctypes.c_uint64, ctypes.c_int32, _P]),
     "mca_eval_losses": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
     "mca_eval_losses_noalloc": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
+    "mca_propose_channels": (ctypes.c_int, [_P, ctypes.c_uint64, ctypes.c_int32, _P]),
+    "mca_eval_channels": (ctypes.c_int, [_P, _P, ctypes.c_int32, _P, _P]),
     "mca_commit": (ctypes.c_int, [_P, ctypes.c_int32]),
     "mca_rollback": (ctypes.c_int, [_P]),
     "mca_set_option": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int64]),
@@ -169,13 +182,15 @@ def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta
              ternary_scales: Optional[Sequence[float]] = None, pick: str = "weight",
              bound: float = 0.0, accept_ties: bool = False, seed: int = 0,
              stream_tag: int = 0, beta: float = 0.0, n_prune: int = 0, subset_size: int = 0,
-             subset_period: int = 1) -> mca_net_desc:
+             subset_period: int = 1, mutation: str = "single") -> mca_net_desc:
     d = mca_net_desc()
     d.kind = MCA_NET_MLP
     d.n_layers = len(widths) - 1
     for n, w in enumerate(widths):
         d.widths[n] = int(w)
-    d.act = {"tanh": MCA_ACT_TANH, "gauss": MCA_ACT_GAUSS}[act]
+    d.act = {"tanh": MCA_ACT_TANH, "gauss": MCA_ACT_GAUSS, "relu": MCA_ACT_RELU}[act]
+    d.mutation = {"single": MCA_MUTATE_SINGLE, "channel_redraw": MCA_MUTATE_CHANNEL_REDRAW,
+                  "channel_zero": MCA_MUTATE_CHANNEL_ZERO}[mutation]
     d.gamma = gamma
     if ternary_scales is not None:
         d.weight_mode = MCA_WEIGHTS_TERNARY
@@ -287,6 +302,22 @@ def mca_eval_losses_noalloc(ctx, cands: np.ndarray):
     dloss = np.zeros(K)
     _check(load_library().mca_eval_losses_noalloc(ctx, cands.ctypes.data, K, loss.ctypes.data,
                                                   dloss.ctypes.data), ctx)
+    return loss, dloss
+
+
+def mca_propose_channels(ctx, step: int, K: int) -> np.ndarray:
+    out = np.zeros(K, dtype=CHANNEL_DTYPE)
+    _check(load_library().mca_propose_channels(ctx, step, K, out.ctypes.data), ctx)
+    return out
+
+
+def mca_eval_channels(ctx, chans: np.ndarray):
+    chans = np.ascontiguousarray(chans, dtype=CHANNEL_DTYPE)
+    K = len(chans)
+    loss = np.zeros(K)
+    dloss = np.zeros(K)
+    _check(load_library().mca_eval_channels(ctx, chans.ctypes.data, K, loss.ctypes.data,
+                                            dloss.ctypes.data), ctx)
     return loss, dloss
 
 
@@ -406,6 +437,12 @@ class Context:
 
     def eval_losses(self, cands):
         return mca_eval_losses(self.ctx, cands)
+
+    def propose_channels(self, step, K):
+        return mca_propose_channels(self.ctx, step, K)
+
+    def eval_channels(self, chans):
+        return mca_eval_channels(self.ctx, chans)
 
     def commit(self, k):
         mca_commit(self.ctx, k)

@@ -41,6 +41,13 @@ TIE = 1e-6
 U32 = 2.0 ** -24
 
 
+def cand_mode(cfg):
+    """How the config's candidates are drawn: a channel scheme (Sec. 2.3) or
+    the single-parameter pick."""
+    m = getattr(cfg, "mutation", "single")
+    return m if m.startswith("channel_") else getattr(cfg, "layer_pick", "weight")
+
+
 def mlp_kappa(widths, layer):
     """Rounding budget of an MLP candidate in `layer` (units of 2^-24 A_k):
     128 for the column, rank-1 and cross-entropy work with its tile sums,
@@ -84,7 +91,8 @@ def make_pair(cfg, w, k_max, oracle="incremental", bound=0.0, beta=0.0, n_prune=
                         ternary_scales=scales, pick=cfg.layer_pick,
                         accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
                         stream_tag=cfg.stream_tag, bound=bound, beta=beta, n_prune=n_prune,
-                        subset_size=subset[0], subset_period=subset[1])
+                        subset_size=subset[0], subset_period=subset[1],
+                        mutation=getattr(cfg, "mutation", "single"))
     ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=k_max, codes=w["codes"])
     cls = IncrementalMLP if oracle == "incremental" else FullMLP
     ref = cls(MLPState(w["weights"], w["codes"], scales), w["X"], w["y"], cfg.act, cfg.gamma)
@@ -113,7 +121,11 @@ def check_batch(stats, gpu_dl, ref, cfg, t, K, kappa=None, beta=0.0):
 
 
 def _bounded(ref, c, bound):
-    return bound > 0 and abs(float(ref.state.new_value(c))) >= bound
+    if bound <= 0:
+        return False
+    if hasattr(c, "units"):  # a channel: any path weight outside the bound
+        return any(abs(float(w)) >= bound for w in c.w_new)
+    return abs(float(ref.state.new_value(c))) >= bound
 
 
 def check_step(stats, gpu_dl, ref_dl, mags, kappas, thetas, accept_ties, chosen_gpu,
@@ -165,13 +177,12 @@ def _oracle_step(ref, cfg, t, K, bound, beta, n_prune, subset=(0, 1)):
     if hasattr(ref, "evaluate_all"):
         assert not subset[0]
         L_t, rc, dls, mags, th, chosen = ref.evaluate_all(
-            t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-            getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune)
+            t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta, cand_mode(cfg), cfg.accept_ties,
+            beta=beta, n_prune=n_prune)
     else:
         L_t, rc, dls, mags, th, chosen = omca.evaluate_all(
-            ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
-            getattr(cfg, "layer_pick", "weight"), cfg.accept_ties, beta=beta, n_prune=n_prune,
-            subset=subset)
+            ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta, cand_mode(cfg),
+            cfg.accept_ties, beta=beta, n_prune=n_prune, subset=subset)
     bounded = [_bounded(ref, c, bound) for c in rc]
     if bound > 0:
         dls = [math.inf if b else d for b, d in zip(bounded, dls)]
@@ -222,7 +233,7 @@ def replay_trace(ref, cfg, t0, chosen, dloss, K, stats=None, beta=0.0, kappa=Non
         L_t, rc, dls, mags, th, orc, bounded = _oracle_step(ref, cfg, t, K, bound, beta, n_prune,
                                                             subset)
         if kappa is None:
-            kap = [mlp_kappa(cfg.widths, c.layer) for c in rc]
+            kap = [mlp_kappa(cfg.widths, getattr(c, "layer", 0)) for c in rc]
         else:
             kap = [kappa(c) for c in rc]
         g = int(chosen[n])

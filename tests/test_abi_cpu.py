@@ -45,7 +45,7 @@ def test_struct_mirrors(binding):
         assert lib.mca_struct_size(n) == ctypes.sizeof(st)
     assert ctypes.sizeof(binding.mca_cand) == 32 == binding.CAND_DTYPE.itemsize
     assert lib.mca_struct_size(99) == 0
-    assert binding.mca_abi_version() == 2
+    assert binding.mca_abi_version() == 3
 
 
 def test_plan_sizes(binding):
@@ -129,3 +129,35 @@ def test_last_error_message(binding):
     with pytest.raises(binding.MCAError):
         binding.mca_plan(d, 1024, 5000)
     assert "k_max" in binding.mca_last_error(None)
+
+
+def test_plan_channel_rules(binding):
+    """Channel mutation (Sec. 2.3): hidden layers all 256, 512 or 1024 wide,
+    fp32 weights, no pruning candidates, every sample; deep nets of 512 or
+    1024 units plan in channel mode although single mutations do not."""
+    for w in (256, 512, 1024):
+        for mode in ("channel_redraw", "channel_zero"):
+            d = binding.mlp_desc((784, w, w, w, 10), "relu", mutation=mode)
+            assert binding.mca_plan(d, 8192, 16) > 0
+    assert binding.mca_plan(binding.mlp_desc((784, 512, 10), "relu", mutation="channel_zero"),
+                            1000, 4) > 0
+    bad = [
+        (binding.mlp_desc((784, 300, 300, 10), "relu", mutation="channel_redraw"), "MCA_EUNSUPPORTED"),
+        (binding.mlp_desc((784, 256, 512, 10), "relu", mutation="channel_redraw"), "MCA_EUNSUPPORTED"),
+        (binding.mlp_desc((784, 10), "relu", mutation="channel_redraw"), "MCA_EUNSUPPORTED"),
+        (binding.mlp_desc((784, 256, 10), "relu", mutation="channel_redraw", n_prune=2), "MCA_EUNSUPPORTED"),
+        (binding.mlp_desc((784, 256, 10), "relu", mutation="channel_redraw", subset_size=100), "MCA_EUNSUPPORTED"),
+        (binding.mlp_desc((784, 256, 10), "relu", ternary_scales=[0.1, 0.1], mutation="channel_zero"), "MCA_EUNSUPPORTED"),
+    ]
+    for d, code in bad:
+        with pytest.raises(binding.MCAError) as e:
+            binding.mca_plan(d, 1000, 4)
+        assert code in str(e.value)
+    d = binding.mlp_desc((784, 256, 10), "relu")
+    d.mutation = 9
+    with pytest.raises(binding.MCAError) as e:
+        binding.mca_plan(d, 1000, 4)
+    assert "MCA_EINVAL" in str(e.value)
+    # single mutations on a 512-wide deep net stay unsupported
+    with pytest.raises(binding.MCAError):
+        binding.mca_plan(binding.mlp_desc((784, 512, 512, 512, 10), "relu"), 1000, 4)

@@ -38,17 +38,18 @@ class MLPConfig:
     """
     name: str
     widths: Tuple[int, ...]
-    act: str                    # "tanh" or "gauss" (exp(-gamma z^2))
+    act: str                    # "tanh", "relu" or "gauss" (exp(-gamma z^2))
     n_samples: int
     delta: float                # mutation amplitude (learning rate of Eq. 1)
     K: int                      # candidates scored per step
     steps: int                  # length of the timing window
     data: str                   # "sparse_uniform" or "templates"
-    init: str                   # "uniform_half", "uniform_fanin", "ternary"
+    init: str                   # "uniform_half", "uniform_fanin", "he", "ternary"
     weight_mode: str = "fp32"   # "fp32" or "ternary"
     layer_pick: str = "weight"  # "weight": uniform over all weights; "layer": layer first
     gamma: float = 1.0
     accept_ties: bool = False   # False: accept iff dL < 0; True: dL <= 0 (Eq. 6)
+    mutation: str = "single"    # "single", "channel_redraw" or "channel_zero" (Sec. 2.3)
     seed_data: int = 0
     seed_teacher: int = 0
     seed_init: int = 0
@@ -139,6 +140,13 @@ CONFIGS = {
                          init="ternary", weight_mode="ternary", gamma=1.0, **_seeds(4)),
     # char-level decoder: vocab 65, ctx 128, d 128, 2 layers, 4 heads, MLP 512,
     # 64 sequences of 129 tokens from an order-3 Markov chain, delta 0.02, K=16.
+    # channel mutation (Sec. 2.3): five layers 784-1024-1024-1024-10, ReLU,
+    # He-scaled weights U(-sqrt(8/n), sqrt(8/n)), no biases, no LN; every
+    # candidate re-draws one input-to-output path of weights; a candidate is
+    # accepted when the loss does not increase; N=8192, K=16.
+    "channel": MLPConfig(name="channel", widths=(784, 1024, 1024, 1024, 10), act="relu",
+                         n_samples=8192, delta=0.0, K=16, steps=200, data="templates",
+                         init="he", accept_ties=True, mutation="channel_redraw", **_seeds(6)),
     "transformer": TransformerConfig(name="transformer", vocab=65, ctx=128, d_model=128,
                                      n_layer=2, n_head=4, d_mlp=512, n_seq=64, delta=0.02,
                                      K=16, steps=200, seed_data=1005, seed_init=3005,
@@ -228,7 +236,12 @@ def _init_weights(cfg: MLPConfig):
         return Ws, codes, scales
     for l in range(cfg.n_layers):
         shape = (cfg.widths[l + 1], cfg.widths[l])
-        a = 0.5 if cfg.init == "uniform_half" else 1.0 / np.sqrt(cfg.widths[l])
+        if cfg.init == "uniform_half":
+            a = 0.5
+        elif cfg.init == "he":  # He scale of Sec. 2.2: sqrt(8 / fan_in)
+            a = np.sqrt(8.0 / cfg.widths[l])
+        else:
+            a = 1.0 / np.sqrt(cfg.widths[l])
         Ws.append(rng.uniform(-a, a, size=shape).astype(np.float32))
     return Ws, None, None
 
