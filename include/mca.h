@@ -84,6 +84,10 @@ extern "C" {
 /* how a candidate picks its parameter */
 #define MCA_PICK_WEIGHT 0 /* uniform over all parameters */
 #define MCA_PICK_LAYER 1  /* uniform layer, then uniform inside it */
+#define MCA_PICK_STICKY 2 /* Sec. 2.1's current-layer schedule: the steps of block
+                           * e = floor(t / sticky_steps) all mutate layer
+                           * floor(w0 L / 2^64), w0 = word 0 of the Philox block at
+                           * counter (e, 0, 0, 1); uniform inside that layer */
 
 typedef struct mca_net_desc {
   int32_t kind;                         /* MCA_NET_* */
@@ -130,7 +134,19 @@ typedef struct mca_net_desc {
    * mca_eval_channels), scored against the committed state like single
    * mutations and committed, rolled back and run (mca_run_steps) the same way. */
   int32_t mutation;
-  int32_t reserved0;
+  /* Deep nets of Sec. 2.1 (MLPs).  biases = 1: layer l has one bias per
+   * unit; its parameter tensor is the augmented matrix [n_{l+1}][n_l + 1]
+   * (row j: unit j's incoming weights, then its bias), and a candidate with
+   * i = n_l mutates that bias.  layer_norm = 1: every hidden local field is
+   * normalized over the units of its layer, sample by sample,
+   * h = (z - mean z) / sqrt(var z + ln_eps) (population variance, no gain or
+   * bias), before the transfer function; the logits are not normalized.
+   * Either needs L >= 2, every hidden layer 256, 512 or 1024 units wide,
+   * fp32 weights and single mutations.  sticky_steps: block length of
+   * MCA_PICK_STICKY (>= 1), ignored by the other picks. */
+  int32_t biases;
+  int32_t layer_norm;
+  int32_t sticky_steps;
 } mca_net_desc;
 
 /* mca_cand.flags */
@@ -218,7 +234,7 @@ int mca_plan(const mca_net_desc* net, int64_t n_samples, int32_t k_max,
  * workspace, run the full forward pass over all samples to fill the local-field
  * and per-sample loss caches (Sec. 2.1, Sec. 2.4), set the step counter to 0.
  * params: n_params host pointers in canonical order (MLP: the L weight
- * matrices).  codes: ternary only, L host int8 arrays of the same shapes
+ * matrices, augmented with their bias column when biases = 1).  codes: ternary only, L host int8 arrays of the same shapes
  * (params must then equal code * scale); NULL otherwise.  Synchronises. */
 int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
              int32_t n_params, const int8_t* const* codes, const mca_data* data,

@@ -62,6 +62,13 @@ struct NetDev {
   int32_t mutation;                   // MCA_MUTATE_*
   int32_t pad1;
   float chan_amp[MCA_MAX_LAYERS];     // fl32(sqrt(8 / n_l)): amplitude of a re-drawn channel weight
+  // deep nets of Sec. 2.1: biases (candidate column i = n_l of layer l),
+  // normalized hidden fields, the layer-sticky schedule
+  int32_t bias;                       // 1: every layer has a bias vector B[l]
+  int32_t ln;                         // 1: hidden fields are normalized over their layer
+  float ln_eps;
+  int32_t sticky;                     // steps per block of the MCA_PICK_STICKY schedule
+  float* B[MCA_MAX_LAYERS];           // biases [n_{l+1}], or null
 };
 
 // Kernels index the pointer and size arrays of NetDev with runtime values (the
@@ -375,8 +382,13 @@ __device__ __forceinline__ mca_cand decode_index(const NetDev& net, uint64_t t, 
   const Words w = philox4x64_10(t, k, 0, 0, net.seed, net.tag);
   int layer;
   int64_t off;
-  if (net.pick == MCA_PICK_LAYER) {
-    layer = (int)__umul64hi(w.w1, (uint64_t)net.L);
+  if (net.pick == MCA_PICK_LAYER || net.pick == MCA_PICK_STICKY) {
+    if (net.pick == MCA_PICK_LAYER) {
+      layer = (int)__umul64hi(w.w1, (uint64_t)net.L);
+    } else {  // the layer of the step's block: word 0 of counter (t / sticky, 0, 0, 1)
+      const Words b = philox4x64_10(t / (uint64_t)net.sticky, 0, 0, 1, net.seed, net.tag);
+      layer = (int)__umul64hi(b.w0, (uint64_t)net.L);
+    }
     const int64_t size = net.offs[layer + 1] - net.offs[layer];
     off = (int64_t)__umul64hi(w.w0, (uint64_t)size);
   } else {
@@ -386,8 +398,9 @@ __device__ __forceinline__ mca_cand decode_index(const NetDev& net, uint64_t t, 
       if (flat >= net.offs[l]) layer = l;
     off = flat - net.offs[layer];
   }
-  // every layer has fewer than 2^31 entries: 32-bit division suffices
-  const uint32_t nin = (uint32_t)net.widths[layer];
+  // every layer has fewer than 2^31 entries: 32-bit division suffices; a
+  // row of a biased layer ends with its bias (column n_l)
+  const uint32_t nin = (uint32_t)(net.widths[layer] + net.bias);
   mca_cand c;
   c.flat = net.offs[layer] + off;
   c.layer = layer;
@@ -418,13 +431,19 @@ __device__ __forceinline__ void finish_ternary(const NetDev& net, mca_cand& c, i
   c.code = nc;
 }
 
+// The committed value of a candidate's parameter: a weight, or a bias (column n_l).
+__device__ __forceinline__ float param_value(const NetDev& net, int l, int j, int i) {
+  if (i == net.widths[l]) return net.B[l][j];
+  return net.W[l][(int64_t)j * net.widths[l] + i];
+}
+
 __device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t t, uint64_t k) {
   mca_cand c = decode_index(net, t, k);
   const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
   if (net.ternary) finish_ternary(net, c, net.codes[c.layer][idx]);
   if (c.flags & MCA_CAND_PRUNE) {  // w' = 0: the increment is -w
     c.code = 0;
-    c.d = 0.0f - net.W[c.layer][idx];
+    c.d = 0.0f - param_value(net, c.layer, c.j, c.i);
   }
   return c;
 }
@@ -433,8 +452,7 @@ __device__ __forceinline__ mca_cand decode_candidate(const NetDev& net, uint64_t
 // candidate's is zero).
 __device__ __forceinline__ Aux prepare_candidate(const NetDev& net, const mca_cand& c) {
   Aux a;
-  const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
-  a.w_old = net.W[c.layer][idx];
+  a.w_old = param_value(net, c.layer, c.j, c.i);
   a.w_new = (c.flags & MCA_CAND_PRUNE) ? 0.0f
             : (net.ternary ? (float)c.code * net.scales[c.layer] : a.w_old + c.d);
   a.de = a.w_new - a.w_old;

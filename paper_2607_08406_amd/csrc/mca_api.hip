@@ -19,6 +19,7 @@
 #include "slab_kernels.hpp"
 #include "chain_kernels.hpp"
 #include "channel_kernels.hpp"
+#include "norm_kernels.hpp"
 #include "tf_kernels.hpp"
 
 using mca::Aux;
@@ -79,7 +80,9 @@ struct Layout {
   size_t cols = 0, nnz = 0;  // nonzero entries of layer L-3 candidates' W_{L-2} columns
   size_t rows = 0, rda = 0, rcnt = 0, pchain = 0;  // deep nets: affected samples, tile sums
   size_t chans = 0, pchan = 0;                      // channel mutations: records, tile sums
-  int nchain = 0, nchan = 0;
+  size_t pnorm = 0;                                 // nets with biases / normalization: tile sums
+  size_t b[MCA_MAX_LAYERS] = {}, mu[MCA_MAX_LAYERS] = {}, S[MCA_MAX_LAYERS] = {};
+  int nchain = 0, nchan = 0, nnorm = 0;
   int nslab = 0;
   int loop_T = 0, loop_G = 0;
   size_t w[MCA_MAX_LAYERS] = {}, codes[MCA_MAX_LAYERS] = {}, z[MCA_MAX_LAYERS] = {};
@@ -130,7 +133,13 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
     for (int l = 0; l < L; ++l)
       if (!(std::isfinite(net->scales[l]) && net->scales[l] > 0.f))
         return "ternary scales must be finite and positive";
-  if (net->pick != MCA_PICK_WEIGHT && net->pick != MCA_PICK_LAYER) return "unknown pick mode";
+  if (net->pick != MCA_PICK_WEIGHT && net->pick != MCA_PICK_LAYER && net->pick != MCA_PICK_STICKY)
+    return "unknown pick mode";
+  if (net->pick == MCA_PICK_STICKY && net->sticky_steps < 1) return "sticky_steps must be >= 1";
+  if ((net->biases != 0 && net->biases != 1) || (net->layer_norm != 0 && net->layer_norm != 1))
+    return "biases and layer_norm take 0 or 1";
+  if (net->layer_norm && !(std::isfinite(net->ln_eps) && net->ln_eps > 0.f))
+    return "ln_eps must be finite and positive";
   if (!std::isfinite(net->delta) || net->delta < 0.f) return "delta must be finite and >= 0";
   if (!std::isfinite(net->bound)) return "bound must be finite (<= 0 disables it)";
   if (n_samples < 1 || n_samples > ((int64_t)1 << 31)) return "n_samples out of range";
@@ -138,6 +147,17 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
   {
     std::string m = check_selection(net, n_samples, code);
     if (!m.empty()) return m;
+  }
+  if (net->biases || net->layer_norm) {
+    *code = MCA_EUNSUPPORTED;
+    if (L < 2) return "biases and normalization need at least one hidden layer";
+    if (net->weight_mode != MCA_WEIGHTS_FP32) return "biases and normalization take continuous weights";
+    if (net->mutation != MCA_MUTATE_SINGLE) return "channel mutations take no biases or normalization";
+    for (int l = 1; l < L; ++l)
+      if (net->widths[l] != net->widths[1] || !mca::norm_width_ok(net->widths[l]))
+        return "nets with biases or normalization need every hidden layer 256, 512 or 1024 units wide";
+    *code = MCA_OK;
+    return "";
   }
   if (net->mutation != MCA_MUTATE_SINGLE) {
     *code = MCA_EUNSUPPORTED;
@@ -290,8 +310,16 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     return at;
   };
   const int L = net->n_layers;
+  const bool norm = net->biases || net->layer_norm;
   lo.xt = take((size_t)net->widths[0] * lo.Ns * sizeof(float));
   for (int l = 0; l < L; ++l) lo.w[l] = take((size_t)net->widths[l + 1] * net->widths[l] * sizeof(float));
+  if (net->biases)
+    for (int l = 0; l < L; ++l) lo.b[l] = take((size_t)net->widths[l + 1] * sizeof(float));
+  if (net->layer_norm)
+    for (int l = 0; l + 1 < L; ++l) {
+      lo.mu[l] = take(lo.Ns * sizeof(float));
+      lo.S[l] = take(lo.Ns * sizeof(float));
+    }
   if (net->weight_mode == MCA_WEIGHTS_TERNARY)
     for (int l = 0; l < L; ++l) lo.codes[l] = take((size_t)net->widths[l + 1] * net->widths[l]);
   for (int l = 0; l < L; ++l) lo.z[l] = take((size_t)net->widths[l + 1] * lo.Ns * sizeof(float));
@@ -309,7 +337,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * k_max * sizeof(double));
   const bool chan = net->mutation != MCA_MUTATE_SINGLE;
-  if (L >= 3) {
+  if (L >= 3 && !norm) {
     lo.wt = take((size_t)net->widths[L - 2] * net->widths[L - 1] * sizeof(float));
     const int T = mca::slab_tile(net->widths[L]);
     lo.nslab = (int)((N + T - 1) / T);
@@ -317,12 +345,16 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     lo.cols = take((size_t)k_max * net->widths[L - 1] * sizeof(uint64_t));
     lo.nnz = take((size_t)k_max * sizeof(int32_t));
   }
-  if (L >= 4 && !chan) {
+  if (L >= 4 && !chan && !norm) {
     lo.nchain = (int)((N + mca::kChainT - 1) / mca::kChainT);
     lo.rows = take((size_t)k_max * N * sizeof(int32_t));
     lo.rda = take((size_t)k_max * N * sizeof(float));
     lo.rcnt = take((size_t)k_max * sizeof(int32_t));
     lo.pchain = take((size_t)k_max * lo.nchain * sizeof(float));
+  }
+  if (norm) {
+    lo.nnorm = mca::norm_tiles(N, net->widths[1]);
+    lo.pnorm = take((size_t)k_max * lo.nnorm * sizeof(float));
   }
   if (net->mutation != MCA_MUTATE_SINGLE) {
     lo.nchan = mca::channel_tiles(N, net->widths[1]);
@@ -373,6 +405,9 @@ struct mca_ctx {
   bool chan = false;             // candidates are channel mutations (Sec. 2.3)
   mca_channel* chans = nullptr;  // their records
   float* pchan = nullptr;        // their tile sums
+  bool norm = false;             // biases and / or normalized hidden fields (Sec. 2.1)
+  mca::NormDev nd{};             // normalization statistics
+  float* pnorm = nullptr;        // tile sums of the dense evaluation
   double* dl = nullptr;
   double* bsum = nullptr;
   DevState* st = nullptr;
@@ -485,7 +520,12 @@ int run_forward(mca_ctx* ctx) {
     }));
     return MCA_OK;
   }
-  MCA_HIP(ctx, timed(ctx, 5, [&] { return mca::launch_forward(ctx->net, ctx->bsum, ctx->st, ctx->stream); }));
+  if (ctx->norm)
+    MCA_HIP(ctx, timed(ctx, 5, [&] {
+      return mca::launch_forward_norm(ctx->net, ctx->nd, ctx->bsum, ctx->st, ctx->stream);
+    }));
+  else
+    MCA_HIP(ctx, timed(ctx, 5, [&] { return mca::launch_forward(ctx->net, ctx->bsum, ctx->st, ctx->stream); }));
   return MCA_OK;
 }
 
@@ -515,7 +555,7 @@ int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const*
   if (tern && codes == nullptr) return fail(ctx, MCA_EINVAL, "ternary weights need codes");
   for (int l = 0; l < L; ++l) {
     if (params[l] == nullptr) return fail(ctx, MCA_EINVAL, "a parameter pointer is NULL");
-    const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
+    const size_t n = (size_t)d.widths[l + 1] * (d.widths[l] + d.biases);
     if (tern) {
       if (codes[l] == nullptr) return fail(ctx, MCA_EINVAL, "a code pointer is NULL");
       for (size_t e = 0; e < n; ++e) {
@@ -532,6 +572,14 @@ int upload_params(mca_ctx* ctx, const float* const* params, const int8_t* const*
   }
   for (int l = 0; l < L; ++l) {
     const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
+    if (d.biases) {  // the augmented matrix [n_{l+1}][n_l + 1]: weights, then the bias column
+      const size_t w = (size_t)d.widths[l], rows = (size_t)d.widths[l + 1];
+      MCA_HIP(ctx, hipMemcpy2DAsync(ctx->net.W[l], w * sizeof(float), params[l], (w + 1) * sizeof(float),
+                                    w * sizeof(float), rows, hipMemcpyHostToDevice, ctx->stream));
+      MCA_HIP(ctx, hipMemcpy2DAsync(ctx->net.B[l], sizeof(float), params[l] + w, (w + 1) * sizeof(float),
+                                    sizeof(float), rows, hipMemcpyHostToDevice, ctx->stream));
+      continue;
+    }
     MCA_HIP(ctx, hipMemcpyAsync(ctx->net.W[l], params[l], n * sizeof(float), hipMemcpyHostToDevice, ctx->stream));
     if (tern) MCA_HIP(ctx, hipMemcpyAsync(ctx->net.codes[l], codes[l], n, hipMemcpyHostToDevice, ctx->stream));
   }
@@ -577,7 +625,7 @@ int check_cands(mca_ctx* ctx, const mca_cand* c, int K) {
   for (int k = 0; k < K; ++k) {
     const int l = c[k].layer;
     if (l < 0 || l >= d.n_layers) return fail(ctx, MCA_EINVAL, "candidate layer out of range");
-    if (c[k].j < 0 || c[k].j >= d.widths[l + 1] || c[k].i < 0 || c[k].i >= d.widths[l])
+    if (c[k].j < 0 || c[k].j >= d.widths[l + 1] || c[k].i < 0 || c[k].i >= d.widths[l] + d.biases)
       return fail(ctx, MCA_EINVAL, "candidate index out of range");
     if (c[k].flags & ~MCA_CAND_PRUNE) return fail(ctx, MCA_EINVAL, "unknown candidate flags");
     if (d.weight_mode == MCA_WEIGHTS_TERNARY) {
@@ -618,21 +666,26 @@ hipError_t propose_dev(mca_ctx* ctx, uint64_t step, bool use_dev_t, int K) {
   if (ctx->tf)
     return mca::tf_launch_propose(ctx->tfd, ctx->tfh, step, use_dev_t, ctx->st, K, ctx->cands,
                                   ctx->aux, ctx->stream);
+  // (a bias of a first-layer unit has no input feature: no tile list for it)
   return mca::launch_propose(ctx->net, step, use_dev_t, ctx->st, K, ctx->cands, ctx->aux,
-                             ctx->fmask, ctx->cmask, ctx->stream);
+                             ctx->norm ? nullptr : ctx->fmask, ctx->cmask, ctx->stream);
 }
 
 hipError_t prepare_into(mca_ctx* ctx, const Bufs& b, int K) {
   if (ctx->chan)
     return mca::launch_channel_prepare(ctx->net, ctx->chans, K, b.cands, b.aux, ctx->stream);
   if (ctx->tf) return mca::tf_launch_prepare(ctx->tfd, b.cands, K, b.aux, ctx->stream);
-  return mca::launch_prepare(ctx->net, b.cands, K, b.aux, ctx->fmask, b.cmask, ctx->stream);
+  return mca::launch_prepare(ctx->net, b.cands, K, b.aux, ctx->norm ? nullptr : ctx->fmask,
+                             b.cmask, ctx->stream);
 }
 hipError_t prepare_dev(mca_ctx* ctx, int K) { return prepare_into(ctx, ctx_bufs(ctx), K); }
 
 // Scores the K staged candidates: the column kernel for the last two layers,
 // the tile kernel for layer L-3, the dense chain for layers 0..L-4.
 hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
+  if (ctx->norm)
+    return mca::launch_norm(net, ctx->nd, b.cands, b.aux, K, ctx->pnorm, ctx->lo.nnorm, -2,
+                            ctx->st, b.dl, ctx->stream);
   if (ctx->chan)
     return mca::launch_channel(net, ctx->chans, b.aux, K, ctx->pchan, ctx->lo.nchan, -2,
                                ctx->st, b.dl, ctx->stream);
@@ -655,6 +708,13 @@ hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
 
 hipError_t select_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K, bool do_select,
                        int32_t* trc, double* trd) {
+  if (ctx->norm) {
+    NetDev one = net;  // one source of tile sums for every candidate
+    one.L = 0;
+    return mca::launch_select(one, ctx->pnorm, ctx->lo.nnorm, b.cands, nullptr, 0, nullptr, 0,
+                              b.aux, K, b.dl, ctx->st, do_select, trc, trd, kTraceCap,
+                              ctx->stream);
+  }
   if (ctx->chan) {
     // every channel has one source of tile sums (an L = 0 view of the net
     // selects it)
@@ -680,6 +740,9 @@ hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, in
 // Commits candidate k (k < 0: the device decision); each kernel applies only
 // the candidates of the layers it scores.
 hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
+  if (ctx->norm)
+    return mca::launch_norm(net, ctx->nd, ctx->cands, ctx->aux, 0, ctx->pnorm, ctx->lo.nnorm, k,
+                            ctx->st, ctx->dl, ctx->stream);
   if (ctx->chan)
     return mca::launch_channel(net, ctx->chans, ctx->aux, 0, ctx->pchan, ctx->lo.nchan, k,
                                ctx->st, ctx->dl, ctx->stream);
@@ -908,11 +971,16 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.Ns = lo.Ns;
   nd.mutation = net->mutation;
   for (int l = 0; l < L; ++l) nd.chan_amp[l] = (float)std::sqrt(8.0 / (double)net->widths[l]);
+  nd.bias = net->biases;
+  nd.ln = net->layer_norm;
+  nd.ln_eps = net->ln_eps;
+  nd.sticky = net->pick == MCA_PICK_STICKY ? net->sticky_steps : 1;
   int64_t off = 0;
   for (int l = 0; l <= L; ++l) nd.widths[l] = net->widths[l];
   for (int l = 0; l < L; ++l) {
     nd.offs[l] = off;
-    off += (int64_t)net->widths[l + 1] * net->widths[l];
+    off += (int64_t)net->widths[l + 1] * (net->widths[l] + net->biases);
+    nd.B[l] = net->biases ? (float*)(ws + lo.b[l]) : nullptr;
     nd.scales[l] = net->scales[l];
     nd.W[l] = (float*)(ws + lo.w[l]);
     nd.codes[l] = nd.ternary ? (int8_t*)(ws + lo.codes[l]) : nullptr;
@@ -924,12 +992,22 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.ell = (float*)(ws + lo.ell);
   nd.prob = (float*)(ws + lo.pr);
   nd.y = (const int32_t*)(ws + lo.y);
-  nd.WT = (L >= 3) ? (float*)(ws + lo.wt) : nullptr;
-  ctx->pslab = (L >= 3) ? (float*)(ws + lo.pslab) : nullptr;
-  ctx->cols = (L >= 3) ? (uint64_t*)(ws + lo.cols) : nullptr;
-  ctx->nnz = (L >= 3) ? (int*)(ws + lo.nnz) : nullptr;
+  ctx->norm = net->biases || net->layer_norm;
+  const bool slab = L >= 3 && !ctx->norm;
+  nd.WT = slab ? (float*)(ws + lo.wt) : nullptr;
+  ctx->pslab = slab ? (float*)(ws + lo.pslab) : nullptr;
+  ctx->cols = slab ? (uint64_t*)(ws + lo.cols) : nullptr;
+  ctx->nnz = slab ? (int*)(ws + lo.nnz) : nullptr;
+  if (ctx->norm) {
+    for (int l = 0; l + 1 < L && net->layer_norm; ++l) {
+      ctx->nd.MU[l] = (float*)(ws + lo.mu[l]);
+      ctx->nd.S[l] = (float*)(ws + lo.S[l]);
+    }
+    ctx->pnorm = (float*)(ws + lo.pnorm);
+    ctx->use_loop = false;
+  }
   ctx->chan = net->mutation != MCA_MUTATE_SINGLE;
-  const bool deep = L >= 4 && !ctx->chan;
+  const bool deep = L >= 4 && !ctx->chan && !ctx->norm;
   ctx->rows = deep ? (int*)(ws + lo.rows) : nullptr;
   ctx->rda = deep ? (float*)(ws + lo.rda) : nullptr;
   ctx->rcnt = deep ? (int*)(ws + lo.rcnt) : nullptr;
@@ -1105,7 +1183,8 @@ int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
                             double* loss_out, double* dloss_out) {
   MCA_LIVE(ctx);
   if (ctx->tf) return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes MLP contexts");
-  if (ctx->chan) return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes single-mutation contexts");
+  if (ctx->chan || ctx->norm)
+    return fail(ctx, MCA_EUNSUPPORTED, "the no-allocation evaluation takes nets without biases or normalization and single mutations");
   if (K < 1 || K > mca::kMaxK) return fail(ctx, MCA_EINVAL, "K out of range [1, 1024]");
   if (cands_host == nullptr) return fail(ctx, MCA_EINVAL, "cands_host is NULL");
   if (ctx->scratch_dev == nullptr) return fail(ctx, MCA_EDEVICE, "no scratch array on this device");
@@ -1324,6 +1403,14 @@ int mca_get_params(mca_ctx* ctx, float* const* params_out, int8_t* const* codes_
   for (int l = 0; l < d.n_layers; ++l) {
     const size_t n = (size_t)d.widths[l + 1] * d.widths[l];
     if (params_out[l] == nullptr) return fail(ctx, MCA_EINVAL, "a params_out pointer is NULL");
+    if (d.biases) {
+      const size_t w = (size_t)d.widths[l], rows = (size_t)d.widths[l + 1];
+      MCA_HIP(ctx, hipMemcpy2DAsync(params_out[l], (w + 1) * sizeof(float), ctx->net.W[l], w * sizeof(float),
+                                    w * sizeof(float), rows, hipMemcpyDeviceToHost, ctx->stream));
+      MCA_HIP(ctx, hipMemcpy2DAsync(params_out[l] + w, (w + 1) * sizeof(float), ctx->net.B[l], sizeof(float),
+                                    sizeof(float), rows, hipMemcpyDeviceToHost, ctx->stream));
+      continue;
+    }
     MCA_HIP(ctx, hipMemcpyAsync(params_out[l], ctx->net.W[l], n * sizeof(float), hipMemcpyDeviceToHost, ctx->stream));
     if (codes_out != nullptr && ctx->net.ternary && codes_out[l] != nullptr)
       MCA_HIP(ctx, hipMemcpyAsync(codes_out[l], ctx->net.codes[l], n, hipMemcpyDeviceToHost, ctx->stream));

@@ -15,6 +15,7 @@
 
 #include "device_common.hpp"
 #include "mlp_kernels.hpp"
+#include "norm_kernels.hpp"
 
 namespace mca {
 
@@ -534,11 +535,17 @@ __global__ __launch_bounds__(kTile) void k_commit_column(NetDev net_arg, const m
 // ---------------------------------------------------------------------------
 
 // C[M][ldc] = A[M][Kd] * f(B[Kd][ldb]), 64x64 tile per block, 4x4 per thread.
+// C = A op(B) (+ bias): op applies the transfer function to each input, after
+// normalizing it with its column's statistics when bmu is given
+// ((b - mu) / sqrt(S)); bias (may be null) adds one value per output row.
 template <int ACT>  // -1: identity, else MCA_ACT_*
 __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, int M, int Kd,
                                                   const float* __restrict__ B, int64_t ldb,
                                                   int64_t ncols, float* __restrict__ Cm,
-                                                  int64_t ldc, float gamma) {
+                                                  int64_t ldc, float gamma,
+                                                  const float* __restrict__ bmu,
+                                                  const float* __restrict__ bS,
+                                                  const float* __restrict__ bias) {
   __shared__ float As[16][64 + 4];
   __shared__ float Bs[16][64 + 4];
   const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
@@ -562,6 +569,7 @@ __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, i
       float v = 0.f;
       if (gk < Kd && gn < ncols) {
         v = B[(int64_t)gk * ldb + gn];
+        if (bmu != nullptr) v = (v - bmu[gn]) * (1.0f / sqrtf(bS[gn]));
         if (ACT >= 0) v = act_fn(v, ACT, gamma);
       }
       Bs[kk][cc] = v;
@@ -585,10 +593,11 @@ __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, i
   for (int r = 0; r < 4; ++r) {
     const int64_t gm = m0 + ty * 4 + r;
     if (gm >= M) continue;
+    const float b = (bias != nullptr) ? bias[gm] : 0.f;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int64_t gn = n0 + tx * 4 + c;
-      if (gn < ncols) Cm[gm * ldc + gn] = acc[r][c];
+      if (gn < ncols) Cm[gm * ldc + gn] = (bias != nullptr) ? acc[r][c] + b : acc[r][c];
     }
   }
 }
@@ -762,6 +771,43 @@ hipError_t launch_loss_refresh(const NetDev& net, double* bsum, DevState* st, hi
   return hipGetLastError();
 }
 
+// Forward pass of a net with biases and / or normalized hidden fields: each
+// layer's GEMM normalizes and transforms its input with the statistics of the
+// layer before, adds the biases, then the layer's own statistics.
+hipError_t launch_forward_norm(const NetDev& net, const NormDev& nd, double* bsum, DevState* st,
+                               hipStream_t s) {
+  const int64_t N = net.N;
+  for (int l = 0; l < net.L; ++l) {
+    const int M = net.widths[l + 1], Kd = net.widths[l];
+    const float* B = (l == 0) ? net.XT : net.Z[l - 1];
+    const float* mu = (l > 0 && net.ln) ? nd.MU[l - 1] : nullptr;
+    const float* S = (l > 0 && net.ln) ? nd.S[l - 1] : nullptr;
+    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+    if (l == 0)
+      hipLaunchKernelGGL(k_gemm_fwd<-1>, grid, dim3(256), 0, s, net.W[0], M, Kd, B, net.Ns, N,
+                         net.Z[0], net.Ns, net.gamma, nullptr, nullptr, net.B[0]);
+    else if (net.act == MCA_ACT_TANH)
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
+    else if (net.act == MCA_ACT_RELU)
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_RELU>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
+    else
+      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (net.ln && l < net.L - 1) {
+      e = launch_norm_stats(net, nd, l, s);
+      if (e != hipSuccess) return e;
+    }
+  }
+  const int nb = (int)((N + kTile - 1) / kTile);
+  hipLaunchKernelGGL(k_ce_forward, dim3(nb), dim3(kTile), 0, s, net, bsum);
+  hipLaunchKernelGGL(k_loss_total, dim3(1), dim3(64), 0, s, net, bsum, nb, st);
+  return hipGetLastError();
+}
+
 hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s) {
   const int64_t N = net.N;
   for (int l = 0; l < net.L; ++l) {
@@ -770,16 +816,16 @@ hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStre
     dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
     if (l == 0)
       hipLaunchKernelGGL(k_gemm_fwd<-1>, grid, dim3(256), 0, s, net.W[0], M, Kd, B, net.Ns, N,
-                         net.Z[0], net.Ns, net.gamma);
+                         net.Z[0], net.Ns, net.gamma, nullptr, nullptr, nullptr);
     else if (net.act == MCA_ACT_TANH)
       hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
     else if (net.act == MCA_ACT_RELU)
       hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_RELU>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
     else
       hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma);
+                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include "device_common.hpp"
+#include "norm_kernels.hpp"
 
 namespace mca {
 
@@ -33,5 +34,8 @@ hipError_t launch_commit(const NetDev& net, const mca_cand* cands, const Aux* au
 // from them again): with a minibatch the loss is not the sum of the changes.
 hipError_t launch_loss_refresh(const NetDev& net, double* bsum, DevState* st, hipStream_t s);
 hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStream_t s);
+// The forward pass of a net with biases and / or normalized hidden fields.
+hipError_t launch_forward_norm(const NetDev& net, const NormDev& nd, double* bsum, DevState* st,
+                               hipStream_t s);
 
 }  // namespace mca

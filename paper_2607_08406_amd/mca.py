@@ -27,7 +27,7 @@ MCA_NET_MLP, MCA_NET_TRANSFORMER = 0, 1
 MCA_ACT_TANH, MCA_ACT_GAUSS, MCA_ACT_RELU = 0, 1, 2
 MCA_MUTATE_SINGLE, MCA_MUTATE_CHANNEL_REDRAW, MCA_MUTATE_CHANNEL_ZERO = 0, 1, 2
 MCA_WEIGHTS_FP32, MCA_WEIGHTS_TERNARY = 0, 1
-MCA_PICK_WEIGHT, MCA_PICK_LAYER = 0, 1
+MCA_PICK_WEIGHT, MCA_PICK_LAYER, MCA_PICK_STICKY = 0, 1, 2
 MCA_RULE_GREEDY, MCA_RULE_METROPOLIS = 0, 1
 MCA_OPT_PERSISTENT_LOOP, MCA_OPT_LOOP_TILE, MCA_OPT_LOOP_LAUNCH = 1, 2, 3
 
@@ -54,7 +54,8 @@ class mca_net_desc(ctypes.Structure):
                 ("accept_rule", ctypes.c_int32), ("n_prune", ctypes.c_int32),
                 ("beta", ctypes.c_double), ("subset_size", ctypes.c_int64),
                 ("subset_period", ctypes.c_int64), ("mutation", ctypes.c_int32),
-                ("reserved0", ctypes.c_int32)]
+                ("biases", ctypes.c_int32), ("layer_norm", ctypes.c_int32),
+                ("sticky_steps", ctypes.c_int32)]
 
 
 class mca_cand(ctypes.Structure):
@@ -182,7 +183,9 @@ def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta
              ternary_scales: Optional[Sequence[float]] = None, pick: str = "weight",
              bound: float = 0.0, accept_ties: bool = False, seed: int = 0,
              stream_tag: int = 0, beta: float = 0.0, n_prune: int = 0, subset_size: int = 0,
-             subset_period: int = 1, mutation: str = "single") -> mca_net_desc:
+             subset_period: int = 1, mutation: str = "single", biases: bool = False,
+             layer_norm: bool = False, ln_eps: float = 1e-5,
+             sticky_steps: int = 0) -> mca_net_desc:
     d = mca_net_desc()
     d.kind = MCA_NET_MLP
     d.n_layers = len(widths) - 1
@@ -196,7 +199,11 @@ def mlp_desc(widths: Sequence[int], act: str = "tanh", gamma: float = 1.0, delta
         d.weight_mode = MCA_WEIGHTS_TERNARY
         for n, s in enumerate(ternary_scales):
             d.scales[n] = float(np.float32(s))
-    d.pick = {"weight": MCA_PICK_WEIGHT, "layer": MCA_PICK_LAYER}[pick]
+    d.pick = {"weight": MCA_PICK_WEIGHT, "layer": MCA_PICK_LAYER, "sticky": MCA_PICK_STICKY}[pick]
+    d.biases = int(biases)
+    d.layer_norm = int(layer_norm)
+    d.ln_eps = float(np.float32(ln_eps))
+    d.sticky_steps = int(sticky_steps)
     d.delta = float(np.float32(delta))
     d.bound = bound
     d.accept_ties = int(accept_ties)

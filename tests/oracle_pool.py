@@ -40,6 +40,12 @@ def _recv(f):
 
 
 def _build(kind, cfg):
+    if kind == "mlp" and (cfg.biases or cfg.layer_norm):
+        from oracle.normmlp import NormMLP
+        from workloads import mlp_workload
+        w = mlp_workload(cfg)
+        return NormMLP(w["weights"], w["X"], w["y"], cfg.act, cfg.gamma, bias=cfg.biases,
+                       ln=cfg.layer_norm, eps=cfg.ln_eps, sticky=cfg.sticky_steps)
     if kind == "mlp":
         from oracle.mlp import IncrementalMLP, MLPState
         from workloads import mlp_workload
@@ -75,7 +81,8 @@ def _worker_main():
         elif msg[0] == "commit":
             model.commit(msg[1], msg[2])
         elif msg[0] == "state":
-            _send(fout, model.state.weights if kind == "mlp" else model.params)
+            _send(fout, model.state_weights() if hasattr(model, "state_weights")
+                  else (model.state.weights if kind == "mlp" else model.params))
         else:
             break
 

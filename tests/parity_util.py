@@ -35,6 +35,7 @@ import numpy as np
 
 from oracle import mca as omca
 from oracle.mlp import FullMLP, IncrementalMLP, MLPState
+from oracle.normmlp import NormMLP
 
 REL_TOL = 1e-5
 TIE = 1e-6
@@ -55,6 +56,23 @@ def mlp_kappa(widths, layer):
     L = len(widths) - 1
     dense = max(0, L - 3 - layer)
     return 128.0 + 64.0 * dense
+
+
+def norm_kappa(widths, layer):
+    """The same budget for a net with biases and normalized hidden fields:
+    128 for the column and cross-entropy work, plus, for every layer the
+    change then passes through, 256: its normalization pass (two row sums
+    added in runs of 64 terms, up to 64 ulp of their terms' sizes each, and
+    the difference form of the normalized field) and its dense product of W
+    terms (64)."""
+    L = len(widths) - 1
+    return 128.0 + 256.0 * (L - 1 - layer)
+
+
+def kappa_of(cfg, c):
+    if getattr(cfg, "layer_norm", False) or getattr(cfg, "biases", False):
+        return norm_kappa(cfg.widths, c.layer)
+    return mlp_kappa(cfg.widths, getattr(c, "layer", 0))
 
 
 REPORTS = []  # every ParityStats made in this session, printed in the terminal summary
@@ -92,8 +110,14 @@ def make_pair(cfg, w, k_max, oracle="incremental", bound=0.0, beta=0.0, n_prune=
                         accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
                         stream_tag=cfg.stream_tag, bound=bound, beta=beta, n_prune=n_prune,
                         subset_size=subset[0], subset_period=subset[1],
-                        mutation=getattr(cfg, "mutation", "single"))
+                        mutation=getattr(cfg, "mutation", "single"), biases=cfg.biases,
+                        layer_norm=cfg.layer_norm, ln_eps=cfg.ln_eps,
+                        sticky_steps=cfg.sticky_steps)
     ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=k_max, codes=w["codes"])
+    if cfg.biases or cfg.layer_norm:
+        ref = NormMLP(w["weights"], w["X"], w["y"], cfg.act, cfg.gamma, bias=cfg.biases,
+                      ln=cfg.layer_norm, eps=cfg.ln_eps, sticky=cfg.sticky_steps)
+        return ctx, ref
     cls = IncrementalMLP if oracle == "incremental" else FullMLP
     ref = cls(MLPState(w["weights"], w["codes"], scales), w["X"], w["y"], cfg.act, cfg.gamma)
     return ctx, ref
@@ -114,7 +138,7 @@ def check_batch(stats, gpu_dl, ref, cfg, t, K, kappa=None, beta=0.0):
     L_t, rc, dls, mags, th, chosen = omca.evaluate_all(
         ref, t, K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
         getattr(cfg, "layer_pick", "weight"), cfg.accept_ties)
-    kap = [kappa(c) if kappa else mlp_kappa(cfg.widths, c.layer) for c in rc]
+    kap = [kappa(c) if kappa else kappa_of(cfg, c) for c in rc]
     gch = next((k for k in range(K) if omca.accepts(float(gpu_dl[k]), cfg.accept_ties, th[k])), -1)
     check_step(stats, gpu_dl, dls, mags, kap, th, cfg.accept_ties, gch, chosen, tag=f"step {t}")
     return L_t, rc, dls, chosen
@@ -207,7 +231,7 @@ def explicit_steps(ctx, ref, cfg, t0, n_steps, K, stats=None, bound=0.0, beta=0.
         if subset[0]:
             ctx.set_step(t)
         _, gdl = ctx.eval_losses(cands)
-        kap = [mlp_kappa(cfg.widths, c.layer) for c in rc]
+        kap = [kappa_of(cfg, c) for c in rc]
         gch = next((k for k in range(K) if omca.accepts(float(gdl[k]), cfg.accept_ties, th[k])), -1)
         take = check_step(stats, gdl, dls, mags, kap, th, cfg.accept_ties, gch, chosen,
                           bounded, tag=f"step {t}")
@@ -233,7 +257,7 @@ def replay_trace(ref, cfg, t0, chosen, dloss, K, stats=None, beta=0.0, kappa=Non
         L_t, rc, dls, mags, th, orc, bounded = _oracle_step(ref, cfg, t, K, bound, beta, n_prune,
                                                             subset)
         if kappa is None:
-            kap = [mlp_kappa(cfg.widths, getattr(c, "layer", 0)) for c in rc]
+            kap = [kappa_of(cfg, c) for c in rc]
         else:
             kap = [kappa(c) for c in rc]
         g = int(chosen[n])

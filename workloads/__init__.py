@@ -44,12 +44,16 @@ class MLPConfig:
     K: int                      # candidates scored per step
     steps: int                  # length of the timing window
     data: str                   # "sparse_uniform" or "templates"
-    init: str                   # "uniform_half", "uniform_fanin", "he", "ternary"
+    init: str                   # "uniform_half", "uniform_fanin", "he", "small", "ternary"
     weight_mode: str = "fp32"   # "fp32" or "ternary"
     layer_pick: str = "weight"  # "weight": uniform over all weights; "layer": layer first
     gamma: float = 1.0
     accept_ties: bool = False   # False: accept iff dL < 0; True: dL <= 0 (Eq. 6)
     mutation: str = "single"    # "single", "channel_redraw" or "channel_zero" (Sec. 2.3)
+    biases: bool = False        # augmented weights [W_l | b_l] (Sec. 2.1's deep nets)
+    layer_norm: bool = False    # hidden fields normalized over their layer (Sec. 2.1)
+    ln_eps: float = 1e-5
+    sticky_steps: int = 0       # block length of the "sticky" layer pick (Sec. 2.1)
     seed_data: int = 0
     seed_teacher: int = 0
     seed_init: int = 0
@@ -66,7 +70,8 @@ class MLPConfig:
         return self.widths[-1]
 
     def layer_sizes(self):
-        return [self.widths[l + 1] * self.widths[l] for l in range(self.n_layers)]
+        b = 1 if self.biases else 0
+        return [self.widths[l + 1] * (self.widths[l] + b) for l in range(self.n_layers)]
 
     @property
     def n_params(self) -> int:
@@ -147,6 +152,14 @@ CONFIGS = {
     "channel": MLPConfig(name="channel", widths=(784, 1024, 1024, 1024, 10), act="relu",
                          n_samples=8192, delta=0.0, K=16, steps=200, data="templates",
                          init="he", accept_ties=True, mutation="channel_redraw", **_seeds(6)),
+    # deep net of Sec. 2.1: 784-256-256-256-10 ReLU with a bias per unit and
+    # normalized hidden fields, small weights U(-sqrt(0.1/n), sqrt(0.1/n))
+    # with n the hidden width, biases 0, delta 0.01; the layer-sticky schedule
+    # (blocks of 32 steps); N=8192, K=32.
+    "deepln": MLPConfig(name="deepln", widths=(784, 256, 256, 256, 10), act="relu",
+                        n_samples=8192, delta=0.01, K=32, steps=200, data="templates",
+                        init="small", biases=True, layer_norm=True, layer_pick="sticky",
+                        sticky_steps=32, **_seeds(7)),
     "transformer": TransformerConfig(name="transformer", vocab=65, ctx=128, d_model=128,
                                      n_layer=2, n_head=4, d_mlp=512, n_seq=64, delta=0.02,
                                      K=16, steps=200, seed_data=1005, seed_init=3005,
@@ -238,11 +251,16 @@ def _init_weights(cfg: MLPConfig):
         shape = (cfg.widths[l + 1], cfg.widths[l])
         if cfg.init == "uniform_half":
             a = 0.5
+        elif cfg.init == "small":  # Sec. 2.1: sqrt(0.1 / n), n the hidden width
+            a = np.sqrt(0.1 / cfg.widths[1])
         elif cfg.init == "he":  # He scale of Sec. 2.2: sqrt(8 / fan_in)
             a = np.sqrt(8.0 / cfg.widths[l])
         else:
             a = 1.0 / np.sqrt(cfg.widths[l])
-        Ws.append(rng.uniform(-a, a, size=shape).astype(np.float32))
+        w = rng.uniform(-a, a, size=shape).astype(np.float32)
+        if cfg.biases:  # the bias column, starting at zero
+            w = np.concatenate([w, np.zeros((shape[0], 1), np.float32)], axis=1)
+        Ws.append(w)
     return Ws, None, None
 
 
