@@ -117,6 +117,26 @@ def candidate_flops(cfg, w, cands, params):
     return total
 
 
+def dense_path_flops(cfg, cands, channel: bool):
+    """Algorithmic flops of one step on the channel-mutation net (Sec. 2.3) or
+    the deep net with biases and normalization (Sec. 2.1), an FMA counting 2.
+    Every sample changes.  A channel: its first-layer column (2 N), the
+    rank-1 term into the second layer (2 N W), a dense product per later
+    hidden layer (2 N W^2) and the logits (2 N W C).  A single mutation in
+    layer l below the logits: a dense product per later hidden layer
+    (2 N W^2) and the logits (2 N W C); in the logit layer: 2 N."""
+    L, C, N, W = cfg.n_layers, cfg.n_classes, cfg.n_samples, cfg.widths[1]
+    total = 0.0
+    for c in cands:
+        if channel:
+            total += 2 * N + (2 * N * W if L >= 3 else 2 * N * C) + \
+                max(0, L - 3) * 2 * N * W * W + (2 * N * W * C if L >= 3 else 0)
+        else:
+            l = int(c["layer"])
+            total += 2 * N if l == L - 1 else (L - 2 - l) * 2 * N * W * W + 2 * N * W * C
+    return total
+
+
 def transformer_flops(cfg, cands):
     """Algorithmic flops of one step's Transformer candidates: each runs the
     forward pass from the stage of its tensor (an embedding change: every
@@ -180,8 +200,16 @@ def workload_config(cfg):
                              f"{cfg.n_layer} blocks, {cfg.n_seq} sequences, K={cfg.K}, "
                              f"delta={cfg.delta}"),
                 "K": cfg.K, "n_samples": cfg.n_samples, "n_params": cfg.n_params}
+    extra = ""
+    if cfg.mutation != "single":
+        extra += f", {cfg.mutation.replace('_', ' ')} mutations"
+    if cfg.biases or cfg.layer_norm:
+        extra += (f", {'biases' if cfg.biases else 'no biases'}"
+                  f"{', layer-normalized hidden fields' if cfg.layer_norm else ''}")
+    if cfg.layer_pick == "sticky":
+        extra += f", layer-sticky blocks of {cfg.sticky_steps} steps"
     return {"workload": (f"{cfg.name} MLP {'-'.join(map(str, cfg.widths))} {cfg.act}, "
-                         f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}"),
+                         f"N={cfg.n_samples}, K={cfg.K}, delta={cfg.delta}{extra}"),
             "K": cfg.K, "n_samples": cfg.n_samples, "widths": list(cfg.widths),
             "n_params": cfg.n_params}
 
@@ -202,6 +230,10 @@ def oracle_model(cfg, w, mode):
         from oracle.transformer import TransformerModel
         return TransformerModel(w["params"], w["tokens"], w["targets"], cfg.vocab, cfg.ctx,
                                 cfg.d_model, cfg.n_layer, cfg.n_head, cfg.d_mlp, cfg.ln_eps)
+    if cfg.biases or cfg.layer_norm:
+        from oracle.normmlp import NormMLP
+        return NormMLP(w["weights"], w["X"], w["y"], cfg.act, cfg.gamma, bias=cfg.biases,
+                       ln=cfg.layer_norm, eps=cfg.ln_eps, sticky=cfg.sticky_steps)
     from oracle.mlp import FullMLP, IncrementalMLP, MLPState
     cls = IncrementalMLP if mode == "incremental" else FullMLP
     return cls(MLPState(w["weights"], w["codes"], w["scales"]), w["X"], w["y"], cfg.act, cfg.gamma)
@@ -219,6 +251,8 @@ def cpu_baseline(cfg, w, seconds: float, mode: str, scan_all: bool):
     t_init = time.perf_counter() - t0
     n_steps = evals = acc = 0
     pick = getattr(cfg, "layer_pick", "weight")
+    if getattr(cfg, "mutation", "single") != "single":
+        pick = cfg.mutation  # channel candidates (Sec. 2.3)
     t0 = time.perf_counter()
     while evals == 0 or time.perf_counter() - t0 < seconds:
         rec = omca.step(ref, n_steps, cfg.K, cfg.seed_stream, cfg.stream_tag, cfg.delta,
@@ -251,7 +285,9 @@ def make_context(cfg, w, k_max, args):
     desc = mca.mlp_desc(cfg.widths, cfg.act, gamma=cfg.gamma, delta=cfg.delta,
                         ternary_scales=w["scales"], pick=cfg.layer_pick,
                         accept_ties=cfg.accept_ties, seed=cfg.seed_stream,
-                        stream_tag=cfg.stream_tag)
+                        stream_tag=cfg.stream_tag, mutation=cfg.mutation, biases=cfg.biases,
+                        layer_norm=cfg.layer_norm, ln_eps=cfg.ln_eps,
+                        sticky_steps=cfg.sticky_steps)
     ctx = mca.Context(desc, w["weights"], w["X"], w["y"], k_max=k_max, codes=w["codes"])
     if args.tile:
         ctx.set_option(mca.MCA_OPT_LOOP_TILE, args.tile)
@@ -302,6 +338,16 @@ def measure(cfg, w, steps, warmup, args, eval_batch=0):
                 "achieved": achieved, "peak": MFMA_FP32_PEAK_TFS, "unit": "TFLOP/s",
                 "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
                 "flops_per_launch": per_step}
+    elif cfg.mutation != "single" or cfg.biases or cfg.layer_norm:
+        channel = cfg.mutation != "single"
+        per_step = float(np.mean([
+            dense_path_flops(cfg, ctx.propose_channels(t_first + n, cfg.K) if channel
+                             else ctx.propose(t_first + n, cfg.K), channel) for n in sample]))
+        achieved = per_step / avg_s / 1e12
+        roof = {"bound": "mfma", "kernel": "eval phase (k_channel)" if channel
+                else "eval phase (k_norm)", "achieved": achieved, "peak": MFMA_FP32_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
+                "flops_per_launch": per_step}
     elif cfg.n_layers <= 2:
         kernel = "k_step_loop" if loop else "k_eval_tiles"
         # one loop launch covers all timed steps; one eval launch covers one step
@@ -351,7 +397,7 @@ def copy_calibration(nbytes: int):
 # Per-config windows of the multi-config line (the headline config times
 # exactly --steps): long enough that launch and copy overheads are small.
 SUB_STEPS = {"tiny": (20000, 200), "deep": (60, 3), "ternary": (1000, 20),
-             "transformer": (100, 5)}
+             "transformer": (100, 5), "channel": (20, 2), "deepln": (100, 5)}
 
 
 def main():
@@ -360,7 +406,7 @@ def main():
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="wide", help="the headline workload")
-    ap.add_argument("--configs", default="tiny,deep,ternary,transformer",
+    ap.add_argument("--configs", default="tiny,deep,ternary,transformer,channel,deepln",
                     help="the other workloads measured into the same line ('' for none)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--sub-cpu-seconds", type=float, default=3.0)
