@@ -475,19 +475,23 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
   if (tid == 0) stage_cnt = 0;
   // pair slots start clear; after each step wave 0 clears those it summed
   for (int i = tid; i < kLoopMaxK * 68; i += kLoopThreads) (&dlp_lds[0][0])[i] = 0.f;
-  if (wave == 1)
-    for (uint64_t d = 0; d < 3 && d < a.n_steps; ++d) draw(t0 + d, (int)d);
+  // the first step's draw, its loads, and the next two draws while those
+  // loads are in flight
+  if (wave == 1) draw(t0, 0);
   __syncthreads();
   if (wave == 1) {
     issue_cand(0);
+    for (uint64_t d = 1; d < 3 && d < a.n_steps; ++d) draw(t0 + d, (int)d);
     land_cand(0, 0, 1);
-    if (a.n_steps > 1) issue_cand(1);
   } else if (wave >= 2) {
     issue_samples(0);
     land_samples(0, 0, 1, t0);
-    if (a.n_steps > 1) issue_samples(1);
   }
   __syncthreads();
+  if (a.n_steps > 1) {
+    if (wave == 1) issue_cand(1);
+    else if (wave >= 2) issue_samples(1);
+  }
 
   // A step takes two workgroup barriers: after the scoring, and at its end,
   // when wave 0 has decided and committed and waves 1-15 have staged and
@@ -756,12 +760,19 @@ __global__ __launch_bounds__(kLoopThreads) void k_step_loop(LoopArgs a) {
 }
 
 // Clears the tags before a launch (a fill kernel, so the sequence can be
-// captured in a graph).  The abort word is cleared once per call, by the
-// caller: a launch after one that gave up must see it.
-__global__ void k_reset_loop(uint64_t* partials, int64_t n_words, uint64_t* dls) {
+// captured in a graph).  With snap given (the first launch of a call) it also
+// records the counters the call's statistics are taken against and clears the
+// abort word; later launches of the call keep it, so a launch after one that
+// gave up sees it.
+__global__ void k_reset_loop(uint64_t* partials, int64_t n_words, uint64_t* dls,
+                             const DevState* st, DevState* snap, LoopSync* sync) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_words) partials[i] = 0;
   if (i < (int64_t)kLoopReplicas * kLoopMaxK) dls[i] = 0;
+  if (snap != nullptr && i == 0) {
+    *snap = *st;
+    sync->abort = 0;
+  }
 }
 
 namespace {
@@ -773,13 +784,15 @@ const void* pick_loop(int K, int C) {
 
 int step_loop_reducers(int K) { return (K + kReducerWaves - 1) / kReducerWaves; }
 
-hipError_t launch_step_loop(const LoopArgs& a, bool cooperative, hipStream_t s) {
+hipError_t launch_loop_reset(const LoopArgs& a, DevState* snap, hipStream_t s) {
   const int64_t words = 2 * (int64_t)a.K * a.gpad;
   const int64_t n = words > (int64_t)kLoopReplicas * kLoopMaxK ? words : (int64_t)kLoopReplicas * kLoopMaxK;
   hipLaunchKernelGGL(k_reset_loop, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                     a.partials, words, a.dls);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+                     a.partials, words, a.dls, a.st, snap, a.sync);
+  return hipGetLastError();
+}
+
+hipError_t launch_step_loop(const LoopArgs& a, bool cooperative, hipStream_t s) {
   // G tile workgroups and the candidate reducers; every workgroup must be
   // resident at once (the caller checked the occupancy).  The cooperative
   // launch has the runtime guarantee it; the ordinary one relies on the

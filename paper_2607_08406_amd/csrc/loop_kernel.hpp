@@ -40,6 +40,10 @@ constexpr int kLoopMaxTiles = 64 * 4;  // one workgroup per CU: at most the CU c
 
 // Workgroups of the candidate reducers for K candidates (four candidates each).
 int step_loop_reducers(int K);
+// Clears the exchange words before each launch; snap non-null (a call's first
+// launch): also snapshots the counters into snap and clears the abort word.
+hipError_t launch_loop_reset(const LoopArgs& a, DevState* snap, hipStream_t s);
+// The loop kernel alone (its words cleared by launch_loop_reset first).
 hipError_t launch_step_loop(const LoopArgs& a, bool cooperative, hipStream_t s);
 hipError_t step_loop_max_blocks(int K, int C, int* out);
 

@@ -417,6 +417,7 @@ struct mca_ctx {
   uint64_t* loop_dls = nullptr;
   mca::LoopSync* loop_sync = nullptr;
   DevState* snap = nullptr;  // counters at the start of the current run_steps call
+  unsigned char* host_blk = nullptr;  // pinned host copy of the state block (null: none)
   bool use_loop = true;
   bool loop_coop = false;    // cooperative launch of the step loop (default: ordinary)
   void* scratch_dev = nullptr;  // this device's static scratch array (no-allocation entry point)
@@ -879,6 +880,12 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
     delete ctx;
     return rc;
   }
+  // pinned host memory for the state read-back of every run_steps call (a
+  // plain host buffer is used if it cannot be had)
+  if (hipHostMalloc((void**)&ctx->host_blk, kStateBlock, hipHostMallocDefault) != hipSuccess) {
+    ctx->host_blk = nullptr;
+    (void)hipGetLastError();
+  }
   *out = ctx;
   return MCA_OK;
 }
@@ -1069,6 +1076,12 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
     g_thread_error = ctx->err;
     delete ctx;
     return rc;
+  }
+  // pinned host memory for the state read-back of every run_steps call (a
+  // plain host buffer is used if it cannot be had)
+  if (hipHostMalloc((void**)&ctx->host_blk, kStateBlock, hipHostMallocDefault) != hipSuccess) {
+    ctx->host_blk = nullptr;
+    (void)hipGetLastError();
   }
   *out = ctx;
   return MCA_OK;
@@ -1289,9 +1302,6 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   // launch's first step, a snapshot kernel records the counters the call's
   // statistics are taken against, and one copy returns state, snapshot and
   // abort word together.
-  hipLaunchKernelGGL(k_call_start, dim3(1), dim3(1), 0, ctx->stream, ctx->st, ctx->snap,
-                     ctx->loop_sync);
-  MCA_HIP(ctx, hipGetLastError());
   const NetDev& net = ctx->net;
   uint64_t done = 0;
   const bool mlp2 = !ctx->tf && net.L <= 2;
@@ -1309,6 +1319,15 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   const bool loop_ok = ctx->use_loop && mlp2 && offsets_fit && K <= mca::kLoopMaxK &&
                        ctx->lo.loop_G <= mca::kLoopMaxTiles &&
                        ctx->lo.loop_G + mca::step_loop_reducers(K) <= ctx->loop_fit;
+  // the call's start (counter snapshot, abort word cleared): in the loop's
+  // first reset launch, or a launch of its own
+  bool started = false;
+  if (!loop_ok || n_steps == 0) {
+    hipLaunchKernelGGL(k_call_start, dim3(1), dim3(1), 0, ctx->stream, ctx->st, ctx->snap,
+                       ctx->loop_sync);
+    MCA_HIP(ctx, hipGetLastError());
+    started = true;
+  }
   while (loop_ok && done < n_steps) {
     const uint64_t cap = trace ? (uint64_t)kTraceCap : ((uint64_t)1 << 22);
     const uint64_t chunk = std::min<uint64_t>(n_steps - done, cap);
@@ -1327,6 +1346,8 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
     a.tr_dl = (trace && trace->dloss) ? ctx->tr_dl : nullptr;
     a.tr_cap = kTraceCap;
     a.spin_limit = 1u << 22;
+    MCA_HIP(ctx, mca::launch_loop_reset(a, started ? nullptr : ctx->snap, ctx->stream));
+    started = true;
     MCA_HIP(ctx, timed(ctx, 4, [&] { return mca::launch_step_loop(a, ctx->loop_coop, ctx->stream); }));
     if (trace != nullptr) {  // the next chunk reuses the device trace buffers
       MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));
@@ -1362,8 +1383,10 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   }
   if (!ctx->tf && net.sub_size > 0)  // the loss over every sample, from the logits
     MCA_HIP(ctx, mca::launch_loss_refresh(net, ctx->bsum, ctx->st, ctx->stream));
-  // state, snapshot and abort word: one copy
-  alignas(8) unsigned char blk[kStateBlock];
+  // state, snapshot and abort word: one copy (into pinned memory when the
+  // context has it)
+  alignas(8) unsigned char local[kStateBlock];
+  unsigned char* blk = ctx->host_blk ? ctx->host_blk : local;
   MCA_HIP(ctx, hipMemcpyAsync(blk, ctx->st, kStateBlock, hipMemcpyDeviceToHost, ctx->stream));
   MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
   DevState after, before;
@@ -1479,6 +1502,7 @@ void mca_destroy(mca_ctx* ctx) {
     (void)hipEventDestroy(r.b);
   }
   for (auto e : ctx->pool) (void)hipEventDestroy(e);
+  if (ctx->host_blk) (void)hipHostFree(ctx->host_blk);
   delete ctx;
 }
 
