@@ -138,28 +138,42 @@ def dense_path_flops(cfg, cands, channel: bool):
 
 
 def transformer_flops(cfg, cands):
-    """Algorithmic flops of one step's Transformer candidates: each runs the
-    forward pass from the stage of its tensor (an embedding change: every
-    block; a change in block b: blocks b..; the final LayerNorm or output
-    layer: only the output layer).  Per block: Q, K, V and output projections
-    (4 x 2 N d^2), causal attention (scores and weighted values over the
-    T (T+1) / 2 visible pairs per sequence and head), and the MLP (2 x 2 N d m);
-    the output layer 2 N d V."""
+    """Algorithmic flops of one step's Transformer candidates (an FMA counts
+    2).  Per block: Q, K, V and output projections (4 x 2 N d^2), causal
+    attention (scores and weighted values over the T (T+1) / 2 visible pairs
+    per sequence and head) and the MLP (2 x 2 N d m); the final LayerNorm and
+    output layer 2 N d V.  By the candidate's tensor: an embedding or a
+    block's LayerNorm or attention tensor recomputes from its block on (every
+    block for the embeddings); an MLP weight or bias of block b moves one
+    column of x_{b+1} (2 N; an up-projection adds its rank-1 term through
+    the down-projection, 2 N d) and recomputes the blocks after b and the
+    output layer; an output-layer or final-LayerNorm parameter moves one
+    logit column (2 N) or a rank-1 term into every logit (2 N V).  The
+    cross-entropy (about 3 N V) is counted for every candidate."""
     N, D, M, V = cfg.n_samples, cfg.d_model, cfg.d_mlp, cfg.vocab
     T, H, S, NB = cfg.ctx, cfg.n_head, cfg.n_seq, cfg.n_layer
     attn = 2 * 2 * S * H * (T * (T + 1) / 2) * (D // H)
     block = 4 * 2 * N * D * D + attn + 2 * 2 * N * D * M
     out = 2 * N * D * V
+    ce = 3 * N * V
+    n_tensors = 2 + 16 * NB + 4
     total = 0.0
     for c in cands:
         t = int(c["layer"])
-        if t < 2:
-            nb = NB
-        elif t < 2 + 16 * NB:
-            nb = NB - (t - 2) // 16
+        if t >= n_tensors - 2:
+            total += 2 * N + ce
+        elif t >= n_tensors - 4:
+            total += 2 * N * V + ce
+        elif t < 2:
+            total += NB * block + out + ce
         else:
-            nb = 0
-        total += nb * block + out
+            b, role = (t - 2) // 16, (t - 2) % 16
+            if role in (14, 15):      # down-projection weight, bias
+                total += 2 * N + (NB - 1 - b) * block + out + ce
+            elif role in (12, 13):    # up-projection weight, bias
+                total += 2 * N + 2 * N * D + (NB - 1 - b) * block + out + ce
+            else:
+                total += (NB - b) * block + out + ce
     return total
 
 

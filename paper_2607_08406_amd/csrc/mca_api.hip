@@ -244,8 +244,10 @@ struct TfLayout {
   size_t param[mca::kTfMaxTensors] = {};
   size_t tok = 0, tgt = 0, x = 0, ell = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0;
   size_t state = 0, tr_chosen = 0, tr_dl = 0;
-  size_t sx = 0, sh = 0, sln = 0, sqkv = 0, satt = 0, sfc = 0, sell = 0, scopy = 0;
-  size_t table = 0, start = 0, dev = 0;
+  size_t sx = 0, sh = 0, sln = 0, sln2 = 0, su = 0, sqkv = 0, satt = 0, sfc = 0, snhat = 0;
+  size_t slog = 0, sell = 0, scopy = 0;
+  size_t ch = 0, cln2 = 0, cu = 0, cnhat = 0, cz = 0;  // committed intermediate fields
+  size_t table = 0, start = 0, xin = 0, kind = 0, run = 0, pass = 0, dev = 0;
   int64_t copy_stride = 0;
   int nblk = 0, n_tensors = 0;
   size_t total = 0;
@@ -268,7 +270,7 @@ TfLayout tf_make_layout(const mca_net_desc* d, int64_t N, int32_t k_max) {
     maxsz = std::max(maxsz, n);
   }
   const size_t K = (size_t)k_max, n = (size_t)N, D = (size_t)d->d_model;
-  const size_t NB = (size_t)d->n_block, FCW = (size_t)std::max(d->d_mlp, d->vocab);
+  const size_t NB = (size_t)d->n_block, M = (size_t)d->d_mlp, V = (size_t)d->vocab;
   lo.nblk = mca::tf_loss_blocks(N);
   lo.tok = take(n * sizeof(int32_t));
   lo.tgt = take(n * sizeof(int32_t));
@@ -282,17 +284,30 @@ TfLayout tf_make_layout(const mca_net_desc* d, int64_t N, int32_t k_max) {
   lo.state = take(kStateBlock);
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * K * sizeof(double));
+  lo.ch = take(NB * n * D * sizeof(float));
+  lo.cln2 = take(NB * n * D * sizeof(float));
+  lo.cu = take(NB * n * M * sizeof(float));
+  lo.cnhat = take(n * D * sizeof(float));
+  lo.cz = take(n * V * sizeof(float));
   lo.sx = take(K * (NB + 1) * n * D * sizeof(float));
-  lo.sh = take(K * n * D * sizeof(float));
+  lo.sh = take(K * NB * n * D * sizeof(float));
   lo.sln = take(K * n * D * sizeof(float));
+  lo.sln2 = take(K * NB * n * D * sizeof(float));
+  lo.su = take(K * NB * n * M * sizeof(float));
   lo.satt = take(K * n * D * sizeof(float));
   lo.sqkv = take(K * n * 3 * D * sizeof(float));
-  lo.sfc = take(K * n * FCW * sizeof(float));
+  lo.sfc = take(K * n * M * sizeof(float));
+  lo.snhat = take(K * n * D * sizeof(float));
+  lo.slog = take(K * n * V * sizeof(float));
   lo.sell = take(K * n * sizeof(float));
   lo.copy_stride = (maxsz + 63) / 64 * 64;
   lo.scopy = take(K * (size_t)lo.copy_stride * sizeof(float));
   lo.table = take(K * (size_t)lo.n_tensors * sizeof(float*));
   lo.start = take(K * sizeof(int32_t));
+  lo.xin = take(K * sizeof(int32_t));
+  lo.kind = take(K * sizeof(int32_t));
+  lo.run = take(K * sizeof(int32_t));
+  lo.pass = take(sizeof(int32_t));
   lo.dev = take(sizeof(mca::TfDev));
   lo.total = off;
   return lo;
@@ -429,6 +444,7 @@ struct mca_ctx {
   int tf_nblk = 0;            // loss tiles of 256 positions
   bool pending = false;
   int32_t pending_K = 0;
+  std::vector<double> pending_dl;  // loss changes of the pending batch (+inf: rejected unevaluated)
   bool poisoned = false;
   std::string err;
   // phase timing
@@ -516,7 +532,7 @@ int run_forward(mca_ctx* ctx) {
                                          ctx->partial, ctx->tf_nblk, ctx->stream);
       if (e == hipSuccess)
         e = mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, 0,
-                                  true, ctx->bsum, ctx->stream);
+                                  true, ctx->bsum, ctx->partial, ctx->tf_nblk, ctx->stream);
       return e;
     }));
     return MCA_OK;
@@ -738,9 +754,9 @@ hipError_t select_all(mca_ctx* ctx, const NetDev& net, int K, bool do_select, in
   return select_into(ctx, net, ctx_bufs(ctx), K, do_select, trc, trd);
 }
 
-// Commits candidate k (k < 0: the device decision); each kernel applies only
-// the candidates of the layers it scores.
-hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
+// Commits candidate k (k < 0: the device decision) of a batch of K; each
+// kernel applies only the candidates of the layers it scores.
+hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k, int K) {
   if (ctx->norm)
     return mca::launch_norm(net, ctx->nd, ctx->cands, ctx->aux, 0, ctx->pnorm, ctx->lo.nnorm, k,
                             ctx->st, ctx->dl, ctx->stream);
@@ -749,7 +765,7 @@ hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k) {
                                ctx->st, ctx->dl, ctx->stream);
   if (ctx->tf)
     return mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, k,
-                                 false, ctx->bsum, ctx->stream);
+                                 false, ctx->bsum, ctx->partial, ctx->tf_nblk, ctx->stream);
   hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
@@ -823,9 +839,20 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   const int64_t ND = N * h.D;
   for (int b = 0; b <= h.NB; ++b) h.x[b] = (float*)(ws + lo.x) + (int64_t)b * ND;
   h.ell = (float*)(ws + lo.ell);
+  for (int b = 0; b < h.NB; ++b) {
+    h.ch[b] = (float*)(ws + lo.ch) + (int64_t)b * ND;
+    h.cln2[b] = (float*)(ws + lo.cln2) + (int64_t)b * ND;
+    h.cu[b] = (float*)(ws + lo.cu) + (int64_t)b * N * h.M;
+  }
+  h.cnhat = (float*)(ws + lo.cnhat);
+  h.cz = (float*)(ws + lo.cz);
   h.sx = (float*)(ws + lo.sx);
   h.sh = (float*)(ws + lo.sh);
   h.sln = (float*)(ws + lo.sln);
+  h.sln2 = (float*)(ws + lo.sln2);
+  h.su = (float*)(ws + lo.su);
+  h.snhat = (float*)(ws + lo.snhat);
+  h.slog = (float*)(ws + lo.slog);
   h.sqkv = (float*)(ws + lo.sqkv);
   h.satt = (float*)(ws + lo.satt);
   h.sfc = (float*)(ws + lo.sfc);
@@ -834,6 +861,10 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   h.copy_stride = lo.copy_stride;
   h.table = (float**)(ws + lo.table);
   h.start = (int32_t*)(ws + lo.start);
+  h.xin = (int32_t*)(ws + lo.xin);
+  h.kind = (int32_t*)(ws + lo.kind);
+  h.run = (int32_t*)(ws + lo.run);
+  h.pass = (int32_t*)(ws + lo.pass);
   ctx->tfd = (mca::TfDev*)(ws + lo.dev);
   ctx->tf_nblk = lo.nblk;
   ctx->cands = (mca_cand*)(ws + lo.cands);
@@ -1124,6 +1155,7 @@ int mca_eval_losses(mca_ctx* ctx, const mca_cand* cands_host, int32_t K, double*
   }
   ctx->pending = true;
   ctx->pending_K = K;
+  ctx->pending_dl = dl;
   return MCA_OK;
 }
 
@@ -1131,7 +1163,9 @@ int mca_commit(mca_ctx* ctx, int32_t k) {
   MCA_LIVE(ctx);
   if (!ctx->pending) return fail(ctx, MCA_ESTATE, "no pending batch");
   if (k < 0 || k >= ctx->pending_K) return fail(ctx, MCA_EINVAL, "k outside the pending batch");
-  MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, ctx->net, k); }));
+  if (k < (int)ctx->pending_dl.size() && !std::isfinite(ctx->pending_dl[k]))
+    return fail(ctx, MCA_EINVAL, "candidate k was rejected unevaluated (weight bound): it cannot be committed");
+  MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, ctx->net, k, ctx->pending_K); }));
   if (!ctx->tf && ctx->net.sub_size > 0)  // the loss over every sample, from the logits
     MCA_HIP(ctx, mca::launch_loss_refresh(ctx->net, ctx->bsum, ctx->st, ctx->stream));
   ctx->pending = false;
@@ -1189,6 +1223,7 @@ int mca_eval_channels(mca_ctx* ctx, const mca_channel* chans_host, int32_t K, do
   }
   ctx->pending = true;
   ctx->pending_K = K;
+  ctx->pending_dl = dl;
   return MCA_OK;
 }
 
@@ -1371,7 +1406,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
       MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_dev(ctx, 0, true, K); }));
       MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K); }));
       MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, net, K, true, trc, trd); }));
-      MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1); }));
+      MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1, K); }));
     }
     if (trace != nullptr) {
       MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));

@@ -19,6 +19,8 @@
 // of the paper fixed for the oracle.  The dense products run on the matrix
 // cores (v_mfma_f32_16x16x4f32); LayerNorm, attention, GELU and the loss in
 // fp32 on the vector units.
+#include <algorithm>
+
 #include "tf_kernels.hpp"
 
 namespace mca {
@@ -38,15 +40,25 @@ constexpr int kCopyThreads = 256;
 constexpr int kCopyChunk = 4096;   // floats of a private tensor copy per block
 constexpr int kEmbedPer = 4;       // embedding elements per thread
 
-__device__ __forceinline__ int64_t fc_width(const TfDev* tf) {
-  return tf->M > tf->V ? tf->M : tf->V;
-}
 __device__ __forceinline__ float* slot_x(const TfDev* tf, int k, int b) {
   return tf->sx + ((int64_t)k * (tf->NB + 1) + b) * tf->N * tf->D;
 }
-// x_{stage-1}, the residual stream entering stage `stage` (1..NB+1)
+__device__ __forceinline__ float* slot_h(const TfDev* tf, int k, int b) {
+  return tf->sh + ((int64_t)k * tf->NB + b) * tf->N * tf->D;
+}
+__device__ __forceinline__ float* slot_ln2(const TfDev* tf, int k, int b) {
+  return tf->sln2 + ((int64_t)k * tf->NB + b) * tf->N * tf->D;
+}
+__device__ __forceinline__ float* slot_u(const TfDev* tf, int k, int b) {
+  return tf->su + ((int64_t)k * tf->NB + b) * tf->N * tf->M;
+}
+__device__ __forceinline__ float* slot_fc(const TfDev* tf, int k) { return tf->sfc + (int64_t)k * tf->N * tf->M; }
+__device__ __forceinline__ float* slot_log(const TfDev* tf, int k) { return tf->slog + (int64_t)k * tf->N * tf->V; }
+__device__ __forceinline__ float* slot_nhat(const TfDev* tf, int k) { return tf->snhat + (int64_t)k * tf->N * tf->D; }
+// x_{stage-1}, the residual stream entering stage `stage` (1..NB+1): the
+// candidate's own once it has changed, the committed one before
 __device__ __forceinline__ const float* stage_input(const TfDev* tf, int k, int stage) {
-  return (tf->start[k] == stage) ? tf->x[stage - 1] : slot_x(tf, k, stage - 1);
+  return (tf->xin[k] > stage - 1) ? tf->x[stage - 1] : slot_x(tf, k, stage - 1);
 }
 // erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
 // erf x = 1 - (a1 t + ... + a5 t^5) e^{-x^2}, t = 1 / (1 + p x), x >= 0,
@@ -68,6 +80,39 @@ __device__ __forceinline__ float erf_as(float x) {
 // of the result.
 __device__ __forceinline__ float gelu(float y) {
   return 0.5f * y * (1.0f + erf_as(y * 0.70710678118654752f));
+}
+
+// The change of logit v at position n under an output-layer candidate
+// (kTfOutCol: only logit c.j moves, by de times the final LayerNorm output
+// of column c.i, or de for the bias) or a final-LayerNorm candidate
+// (kTfLnfCol: column c.j of that output moves by de times its normalized
+// value, or de for the bias, and reaches every logit through W_out[:, c.j]).
+// The evaluation and the commit use this one expression.
+__device__ __forceinline__ float out_delta(const TfDev* tf, int kind, const mca_cand& c, float de,
+                                           int64_t n, int v) {
+  const int D = tf->D, nt = tf->n_tensors;
+  if (kind == kTfOutCol) {
+    if (v != c.j) return 0.f;
+    if (c.layer == nt - 1) return de;
+    const float lnf = tf->cnhat[n * D + c.i] * tf->param[nt - 4][c.i] + tf->param[nt - 3][c.i];
+    return de * lnf;
+  }
+  const float dl = (c.layer == nt - 4) ? de * tf->cnhat[n * D + c.j] : de;
+  return dl * tf->param[nt - 2][(int64_t)v * D + c.j];
+}
+
+// The new pre-activation of hidden unit c.j of block b at position n under an
+// up-projection candidate (weight: de times the LN2 output of column c.i;
+// bias: de), and the change of its GELU.
+__device__ __forceinline__ float fc_new_u(const TfDev* tf, const mca_cand& c, float de, int b,
+                                          int role, int64_t n) {
+  const float u = tf->cu[b][n * tf->M + c.j];
+  const float du = (role == kBfc) ? de : de * tf->cln2[b][n * tf->D + c.i];
+  return u + du;
+}
+__device__ __forceinline__ float fc_change(const TfDev* tf, const mca_cand& c, float de, int b,
+                                           int role, int64_t n) {
+  return gelu(fc_new_u(tf, c, de, b, role, n)) - gelu(tf->cu[b][n * tf->M + c.j]);
 }
 
 }  // namespace
@@ -124,27 +169,73 @@ __global__ void k_tf_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
 // Blocks (x, k): candidate k's patched private copy of its tensor, a chunk of
 // kCopyChunk floats per block; block (0, k) also writes the tensor table and
 // the candidate's first stage.  identity: slot 0 with the committed tensors.
+// mode kPrepEval: every candidate of the batch; kPrepIdentity: slot 0 with
+// the committed tensors (cache fill); kPrepRedo (before a commit, a grid of
+// one slot): the chosen candidate (k_host, or st->chosen when negative) is
+// recomputed as a dense candidate if it was evaluated incrementally, and
+// the pass does nothing otherwise.  The kind array is left as the
+// evaluation wrote it, so that every block takes the same decision.
+enum { kPrepEval = 0, kPrepIdentity = 1, kPrepRedo = 2 };
 __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const mca_cand* cands,
-                                                          const Aux* aux, int identity) {
-  const int k = blockIdx.y;
+                                                          const Aux* aux, int mode, int k_host,
+                                                          const DevState* st) {
+  int k = blockIdx.y;
+  if (mode == kPrepRedo) {
+    const int kc = (k_host >= 0) ? k_host : st->chosen;
+    const bool redo = kc >= 0 && tf->kind[kc] != kTfDense;
+    k = kc >= 0 ? kc : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      *tf->pass = k;
+      if (!redo) tf->run[k] = tf->NB + 2;
+    }
+    if (!redo) return;
+  } else if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    *tf->pass = -1;
+  }
   const int nt = tf->n_tensors;
   float** tab = tf->table + (int64_t)k * nt;
-  if (identity) {
+  if (mode == kPrepIdentity) {
     if (blockIdx.x == 0) {
       for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = tf->param[t];
-      if (threadIdx.x == 0) tf->start[k] = 0;
+      if (threadIdx.x == 0) {
+        tf->start[k] = tf->run[k] = 0;
+        tf->xin[k] = 0;
+        tf->kind[k] = kTfDense;
+      }
     }
     return;
   }
   const mca_cand c = cands[k];
   const Aux a = aux[k];
-  const int l = c.layer;
+  const int l = c.layer, NB = tf->NB;
+  int kind = kTfDense;
+  if (l >= nt - 2) kind = kTfOutCol;
+  else if (l >= nt - 4) kind = kTfLnfCol;
+  else if (l >= 2) {
+    const int role = (l - 2) % kBlockTensors;
+    if (role == kWproj || role == kBproj) kind = kTfProjCol;
+    if (role == kWfc || role == kBfc) kind = kTfFcCol;
+  }
+  if (mode == kPrepRedo) kind = kTfDense;
+  const bool dense = kind == kTfDense;
   float* cp = tf->scopy + (int64_t)k * tf->copy_stride;
   if (blockIdx.x == 0) {
-    for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = (t == l && a.valid) ? cp : tf->param[t];
-    if (threadIdx.x == 0) tf->start[k] = a.valid ? tf_stage(l, tf->NB) : tf->NB + 2;
+    for (int t = threadIdx.x; t < nt; t += blockDim.x)
+      tab[t] = (t == l && a.valid && dense) ? cp : tf->param[t];
+    if (threadIdx.x == 0) {
+      const int blk = (l - 2) / kBlockTensors;
+      int start = NB + 2, xin = NB + 2;  // nothing recomputed: rejected, or the last stage's own
+      if (a.valid && dense) start = xin = tf_stage(l, NB);
+      if (a.valid && (kind == kTfProjCol || kind == kTfFcCol)) {
+        start = blk + 2;  // the stages after the block, from its patched output stream
+        xin = blk + 1;
+      }
+      tf->start[k] = tf->run[k] = start;
+      tf->xin[k] = xin;
+      if (mode != kPrepRedo) tf->kind[k] = a.valid ? kind : kTfDense;
+    }
   }
-  if (!a.valid) return;
+  if (!a.valid || !dense) return;
   const int64_t n = (int64_t)tf->rows[l] * tf->cols[l];
   const int64_t at = (int64_t)c.j * tf->cols[l] + c.i;
   const float* src = tf->param[l];
@@ -153,10 +244,36 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
     cp[e] = (e == at) ? a.w_new : src[e];
 }
 
+// x_{b+1} of an MLP candidate of block b (kTfProjCol, kTfFcCol): the
+// committed stream plus the candidate's change, from the committed
+// pre-activations and LN2 output of the block.
+__global__ __launch_bounds__(kCopyThreads) void k_tf_patch(const TfDev* tf, const mca_cand* cands,
+                                                           const Aux* aux) {
+  const int k = tf_slot(tf, blockIdx.y);
+  const int kind = tf->kind[k];
+  if (kind != kTfProjCol && kind != kTfFcCol) return;
+  const mca_cand c = cands[k];
+  const float de = aux[k].de;
+  const int D = tf->D, M = tf->M;
+  const int b = (c.layer - 2) / kBlockTensors, role = (c.layer - 2) % kBlockTensors;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= tf->N * D) return;
+  const int64_t n = e / D;
+  const int col = (int)(e - n * D);
+  float dx = 0.f;
+  if (kind == kTfProjCol) {
+    if (col == c.j) dx = (role == kBproj) ? de : de * gelu(tf->cu[b][n * M + c.i]);
+  } else {
+    dx = fc_change(tf, c, de, b, role, n) *
+         tf->param[2 + kBlockTensors * b + kWproj][(int64_t)col * M + c.j];
+  }
+  slot_x(tf, k, b + 1)[e] = tf->x[b + 1][e] + dx;
+}
+
 // x_0 = tok_emb[token] + pos_emb[position] for the candidates of stage 0
 __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf) {
-  const int k = blockIdx.y;
-  if (tf->start[k] != 0) return;
+  const int k = tf_slot(tf, blockIdx.y);
+  if (tf->run[k] != 0) return;
   const int D = tf->D;
   const int64_t ND = tf->N * D;
   float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
@@ -180,8 +297,8 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf) {
 // which: 0 LN1 of the stage's block (input x_{stage-1}), 1 LN2 (input: after
 // attention), 2 the final LayerNorm (stage NB+1).
 __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage, int which) {
-  const int k = blockIdx.y;
-  if (tf->start[k] > stage) return;
+  const int k = tf_slot(tf, blockIdx.y);
+  if (tf->run[k] > stage) return;
   const int D = tf->D;
   const int64_t N = tf->N, ND = N * D;
   const int lane = threadIdx.x & 63;
@@ -194,7 +311,7 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
     g = tab[tb + kLn1G];
     bb = tab[tb + kLn1B];
   } else if (which == 1) {
-    in = tf->sh + k * ND;
+    in = slot_h(tf, k, stage - 1);
     g = tab[tb + kLn2G];
     bb = tab[tb + kLn2B];
   } else {
@@ -203,7 +320,8 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
     bb = tab[tf->n_tensors - 3];
   }
   const float eps = tf->eps;
-  float* const outk = tf->sln + k * ND;
+  float* const outk = (which == 1) ? slot_ln2(tf, k, stage - 1) : tf->sln + k * ND;
+  float* const nhk = (which == 2) ? slot_nhat(tf, k) : nullptr;  // the final one, before its affine part
   constexpr int kMaxPer = 4;  // D <= 256
   float gv[kMaxPer], bv[kMaxPer];
 #pragma unroll
@@ -240,7 +358,9 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
 #pragma unroll
     for (int u = 0; u < kMaxPer; ++u) {
       const int c = lane + 64 * u;
-      if (c < D) out[c] = (v[u] - mean) * rstd * gv[u] + bv[u];
+      const float nh = (v[u] - mean) * rstd;
+      if (c < D) out[c] = nh * gv[u] + bv[u];
+      if (nhk != nullptr && c < D) nhk[n * D + c] = nh;
     }
   }
 }
@@ -261,10 +381,10 @@ __global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage
 // without a residual to hold, three blocks share a CU (40 KB of LDS each).
 template <int EPI>
 __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(const TfDev* tf, int stage, int role) {
-  const int k = blockIdx.z;
-  if (tf->start[k] > stage) return;
+  const int k = tf_slot(tf, blockIdx.z);
+  if (tf->run[k] > stage) return;
   const int D = tf->D, M = tf->M, V = tf->V;
-  const int64_t N = tf->N, ND = N * D, FC = N * fc_width(tf);
+  const int64_t N = tf->N, ND = N * D;
   float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
   const int b = stage - 1;
   const int tb = 2 + kBlockTensors * b;
@@ -273,23 +393,25 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
   bool qkv = false;
   const float *W = nullptr, *bias = nullptr, *R = nullptr;
   float* Y = nullptr;
+  float* Y2 = nullptr;  // the MLP's pre-activations (before the GELU epilogue)
   switch (role) {
     case kGemmQKV:
       Y = tf->sqkv + 3 * k * ND; ldY = 3 * D; Nout = 3 * D; qkv = true;
       break;
     case kGemmO:
-      X = tf->satt + k * ND; W = tab[tb + kWo]; bias = tab[tb + kBo]; Y = tf->sh + k * ND;
+      X = tf->satt + k * ND; W = tab[tb + kWo]; bias = tab[tb + kBo]; Y = slot_h(tf, k, b);
       R = stage_input(tf, k, stage);
       break;
     case kGemmFc:
-      W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = tf->sfc + k * FC; ldY = M; Nout = M;
+      X = slot_ln2(tf, k, b); W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = slot_fc(tf, k);
+      Y2 = slot_u(tf, k, b); ldY = M; Nout = M;
       break;
     case kGemmProj:
-      X = tf->sfc + k * FC; ldX = M; Kd = M; W = tab[tb + kWproj]; bias = tab[tb + kBproj];
-      Y = slot_x(tf, k, b + 1); R = tf->sh + k * ND;
+      X = slot_fc(tf, k); ldX = M; Kd = M; W = tab[tb + kWproj]; bias = tab[tb + kBproj];
+      Y = slot_x(tf, k, b + 1); R = slot_h(tf, k, b);
       break;
     default:  // kGemmOut: logits of the final stage
-      W = tab[tf->n_tensors - 2]; bias = tab[tf->n_tensors - 1]; Y = tf->sfc + k * FC; ldY = V;
+      W = tab[tf->n_tensors - 2]; bias = tab[tf->n_tensors - 1]; Y = slot_log(tf, k); ldY = V;
       Nout = V;
       break;
   }
@@ -420,7 +542,10 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
         const int n = n0 + 64 * wc + 16 * cb + li;
         if (m < N && n < Nout) {
           float y = acc[sb][cb][v] + bvv[cb];
-          if constexpr (EPI == 1) y = gelu(y);
+          if constexpr (EPI == 1) {
+            Y2[m * ldY + n] = y;
+            y = gelu(y);
+          }
           if constexpr (EPI == 2) y = res[sb][cb][v] + y;
           Y[m * ldY + n] = y;
         }
@@ -437,8 +562,8 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
 // A-operand layout.  Wave w takes row blocks w and 7-w (T = 128: every wave
 // walks 9 tiles); keys after the query are masked.
 __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage) {
-  const int k = blockIdx.y;
-  if (tf->start[k] > stage) return;
+  const int k = tf_slot(tf, blockIdx.y);
+  if (tf->run[k] > stage) return;
   constexpr int kS = kTfHeadDim + 4;  // padded row
   __shared__ __attribute__((aligned(16))) float Qs[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Ks[kTfMaxCtx][kS];
@@ -560,19 +685,34 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage) {
 // the committed loss, and the block's sum of changes over its 256 positions
 // (in order).  The block's logits are contiguous; they are staged in LDS with
 // coalesced loads and each thread then takes one position (row stride V).
-__global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, float* partial, int nblk) {
+__global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, const mca_cand* cands,
+                                                        const Aux* aux, float* partial, int nblk,
+                                                        int redo) {
   __shared__ float zl[kLossThreads * kTfMaxVocab];
   __shared__ float dl[kLossThreads];
-  const int k = blockIdx.y;
-  const bool active = tf->start[k] <= tf->NB + 1;
+  const int k = tf_slot(tf, blockIdx.y);
+  const int kind = tf->kind[k];
+  // from the committed logits (evaluation only: a redo reads the slot's own)
+  const bool col = !redo && (kind == kTfOutCol || kind == kTfLnfCol);
+  const bool active = tf->run[k] <= tf->NB + 1 || col;
   const int V = tf->V;
   const int64_t n0 = (int64_t)blockIdx.x * kLossThreads;
   const int64_t nrows = (tf->N - n0 < kLossThreads) ? tf->N - n0 : kLossThreads;
   if (active) {
-    const float* zk = tf->sfc + k * tf->N * fc_width(tf) + n0 * V;
+    const float* zk = (col ? tf->cz : slot_log(tf, k)) + n0 * V;
     for (int64_t e = threadIdx.x; e < nrows * V; e += kLossThreads) zl[e] = zk[e];
   }
   __syncthreads();
+  if (col) {  // the committed logits plus the candidate's change (out_delta)
+    const mca_cand c = cands[k];
+    const float de = aux[k].de;
+    for (int64_t e = threadIdx.x; e < nrows * V; e += kLossThreads) {
+      const int64_t r = e / V;
+      const int v = (int)(e - r * V);
+      zl[e] = zl[e] + out_delta(tf, kind, c, de, n0 + r, v);
+    }
+    __syncthreads();
+  }
   const int r = threadIdx.x;
   float d = 0.f;
   if (active && r < nrows) {
@@ -595,20 +735,37 @@ __global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, float* 
   if (threadIdx.x == 0) partial[(int64_t)k * nblk + blockIdx.x] = dl[0];
 }
 
-// The winner's (or slot 0's, fill) residual streams from its first stage on
-// and its per-position losses become the committed ones; block 0 applies the
-// parameter and the state.
+// The winner's (or slot 0's, fill) state becomes the committed one: its
+// residual streams from the first one it changed, the intermediate fields of
+// every block it recomputed, the final normalized stream, the logits and the
+// per-position losses (the winner was recomputed densely first when it had
+// been evaluated incrementally); block 0 applies the parameter and the
+// state.  One thread per element of the largest array (N x max(M, D, V)).
 __global__ __launch_bounds__(kCopyThreads) void k_tf_commit(const TfDev* tf, const mca_cand* cands,
                                                             const Aux* aux, const double* dL,
                                                             DevState* st, int k_host, int fill) {
   const int k = fill ? 0 : ((k_host >= 0) ? k_host : st->chosen);
   if (k < 0) return;
-  const int64_t ND = tf->N * tf->D;
+  const int D = tf->D, M = tf->M, V = tf->V, NB = tf->NB;
+  const int64_t N = tf->N, ND = N * D, NM = N * M, NV = N * V;
   const int s0 = fill ? 0 : tf->start[k];
+  const int x0 = fill ? 0 : tf->xin[k];
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e < ND)
-    for (int b = s0; b <= tf->NB; ++b) tf->x[b][e] = slot_x(tf, k, b)[e];
-  if (e < tf->N) tf->ell[e] = tf->sell[(int64_t)k * tf->N + e];
+  if (s0 <= NB + 1) {
+    if (e < ND)
+      for (int b = x0; b <= NB; ++b) tf->x[b][e] = slot_x(tf, k, b)[e];
+    for (int b = 0; b < NB; ++b) {
+      if (b + 1 < s0) continue;  // block b (stage b + 1) was not recomputed
+      if (e < ND) {
+        tf->ch[b][e] = slot_h(tf, k, b)[e];
+        tf->cln2[b][e] = slot_ln2(tf, k, b)[e];
+      }
+      if (e < NM) tf->cu[b][e] = slot_u(tf, k, b)[e];
+    }
+    if (e < ND) tf->cnhat[e] = slot_nhat(tf, k)[e];
+    if (e < NV) tf->cz[e] = slot_log(tf, k)[e];
+    if (e < N) tf->ell[e] = tf->sell[(int64_t)k * N + e];
+  }
   if (!fill && blockIdx.x == 0 && threadIdx.x == 0) {
     const mca_cand c = cands[k];
     tf->param[c.layer][(int64_t)c.j * tf->cols[c.layer] + c.i] = aux[k].w_new;
@@ -657,15 +814,22 @@ hipError_t tf_launch_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
   return hipGetLastError();
 }
 
-hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands,
-                          const Aux* aux, int K, bool identity, float* partial, int nblk,
-                          hipStream_t s) {
-  const unsigned KK = identity ? 1u : (unsigned)K;
+namespace {
+// One pass of the stage kernels over the K slots: the patch of the MLP
+// candidates (evaluation only), the embedding, each block, the final stage
+// and the per-position losses.
+hipError_t run_pass(const TfDev* tf, const TfDev& h, const mca_cand* cands, const Aux* aux,
+                    unsigned KK, int mode, int k_host, const DevState* st, float* partial,
+                    int nblk, hipStream_t s) {
   const int64_t N = h.N;
   const unsigned mt = (unsigned)((N + kGemmRows - 1) / kGemmRows);
   hipLaunchKernelGGL(k_tf_prep,
                      dim3((unsigned)((h.copy_stride + kCopyChunk - 1) / kCopyChunk), KK),
-                     dim3(kCopyThreads), 0, s, tf, cands, aux, identity ? 1 : 0);
+                     dim3(kCopyThreads), 0, s, tf, cands, aux, mode, k_host, st);
+  if (mode == kPrepEval)
+    hipLaunchKernelGGL(k_tf_patch,
+                       dim3((unsigned)((N * h.D + kCopyThreads - 1) / kCopyThreads), KK),
+                       dim3(kCopyThreads), 0, s, tf, cands, aux);
   hipLaunchKernelGGL(k_tf_embed,
                      dim3((unsigned)((N * h.D + kCopyThreads * kEmbedPer - 1) / (kCopyThreads * kEmbedPer)), KK),
                      dim3(kCopyThreads), 0, s, tf);
@@ -689,16 +853,30 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, fin, 2);
   hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, (unsigned)((h.V + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
                      s, tf, fin, (int)kGemmOut);
-  hipLaunchKernelGGL(k_tf_ce, dim3((unsigned)nblk, KK), dim3(kLossThreads), 0, s, tf, partial,
-                     nblk);
+  hipLaunchKernelGGL(k_tf_ce, dim3((unsigned)nblk, KK), dim3(kLossThreads), 0, s, tf, cands, aux,
+                     partial, nblk, mode == kPrepRedo ? 1 : 0);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands,
+                          const Aux* aux, int K, bool identity, float* partial, int nblk,
+                          hipStream_t s) {
+  return run_pass(tf, h, cands, aux, identity ? 1u : (unsigned)K,
+                  identity ? kPrepIdentity : kPrepEval, -1, nullptr, partial, nblk, s);
 }
 
 hipError_t tf_launch_commit(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                             const Aux* aux, const double* dL, DevState* st, int k, bool fill,
-                            double* bsum, hipStream_t s) {
-  const int64_t ND = h.N * h.D;
-  hipLaunchKernelGGL(k_tf_commit, dim3((unsigned)((ND + kCopyThreads - 1) / kCopyThreads)),
+                            double* bsum, float* partial, int nblk, hipStream_t s) {
+  if (!fill) {
+    // the winner, if it was evaluated incrementally, recomputed densely
+    const hipError_t e = run_pass(tf, h, cands, aux, 1u, kPrepRedo, k, st, partial, nblk, s);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t w = std::max(std::max(h.M, h.D), h.V);
+  const int64_t n = h.N * w;
+  hipLaunchKernelGGL(k_tf_commit, dim3((unsigned)((n + kCopyThreads - 1) / kCopyThreads)),
                      dim3(kCopyThreads), 0, s, tf, cands, aux, dL, st, k, fill ? 1 : 0);
   if (fill) {
     const int nb = tf_loss_blocks(h.N);

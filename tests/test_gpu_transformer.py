@@ -176,3 +176,57 @@ def test_full_transformer_workload(mca):
     replay(ref, cfg, 2, ch, dl, 16, ps)
     assert_params_equal(ctx, ref)
     ctx.close()
+
+
+KIND_TENSORS = ["wout", "bout", "lnf.g", "lnf.b", "h0.wproj", "h0.bproj", "h0.wfc", "h0.bfc",
+                "h1.wproj", "h1.wfc", "h1.bfc", "h0.wq", "pos_emb", "tok_emb"]
+
+
+def test_commit_of_every_evaluation_kind(mca):
+    """One candidate on each kind of tensor -- output layer and its bias,
+    final-LayerNorm gain and bias (from the committed logits), MLP
+    down-projection and up-projection weights and biases of both blocks
+    (from the committed block fields), and dense tensors -- evaluated,
+    committed, and followed by a batch from the stream scored against the
+    new state: every loss change against the oracle, every committed tensor
+    bit-exact, the cached losses equal to a fresh forward pass's."""
+    from workloads import transformer_param_shapes
+    cfg = small_cfg(name="tf_kinds", n_seq=3)
+    ctx, ref, w = make_pair(mca, cfg, k_max=8)
+    names = [n for n, _ in transformer_param_shapes(cfg)]
+    shapes = [np.shape(p) for p in w["params"]]
+    offs = np.concatenate([[0], np.cumsum([int(np.prod(s)) for s in shapes])])
+    rng = np.random.default_rng(7)
+    ps = ParityStats("transformer commit of every kind")
+    from oracle.philox import Candidate
+    for step, name in enumerate(KIND_TENSORS):
+        t = names.index(name)
+        shp = shapes[t]
+        j = int(rng.integers(shp[0]))
+        i = int(rng.integers(shp[1])) if len(shp) == 2 else 0
+        flat = int(offs[t]) + (j * shp[1] + i if len(shp) == 2 else j)
+        cand = np.zeros(1, dtype=mca.CAND_DTYPE)
+        cand[0]["flat"], cand[0]["layer"], cand[0]["j"], cand[0]["i"] = flat, t, j, i
+        cand[0]["d"] = np.float32(0.03)
+        _, gdl = ctx.eval_losses(cand)
+        oc = Candidate(flat, t, j, i, np.float32(0.03), 0)
+        dl, mag = ref.delta(oc)
+        check_step(ps, gdl, [dl], [mag], [KAPPA_TF], [0.0], False, -1, -1, tag=name)
+        ctx.commit(0)
+        ref.commit(oc, ref.loss() + dl)
+        # the stream's next batch against the new state
+        cands = ctx.propose(100 + step, 8)
+        _, gdl = ctx.eval_losses(cands)
+        ctx.rollback()
+        L_t, rc, dls, mags, th, _ = omca.evaluate_all(ref, 100 + step, 8, cfg.seed_stream,
+                                                      cfg.stream_tag, cfg.delta, "weight",
+                                                      cfg.accept_ties)
+        assert_cands_equal(cands, rc)
+        check_step(ps, gdl, dls, mags, [KAPPA_TF] * 8, th, False, -1, -1, tag=f"after {name}")
+    assert_params_equal(ctx, ref)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss_of(ref.params)) <= REL_TOL * L
+    before = ctx.sample_losses()
+    ctx.refresh()
+    np.testing.assert_allclose(before, ctx.sample_losses(), rtol=1e-5, atol=1e-6)
+    ctx.close()
