@@ -244,10 +244,9 @@ struct TfLayout {
   size_t param[mca::kTfMaxTensors] = {};
   size_t tok = 0, tgt = 0, x = 0, ell = 0, cands = 0, aux = 0, partial = 0, dl = 0, bsum = 0;
   size_t state = 0, tr_chosen = 0, tr_dl = 0;
-  size_t sx = 0, sh = 0, sln = 0, sln2 = 0, su = 0, sqkv = 0, satt = 0, sfc = 0, snhat = 0;
-  size_t slog = 0, sell = 0, scopy = 0;
-  size_t ch = 0, cln2 = 0, cu = 0, cnhat = 0, cz = 0;  // committed intermediate fields
-  size_t table = 0, start = 0, xin = 0, kind = 0, run = 0, pass = 0, dev = 0;
+  size_t sx = 0, sh = 0, sqkv = 0, satt = 0, sfc = 0, slog = 0, sell = 0, sst = 0, scopy = 0;
+  size_t ch = 0, cz = 0;  // committed attention outputs and logits
+  size_t table = 0, start = 0, xin = 0, kind = 0, run = 0, half = 0, redo = 0, dev = 0;
   int64_t copy_stride = 0;
   int nblk = 0, n_tensors = 0;
   size_t total = 0;
@@ -285,29 +284,26 @@ TfLayout tf_make_layout(const mca_net_desc* d, int64_t N, int32_t k_max) {
   lo.tr_chosen = take((size_t)kTraceCap * sizeof(int32_t));
   lo.tr_dl = take((size_t)kTraceCap * K * sizeof(double));
   lo.ch = take(NB * n * D * sizeof(float));
-  lo.cln2 = take(NB * n * D * sizeof(float));
-  lo.cu = take(NB * n * M * sizeof(float));
-  lo.cnhat = take(n * D * sizeof(float));
   lo.cz = take(n * V * sizeof(float));
-  lo.sx = take(K * (NB + 1) * n * D * sizeof(float));
-  lo.sh = take(K * NB * n * D * sizeof(float));
-  lo.sln = take(K * n * D * sizeof(float));
-  lo.sln2 = take(K * NB * n * D * sizeof(float));
-  lo.su = take(K * NB * n * M * sizeof(float));
-  lo.satt = take(K * n * D * sizeof(float));
-  lo.sqkv = take(K * n * 3 * D * sizeof(float));
-  lo.sfc = take(K * n * M * sizeof(float));
-  lo.snhat = take(K * n * D * sizeof(float));
-  lo.slog = take(K * n * V * sizeof(float));
-  lo.sell = take(K * n * sizeof(float));
+  // K candidate slots and one for the pending dense recomputation of a winner
+  const size_t KS = K + 1;
+  lo.sx = take(KS * (NB + 1) * n * D * sizeof(float));
+  lo.sh = take(KS * NB * n * D * sizeof(float));
+  lo.satt = take(KS * n * D * sizeof(float));
+  lo.sqkv = take(KS * n * 3 * D * sizeof(float));
+  lo.sfc = take(KS * n * M * sizeof(float));
+  lo.slog = take(KS * n * V * sizeof(float));
+  lo.sell = take(KS * n * sizeof(float));
+  lo.sst = take(KS * n * 2 * sizeof(float));
   lo.copy_stride = (maxsz + 63) / 64 * 64;
-  lo.scopy = take(K * (size_t)lo.copy_stride * sizeof(float));
-  lo.table = take(K * (size_t)lo.n_tensors * sizeof(float*));
-  lo.start = take(K * sizeof(int32_t));
-  lo.xin = take(K * sizeof(int32_t));
-  lo.kind = take(K * sizeof(int32_t));
-  lo.run = take(K * sizeof(int32_t));
-  lo.pass = take(sizeof(int32_t));
+  lo.scopy = take(KS * (size_t)lo.copy_stride * sizeof(float));
+  lo.table = take(KS * (size_t)lo.n_tensors * sizeof(float*));
+  lo.start = take(KS * sizeof(int32_t));
+  lo.xin = take(KS * sizeof(int32_t));
+  lo.kind = take(KS * sizeof(int32_t));
+  lo.run = take(KS * sizeof(int32_t));
+  lo.half = take(KS * sizeof(int32_t));
+  lo.redo = take(4 * sizeof(int32_t));
   lo.dev = take(sizeof(mca::TfDev));
   lo.total = off;
   return lo;
@@ -532,7 +528,7 @@ int run_forward(mca_ctx* ctx) {
                                          ctx->partial, ctx->tf_nblk, ctx->stream);
       if (e == hipSuccess)
         e = mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, 0,
-                                  true, ctx->bsum, ctx->partial, ctx->tf_nblk, ctx->stream);
+                                  true, ctx->bsum, ctx->stream);
       return e;
     }));
     return MCA_OK;
@@ -765,7 +761,7 @@ hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k, int K) {
                                ctx->st, ctx->dl, ctx->stream);
   if (ctx->tf)
     return mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, k,
-                                 false, ctx->bsum, ctx->partial, ctx->tf_nblk, ctx->stream);
+                                 false, ctx->bsum, ctx->stream);
   hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
@@ -841,22 +837,16 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   h.ell = (float*)(ws + lo.ell);
   for (int b = 0; b < h.NB; ++b) {
     h.ch[b] = (float*)(ws + lo.ch) + (int64_t)b * ND;
-    h.cln2[b] = (float*)(ws + lo.cln2) + (int64_t)b * ND;
-    h.cu[b] = (float*)(ws + lo.cu) + (int64_t)b * N * h.M;
   }
-  h.cnhat = (float*)(ws + lo.cnhat);
   h.cz = (float*)(ws + lo.cz);
   h.sx = (float*)(ws + lo.sx);
   h.sh = (float*)(ws + lo.sh);
-  h.sln = (float*)(ws + lo.sln);
-  h.sln2 = (float*)(ws + lo.sln2);
-  h.su = (float*)(ws + lo.su);
-  h.snhat = (float*)(ws + lo.snhat);
   h.slog = (float*)(ws + lo.slog);
   h.sqkv = (float*)(ws + lo.sqkv);
   h.satt = (float*)(ws + lo.satt);
   h.sfc = (float*)(ws + lo.sfc);
   h.sell = (float*)(ws + lo.sell);
+  h.sst = (float2*)(ws + lo.sst);
   h.scopy = (float*)(ws + lo.scopy);
   h.copy_stride = lo.copy_stride;
   h.table = (float**)(ws + lo.table);
@@ -864,7 +854,9 @@ int tf_init(mca_ctx** out, const mca_net_desc* net, const float* const* params, 
   h.xin = (int32_t*)(ws + lo.xin);
   h.kind = (int32_t*)(ws + lo.kind);
   h.run = (int32_t*)(ws + lo.run);
-  h.pass = (int32_t*)(ws + lo.pass);
+  h.half = (int32_t*)(ws + lo.half);
+  h.redo = (int32_t*)(ws + lo.redo);
+  h.kr = k_max;
   ctx->tfd = (mca::TfDev*)(ws + lo.dev);
   ctx->tf_nblk = lo.nblk;
   ctx->cands = (mca_cand*)(ws + lo.cands);

@@ -1,24 +1,31 @@
 // HIP kernels (gfx950) of the decoder Transformer path of MCA (Sec. 2.5):
-// the candidate stream over all parameter tensors,
-// each candidate's forward pass from the first stage its parameter changes,
-// the per-position cross-entropy and its change against the committed
-// per-position losses, and the commit.
+// the candidate stream over all parameter tensors, each candidate's loss
+// change, and the commit.
 //
-// Every candidate has a slot: its own copy of the mutated tensor (patched
-// with the new value), a table of tensor pointers, and its activations.  A
-// launch covers all K candidates (grid z or y); a candidate whose parameter
-// lies in a later stage skips the stage and the next stage reads the
-// committed residual stream.  The kernels are deterministic and treat every
-// position alike, so a position the mutation cannot reach (before a changed
-// position-embedding row, say) reproduces its committed loss bit for bit and
-// adds exactly zero to the loss change.  The commit copies the winner's slot
-// into the committed state.
+// Every candidate has a slot.  A candidate whose parameter sits in the
+// embeddings, a LayerNorm before attention or the MLP, or the attention
+// projections is evaluated densely: its own copy of the mutated tensor and a
+// forward pass from the first stage that tensor enters.  The others follow
+// the structure of the network: an MLP parameter of block b moves block b's
+// output stream by a rank-1 term (then the later stages run densely), an
+// output-layer or final-LayerNorm parameter moves the logits by a rank-1
+// term (then only the cross-entropy runs).  A launch covers all slots (grid
+// y or z); a slot whose first stage is later skips the stage and the next
+// stage reads the committed state.  The kernels are deterministic and treat
+// every position alike, so a position a dense candidate cannot reach (before
+// a changed position-embedding row, say) reproduces its committed loss bit
+// for bit and adds exactly zero to the loss change.
+//
+// The committed fields are always those of a dense pass: a winner scored
+// incrementally is recomputed densely in slot kr of the next evaluation pass
+// (see TfRedo), and the next commit folds that slot in before the new
+// winner's own.
 //
 // The model (pre-LN blocks, learned positions, erf GELU, final LayerNorm,
 // untied output layer with bias; linear layers y = x W^T + b) is the reading
 // of the paper fixed for the oracle.  The dense products run on the matrix
-// cores (v_mfma_f32_16x16x4f32); LayerNorm, attention, GELU and the loss in
-// fp32 on the vector units.
+// cores (v_mfma_f32_16x16x4f32) with each LayerNorm folded into the product
+// that reads it; attention, GELU and the loss run in fp32 on the vector units.
 #include <algorithm>
 
 #include "tf_kernels.hpp"
@@ -33,12 +40,14 @@ constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 
 constexpr int kGemmRows = 128;     // rows (positions) per block
 constexpr int kGemmCols = 128;     // output columns per block
 constexpr int kChunkK = 16;        // reduction chunk staged in LDS
-constexpr int kLnThreads = 256;    // a wave per row, kLnRows rows per wave
-constexpr int kLnRows = 16;
+constexpr int kStatRows = 8;       // rows whose LayerNorm statistics a wave takes at once
+constexpr int kRowThreads = 256;   // row kernels: a wave per row
+constexpr int kPatchRows = 4;      // rows per wave in the MLP patch
 constexpr int kLossThreads = 256;
 constexpr int kCopyThreads = 256;
 constexpr int kCopyChunk = 4096;   // floats of a private tensor copy per block
 constexpr int kEmbedPer = 4;       // embedding elements per thread
+constexpr int kMaxPer = 4;         // row elements per lane (d_model <= 256)
 
 __device__ __forceinline__ float* slot_x(const TfDev* tf, int k, int b) {
   return tf->sx + ((int64_t)k * (tf->NB + 1) + b) * tf->N * tf->D;
@@ -46,20 +55,75 @@ __device__ __forceinline__ float* slot_x(const TfDev* tf, int k, int b) {
 __device__ __forceinline__ float* slot_h(const TfDev* tf, int k, int b) {
   return tf->sh + ((int64_t)k * tf->NB + b) * tf->N * tf->D;
 }
-__device__ __forceinline__ float* slot_ln2(const TfDev* tf, int k, int b) {
-  return tf->sln2 + ((int64_t)k * tf->NB + b) * tf->N * tf->D;
-}
-__device__ __forceinline__ float* slot_u(const TfDev* tf, int k, int b) {
-  return tf->su + ((int64_t)k * tf->NB + b) * tf->N * tf->M;
-}
 __device__ __forceinline__ float* slot_fc(const TfDev* tf, int k) { return tf->sfc + (int64_t)k * tf->N * tf->M; }
 __device__ __forceinline__ float* slot_log(const TfDev* tf, int k) { return tf->slog + (int64_t)k * tf->N * tf->V; }
-__device__ __forceinline__ float* slot_nhat(const TfDev* tf, int k) { return tf->snhat + (int64_t)k * tf->N * tf->D; }
-// x_{stage-1}, the residual stream entering stage `stage` (1..NB+1): the
-// candidate's own once it has changed, the committed one before
-__device__ __forceinline__ const float* stage_input(const TfDev* tf, int k, int stage) {
-  return (tf->xin[k] > stage - 1) ? tf->x[stage - 1] : slot_x(tf, k, stage - 1);
+__device__ __forceinline__ float* slot_ell(const TfDev* tf, int k) { return tf->sell + (int64_t)k * tf->N; }
+
+// Grid row idx of a launch over ncand candidates: candidate idx, or the
+// pending recomputation's slot for the extra last row.
+__device__ __forceinline__ int slot_of(const TfDev* tf, unsigned idx, int ncand) {
+  return (int)idx < ncand ? (int)idx : tf->kr;
 }
+// Whether the pending recomputation runs in this pass, and the committed
+// fields as the rest of the pass sees them (TfRedo).
+__device__ __forceinline__ bool redo_on(const TfDev* tf) { return tf->run[tf->kr] <= tf->NB + 1; }
+__device__ __forceinline__ bool runs_attention(const TfDev* tf, int k, int b) {
+  return tf->run[k] <= b + 1 && tf->half[k] != b + 1;
+}
+__device__ __forceinline__ const float* view_x(const TfDev* tf, int j) {
+  const int kr = tf->kr;
+  return (redo_on(tf) && j >= tf->xin[kr]) ? slot_x(tf, kr, j) : tf->x[j];
+}
+__device__ __forceinline__ const float* view_h(const TfDev* tf, int b) {
+  return runs_attention(tf, tf->kr, b) ? slot_h(tf, tf->kr, b) : tf->ch[b];
+}
+__device__ __forceinline__ const float* view_z(const TfDev* tf) {
+  return redo_on(tf) ? slot_log(tf, tf->kr) : tf->cz;
+}
+__device__ __forceinline__ const float* view_ell(const TfDev* tf) {
+  return redo_on(tf) ? slot_ell(tf, tf->kr) : tf->ell;
+}
+// x_{stage-1}, the residual stream entering stage `stage` (1..NB+1): the
+// slot's own once it has changed, the committed one before
+__device__ __forceinline__ const float* stage_input(const TfDev* tf, int k, int stage) {
+  return (tf->xin[k] > stage - 1) ? view_x(tf, stage - 1) : slot_x(tf, k, stage - 1);
+}
+// the attention output block b's MLP half reads: the slot's own, or the
+// committed one for a recomputation that starts at that MLP half
+__device__ __forceinline__ const float* mlp_input(const TfDev* tf, int k, int b) {
+  return (tf->half[k] == b + 1) ? tf->ch[b] : slot_h(tf, k, b);
+}
+
+// A row of D <= 256 values held by a wave: element c = lane + 64 u in v[u]
+// (zero beyond D).
+__device__ __forceinline__ void load_row(const float* row, int D, int lane, float (&v)[kMaxPer]) {
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int c = lane + 64 * u;
+    v[u] = (c < D) ? gload(row + c) : 0.f;
+  }
+}
+// Its mean and 1/sqrt(biased variance + eps): the sum by a fixed butterfly,
+// then the centred sum of squares.
+__device__ __forceinline__ void row_stats(const float (&v)[kMaxPer], int D, int lane, float eps,
+                                          float& mean, float& rstd) {
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) s += v[u];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  mean = s / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const float dv = (lane + 64 * u < D) ? v[u] - mean : 0.f;
+    q += dv * dv;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  rstd = 1.0f / sqrtf(q / (float)D + eps);
+}
+
 // erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
 // erf x = 1 - (a1 t + ... + a5 t^5) e^{-x^2}, t = 1 / (1 + p x), x >= 0,
 // absolute error at most 1.5e-7 (odd extension for x < 0).
@@ -82,37 +146,13 @@ __device__ __forceinline__ float gelu(float y) {
   return 0.5f * y * (1.0f + erf_as(y * 0.70710678118654752f));
 }
 
-// The change of logit v at position n under an output-layer candidate
-// (kTfOutCol: only logit c.j moves, by de times the final LayerNorm output
-// of column c.i, or de for the bias) or a final-LayerNorm candidate
-// (kTfLnfCol: column c.j of that output moves by de times its normalized
-// value, or de for the bias, and reaches every logit through W_out[:, c.j]).
-// The evaluation and the commit use this one expression.
-__device__ __forceinline__ float out_delta(const TfDev* tf, int kind, const mca_cand& c, float de,
-                                           int64_t n, int v) {
-  const int D = tf->D, nt = tf->n_tensors;
-  if (kind == kTfOutCol) {
-    if (v != c.j) return 0.f;
-    if (c.layer == nt - 1) return de;
-    const float lnf = tf->cnhat[n * D + c.i] * tf->param[nt - 4][c.i] + tf->param[nt - 3][c.i];
-    return de * lnf;
-  }
-  const float dl = (c.layer == nt - 4) ? de * tf->cnhat[n * D + c.j] : de;
-  return dl * tf->param[nt - 2][(int64_t)v * D + c.j];
-}
-
-// The new pre-activation of hidden unit c.j of block b at position n under an
-// up-projection candidate (weight: de times the LN2 output of column c.i;
-// bias: de), and the change of its GELU.
-__device__ __forceinline__ float fc_new_u(const TfDev* tf, const mca_cand& c, float de, int b,
-                                          int role, int64_t n) {
-  const float u = tf->cu[b][n * tf->M + c.j];
-  const float du = (role == kBfc) ? de : de * tf->cln2[b][n * tf->D + c.i];
-  return u + du;
-}
-__device__ __forceinline__ float fc_change(const TfDev* tf, const mca_cand& c, float de, int b,
-                                           int role, int64_t n) {
-  return gelu(fc_new_u(tf, c, de, b, role, n)) - gelu(tf->cu[b][n * tf->M + c.j]);
+// Cross-entropy of one position from its V logits (max-shifted).
+__device__ __forceinline__ float cross_entropy(const float* z, int V, int y) {
+  float m = z[0];
+  for (int v = 1; v < V; ++v) m = fmaxf(m, z[v]);
+  float sum = 0.f;
+  for (int v = 0; v < V; ++v) sum += fast_exp(z[v] - m);
+  return (fast_log(sum) + m) - z[y];
 }
 
 }  // namespace
@@ -166,48 +206,40 @@ __global__ void k_tf_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
   aux[k] = a;
 }
 
-// Blocks (x, k): candidate k's patched private copy of its tensor, a chunk of
-// kCopyChunk floats per block; block (0, k) also writes the tensor table and
-// the candidate's first stage.  identity: slot 0 with the committed tensors.
-// mode kPrepEval: every candidate of the batch; kPrepIdentity: slot 0 with
-// the committed tensors (cache fill); kPrepRedo (before a commit, a grid of
-// one slot): the chosen candidate (k_host, or st->chosen when negative) is
-// recomputed as a dense candidate if it was evaluated incrementally, and
-// the pass does nothing otherwise.  The kind array is left as the
-// evaluation wrote it, so that every block takes the same decision.
-enum { kPrepEval = 0, kPrepIdentity = 1, kPrepRedo = 2 };
+// Blocks (x, row): the slot's tensor table, first stage and kind (block 0),
+// and a candidate's patched private copy of its tensor, kCopyChunk floats per
+// block.  kPrepEval: candidates 0..ncand-1 and, in the extra last row, the
+// pending recomputation (every committed tensor, its stages from TfRedo);
+// kPrepIdentity: slot 0 with the committed tensors (cache fill), and no
+// recomputation.
+enum { kPrepEval = 0, kPrepIdentity = 1 };
 __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const mca_cand* cands,
-                                                          const Aux* aux, int mode, int k_host,
-                                                          const DevState* st) {
-  int k = blockIdx.y;
-  if (mode == kPrepRedo) {
-    const int kc = (k_host >= 0) ? k_host : st->chosen;
-    const bool redo = kc >= 0 && tf->kind[kc] != kTfDense;
-    k = kc >= 0 ? kc : 0;
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      *tf->pass = k;
-      if (!redo) tf->run[k] = tf->NB + 2;
-    }
-    if (!redo) return;
-  } else if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
-    *tf->pass = -1;
-  }
-  const int nt = tf->n_tensors;
+                                                          const Aux* aux, int mode, int ncand) {
+  const int k = slot_of(tf, blockIdx.y, ncand);
+  const int nt = tf->n_tensors, NB = tf->NB;
   float** tab = tf->table + (int64_t)k * nt;
-  if (mode == kPrepIdentity) {
+  if (mode == kPrepIdentity || k == tf->kr) {
     if (blockIdx.x == 0) {
       for (int t = threadIdx.x; t < nt; t += blockDim.x) tab[t] = tf->param[t];
       if (threadIdx.x == 0) {
-        tf->start[k] = tf->run[k] = 0;
-        tf->xin[k] = 0;
         tf->kind[k] = kTfDense;
+        if (mode == kPrepIdentity) {
+          tf->start[k] = tf->run[k] = 0;
+          tf->xin[k] = 0;
+          tf->half[k] = 0;
+          tf->run[tf->kr] = NB + 2;  // nothing else runs in a cache fill
+        } else {
+          tf->start[k] = tf->run[k] = tf->redo[kRedoStart];
+          tf->half[k] = tf->redo[kRedoHalf];
+          tf->xin[k] = tf->redo[kRedoXin];
+        }
       }
     }
     return;
   }
   const mca_cand c = cands[k];
   const Aux a = aux[k];
-  const int l = c.layer, NB = tf->NB;
+  const int l = c.layer;
   int kind = kTfDense;
   if (l >= nt - 2) kind = kTfOutCol;
   else if (l >= nt - 4) kind = kTfLnfCol;
@@ -216,7 +248,6 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
     if (role == kWproj || role == kBproj) kind = kTfProjCol;
     if (role == kWfc || role == kBfc) kind = kTfFcCol;
   }
-  if (mode == kPrepRedo) kind = kTfDense;
   const bool dense = kind == kTfDense;
   float* cp = tf->scopy + (int64_t)k * tf->copy_stride;
   if (blockIdx.x == 0) {
@@ -232,7 +263,8 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
       }
       tf->start[k] = tf->run[k] = start;
       tf->xin[k] = xin;
-      if (mode != kPrepRedo) tf->kind[k] = a.valid ? kind : kTfDense;
+      tf->half[k] = 0;
+      tf->kind[k] = a.valid ? kind : kTfDense;
     }
   }
   if (!a.valid || !dense) return;
@@ -244,35 +276,106 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
     cp[e] = (e == at) ? a.w_new : src[e];
 }
 
-// x_{b+1} of an MLP candidate of block b (kTfProjCol, kTfFcCol): the
-// committed stream plus the candidate's change, from the committed
-// pre-activations and LN2 output of the block.
-__global__ __launch_bounds__(kCopyThreads) void k_tf_patch(const TfDev* tf, const mca_cand* cands,
-                                                           const Aux* aux) {
-  const int k = tf_slot(tf, blockIdx.y);
+// x_{b+1} of the MLP candidates of block b (kTfProjCol, kTfFcCol), a wave
+// per row: the committed stream plus the candidate's change.  The one
+// pre-activation a candidate needs (unit c.j of an up-projection candidate,
+// unit c.i of a down-projection weight) is recomputed from the committed
+// attention output: LN2 of the row, its dot product with the unit's weight
+// row, plus the unit's bias.  An up-projection candidate moves that unit's
+// pre-activation by de times LN2 column c.i (de for the bias), and the
+// change of its GELU enters every column through the down-projection's
+// column c.j; a down-projection candidate moves column c.j by de times the
+// GELU of unit c.i (de for the bias).
+__global__ __launch_bounds__(kRowThreads) void k_tf_patch(const TfDev* tf, const mca_cand* cands,
+                                                          const Aux* aux, int b) {
+  const int k = blockIdx.y;
   const int kind = tf->kind[k];
   if (kind != kTfProjCol && kind != kTfFcCol) return;
   const mca_cand c = cands[k];
+  if ((c.layer - 2) / kBlockTensors != b) return;
+  const int role = (c.layer - 2) % kBlockTensors;
   const float de = aux[k].de;
   const int D = tf->D, M = tf->M;
-  const int b = (c.layer - 2) / kBlockTensors, role = (c.layer - 2) % kBlockTensors;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= tf->N * D) return;
-  const int64_t n = e / D;
-  const int col = (int)(e - n * D);
-  float dx = 0.f;
-  if (kind == kTfProjCol) {
-    if (col == c.j) dx = (role == kBproj) ? de : de * gelu(tf->cu[b][n * M + c.i]);
-  } else {
-    dx = fc_change(tf, c, de, b, role, n) *
-         tf->param[2 + kBlockTensors * b + kWproj][(int64_t)col * M + c.j];
+  const int64_t N = tf->N;
+  const int lane = threadIdx.x & 63;
+  const int tb = 2 + kBlockTensors * b;
+  const float* hc = view_h(tf, b);
+  const float* xc = view_x(tf, b + 1);
+  float* xo = slot_x(tf, k, b + 1);
+  const bool fc = kind == kTfFcCol;
+  const bool need_u = fc || role == kWproj;
+  const int unit = fc ? c.j : c.i;
+  const float* g2 = tf->param[tb + kLn2G];
+  const float* b2 = tf->param[tb + kLn2B];
+  const float* wfc = tf->param[tb + kWfc] + (int64_t)unit * D;
+  const float* wproj = tf->param[tb + kWproj];
+  float gv[kMaxPer], bv[kMaxPer], wu[kMaxPer], wp[kMaxPer];
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int cc = lane + 64 * u;
+    const bool ok = cc < D;
+    gv[u] = ok ? g2[cc] : 0.f;
+    bv[u] = ok ? b2[cc] : 0.f;
+    wu[u] = (ok && need_u) ? wfc[cc] : 0.f;
+    wp[u] = (ok && fc) ? wproj[(int64_t)cc * M + c.j] : 0.f;
   }
-  slot_x(tf, k, b + 1)[e] = tf->x[b + 1][e] + dx;
+  const float bu = need_u ? tf->param[tb + kBfc][unit] : 0.f;
+  const int64_t r0 = ((int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6)) * kPatchRows;
+  // every row's loads first, then the arithmetic
+  float hv[kPatchRows][kMaxPer], xv[kPatchRows][kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kPatchRows; ++i) {
+    const int64_t m = r0 + i < N ? r0 + i : N - 1;
+    if (need_u) load_row(hc + m * D, D, lane, hv[i]);
+    load_row(xc + m * D, D, lane, xv[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < kPatchRows; ++i) {
+    float dg = de;  // a down-projection bias
+    if (need_u) {
+      float mean, rstd;
+      row_stats(hv[i], D, lane, tf->eps, mean, rstd);
+      float ln[kMaxPer];
+      float dot = 0.f;
+#pragma unroll
+      for (int u = 0; u < kMaxPer; ++u) {
+        ln[u] = (lane + 64 * u < D) ? (hv[i][u] - mean) * rstd * gv[u] + bv[u] : 0.f;
+        dot += ln[u] * wu[u];
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
+      const float uu = dot + bu;
+      if (fc) {
+        float du = de;
+        if (role == kWfc) {
+          float sel = ln[0];
+#pragma unroll
+          for (int u = 1; u < kMaxPer; ++u)
+            if (u == (c.i >> 6)) sel = ln[u];
+          du = de * __shfl(sel, c.i & 63, 64);
+        }
+        dg = gelu(uu + du) - gelu(uu);
+      } else {
+        dg = de * gelu(uu);
+      }
+    }
+    if (r0 + i < N) {
+      float* xw = xo + (r0 + i) * D;
+#pragma unroll
+      for (int u = 0; u < kMaxPer; ++u) {
+        const int cc = lane + 64 * u;
+        if (cc < D) {
+          const float x = xv[i][u];
+          xw[cc] = fc ? x + dg * wp[u] : (cc == c.j ? x + dg : x);
+        }
+      }
+    }
+  }
 }
 
-// x_0 = tok_emb[token] + pos_emb[position] for the candidates of stage 0
-__global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf) {
-  const int k = tf_slot(tf, blockIdx.y);
+// x_0 = tok_emb[token] + pos_emb[position] for the slots of stage 0
+__global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf, int ncand) {
+  const int k = slot_of(tf, blockIdx.y, ncand);
   if (tf->run[k] != 0) return;
   const int D = tf->D;
   const int64_t ND = tf->N * D;
@@ -293,109 +396,75 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf) {
   }
 }
 
-// LayerNorm (biased variance, eps inside the root, affine), a wave per row.
-// which: 0 LN1 of the stage's block (input x_{stage-1}), 1 LN2 (input: after
-// attention), 2 the final LayerNorm (stage NB+1).
-__global__ __launch_bounds__(kLnThreads) void k_tf_ln(const TfDev* tf, int stage, int which) {
-  const int k = tf_slot(tf, blockIdx.y);
-  if (tf->run[k] > stage) return;
-  const int D = tf->D;
-  const int64_t N = tf->N, ND = N * D;
-  const int lane = threadIdx.x & 63;
-  float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
-  const int tb = 2 + kBlockTensors * (stage - 1);
-  const float* in;
-  const float *g, *bb;
-  if (which == 0) {
-    in = stage_input(tf, k, stage);
-    g = tab[tb + kLn1G];
-    bb = tab[tb + kLn1B];
-  } else if (which == 1) {
-    in = slot_h(tf, k, stage - 1);
-    g = tab[tb + kLn2G];
-    bb = tab[tb + kLn2B];
-  } else {
-    in = stage_input(tf, k, stage);
-    g = tab[tf->n_tensors - 4];
-    bb = tab[tf->n_tensors - 3];
+// Mean and 1/sqrt(biased variance + eps) of every row of a LayerNorm's
+// input, for the slots that run it: which 0 LN1 (the input of stage
+// `stage`), 1 LN2 (the attention output block stage-1's MLP reads), 2 the
+// final LayerNorm (the input of stage NB+1).  A wave takes kStatRows rows
+// with all their loads in flight.
+__global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, int stage, int which,
+                                                          int ncand) {
+  const int k = slot_of(tf, blockIdx.y, ncand);
+  if (which == 0 ? !runs_attention(tf, k, stage - 1) : tf->run[k] > stage) return;
+  const int D = tf->D, lane = threadIdx.x & 63;
+  const int64_t N = tf->N;
+  const float* X = (which == 1) ? mlp_input(tf, k, stage - 1) : stage_input(tf, k, stage);
+  float2* out = tf->sst + (int64_t)k * N;
+  const int64_t r0 = ((int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6)) * kStatRows;
+  float v[kStatRows][kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kStatRows; ++i) {
+    const int64_t m = r0 + i;
+    load_row(X + (m < N ? m : N - 1) * D, D, lane, v[i]);
   }
-  const float eps = tf->eps;
-  float* const outk = (which == 1) ? slot_ln2(tf, k, stage - 1) : tf->sln + k * ND;
-  float* const nhk = (which == 2) ? slot_nhat(tf, k) : nullptr;  // the final one, before its affine part
-  constexpr int kMaxPer = 4;  // D <= 256
-  float gv[kMaxPer], bv[kMaxPer];
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    gv[u] = (c < D) ? g[c] : 0.f;
-    bv[u] = (c < D) ? bb[c] : 0.f;
-  }
-  const int64_t r0 = ((int64_t)blockIdx.x * (kLnThreads / 64) + (threadIdx.x >> 6)) * kLnRows;
-  for (int64_t n = r0; n < r0 + kLnRows && n < N; ++n) {
-    const float* inr = in + n * D;
-    float v[kMaxPer];
-    float s = 0.f;
-#pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int c = lane + 64 * u;
-      v[u] = (c < D) ? inr[c] : 0.f;
-      s += v[u];
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-    const float mean = s / (float)D;
-    float q = 0.f;
-#pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int c = lane + 64 * u;
-      const float dv = (c < D) ? v[u] - mean : 0.f;
-      q += dv * dv;
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-    const float rstd = 1.0f / sqrtf(q / (float)D + eps);
-    float* out = outk + n * D;
-#pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int c = lane + 64 * u;
-      const float nh = (v[u] - mean) * rstd;
-      if (c < D) out[c] = nh * gv[u] + bv[u];
-      if (nhk != nullptr && c < D) nhk[n * D + c] = nh;
-    }
+  for (int i = 0; i < kStatRows; ++i) {
+    float mean, rstd;
+    row_stats(v[i], D, lane, tf->eps, mean, rstd);
+    if (lane == 0 && r0 + i < N) out[r0 + i] = make_float2(mean, rstd);
   }
 }
 
-// Y = X W^T + b with an epilogue, for the candidates active in `stage`.
+// Y = LN(X) W^T + b (LN: the LayerNorm of the input rows, for the products
+// that read one) with an epilogue, for the slots active in `stage`.
 // A 128 x 128 output tile per block; wave (wr, wc) takes the 64 x 64
 // quarter (wr, wc) as four by four 16 x 16 MFMA tiles, so each operand
 // fragment read from LDS feeds four MFMAs.  The reduction dimension runs in
 // chunks of 16 staged in LDS (double-buffered: the next chunk's global loads
-// are in flight while the current one is multiplied).  Inside a chunk, k runs in blocks of 16; lane group q holds
-// k = 16 kb + 4 q + t (t = 0..3), used by four MFMAs in turn, so each lane
-// reads its operands as float4.  Rows and columns beyond the matrix are
-// clamped on load and dropped on store.  Requires Kd % 16 == 0.  The Q, K and
-// V projections are one product with 3 D output columns: column n takes its
-// weight row and bias from tensor n / D of the three.
-// EPI: 0 bias only (Q, K, V; output layer), 1 GELU (MLP up), 2 residual
-// (attention output, MLP down): each epilogue gets its own register budget;
-// without a residual to hold, three blocks share a CU (40 KB of LDS each).
+// are in flight while the current one is multiplied).  Inside a chunk, k
+// runs in blocks of 16; lane group q holds k = 16 kb + 4 q + t (t = 0..3),
+// used by four MFMAs in turn, so each lane reads its operands as float4.
+// Rows and columns beyond the matrix are clamped on load and dropped on
+// store.  Requires Kd % 16 == 0.  The Q, K and V projections are one
+// product with 3 D output columns: column n takes its weight row and bias
+// from tensor n / D of the three.
+// LayerNorm (Q, K, V: LN1 of the stage input; MLP up: LN2 of the attention
+// output; output layer: the final LayerNorm): with the mean and
+// 1/sqrt(variance + eps) of each input row from k_tf_stats, each staged
+// operand element becomes (x - mean) rstd g + b on its way into LDS.
+// EPI: 0 bias only (Q, K, V), 1 GELU (MLP up), 2 residual (attention
+// output, MLP down), 3 logits and each position's cross-entropy (output
+// layer; one column tile): each epilogue gets its own register and LDS
+// budget.
 template <int EPI>
-__global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(const TfDev* tf, int stage, int role) {
-  const int k = tf_slot(tf, blockIdx.z);
-  if (tf->run[k] > stage) return;
-  const int D = tf->D, M = tf->M, V = tf->V;
+__global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : (EPI == 3 ? 1 : 3)) void k_tf_gemm(
+    const TfDev* tf, int stage, int role, int ncand) {
+  const int k = slot_of(tf, blockIdx.z, ncand);
+  const bool attn_half = role == kGemmQKV || role == kGemmO;
+  if (tf->run[k] > stage || (attn_half && tf->half[k] == stage)) return;
+  const int D = tf->D, M = tf->M, V = tf->V, nt = tf->n_tensors;
   const int64_t N = tf->N, ND = N * D;
-  float* const* tab = tf->table + (int64_t)k * tf->n_tensors;
+  float* const* tab = tf->table + (int64_t)k * nt;
   const int b = stage - 1;
   const int tb = 2 + kBlockTensors * b;
-  const float* X = tf->sln + k * ND;
+  const float* X = nullptr;
   int ldX = D, Kd = D, ldY = D, Nout = D;
   bool qkv = false;
   const float *W = nullptr, *bias = nullptr, *R = nullptr;
+  const float *lg = nullptr, *lb = nullptr;  // LayerNorm gain and bias of the input rows
   float* Y = nullptr;
-  float* Y2 = nullptr;  // the MLP's pre-activations (before the GELU epilogue)
   switch (role) {
     case kGemmQKV:
+      X = stage_input(tf, k, stage); lg = tab[tb + kLn1G]; lb = tab[tb + kLn1B];
       Y = tf->sqkv + 3 * k * ND; ldY = 3 * D; Nout = 3 * D; qkv = true;
       break;
     case kGemmO:
@@ -403,16 +472,16 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
       R = stage_input(tf, k, stage);
       break;
     case kGemmFc:
-      X = slot_ln2(tf, k, b); W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = slot_fc(tf, k);
-      Y2 = slot_u(tf, k, b); ldY = M; Nout = M;
+      X = mlp_input(tf, k, b); lg = tab[tb + kLn2G]; lb = tab[tb + kLn2B];
+      W = tab[tb + kWfc]; bias = tab[tb + kBfc]; Y = slot_fc(tf, k); ldY = M; Nout = M;
       break;
     case kGemmProj:
       X = slot_fc(tf, k); ldX = M; Kd = M; W = tab[tb + kWproj]; bias = tab[tb + kBproj];
-      Y = slot_x(tf, k, b + 1); R = slot_h(tf, k, b);
+      Y = slot_x(tf, k, b + 1); R = mlp_input(tf, k, b);
       break;
     default:  // kGemmOut: logits of the final stage
-      W = tab[tf->n_tensors - 2]; bias = tab[tf->n_tensors - 1]; Y = slot_log(tf, k); ldY = V;
-      Nout = V;
+      X = stage_input(tf, k, stage); lg = tab[nt - 4]; lb = tab[nt - 3];
+      W = tab[nt - 2]; bias = tab[nt - 1]; Y = slot_log(tf, k); ldY = V; Nout = V;
       break;
   }
   const int n0 = blockIdx.y * kGemmCols;
@@ -428,23 +497,36 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
     const int w = n / D;
     return tab[tb + kBq + 2 * w][n - w * D];
   };
-  __shared__ __attribute__((aligned(16))) float As[2][kGemmRows][kChunkK + 4];
-  __shared__ __attribute__((aligned(16))) float Bs[2][kGemmCols][kChunkK + 4];
+  constexpr int kStage = 2 * kGemmRows * (kChunkK + 4);  // floats of one operand's double buffer
+  constexpr int kZ = kGemmRows * (kTfMaxVocab + 1);      // the output layer's logit tile
+  constexpr int kSmem = (EPI == 3 && kZ > 2 * kStage) ? kZ : 2 * kStage;
+  __shared__ __attribute__((aligned(16))) float smem[kSmem];
+  auto As = reinterpret_cast<float (*)[kGemmRows][kChunkK + 4]>(smem);
+  auto Bs = reinterpret_cast<float (*)[kGemmCols][kChunkK + 4]>(smem + kStage);
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
   const int wr = wave >> 1, wc = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.x * kGemmRows;
+  const bool ln = lg != nullptr;
+  const float2* stats = tf->sst + (int64_t)k * N;  // the input rows' LayerNorm statistics
   // staging: thread tid loads float4 number tid + 256 u of the A chunk
-  // (128 rows x 8 float4) and of the B chunk (128 rows x 8 float4)
-  constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 4
-  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 4
+  // (128 rows x 4 float4) and of the B chunk (128 rows x 4 float4); its A
+  // elements sit in one float4 column group of every chunk
+  constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 2
+  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 2
+  const int acol = 4 * (tid % (kChunkK / 4));
   const float* ga[kA4];
   const float* gb[kB4];
+  float amu[kA4], ars[kA4];
 #pragma unroll
   for (int u = 0; u < kA4; ++u) {
     const int e = tid + kGemmThreads * u;
-    const int64_t r = m0 + e / (kChunkK / 4);
-    ga[u] = X + (r < N ? r : N - 1) * ldX + 4 * (e % (kChunkK / 4));
+    const int r = e / (kChunkK / 4);
+    const int64_t m = m0 + r;
+    ga[u] = X + (m < N ? m : N - 1) * ldX + acol;
+    const float2 st2 = ln ? stats[m < N ? m : N - 1] : make_float2(0.f, 1.f);
+    amu[u] = st2.x;
+    ars[u] = st2.y;
   }
 #pragma unroll
   for (int u = 0; u < kB4; ++u) {
@@ -452,18 +534,29 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
     const int n = n0 + e / (kChunkK / 4);
     gb[u] = wrow(n < Nout ? n : Nout - 1) + 4 * (e % (kChunkK / 4));
   }
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   floatx4 ra0[kA4], rb0[kB4];
+  floatx4 rg = zero, rbe = zero;  // LayerNorm gain and bias of the thread's A columns
   auto fetch = [&](int c, floatx4 (&ra)[kA4], floatx4 (&rb)[kB4]) {
 #pragma unroll
     for (int u = 0; u < kA4; ++u) ra[u] = gload(reinterpret_cast<const floatx4*>(ga[u] + kChunkK * c));
 #pragma unroll
     for (int u = 0; u < kB4; ++u) rb[u] = gload(reinterpret_cast<const floatx4*>(gb[u] + kChunkK * c));
+    if (ln) {
+      rg = gload(reinterpret_cast<const floatx4*>(lg + kChunkK * c + acol));
+      rbe = gload(reinterpret_cast<const floatx4*>(lb + kChunkK * c + acol));
+    }
   };
   auto store = [&](int buf, const floatx4 (&ra)[kA4], const floatx4 (&rb)[kB4]) {
 #pragma unroll
     for (int u = 0; u < kA4; ++u) {
       const int e = tid + kGemmThreads * u;
-      *reinterpret_cast<floatx4*>(&As[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = ra[u];
+      floatx4 a = ra[u];
+      if (ln) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) a[t] = fmaf((a[t] - amu[u]) * ars[u], rg[t], rbe[t]);
+      }
+      *reinterpret_cast<floatx4*>(&As[buf][e / (kChunkK / 4)][acol]) = a;
     }
 #pragma unroll
     for (int u = 0; u < kB4; ++u) {
@@ -471,7 +564,6 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
       *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = rb[u];
     }
   };
-  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   floatx4 acc[4][4];
 #pragma unroll
   for (int sb = 0; sb < 4; ++sb)
@@ -532,6 +624,30 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
     const int n = n0 + 64 * wc + 16 * cb + li;
     bvv[cb] = (n < Nout) ? bias_of(n) : 0.f;
   }
+  if constexpr (EPI == 3) {
+    // the logits into LDS (the operand buffers are free) and to the slot,
+    // then a thread per position
+    const int ldz = V + 1;
+    float* Z = smem;
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = 64 * wr + 16 * sb + 4 * q + v;
+          const int n = 64 * wc + 16 * cb + li;
+          if (n < Nout) {
+            const float y = acc[sb][cb][v] + bvv[cb];
+            Z[r * ldz + n] = y;
+            if (m0 + r < N) Y[(m0 + r) * ldY + n] = y;
+          }
+        }
+    __syncthreads();
+    if (tid < kGemmRows && m0 + tid < N)
+      slot_ell(tf, k)[m0 + tid] = cross_entropy(Z + tid * ldz, V, tf->tgt[m0 + tid]);
+    return;
+  }
 #pragma unroll
   for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
@@ -542,10 +658,7 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
         const int n = n0 + 64 * wc + 16 * cb + li;
         if (m < N && n < Nout) {
           float y = acc[sb][cb][v] + bvv[cb];
-          if constexpr (EPI == 1) {
-            Y2[m * ldY + n] = y;
-            y = gelu(y);
-          }
+          if constexpr (EPI == 1) y = gelu(y);
           if constexpr (EPI == 2) y = res[sb][cb][v] + y;
           Y[m * ldY + n] = y;
         }
@@ -561,9 +674,9 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : 3) void k_tf_gemm(cons
 // that hold a row, then O = P V with P re-laid out through LDS into the
 // A-operand layout.  Wave w takes row blocks w and 7-w (T = 128: every wave
 // walks 9 tiles); keys after the query are masked.
-__global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage) {
-  const int k = tf_slot(tf, blockIdx.y);
-  if (tf->run[k] > stage) return;
+__global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int ncand) {
+  const int k = slot_of(tf, blockIdx.y, ncand);
+  if (!runs_attention(tf, k, stage - 1)) return;
   constexpr int kS = kTfHeadDim + 4;  // padded row
   __shared__ __attribute__((aligned(16))) float Qs[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Ks[kTfMaxCtx][kS];
@@ -681,50 +794,63 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage) {
   }
 }
 
-// Per-position cross-entropy of the candidate's logits, its change against
-// the committed loss, and the block's sum of changes over its 256 positions
-// (in order).  The block's logits are contiguous; they are staged in LDS with
-// coalesced loads and each thread then takes one position (row stride V).
-__global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, const mca_cand* cands,
-                                                        const Aux* aux, float* partial, int nblk,
-                                                        int redo) {
+// Per-position loss changes of candidate k against the committed losses,
+// and the block's sum over its 256 positions (in order).  A dense or MLP
+// candidate's losses come from its own final stage.  An output-layer or
+// final-LayerNorm candidate's come from the committed logits plus its change:
+// an output weight (j, i) moves logit j by de times column i of the final
+// LayerNorm's output (de for the bias); a final-LayerNorm gain or bias of
+// column j moves that column by de times its normalized value (or de), which
+// reaches every logit through column j of the output weights.  The
+// normalized value is recomputed from the committed x_NB, a wave per row.
+__global__ __launch_bounds__(kLossThreads) void k_tf_dl(const TfDev* tf, const mca_cand* cands,
+                                                        const Aux* aux, float* partial, int nblk) {
   __shared__ float zl[kLossThreads * kTfMaxVocab];
+  __shared__ float nh[kLossThreads];
   __shared__ float dl[kLossThreads];
-  const int k = tf_slot(tf, blockIdx.y);
+  const int k = blockIdx.y;
   const int kind = tf->kind[k];
-  // from the committed logits (evaluation only: a redo reads the slot's own)
-  const bool col = !redo && (kind == kTfOutCol || kind == kTfLnfCol);
-  const bool active = tf->run[k] <= tf->NB + 1 || col;
-  const int V = tf->V;
+  const bool col = kind == kTfOutCol || kind == kTfLnfCol;
+  const bool active = tf->run[k] <= tf->NB + 1;
+  const int V = tf->V, D = tf->D, nt = tf->n_tensors;
+  const int64_t N = tf->N;
   const int64_t n0 = (int64_t)blockIdx.x * kLossThreads;
-  const int64_t nrows = (tf->N - n0 < kLossThreads) ? tf->N - n0 : kLossThreads;
-  if (active) {
-    const float* zk = (col ? tf->cz : slot_log(tf, k)) + n0 * V;
-    for (int64_t e = threadIdx.x; e < nrows * V; e += kLossThreads) zl[e] = zk[e];
-  }
-  __syncthreads();
-  if (col) {  // the committed logits plus the candidate's change (out_delta)
-    const mca_cand c = cands[k];
-    const float de = aux[k].de;
-    for (int64_t e = threadIdx.x; e < nrows * V; e += kLossThreads) {
-      const int64_t r = e / V;
-      const int v = (int)(e - r * V);
-      zl[e] = zl[e] + out_delta(tf, kind, c, de, n0 + r, v);
-    }
-    __syncthreads();
-  }
+  const int nrows = (int)((N - n0 < kLossThreads) ? N - n0 : kLossThreads);
+  const float* ell = view_ell(tf);
   const int r = threadIdx.x;
   float d = 0.f;
-  if (active && r < nrows) {
-    const float* z = zl + r * V;
-    float m = z[0];
-    for (int v = 1; v < V; ++v) m = fmaxf(m, z[v]);
-    float sum = 0.f;
-    for (int v = 0; v < V; ++v) sum += fast_exp(z[v] - m);
-    const int64_t n = n0 + r;
-    const float ln = (fast_log(sum) + m) - z[tf->tgt[n]];
-    tf->sell[k * tf->N + n] = ln;
-    d = ln - tf->ell[n];
+  if (col) {
+    const mca_cand c = cands[k];
+    const float de = aux[k].de;
+    const float* zc = view_z(tf) + n0 * V;
+    for (int e = threadIdx.x; e < nrows * V; e += kLossThreads) zl[e] = zc[e];
+    const bool out_w = c.layer == nt - 2, lnf_g = c.layer == nt - 4;
+    if (out_w || lnf_g) {
+      const int cc = out_w ? c.i : c.j;
+      const float* xs = view_x(tf, tf->NB);
+      const int lane = threadIdx.x & 63;
+      for (int i = threadIdx.x >> 6; i < nrows; i += kLossThreads / 64) {
+        float v[kMaxPer];
+        load_row(xs + (n0 + i) * D, D, lane, v);
+        float mean, rstd;
+        row_stats(v, D, lane, tf->eps, mean, rstd);
+        if (lane == 0) nh[i] = (xs[(n0 + i) * D + cc] - mean) * rstd;
+      }
+    }
+    __syncthreads();
+    if (r < nrows) {
+      float* z = zl + r * V;
+      if (kind == kTfOutCol) {
+        z[c.j] += out_w ? de * fmaf(nh[r], tf->param[nt - 4][c.i], tf->param[nt - 3][c.i]) : de;
+      } else {
+        const float dcol = lnf_g ? de * nh[r] : de;
+        const float* wo = tf->param[nt - 2];
+        for (int v = 0; v < V; ++v) z[v] += dcol * wo[(int64_t)v * D + c.j];
+      }
+      d = cross_entropy(z, V, tf->tgt[n0 + r]) - ell[n0 + r];
+    }
+  } else if (active && r < nrows) {
+    d = slot_ell(tf, k)[n0 + r] - ell[n0 + r];
   }
   dl[r] = d;
   __syncthreads();
@@ -735,42 +861,56 @@ __global__ __launch_bounds__(kLossThreads) void k_tf_ce(const TfDev* tf, const m
   if (threadIdx.x == 0) partial[(int64_t)k * nblk + blockIdx.x] = dl[0];
 }
 
-// The winner's (or slot 0's, fill) state becomes the committed one: its
-// residual streams from the first one it changed, the intermediate fields of
-// every block it recomputed, the final normalized stream, the logits and the
-// per-position losses (the winner was recomputed densely first when it had
-// been evaluated incrementally); block 0 applies the parameter and the
-// state.  One thread per element of the largest array (N x max(M, D, V)).
+// The commit: first the pending recomputation's fields (slot kr, where it
+// ran this pass), then the winner's own if it was evaluated densely (or
+// slot 0 of a fill): its residual streams from the first one it changed,
+// the attention outputs of the blocks whose attention it ran, the logits
+// and the per-position losses.  One thread per element of the largest array
+// (N x max(D, V)); block 0 applies the parameter and the state and records
+// the winner as the next pending recomputation if it was scored
+// incrementally.
 __global__ __launch_bounds__(kCopyThreads) void k_tf_commit(const TfDev* tf, const mca_cand* cands,
                                                             const Aux* aux, const double* dL,
                                                             DevState* st, int k_host, int fill) {
-  const int k = fill ? 0 : ((k_host >= 0) ? k_host : st->chosen);
-  if (k < 0) return;
-  const int D = tf->D, M = tf->M, V = tf->V, NB = tf->NB;
-  const int64_t N = tf->N, ND = N * D, NM = N * M, NV = N * V;
-  const int s0 = fill ? 0 : tf->start[k];
-  const int x0 = fill ? 0 : tf->xin[k];
+  const int NB = tf->NB, kr = tf->kr;
+  const int w = fill ? 0 : ((k_host >= 0) ? k_host : st->chosen);
+  const bool wd = w >= 0 && tf->kind[w] == kTfDense && tf->start[w] <= NB + 1;
+  const bool rd = !fill && redo_on(tf);
+  const int64_t N = tf->N, ND = N * tf->D, NV = N * tf->V;
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (s0 <= NB + 1) {
-    if (e < ND)
-      for (int b = x0; b <= NB; ++b) tf->x[b][e] = slot_x(tf, k, b)[e];
-    for (int b = 0; b < NB; ++b) {
-      if (b + 1 < s0) continue;  // block b (stage b + 1) was not recomputed
-      if (e < ND) {
-        tf->ch[b][e] = slot_h(tf, k, b)[e];
-        tf->cln2[b][e] = slot_ln2(tf, k, b)[e];
-      }
-      if (e < NM) tf->cu[b][e] = slot_u(tf, k, b)[e];
+  if (e < ND) {
+    for (int j = 0; j <= NB; ++j) {
+      const float* src = (wd && j >= tf->xin[w]) ? slot_x(tf, w, j)
+                         : (rd && j >= tf->xin[kr]) ? slot_x(tf, kr, j) : nullptr;
+      if (src != nullptr) tf->x[j][e] = src[e];
     }
-    if (e < ND) tf->cnhat[e] = slot_nhat(tf, k)[e];
-    if (e < NV) tf->cz[e] = slot_log(tf, k)[e];
-    if (e < N) tf->ell[e] = tf->sell[(int64_t)k * N + e];
+    for (int b = 0; b < NB; ++b) {
+      const float* src = (wd && runs_attention(tf, w, b)) ? slot_h(tf, w, b)
+                         : (rd && runs_attention(tf, kr, b)) ? slot_h(tf, kr, b) : nullptr;
+      if (src != nullptr) tf->ch[b][e] = src[e];
+    }
   }
-  if (!fill && blockIdx.x == 0 && threadIdx.x == 0) {
-    const mca_cand c = cands[k];
-    tf->param[c.layer][(int64_t)c.j * tf->cols[c.layer] + c.i] = aux[k].w_new;
-    st->L += dL[k];
-    st->accepted += 1;
+  const float* zs = wd ? slot_log(tf, w) : (rd ? slot_log(tf, kr) : nullptr);
+  if (zs != nullptr && e < NV) tf->cz[e] = zs[e];
+  const float* ls = wd ? slot_ell(tf, w) : (rd ? slot_ell(tf, kr) : nullptr);
+  if (ls != nullptr && e < N) tf->ell[e] = ls[e];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    int rs = NB + 2, rh = 0, rx = NB + 2;  // no recomputation pending
+    if (!fill && w >= 0) {
+      const mca_cand c = cands[w];
+      tf->param[c.layer][(int64_t)c.j * tf->cols[c.layer] + c.i] = aux[w].w_new;
+      st->L += dL[w];
+      st->accepted += 1;
+      const int kind = tf->kind[w];
+      if (kind == kTfProjCol || kind == kTfFcCol) {
+        rs = rh = rx = (c.layer - 2) / kBlockTensors + 1;  // from the block's MLP half
+      } else if (kind != kTfDense) {
+        rs = rx = NB + 1;  // the final stage
+      }
+    }
+    tf->redo[kRedoStart] = rs;
+    tf->redo[kRedoHalf] = rh;
+    tf->redo[kRedoXin] = rx;
   }
 }
 
@@ -814,68 +954,53 @@ hipError_t tf_launch_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
   return hipGetLastError();
 }
 
-namespace {
-// One pass of the stage kernels over the K slots: the patch of the MLP
-// candidates (evaluation only), the embedding, each block, the final stage
-// and the per-position losses.
-hipError_t run_pass(const TfDev* tf, const TfDev& h, const mca_cand* cands, const Aux* aux,
-                    unsigned KK, int mode, int k_host, const DevState* st, float* partial,
-                    int nblk, hipStream_t s) {
-  const int64_t N = h.N;
-  const unsigned mt = (unsigned)((N + kGemmRows - 1) / kGemmRows);
-  hipLaunchKernelGGL(k_tf_prep,
-                     dim3((unsigned)((h.copy_stride + kCopyChunk - 1) / kCopyChunk), KK),
-                     dim3(kCopyThreads), 0, s, tf, cands, aux, mode, k_host, st);
-  if (mode == kPrepEval)
-    hipLaunchKernelGGL(k_tf_patch,
-                       dim3((unsigned)((N * h.D + kCopyThreads - 1) / kCopyThreads), KK),
-                       dim3(kCopyThreads), 0, s, tf, cands, aux);
-  hipLaunchKernelGGL(k_tf_embed,
-                     dim3((unsigned)((N * h.D + kCopyThreads * kEmbedPer - 1) / (kCopyThreads * kEmbedPer)), KK),
-                     dim3(kCopyThreads), 0, s, tf);
-  const int64_t ln_rows = (int64_t)(kLnThreads / 64) * kLnRows;
-  const dim3 lng((unsigned)((N + ln_rows - 1) / ln_rows), KK);
-  for (int b = 0; b < h.NB; ++b) {
-    const int stage = b + 1;
-    hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 0);
-    hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, (unsigned)((3 * h.D + kGemmCols - 1) / kGemmCols), KK),
-                       dim3(kGemmThreads), 0, s, tf, stage, (int)kGemmQKV);
-    hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), KK), dim3(256), 0, s, tf, stage);
-    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
-                       s, tf, stage, (int)kGemmO);
-    hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, stage, 1);
-    hipLaunchKernelGGL(k_tf_gemm<1>, dim3(mt, (unsigned)((h.M + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
-                       s, tf, stage, (int)kGemmFc);
-    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, (unsigned)((h.D + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
-                       s, tf, stage, (int)kGemmProj);
-  }
-  const int fin = h.NB + 1;
-  hipLaunchKernelGGL(k_tf_ln, lng, dim3(kLnThreads), 0, s, tf, fin, 2);
-  hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, (unsigned)((h.V + kGemmCols - 1) / kGemmCols), KK), dim3(kGemmThreads), 0,
-                     s, tf, fin, (int)kGemmOut);
-  hipLaunchKernelGGL(k_tf_ce, dim3((unsigned)nblk, KK), dim3(kLossThreads), 0, s, tf, cands, aux,
-                     partial, nblk, mode == kPrepRedo ? 1 : 0);
-  return hipGetLastError();
-}
-}  // namespace
 
 hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                           const Aux* aux, int K, bool identity, float* partial, int nblk,
                           hipStream_t s) {
-  return run_pass(tf, h, cands, aux, identity ? 1u : (unsigned)K,
-                  identity ? kPrepIdentity : kPrepEval, -1, nullptr, partial, nblk, s);
+  const int ncand = identity ? 1 : K;
+  const unsigned rows = identity ? 1u : (unsigned)(K + 1);  // + the pending recomputation
+  const int64_t N = h.N;
+  const unsigned mt = (unsigned)((N + kGemmRows - 1) / kGemmRows);
+  auto tiles = [](int64_t n) { return (unsigned)((n + kGemmCols - 1) / kGemmCols); };
+  hipLaunchKernelGGL(k_tf_prep,
+                     dim3((unsigned)((h.copy_stride + kCopyChunk - 1) / kCopyChunk), rows),
+                     dim3(kCopyThreads), 0, s, tf, cands, aux, identity ? kPrepIdentity : kPrepEval,
+                     ncand);
+  hipLaunchKernelGGL(k_tf_embed,
+                     dim3((unsigned)((N * h.D + kCopyThreads * kEmbedPer - 1) / (kCopyThreads * kEmbedPer)), rows),
+                     dim3(kCopyThreads), 0, s, tf, ncand);
+  const dim3 srow((unsigned)((N + (kRowThreads / 64) * kStatRows - 1) / ((kRowThreads / 64) * kStatRows)), rows);
+  const unsigned prow = (unsigned)((N + (kRowThreads / 64) * kPatchRows - 1) / ((kRowThreads / 64) * kPatchRows));
+  for (int b = 0; b < h.NB; ++b) {
+    const int stage = b + 1;
+    hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, stage, 0, ncand);
+    hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, tiles(3 * h.D), rows), dim3(kGemmThreads), 0, s, tf,
+                       stage, (int)kGemmQKV, ncand);
+    hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), rows), dim3(256), 0, s, tf, stage, ncand);
+    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
+                       (int)kGemmO, ncand);
+    hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, stage, 1, ncand);
+    hipLaunchKernelGGL(k_tf_gemm<1>, dim3(mt, tiles(h.M), rows), dim3(kGemmThreads), 0, s, tf, stage,
+                       (int)kGemmFc, ncand);
+    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
+                       (int)kGemmProj, ncand);
+    if (!identity)
+      hipLaunchKernelGGL(k_tf_patch, dim3(prow, (unsigned)K), dim3(kRowThreads), 0, s, tf, cands, aux, b);
+  }
+  hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, h.NB + 1, 2, ncand);
+  hipLaunchKernelGGL(k_tf_gemm<3>, dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
+                     (int)kGemmOut, ncand);
+  if (!identity)
+    hipLaunchKernelGGL(k_tf_dl, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf, cands,
+                       aux, partial, nblk);
+  return hipGetLastError();
 }
 
 hipError_t tf_launch_commit(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                             const Aux* aux, const double* dL, DevState* st, int k, bool fill,
-                            double* bsum, float* partial, int nblk, hipStream_t s) {
-  if (!fill) {
-    // the winner, if it was evaluated incrementally, recomputed densely
-    const hipError_t e = run_pass(tf, h, cands, aux, 1u, kPrepRedo, k, st, partial, nblk, s);
-    if (e != hipSuccess) return e;
-  }
-  const int64_t w = std::max(std::max(h.M, h.D), h.V);
-  const int64_t n = h.N * w;
+                            double* bsum, hipStream_t s) {
+  const int64_t n = h.N * std::max(h.D, h.V);
   hipLaunchKernelGGL(k_tf_commit, dim3((unsigned)((n + kCopyThreads - 1) / kCopyThreads)),
                      dim3(kCopyThreads), 0, s, tf, cands, aux, dL, st, k, fill ? 1 : 0);
   if (fill) {

@@ -42,42 +42,32 @@ struct TfDev {
   const int32_t* tok;                // [N] input symbols
   const int32_t* tgt;                // [N] next-symbol targets
   float* x[kTfMaxBlocks + 1];        // committed residual streams x_0 .. x_NB
+  float* ch[kTfMaxBlocks];           // committed residual stream after attention, per block
+  float* cz;                         // committed logits [N][V]
   float* ell;                        // committed per-position losses
-  // committed intermediate fields, kept for the incremental evaluation of
-  // the MLP, final-LayerNorm and output-layer parameters
-  float* ch[kTfMaxBlocks];           // [N][D] residual stream after attention
-  float* cln2[kTfMaxBlocks];         // [N][D] LN2 output (the MLP input)
-  float* cu[kTfMaxBlocks];           // [N][M] MLP pre-activations
-  float* cnhat;                      // [N][D] final LayerNorm before its gain and bias
-  float* cz;                         // [N][V] logits
-  // per-candidate slots
-  float* sx;      // [K][NB+1][N][D] the candidate's residual streams
-  float* sh;      // [K][NB][N][D] after attention, per block
-  float* sln;     // [K][N][D] LN1 / final LayerNorm output (the next product's input)
-  float* sln2;    // [K][NB][N][D] LN2 output, per block
-  float* su;      // [K][NB][N][M] MLP pre-activations, per block
-  float* sqkv;    // [K][N][3D]
-  float* satt;    // [K][N][D]
-  float* sfc;     // [K][N][M] MLP hidden (GELU of the pre-activations)
-  float* snhat;   // [K][N][D] final LayerNorm before its gain and bias
-  float* slog;    // [K][N][V] logits
-  float* sell;    // [K][N] the candidate's per-position losses
-  float* scopy;   // [K][copy_stride] private copy of the mutated tensor
+  // per-slot activations: slots 0 .. K-1 hold the candidates of a batch,
+  // slot kr the dense recomputation of the last winner that was scored
+  // incrementally (see TfRedo)
+  float* sx;      // [K+1][NB+1][N][D] the slot's residual streams
+  float* sh;      // [K+1][NB][N][D] after attention, per block
+  float* sqkv;    // [K+1][N][3D]
+  float* satt;    // [K+1][N][D]
+  float* sfc;     // [K+1][N][M] MLP hidden (GELU of the pre-activations)
+  float* slog;    // [K+1][N][V] logits
+  float* sell;    // [K+1][N] the slot's per-position losses
+  float2* sst;    // [K+1][N] mean and 1/sqrt(var + eps) of the rows entering the next LayerNorm
+  float* scopy;   // [K+1][copy_stride] private copy of the mutated tensor
   int64_t copy_stride;
-  float** table;  // [K][n_tensors] tensor pointers per candidate
-  int32_t* start; // [K] first stage the candidate recomputes (NB+2: none)
-  int32_t* run;   // [K] first stage it runs in the current pass (NB+2: none)
-  int32_t* xin;   // [K] first residual stream the candidate changes (its slot holds x_xin .. x_NB)
-  int32_t* kind;  // [K] TfKind of the candidate
-  int32_t* pass;  // [1] the slot every block of a one-slot pass works on (-1: its blockIdx)
+  float** table;  // [K+1][n_tensors] tensor pointers per slot
+  int32_t* start; // [K+1] first stage the slot recomputes (NB+2: none)
+  int32_t* run;   // [K+1] first stage it runs in the current pass (NB+2: none)
+  int32_t* xin;   // [K+1] first residual stream it changes (its slot holds x_xin .. x_NB)
+  int32_t* half;  // [K+1] stage whose attention half it takes from the committed state (0: none)
+  int32_t* kind;  // [K+1] TfKind of the candidate
+  int32_t* redo;  // [3] TfRedo: the pending dense recomputation (start, half, xin)
+  int32_t kr;     // the slot of that recomputation (= the largest batch)
+  int32_t pad1;
 };
-
-// The slot a block works on: its grid index, or the one slot of a pass that
-// recomputes a single candidate.
-__device__ inline int tf_slot(const TfDev* tf, unsigned grid_index) {
-  const int p = *tf->pass;
-  return p >= 0 ? p : (int)grid_index;
-}
 
 // How a candidate is evaluated (by its tensor):
 //  kTfDense   the stages from its tensor's on, densely (embeddings, LayerNorm
@@ -98,6 +88,17 @@ __device__ inline int tf_slot(const TfDev* tf, unsigned grid_index) {
 //             block b densely.
 enum TfKind { kTfDense = 0, kTfOutCol = 1, kTfLnfCol = 2, kTfProjCol = 3, kTfFcCol = 4 };
 
+// A winner scored incrementally changes the committed parameters at once,
+// but its fields are recomputed densely (with the committed parameters) in
+// the slot kr of the next evaluation pass, so that the committed fields stay
+// exactly those of a dense pass.  Until the commit after that pass folds
+// them in, the committed state is read through views: x_j from slot kr for
+// j >= xin, the attention output of block b from slot kr where it recomputed
+// that block's attention, the logits and losses from slot kr.  An MLP
+// winner of block b starts at block b's MLP half (half = start = b + 1),
+// an output-layer or final-LayerNorm winner at the final stage.
+enum TfRedo { kRedoStart = 0, kRedoHalf = 1, kRedoXin = 2 };
+
 // Stage of tensor t.
 __host__ __device__ inline int tf_stage(int t, int NB) {
   if (t < 2) return 0;
@@ -115,21 +116,23 @@ hipError_t tf_launch_propose(const TfDev* tf, const TfDev& h, uint64_t t, bool u
 // New values of given candidate records (explicit evaluation).
 hipError_t tf_launch_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux* aux,
                              hipStream_t s);
-// Every stage of every candidate's forward pass from its first changed stage,
-// and the tile sums of its per-position loss changes: partial[k * nblk + b].
+// Every stage of every candidate's forward pass from its first changed stage
+// (and the pending dense recomputation in slot kr), and the tile sums of
+// each candidate's per-position loss changes: partial[k * nblk + b].
 // K = 0 with `identity` runs one unmutated pass in slot 0 (cache fill).
 hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                           const Aux* aux, int K, bool identity, float* partial, int nblk,
                           hipStream_t s);
-// Commit candidate k (k < 0: st->chosen) into the committed state; `fill`
-// copies slot 0 of an identity pass instead and sets the loss.  A candidate
-// that was evaluated incrementally (an MLP, final-LayerNorm or output-layer
-// parameter) is first recomputed densely from its stage, so that the
-// committed fields are always those a dense pass gives (a later dense
-// evaluation then reproduces every position it does not reach, bit for bit).
+// Commit candidate k (k < 0: st->chosen; none if that is negative) into the
+// committed state after the pending recomputation of the previous pass; a
+// winner scored incrementally becomes the next pending recomputation.
+// `fill` copies slot 0 of an identity pass instead, clears the pending
+// recomputation and sets the loss.  Because every committed field is one a
+// dense pass gives, a later dense evaluation reproduces every position it
+// does not reach, bit for bit.
 hipError_t tf_launch_commit(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                             const Aux* aux, const double* dL, DevState* st, int k, bool fill,
-                            double* bsum, float* partial, int nblk, hipStream_t s);
+                            double* bsum, hipStream_t s);
 int tf_loss_blocks(int64_t N);
 
 }  // namespace mca
