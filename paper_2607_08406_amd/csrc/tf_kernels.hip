@@ -35,19 +35,19 @@ namespace mca {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 per wave
 constexpr int kGemmRows = 128;     // rows (positions) per block
 constexpr int kGemmCols = 128;     // output columns per block
 constexpr int kChunkK = 16;        // reduction chunk staged in LDS
-constexpr int kStatRows = 8;       // rows whose LayerNorm statistics a wave takes at once
+constexpr int kStatSteps = 4;      // groups of four rows whose LayerNorm statistics a wave takes at once
 constexpr int kRowThreads = 256;   // row kernels: a wave per row
-constexpr int kPatchRows = 4;      // rows per wave in the MLP patch
+constexpr int kDlSteps = 4;        // groups of four rows a wave of the loss-change kernel loads at once
 constexpr int kLossThreads = 256;
 constexpr int kCopyThreads = 256;
 constexpr int kCopyChunk = 4096;   // floats of a private tensor copy per block
 constexpr int kEmbedPer = 4;       // embedding elements per thread
-constexpr int kMaxPer = 4;         // row elements per lane (d_model <= 256)
 
 __device__ __forceinline__ float* slot_x(const TfDev* tf, int k, int b) {
   return tf->sx + ((int64_t)k * (tf->NB + 1) + b) * tf->N * tf->D;
@@ -94,34 +94,55 @@ __device__ __forceinline__ const float* mlp_input(const TfDev* tf, int k, int b)
   return (tf->half[k] == b + 1) ? tf->ch[b] : slot_h(tf, k, b);
 }
 
-// A row of D <= 256 values held by a wave: element c = lane + 64 u in v[u]
-// (zero beyond D).
-__device__ __forceinline__ void load_row(const float* row, int D, int lane, float (&v)[kMaxPer]) {
+// Rows held by 16 lanes (a quarter wave): lane l of the group holds the
+// column pairs (32 i + 2 l, 32 i + 2 l + 1), i < np = D / 32, so that a
+// float2 load of the group is 128 contiguous bytes; sums over the group by
+// a fixed butterfly.
+template <int P>
+__device__ __forceinline__ void load_pairs(const float* row, int np, int l, floatx2 (&v)[P]) {
+  const floatx2 z2 = {0.f, 0.f};
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    v[u] = (c < D) ? gload(row + c) : 0.f;
-  }
+  for (int i = 0; i < P; ++i)
+    v[i] = (i < np) ? gload(reinterpret_cast<const floatx2*>(row + 32 * i + 2 * l)) : z2;
 }
-// Its mean and 1/sqrt(biased variance + eps): the sum by a fixed butterfly,
-// then the centred sum of squares.
-__device__ __forceinline__ void row_stats(const float (&v)[kMaxPer], int D, int lane, float eps,
-                                          float& mean, float& rstd) {
+__device__ __forceinline__ float sum16(float s) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 16);
+  return s;
+}
+__device__ __forceinline__ float max16(float s) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) s = fmaxf(s, __shfl_xor(s, o, 16));
+  return s;
+}
+// mean and 1/sqrt(biased variance + eps) of a row (zeros beyond np pairs)
+template <int P>
+__device__ __forceinline__ void stats16(const floatx2 (&v)[P], int np, int D, float eps,
+                                        float& mean, float& rstd) {
   float s = 0.f;
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) s += v[u];
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-  mean = s / (float)D;
+  for (int i = 0; i < P; ++i) s += v[i].x + v[i].y;
+  mean = sum16(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const float dv = (lane + 64 * u < D) ? v[u] - mean : 0.f;
-    q += dv * dv;
+  for (int i = 0; i < P; ++i) {
+    if (i < np) {
+      const float a = v[i].x - mean, b = v[i].y - mean;
+      q += a * a + b * b;
+    }
   }
+  rstd = 1.0f / sqrtf(sum16(q) / (float)D + eps);
+}
+// column c of a row held by the group whose first lane is gbase (every lane
+// of the group gets it)
+template <int P>
+__device__ __forceinline__ float col16(const floatx2 (&v)[P], int c, int gbase) {
+  const int i = c >> 5;
+  float sel = 0.f;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  rstd = 1.0f / sqrtf(q / (float)D + eps);
+  for (int ii = 0; ii < P; ++ii)
+    if (ii == i) sel = (c & 1) ? v[ii].y : v[ii].x;
+  return __shfl(sel, gbase + ((c & 31) >> 1), 64);
 }
 
 // erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
@@ -276,103 +297,6 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
     cp[e] = (e == at) ? a.w_new : src[e];
 }
 
-// x_{b+1} of the MLP candidates of block b (kTfProjCol, kTfFcCol), a wave
-// per row: the committed stream plus the candidate's change.  The one
-// pre-activation a candidate needs (unit c.j of an up-projection candidate,
-// unit c.i of a down-projection weight) is recomputed from the committed
-// attention output: LN2 of the row, its dot product with the unit's weight
-// row, plus the unit's bias.  An up-projection candidate moves that unit's
-// pre-activation by de times LN2 column c.i (de for the bias), and the
-// change of its GELU enters every column through the down-projection's
-// column c.j; a down-projection candidate moves column c.j by de times the
-// GELU of unit c.i (de for the bias).
-__global__ __launch_bounds__(kRowThreads) void k_tf_patch(const TfDev* tf, const mca_cand* cands,
-                                                          const Aux* aux, int b) {
-  const int k = blockIdx.y;
-  const int kind = tf->kind[k];
-  if (kind != kTfProjCol && kind != kTfFcCol) return;
-  const mca_cand c = cands[k];
-  if ((c.layer - 2) / kBlockTensors != b) return;
-  const int role = (c.layer - 2) % kBlockTensors;
-  const float de = aux[k].de;
-  const int D = tf->D, M = tf->M;
-  const int64_t N = tf->N;
-  const int lane = threadIdx.x & 63;
-  const int tb = 2 + kBlockTensors * b;
-  const float* hc = view_h(tf, b);
-  const float* xc = view_x(tf, b + 1);
-  float* xo = slot_x(tf, k, b + 1);
-  const bool fc = kind == kTfFcCol;
-  const bool need_u = fc || role == kWproj;
-  const int unit = fc ? c.j : c.i;
-  const float* g2 = tf->param[tb + kLn2G];
-  const float* b2 = tf->param[tb + kLn2B];
-  const float* wfc = tf->param[tb + kWfc] + (int64_t)unit * D;
-  const float* wproj = tf->param[tb + kWproj];
-  float gv[kMaxPer], bv[kMaxPer], wu[kMaxPer], wp[kMaxPer];
-#pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int cc = lane + 64 * u;
-    const bool ok = cc < D;
-    gv[u] = ok ? g2[cc] : 0.f;
-    bv[u] = ok ? b2[cc] : 0.f;
-    wu[u] = (ok && need_u) ? wfc[cc] : 0.f;
-    wp[u] = (ok && fc) ? wproj[(int64_t)cc * M + c.j] : 0.f;
-  }
-  const float bu = need_u ? tf->param[tb + kBfc][unit] : 0.f;
-  const int64_t r0 = ((int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6)) * kPatchRows;
-  // every row's loads first, then the arithmetic
-  float hv[kPatchRows][kMaxPer], xv[kPatchRows][kMaxPer];
-#pragma unroll
-  for (int i = 0; i < kPatchRows; ++i) {
-    const int64_t m = r0 + i < N ? r0 + i : N - 1;
-    if (need_u) load_row(hc + m * D, D, lane, hv[i]);
-    load_row(xc + m * D, D, lane, xv[i]);
-  }
-#pragma unroll
-  for (int i = 0; i < kPatchRows; ++i) {
-    float dg = de;  // a down-projection bias
-    if (need_u) {
-      float mean, rstd;
-      row_stats(hv[i], D, lane, tf->eps, mean, rstd);
-      float ln[kMaxPer];
-      float dot = 0.f;
-#pragma unroll
-      for (int u = 0; u < kMaxPer; ++u) {
-        ln[u] = (lane + 64 * u < D) ? (hv[i][u] - mean) * rstd * gv[u] + bv[u] : 0.f;
-        dot += ln[u] * wu[u];
-      }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
-      const float uu = dot + bu;
-      if (fc) {
-        float du = de;
-        if (role == kWfc) {
-          float sel = ln[0];
-#pragma unroll
-          for (int u = 1; u < kMaxPer; ++u)
-            if (u == (c.i >> 6)) sel = ln[u];
-          du = de * __shfl(sel, c.i & 63, 64);
-        }
-        dg = gelu(uu + du) - gelu(uu);
-      } else {
-        dg = de * gelu(uu);
-      }
-    }
-    if (r0 + i < N) {
-      float* xw = xo + (r0 + i) * D;
-#pragma unroll
-      for (int u = 0; u < kMaxPer; ++u) {
-        const int cc = lane + 64 * u;
-        if (cc < D) {
-          const float x = xv[i][u];
-          xw[cc] = fc ? x + dg * wp[u] : (cc == c.j ? x + dg : x);
-        }
-      }
-    }
-  }
-}
-
 // x_0 = tok_emb[token] + pos_emb[position] for the slots of stage 0
 __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf, int ncand) {
   const int k = slot_of(tf, blockIdx.y, ncand);
@@ -399,28 +323,133 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_embed(const TfDev* tf, int 
 // Mean and 1/sqrt(biased variance + eps) of every row of a LayerNorm's
 // input, for the slots that run it: which 0 LN1 (the input of stage
 // `stage`), 1 LN2 (the attention output block stage-1's MLP reads), 2 the
-// final LayerNorm (the input of stage NB+1).  A wave takes kStatRows rows
-// with all their loads in flight.
-__global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, int stage, int which,
+// final LayerNorm (the input of stage NB+1).  Rows in the 16-lane layout; a
+// wave takes four rows at a time and kStatSteps such groups with every load
+// in flight.  Every product that folds a LayerNorm in takes its statistics
+// from here.  P = D / 32 rounded up to 4 or 8.
+//
+// An MLP candidate of block b (kTfProjCol, kTfFcCol) enters stage b + 2 here
+// with its patched x_{b+1}: the committed stream plus its change, written
+// to its slot before the statistics are taken.  The one pre-activation it
+// needs (unit c.j of an up-projection candidate, unit c.i of a
+// down-projection weight) is recomputed from the committed attention
+// output: LN2 of the row, its dot product with the unit's weight row, plus
+// the unit's bias.  An up-projection candidate moves that pre-activation by
+// de times LN2 column c.i (de for the bias), and the change of its GELU
+// enters every column through the down-projection's column c.j; a
+// down-projection candidate moves column c.j by de times the GELU of unit
+// c.i (de for the bias).
+template <int P>
+__global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const mca_cand* cands,
+                                                          const Aux* aux, int stage, int which,
                                                           int ncand) {
   const int k = slot_of(tf, blockIdx.y, ncand);
   if (which == 0 ? !runs_attention(tf, k, stage - 1) : tf->run[k] > stage) return;
-  const int D = tf->D, lane = threadIdx.x & 63;
+  const int D = tf->D, np = D / 32, lane = threadIdx.x & 63, g = lane >> 4, l = lane & 15;
   const int64_t N = tf->N;
-  const float* X = (which == 1) ? mlp_input(tf, k, stage - 1) : stage_input(tf, k, stage);
   float2* out = tf->sst + (int64_t)k * N;
-  const int64_t r0 = ((int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6)) * kStatRows;
-  float v[kStatRows][kMaxPer];
+  constexpr int kRowsPerWave = 4 * kStatSteps;
+  const int64_t r0 = ((int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6)) * kRowsPerWave;
+  const int kind = tf->kind[k];
+  const bool patch = which != 1 && (kind == kTfProjCol || kind == kTfFcCol) && tf->run[k] == stage;
+  if (!patch) {
+    const float* X = (which == 1) ? mlp_input(tf, k, stage - 1) : stage_input(tf, k, stage);
+    floatx2 v[kStatSteps][P];
 #pragma unroll
-  for (int i = 0; i < kStatRows; ++i) {
-    const int64_t m = r0 + i;
-    load_row(X + (m < N ? m : N - 1) * D, D, lane, v[i]);
+    for (int st = 0; st < kStatSteps; ++st) {
+      const int64_t m = r0 + 4 * st + g;
+      load_pairs(X + (m < N ? m : N - 1) * D, np, l, v[st]);
+    }
+#pragma unroll
+    for (int st = 0; st < kStatSteps; ++st) {
+      float mean, rstd;
+      stats16(v[st], np, D, tf->eps, mean, rstd);
+      const int64_t m = r0 + 4 * st + g;
+      if (l == 0 && m < N) out[m] = make_float2(mean, rstd);
+    }
+    return;
+  }
+  const mca_cand c = cands[k];
+  const int b = stage - 2, M = tf->M;
+  const int role = (c.layer - 2) % kBlockTensors, tb = 2 + kBlockTensors * b;
+  const float de = aux[k].de;
+  const bool fc = kind == kTfFcCol, need_u = fc || role == kWproj;
+  const int unit = fc ? c.j : c.i;
+  const float* g2 = tf->param[tb + kLn2G];
+  const float* b2 = tf->param[tb + kLn2B];
+  const float* wfc = tf->param[tb + kWfc] + (int64_t)unit * D;
+  const float* wproj = tf->param[tb + kWproj];
+  const floatx2 z2 = {0.f, 0.f};
+  floatx2 gv[P], bv[P], wu[P], wp[P];
+#pragma unroll
+  for (int i = 0; i < P; ++i) {
+    const int cc = 32 * i + 2 * l;
+    const bool ok = i < np;
+    gv[i] = ok ? gload(reinterpret_cast<const floatx2*>(g2 + cc)) : z2;
+    bv[i] = ok ? gload(reinterpret_cast<const floatx2*>(b2 + cc)) : z2;
+    wu[i] = (ok && need_u) ? gload(reinterpret_cast<const floatx2*>(wfc + cc)) : z2;
+    wp[i] = z2;
+    if (ok && fc) {
+      wp[i].x = wproj[(int64_t)cc * M + c.j];
+      wp[i].y = wproj[(int64_t)(cc + 1) * M + c.j];
+    }
+  }
+  const float bu = need_u ? tf->param[tb + kBfc][unit] : 0.f;
+  const float* hc = view_h(tf, b);
+  const float* xc = view_x(tf, b + 1);
+  float* xo = slot_x(tf, k, b + 1);
+  floatx2 hv[kStatSteps][P], xv[kStatSteps][P];
+#pragma unroll
+  for (int st = 0; st < kStatSteps; ++st) {
+    const int64_t m0 = r0 + 4 * st + g, m = m0 < N ? m0 : N - 1;
+    if (need_u) load_pairs(hc + m * D, np, l, hv[st]);
+    load_pairs(xc + m * D, np, l, xv[st]);
   }
 #pragma unroll
-  for (int i = 0; i < kStatRows; ++i) {
+  for (int st = 0; st < kStatSteps; ++st) {
+    float dg = de;  // a down-projection bias
+    if (need_u) {
+      float mean, rstd;
+      stats16(hv[st], np, D, tf->eps, mean, rstd);
+      floatx2 lnv[P];
+      float dot = 0.f;
+#pragma unroll
+      for (int i = 0; i < P; ++i) {
+        lnv[i] = z2;
+        if (i < np) {
+          lnv[i].x = (hv[st][i].x - mean) * rstd * gv[i].x + bv[i].x;
+          lnv[i].y = (hv[st][i].y - mean) * rstd * gv[i].y + bv[i].y;
+          dot += lnv[i].x * wu[i].x + lnv[i].y * wu[i].y;
+        }
+      }
+      const float uu = sum16(dot) + bu;
+      if (fc) {
+        const float du = (role == kWfc) ? de * col16(lnv, c.i, lane & ~15) : de;
+        dg = gelu(uu + du) - gelu(uu);
+      } else {
+        dg = de * gelu(uu);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < P; ++i) {
+      const int cc = 32 * i + 2 * l;
+      if (fc) {
+        xv[st][i].x += dg * wp[i].x;
+        xv[st][i].y += dg * wp[i].y;
+      } else {
+        if (cc == c.j) xv[st][i].x += dg;
+        if (cc + 1 == c.j) xv[st][i].y += dg;
+      }
+    }
+    const int64_t m = r0 + 4 * st + g;
+    if (m < N) {
+#pragma unroll
+      for (int i = 0; i < P; ++i)
+        if (i < np) *reinterpret_cast<floatx2*>(xo + m * D + 32 * i + 2 * l) = xv[st][i];
+    }
     float mean, rstd;
-    row_stats(v[i], D, lane, tf->eps, mean, rstd);
-    if (lane == 0 && r0 + i < N) out[r0 + i] = make_float2(mean, rstd);
+    stats16(xv[st], np, D, tf->eps, mean, rstd);
+    if (l == 0 && m < N) out[m] = make_float2(mean, rstd);
   }
 }
 
@@ -442,11 +471,10 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, int s
 // 1/sqrt(variance + eps) of each input row from k_tf_stats, each staged
 // operand element becomes (x - mean) rstd g + b on its way into LDS.
 // EPI: 0 bias only (Q, K, V), 1 GELU (MLP up), 2 residual (attention
-// output, MLP down), 3 logits and each position's cross-entropy (output
-// layer; one column tile): each epilogue gets its own register and LDS
-// budget.
+// output, MLP down), 3 logits and each position's cross-entropy (output layer; one column
+// tile, with the logit tile in LDS).
 template <int EPI>
-__global__ __launch_bounds__(kGemmThreads, EPI == 2 ? 2 : (EPI == 3 ? 1 : 3)) void k_tf_gemm(
+__global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_tf_gemm(
     const TfDev* tf, int stage, int role, int ncand) {
   const int k = slot_of(tf, blockIdx.z, ncand);
   const bool attn_half = role == kGemmQKV || role == kGemmO;
@@ -802,11 +830,12 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
 // LayerNorm's output (de for the bias); a final-LayerNorm gain or bias of
 // column j moves that column by de times its normalized value (or de), which
 // reaches every logit through column j of the output weights.  The
-// normalized value is recomputed from the committed x_NB, a wave per row.
+// normalized value is recomputed from the committed x_NB.  Rows of such a
+// candidate in the 16-lane layout (logit v on lane v mod 16), kDlSteps
+// groups of four rows per wave with every load in flight.
+template <int P>
 __global__ __launch_bounds__(kLossThreads) void k_tf_dl(const TfDev* tf, const mca_cand* cands,
                                                         const Aux* aux, float* partial, int nblk) {
-  __shared__ float zl[kLossThreads * kTfMaxVocab];
-  __shared__ float nh[kLossThreads];
   __shared__ float dl[kLossThreads];
   const int k = blockIdx.y;
   const int kind = tf->kind[k];
@@ -818,41 +847,81 @@ __global__ __launch_bounds__(kLossThreads) void k_tf_dl(const TfDev* tf, const m
   const int nrows = (int)((N - n0 < kLossThreads) ? N - n0 : kLossThreads);
   const float* ell = view_ell(tf);
   const int r = threadIdx.x;
-  float d = 0.f;
+  dl[r] = (!col && active && r < nrows) ? slot_ell(tf, k)[n0 + r] - ell[n0 + r] : 0.f;
   if (col) {
+    __syncthreads();
     const mca_cand c = cands[k];
     const float de = aux[k].de;
-    const float* zc = view_z(tf) + n0 * V;
-    for (int e = threadIdx.x; e < nrows * V; e += kLossThreads) zl[e] = zc[e];
-    const bool out_w = c.layer == nt - 2, lnf_g = c.layer == nt - 4;
-    if (out_w || lnf_g) {
-      const int cc = out_w ? c.i : c.j;
-      const float* xs = view_x(tf, tf->NB);
-      const int lane = threadIdx.x & 63;
-      for (int i = threadIdx.x >> 6; i < nrows; i += kLossThreads / 64) {
-        float v[kMaxPer];
-        load_row(xs + (n0 + i) * D, D, lane, v);
-        float mean, rstd;
-        row_stats(v, D, lane, tf->eps, mean, rstd);
-        if (lane == 0) nh[i] = (xs[(n0 + i) * D + cc] - mean) * rstd;
+    const bool out_w = c.layer == nt - 2, lnf_g = c.layer == nt - 4, need_nh = out_w || lnf_g;
+    const int cc = out_w ? c.i : c.j;
+    const float* zc = view_z(tf);
+    const float* xs = view_x(tf, tf->NB);
+    const float* wo = tf->param[nt - 2];
+    const int lane = threadIdx.x & 63, g = lane >> 4, l = lane & 15, wave = threadIdx.x >> 6;
+    const int np = D / 32;
+    constexpr int kVPer = kTfMaxVocab / 16;
+    float wov[kVPer];
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const int v = l + 16 * j;
+      wov[j] = (kind == kTfLnfCol && v < V) ? wo[(int64_t)v * D + c.j] : 0.f;
+    }
+    const float gi = out_w ? tf->param[nt - 4][c.i] : 0.f;
+    const float bi = out_w ? tf->param[nt - 3][c.i] : 0.f;
+    constexpr int kBatch = 4 * (kLossThreads / 64) * kDlSteps;  // rows per batch of the block
+    for (int base = 0; base < nrows; base += kBatch) {
+      floatx2 xv[kDlSteps][P];
+      float z[kDlSteps][kVPer];
+#pragma unroll
+      for (int st = 0; st < kDlSteps; ++st) {
+        const int rr = base + (wave * kDlSteps + st) * 4 + g;
+        const int64_t n = n0 + (rr < nrows ? rr : 0);
+        if (need_nh) load_pairs(xs + n * D, np, l, xv[st]);
+#pragma unroll
+        for (int j = 0; j < kVPer; ++j) {
+          const int v = l + 16 * j;
+          z[st][j] = (v < V) ? zc[n * V + v] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < kDlSteps; ++st) {
+        const int rr = base + (wave * kDlSteps + st) * 4 + g;
+        const int64_t n = n0 + (rr < nrows ? rr : 0);
+        float nhv = 0.f;
+        if (need_nh) {
+          float mean, rstd;
+          stats16(xv[st], np, D, tf->eps, mean, rstd);
+          nhv = (col16(xv[st], cc, lane & ~15) - mean) * rstd;
+        }
+        const float dz = out_w ? de * fmaf(nhv, gi, bi) : de;
+        const float dcol = lnf_g ? de * nhv : de;
+        float mx = -__builtin_huge_valf();
+#pragma unroll
+        for (int j = 0; j < kVPer; ++j) {
+          const int v = l + 16 * j;
+          if (kind == kTfOutCol) {
+            if (v == c.j) z[st][j] += dz;
+          } else {
+            z[st][j] += dcol * wov[j];
+          }
+          if (v < V) mx = fmaxf(mx, z[st][j]);
+        }
+        mx = max16(mx);
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < kVPer; ++j)
+          if (l + 16 * j < V) sum += fast_exp(z[st][j] - mx);
+        sum = sum16(sum);
+        const int yt = tf->tgt[n];
+        float sel = 0.f;
+#pragma unroll
+        for (int j = 0; j < kVPer; ++j)
+          if (j == (yt >> 4)) sel = z[st][j];
+        const float zt = __shfl(sel, (lane & ~15) + (yt & 15), 64);
+        if (l == 0 && rr < nrows) dl[rr] = ((fast_log(sum) + mx) - zt) - ell[n];
       }
     }
-    __syncthreads();
-    if (r < nrows) {
-      float* z = zl + r * V;
-      if (kind == kTfOutCol) {
-        z[c.j] += out_w ? de * fmaf(nh[r], tf->param[nt - 4][c.i], tf->param[nt - 3][c.i]) : de;
-      } else {
-        const float dcol = lnf_g ? de * nh[r] : de;
-        const float* wo = tf->param[nt - 2];
-        for (int v = 0; v < V; ++v) z[v] += dcol * wo[(int64_t)v * D + c.j];
-      }
-      d = cross_entropy(z, V, tf->tgt[n0 + r]) - ell[n0 + r];
-    }
-  } else if (active && r < nrows) {
-    d = slot_ell(tf, k)[n0 + r] - ell[n0 + r];
   }
-  dl[r] = d;
   __syncthreads();
   for (int o = kLossThreads / 2; o > 0; o >>= 1) {
     if (threadIdx.x < o) dl[threadIdx.x] += dl[threadIdx.x + o];
@@ -970,30 +1039,39 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   hipLaunchKernelGGL(k_tf_embed,
                      dim3((unsigned)((N * h.D + kCopyThreads * kEmbedPer - 1) / (kCopyThreads * kEmbedPer)), rows),
                      dim3(kCopyThreads), 0, s, tf, ncand);
-  const dim3 srow((unsigned)((N + (kRowThreads / 64) * kStatRows - 1) / ((kRowThreads / 64) * kStatRows)), rows);
-  const unsigned prow = (unsigned)((N + (kRowThreads / 64) * kPatchRows - 1) / ((kRowThreads / 64) * kPatchRows));
+  const dim3 srow((unsigned)((N + (kRowThreads / 64) * 4 * kStatSteps - 1) / ((kRowThreads / 64) * 4 * kStatSteps)), rows);
+  const bool wide = h.D > 128;  // row pairs per lane of the 16-lane layout: 4 or 8
+  auto stats = [&](int stage, int which) {
+    if (wide)
+      hipLaunchKernelGGL(k_tf_stats<8>, srow, dim3(kRowThreads), 0, s, tf, cands, aux, stage, which, ncand);
+    else
+      hipLaunchKernelGGL(k_tf_stats<4>, srow, dim3(kRowThreads), 0, s, tf, cands, aux, stage, which, ncand);
+  };
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
-    hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, stage, 0, ncand);
+    stats(stage, 0);
     hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, tiles(3 * h.D), rows), dim3(kGemmThreads), 0, s, tf,
                        stage, (int)kGemmQKV, ncand);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), rows), dim3(256), 0, s, tf, stage, ncand);
     hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmO, ncand);
-    hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, stage, 1, ncand);
+    stats(stage, 1);
     hipLaunchKernelGGL(k_tf_gemm<1>, dim3(mt, tiles(h.M), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmFc, ncand);
     hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmProj, ncand);
-    if (!identity)
-      hipLaunchKernelGGL(k_tf_patch, dim3(prow, (unsigned)K), dim3(kRowThreads), 0, s, tf, cands, aux, b);
   }
-  hipLaunchKernelGGL(k_tf_stats, srow, dim3(kRowThreads), 0, s, tf, h.NB + 1, 2, ncand);
+  stats(h.NB + 1, 2);
   hipLaunchKernelGGL(k_tf_gemm<3>, dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
                      (int)kGemmOut, ncand);
-  if (!identity)
-    hipLaunchKernelGGL(k_tf_dl, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf, cands,
-                       aux, partial, nblk);
+  if (!identity) {
+    if (wide)
+      hipLaunchKernelGGL(k_tf_dl<8>, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf,
+                         cands, aux, partial, nblk);
+    else
+      hipLaunchKernelGGL(k_tf_dl<4>, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf,
+                         cands, aux, partial, nblk);
+  }
   return hipGetLastError();
 }
 
