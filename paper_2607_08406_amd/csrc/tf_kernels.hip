@@ -458,8 +458,8 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // A 128 x 128 output tile per block; wave (wr, wc) takes the 64 x 64
 // quarter (wr, wc) as four by four 16 x 16 MFMA tiles, so each operand
 // fragment read from LDS feeds four MFMAs.  The reduction dimension runs in
-// chunks of 16 staged in LDS (double-buffered: the next chunk's global loads
-// are in flight while the current one is multiplied).  Inside a chunk, k
+// chunks of 16 staged in LDS (two buffers; the loads run two chunks ahead of
+// the products).  Inside a chunk, k
 // runs in blocks of 16; lane group q holds k = 16 kb + 4 q + t (t = 0..3),
 // used by four MFMAs in turn, so each lane reads its operands as float4.
 // Rows and columns beyond the matrix are clamped on load and dropped on
@@ -468,8 +468,9 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // from tensor n / D of the three.
 // LayerNorm (Q, K, V: LN1 of the stage input; MLP up: LN2 of the attention
 // output; output layer: the final LayerNorm): with the mean and
-// 1/sqrt(variance + eps) of each input row from k_tf_stats, each staged
-// operand element becomes (x - mean) rstd g + b on its way into LDS.
+// 1/sqrt(variance + eps) of each input row from k_tf_stats and the gain and
+// bias staged in LDS, each staged operand element becomes
+// (x - mean) rstd g + b on its way into LDS.
 // EPI: 0 bias only (Q, K, V), 1 GELU (MLP up), 2 residual (attention
 // output, MLP down), 3 logits and each position's cross-entropy (output layer; one column
 // tile, with the logit tile in LDS).
@@ -535,8 +536,15 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
   const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
   const int wr = wave >> 1, wc = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.x * kGemmRows;
-  const bool ln = lg != nullptr;
+  constexpr bool ln = EPI != 2;  // the products that read a LayerNorm
   const float2* stats = tf->sst + (int64_t)k * N;  // the input rows' LayerNorm statistics
+  __shared__ __attribute__((aligned(16))) float s_g[ln ? 256 : 4], s_b[ln ? 256 : 4];
+  if constexpr (ln) {
+    for (int c = threadIdx.x; c < Kd; c += kGemmThreads) {
+      s_g[c] = lg[c];
+      s_b[c] = lb[c];
+    }
+  }
   // staging: thread tid loads float4 number tid + 256 u of the A chunk
   // (128 rows x 4 float4) and of the B chunk (128 rows x 4 float4); its A
   // elements sit in one float4 column group of every chunk
@@ -563,33 +571,35 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
     gb[u] = wrow(n < Nout ? n : Nout - 1) + 4 * (e % (kChunkK / 4));
   }
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-  floatx4 ra0[kA4], rb0[kB4];
-  floatx4 rg = zero, rbe = zero;  // LayerNorm gain and bias of the thread's A columns
-  auto fetch = [&](int c, floatx4 (&ra)[kA4], floatx4 (&rb)[kB4]) {
-#pragma unroll
-    for (int u = 0; u < kA4; ++u) ra[u] = gload(reinterpret_cast<const floatx4*>(ga[u] + kChunkK * c));
-#pragma unroll
-    for (int u = 0; u < kB4; ++u) rb[u] = gload(reinterpret_cast<const floatx4*>(gb[u] + kChunkK * c));
-    if (ln) {
-      rg = gload(reinterpret_cast<const floatx4*>(lg + kChunkK * c + acol));
-      rbe = gload(reinterpret_cast<const floatx4*>(lb + kChunkK * c + acol));
-    }
+  // a chunk's operands on their way from memory into LDS
+  struct Staged {
+    floatx4 a[kA4];
+    floatx4 b[kB4];
   };
-  auto store = [&](int buf, const floatx4 (&ra)[kA4], const floatx4 (&rb)[kB4]) {
+  auto fetch = [&](int c, Staged& S) {
+#pragma unroll
+    for (int u = 0; u < kA4; ++u) S.a[u] = gload(reinterpret_cast<const floatx4*>(ga[u] + kChunkK * c));
+#pragma unroll
+    for (int u = 0; u < kB4; ++u) S.b[u] = gload(reinterpret_cast<const floatx4*>(gb[u] + kChunkK * c));
+  };
+  auto store = [&](int c, const Staged& S) {
+    const int buf = c & 1;
 #pragma unroll
     for (int u = 0; u < kA4; ++u) {
       const int e = tid + kGemmThreads * u;
-      floatx4 a = ra[u];
-      if (ln) {
+      floatx4 a = S.a[u];
+      if constexpr (ln) {
+        const floatx4 g4 = *reinterpret_cast<const floatx4*>(&s_g[kChunkK * c + acol]);
+        const floatx4 b4 = *reinterpret_cast<const floatx4*>(&s_b[kChunkK * c + acol]);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) a[t] = fmaf((a[t] - amu[u]) * ars[u], rg[t], rbe[t]);
+        for (int t = 0; t < 4; ++t) a[t] = fmaf((a[t] - amu[u]) * ars[u], g4[t], b4[t]);
       }
       *reinterpret_cast<floatx4*>(&As[buf][e / (kChunkK / 4)][acol]) = a;
     }
 #pragma unroll
     for (int u = 0; u < kB4; ++u) {
       const int e = tid + kGemmThreads * u;
-      *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = rb[u];
+      *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = S.b[u];
     }
   };
   floatx4 acc[4][4];
@@ -633,18 +643,27 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
           res[sb][cb][v] = (m < N && n < Nout) ? R[m * D + n] : 0.f;
         }
   };
+  // Chunk c + 2's loads are issued while chunk c is multiplied and chunk
+  // c + 1 (loaded one chunk earlier) goes into the other LDS buffer: two
+  // register sets, the loop unrolled by two so that each is fixed.
   const int nc = Kd / kChunkK;
-  fetch(0, ra0, rb0);
-  store(0, ra0, rb0);
+  Staged S0, S1;
+  fetch(0, S0);
+  if (nc > 1) fetch(1, S1);
+  if constexpr (ln) __syncthreads();  // the LayerNorm gain and bias are in LDS
+  store(0, S0);
   __syncthreads();
-  for (int c = 0; c < nc; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < nc) fetch(c + 1, ra0, rb0);
+  auto step = [&](int c, Staged& Sfree, Staged& Snext) {
+    if (c + 2 < nc) fetch(c + 2, Sfree);
     if constexpr (EPI == 2)
       if (c + 1 == nc) load_residual();
-    compute(buf);
-    if (c + 1 < nc) store(buf ^ 1, ra0, rb0);
+    compute(c & 1);
+    if (c + 1 < nc) store(c + 1, Snext);
     __syncthreads();
+  };
+  for (int c = 0; c < nc; c += 2) {
+    step(c, S0, S1);
+    if (c + 1 < nc) step(c + 1, S1, S0);
   }
   float bvv[4];
 #pragma unroll
