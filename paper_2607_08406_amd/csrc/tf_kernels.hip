@@ -463,7 +463,7 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // runs in blocks of 16; lane group q holds k = 16 kb + 4 q + t (t = 0..3),
 // used by four MFMAs in turn, so each lane reads its operands as float4.
 // Rows and columns beyond the matrix are clamped on load and dropped on
-// store.  Requires Kd % 16 == 0.  The Q, K and V projections are one
+// store.  Requires Kd % 32 == 0.  The Q, K and V projections are one
 // product with 3 D output columns: column n takes its weight row and bias
 // from tensor n / D of the three.
 // LayerNorm (Q, K, V: LN1 of the stage input; MLP up: LN2 of the attention
@@ -645,26 +645,32 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
   };
   // Chunk c + 2's loads are issued while chunk c is multiplied and chunk
   // c + 1 (loaded one chunk earlier) goes into the other LDS buffer: two
-  // register sets, the loop unrolled by two so that each is fixed.
+  // register sets, the loop unrolled by two so that each is fixed.  The
+  // number of chunks is even (Kd % 32 == 0), so every load in the loop is
+  // unconditional and each store waits only for its own chunk's loads.
   const int nc = Kd / kChunkK;
   Staged S0, S1;
   fetch(0, S0);
-  if (nc > 1) fetch(1, S1);
+  fetch(1, S1);
   if constexpr (ln) __syncthreads();  // the LayerNorm gain and bias are in LDS
   store(0, S0);
   __syncthreads();
-  auto step = [&](int c, Staged& Sfree, Staged& Snext) {
-    if (c + 2 < nc) fetch(c + 2, Sfree);
-    if constexpr (EPI == 2)
-      if (c + 1 == nc) load_residual();
-    compute(c & 1);
-    if (c + 1 < nc) store(c + 1, Snext);
+  for (int c = 0; c + 2 < nc; c += 2) {
+    fetch(c + 2, S0);
+    compute(0);
+    store(c + 1, S1);
     __syncthreads();
-  };
-  for (int c = 0; c < nc; c += 2) {
-    step(c, S0, S1);
-    if (c + 1 < nc) step(c + 1, S1, S0);
+    fetch(c + 3, S1);
+    compute(1);
+    store(c + 2, S0);
+    __syncthreads();
   }
+  compute(0);
+  store(nc - 1, S1);
+  __syncthreads();
+  if constexpr (EPI == 2) load_residual();
+  compute(1);
+  __syncthreads();
   float bvv[4];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb) {
