@@ -39,7 +39,6 @@ typedef float floatx2 __attribute__((ext_vector_type(2)));
 
 constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 per wave
 constexpr int kGemmRows = 128;     // rows (positions) per block
-constexpr int kGemmCols = 128;     // output columns per block
 constexpr int kChunkK = 16;        // reduction chunk staged in LDS
 constexpr int kStatSteps = 4;      // groups of four rows whose LayerNorm statistics a wave takes at once
 constexpr int kRowThreads = 256;   // row kernels: a wave per row
@@ -455,9 +454,9 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 
 // Y = LN(X) W^T + b (LN: the LayerNorm of the input rows, for the products
 // that read one) with an epilogue, for the slots active in `stage`.
-// A 128 x 128 output tile per block; wave (wr, wc) takes the 64 x 64
-// quarter (wr, wc) as four by four 16 x 16 MFMA tiles, so each operand
-// fragment read from LDS feeds four MFMAs.  The reduction dimension runs in
+// A 128 x 32 CB output tile per block; wave (wr, wc) takes the 64 x 16 CB
+// quarter (wr, wc) as four by CB 16 x 16 MFMA tiles, so each operand
+// fragment read from LDS feeds several MFMAs.  The reduction dimension runs in
 // chunks of 16 staged in LDS (two buffers; the loads run two chunks ahead of
 // the products).  Inside a chunk, k
 // runs in blocks of 16; lane group q holds k = 16 kb + 4 q + t (t = 0..3),
@@ -474,8 +473,8 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // EPI: 0 bias only (Q, K, V), 1 GELU (MLP up), 2 residual (attention
 // output, MLP down), 3 logits and each position's cross-entropy (output layer; one column
 // tile, with the logit tile in LDS).
-template <int EPI>
-__global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_tf_gemm(
+template <int EPI, int CB>
+__global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2 : 3) void k_tf_gemm(
     const TfDev* tf, int stage, int role, int ncand) {
   const int k = slot_of(tf, blockIdx.z, ncand);
   const bool attn_half = role == kGemmQKV || role == kGemmO;
@@ -513,7 +512,8 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
       W = tab[nt - 2]; bias = tab[nt - 1]; Y = slot_log(tf, k); ldY = V; Nout = V;
       break;
   }
-  const int n0 = blockIdx.y * kGemmCols;
+  constexpr int kTileN = 32 * CB;  // output columns of the block, 16 CB per wave
+  const int n0 = blockIdx.y * kTileN;
   if (n0 >= Nout) return;
   // weight row and bias of output column n
   auto wrow = [&](int n) -> const float* {
@@ -526,12 +526,13 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
     const int w = n / D;
     return tab[tb + kBq + 2 * w][n - w * D];
   };
-  constexpr int kStage = 2 * kGemmRows * (kChunkK + 4);  // floats of one operand's double buffer
+  constexpr int kStage = 2 * kGemmRows * (kChunkK + 4);  // floats of the A operand's double buffer
+  constexpr int kStageB = 2 * kTileN * (kChunkK + 4);
   constexpr int kZ = kGemmRows * (kTfMaxVocab + 1);      // the output layer's logit tile
-  constexpr int kSmem = (EPI == 3 && kZ > 2 * kStage) ? kZ : 2 * kStage;
+  constexpr int kSmem = (EPI == 3 && kZ > kStage + kStageB) ? kZ : kStage + kStageB;
   __shared__ __attribute__((aligned(16))) float smem[kSmem];
   auto As = reinterpret_cast<float (*)[kGemmRows][kChunkK + 4]>(smem);
-  auto Bs = reinterpret_cast<float (*)[kGemmCols][kChunkK + 4]>(smem + kStage);
+  auto Bs = reinterpret_cast<float (*)[kTileN][kChunkK + 4]>(smem + kStage);
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
   const int wr = wave >> 1, wc = wave & 1;
@@ -549,7 +550,7 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
   // (128 rows x 4 float4) and of the B chunk (128 rows x 4 float4); its A
   // elements sit in one float4 column group of every chunk
   constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 2
-  constexpr int kB4 = kGemmCols * kChunkK / 4 / kGemmThreads;  // 2
+  constexpr int kB4 = kTileN * kChunkK / 4 / kGemmThreads;  // CB / 2
   const int acol = 4 * (tid % (kChunkK / 4));
   const float* ga[kA4];
   const float* gb[kB4];
@@ -602,44 +603,44 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
       *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = S.b[u];
     }
   };
-  floatx4 acc[4][4];
+  floatx4 acc[4][CB];
 #pragma unroll
   for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[sb][cb] = zero;
+    for (int cb = 0; cb < CB; ++cb) acc[sb][cb] = zero;
   auto compute = [&](int buf) {
 #pragma unroll
     for (int kb = 0; kb < kChunkK / 16; ++kb) {
-      floatx4 a[4], bv[4];
+      floatx4 a[4], bv[CB];
 #pragma unroll
       for (int sb = 0; sb < 4; ++sb)
         a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][64 * wr + 16 * sb + li][16 * kb + 4 * q]);
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][64 * wc + 16 * cb + li][16 * kb + 4 * q]);
+      for (int cb = 0; cb < CB; ++cb)
+        bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][16 * CB * wc + 16 * cb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
-          for (int cb = 0; cb < 4; ++cb)
+          for (int cb = 0; cb < CB; ++cb)
             acc[sb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sb][t], bv[cb][t], acc[sb][cb], 0, 0, 0);
     }
   };
   // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li.
   // The residual a lane adds is loaded before the last chunk's products, so
   // its latency hides behind them.
-  float res[4][4][4];
+  float res[4][CB][4];
   (void)res;
   auto load_residual = [&]() {
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
-          const int n = n0 + 64 * wc + 16 * cb + li;
+          const int n = n0 + 16 * CB * wc + 16 * cb + li;
           res[sb][cb][v] = (m < N && n < Nout) ? R[m * D + n] : 0.f;
         }
   };
@@ -671,10 +672,10 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
   if constexpr (EPI == 2) load_residual();
   compute(1);
   __syncthreads();
-  float bvv[4];
+  float bvv[CB];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) {
-    const int n = n0 + 64 * wc + 16 * cb + li;
+  for (int cb = 0; cb < CB; ++cb) {
+    const int n = n0 + 16 * CB * wc + 16 * cb + li;
     bvv[cb] = (n < Nout) ? bias_of(n) : 0.f;
   }
   if constexpr (EPI == 3) {
@@ -685,11 +686,11 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
 #pragma unroll
     for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int r = 64 * wr + 16 * sb + 4 * q + v;
-          const int n = 64 * wc + 16 * cb + li;
+          const int n = 16 * CB * wc + 16 * cb + li;
           if (n < Nout) {
             const float y = acc[sb][cb][v] + bvv[cb];
             Z[r * ldz + n] = y;
@@ -704,11 +705,11 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 2 || EPI == 3 ? 2 : 3) void k_
 #pragma unroll
   for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb)
+    for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
-        const int n = n0 + 64 * wc + 16 * cb + li;
+        const int n = n0 + 16 * CB * wc + 16 * cb + li;
         if (m < N && n < Nout) {
           float y = acc[sb][cb][v] + bvv[cb];
           if constexpr (EPI == 1) y = gelu(y);
@@ -1056,7 +1057,7 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   const unsigned rows = identity ? 1u : (unsigned)(K + 1);  // + the pending recomputation
   const int64_t N = h.N;
   const unsigned mt = (unsigned)((N + kGemmRows - 1) / kGemmRows);
-  auto tiles = [](int64_t n) { return (unsigned)((n + kGemmCols - 1) / kGemmCols); };
+  auto tiles = [](int64_t n, int w) { return (unsigned)((n + w - 1) / w); };
   hipLaunchKernelGGL(k_tf_prep,
                      dim3((unsigned)((h.copy_stride + kCopyChunk - 1) / kCopyChunk), rows),
                      dim3(kCopyThreads), 0, s, tf, cands, aux, identity ? kPrepIdentity : kPrepEval,
@@ -1075,19 +1076,19 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     stats(stage, 0);
-    hipLaunchKernelGGL(k_tf_gemm<0>, dim3(mt, tiles(3 * h.D), rows), dim3(kGemmThreads), 0, s, tf,
+    hipLaunchKernelGGL((k_tf_gemm<0, 4>), dim3(mt, tiles(3 * h.D, 128), rows), dim3(kGemmThreads), 0, s, tf,
                        stage, (int)kGemmQKV, ncand);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), rows), dim3(256), 0, s, tf, stage, ncand);
-    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmO, ncand);
     stats(stage, 1);
-    hipLaunchKernelGGL(k_tf_gemm<1>, dim3(mt, tiles(h.M), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<1, 4>), dim3(mt, tiles(h.M, 128), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmFc, ncand);
-    hipLaunchKernelGGL(k_tf_gemm<2>, dim3(mt, tiles(h.D), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmProj, ncand);
   }
   stats(h.NB + 1, 2);
-  hipLaunchKernelGGL(k_tf_gemm<3>, dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
+  hipLaunchKernelGGL((k_tf_gemm<3, 4>), dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
                      (int)kGemmOut, ncand);
   if (!identity) {
     if (wide)
