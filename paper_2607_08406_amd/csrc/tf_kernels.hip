@@ -1076,13 +1076,13 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     stats(stage, 0);
-    hipLaunchKernelGGL((k_tf_gemm<0, 4>), dim3(mt, tiles(3 * h.D, 128), rows), dim3(kGemmThreads), 0, s, tf,
+    hipLaunchKernelGGL((k_tf_gemm<0, 2>), dim3(mt, tiles(3 * h.D, 64), rows), dim3(kGemmThreads), 0, s, tf,
                        stage, (int)kGemmQKV, ncand);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), rows), dim3(256), 0, s, tf, stage, ncand);
     hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmO, ncand);
     stats(stage, 1);
-    hipLaunchKernelGGL((k_tf_gemm<1, 4>), dim3(mt, tiles(h.M, 128), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<1, 2>), dim3(mt, tiles(h.M, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmFc, ncand);
     hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmProj, ncand);
