@@ -720,14 +720,18 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
 }
 
 // Causal softmax attention, scale 1/sqrt(32), on the matrix cores: a block
-// of 4 waves per (sequence, head) of one candidate.  Q, K and V of the
-// sequence and head sit in LDS (rows padded).  Row block rb (16 queries)
-// takes key blocks 0..rb: the scores S = Q K^T tile by tile (16 x 16, two
-// k-blocks of 16 over the head dimension, operands read as float4), the row
-// maximum and the sum of exponentials by a fixed butterfly over the 16 lanes
-// that hold a row, then O = P V with P re-laid out through LDS into the
-// A-operand layout.  Wave w takes row blocks w and 7-w (T = 128: every wave
-// walks 9 tiles); keys after the query are masked.
+// of 4 waves per (sequence, head) of one slot.  Q, K and V of the sequence
+// and head sit in LDS (rows padded).  Query block rb (16 queries) takes key
+// blocks 0..rb and works on transposed tiles: the scores S^T = K Q^T (keys
+// as rows, queries as columns; two k-blocks of 16 over the head dimension,
+// operands read as float4), so that lane (q, li) holds keys 4 q + v of each
+// key block for query li.  The softmax of a query is then a reduction over
+// the lane's registers and the four lanes li, li + 16, li + 32, li + 48 (a
+// fixed butterfly), and the probabilities are already in the B-operand
+// layout of O^T = V^T P^T: the product's k index runs over keys
+// 16 cb + 4 q + t, the same order for both operands, with V read from LDS.
+// Wave w takes query blocks w and 7-w (T = 128: every wave walks 9 tiles);
+// keys after the query are masked.
 __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int ncand) {
   const int k = slot_of(tf, blockIdx.y, ncand);
   if (!runs_attention(tf, k, stage - 1)) return;
@@ -735,7 +739,6 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
   __shared__ __attribute__((aligned(16))) float Qs[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Ks[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Vs[kTfMaxCtx][kS];
-  __shared__ float Ps[4][16][17];
   const int T = tf->T, D = tf->D, H = tf->H;
   const int s = blockIdx.x / H, h = blockIdx.x - (blockIdx.x / H) * H;
   const int64_t ND = tf->N * D;
@@ -774,12 +777,13 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
   for (int pass = 0; pass < 2; ++pass) {
     const int rb = (pass == 0) ? wave : 7 - wave;
     if (rb >= nrb || (pass == 1 && rb == wave)) continue;
-    // scores of row block rb against key blocks 0..rb
+    const int query = 16 * rb + li;
+    // scores S^T of key blocks 0..rb against query block rb
     floatx4 sc[kTfMaxCtx / 16];
-    floatx4 qa[2];
+    floatx4 qb[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
-      qa[kb] = *reinterpret_cast<const floatx4*>(&Qs[16 * rb + li][16 * kb + 4 * q]);
+      qb[kb] = *reinterpret_cast<const floatx4*>(&Qs[16 * rb + li][16 * kb + 4 * q]);
 #pragma unroll
     for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
       sc[cb] = zero;
@@ -789,60 +793,52 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
           const floatx4 kk = *reinterpret_cast<const floatx4*>(&Ks[16 * cb + li][16 * kb + 4 * q]);
 #pragma unroll
           for (int t = 0; t < 4; ++t)
-            sc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[kb][t], kk[t], sc[cb], 0, 0, 0);
+            sc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(kk[t], qb[kb][t], sc[cb], 0, 0, 0);
         }
       }
     }
-    // lane (q, li) holds scores of rows 16 rb + 4 q + v, keys 16 cb + li
-    float mx[4], sm[4];
+    // lane (q, li): keys 16 cb + 4 q + v of query li
+    float m = -__builtin_huge_valf();
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = 16 * rb + 4 * q + v;
-      float m = -__builtin_huge_valf();
+    for (int cb = 0; cb < kTfMaxCtx / 16; ++cb)
 #pragma unroll
-      for (int cb = 0; cb < kTfMaxCtx / 16; ++cb)
-        if (cb <= rb && 16 * cb + li <= row) m = fmaxf(m, sc[cb][v] * scale);
+      for (int v = 0; v < 4; ++v)
+        if (cb <= rb && 16 * cb + 4 * q + v <= query) m = fmaxf(m, sc[cb][v] * scale);
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    float sum = 0.f;
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-      mx[v] = m;
-      float sum = 0.f;
+    for (int cb = 0; cb < kTfMaxCtx / 16; ++cb)
 #pragma unroll
-      for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
-        const float p = (cb <= rb && 16 * cb + li <= row) ? fast_exp(sc[cb][v] * scale - m) : 0.f;
+      for (int v = 0; v < 4; ++v) {
+        const float p = (cb <= rb && 16 * cb + 4 * q + v <= query) ? fast_exp(sc[cb][v] * scale - m) : 0.f;
         sc[cb][v] = p;
         sum += p;
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, 64);
-      sm[v] = sum;
-    }
-    // O = P V: per key block, P through LDS into the A layout (row li, key 4 t + q)
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+    // O^T = V^T P^T, dims 16 db + row, queries as columns
     floatx4 oc[2] = {zero, zero};
 #pragma unroll
     for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
       if (cb > rb) break;  // uniform over the wave
 #pragma unroll
-      for (int v = 0; v < 4; ++v) Ps[wave][4 * q + v][li] = sc[cb][v];
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const float pa = Ps[wave][li][4 * t + q];
-        const int key = 16 * cb + 4 * t + q;
+        const int key = 16 * cb + 4 * q + t;
 #pragma unroll
         for (int db = 0; db < 2; ++db)
-          oc[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, Vs[key][16 * db + li], oc[db], 0, 0, 0);
+          oc[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(Vs[key][16 * db + li], sc[cb][t], oc[db], 0, 0, 0);
       }
-      __builtin_amdgcn_wave_barrier();  // every lane read Ps before the next tile rewrites it
     }
-    // lane (q, li) holds O rows 16 rb + 4 q + v, columns 16 db + li
+    // lane (q, li) holds O[query li][dims 16 db + 4 q + v]
+    if (query < T) {
+      const float inv = 1.0f / sum;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = 16 * rb + 4 * q + v;
-      if (row < T) {
+      for (int db = 0; db < 2; ++db) {
+        floatx4 o;
 #pragma unroll
-        for (int db = 0; db < 2; ++db) outb[(int64_t)row * D + 16 * db + li] = oc[db][v] / sm[v];
+        for (int v = 0; v < 4; ++v) o[v] = oc[db][v] * inv;
+        *reinterpret_cast<floatx4*>(outb + (int64_t)query * D + 16 * db + 4 * q) = o;
       }
     }
   }
