@@ -720,8 +720,9 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
 }
 
 // Causal softmax attention, scale 1/sqrt(32), on the matrix cores: a block
-// of 4 waves per (sequence, head) of one slot.  Q, K and V of the sequence
-// and head sit in LDS (rows padded).  Query block rb (16 queries) takes key
+// of 4 waves per (sequence, head) of one slot.  K and V of the sequence and
+// head sit in LDS (rows padded); each wave reads its own queries from
+// memory.  Query block rb (16 queries) takes key
 // blocks 0..rb and works on transposed tiles: the scores S^T = K Q^T (keys
 // as rows, queries as columns; two k-blocks of 16 over the head dimension,
 // operands read as float4), so that lane (q, li) holds keys 4 q + v of each
@@ -736,7 +737,6 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
   const int k = slot_of(tf, blockIdx.y, ncand);
   if (!runs_attention(tf, k, stage - 1)) return;
   constexpr int kS = kTfHeadDim + 4;  // padded row
-  __shared__ __attribute__((aligned(16))) float Qs[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Ks[kTfMaxCtx][kS];
   __shared__ __attribute__((aligned(16))) float Vs[kTfMaxCtx][kS];
   const int T = tf->T, D = tf->D, H = tf->H;
@@ -747,7 +747,7 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
     // 128 rows x 8 float4 per tensor: four float4 of each per thread, every
     // load issued before the LDS stores
     constexpr int kPer = kTfMaxCtx * kTfHeadDim / 4 / 256;
-    floatx4 rq[kPer], rk[kPer], rv[kPer];
+    floatx4 rk[kPer], rv[kPer];
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const int e = threadIdx.x + 256 * u;
@@ -755,7 +755,6 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
       const bool ok = t < T;
       const float* row = base + (int64_t)(ok ? t : 0) * 3 * D + 4 * c4;
       const floatx4 z = {0.f, 0.f, 0.f, 0.f};
-      rq[u] = ok ? gload(reinterpret_cast<const floatx4*>(row)) : z;
       rk[u] = ok ? gload(reinterpret_cast<const floatx4*>(row + D)) : z;
       rv[u] = ok ? gload(reinterpret_cast<const floatx4*>(row + 2 * D)) : z;
     }
@@ -763,7 +762,6 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
     for (int u = 0; u < kPer; ++u) {
       const int e = threadIdx.x + 256 * u;
       const int t = e / (kTfHeadDim / 4), c4 = e - t * (kTfHeadDim / 4);
-      *reinterpret_cast<floatx4*>(&Qs[t][4 * c4]) = rq[u];
       *reinterpret_cast<floatx4*>(&Ks[t][4 * c4]) = rk[u];
       *reinterpret_cast<floatx4*>(&Vs[t][4 * c4]) = rv[u];
     }
@@ -783,7 +781,8 @@ __global__ __launch_bounds__(256) void k_tf_attn(const TfDev* tf, int stage, int
     floatx4 qb[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
-      qb[kb] = *reinterpret_cast<const floatx4*>(&Qs[16 * rb + li][16 * kb + 4 * q]);
+      qb[kb] = (query < T) ? gload(reinterpret_cast<const floatx4*>(base + (int64_t)query * 3 * D + 16 * kb + 4 * q))
+                           : zero;
 #pragma unroll
     for (int cb = 0; cb < kTfMaxCtx / 16; ++cb) {
       sc[cb] = zero;
