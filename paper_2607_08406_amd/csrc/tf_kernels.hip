@@ -454,9 +454,10 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 
 // Y = LN(X) W^T + b (LN: the LayerNorm of the input rows, for the products
 // that read one) with an epilogue, for the slots active in `stage`.
-// A 128 x 32 CB output tile per block; wave (wr, wc) takes the 64 x 16 CB
-// quarter (wr, wc) as four by CB 16 x 16 MFMA tiles, so each operand
-// fragment read from LDS feeds several MFMAs.  The reduction dimension runs in
+// A 128 x 16 CB WC output tile per block: the 4 waves form a (4 / WC) x WC
+// grid and wave (wr, wc) takes its 16 SB x 16 CB part (SB = 2 WC) as SB by
+// CB 16 x 16 MFMA tiles, so each operand fragment read from LDS feeds
+// several MFMAs.  The reduction dimension runs in
 // chunks of 16 staged in LDS (two buffers; the loads run two chunks ahead of
 // the products).  Inside a chunk, k
 // runs in blocks of 16; lane group q holds k = 16 kb + 4 q + t (t = 0..3),
@@ -473,8 +474,8 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // EPI: 0 bias only (Q, K, V), 1 GELU (MLP up), 2 residual (attention
 // output, MLP down), 3 logits and each position's cross-entropy (output layer; one column
 // tile, with the logit tile in LDS).
-template <int EPI, int CB>
-__global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2 : 3) void k_tf_gemm(
+template <int EPI, int CB, int WC>
+__global__ __launch_bounds__(kGemmThreads, EPI == 2 && CB == 4 ? 2 : 3) void k_tf_gemm(
     const TfDev* tf, int stage, int role, int ncand) {
   const int k = slot_of(tf, blockIdx.z, ncand);
   const bool attn_half = role == kGemmQKV || role == kGemmO;
@@ -512,7 +513,9 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
       W = tab[nt - 2]; bias = tab[nt - 1]; Y = slot_log(tf, k); ldY = V; Nout = V;
       break;
   }
-  constexpr int kTileN = 32 * CB;  // output columns of the block, 16 CB per wave
+  constexpr int kWR = 4 / WC;          // waves along the rows
+  constexpr int SB = 8 / kWR;          // 16-row MFMA tiles per wave
+  constexpr int kTileN = 16 * CB * WC; // output columns of the block, 16 CB per wave
   const int n0 = blockIdx.y * kTileN;
   if (n0 >= Nout) return;
   // weight row and bias of output column n
@@ -528,14 +531,14 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
   };
   constexpr int kStage = 2 * kGemmRows * (kChunkK + 4);  // floats of the A operand's double buffer
   constexpr int kStageB = 2 * kTileN * (kChunkK + 4);
-  constexpr int kZ = kGemmRows * (kTfMaxVocab + 1);      // the output layer's logit tile
+  constexpr int kZ = kGemmRows * (kTileN + 1);           // the output layer's logit tile
   constexpr int kSmem = (EPI == 3 && kZ > kStage + kStageB) ? kZ : kStage + kStageB;
   __shared__ __attribute__((aligned(16))) float smem[kSmem];
   auto As = reinterpret_cast<float (*)[kGemmRows][kChunkK + 4]>(smem);
   auto Bs = reinterpret_cast<float (*)[kTileN][kChunkK + 4]>(smem + kStage);
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / WC, wc = wave % WC;
   const int64_t m0 = (int64_t)blockIdx.x * kGemmRows;
   constexpr bool ln = EPI != 2;  // the products that read a LayerNorm
   const float2* stats = tf->sst + (int64_t)k * N;  // the input rows' LayerNorm statistics
@@ -550,7 +553,9 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
   // (128 rows x 4 float4) and of the B chunk (128 rows x 4 float4); its A
   // elements sit in one float4 column group of every chunk
   constexpr int kA4 = kGemmRows * kChunkK / 4 / kGemmThreads;  // 2
-  constexpr int kB4 = kTileN * kChunkK / 4 / kGemmThreads;  // CB / 2
+  // (the B chunk has kTileN x 4 float4: threads beyond it load a clamped row
+  // and store nothing)
+  constexpr int kB4 = (kTileN * kChunkK / 4 + kGemmThreads - 1) / kGemmThreads;
   const int acol = 4 * (tid % (kChunkK / 4));
   const float* ga[kA4];
   const float* gb[kB4];
@@ -600,28 +605,29 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
 #pragma unroll
     for (int u = 0; u < kB4; ++u) {
       const int e = tid + kGemmThreads * u;
-      *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = S.b[u];
+      if ((kTileN * kChunkK / 4) % kGemmThreads == 0 || e < kTileN * kChunkK / 4)
+        *reinterpret_cast<floatx4*>(&Bs[buf][e / (kChunkK / 4)][4 * (e % (kChunkK / 4))]) = S.b[u];
     }
   };
-  floatx4 acc[4][CB];
+  floatx4 acc[SB][CB];
 #pragma unroll
-  for (int sb = 0; sb < 4; ++sb)
+  for (int sb = 0; sb < SB; ++sb)
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) acc[sb][cb] = zero;
   auto compute = [&](int buf) {
 #pragma unroll
     for (int kb = 0; kb < kChunkK / 16; ++kb) {
-      floatx4 a[4], bv[CB];
+      floatx4 a[SB], bv[CB];
 #pragma unroll
-      for (int sb = 0; sb < 4; ++sb)
-        a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][64 * wr + 16 * sb + li][16 * kb + 4 * q]);
+      for (int sb = 0; sb < SB; ++sb)
+        a[sb] = *reinterpret_cast<const floatx4*>(&As[buf][16 * SB * wr + 16 * sb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
         bv[cb] = *reinterpret_cast<const floatx4*>(&Bs[buf][16 * CB * wc + 16 * cb + li][16 * kb + 4 * q]);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int sb = 0; sb < 4; ++sb)
+        for (int sb = 0; sb < SB; ++sb)
 #pragma unroll
           for (int cb = 0; cb < CB; ++cb)
             acc[sb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sb][t], bv[cb][t], acc[sb][cb], 0, 0, 0);
@@ -630,16 +636,16 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
   // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li.
   // The residual a lane adds is loaded before the last chunk's products, so
   // its latency hides behind them.
-  float res[4][CB][4];
+  float res[SB][CB][4];
   (void)res;
   auto load_residual = [&]() {
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb)
+    for (int sb = 0; sb < SB; ++sb)
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
+          const int64_t m = m0 + 16 * SB * wr + 16 * sb + 4 * q + v;
           const int n = n0 + 16 * CB * wc + 16 * cb + li;
           res[sb][cb][v] = (m < N && n < Nout) ? R[m * D + n] : 0.f;
         }
@@ -684,12 +690,12 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
     const int ldz = V + 1;
     float* Z = smem;
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb)
+    for (int sb = 0; sb < SB; ++sb)
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int r = 64 * wr + 16 * sb + 4 * q + v;
+          const int r = 16 * SB * wr + 16 * sb + 4 * q + v;
           const int n = 16 * CB * wc + 16 * cb + li;
           if (n < Nout) {
             const float y = acc[sb][cb][v] + bvv[cb];
@@ -703,12 +709,12 @@ __global__ __launch_bounds__(kGemmThreads, EPI == 3 || (EPI == 2 && CB == 4) ? 2
     return;
   }
 #pragma unroll
-  for (int sb = 0; sb < 4; ++sb)
+  for (int sb = 0; sb < SB; ++sb)
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
+        const int64_t m = m0 + 16 * SB * wr + 16 * sb + 4 * q + v;
         const int n = n0 + 16 * CB * wc + 16 * cb + li;
         if (m < N && n < Nout) {
           float y = acc[sb][cb][v] + bvv[cb];
@@ -1071,20 +1077,25 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   for (int b = 0; b < h.NB; ++b) {
     const int stage = b + 1;
     stats(stage, 0);
-    hipLaunchKernelGGL((k_tf_gemm<0, 2>), dim3(mt, tiles(3 * h.D, 64), rows), dim3(kGemmThreads), 0, s, tf,
+    hipLaunchKernelGGL((k_tf_gemm<0, 2, 2>), dim3(mt, tiles(3 * h.D, 64), rows), dim3(kGemmThreads), 0, s, tf,
                        stage, (int)kGemmQKV, ncand);
     hipLaunchKernelGGL(k_tf_attn, dim3((unsigned)(h.S * h.H), rows), dim3(256), 0, s, tf, stage, ncand);
-    hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<2, 2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmO, ncand);
     stats(stage, 1);
-    hipLaunchKernelGGL((k_tf_gemm<1, 2>), dim3(mt, tiles(h.M, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<1, 2, 2>), dim3(mt, tiles(h.M, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmFc, ncand);
-    hipLaunchKernelGGL((k_tf_gemm<2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
+    hipLaunchKernelGGL((k_tf_gemm<2, 2, 2>), dim3(mt, tiles(h.D, 64), rows), dim3(kGemmThreads), 0, s, tf, stage,
                        (int)kGemmProj, ncand);
   }
   stats(h.NB + 1, 2);
-  hipLaunchKernelGGL((k_tf_gemm<3, 4>), dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
-                     (int)kGemmOut, ncand);
+  // the output layer: one column tile over the vocabulary (80 or 128 wide)
+  if (h.V <= 80)
+    hipLaunchKernelGGL((k_tf_gemm<3, 5, 1>), dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
+                       (int)kGemmOut, ncand);
+  else
+    hipLaunchKernelGGL((k_tf_gemm<3, 8, 1>), dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
+                       (int)kGemmOut, ncand);
   if (!identity) {
     if (wide)
       hipLaunchKernelGGL(k_tf_dl<8>, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf,

@@ -117,6 +117,24 @@ def test_transformer_small_explicit_and_device(mca):
     ctx.close()
 
 
+@pytest.mark.parametrize("vocab", [100, 128])
+def test_transformer_wide_vocabulary(mca, vocab):
+    """Vocabularies past 80 symbols take the 128-wide output tile; explicit
+    steps and a replayed device run against the oracle."""
+    cfg = small_cfg(name=f"tf_vocab{vocab}", vocab=vocab)
+    banner(f"{cfg.name} vocab={vocab}")
+    ctx, ref, _ = make_pair(mca, cfg, k_max=8)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss(), (L, ref.loss())
+    ps = ParityStats(f"transformer vocab {vocab}")
+    explicit_steps(ctx, ref, cfg, 0, 8, 8, ps)
+    ctx.set_step(8)
+    st, ch, dl = ctx.run_steps(8, 8, trace=True, trace_dloss=True)
+    replay(ref, cfg, 8, ch, dl, 8, ps)
+    assert_params_equal(ctx, ref)
+    ctx.close()
+
+
 def test_position_embedding_change_is_causal(mca):
     """A change of pos_emb[p] leaves the loss of every position before p
     bit-identical, and moves the loss by what the oracle says."""
