@@ -744,7 +744,7 @@ hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
   int max_tiles = ntiles;
   if (src.slab_layer >= 0 && nslab > max_tiles) max_tiles = nslab;
   if (src.chain_top >= 0 && nchain > max_tiles) max_tiles = nchain;
-  const int summed = K > kMaxK / 16 || max_tiles > 128;
+  const int summed = K > kMaxK / 16 || max_tiles > 1024;
   if (summed) {
     constexpr int per = kReduceThreads / 16;
     hipLaunchKernelGGL(k_reduce_dl, dim3((K + per - 1) / per), dim3(kReduceThreads), 0, s, net,

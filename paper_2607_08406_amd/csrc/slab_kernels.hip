@@ -480,12 +480,15 @@ int slab_tile(int C) { return C <= 10 ? SlabTile<10>::T : SlabTile<kCMax>::T; }
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
                        const double* dL, hipStream_t s) {
-  // the column lists: every candidate for an evaluation, the one committed
-  // candidate otherwise
-  hipLaunchKernelGGL(k_columns, dim3(k_mode == -2 ? K : 1), dim3(kSlabThreads), 0, s, net, cands,
-                     aux, k_mode, st, cols, nnz);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // the column lists of every candidate, built by an evaluation; a commit
+  // follows the evaluation of its batch (nothing changes W_1 in between) and
+  // reads its candidate's list from there
+  if (k_mode == -2) {
+    hipLaunchKernelGGL(k_columns, dim3(K), dim3(kSlabThreads), 0, s, net, cands, aux, k_mode, st,
+                       cols, nnz);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (net.C <= 10)
     hipLaunchKernelGGL(k_slab<10>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
                        cols, nnz, partial, nblk, k_mode, st, dL);
