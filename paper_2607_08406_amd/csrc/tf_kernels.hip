@@ -475,7 +475,7 @@ __global__ __launch_bounds__(kRowThreads) void k_tf_stats(const TfDev* tf, const
 // output, MLP down), 3 logits and each position's cross-entropy (output layer; one column
 // tile, with the logit tile in LDS).
 template <int EPI, int CB, int WC>
-__global__ __launch_bounds__(kGemmThreads, EPI == 2 && CB == 4 ? 2 : 3) void k_tf_gemm(
+__global__ __launch_bounds__(kGemmThreads, (EPI == 2 && CB == 4) || (EPI == 3 && CB == 8) ? 2 : 3) void k_tf_gemm(
     const TfDev* tf, int stage, int role, int ncand) {
   const int k = slot_of(tf, blockIdx.z, ncand);
   const bool attn_half = role == kGemmQKV || role == kGemmO;
