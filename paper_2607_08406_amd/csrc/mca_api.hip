@@ -107,6 +107,19 @@ std::string check_selection(const mca_net_desc* net, int64_t n_samples, int* cod
   *code = MCA_OK;
   return "";
 }
+// Nets scored layer by layer with dense products (k_norm): those with
+// biases or normalized hidden fields, and plain deep nets (four or more
+// layers) whose hidden layers are all 512 or all 1024 wide (the column and
+// chain kernels of plain deep nets take 256).
+bool dense_path(const mca_net_desc* net) {
+  if (net->biases || net->layer_norm) return true;
+  const int L = net->n_layers;
+  if (L < 4 || net->mutation != MCA_MUTATE_SINGLE) return false;
+  for (int l = 1; l < L; ++l)
+    if (net->widths[l] != net->widths[1]) return false;
+  return net->widths[1] != mca::kChainUnits && mca::norm_width_ok(net->widths[1]);
+}
+
 
 std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max, int* code) {
   *code = MCA_EINVAL;
@@ -148,10 +161,11 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
     std::string m = check_selection(net, n_samples, code);
     if (!m.empty()) return m;
   }
-  if (net->biases || net->layer_norm) {
+  if (dense_path(net)) {
     *code = MCA_EUNSUPPORTED;
     if (L < 2) return "biases and normalization need at least one hidden layer";
-    if (net->weight_mode != MCA_WEIGHTS_FP32) return "biases and normalization take continuous weights";
+    if (net->weight_mode != MCA_WEIGHTS_FP32)
+      return "biases, normalization and deep hidden layers 512 or 1024 wide take continuous weights";
     if (net->mutation != MCA_MUTATE_SINGLE) return "channel mutations take no biases or normalization";
     for (int l = 1; l < L; ++l)
       if (net->widths[l] != net->widths[1] || !mca::norm_width_ok(net->widths[l]))
@@ -179,7 +193,7 @@ std::string check_desc(const mca_net_desc* net, int64_t n_samples, int32_t k_max
     for (int l = 1; l < L; ++l)
       if (net->widths[l] != mca::kChainUnits) {
         *code = MCA_EUNSUPPORTED;
-        return "MLPs with four or more layers need every hidden layer 256 units wide";
+        return "MLPs with four or more layers need every hidden layer 256 units wide (all 512 or all 1024 with continuous weights)";
       }
   *code = MCA_OK;
   return "";
@@ -321,7 +335,7 @@ Layout make_layout(const mca_net_desc* net, int64_t N, int32_t k_max) {
     return at;
   };
   const int L = net->n_layers;
-  const bool norm = net->biases || net->layer_norm;
+  const bool norm = dense_path(net);
   lo.xt = take((size_t)net->widths[0] * lo.Ns * sizeof(float));
   for (int l = 0; l < L; ++l) lo.w[l] = take((size_t)net->widths[l + 1] * net->widths[l] * sizeof(float));
   if (net->biases)
@@ -1022,7 +1036,7 @@ int mca_init(mca_ctx** out, const mca_net_desc* net, const float* const* params,
   nd.ell = (float*)(ws + lo.ell);
   nd.prob = (float*)(ws + lo.pr);
   nd.y = (const int32_t*)(ws + lo.y);
-  ctx->norm = net->biases || net->layer_norm;
+  ctx->norm = dense_path(net);
   const bool slab = L >= 3 && !ctx->norm;
   nd.WT = slab ? (float*)(ws + lo.wt) : nullptr;
   ctx->pslab = slab ? (float*)(ws + lo.pslab) : nullptr;

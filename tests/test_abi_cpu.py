@@ -75,8 +75,9 @@ def test_plan_rejects_bad_descriptions(binding, mutate, code):
 
 
 def test_plan_layer_limits(binding):
-    """Three-layer MLPs up to a 1024-unit second hidden layer are planned;
-    deeper nets and wider second layers are reported as unsupported."""
+    """Three-layer MLPs up to a 1024-unit second hidden layer are planned, and
+    deeper nets with every hidden layer 256 (or all 512, all 1024) wide;
+    other shapes are reported as unsupported."""
     d3 = binding.mlp_desc((784, 1024, 1024, 10), "gauss", delta=0.0)
     b3 = binding.mca_plan(d3, 8192, 64)
     # X^T, W_0..W_2, W_1 transposed, Z_0..Z_2 dominate
@@ -89,6 +90,15 @@ def test_plan_layer_limits(binding):
         with pytest.raises(binding.MCAError) as e:
             binding.mca_plan(d, 1024, 8)
         assert "MCA_EUNSUPPORTED" in str(e.value)
+    # plain deep nets with every hidden layer 512 or 1024 wide take the dense
+    # per-layer path (continuous weights only)
+    for w in (512, 1024):
+        d = binding.mlp_desc((784, w, w, w, 10), "tanh", delta=0.1)
+        assert binding.mca_plan(d, 1024, 8) > 4 * 1024 * w * 3
+    d = binding.mlp_desc((784, 512, 512, 512, 10), "tanh", ternary_scales=[0.1] * 4)
+    with pytest.raises(binding.MCAError) as e:
+        binding.mca_plan(d, 1024, 8)
+    assert "MCA_EUNSUPPORTED" in str(e.value)
 
 
 def test_plan_transformer(binding):
@@ -158,6 +168,6 @@ def test_plan_channel_rules(binding):
     with pytest.raises(binding.MCAError) as e:
         binding.mca_plan(d, 1000, 4)
     assert "MCA_EINVAL" in str(e.value)
-    # single mutations on a 512-wide deep net stay unsupported
+    # single mutations on a deep net of mixed widths stay unsupported
     with pytest.raises(binding.MCAError):
-        binding.mca_plan(binding.mlp_desc((784, 512, 512, 512, 10), "relu"), 1000, 4)
+        binding.mca_plan(binding.mlp_desc((784, 512, 1024, 512, 10), "relu"), 1000, 4)

@@ -53,6 +53,10 @@ CASES = [
     ((784, 1024, 1024, 10), "gauss", True, True, 500, "layer", 0),
     ((784, 256, 256, 10), "relu", False, True, 800, "layer", 0),
     ((784, 256, 256, 256, 10), "tanh", True, False, 600, "layer", 0),
+    # plain deep nets (no biases, no normalization) 512 and 1024 wide take
+    # the same dense per-layer path
+    ((784, 512, 512, 512, 10), "tanh", False, False, 600, "layer", 0),
+    ((784, 1024, 1024, 1024, 10), "relu", False, False, 400, "layer", 0),
 ]
 
 
