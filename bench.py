@@ -147,7 +147,7 @@ def transformer_flops(cfg, cands):
     block for the embeddings); an MLP weight or bias of block b moves one
     column of x_{b+1} (2 N; an up-projection adds its rank-1 term through
     the down-projection, 2 N d) and recomputes the blocks after b and the
-    output layer; an output-layer or final-LayerNorm parameter moves one
+    output layer; an LN2 gain or bias recomputes block b's MLP and the rest; an output-layer or final-LayerNorm parameter moves one
     logit column (2 N) or a rank-1 term into every logit (2 N V).  The
     cross-entropy (about 3 N V) is counted for every candidate."""
     N, D, M, V = cfg.n_samples, cfg.d_model, cfg.d_mlp, cfg.vocab
@@ -172,6 +172,8 @@ def transformer_flops(cfg, cands):
                 total += 2 * N + (NB - 1 - b) * block + out + ce
             elif role in (12, 13):    # up-projection weight, bias
                 total += 2 * N + 2 * N * D + (NB - 1 - b) * block + out + ce
+            elif role in (10, 11):    # LN2 gain, bias: the block's MLP half on
+                total += 2 * 2 * N * D * M + (NB - 1 - b) * block + out + ce
             else:
                 total += (NB - b) * block + out + ce
     return total

@@ -88,9 +88,10 @@ __device__ __forceinline__ const float* stage_input(const TfDev* tf, int k, int 
   return (tf->xin[k] > stage - 1) ? view_x(tf, stage - 1) : slot_x(tf, k, stage - 1);
 }
 // the attention output block b's MLP half reads: the slot's own, or the
-// committed one for a recomputation that starts at that MLP half
+// committed one (as this pass sees it) for a slot that starts at that MLP
+// half
 __device__ __forceinline__ const float* mlp_input(const TfDev* tf, int k, int b) {
-  return (tf->half[k] == b + 1) ? tf->ch[b] : slot_h(tf, k, b);
+  return (tf->half[k] == b + 1) ? view_h(tf, b) : slot_h(tf, k, b);
 }
 
 // Rows held by 16 lanes (a quarter wave): lane l of the group holds the
@@ -276,14 +277,20 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_prep(const TfDev* tf, const
     if (threadIdx.x == 0) {
       const int blk = (l - 2) / kBlockTensors;
       int start = NB + 2, xin = NB + 2;  // nothing recomputed: rejected, or the last stage's own
+      int half = 0;
       if (a.valid && dense) start = xin = tf_stage(l, NB);
+      if (a.valid && dense && l >= 2 && l < nt - 4) {
+        // an LN2 gain or bias leaves its block's attention half as committed
+        const int role = (l - 2) % kBlockTensors;
+        if (role == kLn2G || role == kLn2B) half = blk + 1;
+      }
       if (a.valid && (kind == kTfProjCol || kind == kTfFcCol)) {
         start = blk + 2;  // the stages after the block, from its patched output stream
         xin = blk + 1;
       }
       tf->start[k] = tf->run[k] = start;
       tf->xin[k] = xin;
-      tf->half[k] = 0;
+      tf->half[k] = half;
       tf->kind[k] = a.valid ? kind : kTfDense;
     }
   }

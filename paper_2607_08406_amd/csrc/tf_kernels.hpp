@@ -71,7 +71,8 @@ struct TfDev {
 
 // How a candidate is evaluated (by its tensor):
 //  kTfDense   the stages from its tensor's on, densely (embeddings, LayerNorm
-//             1 and 2, attention projections);
+//             1 and 2, attention projections); an LN2 gain or bias from its
+//             block's MLP half, reading the committed attention output;
 //  kTfOutCol  an output-layer weight or bias: one logit column moves by
 //             de times the final LayerNorm column (1 for the bias), then the
 //             cross-entropy;

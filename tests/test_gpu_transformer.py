@@ -197,14 +197,16 @@ def test_full_transformer_workload(mca):
 
 
 KIND_TENSORS = ["wout", "bout", "lnf.g", "lnf.b", "h0.wproj", "h0.bproj", "h0.wfc", "h0.bfc",
-                "h1.wproj", "h1.wfc", "h1.bfc", "h0.wq", "pos_emb", "tok_emb"]
+                "h1.wproj", "h1.wfc", "h1.bfc", "h0.ln2.g", "h1.ln2.b", "h0.wq", "pos_emb",
+                "tok_emb"]
 
 
 def test_commit_of_every_evaluation_kind(mca):
     """One candidate on each kind of tensor -- output layer and its bias,
     final-LayerNorm gain and bias (from the committed logits), MLP
     down-projection and up-projection weights and biases of both blocks
-    (from the committed block fields), and dense tensors -- evaluated,
+    (from the committed block fields), LN2 gains and biases (from their
+    block's MLP half), and dense tensors -- evaluated,
     committed, and followed by a batch from the stream scored against the
     new state: every loss change against the oracle, every committed tensor
     bit-exact, the cached losses equal to a fresh forward pass's."""
