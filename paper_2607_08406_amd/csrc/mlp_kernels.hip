@@ -602,6 +602,166 @@ __global__ __launch_bounds__(256) void k_gemm_fwd(const float* __restrict__ A, i
   }
 }
 
+// The same product on the matrix cores (v_mfma_f32_16x16x4f32), for Kd a
+// multiple of 16: a 128 x 128 tile of C per block, wave (wr, wc) its 64 x 64
+// quarter as four by four 16 x 16 MFMA tiles.  The reduction runs in chunks
+// of 16: A's rows (row-major, 16 k) staged as float4 and read back as float4
+// (lane group q holds k = 4 q + t of the chunk, t = 0..3, one per MFMA); B's
+// chunk ([16 k][128 columns], columns contiguous) transformed by op on its
+// way into LDS and read one value per MFMA (conflict-free: the 16 lanes of a
+// group read consecutive columns, the four groups rows 4 apart on a padded
+// row).  The next chunk's loads are in flight while the current one is
+// multiplied (double-buffered LDS).  Rows and columns beyond the matrix are
+// clamped on load and dropped on store.
+constexpr int kFwdT = 128;       // rows and columns of the block's tile
+constexpr int kFwdK = 16;        // reduction chunk
+constexpr int kFwdThreads = 256;
+typedef float fwdx4 __attribute__((ext_vector_type(4)));
+
+template <int ACT>  // -1: identity, else MCA_ACT_*
+__global__ __launch_bounds__(kFwdThreads, 3) void k_gemm_fwd_mfma(
+    const float* __restrict__ A, int M, int Kd, const float* __restrict__ B, int64_t ldb,
+    int64_t ncols, float* __restrict__ Cm, int64_t ldc, float gamma,
+    const float* __restrict__ bmu, const float* __restrict__ bS,
+    const float* __restrict__ bias) {
+  __shared__ __attribute__((aligned(16))) float As[2][kFwdT][kFwdK + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kFwdK][kFwdT + 4];
+  const int64_t m0 = (int64_t)blockIdx.y * kFwdT, n0 = (int64_t)blockIdx.x * kFwdT;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
+  const int wr = wave >> 1, wc = wave & 1;
+  // staging: thread tid loads float4 number tid + 256 u of A's chunk
+  // (128 rows x 4 float4) and of B's chunk (16 rows x 32 float4)
+  constexpr int kA4 = kFwdT * kFwdK / 4 / kFwdThreads;  // 2
+  constexpr int kB4 = kFwdK * kFwdT / 4 / kFwdThreads;  // 2
+  const float* ga[kA4];
+  const float* gb[kB4];
+  float nmu[kB4][4], nrs[kB4][4];  // B's column statistics (normalized inputs)
+#pragma unroll
+  for (int u = 0; u < kA4; ++u) {
+    const int e = tid + kFwdThreads * u;
+    const int64_t m = m0 + e / (kFwdK / 4);
+    ga[u] = A + (m < M ? m : M - 1) * (int64_t)Kd + 4 * (e % (kFwdK / 4));
+  }
+#pragma unroll
+  for (int u = 0; u < kB4; ++u) {
+    const int e = tid + kFwdThreads * u;
+    const int kk = e / (kFwdT / 4);
+    const int64_t nb = n0 + 4 * (e % (kFwdT / 4));
+    gb[u] = B + (int64_t)kk * ldb + (nb < ncols ? nb : 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t nn = nb + t < ncols ? nb + t : 0;
+      nmu[u][t] = bmu != nullptr ? bmu[nn] : 0.f;
+      nrs[u][t] = bmu != nullptr ? 1.0f / sqrtf(bS[nn]) : 1.f;
+    }
+  }
+  fwdx4 ra[kA4], rb[kB4];
+  auto fetch = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < kA4; ++u) ra[u] = *reinterpret_cast<const fwdx4*>(ga[u] + kFwdK * c);
+#pragma unroll
+    for (int u = 0; u < kB4; ++u) rb[u] = *reinterpret_cast<const fwdx4*>(gb[u] + (int64_t)kFwdK * c * ldb);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < kA4; ++u) {
+      const int e = tid + kFwdThreads * u;
+      *reinterpret_cast<fwdx4*>(&As[buf][e / (kFwdK / 4)][4 * (e % (kFwdK / 4))]) = ra[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kB4; ++u) {
+      const int e = tid + kFwdThreads * u;
+      const int kk = e / (kFwdT / 4), c4 = e % (kFwdT / 4);
+      const int64_t nb = n0 + 4 * c4;
+      fwdx4 v = rb[u];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float x = v[t];
+        if (bmu != nullptr) x = (x - nmu[u][t]) * nrs[u][t];
+        if (ACT >= 0) x = act_fn(x, ACT, gamma);
+        v[t] = (nb + t < ncols) ? x : 0.f;
+      }
+      *reinterpret_cast<fwdx4*>(&Bs[buf][kk][4 * c4]) = v;
+    }
+  };
+  const fwdx4 zero = {0.f, 0.f, 0.f, 0.f};
+  fwdx4 acc[4][4];
+#pragma unroll
+  for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[sb][cb] = zero;
+  auto compute = [&](int buf) {
+    fwdx4 a[4];
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb)
+      a[sb] = *reinterpret_cast<const fwdx4*>(&As[buf][64 * wr + 16 * sb + li][4 * q]);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      float bv[4];
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) bv[cb] = Bs[buf][4 * q + t][64 * wc + 16 * cb + li];
+#pragma unroll
+      for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+          acc[sb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sb][t], bv[cb], acc[sb][cb], 0, 0, 0);
+    }
+  };
+  const int nc = Kd / kFwdK;
+  fetch(0);
+  store(0);
+  __syncthreads();
+  for (int c = 0; c < nc; ++c) {
+    if (c + 1 < nc) fetch(c + 1);
+    compute(c & 1);
+    if (c + 1 < nc) store((c + 1) & 1);
+    __syncthreads();
+  }
+  // D layout: lane (q, li), element v -> row 16 sb + 4 q + v, column 16 cb + li
+#pragma unroll
+  for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t m = m0 + 64 * wr + 16 * sb + 4 * q + v;
+      if (m >= M) continue;
+      const float b = (bias != nullptr) ? bias[m] : 0.f;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const int64_t n = n0 + 64 * wc + 16 * cb + li;
+        if (n < ncols) Cm[m * ldc + n] = (bias != nullptr) ? acc[sb][cb][v] + b : acc[sb][cb][v];
+      }
+    }
+}
+
+// One layer of the forward pass: the matrix-core product when the reduction
+// width is a multiple of 16 (every configuration here), the vector one
+// otherwise.
+template <int ACT>
+hipError_t forward_layer(const float* A, int M, int Kd, const float* B, int64_t ldb, int64_t N,
+                         float* Cm, int64_t ldc, float gamma, const float* mu, const float* S,
+                         const float* bias, hipStream_t s) {
+  if (Kd % kFwdK == 0) {
+    dim3 grid((unsigned)((N + kFwdT - 1) / kFwdT), (unsigned)((M + kFwdT - 1) / kFwdT));
+    hipLaunchKernelGGL(k_gemm_fwd_mfma<ACT>, grid, dim3(kFwdThreads), 0, s, A, M, Kd, B, ldb, N,
+                       Cm, ldc, gamma, mu, S, bias);
+  } else {
+    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+    hipLaunchKernelGGL(k_gemm_fwd<ACT>, grid, dim3(256), 0, s, A, M, Kd, B, ldb, N, Cm, ldc,
+                       gamma, mu, S, bias);
+  }
+  return hipGetLastError();
+}
+hipError_t forward_layer_act(int act, bool first, const float* A, int M, int Kd, const float* B,
+                             int64_t ldb, int64_t N, float* Cm, int64_t ldc, float gamma,
+                             const float* mu, const float* S, const float* bias, hipStream_t s) {
+  if (first) return forward_layer<-1>(A, M, Kd, B, ldb, N, Cm, ldc, gamma, mu, S, bias, s);
+  if (act == MCA_ACT_TANH)
+    return forward_layer<MCA_ACT_TANH>(A, M, Kd, B, ldb, N, Cm, ldc, gamma, mu, S, bias, s);
+  if (act == MCA_ACT_RELU)
+    return forward_layer<MCA_ACT_RELU>(A, M, Kd, B, ldb, N, Cm, ldc, gamma, mu, S, bias, s);
+  return forward_layer<MCA_ACT_GAUSS>(A, M, Kd, B, ldb, N, Cm, ldc, gamma, mu, S, bias, s);
+}
+
 // l_n and the softmax of every sample from the cached logits; fp64 block sums
 // of l_n.
 __global__ __launch_bounds__(kTile) void k_ce_forward(NetDev net_arg, double* bsum) {
@@ -782,20 +942,8 @@ hipError_t launch_forward_norm(const NetDev& net, const NormDev& nd, double* bsu
     const float* B = (l == 0) ? net.XT : net.Z[l - 1];
     const float* mu = (l > 0 && net.ln) ? nd.MU[l - 1] : nullptr;
     const float* S = (l > 0 && net.ln) ? nd.S[l - 1] : nullptr;
-    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
-    if (l == 0)
-      hipLaunchKernelGGL(k_gemm_fwd<-1>, grid, dim3(256), 0, s, net.W[0], M, Kd, B, net.Ns, N,
-                         net.Z[0], net.Ns, net.gamma, nullptr, nullptr, net.B[0]);
-    else if (net.act == MCA_ACT_TANH)
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
-    else if (net.act == MCA_ACT_RELU)
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_RELU>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
-    else
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, mu, S, net.B[l]);
-    hipError_t e = hipGetLastError();
+    hipError_t e = forward_layer_act(net.act, l == 0, net.W[l], M, Kd, B, net.Ns, N, net.Z[l],
+                                     net.Ns, net.gamma, mu, S, net.B[l], s);
     if (e != hipSuccess) return e;
     if (net.ln && l < net.L - 1) {
       e = launch_norm_stats(net, nd, l, s);
@@ -813,20 +961,8 @@ hipError_t launch_forward(const NetDev& net, double* bsum, DevState* st, hipStre
   for (int l = 0; l < net.L; ++l) {
     const int M = net.widths[l + 1], Kd = net.widths[l];
     const float* B = (l == 0) ? net.XT : net.Z[l - 1];
-    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
-    if (l == 0)
-      hipLaunchKernelGGL(k_gemm_fwd<-1>, grid, dim3(256), 0, s, net.W[0], M, Kd, B, net.Ns, N,
-                         net.Z[0], net.Ns, net.gamma, nullptr, nullptr, nullptr);
-    else if (net.act == MCA_ACT_TANH)
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_TANH>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
-    else if (net.act == MCA_ACT_RELU)
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_RELU>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
-    else
-      hipLaunchKernelGGL(k_gemm_fwd<MCA_ACT_GAUSS>, grid, dim3(256), 0, s, net.W[l], M, Kd, B,
-                         net.Ns, N, net.Z[l], net.Ns, net.gamma, nullptr, nullptr, nullptr);
-    hipError_t e = hipGetLastError();
+    hipError_t e = forward_layer_act(net.act, l == 0, net.W[l], M, Kd, B, net.Ns, N, net.Z[l],
+                                     net.Ns, net.gamma, nullptr, nullptr, nullptr, s);
     if (e != hipSuccess) return e;
   }
   const int nb = (int)((N + kTile - 1) / kTile);
