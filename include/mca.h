@@ -351,7 +351,10 @@ int mca_set_state(mca_ctx* ctx, const float* const* params, const int8_t* const*
  * pass (removes drift of the incremental updates).  Synchronises. */
 int mca_refresh(mca_ctx* ctx);
 
-/* Copy the cached per-sample losses l_n (fp32, n_samples values).  Synchronises. */
+/* Copy the cached per-sample losses l_n (fp32, n_samples values).  A
+ * Transformer context first completes the dense recomputation of its last
+ * incrementally scored winner (Sec. 2.5), which the next evaluation would
+ * otherwise do.  Synchronises. */
 int mca_get_sample_losses(mca_ctx* ctx, float* out_host);
 
 /* Phase timers: phase_mask bit p enables recording a pair of HIP events on the

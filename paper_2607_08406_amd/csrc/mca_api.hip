@@ -1515,6 +1515,15 @@ int mca_refresh(mca_ctx* ctx) {
 int mca_get_sample_losses(mca_ctx* ctx, float* out_host) {
   MCA_LIVE(ctx);
   if (out_host == nullptr) return fail(ctx, MCA_EINVAL, "out_host is NULL");
+  if (ctx->tf) {
+    // a winner scored incrementally has its per-position losses recomputed
+    // in the next evaluation pass: run that recomputation alone and fold it
+    // in (no winner), so the copy holds the committed losses
+    MCA_HIP(ctx, mca::tf_launch_eval(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, 0, false,
+                                     ctx->partial, ctx->tf_nblk, ctx->stream));
+    MCA_HIP(ctx, mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl,
+                                       ctx->st, -2, false, ctx->bsum, ctx->stream));
+  }
   MCA_HIP(ctx, hipMemcpyAsync(out_host, ctx->net.ell, (size_t)ctx->net.N * sizeof(float), hipMemcpyDeviceToHost, ctx->stream));
   MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
   return MCA_OK;

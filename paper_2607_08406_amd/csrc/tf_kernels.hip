@@ -976,7 +976,8 @@ __global__ __launch_bounds__(kCopyThreads) void k_tf_commit(const TfDev* tf, con
                                                             const Aux* aux, const double* dL,
                                                             DevState* st, int k_host, int fill) {
   const int NB = tf->NB, kr = tf->kr;
-  const int w = fill ? 0 : ((k_host >= 0) ? k_host : st->chosen);
+  // k_host -2: no winner (only the pending recomputation is folded in)
+  const int w = fill ? 0 : (k_host >= 0 ? k_host : (k_host == -2 ? -1 : st->chosen));
   const bool wd = w >= 0 && tf->kind[w] == kTfDense && tf->start[w] <= NB + 1;
   const bool rd = !fill && redo_on(tf);
   const int64_t N = tf->N, ND = N * tf->D, NV = N * tf->V;
@@ -1103,7 +1104,7 @@ hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands
   else
     hipLaunchKernelGGL((k_tf_gemm<3, 8, 1>), dim3(mt, 1, rows), dim3(kGemmThreads), 0, s, tf, h.NB + 1,
                        (int)kGemmOut, ncand);
-  if (!identity) {
+  if (!identity && K > 0) {
     if (wide)
       hipLaunchKernelGGL(k_tf_dl<8>, dim3((unsigned)nblk, (unsigned)K), dim3(kLossThreads), 0, s, tf,
                          cands, aux, partial, nblk);

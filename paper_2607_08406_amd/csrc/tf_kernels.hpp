@@ -120,12 +120,14 @@ hipError_t tf_launch_prepare(const TfDev* tf, const mca_cand* cands, int K, Aux*
 // Every stage of every candidate's forward pass from its first changed stage
 // (and the pending dense recomputation in slot kr), and the tile sums of
 // each candidate's per-position loss changes: partial[k * nblk + b].
-// K = 0 with `identity` runs one unmutated pass in slot 0 (cache fill).
+// K = 0 with `identity` runs one unmutated pass in slot 0 (cache fill);
+// K = 0 without it runs only the pending recomputation.
 hipError_t tf_launch_eval(const TfDev* tf, const TfDev& h, const mca_cand* cands,
                           const Aux* aux, int K, bool identity, float* partial, int nblk,
                           hipStream_t s);
-// Commit candidate k (k < 0: st->chosen; none if that is negative) into the
-// committed state after the pending recomputation of the previous pass; a
+// Commit candidate k (-1: st->chosen, none if that is negative; -2: none)
+// into the committed state after the pending recomputation of the previous
+// pass; a
 // winner scored incrementally becomes the next pending recomputation.
 // `fill` copies slot 0 of an identity pass instead, clears the pending
 // recomputation and sets the loss.  Because every committed field is one a

@@ -198,7 +198,7 @@ def test_full_transformer_workload(mca):
 
 KIND_TENSORS = ["wout", "bout", "lnf.g", "lnf.b", "h0.wproj", "h0.bproj", "h0.wfc", "h0.bfc",
                 "h1.wproj", "h1.wfc", "h1.bfc", "h0.ln2.g", "h1.ln2.b", "h0.wq", "pos_emb",
-                "tok_emb"]
+                "tok_emb", "h0.wfc"]  # the last commit is scored incrementally
 
 
 def test_commit_of_every_evaluation_kind(mca):
@@ -209,7 +209,8 @@ def test_commit_of_every_evaluation_kind(mca):
     block's MLP half), and dense tensors -- evaluated,
     committed, and followed by a batch from the stream scored against the
     new state: every loss change against the oracle, every committed tensor
-    bit-exact, the cached losses equal to a fresh forward pass's."""
+    bit-exact, the cached losses (read right after an incrementally scored
+    commit) equal to a fresh forward pass's."""
     from workloads import transformer_param_shapes
     cfg = small_cfg(name="tf_kinds", n_seq=3)
     ctx, ref, w = make_pair(mca, cfg, k_max=8)
