@@ -135,6 +135,29 @@ def test_transformer_wide_vocabulary(mca, vocab):
     ctx.close()
 
 
+@pytest.mark.parametrize("d_model,n_head", [(256, 8), (96, 3), (32, 1)])
+def test_transformer_model_widths(mca, d_model, n_head):
+    """d_model past 128 (rows held as eight float pairs per lane), an odd head
+    count, and a single head: explicit steps and a replayed device run
+    against the oracle."""
+    cfg = small_cfg(name=f"tf_d{d_model}", ctx=16, d_model=d_model, n_head=n_head, d_mlp=64,
+                    n_seq=3)
+    banner(f"{cfg.name} d={d_model} heads={n_head}")
+    ctx, ref, _ = make_pair(mca, cfg, k_max=8)
+    L, _ = ctx.loss()
+    assert abs(L - ref.loss()) <= REL_TOL * ref.loss(), (L, ref.loss())
+    ps = ParityStats(f"transformer d {d_model} heads {n_head}")
+    explicit_steps(ctx, ref, cfg, 0, 8, 8, ps)
+    ctx.set_step(8)
+    st, ch, dl = ctx.run_steps(8, 8, trace=True, trace_dloss=True)
+    replay(ref, cfg, 8, ch, dl, 8, ps)
+    assert_params_equal(ctx, ref)
+    before = ctx.sample_losses()
+    ctx.refresh()
+    np.testing.assert_allclose(before, ctx.sample_losses(), rtol=1e-5, atol=1e-6)
+    ctx.close()
+
+
 def test_position_embedding_change_is_causal(mca):
     """A change of pos_emb[p] leaves the loss of every position before p
     bit-identical, and moves the loss by what the oracle says."""
