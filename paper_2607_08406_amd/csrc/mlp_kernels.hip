@@ -733,14 +733,91 @@ __global__ __launch_bounds__(kFwdThreads, 3) void k_gemm_fwd_mfma(
     }
 }
 
-// One layer of the forward pass: the matrix-core product when the reduction
-// width is a multiple of 16 (every configuration here), the vector one
-// otherwise.
+// The product for at most 16 output rows (a logit layer): a block takes 64
+// columns and eight waves, each wave an eighth of the reduction (Kd a
+// multiple of 128) as four 16 x 16 MFMA tiles.  Lane (q, li) holds columns
+// n0 + 4 li + j of tile j, so that op(B) arrives as one float4 per row, and
+// k = 4 q + t of each block of 16 (A's row li as one float4); the next
+// block's values are requested before the current one's products.  The
+// eight partial tiles meet in LDS and are added in wave order.
+constexpr int kSkinnyCols = 64;
+constexpr int kSkinnyWaves = 8;
+template <int ACT>
+__global__ __launch_bounds__(64 * kSkinnyWaves) void k_gemm_fwd_skinny(
+    const float* __restrict__ A, int M, int Kd, const float* __restrict__ B, int64_t ldb,
+    int64_t ncols, float* __restrict__ Cm, int64_t ldc, float gamma,
+    const float* __restrict__ bmu, const float* __restrict__ bS,
+    const float* __restrict__ bias) {
+  __shared__ float part[kSkinnyWaves][16][kSkinnyCols + 1];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, q = lane >> 4, li = lane & 15;
+  const int64_t n0 = (int64_t)blockIdx.x * kSkinnyCols, nb = n0 + 4 * li;
+  float nmu[4], nrs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t nn = nb + j < ncols ? nb + j : 0;
+    nmu[j] = bmu != nullptr ? bmu[nn] : 0.f;
+    nrs[j] = bmu != nullptr ? 1.0f / sqrtf(bS[nn]) : 1.f;
+  }
+  const int kq = Kd / kSkinnyWaves, nkb = kq / 16;
+  const int64_t k0 = (int64_t)wave * kq + 4 * q;
+  const bool mrow = li < M;
+  const float* arow = A + (int64_t)(mrow ? li : 0) * Kd + k0;
+  const float* bp = B + k0 * ldb + (nb < ncols ? nb : 0);
+  const fwdx4 zero = {0.f, 0.f, 0.f, 0.f};
+  fwdx4 acc[4] = {zero, zero, zero, zero};
+  fwdx4 a_nx, b_nx[4];
+  auto fetch = [&](int kb) {
+    a_nx = *reinterpret_cast<const fwdx4*>(arow + 16 * kb);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) b_nx[t] = *reinterpret_cast<const fwdx4*>(bp + (int64_t)(16 * kb + t) * ldb);
+  };
+  fetch(0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    const fwdx4 a4 = mrow ? a_nx : zero;
+    fwdx4 bv[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) bv[t] = b_nx[t];
+    if (kb + 1 < nkb) fetch(kb + 1);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float x = bv[t][j];
+        if (bmu != nullptr) x = (x - nmu[j]) * nrs[j];
+        if (ACT >= 0) x = act_fn(x, ACT, gamma);
+        x = (nb + j < ncols) ? x : 0.f;
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[t], x, acc[j], 0, 0, 0);
+      }
+  }
+  // D layout: lane (q, li), element v of tile j -> row 4 q + v, column 4 li + j
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) part[wave][4 * q + v][4 * li + j] = acc[j][v];
+  __syncthreads();
+  for (int e = tid; e < 16 * kSkinnyCols; e += 64 * kSkinnyWaves) {
+    const int m = e / kSkinnyCols, c = e - m * kSkinnyCols;
+    const int64_t n = n0 + c;
+    if (m < M && n < ncols) {
+      float v = part[0][m][c];
+#pragma unroll
+      for (int w = 1; w < kSkinnyWaves; ++w) v += part[w][m][c];
+      Cm[(int64_t)m * ldc + n] = (bias != nullptr) ? v + bias[m] : v;
+    }
+  }
+}
+
+// One layer of the forward pass: the skinny matrix-core product for a logit
+// layer (at most 16 rows, reduction a multiple of 128), the tiled one when the
+// reduction width is a multiple of 16, the vector one otherwise.
 template <int ACT>
 hipError_t forward_layer(const float* A, int M, int Kd, const float* B, int64_t ldb, int64_t N,
                          float* Cm, int64_t ldc, float gamma, const float* mu, const float* S,
                          const float* bias, hipStream_t s) {
-  if (Kd % kFwdK == 0) {
+  if (M <= 16 && Kd % (16 * kSkinnyWaves) == 0 && ldb % 4 == 0) {
+    hipLaunchKernelGGL(k_gemm_fwd_skinny<ACT>, dim3((unsigned)((N + kSkinnyCols - 1) / kSkinnyCols)),
+                       dim3(64 * kSkinnyWaves), 0, s, A, M, Kd, B, ldb, N, Cm, ldc, gamma, mu, S, bias);
+  } else if (Kd % kFwdK == 0) {
     dim3 grid((unsigned)((N + kFwdT - 1) / kFwdT), (unsigned)((M + kFwdT - 1) / kFwdT));
     hipLaunchKernelGGL(k_gemm_fwd_mfma<ACT>, grid, dim3(kFwdThreads), 0, s, A, M, Kd, B, ldb, N,
                        Cm, ldc, gamma, mu, S, bias);
