@@ -129,7 +129,9 @@ struct DevState {
   int32_t K;
   uint64_t steps, evaluated, accepted, wasted, tie;
   uint64_t trace_base;   // step index stored at trace slot 0
-  uint64_t pad[6];
+  uint32_t sel_done;     // blocks of the selection kernel done (zero between launches)
+  uint32_t pad32;
+  uint64_t pad[5];
 };
 static_assert(sizeof(DevState) <= 256, "state block");
 
@@ -180,14 +182,19 @@ __device__ __forceinline__ float act_fn(float z, int act, float gamma) {
   return fast_exp(-t);
 }
 
-// e^x - 1 for every x, a few ulp: the polynomial near zero, elsewhere
-// Kahan's (u - 1) x / ln u with u = e^x, which cancels the rounding of u.
-__device__ __forceinline__ float em1(float x) {
+// e^x - 1 away from zero (|x| >= kEm1Small), a few ulp: Kahan's
+// (u - 1) x / ln u with u = e^x, which cancels the rounding of u.
+__device__ __forceinline__ float em1_large(float x) {
   const float u = fast_exp(x);
   const float k = (u - 1.0f) * (x * __builtin_amdgcn_rcpf(fast_log(u)));
-  float r = (x < -17.0f) ? -1.0f : k;  // fl32(e^x - 1) = -1 below -17
-  r = (u == __builtin_huge_valf()) ? u : r;
-  return (fabsf(x) < kEm1Small) ? em1_small(x) : r;
+  const float r = (x < -17.0f) ? -1.0f : k;  // fl32(e^x - 1) = -1 below -17
+  return (u == __builtin_huge_valf()) ? u : r;
+}
+
+// e^x - 1 for every x, a few ulp: the polynomial near zero, Kahan's form
+// elsewhere.
+__device__ __forceinline__ float em1(float x) {
+  return (fabsf(x) < kEm1Small) ? em1_small(x) : em1_large(x);
 }
 
 // ln(1 + s) for s > -1, a few ulp: Kahan's ln(u) s / (u - 1) with u = 1 + s.
@@ -215,12 +222,14 @@ __device__ __forceinline__ float dtanh(float z, float dz) {
 
 // exp(-g (z + dz)^2) - exp(-g z^2) = exp(-g z^2) expm1(-g dz (2 z + dz));
 // a move out of a far tail (the expm1 argument above 30) has nothing to
-// cancel and takes the plain difference.  Exactly zero where dz is zero.
+// cancel and takes the plain difference.  The far tail lies in the branch of
+// arguments away from zero, so the common case of a small move costs one
+// exponential.  Exactly zero where dz is zero.
 __device__ __forceinline__ float dgauss(float z, float dz, float g) {
   const float x = (-g * dz) * fmaf(2.0f, z, dz);
-  const float near = act_fn(z, MCA_ACT_GAUSS, g) * em1(x);
-  const float far = act_fn(z + dz, MCA_ACT_GAUSS, g) - act_fn(z, MCA_ACT_GAUSS, g);
-  return (x > 30.0f) ? far : near;
+  const float pz = act_fn(z, MCA_ACT_GAUSS, g);
+  if (fabsf(x) < kEm1Small) return pz * em1_small(x);
+  return (x > 30.0f) ? act_fn(z + dz, MCA_ACT_GAUSS, g) - pz : pz * em1_large(x);
 }
 
 // max(0, z + dz) - max(0, z): dz itself where both fields are positive (no

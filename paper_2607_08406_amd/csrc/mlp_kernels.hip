@@ -437,67 +437,59 @@ __device__ __forceinline__ double candidate_dl(const NetDev& net, const PartialS
   return (k < K && aux[k].valid) ? s / subset_count(net) : __builtin_huge_val();
 }
 
-// Loss changes of many candidates: block b adds the tile sums of candidates
-// 16b .. 16b+15 into dL (the same arithmetic as the one-block selection).
-constexpr int kReduceThreads = 256;
-__global__ __launch_bounds__(kReduceThreads) void k_reduce_dl(const NetDev net, PartialSrc src,
-                                                             const mca_cand* cands,
-                                                             const Aux* aux, int K, double* dL) {
-  const int k = blockIdx.x * (kReduceThreads / 16) + (threadIdx.x >> 4), r = threadIdx.x & 15;
-  const double v = candidate_dl(net, src, cands, aux, K, k, r);
-  if (k < K && r == 0) dL[k] = v;
-}
-
-// The selection proper: the first candidate that passes the test, the trace
-// and the counters.  With summed = 0 it also adds the tile sums (one block
-// for all K: the few-candidate steps of the per-phase loop); with summed = 1
-// k_reduce_dl has already written dL.
-__global__ __launch_bounds__(kMaxK) void k_select(const NetDev net, PartialSrc src,
-                                                  const mca_cand* cands, const Aux* aux, int K,
-                                                  int summed, double* dL, DevState* st,
-                                                  int do_select, int32_t* tr_chosen,
-                                                  double* tr_dl, int64_t tr_cap) {
-  __shared__ int first;
-  __shared__ int ntie;
-  __shared__ double vals[kMaxK];
+// Loss changes and the selection in one launch.  Block b adds the tile sums
+// of candidates 4b .. 4b+3 (16 lanes each, in the order of candidate_dl) into
+// dL, so the partial sums of a batch are read by many CUs at once.  With
+// do_select, the block that finishes last (counted in st->sel_done, which is
+// zero between launches) reads every dL and takes the decision: the first
+// candidate that passes the test (Eq. 6 or Eq. 7), the trace and the
+// counters.
+constexpr int kSelThreads = 64;
+constexpr int kSelPerBlock = kSelThreads / 16;
+__global__ __launch_bounds__(kSelThreads) void k_reduce_select(
+    const NetDev net, PartialSrc src, const mca_cand* cands, const Aux* aux, int K, double* dL,
+    DevState* st, int do_select, int32_t* tr_chosen, double* tr_dl, int64_t tr_cap) {
   const int tid = threadIdx.x;
-  if (tid == 0) { first = K; ntie = 0; }
-  if (summed) {
-    if (tid < K) vals[tid] = dL[tid];
-  } else {
-    for (int k0 = 0; k0 < K; k0 += kMaxK / 16) {
-      const int k = k0 + (tid >> 4), r = tid & 15;
-      const double v = candidate_dl(net, src, cands, aux, K, k, r);
-      if (k < K && r == 0) vals[k] = v;
-    }
-  }
-  __syncthreads();
-  const int k = tid;
-  double v = 0.0;
-  if (k < K) {
-    v = vals[k];
-    dL[k] = v;
-    if (do_select && accepts(v, net.ties, aux[k].theta)) atomicMin(&first, k);
+  {
+    const int k = blockIdx.x * kSelPerBlock + (tid >> 4), r = tid & 15;
+    const double v = candidate_dl(net, src, cands, aux, K, k, r);
+    if (k < K && r == 0) dL[k] = v;
   }
   if (!do_select) return;
+  __shared__ int last, first;
+  __threadfence();  // this block's loss changes before its count
   __syncthreads();
-  const int kc = first;
-  if (k < K && k <= kc && fabs(v) < 1e-6) atomicAdd(&ntie, 1);
-  __syncthreads();
-  if (tr_chosen != nullptr) {
-    const int64_t slot = (int64_t)(st->t - st->trace_base);
-    if (slot >= 0 && slot < tr_cap) {
-      if (k == 0) tr_chosen[slot] = (kc < K) ? kc : -1;
-      if (tr_dl != nullptr && k < K) tr_dl[slot * K + k] = v;
-    }
+  if (tid == 0) {
+    last = atomicAdd(&st->sel_done, 1u) == gridDim.x - 1;
+    first = K;
   }
   __syncthreads();
-  if (k == 0) {
+  if (!last) return;
+  __threadfence();  // every block's loss changes after the count
+  for (int k = tid; k < K; k += kSelThreads) {
+    const double v = __hip_atomic_load(&dL[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (accepts(v, net.ties, aux[k].theta)) atomicMin(&first, k);
+  }
+  __syncthreads();
+  const int kc = first;
+  const int64_t slot = (int64_t)(st->t - st->trace_base);
+  const bool traced = tr_chosen != nullptr && slot >= 0 && slot < tr_cap;
+  uint64_t nt = 0;  // loss changes in the tie band up to the decision
+  for (int k = tid; k < K; k += kSelThreads) {
+    const double v = __hip_atomic_load(&dL[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (k <= kc && fabs(v) < 1e-6) ++nt;
+    if (traced && tr_dl != nullptr) tr_dl[slot * K + k] = v;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) nt += __shfl_xor(nt, o, 64);
+  if (tid == 0) {
+    if (traced) tr_chosen[slot] = (kc < K) ? kc : -1;
     st->chosen = (kc < K) ? kc : -1;
     st->t += 1;
     st->steps += 1;
     st->evaluated += (uint64_t)K;
-    st->tie += (uint64_t)ntie;
+    st->tie += nt;
+    st->sel_done = 0u;
   }
 }
 
@@ -976,21 +968,9 @@ hipError_t launch_select(const NetDev& net, const float* partial, int ntiles,
   src.pchain = pchain;
   src.nchain = nchain;
   src.chain_top = (net.L >= 4) ? net.L - 4 : -1;
-  // more candidates than one block sums in one pass, or many tile sums per
-  // candidate (the slab's small tiles): spread the sums over blocks
-  int max_tiles = ntiles;
-  if (src.slab_layer >= 0 && nslab > max_tiles) max_tiles = nslab;
-  if (src.chain_top >= 0 && nchain > max_tiles) max_tiles = nchain;
-  const int summed = K > kMaxK / 16 || max_tiles > 1024;
-  if (summed) {
-    constexpr int per = kReduceThreads / 16;
-    hipLaunchKernelGGL(k_reduce_dl, dim3((K + per - 1) / per), dim3(kReduceThreads), 0, s, net,
-                       src, cands, aux, K, dL);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(k_select, dim3(1), dim3(kMaxK), 0, s, net, src, cands, aux, K, summed, dL,
-                     st, do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
+  const int nblk = K > 0 ? (K + kSelPerBlock - 1) / kSelPerBlock : 1;
+  hipLaunchKernelGGL(k_reduce_select, dim3(nblk), dim3(kSelThreads), 0, s, net, src, cands, aux,
+                     K, dL, st, do_select ? 1 : 0, tr_chosen, tr_dl, tr_cap);
   return hipGetLastError();
 }
 

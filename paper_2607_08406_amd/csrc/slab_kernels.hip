@@ -66,10 +66,10 @@ __device__ __forceinline__ float half_sum(float v) {
 // word, the bits of W_1[m, j] in the high word).  With STORE each lane writes
 // its units' new local fields into the tile.  All 64 lanes of the wave must
 // call this.
-template <int CM, int TS, bool STORE>
+template <int CM, int ACT, int TS, bool STORE>
 __device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, const uint64_t* col,
                                                   int nnz, const int (&tp)[kPairChunk],
-                                                  const float (&dp)[kPairChunk], int np, int act,
+                                                  const float (&dp)[kPairChunk], int np,
                                                   float gamma, bool active,
                                                   float (&acc)[kPairChunk][CM]) {
   const int g = threadIdx.x & (kLanesPerPair - 1);
@@ -103,7 +103,7 @@ __device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, co
           if (p < np) {
             const float zo = zt[m * TS + tp[p]];
             const float dz = dp[p] * w;
-            const float d = dphi(zo, dz, act, gamma);
+            const float d = dphi(zo, dz, ACT, gamma);
             if (STORE) zt[m * TS + tp[p]] = zo + dz;
 #pragma unroll
             for (int c = 0; c < CM; ++c) acc[p][c] = fmaf(d, wr[c], acc[p][c]);
@@ -176,8 +176,9 @@ __global__ __launch_bounds__(kSlabThreads) void k_columns(NetDev net_arg, const 
 
 // k_mode: -2 evaluate every listed candidate of layer L-3; -1 commit the
 // device decision st->chosen; >= 0 commit that candidate.  A commit is a no-op
-// here unless the candidate is in layer L-3.
-template <int CM>
+// here unless the candidate is in layer L-3.  ACT is the net's transfer
+// function (MCA_ACT_*), fixed at compile time.
+template <int CM, int ACT>
 __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca_cand* cands,
                                                        const Aux* aux, int K, const uint64_t* cols,
                                                        const int* nnz, float* partial, int nblk,
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = net.L, C = (CM < kCMax) ? CM : net.C;
   const int l = L - 3;  // the layer whose weights this kernel mutates
-  const int act = net.act;
+  constexpr int act = ACT;
   const float gamma = net.gamma;
   const int n2 = net.widths[L - 1];
   const int64_t Ns = net.Ns, N = net.N;
@@ -395,9 +396,9 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
       const int cnt = active ? gnnz[s] : 0;
       float acc[kPairChunk][CM];
       if (commit)  // the commit also writes the new fields into the tile
-        chunk_logit_delta<CM, TS, true>(zt, w2, col, cnt, tp, dp, np, act, gamma, active, acc);
+        chunk_logit_delta<CM, ACT, TS, true>(zt, w2, col, cnt, tp, dp, np, gamma, active, acc);
       else
-        chunk_logit_delta<CM, TS, false>(zt, w2, col, cnt, tp, dp, np, act, gamma, active, acc);
+        chunk_logit_delta<CM, ACT, TS, false>(zt, w2, col, cnt, tp, dp, np, gamma, active, acc);
       if (active && (tid & (kLanesPerPair - 1)) == 0) {
 #pragma unroll
         for (int p = 0; p < kPairChunk; ++p) {
@@ -489,12 +490,17 @@ hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (net.C <= 10)
-    hipLaunchKernelGGL(k_slab<10>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
-                       cols, nnz, partial, nblk, k_mode, st, dL);
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K, cols,
+                       nnz, partial, nblk, k_mode, st, dL);
+  };
+  const bool small = net.C <= 10;
+  if (net.act == MCA_ACT_TANH)
+    small ? go(k_slab<10, MCA_ACT_TANH>) : go(k_slab<kCMax, MCA_ACT_TANH>);
+  else if (net.act == MCA_ACT_RELU)
+    small ? go(k_slab<10, MCA_ACT_RELU>) : go(k_slab<kCMax, MCA_ACT_RELU>);
   else
-    hipLaunchKernelGGL(k_slab<kCMax>, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K,
-                       cols, nnz, partial, nblk, k_mode, st, dL);
+    small ? go(k_slab<10, MCA_ACT_GAUSS>) : go(k_slab<kCMax, MCA_ACT_GAUSS>);
   return hipGetLastError();
 }
 
