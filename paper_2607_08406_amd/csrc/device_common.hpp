@@ -496,6 +496,12 @@ __device__ __forceinline__ bool accepts(double dL, int ties, double theta = 0.0)
   return ties ? (dL <= 0.0) : (dL < 0.0);
 }
 
+// A first-layer weight multiplies the raw input: the evaluation tiles where
+// its feature is zero throughout cannot change (fmask null: no such list).
+__device__ __forceinline__ uint64_t candidate_tiles(const mca_cand& c, const uint64_t* fmask) {
+  return (c.layer == 0 && fmask != nullptr) ? fmask[c.i] : ~0ull;
+}
+
 // Metropolis threshold of candidate k of step t (Eq. 7): U from word 0 of the
 // Philox block at counter (t, k, 1, 0), U = (w0 >> 11) 2^-53, and
 // U < exp(-beta dL) exactly when dL < -ln(U) / beta.  0 under the greedy rule.

@@ -709,7 +709,8 @@ hipError_t prepare_dev(mca_ctx* ctx, int K) { return prepare_into(ctx, ctx_bufs(
 
 // Scores the K staged candidates: the column kernel for the last two layers,
 // the tile kernel for layer L-3, the dense chain for layers 0..L-4.
-hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
+// `listed`: the layer L-3 column lists came with the proposal.
+hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K, bool listed = false) {
   if (ctx->norm)
     return mca::launch_norm(net, ctx->nd, b.cands, b.aux, K, ctx->pnorm, ctx->lo.nnorm, -2,
                             ctx->st, b.dl, ctx->stream);
@@ -723,14 +724,27 @@ hipError_t eval_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K) {
                                   ctx->lo.ntiles_ev, ctx->st, ctx->stream);
   if (e == hipSuccess && net.L >= 3)
     e = mca::launch_slab(net, b.cands, b.aux, K, b.cols, b.nnz, b.pslab, ctx->lo.nslab, -2,
-                         ctx->st, b.dl, ctx->stream);
+                         ctx->st, b.dl, ctx->stream, listed);
   if (e == hipSuccess && net.L >= 4)
     e = mca::launch_chain(net, b.cands, b.aux, K, b.rows, b.rda, b.rcnt, b.pchain,
                           ctx->lo.nchain, -2, ctx->st, b.dl, ctx->stream);
   return e;
 }
-hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K) {
-  return eval_into(ctx, net, ctx_bufs(ctx), K);
+hipError_t eval_all(mca_ctx* ctx, const NetDev& net, int K, bool listed = false) {
+  return eval_into(ctx, net, ctx_bufs(ctx), K, listed);
+}
+
+// The device step's proposal; for a plain MLP with a layer L-3 it also lists
+// the columns that layer's candidates score (one launch instead of two).
+// Returns whether it did.
+bool fused_proposal(const mca_ctx* ctx, const NetDev& net) {
+  return !ctx->chan && !ctx->tf && !ctx->norm && net.L >= 3;
+}
+hipError_t propose_step(mca_ctx* ctx, const NetDev& net, int K) {
+  if (fused_proposal(ctx, net))
+    return mca::launch_propose_columns(net, ctx->st, K, ctx->cands, ctx->aux, ctx->fmask,
+                                       ctx->cmask, ctx->cols, ctx->nnz, ctx->stream);
+  return propose_dev(ctx, 0, true, K);
 }
 
 hipError_t select_into(mca_ctx* ctx, const NetDev& net, const Bufs& b, int K, bool do_select,
@@ -1409,8 +1423,8 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
       trd = trace->dloss ? ctx->tr_dl : nullptr;
     }
     for (uint64_t s = 0; s < chunk; ++s) {
-      MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_dev(ctx, 0, true, K); }));
-      MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K); }));
+      MCA_HIP(ctx, timed(ctx, 0, [&] { return propose_step(ctx, net, K); }));
+      MCA_HIP(ctx, timed(ctx, 1, [&] { return eval_all(ctx, net, K, fused_proposal(ctx, net)); }));
       MCA_HIP(ctx, timed(ctx, 2, [&] { return select_all(ctx, net, K, true, trc, trd); }));
       MCA_HIP(ctx, timed(ctx, 3, [&] { return commit_all(ctx, net, -1, K); }));
     }

@@ -23,12 +23,6 @@ namespace mca {
 // candidate stream
 // ---------------------------------------------------------------------------
 
-// A first-layer weight multiplies the raw input: the evaluation tiles where
-// its feature is zero throughout cannot change (fmask null: no such list).
-__device__ __forceinline__ uint64_t candidate_tiles(const mca_cand& c, const uint64_t* fmask) {
-  return (c.layer == 0 && fmask != nullptr) ? fmask[c.i] : ~0ull;
-}
-
 __global__ void k_propose(NetDev net_arg, uint64_t t_host, int use_dev_t, const DevState* st,
                           int K, mca_cand* cands, Aux* aux, const uint64_t* fmask,
                           uint64_t* cmask) {
@@ -456,36 +450,43 @@ __global__ __launch_bounds__(kSelThreads) void k_reduce_select(
     if (k < K && r == 0) dL[k] = v;
   }
   if (!do_select) return;
-  __shared__ int last, first;
+  __shared__ int last;
   __threadfence();  // this block's loss changes before its count
   __syncthreads();
-  if (tid == 0) {
-    last = atomicAdd(&st->sel_done, 1u) == gridDim.x - 1;
-    first = K;
-  }
+  if (tid == 0) last = atomicAdd(&st->sel_done, 1u) == gridDim.x - 1;
   __syncthreads();
   if (!last) return;
   __threadfence();  // every block's loss changes after the count
-  for (int k = tid; k < K; k += kSelThreads) {
-    const double v = __hip_atomic_load(&dL[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (accepts(v, net.ties, aux[k].theta)) atomicMin(&first, k);
-  }
-  __syncthreads();
-  const int kc = first;
-  const int64_t slot = (int64_t)(st->t - st->trace_base);
+  // one pass over chunks of 64 candidates (lane = candidate): the first that
+  // passes the test, the tie-band count up to it, the trace of every change
+  const uint64_t t = st->t, tb = st->trace_base;
+  const int64_t slot = (int64_t)(t - tb);
   const bool traced = tr_chosen != nullptr && slot >= 0 && slot < tr_cap;
-  uint64_t nt = 0;  // loss changes in the tie band up to the decision
-  for (int k = tid; k < K; k += kSelThreads) {
-    const double v = __hip_atomic_load(&dL[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (k <= kc && fabs(v) < 1e-6) ++nt;
-    if (traced && tr_dl != nullptr) tr_dl[slot * K + k] = v;
+  int kc = K;
+  uint64_t nt = 0;
+  for (int k0 = 0; k0 < K; k0 += kSelThreads) {
+    const int k = k0 + tid;
+    double v = 0.0, th = 0.0;
+    if (k < K) {
+      v = __hip_atomic_load(&dL[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      th = aux[k].theta;
+    }
+    if (traced && tr_dl != nullptr && k < K) tr_dl[slot * K + k] = v;
+    if (kc < K) continue;  // decided in an earlier chunk
+    const uint64_t acc = __ballot(k < K && accepts(v, net.ties, th));
+    const uint64_t tie = __ballot(k < K && fabs(v) < 1e-6);
+    if (acc != 0ull) {
+      const int f = (int)__ffsll((unsigned long long)acc) - 1;
+      kc = k0 + f;
+      nt += (uint64_t)__popcll(tie & ((f == 63) ? ~0ull : ((2ull << f) - 1ull)));
+    } else {
+      nt += (uint64_t)__popcll(tie);
+    }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) nt += __shfl_xor(nt, o, 64);
   if (tid == 0) {
     if (traced) tr_chosen[slot] = (kc < K) ? kc : -1;
     st->chosen = (kc < K) ? kc : -1;
-    st->t += 1;
+    st->t = t + 1;
     st->steps += 1;
     st->evaluated += (uint64_t)K;
     st->tie += nt;

@@ -132,26 +132,15 @@ __device__ __forceinline__ void chunk_logit_delta(float* zt, const float* w2, co
 
 }  // namespace
 
-// Block k lists the nonzero entries of column j of W_1 for candidate k when it
-// is in layer L-3 (and valid), in increasing unit order: cols[k * n2 + e] =
-// m | bits(W_1[m, j]) << 32, nnz[k] = their count; otherwise nnz[k] = 0.
-__global__ __launch_bounds__(kSlabThreads) void k_columns(NetDev net_arg, const mca_cand* cands,
-                                                          const Aux* aux, int k_mode,
-                                                          const DevState* st, uint64_t* cols,
-                                                          int* nnz) {
+// The nonzero entries of column j of W_1 (the candidate's unit) in increasing
+// unit order, by the whole block: cols[k * n2 + e] = m | bits(W_1[m, j]) << 32,
+// nnz[k] = their count.
+__device__ void list_column(const NetDev& net, int j, int k, uint64_t* cols, int* nnz) {
   __shared__ int wave_n[kSlabThreads / 64];
-  const int k = (k_mode >= 0) ? k_mode : (k_mode == -1 ? st->chosen : (int)blockIdx.x);
-  if (k < 0) return;
-  const int L = net_arg.L;
+  const int L = net.L;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const mca_cand c = cands[k];
-  const bool take = c.layer == L - 3 && (k_mode != -2 || aux[k].valid);
-  if (!take) {
-    if (tid == 0) nnz[k] = 0;
-    return;
-  }
-  const int n2 = net_arg.widths[L - 1];
-  const float* row = net_arg.WT + (int64_t)c.j * n2;
+  const int n2 = net.widths[L - 1];
+  const float* row = net.WT + (int64_t)j * n2;
   int base = 0;
   for (int m0 = 0; m0 < n2; m0 += kSlabThreads) {
     const int m = m0 + tid;
@@ -172,6 +161,48 @@ __global__ __launch_bounds__(kSlabThreads) void k_columns(NetDev net_arg, const 
     __syncthreads();
   }
   if (tid == 0) nnz[k] = base;
+}
+
+// Block k lists the column of candidate k when it is in layer L-3 (and valid);
+// otherwise nnz[k] = 0.
+__global__ __launch_bounds__(kSlabThreads) void k_columns(NetDev net_arg, const mca_cand* cands,
+                                                          const Aux* aux, int k_mode,
+                                                          const DevState* st, uint64_t* cols,
+                                                          int* nnz) {
+  const int k = (k_mode >= 0) ? k_mode : (k_mode == -1 ? st->chosen : (int)blockIdx.x);
+  if (k < 0) return;
+  const mca_cand c = cands[k];
+  const bool take = c.layer == net_arg.L - 3 && (k_mode != -2 || aux[k].valid);
+  if (!take) {
+    if (threadIdx.x == 0) nnz[k] = 0;
+    return;
+  }
+  list_column(net_arg, c.j, k, cols, nnz);
+}
+
+// The candidates of the step st->t (decoded as the proposal kernel does:
+// record, new value, acceptance threshold, tile mask) and, for a valid weight
+// in layer L-3, its column list: block k, candidate k.  Every thread decodes
+// the candidate (the stream needs no state); thread 0 stores it.
+__global__ __launch_bounds__(kSlabThreads) void k_propose_columns(
+    NetDev net_arg, const DevState* st, int K, mca_cand* cands, Aux* aux, const uint64_t* fmask,
+    uint64_t* cmask, uint64_t* cols, int* nnz) {
+  __shared__ NetDev net;
+  stage_net(net, net_arg);
+  const int k = blockIdx.x;
+  const uint64_t t = st->t;
+  const mca_cand c = decode_candidate(net, t, (uint64_t)k);
+  Aux a = prepare_candidate(net, c);
+  if (threadIdx.x == 0) {
+    cands[k] = c;
+    a.theta = accept_theta(net.rule, net.beta, net.seed, net.tag, t, (uint64_t)k);
+    aux[k] = a;
+    cmask[k] = candidate_tiles(c, fmask);
+  }
+  if (c.layer == net.L - 3 && a.valid)
+    list_column(net, c.j, k, cols, nnz);
+  else if (threadIdx.x == 0)
+    nnz[k] = 0;
 }
 
 // k_mode: -2 evaluate every listed candidate of layer L-3; -1 commit the
@@ -259,6 +290,34 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
         const int c = e / n2, m = e - c * n2;
         if (e < CM * n2) w2[m * CM + c] = (c < C) ? v[u] : 0.f;
       }
+    }
+  };
+  // The commit reads and writes only the units of the winner's column list:
+  // their rows of the tile and of the logit-layer weights.
+  auto stage_listed = [&](const uint64_t* col, int cnt) {
+    for (int e0 = tid; e0 < cnt * T; e0 += kStageU * kSlabThreads) {
+      float v[kStageU];
+      int mu[kStageU];
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int q = e / T, t = e - q * T;
+        const bool ok = e < cnt * T && n0 + t < N;
+        mu[u] = (int)(uint32_t)gload(&col[e < cnt * T ? q : 0]);
+        v[u] = gload(&Z2[ok ? (int64_t)mu[u] * Ns + n0 + t : 0]);
+      }
+#pragma unroll
+      for (int u = 0; u < kStageU; ++u) {
+        const int e = e0 + u * kSlabThreads;
+        const int q = e / T, t = e - q * T;
+        if (e < cnt * T) zt[mu[u] * TS + t] = (n0 + t < N) ? v[u] : 0.f;
+      }
+    }
+    const float* WL = net.W[L - 1];
+    for (int e = tid; e < cnt * CM; e += kSlabThreads) {
+      const int q = e / CM, c = e - q * CM;
+      const int m = (int)(uint32_t)gload(&col[q]);
+      w2[m * CM + c] = (c < C) ? gload(&WL[(int64_t)c * n2 + m]) : 0.f;
     }
   };
   // The tile's logits, softmax and labels (the loss change of a pair reads
@@ -364,7 +423,7 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
     __syncthreads();
     const int ni = nitems;
     if (commit && ni > 0) {  // uniform over the block
-      stage();
+      stage_listed(cols + (int64_t)kc * n2, nnz[kc]);
       __syncthreads();
     }
     // 4. score: half-wave h takes items h, h + kHalves, ...; every half-wave
@@ -445,11 +504,15 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   }
   if (!commit) return;
   // the tile's second-layer fields go back to HBM when any sample changed:
-  // whole rows of T samples (the unchanged ones are rewritten with the values
-  // they hold), so each unit is one contiguous store instead of scattered ones
+  // the whole rows of T samples of the listed units (the unchanged samples
+  // are rewritten with the values they hold), so each unit is one contiguous
+  // store instead of scattered ones; a unit off the list did not move
   if (touched != 0u) {
-    for (int e = tid; e < n2 * T; e += kSlabThreads) {
-      const int m = e / T, t = e - m * T;
+    const uint64_t* col = cols + (int64_t)kc * n2;
+    const int cnt = nnz[kc];
+    for (int e = tid; e < cnt * T; e += kSlabThreads) {
+      const int q = e / T, t = e - q * T;
+      const int m = (int)(uint32_t)gload(&col[q]);
       if (n0 + t < N) gstore(&Z2[(int64_t)m * Ns + n0 + t], zt[m * TS + t]);
     }
   }
@@ -478,13 +541,21 @@ __global__ void k_transpose(const float* src, int rows, int cols, float* dst) {
 
 int slab_tile(int C) { return C <= 10 ? SlabTile<10>::T : SlabTile<kCMax>::T; }
 
+hipError_t launch_propose_columns(const NetDev& net, const DevState* st, int K, mca_cand* cands,
+                                 Aux* aux, const uint64_t* fmask, uint64_t* cmask,
+                                 uint64_t* cols, int* nnz, hipStream_t s) {
+  hipLaunchKernelGGL(k_propose_columns, dim3(K), dim3(kSlabThreads), 0, s, net, st, K, cands, aux,
+                     fmask, cmask, cols, nnz);
+  return hipGetLastError();
+}
+
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
-                       const double* dL, hipStream_t s) {
-  // the column lists of every candidate, built by an evaluation; a commit
-  // follows the evaluation of its batch (nothing changes W_1 in between) and
-  // reads its candidate's list from there
-  if (k_mode == -2) {
+                       const double* dL, hipStream_t s, bool listed) {
+  // the column lists of every candidate, built by an evaluation (or with the
+  // proposal, `listed`); a commit follows the evaluation of its batch
+  // (nothing changes W_1 in between) and reads its candidate's list from there
+  if (k_mode == -2 && !listed) {
     hipLaunchKernelGGL(k_columns, dim3(K), dim3(kSlabThreads), 0, s, net, cands, aux, k_mode, st,
                        cols, nnz);
     hipError_t e = hipGetLastError();
