@@ -790,10 +790,14 @@ hipError_t commit_all(mca_ctx* ctx, const NetDev& net, int k, int K) {
   if (ctx->tf)
     return mca::tf_launch_commit(ctx->tfd, ctx->tfh, ctx->cands, ctx->aux, ctx->dl, ctx->st, k,
                                  false, ctx->bsum, ctx->stream);
-  hipError_t e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
-  if (e == hipSuccess && net.L >= 3)
+  // with a layer L-3, its tile kernel also applies a winner of the last two
+  // layers (one launch instead of two)
+  hipError_t e = hipSuccess;
+  if (net.L >= 3)
     e = mca::launch_slab(net, ctx->cands, ctx->aux, 0, ctx->cols, ctx->nnz, ctx->pslab,
-                         ctx->lo.nslab, k, ctx->st, ctx->dl, ctx->stream);
+                         ctx->lo.nslab, k, ctx->st, ctx->dl, ctx->stream, false, true);
+  else
+    e = mca::launch_commit(net, ctx->cands, ctx->aux, ctx->dl, ctx->st, k, ctx->lo.ntiles, ctx->stream);
   if (e == hipSuccess && net.L >= 4)
     e = mca::launch_chain(net, ctx->cands, ctx->aux, 0, ctx->rows, ctx->rda, ctx->rcnt,
                           ctx->pchain, ctx->lo.nchain, k, ctx->st, ctx->dl, ctx->stream);

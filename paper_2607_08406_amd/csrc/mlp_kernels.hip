@@ -54,52 +54,6 @@ __global__ void k_prepare(NetDev net_arg, const mca_cand* cands, int K, Aux* aux
 // per-sample incremental update for a mutation in one of the last two layers
 // ---------------------------------------------------------------------------
 
-// Commit of candidate (l, j, i, de) on sample n, for a weight in the last
-// two layers: the mutated unit's local field moves by dz = de * ain; the
-// logits move by dz (a logit-layer weight) or by da * W_{L-1}[:, j] with
-// da = phi(z + dz) - phi(z) (the expressions of the evaluation); the
-// sample's softmax and loss are recomputed from its new logits.
-__device__ __forceinline__ void column_commit(const NetDev& net, int l, int j, int i, float de,
-                                              int64_t n) {
-  const int L = net.L, C = net.C;
-  const int64_t Ns = net.Ns;
-  const float ain = (l == 0) ? gload(&net.XT[(int64_t)i * Ns + n])
-                             : act_fn(gload(&net.Z[l - 1][(int64_t)i * Ns + n]), net.act, net.gamma);
-  if (ain == 0.f) return;  // nothing changes for this sample
-  float* zrow = net.Z[l] + (int64_t)j * Ns;
-  const float zl = gload(&zrow[n]);
-  const float dz = de * ain;
-  float* ZL = net.Z[L - 1];
-  float zc[kCMax], wc[kCMax];
-#pragma unroll
-  for (int c = 0; c < kCMax; ++c) zc[c] = (c < C) ? gload(&ZL[(int64_t)c * Ns + n]) : 0.f;
-  float da;
-  if (l == L - 1) {
-    da = dz;  // the mutated weight feeds logit j directly
-#pragma unroll
-    for (int c = 0; c < kCMax; ++c) wc[c] = (c == j) ? 1.f : 0.f;
-  } else {
-    // last hidden layer: rank-1 update of the logits through W_L[:, j]
-    da = dphi(zl, dz, net.act, net.gamma);
-    const float* WL = net.W[L - 1];
-    const int nh = net.widths[L - 1];
-#pragma unroll
-    for (int c = 0; c < kCMax; ++c) wc[c] = (c < C) ? gload(&WL[(int64_t)c * nh + j]) : 0.f;
-  }
-  gstore(&zrow[n], zl + dz);
-  if (da == 0.f) return;
-  float z[kCMax], p[kCMax];
-  moved_logits(C, da, wc, zc, z);
-  const float ln = softmax_ce(z, C, gload(&net.y[n]), p);
-#pragma unroll
-  for (int c = 0; c < kCMax; ++c)
-    if (c < C) {
-      gstore(&ZL[(int64_t)c * Ns + n], z[c]);
-      gstore(&net.prob[(int64_t)c * Ns + n], p[c]);
-    }
-  gstore(&net.ell[n], ln);
-}
-
 // Batched scoring of the candidates whose weight is in the last two layers
 // (a mutated hidden unit of layer L-2 moves the logits by a rank-1 update; a
 // logit-layer weight moves one logit), against the committed state.

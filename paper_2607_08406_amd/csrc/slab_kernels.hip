@@ -206,15 +206,16 @@ __global__ __launch_bounds__(kSlabThreads) void k_propose_columns(
 }
 
 // k_mode: -2 evaluate every listed candidate of layer L-3; -1 commit the
-// device decision st->chosen; >= 0 commit that candidate.  A commit is a no-op
-// here unless the candidate is in layer L-3.  ACT is the net's transfer
-// function (MCA_ACT_*), fixed at compile time.
+// device decision st->chosen; >= 0 commit that candidate.  A commit applies a
+// candidate of layer L-3, and with `columns` also one of the last two layers
+// (the column commit, as k_commit_column); others are no-ops here.  ACT is
+// the net's transfer function (MCA_ACT_*), fixed at compile time.
 template <int CM, int ACT>
 __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca_cand* cands,
                                                        const Aux* aux, int K, const uint64_t* cols,
                                                        const int* nnz, float* partial, int nblk,
                                                        int k_mode, DevState* st,
-                                                       const double* dL) {
+                                                       const double* dL, int columns) {
   constexpr int T = SlabTile<CM>::T, TS = T + 1;
   __shared__ NetDev net;
   stage_net(net, net_arg);
@@ -244,7 +245,27 @@ __global__ __launch_bounds__(kSlabThreads) void k_slab(NetDev net_arg, const mca
   int kc = -1;
   if (commit) {
     kc = (k_mode >= 0) ? k_mode : st->chosen;
-    if (kc < 0 || cands[kc].layer != l) return;  // uniform over the block
+    if (kc < 0) return;  // uniform over the block
+    const mca_cand cw = cands[kc];
+    if (cw.layer >= L - 2) {
+      // a winner in the last two layers: the column commit on the block's
+      // samples (the grid covers every sample), the weight by block 0
+      if (!columns) return;
+      const Aux aw = aux[kc];
+      if (tid < T && n0 + tid < N) column_commit(net, cw.layer, cw.j, cw.i, aw.de, n0 + tid);
+      if (blockIdx.x == 0 && tid == 0) {
+        const int64_t idx = (int64_t)cw.j * net.widths[cw.layer] + cw.i;
+        gstore(&net.W[cw.layer][idx], aw.w_new);
+        if (net.ternary) gstore(&net.codes[cw.layer][idx], (int8_t)cw.code);
+        // the transposed copy of W_{L-2}, which the column lists read
+        if (cw.layer == L - 2)
+          gstore(&net.WT[(int64_t)cw.i * net.widths[cw.layer + 1] + cw.j], aw.w_new);
+        if (net.sub_size == 0) st->L += dL[kc];
+        st->accepted += 1;
+      }
+      return;
+    }
+    if (cw.layer != l) return;
   }
   float* const Z1 = net.Z[l];       // fields of the mutated unit's layer
   float* const Z2 = net.Z[l + 1];   // the next hidden layer (the tile)
@@ -551,7 +572,7 @@ hipError_t launch_propose_columns(const NetDev& net, const DevState* st, int K, 
 
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
-                       const double* dL, hipStream_t s, bool listed) {
+                       const double* dL, hipStream_t s, bool listed, bool columns) {
   // the column lists of every candidate, built by an evaluation (or with the
   // proposal, `listed`); a commit follows the evaluation of its batch
   // (nothing changes W_1 in between) and reads its candidate's list from there
@@ -563,7 +584,7 @@ hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux,
   }
   auto go = [&](auto kernel) {
     hipLaunchKernelGGL(kernel, dim3(nblk), dim3(kSlabThreads), 0, s, net, cands, aux, K, cols,
-                       nnz, partial, nblk, k_mode, st, dL);
+                       nnz, partial, nblk, k_mode, st, dL, columns ? 1 : 0);
   };
   const bool small = net.C <= 10;
   if (net.act == MCA_ACT_TANH)

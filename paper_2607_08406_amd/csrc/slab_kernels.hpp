@@ -18,9 +18,12 @@ int slab_tile(int C);
 // >= 0: commit that candidate if it is in layer L-3.  cols (k_max * n_2
 // entries) and nnz (k_max) are scratch for the candidates' column lists.
 // `listed`: the column lists are already built (launch_propose_columns).
+// `columns`: a commit also applies a winner of the last two layers (then
+// k_commit_column is not launched); nblk blocks must cover every sample.
 hipError_t launch_slab(const NetDev& net, const mca_cand* cands, const Aux* aux, int K,
                        uint64_t* cols, int* nnz, float* partial, int nblk, int k_mode, DevState* st,
-                       const double* dL, hipStream_t s, bool listed = false);
+                       const double* dL, hipStream_t s, bool listed = false,
+                       bool columns = false);
 
 // The proposal of step st->t (as launch_propose with the device's step) fused
 // with the column lists of its layer L-3 candidates, for nets with L >= 3.
