@@ -37,7 +37,7 @@ namespace {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 
-constexpr int kGemmThreads = 256;  // 4 waves, a 128 x 128 output tile, 64 x 64 per wave
+constexpr int kGemmThreads = 256;  // 4 waves per output tile of 128 rows x 16 CB WC columns
 constexpr int kGemmRows = 128;     // rows (positions) per block
 constexpr int kChunkK = 16;        // reduction chunk staged in LDS
 constexpr int kStatSteps = 4;      // groups of four rows whose LayerNorm statistics a wave takes at once
