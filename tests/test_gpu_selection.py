@@ -8,7 +8,9 @@ single-weight increment, against the fp64 oracle (through the C ABI):
 * the greedy rule with ties accepted (Eq. 6 as printed: dL <= 0), on data
   with never-lit pixels, so zero changes occur and are committed;
 * the weight bound |w'| < Delta of Eq. 1 at a level that rejects about half
-  of each step's candidates unevaluated;
+  of each step's candidates unevaluated, and at one that rejects nearly all
+  of a batch of 128, so that decisions fall past the first 64 candidates or
+  find no winner;
 * pruning moves (Sec. 2.2, w -> 0) alone and mixed with increments
   (pruning first in stream order), with the remaining-weight ratio.
 """
@@ -136,6 +138,31 @@ def test_bound_splits_batch(mca, persistent):
     st, ch, dl = ctx.run_steps(60, 32, trace=True, trace_dloss=True)
     replay_trace(ref, cfg, 20, ch, dl, 32, ps, bound=bound)
     assert_state_equal(ctx, ref)
+    ctx.close()
+
+
+def test_decision_beyond_one_chunk_of_64(mca):
+    """K = 128 (the one-launch-per-phase loop; the persistent loop takes
+    K <= 64) under a weight bound at the 3 % quantile of the first layer's
+    magnitudes, so that most candidates are rejected unevaluated: the first
+    passing candidate often lies past index 63, and some steps pass none.
+    The selection's last block decides over chunks of 64 candidates; every
+    traced loss change and decision against the oracle's."""
+    cfg = small_wide(name="wide_k128")
+    w = mlp_workload(cfg)
+    K = 128
+    bound = float(np.quantile(np.abs(w["weights"][0]), 0.03))
+    banner(f"bound {bound:.6f} 784-512-10 K={K} device loop")
+    ctx, ref = make_pair(cfg, w, k_max=K, bound=bound)
+    ps = ParityStats(f"bound 784-512-10 K={K}")
+    st, ch, dl = ctx.run_steps(60, K, trace=True, trace_dloss=True)
+    assert st.next_step == 60
+    replay_trace(ref, cfg, 0, ch, dl, K, ps, bound=bound)
+    assert_state_equal(ctx, ref)
+    ch = np.asarray(ch)
+    late, none = int((ch >= 64).sum()), int((ch < 0).sum())
+    print(f"[gpu] decisions past index 63: {late}, steps without a winner: {none}", flush=True)
+    assert late >= 3 and none >= 3, (late, none)
     ctx.close()
 
 
