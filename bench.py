@@ -332,7 +332,8 @@ def measure(cfg, w, steps, warmup, args, eval_batch=0):
     mca.mca_get_timing(ctx.ctx, reset=True)
     # the dominant kernel: the persistent step loop (one launch runs every
     # timed step), or the evaluation phase when each phase is its own launch
-    mca.mca_set_timing(ctx.ctx, (1 << mca.PHASES.index("eval")) | (1 << mca.PHASES.index("step_loop")))
+    mca.mca_set_timing(ctx.ctx, (1 << mca.PHASES.index("eval")) | (1 << mca.PHASES.index("step_loop"))
+                       | (1 << mca.PHASES.index("one_loop")))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     st, _, _ = ctx.run_steps(steps, cfg.K)
@@ -340,8 +341,9 @@ def measure(cfg, w, steps, warmup, args, eval_batch=0):
     wall = time.perf_counter() - t0
     ms, launches = mca.mca_get_timing(ctx.ctx, reset=True)
     mca.mca_set_timing(ctx.ctx, 0)
-    loop = launches[mca.PHASES.index("step_loop")] > 0
-    dominant = mca.PHASES.index("step_loop" if loop else "eval")
+    one = launches[mca.PHASES.index("one_loop")] > 0
+    loop = one or launches[mca.PHASES.index("step_loop")] > 0
+    dominant = mca.PHASES.index("one_loop" if one else "step_loop" if loop else "eval")
     n_launch = max(int(launches[dominant]), 1)
     avg_s = ms[dominant] / 1e3 / n_launch
     t_first = st.next_step - steps
@@ -365,7 +367,7 @@ def measure(cfg, w, steps, warmup, args, eval_batch=0):
                 "unit": "TFLOP/s", "frac": achieved / MFMA_FP32_PEAK_TFS, "traffic": None,
                 "flops_per_launch": per_step}
     elif cfg.n_layers <= 2:
-        kernel = "k_step_loop" if loop else "k_eval_tiles"
+        kernel = "k_one_loop" if one else "k_step_loop" if loop else "k_eval_tiles"
         # one loop launch covers all timed steps; one eval launch covers one step
         bytes_launch = algorithmic_bytes_per_step(cfg) * (steps / n_launch if loop else 1)
         achieved = bytes_launch / avg_s / 1e9

@@ -205,7 +205,8 @@ typedef struct mca_trace {
 
 /* Accumulated device time per phase (HIP events on the context's stream). */
 typedef struct mca_timing {
-  double ms[8];        /* by phase: 0 propose, 1 eval, 2 select, 3 commit, 4 step loop, 5 forward */
+  double ms[8];        /* by phase: 0 propose, 1 eval, 2 select, 3 commit, 4 step loop,
+                          5 forward, 6 one-workgroup step loop */
   uint64_t launches[8];
 } mca_timing;
 
@@ -303,9 +304,14 @@ int mca_eval_losses_noalloc(mca_ctx* ctx, const mca_cand* cands_host, int32_t K,
 /* Tuning options of mca_run_steps (mca_set_option):
  *   MCA_OPT_PERSISTENT_LOOP  1 (default): run eligible nets (mutations reach
  *                            at most the last two layers, K <= 64) in one
- *                            cooperative launch per call; 0: one launch per
- *                            phase per step.  Both give the same results up
- *                            to the order of the loss-change sums.
+ *                            launch per call: one workgroup when the samples
+ *                            and weights fit it (N <= 1024, K <= 2, at most 10
+ *                            classes and 3072 weights; with K = 1 it scores
+ *                            steps t and t + 1 against one state and counts a
+ *                            discarded second score in stats.wasted), else a
+ *                            grid of workgroups; 0: one launch per phase per
+ *                            step.  All give the same decisions up to the
+ *                            order of the loss-change sums.
  *   MCA_OPT_LOOP_TILE        samples per workgroup of the persistent loop,
  *                            16..64 (default 64).
  *   MCA_OPT_LOOP_LAUNCH      1 (default): an ordinary launch of the

@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmca.so")
 SOURCES = ["mca_api.hip", "mlp_kernels.hip", "loop_kernel.hip", "slab_kernels.hip",
            "chain_kernels.hip", "channel_kernels.hip", "norm_kernels.hip",
-           "tf_kernels.hip"]
+           "tf_kernels.hip", "one_loop.hip"]
 
 # Device code: gfx950 only; no fp contraction (explicit fmaf only, so the
 # evaluation, commit and forward kernels round identically); packed fp32

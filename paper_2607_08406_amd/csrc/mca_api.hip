@@ -14,6 +14,7 @@
 
 #include "mca.h"
 #include "device_common.hpp"
+#include "one_loop.hpp"
 #include "loop_kernel.hpp"
 #include "mlp_kernels.hpp"
 #include "slab_kernels.hpp"
@@ -1374,8 +1375,11 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   bool offsets_fit = true;
   for (int l = 0; l < net.L; ++l)
     if ((uint64_t)net.widths[l] * (uint64_t)net.Ns >= ((uint64_t)1 << 32)) offsets_fit = false;
+  // a net whose samples fit one workgroup, with a few candidates per step:
+  // the one-workgroup loop (no exchange between workgroups)
+  const bool one_ok = ctx->use_loop && mlp2 && mca::one_loop_fits(net, K);
   // G tile workgroups plus the candidate reducers must all be resident at once
-  const bool loop_ok = ctx->use_loop && mlp2 && offsets_fit && K <= mca::kLoopMaxK &&
+  const bool loop_ok = !one_ok && ctx->use_loop && mlp2 && offsets_fit && K <= mca::kLoopMaxK &&
                        ctx->lo.loop_G <= mca::kLoopMaxTiles &&
                        ctx->lo.loop_G + mca::step_loop_reducers(K) <= ctx->loop_fit;
   // the call's start (counter snapshot, abort word cleared): in the loop's
@@ -1386,6 +1390,26 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
                        ctx->loop_sync);
     MCA_HIP(ctx, hipGetLastError());
     started = true;
+  }
+  while (one_ok && done < n_steps) {
+    const uint64_t cap = trace ? (uint64_t)kTraceCap : ((uint64_t)1 << 22);
+    const uint64_t chunk = std::min<uint64_t>(n_steps - done, cap);
+    mca::OneArgs a{};
+    a.net = net;
+    a.K = K;
+    a.n_steps = chunk;
+    a.st = ctx->st;
+    a.tr_chosen = trace ? ctx->tr_chosen : nullptr;
+    a.tr_dl = (trace && trace->dloss) ? ctx->tr_dl : nullptr;
+    a.tr_cap = kTraceCap;
+    MCA_HIP(ctx, timed(ctx, 6, [&] { return mca::launch_one_loop(a, ctx->stream); }));
+    if (trace != nullptr) {  // the next chunk reuses the device trace buffers
+      MCA_HIP(ctx, hipMemcpyAsync(trace->chosen + done, ctx->tr_chosen, chunk * sizeof(int32_t), hipMemcpyDeviceToHost, ctx->stream));
+      if (trace->dloss)
+        MCA_HIP(ctx, hipMemcpyAsync(trace->dloss + done * K, ctx->tr_dl, chunk * K * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+      MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    }
+    done += chunk;
   }
   while (loop_ok && done < n_steps) {
     const uint64_t cap = trace ? (uint64_t)kTraceCap : ((uint64_t)1 << 22);

@@ -395,7 +395,7 @@ def mca_get_sample_losses(ctx, n: int) -> np.ndarray:
     return out
 
 
-PHASES = ["propose", "eval", "select", "commit", "step_loop", "forward"]
+PHASES = ["propose", "eval", "select", "commit", "step_loop", "forward", "one_loop"]
 
 
 def mca_set_timing(ctx, phase_mask: int):

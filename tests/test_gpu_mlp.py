@@ -380,6 +380,77 @@ def test_resume_is_exact(mca):
         ctx.close()
 
 
+ONE_LOOP_CASES = {
+    # name: (config overrides on the tiny family, K, steps, make_pair options)
+    "tiny_k2": (dict(), 2, 300, {}),
+    "micro_4_3_2": (dict(widths=(4, 3, 2), n_samples=200), 2, 400, {}),
+    # 16 inputs: a hidden unit keeps several nonzero codes, so no move maps
+    # its field exactly onto its mirror image (where the fp64 oracle's change
+    # is exactly zero and fp32 history leaves a residue)
+    "small_ternary": (dict(widths=(16, 4, 3), n_samples=300, act="gauss", init="ternary",
+                           weight_mode="ternary"), 2, 400, {}),
+    "linear_64_10": (dict(widths=(64, 10), n_samples=500), 2, 200, {}),
+    "ragged_63": (dict(n_samples=63), 2, 200, {}),
+    "single_sample": (dict(n_samples=1), 1, 60, {}),
+    "classes_7": (dict(widths=(64, 32, 7), n_samples=700), 2, 200, {}),
+    "metropolis": (dict(), 2, 300, dict(beta=3e4)),
+    "pruning": (dict(), 2, 300, dict(n_prune=1)),
+    "minibatch": (dict(), 2, 200, dict(subset=(256, 5))),
+    # one candidate per step: passes of two steps scored against one state
+    "tiny_k1": (dict(), 1, 400, {}),
+    "micro_k1_odd": (dict(widths=(4, 3, 2), n_samples=200), 1, 401, {}),
+    "ternary_k1": (dict(widths=(16, 4, 3), n_samples=300, act="gauss", init="ternary",
+                        weight_mode="ternary"), 1, 400, {}),
+    "linear_k1": (dict(widths=(64, 10), n_samples=500), 1, 301, {}),
+    "metropolis_k1": (dict(), 1, 300, dict(beta=3e4)),
+    "pruning_k1": (dict(), 1, 300, dict(n_prune=1)),
+    "minibatch_k1": (dict(), 1, 203, dict(subset=(256, 5))),
+}
+
+
+def speculative_waste(chosen, K):
+    """Evaluations a run of two-step passes discards: with K = 1, a pass
+    whose first step accepts has scored the step after it for nothing."""
+    if K != 1:
+        return 0
+    n, t, waste = len(chosen), 0, 0
+    while t < n:
+        if chosen[t] >= 0:
+            waste += int(t + 1 < n)
+            t += 1
+        else:
+            t += 2
+    return waste
+
+
+@pytest.mark.parametrize("case", sorted(ONE_LOOP_CASES))
+def test_one_workgroup_loop(mca, case):
+    """Nets whose samples and weights fit one workgroup with at most two
+    candidates per step run the one-workgroup loop (sample per thread,
+    decision inside the workgroup; with one candidate, passes of two steps
+    against one state).  Each case replays the device run on the oracle: a ragged and a single-sample set, a net without a hidden layer,
+    7 classes, ternary codes on a 16-4-3 net, the Metropolis rule, pruning
+    moves, a minibatch window, and a 4-3-2 net where consecutive candidates
+    share weights, units and columns all the time (the patches of a commit
+    into the next step's candidates)."""
+    over, K, steps, opts = ONE_LOOP_CASES[case]
+    cfg = CONFIGS["tiny"].scaled(name=f"one_{case}", K=K, **over)
+    banner(f"one-workgroup loop {case}: {cfg.widths} N={cfg.n_samples} K={K} {opts}")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=K, **opts)
+    ps = ParityStats(f"one-workgroup loop {case}")
+    st, ch, dl = ctx.run_steps(steps, K, trace=True, trace_dloss=True)
+    assert st.steps == steps and st.next_step == steps
+    _, acc = replay_trace(ref, cfg, 0, ch, dl, K, ps, **opts)
+    assert acc == st.accepted
+    assert st.wasted == speculative_waste(list(ch), K)
+    assert_state_equal(ctx, ref)
+    L, _ = ctx.loss()
+    if "subset" not in opts:
+        assert abs(L - ref.loss()) <= REL_TOL * ref.loss() + 1e-6
+    ctx.close()
+
+
 @pytest.mark.parametrize("N", [1, 63, 257])
 def test_degenerate_sample_counts(mca, N):
     cfg = CONFIGS["tiny"].scaled(n_samples=N)
