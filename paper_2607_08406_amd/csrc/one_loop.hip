@@ -26,8 +26,9 @@
 //     an image-like input cost any work, and keeps each pair's activation
 //     change for the commit;
 //  3. each thread adds its sample's slots: a fixed-order sum over the 64
-//     lanes of each wave (fp32), then over the 16 waves in order (fp64),
-//     which every wave takes, so every wave knows the decision at once;
+//     lanes of each wave (fp32), then over the 16 waves (fp64, one DPP order
+//     within a row of 16 lanes), which every wave takes, so every wave knows
+//     the decision at once;
 //  4. the listed pairs of the chosen slot are committed with the expressions
 //     the scoring used.
 // Candidates are completed (new value, threshold, logit-layer column) one
@@ -38,9 +39,9 @@
 // completed again from the committed value and code, or a logit weight of a
 // hidden candidate's column).
 // Rows need no state to be located (parameter, row and column come from the
-// ring), so each pass requests, before its scoring, the rows of the pass
-// that follows should none of its steps but the last accept; with K = 1 a
-// pass that resolves one step carries its second step's rows over.
+// ring), so each pass requests, at its start, the rows of the pass that
+// follows should none of its steps but the last accept; with K = 1 a pass
+// that resolves one step carries its second step's rows over.
 // The trace is kept in LDS and written out every 64 steps.
 #include "device_common.hpp"
 #include "one_loop.hpp"
@@ -79,6 +80,24 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
   const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
   const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
   return (r0 + r1) + (r2 + r3);
+}
+
+template <int kCtrl>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, kCtrl, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), kCtrl, 0xF, 0xF, true);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// Sum over each row of 16 lanes in one fixed order (fp64): every step adds
+// a lane's value to its partner's, so both hold the same bits, and after
+// four steps every lane of the row holds the row's sum.
+__device__ __forceinline__ double wave_row_sum_f64(double v) {
+  v += dpp_f64<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f64<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f64<0x141>(v);  // row_half_mirror
+  v += dpp_f64<0x140>(v);  // row_mirror
+  return v;
 }
 
 __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
@@ -262,6 +281,10 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       filled += kRefill;
       __syncthreads();
     }
+    // the rows of the pass after this one, should it start at t + S: they
+    // go out first, so that they have landed before any spill reload of the
+    // pass (a reload waits for every memory operation in flight)
+    load_rows(t + (uint64_t)S, a_pre, z_pre);
     // 1. this pass's rows with the last commit applied (a hidden unit's
     // field row, or a logit weight's input fed by that unit), staged in LDS;
     // the pairs with a non-zero input go on their slot's list (every sample
@@ -300,9 +323,6 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
         if ((m[q] >> lane) & 1ull) list_lds[q][bq + (uint32_t)__popcll(m[q] & below)] = (uint16_t)n;
       }
     }
-    // the rows of the pass after this one, should it start at t + S; they
-    // land while this pass is scored
-    load_rows(t + (uint64_t)S, a_pre, z_pre);
     __syncthreads();  // A: the lists
     const uint32_t ln = list_n;
     const int nl0 = (int)(ln & 0xFFFFu), nl1 = (int)(ln >> 16);
@@ -339,15 +359,22 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
     }
     if (tid == 0) list_n = 0;  // every thread has read the counts
     __syncthreads();  // C
-    // every wave adds the 16 wave sums in order and takes the same decision
+    // every wave adds the 16 wave sums of each slot (fp64, lanes 16q ..
+    // 16q + 15, one DPP order that leaves the same bits in every lane of the
+    // row) and takes the same decision
+    const double row = wave_row_sum_f64((lane >> 4) < nq ? (double)red_lds[lane & 15][(lane >> 4) & 1] : 0.0);
     double v = 0.0;
     bool pass = false;
+    {
+      const uint64_t u = (uint64_t)__double_as_longlong(row);
+      const uint32_t lo0 = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 0);
+      const uint32_t hi0 = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 0);
+      const uint32_t lo1 = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 16);
+      const uint32_t hi1 = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 16);
+      const uint64_t w0 = ((uint64_t)hi0 << 32) | lo0, w1 = ((uint64_t)hi1 << 32) | lo1;
+      v = __longlong_as_double((long long)(lane == 0 ? w0 : w1));
+    }
     if (lane < nq) {
-      float rw[kOneWaves];
-#pragma unroll
-      for (int w = 0; w < kOneWaves; ++w) rw[w] = red_lds[w][lane];
-#pragma unroll
-      for (int w = 0; w < kOneWaves; ++w) v += (double)rw[w];
       const Aux& xq = aux_lds[ent(t, lane)][lane & (K - 1)];
       const bool valid = xq.valid != 0;
       v = valid ? v / count : __builtin_huge_val();
@@ -372,6 +399,10 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       a_cur[1] = a_pre[0];
       z_cur[1] = z_pre[0];
     }
+    // taken here, before the commit's stores: a copy placed after them would
+    // wait for the stores too
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) asm volatile("" : "+v"(a_cur[q]), "+v"(z_cur[q]));
     if (wave == 0) {
       const uint64_t upto = (qc >= 0) ? ((2ull << qc) - 1ull) : ((1ull << nq) - 1ull);
       const uint64_t tie = __ballot(lane < nq && fabs(v) < 1e-6) & upto;
@@ -425,8 +456,6 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
         if (lane == 0) {
           w_lds[woff(c.layer) + idx] = x.w_new;
           c_lds[woff(c.layer) + idx] = (int8_t)c.code;
-          gstore(&net.W[c.layer][idx], x.w_new);
-          if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
         }
         // lane l: candidate l & (K - 1) of step t + (l >> kshift), for the
         // steps after the chosen one that are already completed
@@ -490,6 +519,12 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       lc_layer = c.layer;
       lc_j = c.j;
       lc_moved = chid && live && ain_lds[qc][n] != 0.f;  // this sample's field moved
+      // the weight's HBM copy last: nothing in this pass waits for the store
+      if (wave == kDrawWave && lane == 0) {
+        const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
+        gstore(&net.W[c.layer][idx], x.w_new);
+        if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
+      }
     }
     __syncthreads();  // D
     t = tn;
