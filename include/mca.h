@@ -367,7 +367,9 @@ int mca_get_sample_losses(mca_ctx* ctx, float* out_host);
  * context's stream around every launch of phase p (phases as in mca_timing;
  * 0 disables all); no synchronisation per launch.  mca_get_timing reads (and
  * optionally resets) the accumulated device time per phase and synchronises.
- * The events add a little launch overhead. */
+ * The events add a little launch overhead.  A non-zero mask also makes up to
+ * 32 events ahead (kept until mca_destroy), so the first timed launches
+ * create none. */
 int mca_set_timing(mca_ctx* ctx, int32_t phase_mask);
 int mca_get_timing(mca_ctx* ctx, mca_timing* out, int32_t reset);
 

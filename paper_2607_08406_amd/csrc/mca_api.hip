@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -490,6 +491,23 @@ int device_fail(mca_ctx* ctx, hipError_t e, const char* what) {
     if ((ctx) == nullptr) return fail(nullptr, MCA_EINVAL, "ctx is NULL"); \
     if ((ctx)->poisoned) return fail(ctx, MCA_EPOISONED, "context poisoned by an earlier device error: " + (ctx)->err); \
   } while (0)
+
+// Waits for the stream by polling it for up to a millisecond, then blocks: a
+// blocking wait may put the thread to sleep, and waking it costs tens of
+// microseconds, a large share of a call of a few dozen steps.
+hipError_t wait_stream(hipStream_t s) {
+  const auto t0 = std::chrono::steady_clock::now();
+  while (true) {
+    const hipError_t e = hipStreamQuery(s);
+    if (e != hipErrorNotReady) return e;
+    if (std::chrono::steady_clock::now() - t0 > std::chrono::microseconds(1000)) break;
+  }
+  return hipStreamSynchronize(s);
+}
+
+// Events made ahead when timing is switched on (a step-loop call records one
+// pair per launch; the per-phase loop four pairs per step).
+constexpr size_t kEventsAhead = 32;
 
 hipEvent_t get_event(mca_ctx* ctx) {
   if (!ctx->pool.empty()) {
@@ -1471,7 +1489,7 @@ int mca_run_steps(mca_ctx* ctx, uint64_t n_steps, int32_t K, mca_trace* trace, m
   alignas(8) unsigned char local[kStateBlock];
   unsigned char* blk = ctx->host_blk ? ctx->host_blk : local;
   MCA_HIP(ctx, hipMemcpyAsync(blk, ctx->st, kStateBlock, hipMemcpyDeviceToHost, ctx->stream));
-  MCA_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  MCA_HIP(ctx, wait_stream(ctx->stream));
   DevState after, before;
   mca::LoopSync sync;
   std::memcpy(&after, blk, sizeof after);
@@ -1574,6 +1592,13 @@ int mca_get_sample_losses(mca_ctx* ctx, float* out_host) {
 int mca_set_timing(mca_ctx* ctx, int32_t phase_mask) {
   MCA_LIVE(ctx);
   ctx->timing = phase_mask;
+  // events for the first timed launches are made here, not inside them: an
+  // event's creation costs tens of microseconds of host time
+  while (phase_mask != 0 && ctx->pool.size() < kEventsAhead) {
+    hipEvent_t e = nullptr;
+    MCA_HIP(ctx, hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+    ctx->pool.push_back(e);
+  }
   return MCA_OK;
 }
 
