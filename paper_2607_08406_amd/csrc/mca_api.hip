@@ -1345,7 +1345,9 @@ int mca_set_option(mca_ctx* ctx, int32_t option, int64_t value) {
   MCA_LIVE(ctx);
   if (option == MCA_OPT_PERSISTENT_LOOP) {
     if (value != 0 && value != 1) return fail(ctx, MCA_EINVAL, "MCA_OPT_PERSISTENT_LOOP takes 0 or 1");
-    ctx->use_loop = value != 0;
+    // nets with biases or normalization and channel mutations have no device
+    // loop kernel: they keep the per-phase loop either way
+    ctx->use_loop = value != 0 && !ctx->norm && !ctx->chan;
     return MCA_OK;
   }
   if (option == MCA_OPT_LOOP_LAUNCH) {

@@ -61,7 +61,7 @@ constexpr int kOneCM = 10;    // class bound of the LDS logit tile
 constexpr int kDrawWave = kOneWaves - 1;
 static_assert(kSlots * 16 <= 64, "the draw takes one (slot, class) per lane");
 static_assert(kOneMaxK <= kSlots, "a step fits one pass");
-static_assert(kOneThreads <= 1024 && kSlots <= 2, "list codes are slot << 10 | sample");
+static_assert(kOneThreads < 65536 && kSlots <= 2, "two 16-bit list counts share one word");
 
 template <int kCtrl>
 __device__ __forceinline__ float dpp_f32(float x) {

@@ -89,6 +89,23 @@ def test_normnet_explicit_and_device(mca, widths, act, ln, bias, N, pick, sticky
     ctx.close()
 
 
+def test_normnet_one_hidden_layer_keeps_the_per_phase_loop(mca):
+    """A one-hidden-layer net with biases and normalization is run by the
+    per-phase loop even when the persistent-loop option is set to 1 (neither
+    device loop kernel takes biases): its device steps replay on the oracle."""
+    cfg = cfg_of((784, 256, 10), "relu", True, True, 700, K=8, seed=6, delta=0.05)
+    banner("normnet 784-256-10 with the persistent-loop option on")
+    w = mlp_workload(cfg)
+    ctx, ref = make_pair(cfg, w, k_max=8)
+    ctx.set_option(mca.MCA_OPT_PERSISTENT_LOOP, 1)
+    ps = ParityStats("normnet 784-256-10 loop option on")
+    st, ch, dl = ctx.run_steps(10, 8, trace=True, trace_dloss=True)
+    _, acc = replay_trace(ref, cfg, 0, ch, dl, 8, ps)
+    assert st.accepted == acc
+    assert_state_equal(ctx, ref)
+    ctx.close()
+
+
 def test_normnet_every_bias(mca):
     """A candidate forced onto a bias of every layer (column n_l), the logit
     layer's included, and onto a weight of every layer."""
