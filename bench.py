@@ -419,8 +419,10 @@ def copy_calibration(nbytes: int):
 
 # Per-config windows of the multi-config line (the headline config times
 # exactly --steps): long enough that launch and copy overheads are small.
+# deepln draws its layer once per block of 32 steps (sticky schedule) and the
+# layers differ in cost, so its window spans 20 blocks
 SUB_STEPS = {"tiny": (20000, 200), "deep": (60, 3), "ternary": (1000, 20),
-             "transformer": (100, 5), "channel": (20, 2), "deepln": (100, 5)}
+             "transformer": (100, 5), "channel": (20, 2), "deepln": (640, 32)}
 
 
 def main():
