@@ -111,6 +111,9 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
   __shared__ int8_t c_lds[kOneMaxParams];     // their ternary codes
   __shared__ mca_cand ring_lds[kRing][kOneMaxK];  // decode_index of step t at t mod kRing
   __shared__ double theta_ring[kRing][kOneMaxK];
+  // the record's row offsets (elements): its input row, and its field row for
+  // a hidden unit (-1 for a logit weight, whose field row is not read)
+  __shared__ int2 roff_ring[kRing][kOneMaxK];
   // completed candidates of step t at t mod kAhead
   __shared__ mca_cand cand_lds[kAhead][kOneMaxK];
   __shared__ Aux aux_lds[kAhead][kOneMaxK];
@@ -176,9 +179,11 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       const int m = e >> kshift, k = e & (K - 1);
       const uint64_t t = t_from + (uint64_t)m;
       if (t < t_end) {
-        ring_lds[t & (kRing - 1)][k] = decode_index(net, t, (uint64_t)k);
+        const mca_cand r = decode_index(net, t, (uint64_t)k);
+        ring_lds[t & (kRing - 1)][k] = r;
         theta_ring[t & (kRing - 1)][k] = accept_theta(net.rule, net.beta, net.seed, net.tag, t,
                                                       (uint64_t)k);
+        roff_ring[t & (kRing - 1)][k] = make_int2(r.i * ns32, r.layer == L - 2 ? r.j * ns32 : -1);
       }
     }
   };
@@ -236,11 +241,11 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       zv[q] = 0.f;
       const uint64_t step = tp + (uint64_t)(q >> kshift);
       if (step < t_end) {
-        const mca_cand r = ring_lds[step & (kRing - 1)][q & (K - 1)];
-        const bool hid = r.layer == L - 2;
         // rows are short (N <= 1024): 32-bit offsets
-        av[q] = gload(&(hid ? in_hid : in_log)[r.i * ns32 + n32]);
-        zv[q] = gload(&z_hid[(hid ? r.j : 0) * ns32 + n32]);
+        const int2 o = roff_ring[step & (kRing - 1)][q & (K - 1)];
+        const bool hid = o.y >= 0;
+        av[q] = gload(&(hid ? in_hid : in_log)[o.x + n32]);
+        zv[q] = gload(&z_hid[(hid ? o.y : 0) + n32]);
       }
     }
   };
