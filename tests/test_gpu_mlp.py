@@ -405,6 +405,10 @@ ONE_LOOP_CASES = {
     "metropolis_k1": (dict(), 1, 300, dict(beta=3e4)),
     "pruning_k1": (dict(), 1, 300, dict(n_prune=1)),
     "minibatch_k1": (dict(), 1, 203, dict(subset=(256, 5))),
+    # the weight bound of Eq. 1 at half the init range: about half the draws
+    # are rejected unevaluated (+inf), in either slot of a pass
+    "bound_k1": (dict(), 1, 300, dict(bound=0.25)),
+    "bound_k2": (dict(), 2, 200, dict(bound=0.25)),
 }
 
 
@@ -428,11 +432,12 @@ def test_one_workgroup_loop(mca, case):
     """Nets whose samples and weights fit one workgroup with at most two
     candidates per step run the one-workgroup loop (sample per thread,
     decision inside the workgroup; with one candidate, passes of two steps
-    against one state).  Each case replays the device run on the oracle: a ragged and a single-sample set, a net without a hidden layer,
-    7 classes, ternary codes on a 16-4-3 net, the Metropolis rule, pruning
-    moves, a minibatch window, and a 4-3-2 net where consecutive candidates
-    share weights, units and columns all the time (the patches of a commit
-    into the next step's candidates)."""
+    against one state).  Each case replays the device run on the oracle:
+    ragged and single-sample sets, a net without a hidden layer, 7 classes,
+    ternary codes on a 16-4-3 net, the Metropolis rule, pruning moves, a
+    minibatch window, a weight bound, and a 4-3-2 net where consecutive
+    candidates share weights, units and columns all the time (the patches of
+    a commit into the later steps' completed candidates)."""
     over, K, steps, opts = ONE_LOOP_CASES[case]
     cfg = CONFIGS["tiny"].scaled(name=f"one_{case}", K=K, **over)
     banner(f"one-workgroup loop {case}: {cfg.widths} N={cfg.n_samples} K={K} {opts}")
@@ -444,6 +449,8 @@ def test_one_workgroup_loop(mca, case):
     _, acc = replay_trace(ref, cfg, 0, ch, dl, K, ps, **opts)
     assert acc == st.accepted
     assert st.wasted == speculative_waste(list(ch), K)
+    if "bound" in opts:  # the bound rejected draws, and not all of them
+        assert 0 < int(np.isinf(dl).sum()) < dl.size
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     if "subset" not in opts:
