@@ -409,6 +409,9 @@ ONE_LOOP_CASES = {
     # are rejected unevaluated (+inf), in either slot of a pass
     "bound_k1": (dict(), 1, 300, dict(bound=0.25)),
     "bound_k2": (dict(), 2, 200, dict(bound=0.25)),
+    # Eq. 6 with <= on one sample: a first-layer draw on one of its zero
+    # inputs changes nothing (dL exactly 0) and is accepted
+    "ties_k1": (dict(n_samples=1, accept_ties=True), 1, 301, {}),
 }
 
 
@@ -435,8 +438,8 @@ def test_one_workgroup_loop(mca, case):
     against one state).  Each case replays the device run on the oracle:
     ragged and single-sample sets, a net without a hidden layer, 7 classes,
     ternary codes on a 16-4-3 net, the Metropolis rule, pruning moves, a
-    minibatch window, a weight bound, and a 4-3-2 net where consecutive
-    candidates share weights, units and columns all the time (the patches of
+    minibatch window, a weight bound, Eq. 6 with <= on one sample (zero
+    changes accepted), and a 4-3-2 net where consecutive candidates share weights, units and columns all the time (the patches of
     a commit into the later steps' completed candidates)."""
     over, K, steps, opts = ONE_LOOP_CASES[case]
     cfg = CONFIGS["tiny"].scaled(name=f"one_{case}", K=K, **over)
@@ -451,6 +454,8 @@ def test_one_workgroup_loop(mca, case):
     assert st.wasted == speculative_waste(list(ch), K)
     if "bound" in opts:  # the bound rejected draws, and not all of them
         assert 0 < int(np.isinf(dl).sum()) < dl.size
+    if cfg.accept_ties:  # zero changes occurred and were accepted
+        assert any(dl[t, 0] == 0.0 and ch[t] == 0 for t in range(steps))
     assert_state_equal(ctx, ref)
     L, _ = ctx.loss()
     if "subset" not in opts:
