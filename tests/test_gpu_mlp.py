@@ -439,8 +439,9 @@ def test_one_workgroup_loop(mca, case):
     ragged and single-sample sets, a net without a hidden layer, 7 classes,
     ternary codes on a 16-4-3 net, the Metropolis rule, pruning moves, a
     minibatch window, a weight bound, Eq. 6 with <= on one sample (zero
-    changes accepted), and a 4-3-2 net where consecutive candidates share weights, units and columns all the time (the patches of
-    a commit into the later steps' completed candidates)."""
+    changes accepted), and a 4-3-2 net where consecutive candidates share
+    weights, units and columns all the time (the patches of a commit into
+    the later steps' completed candidates)."""
     over, K, steps, opts = ONE_LOOP_CASES[case]
     cfg = CONFIGS["tiny"].scaled(name=f"one_{case}", K=K, **over)
     banner(f"one-workgroup loop {case}: {cfg.widths} N={cfg.n_samples} K={K} {opts}")
