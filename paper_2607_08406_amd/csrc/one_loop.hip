@@ -59,6 +59,7 @@ constexpr int kTrace = 64;    // steps of trace kept in LDS
 constexpr int kAhead = 8;     // steps of completed candidates kept in LDS (a power of two)
 constexpr int kOneCM = 10;    // class bound of the LDS logit tile
 constexpr int kDrawWave = kOneWaves - 1;
+constexpr int kStoreWave = kOneWaves - 2;  // stores the committed weight to HBM
 static_assert(kSlots * 16 <= 64, "the draw takes one (slot, class) per lane");
 static_assert(kOneMaxK <= kSlots, "a step fits one pass");
 static_assert(kOneThreads < 65536 && kSlots <= 2, "two 16-bit list counts share one word");
@@ -524,8 +525,9 @@ __global__ __launch_bounds__(kOneThreads) void k_one_loop(OneArgs a) {
       lc_layer = c.layer;
       lc_j = c.j;
       lc_moved = chid && live && ain_lds[qc][n] != 0.f;  // this sample's field moved
-      // the weight's HBM copy last: nothing in this pass waits for the store
-      if (wave == kDrawWave && lane == 0) {
+      // the weight's HBM copy last: nothing in this pass waits for the store;
+      // a wave other than the draw wave (whose patch ends the commit) makes it
+      if (wave == kStoreWave && lane == 0) {
         const int64_t idx = (int64_t)c.j * net.widths[c.layer] + c.i;
         gstore(&net.W[c.layer][idx], x.w_new);
         if (net.ternary) gstore(&net.codes[c.layer][idx], (int8_t)c.code);
